@@ -1,0 +1,87 @@
+"""Seeded synthetic workloads for the full CGTP (shared by tests and the benchmark).
+
+This module only draws inputs; it holds none of the tensor-product arithmetic,
+so both the GPU path and the CPU oracle may use it.
+
+Recipe (one per workload): a CPU ``torch.Generator`` seeded with the degree
+L draws x1, then x2, each ``randn(N, (L+1)^2)`` in float64 (iid N(0, 1)
+coefficients, dense, every path present).  The "scaled" workload multiplies
+each degree-l block by 1/(l+1) before the cast.  The draw is then cast to the
+workload's dtype; a checker consumes the cast values upcast to float64, so a
+measured error is the GPU arithmetic error alone.  Large workloads are
+checked on a seeded, sorted subsample of pairs (``randperm`` with seed L+1).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    L: int
+    N: int
+    dtype: str            # "fp32" | "fp64"
+    scaled: bool = False  # degree-l block multiplied by 1/(l+1)
+    check_pairs: int = 0  # 0: check every pair; else size of the seeded subsample
+
+    @property
+    def seed(self) -> int:
+        return self.L
+
+    @property
+    def n_coeffs(self) -> int:
+        return (self.L + 1) ** 2
+
+    @property
+    def n_outputs(self) -> int:
+        return (self.L + 1) ** 4
+
+
+WORKLOADS = [
+    Workload("cgtp_L2_N64_fp64", 2, 64, "fp64"),
+    Workload("cgtp_L4_N100000_fp32", 4, 100_000, "fp32"),
+    Workload("cgtp_L8_N65536_fp32_scaled", 8, 65_536, "fp32", scaled=True),
+    Workload("cgtp_L16_N8192_fp32", 16, 8_192, "fp32", check_pairs=64),
+    Workload("cgtp_L32_N1024_fp32", 32, 1_024, "fp32", check_pairs=4),
+]
+BY_L = {w.L: w for w in WORKLOADS}
+
+
+def block_slice(l: int) -> slice:
+    """Columns of degree l in a [.., (L+1)^2] feature row (index l^2 + l + m)."""
+    return slice(l * l, (l + 1) * (l + 1))
+
+
+def torch_dtype(name: str):
+    import torch
+    return {"fp32": torch.float32, "fp64": torch.float64}[name]
+
+
+def draw(L: int, N: int, dtype: str = "fp32", scaled: bool = False, seed: int | None = None):
+    """Returns (x1, x2) as CPU torch tensors [N, (L+1)^2] of the given dtype."""
+    import torch
+    g = torch.Generator("cpu").manual_seed(L if seed is None else seed)
+    n = (L + 1) ** 2
+    x1 = torch.randn(N, n, dtype=torch.float64, generator=g)
+    x2 = torch.randn(N, n, dtype=torch.float64, generator=g)
+    if scaled:
+        s = torch.empty(n, dtype=torch.float64)
+        for l in range(L + 1):
+            s[block_slice(l)] = 1.0 / (l + 1)
+        x1 = x1 * s
+        x2 = x2 * s
+    return x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype))
+
+
+def workload_inputs(w: Workload):
+    return draw(w.L, w.N, w.dtype, w.scaled, w.seed)
+
+
+def check_indices(w: Workload):
+    """Sorted pair indices a checker compares (all pairs, or the seeded subsample)."""
+    import torch
+    if w.check_pairs == 0 or w.check_pairs >= w.N:
+        return torch.arange(w.N)
+    g = torch.Generator("cpu").manual_seed(w.seed + 1)
+    return torch.sort(torch.randperm(w.N, generator=g)[: w.check_pairs]).values

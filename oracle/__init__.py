@@ -1,0 +1,121 @@
+"""Oracle for the full Clebsch-Gordan tensor product: TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The GPU library never imports, links or
+calls it; the two share no code.
+
+The numerical work is in ``cgtp_oracle.c`` (plain C, fp64, Racah-formula
+Clebsch-Gordan coefficients in long double, naive O(L^6) double sum over
+(m1, m2)).  This module only marshals numpy arrays through ctypes.
+
+Complex inputs (used by the rotation-equivariance pins) are handled by
+bilinearity: (a + ib) (x) (c + id) = a(x)c - b(x)d + i (a(x)d + b(x)c).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cgtp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compiles the oracle shared library with gcc (portable x86-64 code)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O3", "-fopenmp", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build(force=False)
+    lib = ctypes.CDLL(_LIB)
+    lib.oracle_cg.restype = ctypes.c_double
+    lib.oracle_cg.argtypes = [ctypes.c_int] * 6
+    lib.oracle_cgtp.restype = ctypes.c_int
+    lib.oracle_cgtp.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_int]
+    lib.oracle_cg_block.restype = ctypes.c_int
+    lib.oracle_cg_block.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    lib.oracle_num_outputs.restype = ctypes.c_int64
+    lib.oracle_num_outputs.argtypes = [ctypes.c_int]
+    lib.oracle_path_offset.restype = ctypes.c_int64
+    lib.oracle_path_offset.argtypes = [ctypes.c_int] * 4
+    lib.oracle_table_build_seconds.restype = ctypes.c_double
+    lib.oracle_table_build_seconds.argtypes = []
+    lib.oracle_max_threads.restype = ctypes.c_int
+    lib.oracle_max_threads.argtypes = []
+    _lib = lib
+    return lib
+
+
+def cg(j1: int, m1: int, j2: int, m2: int, j: int, m: int) -> float:
+    """C^{j m}_{j1 m1 j2 m2} (Condon-Shortley), Racah formula."""
+    return _load().oracle_cg(j1, m1, j2, m2, j, m)
+
+
+def cg_block(l1: int, l2: int, l3: int) -> np.ndarray:
+    """Array [2 l3 + 1, 2 l1 + 1] of C^{l3 m3}_{l1 m1 l2 (m3 - m1)}."""
+    out = np.zeros((2 * l3 + 1, 2 * l1 + 1), dtype=np.float64)
+    rc = _load().oracle_cg_block(l1, l2, l3, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("invalid triple (%d, %d, %d)" % (l1, l2, l3))
+    return out
+
+
+def num_outputs(L: int) -> int:
+    return (L + 1) ** 4
+
+
+def path_offset(L: int, l1: int, l2: int, l3: int) -> int:
+    """Offset of path (l1, l2, l3) within one pair's output, -1 if not a path."""
+    return int(_load().oracle_path_offset(L, l1, l2, l3))
+
+
+def cgtp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
+    """Full CGTP in fp64.  x1, x2: [N, (L+1)^2] real; returns [N, (L+1)^4]."""
+    a = np.ascontiguousarray(np.asarray(x1, dtype=np.float64))
+    b = np.ascontiguousarray(np.asarray(x2, dtype=np.float64))
+    if a.ndim == 1:
+        a = a[None]
+    if b.ndim == 1:
+        b = b[None]
+    if a.shape != b.shape or a.shape[1] != (L + 1) ** 2:
+        raise ValueError("inputs must both be [N, (L+1)^2]")
+    n = a.shape[0]
+    out = np.empty((n, num_outputs(L)), dtype=np.float64)
+    rc = _load().oracle_cgtp(L, n, a.ctypes.data, b.ctypes.data, out.ctypes.data, int(threads))
+    if rc != 0:
+        raise RuntimeError("oracle_cgtp failed (L=%d, N=%d)" % (L, n))
+    return out
+
+
+def cgtp_complex(L: int, x1, x2, threads: int = 0) -> np.ndarray:
+    """CGTP of complex inputs, by bilinearity of the real oracle."""
+    x1 = np.asarray(x1, dtype=np.complex128)
+    x2 = np.asarray(x2, dtype=np.complex128)
+    rr = cgtp(L, x1.real, x2.real, threads)
+    ii = cgtp(L, x1.imag, x2.imag, threads)
+    ri = cgtp(L, x1.real, x2.imag, threads)
+    ir = cgtp(L, x1.imag, x2.real, threads)
+    return (rr - ii) + 1j * (ri + ir)
+
+
+def table_build_seconds() -> float:
+    return float(_load().oracle_table_build_seconds())
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
