@@ -1,0 +1,162 @@
+"""Benchmark: full-CGTP pairs/s on one MI355X, with roofline and CPU-oracle baseline.
+
+One step = one cgtp_forward over the whole batch (every (l1, l2) block of every
+pair: lift, products, lower, per-path recovery), inputs already resident in
+HBM.  The headline workload is L = 32, N = 1024 pairs, fp32; L = 16,
+N = 8192 is reported beside it.  Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "full-CGTP pairs/sec at L=16 and L=32 + % of HBM/MFMA roofline"
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (and dense fp32 MFMA) peak
+PEAK_FP64_TFLOPS = 78.6
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def time_workload(w, steps, warmup):
+    import torch
+
+    import cgtp_inputs
+    import paper_2602_21466_amd as lib
+
+    x1, x2 = cgtp_inputs.workload_inputs(w)
+    plan = lib.Plan(w.L, dtype=w.dtype)
+    q = plan.query()
+    a, b = x1.cuda(), x2.cuda()
+    out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        plan.forward(a, b, out, stream)
+    torch.cuda.synchronize()
+    # per-launch events on the launch stream bracket exactly one kernel each
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(steps):
+        ev[i][0].record(stream)
+        plan.forward(a, b, out, stream)
+        ev[i][1].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    launch_ms = sorted(s.elapsed_time(e) for s, e in ev)
+    avg_launch_ms = sum(launch_ms) / len(launch_ms)
+    res = {
+        "workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype,
+        "ms_per_step": total_ms / steps, "value": w.N * steps / (total_ms / 1e3),
+        "avg_launch_ms": avg_launch_ms, "median_launch_ms": launch_ms[len(launch_ms) // 2],
+        "wall_s": wall, "plan": q,
+    }
+    plan.close()
+    del out, a, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def roofline(res):
+    flops = res["plan"]["flops_per_pair"] * res["N"]
+    t = res["avg_launch_ms"] / 1e3
+    achieved = flops / t / 1e12
+    peak = PEAK_FP32_TFLOPS if res["dtype"] == "fp32" else PEAK_FP64_TFLOPS
+    hbm = res["plan"]["bytes_per_pair"] * res["N"] / t / 1e9
+    return {"bound": "alu", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "flops_per_launch": flops, "hbm_gbs_compulsory": round(hbm, 1),
+            "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4)}
+
+
+def cpu_baseline(w, budget_s):
+    import numpy as np
+
+    import cgtp_inputs
+    import oracle
+
+    x1, x2 = cgtp_inputs.workload_inputs(w)
+    a = x1.double().numpy()
+    b = x2.double().numpy()
+    oracle.cgtp(w.L, a[:1], b[:1])          # builds the coefficient table (reported separately)
+    table_s = oracle.table_build_seconds()
+    t0 = time.perf_counter()
+    oracle.cgtp(w.L, a[:1], b[:1])
+    t1 = max(time.perf_counter() - t0, 1e-6)
+    k = int(max(1, min(w.N, budget_s / t1)))
+    t0 = time.perf_counter()
+    oracle.cgtp(w.L, a[:k], b[:k])
+    dt = time.perf_counter() - t0
+    return {"value": round(k / dt, 4), "unit": "pairs/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": "first %d of the %d pairs of %s (naive O(L^6) fp64 oracle, OpenMP over pairs x l1; "
+                      "coefficient table built beforehand in %.2f s, not timed)" % (k, w.N, w.name, table_s),
+            "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="cgtp_L32_N1024_fp32")
+    ap.add_argument("--secondary", default="cgtp_L16_N8192_fp32")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only; --gpus %d is not supported "
+              "(pairs are independent: shard N across GPUs and run one process each)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import cgtp_inputs
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    by_name = {w.name: w for w in cgtp_inputs.WORKLOADS}
+    w = by_name[args.workload]
+    log("timing %s: %d warmup, %d steps" % (w.name, args.warmup, args.steps))
+    main_res = time_workload(w, args.steps, args.warmup)
+    log("  %.4f ms/step, %.4g pairs/s" % (main_res["ms_per_step"], main_res["value"]))
+    secondary = []
+    if args.secondary:
+        for name in args.secondary.split(","):
+            w2 = by_name[name]
+            log("timing %s" % w2.name)
+            r2 = time_workload(w2, args.steps, args.warmup)
+            log("  %.4f ms/step, %.4g pairs/s" % (r2["ms_per_step"], r2["value"]))
+            secondary.append({"workload": r2["workload"], "value": round(r2["value"], 1), "unit": "pairs/s",
+                              "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)})
+    line = {
+        "metric": METRIC, "value": round(main_res["value"], 1), "unit": "pairs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(main_res["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "fp32" else "f64", "data": "synthetic",
+        "config": {"workload": w.name, "L": w.L, "pairs": w.N, "outputs_per_pair": w.n_outputs,
+                   "grid": "per-block minimal exact Gauss-Legendre x FFT", "cover": "scalar-scalar + cross"},
+        "roofline": roofline(main_res),
+        "secondary": secondary,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,179 @@
+/*
+ * cgtp.h - C ABI of the MI355X (gfx950) full Clebsch-Gordan tensor product.
+ *
+ * The library computes, for N pairs of real irrep features x1, x2 holding one
+ * copy of every degree 0..L (the (0 + 1 + ... + L) representation of
+ * Appendix B), every Clebsch-Gordan path
+ *
+ *   z^(l1,l2,l3)_m3 = sum_{m1,m2} C^{l3 m3}_{l1 m1 l2 m2} x1^(l1)_m1 x2^(l2)_m2
+ *
+ * (the CGTP of Section 1 and Appendix F.1), the paper's way: each (l1, l2)
+ * block is one irrep-signal tensor product (Section 4.3).  Both inputs are
+ * lifted to scalar and toroidal vector signals on a sphere grid (tensor
+ * spherical harmonics, Definition 4.1), multiplied pointwise (scalar-scalar
+ * product and cross product, Section 5.1, or scalar-vector and dot product
+ * for the alternate cover), transformed back, and each path is divided by the
+ * factor the generalized Gaunt formula (Theorem 4.2) fixes.  Corollary 5.3 is
+ * what makes one such product per block enough.
+ *
+ * Conventions: complex spherical basis with Condon-Shortley phase
+ * (quantum-mechanics conventions, footnote of Section 3.3); coefficients are
+ * real numbers in that basis.  Index of (l, m) in a feature row: l^2 + l + m.
+ *
+ * Errors: every entry point returns a cgtp_status code; nothing is printed,
+ * no exception crosses the ABI, and a call that fails validation launches no
+ * GPU work.
+ */
+#ifndef CGTP_H
+#define CGTP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum cgtp_status {
+    CGTP_OK = 0,
+    CGTP_EINVAL = -1, /* bad argument: NULL pointer, negative size, misaligned or overlapping buffers */
+    CGTP_EGRID = -2,  /* grid too small to integrate the products exactly (it would alias) */
+    CGTP_EDTYPE = -3, /* unknown dtype */
+    CGTP_ENOMEM = -4, /* host or device allocation failed */
+    CGTP_EHIP = -5,   /* a HIP runtime call failed; cgtp_last_hip_error() has the HIP code */
+    CGTP_EUNSUP = -6  /* valid request this build does not support (L above CGTP_MAX_L, FFT size) */
+};
+
+enum cgtp_dtype { CGTP_FP32 = 0, CGTP_FP64 = 1 };
+
+/* Which products recover the paths (Corollary 5.3 leaves the choice open). */
+enum cgtp_cover {
+    /* even l1+l2+l3: scalar-scalar product (the Gaunt product, Section 3.3);
+       odd: cross product of the two toroidal vector lifts (l = j, s = 1),
+       projected on the l3 - 1 vector harmonics (Section 5.1). */
+    CGTP_COVER_DEFAULT = 0,
+    /* even: dot product of the toroidal lifts; odd: scalar x1 times toroidal
+       x2.  Paths whose dot-product factor vanishes by accident, or that have a
+       degree-0 input, fall back to the scalar-scalar product. */
+    CGTP_COVER_ALTERNATE = 1
+};
+
+#define CGTP_MAX_L 32
+
+/*
+ * Grid choice.  A zero field takes the default.
+ *   n_theta: 0 -> per-block minimal exact Gauss-Legendre grid (2*floor((l1+l2)/2)+2
+ *            nodes); else one grid for all blocks with this many nodes, which
+ *            must be even and >= 2L+2 (else CGTP_EGRID for < 2L+1, CGTP_EUNSUP
+ *            for odd values).
+ *   n_phi:   0 -> per-block smallest 2^a 3^b >= 2(l1+l2)+1 longitudes; else one
+ *            size for all blocks, which must be >= 4L+1 (else CGTP_EGRID) and
+ *            of the form 2^a 3^b (else CGTP_EUNSUP).
+ *   dtype:   CGTP_FP32 or CGTP_FP64; inputs and output share it.
+ *   cover:   enum cgtp_cover.
+ */
+typedef struct {
+    int32_t n_theta;
+    int32_t n_phi;
+    int32_t dtype;
+    int32_t cover;
+} cgtp_grid;
+
+typedef struct cgtp_plan_s *cgtp_plan_t;
+
+/*
+ * Builds a plan for degree L on the current HIP device: quadrature nodes,
+ * normalised associated Legendre tables, Clebsch-Gordan tables for the lifts
+ * and the recombination, and 1/K for every path (Theorem 4.2), uploaded to
+ * device memory the plan owns.  grid == NULL takes every default.
+ * Returns CGTP_EINVAL (L < 0, plan_out NULL), CGTP_EUNSUP (L > CGTP_MAX_L),
+ * CGTP_EDTYPE, CGTP_EGRID, CGTP_ENOMEM or CGTP_EHIP; *plan_out is set only on
+ * success.  Not timed work: call once per (L, grid).
+ */
+int cgtp_plan(int32_t L, const cgtp_grid *grid, cgtp_plan_t *plan_out);
+
+/*
+ * Full CGTP of N pairs, asynchronously on hip_stream (NULL: the default
+ * stream).  x1, x2: device arrays [N, (L+1)^2]; out: device array
+ * [N, (L+1)^4]; all row-major, contiguous, of the plan's dtype, 16-byte
+ * aligned.  Path (l1, l2, l3) of pair n occupies out[n, cgtp_path_offset(L,
+ * l1, l2, l3) + l3 + m3], m3 = -l3..l3.  The caller owns all three buffers;
+ * this call allocates nothing.  x1 == x2 is allowed; out overlapping an input
+ * is CGTP_EINVAL.  N == 0 returns CGTP_OK with no launch.  Launch failures
+ * return CGTP_EHIP; faults during execution surface when the caller
+ * synchronises.  A plan may be used from several streams at once.
+ */
+int cgtp_forward(cgtp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N,
+                 void *hip_stream);
+
+/* Frees the plan's device tables.  NULL is a no-op. */
+int cgtp_destroy(cgtp_plan_t plan);
+
+/* (L+1)^4, the output count per pair; -1 for L < 0. */
+int64_t cgtp_num_outputs(int32_t L);
+
+/* Offset of path (l1, l2, l3) within one pair's output: l1^2 (L+1)^2 +
+   (2 l1 + 1) l2^2 + l3^2 - (l1 - l2)^2; -1 if (l1, l2, l3) is not a path of
+   degree L. */
+int64_t cgtp_path_offset(int32_t L, int32_t l1, int32_t l2, int32_t l3);
+
+/*
+ * Plan facts: the largest grid used (n_theta, n_phi), the smallest |K| over
+ * the recovered paths, the algorithmic flops per pair of the method (every
+ * block on its minimal exact grid: lifts, longitude transforms at
+ * 2.5 n log2 n flops per Hermitian transform of n points, pointwise products,
+ * Legendre projection, recombination), and the compulsory HBM bytes per pair
+ * (inputs read once, output written once).  Any pointer may be NULL.
+ */
+int cgtp_plan_query(cgtp_plan_t plan, int32_t *n_theta, int32_t *n_phi, double *min_abs_K,
+                    double *flops_per_pair, double *bytes_per_pair);
+
+/* Static text for a status code. */
+const char *cgtp_strerror(int code);
+
+/* HIP error code of the last CGTP_EHIP on this thread (0 if none). */
+int cgtp_last_hip_error(void);
+
+/* ---- host-side math the plan is built from (no GPU needed) ---- */
+
+/*
+ * Per-path normalisation K of Theorem 4.2 for the product the given cover uses
+ * on path (j1, j2, j3): raw projection = K * z.  *kind receives 0 for the
+ * scalar-scalar product, 1 for the cross product, 2 for scalar-vector, 3 for
+ * the dot product.  Returns CGTP_EINVAL if (j1, j2, j3) violates the triangle
+ * rule or any degree is negative.
+ */
+int cgtp_path_norm(int32_t j1, int32_t j2, int32_t j3, int32_t cover, double *K, int32_t *kind);
+
+/* Wigner 9j symbol {a b c; d e f; g h i} (sum over products of three 6j
+   symbols; the recoupling coefficient defined in Appendix F.1), for testing the closed forms. */
+double cgtp_wigner_9j(int32_t a, int32_t b, int32_t c, int32_t d, int32_t e, int32_t f, int32_t g,
+                      int32_t h, int32_t i);
+
+/* Clebsch-Gordan coefficient C^{j m}_{j1 m1 1 q} for coupling with a vector
+   (closed forms of the j2 = 1 table); 0 outside the selection rules. */
+double cgtp_cg_vector(int32_t j1, int32_t m1, int32_t q, int32_t j, int32_t m);
+
+/* C^{l3 0}_{l1 0 l2 0} from the closed form of the 3j symbol with zero
+   projections; 0 when l1 + l2 + l3 is odd or the triangle rule fails. */
+double cgtp_cg_zero(int32_t l1, int32_t l2, int32_t l3);
+
+/* n Gauss-Legendre nodes (descending, x[0] closest to +1) and weights. */
+int cgtp_gauss_legendre(int32_t n, double *x, double *w);
+
+/* Normalised associated Legendre values P^m_l(x) with Condon-Shortley phase,
+   Y_l^m = P^m_l(cos theta) e^{i m phi}, for 0 <= m <= l <= lmax, written at
+   out[l (l + 1) / 2 + m]. */
+int cgtp_legendre(int32_t lmax, double x, double *out);
+
+/* Grid a block (l1, l2) uses under the given grid request: number of
+   Gauss-Legendre nodes (even; the kernel visits n_theta / 2 northern rings)
+   and longitudes. */
+int cgtp_block_grid(int32_t L, const cgtp_grid *grid, int32_t l1, int32_t l2, int32_t *n_theta,
+                    int32_t *n_phi);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CGTP_H */

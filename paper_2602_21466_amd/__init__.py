@@ -1,0 +1,215 @@
+"""Python binding of the MI355X CGTP library (libcgtp.so): argument marshalling only.
+
+Every step of the tensor product runs in the HIP kernels behind the C ABI
+declared in ``include/cgtp.h``; this module passes raw device pointers and a
+HIP stream through ctypes.  PyTorch is used for device memory and streams.
+There is no CPU fallback: if the shared library is missing or the GPU is
+absent, the calls raise.
+
+The functions carry the C names (``cgtp_plan``, ``cgtp_forward``, ...);
+``Plan`` is a small convenience wrapper around them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from ._build import LIB as _LIB_PATH
+
+CGTP_OK, CGTP_EINVAL, CGTP_EGRID, CGTP_EDTYPE, CGTP_ENOMEM, CGTP_EHIP, CGTP_EUNSUP = 0, -1, -2, -3, -4, -5, -6
+CGTP_FP32, CGTP_FP64 = 0, 1
+CGTP_COVER_DEFAULT, CGTP_COVER_ALTERNATE = 0, 1
+CGTP_MAX_L = 32
+KIND_NAMES = {0: "scalar-scalar", 1: "cross", 2: "scalar-vector", 3: "dot"}
+
+_lib = None
+
+
+class CgtpError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        msg = "%s failed: %s (%d)" % (where, cgtp_strerror(code), code)
+        if code == CGTP_EHIP:
+            msg += ", HIP error %d" % _load().cgtp_last_hip_error()
+        super().__init__(msg)
+
+
+class cgtp_grid(ctypes.Structure):
+    _fields_ = [("n_theta", ctypes.c_int32), ("n_phi", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("cover", ctypes.c_int32)]
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from ._build import build
+        build(force=False)
+    lib = ctypes.CDLL(_LIB_PATH)
+    i32, i64, vp, dp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)
+    sig = {
+        "cgtp_plan": (ctypes.c_int, [i32, ctypes.POINTER(cgtp_grid), ctypes.POINTER(vp)]),
+        "cgtp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
+        "cgtp_destroy": (ctypes.c_int, [vp]),
+        "cgtp_num_outputs": (i64, [i32]),
+        "cgtp_path_offset": (i64, [i32, i32, i32, i32]),
+        "cgtp_plan_query": (ctypes.c_int, [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), dp, dp, dp]),
+        "cgtp_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "cgtp_last_hip_error": (ctypes.c_int, []),
+        "cgtp_path_norm": (ctypes.c_int, [i32, i32, i32, i32, dp, ctypes.POINTER(i32)]),
+        "cgtp_wigner_9j": (ctypes.c_double, [i32] * 9),
+        "cgtp_cg_vector": (ctypes.c_double, [i32] * 5),
+        "cgtp_cg_zero": (ctypes.c_double, [i32] * 3),
+        "cgtp_gauss_legendre": (ctypes.c_int, [i32, vp, vp]),
+        "cgtp_legendre": (ctypes.c_int, [i32, ctypes.c_double, vp]),
+        "cgtp_block_grid": (ctypes.c_int, [i32, ctypes.POINTER(cgtp_grid), i32, i32,
+                                           ctypes.POINTER(i32), ctypes.POINTER(i32)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    """Names of the C ABI entry points this binding expects."""
+    return ["cgtp_plan", "cgtp_forward", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
+            "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
+            "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid"]
+
+
+def _check(rc: int, where: str):
+    if rc != CGTP_OK:
+        raise CgtpError(rc, where)
+
+
+def _grid(n_theta=0, n_phi=0, dtype="fp32", cover=0) -> cgtp_grid:
+    dt = {"fp32": CGTP_FP32, "fp64": CGTP_FP64}.get(dtype, dtype)
+    return cgtp_grid(int(n_theta), int(n_phi), int(dt), int(cover))
+
+
+# ---------------------------------------------------------------- C names
+
+def cgtp_strerror(code: int) -> str:
+    return _load().cgtp_strerror(int(code)).decode()
+
+
+def cgtp_plan(L: int, grid: cgtp_grid | None = None) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    rc = _load().cgtp_plan(int(L), ctypes.byref(grid) if grid is not None else None, ctypes.byref(h))
+    _check(rc, "cgtp_plan(L=%d)" % L)
+    return h
+
+
+def cgtp_forward(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, stream_ptr: int | None) -> None:
+    rc = _load().cgtp_forward(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(out_ptr),
+                              int(N), ctypes.c_void_p(stream_ptr) if stream_ptr else None)
+    _check(rc, "cgtp_forward")
+
+
+def cgtp_destroy(plan) -> None:
+    _check(_load().cgtp_destroy(plan), "cgtp_destroy")
+
+
+def cgtp_num_outputs(L: int) -> int:
+    return int(_load().cgtp_num_outputs(int(L)))
+
+
+def cgtp_path_offset(L: int, l1: int, l2: int, l3: int) -> int:
+    return int(_load().cgtp_path_offset(int(L), int(l1), int(l2), int(l3)))
+
+
+def cgtp_plan_query(plan) -> dict:
+    nt, nph = ctypes.c_int32(), ctypes.c_int32()
+    k, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(_load().cgtp_plan_query(plan, ctypes.byref(nt), ctypes.byref(nph), ctypes.byref(k), ctypes.byref(fl),
+                                   ctypes.byref(by)), "cgtp_plan_query")
+    return {"n_theta": nt.value, "n_phi": nph.value, "min_abs_K": k.value,
+            "flops_per_pair": fl.value, "bytes_per_pair": by.value}
+
+
+def cgtp_path_norm(j1: int, j2: int, j3: int, cover: int = 0):
+    K, kind = ctypes.c_double(), ctypes.c_int32()
+    _check(_load().cgtp_path_norm(j1, j2, j3, cover, ctypes.byref(K), ctypes.byref(kind)), "cgtp_path_norm")
+    return K.value, kind.value
+
+
+def cgtp_wigner_9j(*args) -> float:
+    return float(_load().cgtp_wigner_9j(*[int(a) for a in args]))
+
+
+def cgtp_cg_vector(j1, m1, q, j, m) -> float:
+    return float(_load().cgtp_cg_vector(j1, m1, q, j, m))
+
+
+def cgtp_cg_zero(l1, l2, l3) -> float:
+    return float(_load().cgtp_cg_zero(l1, l2, l3))
+
+
+def cgtp_gauss_legendre(n: int):
+    x = np.zeros(n)
+    w = np.zeros(n)
+    _check(_load().cgtp_gauss_legendre(n, x.ctypes.data, w.ctypes.data), "cgtp_gauss_legendre")
+    return x, w
+
+
+def cgtp_legendre(lmax: int, x: float) -> np.ndarray:
+    out = np.zeros((lmax + 1) * (lmax + 2) // 2)
+    _check(_load().cgtp_legendre(lmax, float(x), out.ctypes.data), "cgtp_legendre")
+    return out
+
+
+def cgtp_block_grid(L: int, l1: int, l2: int, grid: cgtp_grid | None = None):
+    nt, nph = ctypes.c_int32(), ctypes.c_int32()
+    _check(_load().cgtp_block_grid(L, ctypes.byref(grid) if grid is not None else None, l1, l2,
+                                   ctypes.byref(nt), ctypes.byref(nph)), "cgtp_block_grid")
+    return nt.value, nph.value
+
+
+# ---------------------------------------------------------------- convenience
+
+class Plan:
+    """Owns a cgtp plan; forward() takes and returns CUDA (HIP) torch tensors."""
+
+    def __init__(self, L: int, n_theta: int = 0, n_phi: int = 0, dtype: str = "fp32", cover: int = 0):
+        self.L = int(L)
+        self.dtype = dtype
+        self.grid = _grid(n_theta, n_phi, dtype, cover)
+        self._h = cgtp_plan(self.L, self.grid)
+
+    def query(self) -> dict:
+        return cgtp_plan_query(self._h)
+
+    def forward(self, x1, x2, out=None, stream=None):
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        nin = (self.L + 1) ** 2
+        for t in (x1, x2):
+            if not t.is_cuda or t.dtype != tdt or t.dim() != 2 or t.shape[1] != nin or not t.is_contiguous():
+                raise ValueError("inputs must be contiguous %s CUDA tensors [N, %d]" % (tdt, nin))
+        if x1.shape[0] != x2.shape[0]:
+            raise ValueError("x1 and x2 must hold the same number of pairs")
+        N = x1.shape[0]
+        if out is None:
+            out = torch.empty((N, cgtp_num_outputs(self.L)), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, cgtp_num_outputs(self.L)):
+            raise ValueError("out must be a contiguous %s tensor [N, (L+1)^4]" % tdt)
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        cgtp_forward(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, s.cuda_stream)
+        return out
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            cgtp_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,681 @@
+// Host side of the CGTP library: the math the plan is built from, the plan
+// itself (tables uploaded to device memory) and the C ABI entry points.
+//
+// Everything here runs once per plan and is not timed.  The device work is in
+// cgtp_kernels.hip.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <new>
+#include <vector>
+
+#include "../../include/cgtp.h"
+#include "cgtp_internal.h"
+
+using cgtp::BlockDesc;
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+// ------------------------------------------------------------------ factorials
+
+constexpr int kFactMax = 700;
+
+const long double* factorials() {
+    static long double f[kFactMax + 1];
+    static bool init = [] {
+        f[0] = 1.0L;
+        for (int i = 1; i <= kFactMax; ++i) f[i] = f[i - 1] * (long double)i;
+        return true;
+    }();
+    (void)init;
+    return f;
+}
+
+inline bool triangle(int a, int b, int c) {
+    return a >= 0 && b >= 0 && c >= 0 && c >= std::abs(a - b) && c <= a + b;
+}
+
+// ------------------------------------------------------------------ Wigner symbols
+
+// Triangle coefficient of a 6j symbol.
+long double tri_delta(int a, int b, int c) {
+    const long double* f = factorials();
+    return sqrtl(f[a + b - c] * f[a - b + c] * f[-a + b + c] / f[a + b + c + 1]);
+}
+
+// Wigner 6j symbol {j1 j2 j3; j4 j5 j6} by Racah's single-sum formula.
+long double sixj(int j1, int j2, int j3, int j4, int j5, int j6) {
+    if (!triangle(j1, j2, j3) || !triangle(j1, j5, j6) || !triangle(j4, j2, j6) ||
+        !triangle(j4, j5, j3))
+        return 0.0L;
+    const long double* f = factorials();
+    const int a1 = j1 + j2 + j3, a2 = j1 + j5 + j6, a3 = j4 + j2 + j6, a4 = j4 + j5 + j3;
+    const int b1 = j1 + j2 + j4 + j5, b2 = j2 + j3 + j5 + j6, b3 = j3 + j1 + j6 + j4;
+    const int tmin = std::max(std::max(a1, a2), std::max(a3, a4));
+    const int tmax = std::min(b1, std::min(b2, b3));
+    long double s = 0.0L;
+    for (int t = tmin; t <= tmax; ++t) {
+        long double term = f[t + 1] / (f[t - a1] * f[t - a2] * f[t - a3] * f[t - a4] * f[b1 - t] *
+                                       f[b2 - t] * f[b3 - t]);
+        s += (t & 1) ? -term : term;
+    }
+    return s * tri_delta(j1, j2, j3) * tri_delta(j1, j5, j6) * tri_delta(j4, j2, j6) *
+           tri_delta(j4, j5, j3);
+}
+
+// Wigner 9j symbol {a b c; d e f; g h i} as a sum over products of three 6j
+// symbols (integer arguments only).
+long double ninej(int a, int b, int c, int d, int e, int f, int g, int h, int i) {
+    if (!triangle(a, b, c) || !triangle(d, e, f) || !triangle(g, h, i) || !triangle(a, d, g) ||
+        !triangle(b, e, h) || !triangle(c, f, i))
+        return 0.0L;
+    int xmin = std::max(std::abs(a - i), std::max(std::abs(b - f), std::abs(d - h)));
+    int xmax = std::min(a + i, std::min(b + f, d + h));
+    long double s = 0.0L;
+    for (int x = xmin; x <= xmax; ++x)
+        s += (long double)(2 * x + 1) * sixj(a, b, c, f, i, x) * sixj(d, e, f, b, x, h) *
+             sixj(g, h, i, x, a, d);
+    return s;
+}
+
+// C^{j m}_{j1 m1 1 q}: closed forms of the coupling table with a vector.
+long double cg_vec(int j1, int m1, int q, int j, int m) {
+    if (j1 < 0 || j < 0 || q < -1 || q > 1) return 0.0L;
+    if (m != m1 + q || std::abs(m1) > j1 || std::abs(m) > j) return 0.0L;
+    if (!triangle(j1, 1, j)) return 0.0L;
+    const long double J1 = j1, M = m;
+    if (j == j1 + 1) {
+        const long double den2 = (2 * J1 + 1) * (2 * J1 + 2);
+        if (q == 1) return sqrtl((J1 + M) * (J1 + M + 1) / den2);
+        if (q == 0) return sqrtl((J1 - M + 1) * (J1 + M + 1) / ((2 * J1 + 1) * (J1 + 1)));
+        return sqrtl((J1 - M) * (J1 - M + 1) / den2);
+    }
+    if (j == j1) {
+        const long double den = 2 * J1 * (J1 + 1);
+        if (q == 1) return -sqrtl((J1 + M) * (J1 - M + 1) / den);
+        if (q == 0) return M / sqrtl(J1 * (J1 + 1));
+        return sqrtl((J1 - M) * (J1 + M + 1) / den);
+    }
+    // j == j1 - 1
+    const long double den = 2 * J1 * (2 * J1 + 1);
+    if (q == 1) return sqrtl((J1 - M) * (J1 - M + 1) / den);
+    if (q == 0) return -sqrtl((J1 - M) * (J1 + M) / (J1 * (2 * J1 + 1)));
+    return sqrtl((J1 + M + 1) * (J1 + M) / den);
+}
+
+// C^{l3 0}_{l1 0 l2 0} via the closed form of (l1 l2 l3; 0 0 0).
+long double cg_zero(int l1, int l2, int l3) {
+    if (!triangle(l1, l2, l3) || ((l1 + l2 + l3) & 1)) return 0.0L;
+    const long double* f = factorials();
+    const int g = (l1 + l2 + l3) / 2;
+    long double w3 = sqrtl(f[2 * g - 2 * l1] * f[2 * g - 2 * l2] * f[2 * g - 2 * l3] / f[2 * g + 1]) *
+                     f[g] / (f[g - l1] * f[g - l2] * f[g - l3]);
+    if (g & 1) w3 = -w3;
+    long double c = sqrtl((long double)(2 * l3 + 1)) * w3;
+    return ((l1 - l2) & 1) ? -c : c;
+}
+
+const long double kPi = 3.141592653589793238462643383279502884L;
+
+// Theorem 4.2's factor for lifts (j1, l1, s1), (j2, l2, s2) projected on
+// (j3, l3, s3): raw = K * z.
+long double gen_gaunt_K(int j1, int l1, int s1, int j2, int l2, int s2, int j3, int l3, int s3) {
+    long double pre = sqrtl((long double)(2 * j1 + 1) * (2 * j2 + 1) * (2 * l1 + 1) * (2 * l2 + 1) *
+                            (2 * s3 + 1) / (4.0L * kPi));
+    return pre * ninej(j1, l1, s1, j2, l2, s2, j3, l3, s3) * cg_zero(l1, l2, l3);
+}
+
+// Accidental zeros of a cover's factor are replaced by a fallback product.
+constexpr long double kMinAbsK = 1e-3L;
+
+// Chooses the product for path (j1, j2, j3) and returns its K.
+int path_norm(int j1, int j2, int j3, int cover, long double* K, int* kind) {
+    if (!triangle(j1, j2, j3)) return CGTP_EINVAL;
+    const bool even = ((j1 + j2 + j3) & 1) == 0;
+    const bool vec_ok = j1 > 0 && j2 > 0;  // a degree-0 input has no toroidal lift
+    if (cover == CGTP_COVER_ALTERNATE && vec_ok) {
+        if (even) {
+            long double k = gen_gaunt_K(j1, j1, 1, j2, j2, 1, j3, j3, 0);
+            if (fabsl(k) >= kMinAbsK) { *K = k; *kind = cgtp::kDot; return CGTP_OK; }
+        } else {
+            long double k = gen_gaunt_K(j1, j1, 0, j2, j2, 1, j3, j3 - 1, 1);
+            if (fabsl(k) >= kMinAbsK) { *K = k; *kind = cgtp::kSV; return CGTP_OK; }
+        }
+    }
+    if (even) {
+        *K = gen_gaunt_K(j1, j1, 0, j2, j2, 0, j3, j3, 0);
+        *kind = cgtp::kSS;
+    } else {
+        *K = gen_gaunt_K(j1, j1, 1, j2, j2, 1, j3, j3 - 1, 1);
+        *kind = cgtp::kCross;
+    }
+    return CGTP_OK;
+}
+
+// ------------------------------------------------------------------ quadrature
+
+void gauss_legendre(int n, std::vector<long double>& x, std::vector<long double>& w) {
+    x.assign(n, 0.0L);
+    w.assign(n, 0.0L);
+    for (int i = 0; i < n; ++i) {
+        long double z = cosl(kPi * (i + 0.75L) / (n + 0.5L));
+        long double dp = 1.0L;
+        for (int it = 0; it < 100; ++it) {
+            long double p0 = 1.0L, p1 = z;
+            for (int k = 2; k <= n; ++k) {
+                long double p2 = ((2 * k - 1) * z * p1 - (k - 1) * p0) / k;
+                p0 = p1;
+                p1 = p2;
+            }
+            if (n == 1) { p1 = z; p0 = 1.0L; }
+            dp = n * (z * p1 - p0) / (z * z - 1.0L);
+            long double dz = p1 / dp;
+            z -= dz;
+            if (fabsl(dz) < 1e-19L) break;
+        }
+        // recompute the derivative at the converged node
+        long double p0 = 1.0L, p1 = z;
+        for (int k = 2; k <= n; ++k) {
+            long double p2 = ((2 * k - 1) * z * p1 - (k - 1) * p0) / k;
+            p0 = p1;
+            p1 = p2;
+        }
+        dp = n * (z * p1 - p0) / (z * z - 1.0L);
+        x[i] = z;
+        w[i] = 2.0L / ((1.0L - z * z) * dp * dp);
+    }
+}
+
+// Normalised P^m_l(x) with Condon-Shortley phase at out[l(l+1)/2 + m].
+void legendre(int lmax, long double x, long double* out) {
+    auto at = [&](int l, int m) -> long double& { return out[l * (l + 1) / 2 + m]; };
+    const long double s = sqrtl(std::max(0.0L, 1.0L - x * x));
+    at(0, 0) = 1.0L / sqrtl(4.0L * kPi);
+    for (int m = 1; m <= lmax; ++m) at(m, m) = -sqrtl((2.0L * m + 1) / (2.0L * m)) * s * at(m - 1, m - 1);
+    for (int m = 0; m < lmax; ++m) at(m + 1, m) = x * sqrtl(2.0L * m + 3) * at(m, m);
+    for (int m = 0; m <= lmax; ++m)
+        for (int l = m + 2; l <= lmax; ++l) {
+            long double a = sqrtl((4.0L * l * l - 1) / ((long double)l * l - (long double)m * m));
+            long double b = sqrtl(((long double)(l - 1) * (l - 1) - (long double)m * m) /
+                                  (4.0L * (l - 1) * (l - 1) - 1));
+            at(l, m) = a * (x * at(l - 1, m) - b * at(l - 2, m));
+        }
+}
+
+// ------------------------------------------------------------------ grids
+
+bool is_2a3b(int n) {
+    if (n < 1) return false;
+    while (n % 2 == 0) n /= 2;
+    while (n % 3 == 0) n /= 3;
+    return n == 1;
+}
+
+int smallest_2a3b(int n) {
+    int m = std::max(n, 1);
+    while (!is_2a3b(m)) ++m;
+    return m;
+}
+
+// Radix-4 stages first, then radix 2, then radix 3.
+int radices(int n, int* rad) {
+    int k = 0;
+    while (n % 4 == 0) { rad[k++] = 4; n /= 4; }
+    while (n % 2 == 0) { rad[k++] = 2; n /= 2; }
+    while (n % 3 == 0) { rad[k++] = 3; n /= 3; }
+    return k;
+}
+
+constexpr int kMaxPhi = 512;
+
+int check_grid(int L, const cgtp_grid* g) {
+    if (g->dtype != CGTP_FP32 && g->dtype != CGTP_FP64) return CGTP_EDTYPE;
+    if (g->cover != CGTP_COVER_DEFAULT && g->cover != CGTP_COVER_ALTERNATE) return CGTP_EINVAL;
+    if (g->n_theta < 0 || g->n_phi < 0) return CGTP_EINVAL;
+    if (g->n_theta > 0) {
+        if (g->n_theta < 2 * L + 1) return CGTP_EGRID;
+        if (g->n_theta & 1) return CGTP_EUNSUP;
+        if (g->n_theta > 4 * CGTP_MAX_L + 64) return CGTP_EUNSUP;
+    }
+    if (g->n_phi > 0) {
+        if (g->n_phi < 4 * L + 1) return CGTP_EGRID;
+        if (!is_2a3b(g->n_phi) || g->n_phi > kMaxPhi) return CGTP_EUNSUP;
+    }
+    return CGTP_OK;
+}
+
+void block_grid(const cgtp_grid& g, int j1, int j2, int* n_theta, int* n_phi) {
+    const int J = j1 + j2;
+    *n_theta = g.n_theta > 0 ? g.n_theta : 2 * (J / 2) + 2;
+    *n_phi = g.n_phi > 0 ? g.n_phi : smallest_2a3b(2 * J + 1);
+}
+
+int64_t path_offset(int L, int l1, int l2, int l3) {
+    if (L < 0 || l1 < 0 || l2 < 0 || l1 > L || l2 > L) return -1;
+    if (l3 < std::abs(l1 - l2) || l3 > l1 + l2) return -1;
+    return (int64_t)l1 * l1 * (L + 1) * (L + 1) + (int64_t)(2 * l1 + 1) * l2 * l2 + (int64_t)l3 * l3 -
+           (int64_t)(l1 - l2) * (l1 - l2);
+}
+
+// Rows l3 = d, d+2, ..., J of a block's Legendre accumulator; entries per component.
+inline int acc_entries(int d, int J) {
+    const int nrows = (J - d) / 2 + 1;
+    return nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
+}
+
+// Algorithmic flops of one block on its minimal exact grid (default cover).
+double block_flops(int j1, int j2) {
+    const int J = j1 + j2, d = std::abs(j1 - j2);
+    const double R = J / 2 + 1, Phi = 2 * J + 1, H = J + 1;
+    const double f = Phi > 1 ? 2.5 * Phi * std::log2(Phi) : 0.0;
+    const bool vec = j1 > 0 && j2 > 0;
+    const double nin = vec ? 4 : 1;
+    double T = 0, rec = 0;
+    for (int j3 = d; j3 <= J; ++j3) {
+        if (((J + j3) & 1) == 0) { T += 2 * j3 + 1; rec += 2 * j3 + 1; }
+        else { T += 3 * (2 * (j3 - 1) + 1); rec += 7 * (2 * j3 + 1); }
+    }
+    return R * (2 * j1 + 1 + 2 * j2 + 1) * nin   // lift, latitude stage
+         + 2 * nin * R * f                       // lift, longitude synthesis
+         + R * H * (6 + (vec ? 60 : 0))          // pointwise products
+         + nin * R * f                           // longitude analysis
+         + 2 * R * T                             // Legendre projection
+         + rec;                                  // recombination and 1/K
+}
+
+}  // namespace
+
+// ====================================================================== plan
+
+struct cgtp_plan_s {
+    int L = 0;
+    cgtp_grid grid{};
+    int device = 0;
+    void* dmem = nullptr;      // all tables
+    size_t dbytes = 0;
+    cgtp::Tables<float> tf{};
+    cgtp::Tables<double> td{};
+    const int32_t* d_list = nullptr;   // block indices grouped by pairs-per-work-group
+    struct Cls { int pairs; int off; int count; };
+    std::vector<Cls> classes;
+    int lds_bytes = 0;
+    int max_theta = 0, max_phi = 0;
+    double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
+};
+
+namespace {
+
+template <typename T>
+struct HostTables {
+    std::vector<T> pbar, wt, tw, lcg, rcg, ccg, kinv;
+};
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+template <typename T>
+int lds_for(const BlockDesc& b, int pairs, int chunk) {
+    const bool cross = b.kind == cgtp::kBlockCross;
+    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
+    size_t bytes = sizeof(T) * (size_t)pairs * (2 * b.j1 + 1 + 2 * b.j2 + 1);
+    bytes += sizeof(T) * (size_t)pairs * ncomp * acc_entries(b.d, b.J);
+    bytes = align_up(bytes, 16);
+    bytes += 2 * sizeof(T) * 2 * (size_t)chunk * pairs * nslot * b.Phi;
+    return (int)bytes;
+}
+
+template <typename T>
+int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std::vector<int32_t>& list) {
+    const int L = p->L;
+    const cgtp_grid& g = p->grid;
+    // ---- grids: one Legendre table per distinct node count
+    std::map<int, int> grid_lmax;          // n_theta -> largest degree needed
+    std::map<int, int> phi_set;            // Phi -> twiddle offset
+    for (int j1 = 0; j1 <= L; ++j1)
+        for (int j2 = 0; j2 <= L; ++j2) {
+            int nt, np;
+            block_grid(g, j1, j2, &nt, &np);
+            grid_lmax[nt] = std::max(grid_lmax[nt], j1 + j2);
+            phi_set[np] = 0;
+        }
+    std::map<int, int> grid_pbar_off, grid_wt_off, grid_stride;
+    for (auto& kv : grid_lmax) {
+        const int nt = kv.first, lmax = kv.second, R = nt / 2;
+        std::vector<long double> x, w;
+        gauss_legendre(nt, x, w);
+        const int stride = (lmax + 1) * (lmax + 2) / 2;
+        grid_pbar_off[nt] = (int)h.pbar.size();
+        grid_wt_off[nt] = (int)h.wt.size();
+        grid_stride[nt] = stride;
+        std::vector<long double> row(stride);
+        for (int i = 0; i < R; ++i) {
+            legendre(lmax, x[i], row.data());
+            for (int e = 0; e < stride; ++e) h.pbar.push_back((T)row[e]);
+            h.wt.push_back((T)(2.0L * w[i]));   // north and south rings folded
+        }
+        p->max_theta = std::max(p->max_theta, nt);
+    }
+    for (auto& kv : phi_set) {
+        const int n = kv.first;
+        kv.second = (int)(h.tw.size() / 2);
+        for (int k = 0; k < n; ++k) {
+            long double a = -2.0L * kPi * k / n;
+            h.tw.push_back((T)cosl(a));
+            h.tw.push_back((T)sinl(a));
+        }
+        p->max_phi = std::max(p->max_phi, n);
+    }
+    // ---- Clebsch-Gordan tables
+    h.lcg.assign(3 * (size_t)(L + 1) * (L + 1), (T)0);
+    for (int j = 0; j <= L; ++j)
+        for (int q = -1; q <= 1; ++q)
+            for (int m = -j; m <= j; ++m)
+                h.lcg[3 * j * j + (q + 1) * (2 * j + 1) + m + j] = (T)cg_vec(j, m, q, j, m + q);
+    h.rcg.assign(3 * (size_t)(2 * L + 1) * (2 * L + 1), (T)0);
+    for (int j3 = 1; j3 <= 2 * L; ++j3)
+        for (int q = -1; q <= 1; ++q)
+            for (int m3 = -j3; m3 <= j3; ++m3)
+                h.rcg[3 * j3 * j3 + (q + 1) * (2 * j3 + 1) + m3 + j3] = (T)cg_vec(j3 - 1, m3 - q, q, j3, m3);
+    h.ccg.assign(9, (T)0);
+    for (int q1 = -1; q1 <= 1; ++q1)
+        for (int q2 = -1; q2 <= 1; ++q2) h.ccg[(q1 + 1) * 3 + q2 + 1] = (T)cg_vec(1, q1, q2, 1, q1 + q2);
+    // ---- blocks
+    double min_abs_K = 1e300, flops = 0;
+    blocks.clear();
+    for (int j1 = 0; j1 <= L; ++j1)
+        for (int j2 = 0; j2 <= L; ++j2) {
+            BlockDesc b{};
+            b.j1 = j1; b.j2 = j2; b.J = j1 + j2; b.d = std::abs(j1 - j2);
+            int nt, np;
+            block_grid(g, j1, j2, &nt, &np);
+            b.R = nt / 2;
+            b.Phi = np;
+            b.kind = (j1 > 0 && j2 > 0) ? cgtp::kBlockCross : cgtp::kBlockScalar;
+            b.nrad = radices(np, b.rad);
+            b.tw_off = phi_set[np];
+            b.pbar_off = grid_pbar_off[nt];
+            b.pbar_stride = grid_stride[nt];
+            b.wt_off = grid_wt_off[nt];
+            b.kinv_off = (int)h.kinv.size();
+            for (int j3 = b.d; j3 <= b.J; ++j3) {
+                long double K;
+                int kind;
+                if (path_norm(j1, j2, j3, CGTP_COVER_DEFAULT, &K, &kind) != CGTP_OK) return CGTP_EINVAL;
+                const int want = ((b.J + j3) & 1) ? cgtp::kCross : cgtp::kSS;
+                if (kind != want || fabsl(K) < kMinAbsK) return CGTP_EUNSUP;
+                min_abs_K = std::min(min_abs_K, (double)fabsl(K));
+                h.kinv.push_back((T)(1.0L / K));
+            }
+            b.out_off = path_offset(L, j1, j2, b.d);
+            flops += block_flops(j1, j2);
+            // LDS: all rings in one pass if possible, then as many pairs as fit
+            int chunk = b.R;
+            while (chunk > 1 && lds_for<T>(b, 1, chunk) > cgtp::kLdsBudget) --chunk;
+            if (lds_for<T>(b, 1, chunk) > cgtp::kLdsBudget) return CGTP_EUNSUP;
+            int pairs = 1;
+            const int nslot = b.kind == cgtp::kBlockCross ? 4 : 2;
+            while (pairs < 32 && lds_for<T>(b, 2 * pairs, chunk) <= cgtp::kLdsBudget &&
+                   chunk * pairs * nslot * b.Phi < 4096)
+                pairs *= 2;
+            b.chunk = chunk;
+            b.pairs = pairs;
+            b.lds_bytes = lds_for<T>(b, pairs, chunk);
+            p->lds_bytes = std::max(p->lds_bytes, b.lds_bytes);
+            blocks.push_back(b);
+        }
+    p->min_abs_K = min_abs_K;
+    p->flops_per_pair = flops;
+    p->bytes_per_pair = (double)sizeof(T) * (2.0 * (L + 1) * (L + 1) + std::pow((double)(L + 1), 4));
+    // ---- launch classes: fewest pairs (heaviest blocks) first; inside, by cost
+    std::map<int, std::vector<int>> by_pairs;
+    for (int i = 0; i < (int)blocks.size(); ++i) by_pairs[blocks[i].pairs].push_back(i);
+    list.clear();
+    p->classes.clear();
+    if ((int)by_pairs.size() > cgtp::kMaxClasses) return CGTP_EUNSUP;
+    for (auto& kv : by_pairs) {
+        auto& v = kv.second;
+        std::stable_sort(v.begin(), v.end(), [&](int a, int b) {
+            const BlockDesc &x = blocks[a], &y = blocks[b];
+            return (double)x.R * x.Phi * (x.J + 1) > (double)y.R * y.Phi * (y.J + 1);
+        });
+        p->classes.push_back({kv.first, (int)list.size(), (int)v.size()});
+        list.insert(list.end(), v.begin(), v.end());
+    }
+    return CGTP_OK;
+}
+
+template <typename T>
+int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTables<T>& h,
+           const std::vector<int32_t>& list, cgtp::Tables<T>* tb) {
+    const std::vector<T>* parts[] = {&h.pbar, &h.wt, &h.tw, &h.lcg, &h.rcg, &h.ccg, &h.kinv};
+    size_t offs[9];
+    size_t total = 0;
+    for (int i = 0; i < 7; ++i) {
+        offs[i] = total;
+        total = align_up(total + parts[i]->size() * sizeof(T), 256);
+    }
+    offs[7] = total;
+    total = align_up(total + blocks.size() * sizeof(BlockDesc), 256);
+    offs[8] = total;
+    total = align_up(total + list.size() * sizeof(int32_t), 256);
+    std::vector<char> host(total, 0);
+    for (int i = 0; i < 7; ++i)
+        if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
+    std::memcpy(host.data() + offs[7], blocks.data(), blocks.size() * sizeof(BlockDesc));
+    std::memcpy(host.data() + offs[8], list.data(), list.size() * sizeof(int32_t));
+    hipError_t e = hipMalloc(&p->dmem, total);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        p->dmem = nullptr;
+        return e == hipErrorOutOfMemory ? CGTP_ENOMEM : CGTP_EHIP;
+    }
+    e = hipMemcpy(p->dmem, host.data(), total, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        (void)hipFree(p->dmem);
+        p->dmem = nullptr;
+        return CGTP_EHIP;
+    }
+    p->dbytes = total;
+    char* base = (char*)p->dmem;
+    tb->pbar = (const T*)(base + offs[0]);
+    tb->wt = (const T*)(base + offs[1]);
+    tb->tw = (const T*)(base + offs[2]);
+    tb->lcg = (const T*)(base + offs[3]);
+    tb->rcg = (const T*)(base + offs[4]);
+    tb->ccg = (const T*)(base + offs[5]);
+    tb->kinv = (const T*)(base + offs[6]);
+    tb->blocks = (const BlockDesc*)(base + offs[7]);
+    p->d_list = (const int32_t*)(base + offs[8]);
+    return CGTP_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const char *pa = (const char*)a, *pb = (const char*)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+
+extern "C" {
+
+const char* cgtp_strerror(int code) {
+    switch (code) {
+        case CGTP_OK: return "success";
+        case CGTP_EINVAL: return "invalid argument";
+        case CGTP_EGRID: return "grid too small for exact quadrature";
+        case CGTP_EDTYPE: return "unknown dtype";
+        case CGTP_ENOMEM: return "out of memory";
+        case CGTP_EHIP: return "HIP runtime error";
+        case CGTP_EUNSUP: return "unsupported by this build";
+        default: return "unknown status";
+    }
+}
+
+int cgtp_last_hip_error(void) { return g_last_hip_error; }
+
+int64_t cgtp_num_outputs(int32_t L) {
+    if (L < 0) return -1;
+    const int64_t a = (int64_t)(L + 1) * (L + 1);
+    return a * a;
+}
+
+int64_t cgtp_path_offset(int32_t L, int32_t l1, int32_t l2, int32_t l3) { return path_offset(L, l1, l2, l3); }
+
+int cgtp_path_norm(int32_t j1, int32_t j2, int32_t j3, int32_t cover, double* K, int32_t* kind) {
+    if (cover != CGTP_COVER_DEFAULT && cover != CGTP_COVER_ALTERNATE) return CGTP_EINVAL;
+    if (j1 > 4 * CGTP_MAX_L || j2 > 4 * CGTP_MAX_L) return CGTP_EUNSUP;
+    long double k = 0;
+    int kd = 0;
+    int rc = path_norm(j1, j2, j3, cover, &k, &kd);
+    if (rc != CGTP_OK) return rc;
+    if (K) *K = (double)k;
+    if (kind) *kind = kd;
+    return CGTP_OK;
+}
+
+double cgtp_wigner_9j(int32_t a, int32_t b, int32_t c, int32_t d, int32_t e, int32_t f, int32_t g, int32_t h,
+                      int32_t i) {
+    if (a + b + c + d + e + f + g + h + i > kFactMax / 2) return NAN;
+    return (double)ninej(a, b, c, d, e, f, g, h, i);
+}
+
+double cgtp_cg_vector(int32_t j1, int32_t m1, int32_t q, int32_t j, int32_t m) {
+    return (double)cg_vec(j1, m1, q, j, m);
+}
+
+double cgtp_cg_zero(int32_t l1, int32_t l2, int32_t l3) {
+    if (l1 + l2 + l3 > kFactMax / 2) return NAN;
+    return (double)cg_zero(l1, l2, l3);
+}
+
+int cgtp_gauss_legendre(int32_t n, double* x, double* w) {
+    if (n < 1 || n > 4096 || !x || !w) return CGTP_EINVAL;
+    std::vector<long double> xs, ws;
+    gauss_legendre(n, xs, ws);
+    for (int i = 0; i < n; ++i) { x[i] = (double)xs[i]; w[i] = (double)ws[i]; }
+    return CGTP_OK;
+}
+
+int cgtp_legendre(int32_t lmax, double x, double* out) {
+    if (lmax < 0 || lmax > 4096 || !out || !(x >= -1.0 && x <= 1.0)) return CGTP_EINVAL;
+    std::vector<long double> v((size_t)(lmax + 1) * (lmax + 2) / 2);
+    legendre(lmax, x, v.data());
+    for (size_t i = 0; i < v.size(); ++i) out[i] = (double)v[i];
+    return CGTP_OK;
+}
+
+int cgtp_block_grid(int32_t L, const cgtp_grid* grid, int32_t l1, int32_t l2, int32_t* n_theta, int32_t* n_phi) {
+    if (L < 0 || l1 < 0 || l2 < 0 || l1 > L || l2 > L || !n_theta || !n_phi) return CGTP_EINVAL;
+    if (L > CGTP_MAX_L) return CGTP_EUNSUP;
+    cgtp_grid g = grid ? *grid : cgtp_grid{0, 0, CGTP_FP32, CGTP_COVER_DEFAULT};
+    int rc = check_grid(L, &g);
+    if (rc != CGTP_OK) return rc;
+    int nt, np;
+    block_grid(g, l1, l2, &nt, &np);
+    *n_theta = nt;
+    *n_phi = np;
+    return CGTP_OK;
+}
+
+int cgtp_plan(int32_t L, const cgtp_grid* grid, cgtp_plan_t* plan_out) {
+    if (!plan_out || L < 0) return CGTP_EINVAL;
+    if (L > CGTP_MAX_L) return CGTP_EUNSUP;
+    cgtp_grid g = grid ? *grid : cgtp_grid{0, 0, CGTP_FP32, CGTP_COVER_DEFAULT};
+    int rc = check_grid(L, &g);
+    if (rc != CGTP_OK) return rc;
+    if (g.cover != CGTP_COVER_DEFAULT) return CGTP_EUNSUP;
+    cgtp_plan_s* p = new (std::nothrow) cgtp_plan_s();
+    if (!p) return CGTP_ENOMEM;
+    p->L = L;
+    p->grid = g;
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        delete p;
+        return CGTP_EHIP;
+    }
+    std::vector<BlockDesc> blocks;
+    std::vector<int32_t> list;
+    if (g.dtype == CGTP_FP32) {
+        HostTables<float> h;
+        rc = build<float>(p, blocks, h, list);
+        if (rc == CGTP_OK) rc = upload<float>(p, blocks, h, list, &p->tf);
+    } else {
+        HostTables<double> h;
+        rc = build<double>(p, blocks, h, list);
+        if (rc == CGTP_OK) rc = upload<double>(p, blocks, h, list, &p->td);
+    }
+    if (rc != CGTP_OK) {
+        delete p;
+        return rc;
+    }
+    *plan_out = p;
+    return CGTP_OK;
+}
+
+int cgtp_destroy(cgtp_plan_t plan) {
+    if (!plan) return CGTP_OK;
+    int rc = CGTP_OK;
+    if (plan->dmem) {
+        hipError_t e = hipFree(plan->dmem);
+        if (e != hipSuccess) { g_last_hip_error = (int)e; rc = CGTP_EHIP; }
+    }
+    delete plan;
+    return rc;
+}
+
+int cgtp_plan_query(cgtp_plan_t plan, int32_t* n_theta, int32_t* n_phi, double* min_abs_K, double* flops_per_pair,
+                    double* bytes_per_pair) {
+    if (!plan) return CGTP_EINVAL;
+    if (n_theta) *n_theta = plan->max_theta;
+    if (n_phi) *n_phi = plan->max_phi;
+    if (min_abs_K) *min_abs_K = plan->min_abs_K;
+    if (flops_per_pair) *flops_per_pair = plan->flops_per_pair;
+    if (bytes_per_pair) *bytes_per_pair = plan->bytes_per_pair;
+    return CGTP_OK;
+}
+
+int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+    const int L = plan->L;
+    const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)(L + 1) * (L + 1), nout = (size_t)cgtp_num_outputs(L);
+    if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin)) return CGTP_EINVAL;
+    cgtp::LaunchMap map{};
+    map.ncls = (int32_t)plan->classes.size();
+    map.cum[0] = 0;
+    for (int c = 0; c < map.ncls; ++c) {
+        const auto& cl = plan->classes[c];
+        map.pairs[c] = cl.pairs;
+        map.list_off[c] = cl.off;
+        map.ntiles[c] = (N + cl.pairs - 1) / cl.pairs;
+        map.cum[c + 1] = map.cum[c] + map.ntiles[c] * cl.count;
+    }
+    int err;
+    if (plan->grid.dtype == CGTP_FP32)
+        err = cgtp::launch_blocks_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
+                                      (const float*)x2, (float*)out, N, L, hip_stream);
+    else
+        err = cgtp::launch_blocks_f64(plan->td, plan->d_list, map, plan->lds_bytes, (const double*)x1,
+                                      (const double*)x2, (double*)out, N, L, hip_stream);
+    if (err != 0) {
+        g_last_hip_error = err;
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
+
+}  // extern "C"

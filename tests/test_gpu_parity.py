@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 CPU oracle.
+
+Bar: per-path relative L2 error (over every checked pair and component of the
+path) <= 1e-4 for fp32 workloads and <= 1e-10 for fp64 ones.  Full-size
+workloads run in the benchmark's launch configuration and are compared on a
+seeded subsample of pairs, plus identities checked on every pair.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import cgtp_inputs as wl
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "fp64": 1e-10}
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _lib():
+    import paper_2602_21466_amd as lib
+    return lib
+
+
+def path_ids(L):
+    """Path index of every output column, and the list of (l1, l2, l3)."""
+    pid = np.empty((L + 1) ** 4, dtype=np.int64)
+    paths = []
+    for l1 in range(L + 1):
+        for l2 in range(L + 1):
+            for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+                off = oracle.path_offset(L, l1, l2, l3)
+                pid[off:off + 2 * l3 + 1] = len(paths)
+                paths.append((l1, l2, l3))
+    return pid, paths
+
+
+def per_path_rel_err(L, got, ref):
+    pid, paths = path_ids(L)
+    num = np.bincount(pid, weights=((got - ref) ** 2).sum(0), minlength=len(paths))
+    den = np.bincount(pid, weights=(ref ** 2).sum(0), minlength=len(paths))
+    # a path that is exactly zero (x1 = x2, l1 = l2, odd l3) is held to the scale of a typical path
+    typical = np.median(den[den > 0]) if (den > 0).any() else 1.0
+    rel = np.sqrt(num / np.where(den > 1e-20 * typical, den, typical))
+    worst = int(np.argmax(rel))
+    return float(rel[worst]), paths[worst]
+
+
+def run_gpu(L, x1, x2, dtype, **grid):
+    torch = _torch()
+    plan = _lib().Plan(L, dtype=dtype, **grid)
+    a = x1.to("cuda")
+    b = x2.to("cuda") if x2 is not x1 else a
+    out = plan.forward(a, b)
+    torch.cuda.synchronize()
+    return plan, a, b, out
+
+
+def check_against_oracle(L, x1, x2, got, dtype, idx=None):
+    x1d = x1.double().numpy()
+    x2d = x2.double().numpy()
+    if idx is not None:
+        x1d, x2d = x1d[idx], x2d[idx]
+    ref = oracle.cgtp(L, x1d, x2d)
+    err, path = per_path_rel_err(L, got, ref)
+    print("L=%d dtype=%s checked=%d worst per-path rel L2 %.3e at %s" % (L, dtype, ref.shape[0], err, path),
+          flush=True)
+    assert err <= TOL[dtype], (err, path)
+    return err
+
+
+def block_energy_check(L, a, b, out, rtol):
+    """sum_l3 |z^(l1,l2,l3)|^2 = |x1^(l1)|^2 |x2^(l2)|^2 on every pair (CG unitarity)."""
+    torch = _torch()
+    N = out.shape[0]
+    blk_of_col = torch.empty((L + 1) ** 4, dtype=torch.long)
+    for l1 in range(L + 1):
+        for l2 in range(L + 1):
+            off = oracle.path_offset(L, l1, l2, abs(l1 - l2))
+            blk_of_col[off:off + (2 * l1 + 1) * (2 * l2 + 1)] = l1 * (L + 1) + l2
+    blk_of_col = blk_of_col.cuda()
+    deg_of_in = torch.tensor([l for l in range(L + 1) for _ in range(2 * l + 1)], device="cuda")
+    worst = 0.0
+    step = max(1, int(2e8 // out.shape[1]))
+    for s in range(0, N, step):
+        z = out[s:s + step].double()
+        e = torch.zeros(z.shape[0], (L + 1) ** 2, dtype=torch.float64, device="cuda")
+        e.index_add_(1, blk_of_col, z * z)
+        n1 = torch.zeros(z.shape[0], L + 1, dtype=torch.float64, device="cuda").index_add_(
+            1, deg_of_in, a[s:s + step].double() ** 2)
+        n2 = torch.zeros(z.shape[0], L + 1, dtype=torch.float64, device="cuda").index_add_(
+            1, deg_of_in, b[s:s + step].double() ** 2)
+        want = (n1[:, :, None] * n2[:, None, :]).reshape(z.shape[0], -1)
+        rel = ((e - want).abs() / want.clamp_min(1e-30)).max().item()
+        worst = max(worst, rel)
+    print("block energy: worst relative deviation %.3e over %d pairs" % (worst, N), flush=True)
+    assert worst <= rtol
+
+
+# ------------------------------------------------------------ full workloads
+
+SUBSAMPLE = {2: None, 4: 2048, 8: 256}
+
+
+@pytest.mark.parametrize("w", wl.WORKLOADS, ids=[w.name for w in wl.WORKLOADS])
+def test_workload_parity(w):
+    torch = _torch()
+    print("workload %s L=%d N=%d %s" % (w.name, w.L, w.N, w.dtype), flush=True)
+    x1, x2 = wl.workload_inputs(w)
+    plan, a, b, out = run_gpu(w.L, x1, x2, w.dtype)
+    if w.check_pairs:
+        idx = wl.check_indices(w).numpy()
+    elif SUBSAMPLE.get(w.L):
+        g = np.random.default_rng(w.seed)
+        idx = np.unique(np.concatenate([[0, w.N - 1], g.choice(w.N, SUBSAMPLE[w.L], replace=False)]))
+    else:
+        idx = np.arange(w.N)
+    got = out[torch.as_tensor(idx, device="cuda")].double().cpu().numpy()
+    check_against_oracle(w.L, x1, x2, got, w.dtype, idx)
+    block_energy_check(w.L, a, b, out, 1e-4 if w.dtype == "fp32" else 1e-11)
+    assert torch.isfinite(out).all().item()
+
+
+# ------------------------------------------------------------ small cases, every element
+
+@pytest.mark.parametrize("L,N,dtype", [(0, 5, "fp32"), (1, 1, "fp32"), (2, 33, "fp64"), (3, 37, "fp32"),
+                                       (5, 1000, "fp32"), (6, 130, "fp64"), (12, 41, "fp32"), (20, 7, "fp32")])
+def test_small_parity(L, N, dtype):
+    torch = _torch()
+    x1, x2 = wl.draw(L, N, dtype, seed=1000 + L)
+    _, _, _, out = run_gpu(L, x1, x2, dtype)
+    check_against_oracle(L, x1, x2, out.double().cpu().numpy(), dtype)
+
+
+def test_zero_pairs_launches_nothing():
+    torch = _torch()
+    lib = _lib()
+    plan = lib.Plan(3)
+    x = torch.zeros(0, 16, device="cuda")
+    out = torch.full((0, 256), 7.0, device="cuda")
+    plan.forward(x, x, out)
+    torch.cuda.synchronize()
+
+
+def test_aliased_inputs():
+    """x1 == x2 (one buffer): odd paths with l1 = l2 vanish."""
+    torch = _torch()
+    L = 6
+    x1, _ = wl.draw(L, 50, "fp32", seed=77)
+    _, a, _, out = run_gpu(L, x1, x1, "fp32")
+    got = out.double().cpu().numpy()
+    check_against_oracle(L, x1, x1, got, "fp32")
+    for l in range(L + 1):
+        for l3 in range(1, 2 * l + 1, 2):
+            off = oracle.path_offset(L, l, l, l3)
+            assert np.abs(got[:, off:off + 2 * l3 + 1]).max() < 1e-4
+
+
+def test_global_grid_agrees():
+    torch = _torch()
+    L = 7
+    x1, x2 = wl.draw(L, 64, "fp32", seed=5)
+    _, _, _, out = run_gpu(L, x1, x2, "fp32", n_theta=2 * L + 4, n_phi=36)
+    check_against_oracle(L, x1, x2, out.double().cpu().numpy(), "fp32")
+
+
+def test_deterministic_and_stream():
+    torch = _torch()
+    lib = _lib()
+    L = 9
+    x1, x2 = wl.draw(L, 300, "fp32", seed=9)
+    plan = lib.Plan(L)
+    a, b = x1.cuda(), x2.cuda()
+    o1 = plan.forward(a, b)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        o2 = plan.forward(a, b, stream=s)
+    s.synchronize()
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+
+
+def test_forward_rejects_overlap_and_misalignment():
+    torch = _torch()
+    lib = _lib()
+    L = 2
+    plan = lib.Plan(L)
+    buf = torch.zeros(4 * 81 + 64, device="cuda")
+    x = buf[:4 * 9].view(4, 9)
+    with pytest.raises(lib.CgtpError) as e:
+        lib.cgtp_forward(plan._h, x.data_ptr(), x.data_ptr(), buf.data_ptr(), 4, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:
+        lib.cgtp_forward(plan._h, x.data_ptr() + 4, x.data_ptr(), buf.data_ptr() + 4 * 200, 1, None)
+    assert e.value.code == lib.CGTP_EINVAL
