@@ -67,8 +67,8 @@ enum cgtp_cover {
  *            must be even and >= 2L+2 (else CGTP_EGRID for < 2L+1, CGTP_EUNSUP
  *            for odd values).
  *   n_phi:   0 -> per-block smallest 2^a 3^b >= 2(l1+l2)+1 longitudes; else one
- *            size for all blocks, which must be >= 4L+1 (else CGTP_EGRID) and
- *            of the form 2^a 3^b (else CGTP_EUNSUP).
+ *            size for all blocks, which must be >= 4L+1 (else CGTP_EGRID), at
+ *            most 144 and of the form 2^a 3^b (else CGTP_EUNSUP).
  *   dtype:   CGTP_FP32 or CGTP_FP64; inputs and output share it.
  *   cover:   enum cgtp_cover.
  */

@@ -2,52 +2,72 @@
 // (cgtp_kernels.hip).  Not part of the public ABI.
 #pragma once
 
+#include <hip/hip_runtime.h>
+
 #include <cstdint>
 
 namespace cgtp {
 
-constexpr int kMaxRadix = 8;       // FFT stages per transform
-constexpr int kThreads = 256;      // work-group size of the block kernel
-constexpr int kLdsBudget = 64 * 1024;
+constexpr int kThreads = 256;      // work-group size of the block kernel (4 wave64s)
+constexpr int kWaves = kThreads / 64;
+constexpr int kRingGroup = 4;      // rings per pass: the K depth of one 16x16x4 MFMA
+constexpr int kLdsBudget = 80 * 1024;
+constexpr int kMaxPairs = 16;
+
+// MFMA accumulator tiles (16 x 16) each wave may hold, per precision.
+template <typename T> struct MaxTiles;
+template <> struct MaxTiles<float> { static constexpr int value = 28; };
+template <> struct MaxTiles<double> { static constexpr int value = 12; };
 
 // Product kinds per path (mirrors cgtp_path_norm's *kind).
 enum PathKind : int32_t { kSS = 0, kCross = 1, kSV = 2, kDot = 3 };
 
-// One (j1, j2) block: one irrep-signal tensor product on its own grid.
-// Block kinds: which lifts/products the block needs.
+// Which lifts and products a block needs.
 enum BlockKind : int32_t {
     kBlockScalar = 0,   // only scalar-scalar paths (a degree-0 input)
     kBlockCross = 1,    // scalar-scalar (even paths) + cross (odd paths)
 };
 
+// One (j1, j2) block: one irrep-signal tensor product on its own grid.
+//
+// The Phi-point longitude transforms run as two in-register passes: pass 1
+// does A transforms of length B over stride-A inputs, pass 2 does B transforms
+// of length A (Phi = A * B, natural-order output, in place in LDS).
+//
+// The Legendre projection is a batch of small GEMMs, one per |m|: rows
+// l3 = d, d+2, ..., J (those >= |m|), K = rings, columns (sign of m,
+// component, pair).  It runs on 16x16x4 MFMA tiles whose accumulators stay in
+// registers across all rings.
 struct alignas(16) BlockDesc {
     int32_t j1, j2, J, d;      // d = |j1 - j2|
     int32_t R;                 // northern rings of the block's grid
-    int32_t Phi;               // longitudes (FFT size)
+    int32_t Phi, A, B;         // longitudes, Phi = A * B
     int32_t kind;              // BlockKind
-    int32_t nrad;              // FFT stages
-    int32_t rad[kMaxRadix];    // radices, first stage first
+    int32_t pairs;             // pairs per work-group
+    int32_t ntiles;            // MFMA accumulator tiles per work-group
+    int32_t lds_bytes;         // dynamic LDS of one work-group
     int32_t tw_off;            // offset of the Phi-point twiddle table (complex entries)
     int32_t pbar_off;          // offset of the grid's Legendre table (elements)
     int32_t pbar_stride;       // Legendre entries per ring: (lmax+1)(lmax+2)/2
-    int32_t wt_off;            // offset of the grid's ring weights
+    int32_t wtab_off;          // offset of the grid's MFMA weight table (elements)
+    int32_t lmax;              // largest degree of the grid's tables
     int32_t kinv_off;          // offset of 1/K for j3 = d..J
-    int32_t chunk;             // rings per pass through LDS
-    int32_t pairs;             // pairs per work-group
-    int32_t lds_bytes;         // dynamic LDS of one work-group
+    int32_t pad0, pad1;
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
 // Device tables, one allocation per plan; offsets in elements of T.
+//   wtab[grid]: for m' = 0..lmax, ring r, l = m'..lmax:
+//     2 w_r P^{m'}_l(x_r) at  R * (m' (lmax+1) - m' (m'-1) / 2) + r (lmax - m' + 1) + (l - m')
 template <typename T>
 struct Tables {
     const T* pbar;      // [grid][ring][l (l+1)/2 + m]
-    const T* wt;        // [grid][ring]  2 * Gauss weight (north-south folding)
+    const T* wtab;      // see above
     const T* tw;        // complex pairs [Phi][2]: exp(-2 pi i k / Phi)
     const T* lcg;       // [j][q+1][m + j] = C^{j, m+q}_{j, m, 1, q}
     const T* rcg;       // [j3][q+1][m3 + j3] = C^{j3, m3}_{j3-1, m3-q, 1, q}
-    const T* ccg;       // [q1+1][q2+1] = C^{1, q1+q2}_{1 q1 1 q2}
     const T* kinv;      // per block, j3 = d..J: 1 / K
+    T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
     const BlockDesc* blocks;
 };
 
@@ -61,6 +81,35 @@ struct LaunchMap {
     int32_t list_off[kMaxClasses];
     int64_t ntiles[kMaxClasses];
     int64_t cum[kMaxClasses + 1];
+};
+
+// Longitude sizes the kernel supports and their two-pass factorisation.
+// Returns false when Phi is not supported.
+inline bool fft_factors(int phi, int* A, int* B) {
+    static const int tab[][3] = {{1, 1, 1},    {2, 2, 1},    {3, 3, 1},    {4, 2, 2},    {6, 3, 2},
+                                 {8, 4, 2},    {9, 3, 3},    {12, 4, 3},   {16, 4, 4},   {18, 6, 3},
+                                 {24, 6, 4},   {27, 9, 3},   {32, 8, 4},   {36, 6, 6},   {48, 8, 6},
+                                 {54, 9, 6},   {64, 8, 8},   {72, 9, 8},   {81, 9, 9},   {96, 12, 8},
+                                 {108, 12, 9}, {128, 16, 8}, {144, 12, 12}};
+    for (const auto& r : tab)
+        if (r[0] == phi) {
+            *A = r[1];
+            *B = r[2];
+            return true;
+        }
+    return false;
+}
+
+// Accumulator geometry shared by host and device.
+struct TileGeom {
+    int nrows;   // rows l3 = d, d+2, ..., J
+    int ncomp;   // projected components (1 scalar, 4 scalar + vector)
+    int pairs;
+    __host__ __device__ int tmin(int mp, int d) const { return mp > d ? (mp - d + 1) / 2 : 0; }
+    __host__ __device__ int rows(int mp, int d) const { return nrows - tmin(mp, d); }
+    __host__ __device__ int ncols(int mp) const { return (mp == 0 ? 1 : 2) * ncomp * pairs; }
+    __host__ __device__ int nrt(int mp, int d) const { return (rows(mp, d) + 15) / 16; }
+    __host__ __device__ int nct(int mp) const { return (ncols(mp) + 15) / 16; }
 };
 
 // Launches the block kernel over the whole map; returns a hipError_t value.

@@ -1,20 +1,24 @@
 // Device side of the CGTP: one work-group computes one (j1, j2) block for a
 // tile of pairs, i.e. one irrep-signal tensor product (Section 4.3) on the
-// block's own sphere grid, entirely in LDS and registers:
+// block's own sphere grid, in LDS and registers only.
 //
-//   per pass over a chunk of northern rings
-//     1. lift (Definition 4.1 with s = 0 and s = 1, l = j): latitude stage
-//        a_c[m] = coefficient * P^m_j(x_i), packed two real series per complex
-//        transform;
-//     2. longitude synthesis: inverse FFT in LDS (Stockham, radix 4/2/3);
-//     3. pointwise products (Section 4.3 / 5.1): scalar-scalar and the
-//        1 (x) 1 -> 1 Clebsch-Gordan coupling of the two toroidal fields, i.e.
-//        the cross product;
-//     4. longitude analysis: forward FFT in LDS, two real spectra per transform;
-//     5. Legendre projection onto the block's rows l3 = d, d+2, ..., J, folding
-//        the southern rings by parity, accumulated in LDS;
-//   then recombination of the vector components with C^{j3 m3}_{j3-1, m3-q, 1, q},
-//   scaling by 1/K (Theorem 4.2), and one contiguous store of the block.
+// For each group of four northern rings:
+//   1. lift (Definition 4.1, l = j, s = 0 and s = 1) fused into the first
+//      pass of the longitude synthesis: the coefficient a_c[m] =
+//      (coupling) * x_m * P^m_j(x_i) is formed as the pass loads it; two real
+//      series of one input share a complex transform;
+//   2. second synthesis pass (in place);
+//   3. pointwise products on half the circle (the other half is the complex
+//      conjugate): scalar-scalar, and the 1 (x) 1 -> 1 coupling of the two
+//      toroidal fields, i.e. the cross product (Section 5.1);
+//   4. longitude analysis in two passes; each complex transform carries two
+//      real spectra; the needed orders |m| <= J are staged, scaled, in LDS;
+//   5. Legendre projection on MFMA: per |m| a [rows l3] x [4 rings] x
+//      [sign, component, pair] product accumulated in registers, with the
+//      Gauss weights, the north-south folding and P^m_l in the A operand.
+// Then, per pair, the accumulators go through LDS once: the vector
+// components are recombined with C^{j3 m3}_{j3-1, m3-q, 1, q}, every path is
+// scaled by 1/K (Theorem 4.2), and the block is stored contiguously.
 //
 // All quantities use the complex spherical basis with Condon-Shortley phase.
 
@@ -27,305 +31,537 @@
 namespace cgtp {
 namespace {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
 template <typename T> struct Cplx;
-template <> struct Cplx<float> { using type = float2; };
-template <> struct Cplx<double> { using type = double2; };
+template <> struct Cplx<float> { using type = float2; using acc4 = f32x4; };
+template <> struct Cplx<double> { using type = double2; using acc4 = f64x4; };
 
+template <typename C> __device__ __forceinline__ C cmk(decltype(C::x) x, decltype(C::x) y) { C r; r.x = x; r.y = y; return r; }
 template <typename C> __device__ __forceinline__ C cmul(C a, C b) {
-    C r;
-    r.x = a.x * b.x - a.y * b.y;
-    r.y = a.x * b.y + a.y * b.x;
-    return r;
+    return cmk<C>(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
 }
-template <typename C> __device__ __forceinline__ C cadd(C a, C b) { C r; r.x = a.x + b.x; r.y = a.y + b.y; return r; }
-template <typename C> __device__ __forceinline__ C csub(C a, C b) { C r; r.x = a.x - b.x; r.y = a.y - b.y; return r; }
-template <typename C, typename T> __device__ __forceinline__ C cscale(C a, T s) { C r; r.x = a.x * s; r.y = a.y * s; return r; }
-template <typename C> __device__ __forceinline__ C mul_i(C a, bool inv) {
-    // multiply by -i (forward) or +i (inverse)
-    C r;
-    if (inv) { r.x = -a.y; r.y = a.x; } else { r.x = a.y; r.y = -a.x; }
-    return r;
+template <typename C> __device__ __forceinline__ C cmulc(C a, C b) {   // a * conj(b)
+    return cmk<C>(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
+}
+template <typename C> __device__ __forceinline__ C cadd(C a, C b) { return cmk<C>(a.x + b.x, a.y + b.y); }
+template <typename C> __device__ __forceinline__ C csub(C a, C b) { return cmk<C>(a.x - b.x, a.y - b.y); }
+template <typename C> __device__ __forceinline__ C cconj(C a) { return cmk<C>(a.x, -a.y); }
+// multiply by -i (forward) or +i (inverse)
+template <bool INV, typename C> __device__ __forceinline__ C mul_mi(C a) {
+    return INV ? cmk<C>(-a.y, a.x) : cmk<C>(a.y, -a.x);
 }
 
-// In-place-free radix-R DFT of v[0..R-1]; forward uses exp(-2 pi i / R).
-template <typename T, typename C>
-__device__ __forceinline__ void butterfly(C* v, int R, bool inv) {
-    if (R == 2) {
-        C a = v[0], b = v[1];
-        v[0] = cadd(a, b);
-        v[1] = csub(a, b);
-    } else if (R == 4) {
-        C a = v[0], b = v[1], c = v[2], d = v[3];
-        C s0 = cadd(a, c), s1 = csub(a, c), s2 = cadd(b, d), s3 = mul_i(csub(b, d), inv);
-        v[0] = cadd(s0, s2);
-        v[2] = csub(s0, s2);
-        v[1] = cadd(s1, s3);
-        v[3] = csub(s1, s3);
-    } else if (R == 3) {
-        const T h = (T)0.86602540378443864676;  // sqrt(3)/2
-        C a = v[0], b = v[1], c = v[2];
-        C t1 = cadd(b, c), t2 = csub(b, c);
-        C m = csub(a, cscale(t1, (T)0.5));
-        // forward: w = -1/2 - i h;  y1 = m - i h t2, y2 = m + i h t2
-        C r = mul_i(cscale(t2, h), inv);   // -i h t2 (forward) / +i h t2 (inverse)
-        v[0] = cadd(a, t1);
-        v[1] = cadd(m, r);
-        v[2] = csub(m, r);
-    }
-}
+// ---------------------------------------------------------------- twiddle constants
 
-// Batched Stockham FFT over nb transforms of length Phi stored back to back.
-// Reads src, ping-pongs with dst, returns the buffer holding the result.
-template <typename T, typename C>
-__device__ C* fft_batch(C* src, C* dst, int nb, int Phi, const int* rad, int nrad, const C* tw, bool inv) {
-    int Ns = 1;
-    for (int s = 0; s < nrad; ++s) {
-        const int R = rad[s];
-        const int nbf = Phi / R;
-        const int total = nb * nbf;
-        const int step = Phi / (Ns * R);
-        for (int w = threadIdx.x; w < total; w += blockDim.x) {
-            const int f = w / nbf, j = w - f * nbf;
-            const int k = j % Ns;
-            const C* in = src + f * Phi;
-            C* out = dst + f * Phi;
-            C v[4];
-            for (int t = 0; t < R; ++t) v[t] = in[j + t * nbf];
-            for (int t = 1; t < R; ++t) {
-                C wv = tw[t * k * step];
-                if (inv) wv.y = -wv.y;
-                v[t] = cmul(v[t], wv);
-            }
-            butterfly<T, C>(v, R, inv);
-            const int base = (j / Ns) * Ns * R + k;
-            for (int t = 0; t < R; ++t) out[base + t * Ns] = v[t];
+constexpr double kPiD = 3.14159265358979323846264338327950288;
+constexpr double csin_series(double x) {
+    double t = x, s = x;
+    for (int k = 1; k < 30; ++k) { t *= -x * x / ((2.0 * k) * (2.0 * k + 1)); s += t; }
+    return s;
+}
+constexpr double ccos_series(double x) {
+    double t = 1, s = 1;
+    for (int k = 1; k < 30; ++k) { t *= -x * x / ((2.0 * k - 1) * (2.0 * k)); s += t; }
+    return s;
+}
+// exp(-2 pi i e / N) for e < N, evaluated at compile time.
+template <int N> struct TwTab {
+    double re[N > 0 ? N : 1], im[N > 0 ? N : 1];
+    constexpr TwTab() : re(), im() {
+        for (int e = 0; e < N; ++e) {
+            double a = 2.0 * kPiD * e / N;
+            if (a > kPiD) a -= 2.0 * kPiD;
+            re[e] = ccos_series(a);
+            im[e] = -csin_series(a);
         }
-        __syncthreads();
-        C* tmp = src; src = dst; dst = tmp;
-        Ns *= R;
     }
-    return src;
+};
+template <int N> inline constexpr TwTab<N> kTw{};
+
+template <int N, bool INV, typename C> __device__ __forceinline__ C twiddle_c(C v, int e) {
+    using T = decltype(C::x);
+    const T wr = (T)kTw<N>.re[e];
+    const T wi = INV ? (T)-kTw<N>.im[e] : (T)kTw<N>.im[e];
+    if (e == 0) return v;
+    return cmk<C>(v.x * wr - v.y * wi, v.x * wi + v.y * wr);
 }
 
-// Row index n of a flat accumulator entry e, rows l3 = d + 2n of 2 l3 + 1 entries.
-__device__ __forceinline__ int acc_row(int e, int d) {
-    // rowoff(n) = 2 n^2 + (2d - 1) n ; largest n with rowoff(n) <= e
-    const float b = 2.0f * d - 1.0f;
-    int n = (int)((-b + sqrtf(b * b + 8.0f * (float)e)) * 0.25f);
-    if (n < 0) n = 0;
-    while (2 * n * n + (2 * d - 1) * n > e) --n;
-    while (2 * (n + 1) * (n + 1) + (2 * d - 1) * (n + 1) <= e) ++n;
-    return n;
+// ---------------------------------------------------------------- small DFTs in registers
+// Natural-order DFT of x[0..N-1]; forward uses exp(-2 pi i / N).
+
+template <int N, bool INV, typename C> struct Dft;
+
+template <bool INV, typename C> struct Dft<1, INV, C> { __device__ static void run(C*) {} };
+
+template <bool INV, typename C> struct Dft<2, INV, C> {
+    __device__ __forceinline__ static void run(C* x) {
+        const C a = x[0], b = x[1];
+        x[0] = cadd(a, b);
+        x[1] = csub(a, b);
+    }
+};
+
+template <bool INV, typename C> struct Dft<3, INV, C> {
+    __device__ __forceinline__ static void run(C* x) {
+        using T = decltype(C::x);
+        const T h = (T)0.86602540378443864676372317075294;   // sqrt(3)/2
+        const C a = x[0], t1 = cadd(x[1], x[2]), t2 = csub(x[1], x[2]);
+        const C m = cmk<C>(a.x - (T)0.5 * t1.x, a.y - (T)0.5 * t1.y);
+        const C r = mul_mi<INV>(cmk<C>(h * t2.x, h * t2.y));
+        x[0] = cadd(a, t1);
+        x[1] = cadd(m, r);
+        x[2] = csub(m, r);
+    }
+};
+
+template <bool INV, typename C> struct Dft<4, INV, C> {
+    __device__ __forceinline__ static void run(C* x) {
+        const C s0 = cadd(x[0], x[2]), s1 = csub(x[0], x[2]);
+        const C s2 = cadd(x[1], x[3]), s3 = mul_mi<INV>(csub(x[1], x[3]));
+        x[0] = cadd(s0, s2);
+        x[2] = csub(s0, s2);
+        x[1] = cadd(s1, s3);
+        x[3] = csub(s1, s3);
+    }
+};
+
+// Cooley-Tukey in registers: N1 inner transforms of length N2 over stride-N1
+// elements, twiddles exp(-+2 pi i n1 k2 / N), then N2 transforms of length N1.
+template <int N1, int N2, bool INV, typename C> __device__ __forceinline__ void dft_ct(C* x) {
+    constexpr int N = N1 * N2;
+    C y[N];
+#pragma unroll
+    for (int n1 = 0; n1 < N1; ++n1) {
+        C v[N2];
+#pragma unroll
+        for (int n2 = 0; n2 < N2; ++n2) v[n2] = x[n1 + N1 * n2];
+        Dft<N2, INV, C>::run(v);
+#pragma unroll
+        for (int k2 = 0; k2 < N2; ++k2) y[n1 * N2 + k2] = twiddle_c<N, INV>(v[k2], n1 * k2);
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < N2; ++k2) {
+        C v[N1];
+#pragma unroll
+        for (int n1 = 0; n1 < N1; ++n1) v[n1] = y[n1 * N2 + k2];
+        Dft<N1, INV, C>::run(v);
+#pragma unroll
+        for (int k1 = 0; k1 < N1; ++k1) x[k2 + N2 * k1] = v[k1];
+    }
 }
+
+template <bool INV, typename C> struct Dft<6, INV, C> { __device__ static void run(C* x) { dft_ct<2, 3, INV>(x); } };
+template <bool INV, typename C> struct Dft<8, INV, C> { __device__ static void run(C* x) { dft_ct<2, 4, INV>(x); } };
+template <bool INV, typename C> struct Dft<9, INV, C> { __device__ static void run(C* x) { dft_ct<3, 3, INV>(x); } };
+template <bool INV, typename C> struct Dft<12, INV, C> { __device__ static void run(C* x) { dft_ct<4, 3, INV>(x); } };
+template <bool INV, typename C> struct Dft<16, INV, C> { __device__ static void run(C* x) { dft_ct<4, 4, INV>(x); } };
+
+// ---------------------------------------------------------------- MFMA
+
+__device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f64x4 mfma16(double a, double b, f64x4 c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// Row of accumulator element q held by a lane in quarter rq = lane / 16 (the
+// column is lane % 16).  The two 16x16x4 instructions lay their results out
+// differently: f32 keeps four consecutive rows per lane, f64 strides by four.
+template <typename T> __device__ __forceinline__ int acc_row(int rq, int q);
+template <> __device__ __forceinline__ int acc_row<float>(int rq, int q) { return 4 * rq + q; }
+template <> __device__ __forceinline__ int acc_row<double>(int rq, int q) { return rq + 4 * q; }
+
 __device__ __forceinline__ int acc_rowoff(int n, int d) { return 2 * n * n + (2 * d - 1) * n; }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void block_kernel(Tables<T> tb, const int32_t* __restrict__ list,
-                                                         LaunchMap map, const T* __restrict__ x1,
-                                                         const T* __restrict__ x2, T* __restrict__ out, int64_t N,
-                                                         int L) {
-    using C = typename Cplx<T>::type;
-    extern __shared__ __align__(16) unsigned char smem[];
+// ---------------------------------------------------------------- LDS layout
 
-    const int64_t wg = blockIdx.x;
-    int cls = 0;
-    while (cls + 1 < map.ncls && wg >= map.cum[cls + 1]) ++cls;
-    const int pairs = map.pairs[cls];
-    const int64_t ntiles = map.ntiles[cls];
-    const int64_t local = wg - map.cum[cls];
-    const int bi = (int)(local / ntiles);
-    const int64_t tile = local - (int64_t)bi * ntiles;
-    const BlockDesc bd = tb.blocks[list[map.list_off[cls] + bi]];
-    const int j1 = bd.j1, j2 = bd.j2, J = bd.J, d = bd.d, R = bd.R, Phi = bd.Phi;
+struct Layout {
+    int xs, lc, pst, twl, tiles, stage, fbuf, bbuf;   // byte offsets
+    int stage_cols;                                    // padded columns of one staged |m|
+    int fper;                                          // transforms per (ring, pair): nslot + nz
+};
+
+__device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
+
+template <typename T>
+__device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, int nz, int ncomp) {
+    using C = typename Cplx<T>::type;
+    Layout l;
+    const int P = b.pairs, n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
+    int o = 0;
+    l.xs = o; o = align16(o + (int)sizeof(T) * P * (n1 + n2));
+    l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
+    l.pst = o; o = align16(o + (int)sizeof(T) * kRingGroup * (b.j1 + 1 + b.j2 + 1));
+    l.twl = o; o = align16(o + (int)sizeof(C) * b.Phi);
+    l.tiles = o; o = align16(o + 4 * b.ntiles);
+    l.stage_cols = ((2 * ncomp * P + 15) / 16) * 16;
+    l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * (b.J + 1) * l.stage_cols);
+    l.fper = nslot + nz;
+    l.fbuf = o;
+    l.bbuf = l.stage;
+    return l;
+}
+
+// ---------------------------------------------------------------- the block body
+
+template <typename T, int A, int B>
+__device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0, int np, const T* __restrict__ x1,
+                           const T* __restrict__ x2, T* __restrict__ out, int L, unsigned char* smem) {
+    using C = typename Cplx<T>::type;
+    using Acc = typename Cplx<T>::acc4;
+    constexpr int Phi = A * B;
+    constexpr int H = Phi / 2 + 1;
+    constexpr int MT = MaxTiles<T>::value;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j1 = bd.j1, j2 = bd.j2, J = bd.J, d = bd.d, R = bd.R, P = bd.pairs;
     const bool cross = bd.kind == kBlockCross;
-    // synthesis transforms per (ring, pair).  Two real series share a complex
-    // transform only when they come from the same input, so rounding crosstalk
-    // stays proportional to that input's norm (the product is bilinear).
-    const int nslot = cross ? 4 : 2;
+    const int nslot = cross ? 4 : 2;   // synthesis transforms per (ring, pair)
     const int nz = cross ? 2 : 1;      // analysis transforms per (ring, pair)
     const int ncomp = cross ? 4 : 1;   // projected components
     const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
     const int nrows = (J - d) / 2 + 1;
     const int nel = nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
-    const int64_t p0 = tile * pairs;
-    const int np = (int)((N - p0) < pairs ? (N - p0) : pairs);
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
+    const TileGeom geo{nrows, ncomp, P};
 
-    T* xs1 = reinterpret_cast<T*>(smem);
-    T* xs2 = xs1 + pairs * n1;
-    T* acc = xs2 + pairs * n2;
-    size_t head = sizeof(T) * ((size_t)pairs * (n1 + n2) + (size_t)pairs * ncomp * nel);
-    head = (head + 15) & ~(size_t)15;
-    C* bufA = reinterpret_cast<C*>(smem + head);
-    C* bufB = bufA + (size_t)bd.chunk * pairs * nslot * Phi;
+    const Layout ly = make_layout<T>(bd, nslot, nz, ncomp);
+    T* xs = reinterpret_cast<T*>(smem + ly.xs);          // [P][n1] then [P][n2]
+    T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
+    T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1]
+    C* twl = reinterpret_cast<C*>(smem + ly.twl);        // exp(-2 pi i k / Phi)
+    int* tiles = reinterpret_cast<int*>(smem + ly.tiles);
+    T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][|m|][stage_cols]
+    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [ring][pair][fper][Phi]
+    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [comp][nel], end phase only
 
-    int rad[kMaxRadix];
-    for (int s = 0; s < kMaxRadix; ++s) rad[s] = bd.rad[s];
-    const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
-    const T* pbar = tb.pbar + bd.pbar_off;
-    const T* wt = tb.wt + bd.wt_off;
-    const T* lcg1 = tb.lcg + 3 * j1 * j1;
-    const T* lcg2 = tb.lcg + 3 * j2 * j2;
-
-    // ---- inputs of the tile (rows past N read as zero)
-    for (int e = threadIdx.x; e < pairs * n1; e += blockDim.x) {
+    // ---- set-up: inputs of the tile, coupling rows, twiddles, tile table, zeroed staging
+    for (int e = tid; e < P * n1; e += kThreads) {
         const int p = e / n1, m = e - p * n1;
-        xs1[e] = p < np ? x1[(p0 + p) * nin + j1 * j1 + m] : (T)0;
+        xs[e] = p < np ? x1[(p0 + p) * nin + j1 * j1 + m] : (T)0;
     }
-    for (int e = threadIdx.x; e < pairs * n2; e += blockDim.x) {
+    for (int e = tid; e < P * n2; e += kThreads) {
         const int p = e / n2, m = e - p * n2;
-        xs2[e] = p < np ? x2[(p0 + p) * nin + j2 * j2 + m] : (T)0;
+        xs[P * n1 + e] = p < np ? x2[(p0 + p) * nin + j2 * j2 + m] : (T)0;
     }
-    for (int e = threadIdx.x; e < pairs * ncomp * nel; e += blockDim.x) acc[e] = (T)0;
+    for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
+    for (int e = tid; e < 3 * n2; e += kThreads) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
+    {
+        const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
+        for (int e = tid; e < Phi; e += kThreads) twl[e] = tw[e];
+    }
+    for (int e = tid; e < kRingGroup * (J + 1) * ly.stage_cols; e += kThreads) stage[e] = (T)0;
+    if (tid == 0) {
+        int u = 0;
+        for (int mp = 0; mp <= J; ++mp)
+            for (int rt = 0; rt < geo.nrt(mp, d); ++rt)
+                for (int ct = 0; ct < geo.nct(mp); ++ct) tiles[u++] = (mp << 16) | (rt << 8) | ct;
+    }
+
+    Acc acc[MT];
+#pragma unroll
+    for (int s = 0; s < MT; ++s) acc[s] = Acc(0);
+
+    const T* wtab = tb.wtab + bd.wtab_off;
+    const int lmax = bd.lmax;
+    const T cc = tb.cross_cg;
+    // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
+    // unpacking two packed signals, and the cross product's coupling constant
+    const T sc_s = (T)(6.283185307179586476925286766559 / Phi) * (cross ? (T)0.25 : (T)1);
+    const T sc_v = sc_s * cc;
+
+    for (int rg0 = 0; rg0 < R; rg0 += kRingGroup) {
+        const int nrg = (R - rg0) < kRingGroup ? (R - rg0) : kRingGroup;
+        // P^m_j rows of both degrees for the group's rings
+        for (int e = tid; e < nrg * (j1 + 1 + j2 + 1); e += kThreads) {
+            const int r = e / (j1 + 1 + j2 + 1), q = e - r * (j1 + 1 + j2 + 1);
+            const T* prow = tb.pbar + bd.pbar_off + (size_t)(rg0 + r) * bd.pbar_stride;
+            pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
+        }
+        __syncthreads();
+
+        // ---- 1. lift + synthesis pass 1: task (ring, pair, slot, t)
+        {
+            const int ntask = nrg * P * nslot * A;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int t = task % A;
+                int rest = task / A;
+                const int s = rest % nslot;
+                rest /= nslot;
+                const int p = rest % P, r = rest / P;
+                const bool first = cross ? (s < 2) : (s == 0);
+                const int j = first ? j1 : j2;
+                const int nj = 2 * j + 1;
+                const T* xv = first ? xs + p * n1 : xs + P * n1 + p * n2;
+                const T* lcj = first ? lc : lc + 3 * n1;
+                const T* pr = pst + r * (j1 + 1 + j2 + 1) + (first ? 0 : j1 + 1);
+                C v[B];
+#pragma unroll
+                for (int n2i = 0; n2i < B; ++n2i) {
+                    const int n = t + A * n2i;
+                    const int m = n <= j ? n : (n >= Phi - j ? n - Phi : 1 << 20);
+                    T re = 0, im = 0;
+                    if (m != (1 << 20)) {
+                        const int am = m < 0 ? -m : m;
+                        T pv = pr[am];
+                        if (m < 0 && (am & 1)) pv = -pv;
+                        if (!cross) {
+                            re = xv[m + j] * pv;
+                        } else if ((s & 1) == 0) {
+                            // scalar lift (real part) and the q = 0 vector lift (imaginary part)
+                            re = xv[m + j] * pv;
+                            im = lcj[nj + m + j] * xv[m + j] * pv;
+                        } else {
+                            // q = -1 (real part) and q = +1 (imaginary part) vector lifts
+                            if (m - 1 >= -j) re = lcj[m + j] * xv[m - 1 + j] * pv;
+                            if (m + 1 <= j) im = lcj[2 * nj + m + j] * xv[m + 1 + j] * pv;
+                        }
+                    }
+                    v[n2i] = cmk<C>(re, im);
+                }
+                Dft<B, true, C>::run(v);
+                C* f = fbuf + ((size_t)(r * P + p) * ly.fper + s) * Phi;
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) f[k2 + B * t] = k2 == 0 ? v[k2] : cmulc(v[k2], twl[t * k2]);
+            }
+        }
+        __syncthreads();
+        // ---- 2. synthesis pass 2 (in place): task (ring, pair, slot, k2)
+        {
+            const int ntask = nrg * P * nslot * B;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int k2 = task % B;
+                const int f = task / B;
+                const int s = f % nslot, rp = f / nslot;
+                C* fb = fbuf + ((size_t)rp * ly.fper + s) * Phi;
+                C u[A];
+#pragma unroll
+                for (int t = 0; t < A; ++t) u[t] = fb[k2 + B * t];
+                Dft<A, true, C>::run(u);
+#pragma unroll
+                for (int k1 = 0; k1 < A; ++k1) fb[k2 + B * k1] = u[k1];
+            }
+        }
+        __syncthreads();
+        // ---- 3. pointwise products on half the circle, mirrored
+        {
+            const int ntask = nrg * P * H;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int n = task % H, rp = task / H;
+                const int kk = n == 0 ? 0 : Phi - n;
+                C* fb = fbuf + (size_t)rp * ly.fper * Phi;
+                C* zb = fb + (size_t)nslot * Phi;
+                if (!cross) {
+                    const C g = cmul(fb[n], fb[Phi + n]);
+                    zb[n] = g;
+                    zb[kk] = cconj(g);
+                } else {
+                    // unpacked (times 2): fA = F(n) + conj F(-n), fB = -i (F(n) - conj F(-n))
+                    C f[8];
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) {
+                        const C Fn = fb[s * Phi + n], Fk = fb[s * Phi + kk];
+                        f[2 * s] = cmk<C>(Fn.x + Fk.x, Fn.y - Fk.y);
+                        f[2 * s + 1] = cmk<C>(Fn.y + Fk.y, Fk.x - Fn.x);
+                    }
+                    const C as = f[0], a0 = f[1], am = f[2], ap = f[3];
+                    const C bs = f[4], b0 = f[5], bm = f[6], bp = f[7];
+                    const C gs = cmul(as, bs);
+                    // antisymmetric 1 (x) 1 -> 1 coupling, constant applied at staging
+                    const C gp = csub(cmul(ap, b0), cmul(a0, bp));
+                    const C g0 = csub(cmul(ap, bm), cmul(am, bp));
+                    const C gm = csub(cmul(a0, bm), cmul(am, b0));
+                    // z1 = gs + i g0, z2 = g-1 + i g+1; at -n the conjugated signals
+                    zb[n] = cmk<C>(gs.x - g0.y, gs.y + g0.x);
+                    zb[Phi + n] = cmk<C>(gm.x - gp.y, gm.y + gp.x);
+                    if (kk != n) {
+                        zb[kk] = cmk<C>(gs.x + g0.y, g0.x - gs.y);
+                        zb[Phi + kk] = cmk<C>(gm.x + gp.y, gp.x - gm.y);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        // ---- 4a. analysis pass 1: task (ring, pair, z, t); result into slot z
+        {
+            const int ntask = nrg * P * nz * A;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int t = task % A;
+                const int f = task / A;
+                const int z = f % nz, rp = f / nz;
+                const C* zb = fbuf + ((size_t)rp * ly.fper + nslot + z) * Phi;
+                C v[B];
+#pragma unroll
+                for (int n2i = 0; n2i < B; ++n2i) v[n2i] = zb[t + A * n2i];
+                Dft<B, false, C>::run(v);
+                C* yb = fbuf + ((size_t)rp * ly.fper + z) * Phi;
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) yb[k2 + B * t] = k2 == 0 ? v[k2] : cmul(v[k2], twl[t * k2]);
+            }
+        }
+        __syncthreads();
+        // ---- 4b. analysis pass 2 and staging of |m| <= J, scaled
+        {
+            const int ntask = nrg * P * nz * B;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int k2 = task % B;
+                const int f = task / B;
+                const int z = f % nz, rp = f / nz;
+                const int p = rp % P, r = rp / P;
+                const C* yb = fbuf + ((size_t)rp * ly.fper + z) * Phi;
+                C u[A];
+#pragma unroll
+                for (int t = 0; t < A; ++t) u[t] = yb[k2 + B * t];
+                Dft<A, false, C>::run(u);
+                T* st = stage + (size_t)r * (J + 1) * ly.stage_cols;
+#pragma unroll
+                for (int k1 = 0; k1 < A; ++k1) {
+                    const int k = k2 + B * k1;
+                    int mp, sg;
+                    if (k <= J) { mp = k; sg = 0; }
+                    else if (k >= Phi - J) { mp = Phi - k; sg = 1; }
+                    else continue;
+                    const T flip = (sg && (mp & 1)) ? (T)-1 : (T)1;   // P^{-m} = (-1)^m P^m
+                    const int cbase = sg * ncomp * P;
+                    if (!cross) {
+                        st[mp * ly.stage_cols + cbase + p] = u[k1].x * sc_s * flip;
+                    } else {
+                        const int c0 = 2 * z, c1 = 2 * z + 1;
+                        st[mp * ly.stage_cols + cbase + c0 * P + p] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
+                        st[mp * ly.stage_cols + cbase + c1 * P + p] = u[k1].y * sc_v * flip;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        // ---- 5. Legendre projection on MFMA, accumulated over ring groups
+        {
+            const int i = lane & 15, kq = lane >> 4;
+            const int ring = rg0 + kq;
+#pragma unroll
+            for (int s = 0; s < MT; ++s) {
+                const int u = wave + kWaves * s;
+                if (u < bd.ntiles) {
+                    const int code = __builtin_amdgcn_readfirstlane(tiles[u]);   // wave-uniform
+                    const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
+                    const int l3 = d + 2 * (geo.tmin(mp, d) + 16 * rt + i);
+                    T a = 0;
+                    if (ring < R && l3 <= J) {
+                        const int moff = R * (mp * (lmax + 1) - mp * (mp - 1) / 2);
+                        a = wtab[moff + ring * (lmax - mp + 1) + (l3 - mp)];
+                    }
+                    const T bv = stage[((size_t)kq * (J + 1) + mp) * ly.stage_cols + 16 * ct + i];
+                    acc[s] = mfma16(a, bv, acc[s]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- accumulators of every pair -> LDS once, then recombination, 1/K, contiguous store
+    {
+        const int col_in = lane & 15, rq = lane >> 4;
+#pragma unroll
+        for (int s = 0; s < MT; ++s) {
+            const int u = wave + kWaves * s;
+            if (u < bd.ntiles) {
+                const int code = __builtin_amdgcn_readfirstlane(tiles[u]);   // wave-uniform
+                const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
+                const int col = 16 * ct + col_in;
+                const int p = col % P;
+                if (col < geo.ncols(mp) && p < np) {
+                    const int sg = col / (ncomp * P);
+                    const int comp = (col / P) % ncomp;
+                    const int m = sg ? -mp : mp;
+                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nel;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int tr = geo.tmin(mp, d) + 16 * rt + acc_row<T>(rq, q);
+                        const int l3 = d + 2 * tr;
+                        if (l3 <= J) dst[acc_rowoff(tr, d) + l3 + m] = acc[s][q];
+                    }
+                }
+            }
+        }
+    }
     __syncthreads();
-
-    const T twopi_over_phi = (T)(6.283185307179586476925286766559 / (double)Phi);
-    T ccg[9];
-    for (int i = 0; i < 9; ++i) ccg[i] = tb.ccg[i];
-
-    for (int r0 = 0; r0 < R; r0 += bd.chunk) {
-        const int nr = (R - r0) < bd.chunk ? (R - r0) : bd.chunk;
-        // ---- 1. lift, latitude stage: fill the packed synthesis inputs
-        const int nsyn = nr * pairs * nslot;
-        for (int e = threadIdx.x; e < nsyn * Phi; e += blockDim.x) {
-            const int k = e % Phi;
-            const int f = e / Phi;
-            const int slot = f % nslot;
-            const int rp = f / nslot;
-            const int p = rp % pairs;
-            const int ring = r0 + rp / pairs;
-            const T* prow = pbar + (size_t)ring * bd.pbar_stride;
-            T re = 0, im = 0;
-            if (!cross) {
-                // slot 0: scalar lift of x1, slot 1: scalar lift of x2 (real coefficients)
-                const int j = slot == 0 ? j1 : j2;
-                const T* xs = slot == 0 ? xs1 + p * n1 : xs2 + p * n2;
-                const int m = k <= j ? k : (k >= Phi - j ? k - Phi : 1 << 20);
-                if (m != (1 << 20)) {
-                    const int am = m < 0 ? -m : m;
-                    T pv = prow[j * (j + 1) / 2 + am];
-                    if (m < 0 && (am & 1)) pv = -pv;
-                    re = xs[m + j] * pv;
-                }
-            } else {
-                const int j = slot < 2 ? j1 : j2;
-                const T* xs = slot < 2 ? xs1 + p * n1 : xs2 + p * n2;
-                const T* lc = slot < 2 ? lcg1 : lcg2;
-                const int m = k <= j ? k : (k >= Phi - j ? k - Phi : 1 << 20);
-                if (m != (1 << 20)) {
-                    const int am = m < 0 ? -m : m;
-                    T pv = prow[j * (j + 1) / 2 + am];
-                    if (m < 0 && (am & 1)) pv = -pv;
-                    const int nj = 2 * j + 1;
-                    // component c of the lift at order m (orbital order m for vectors)
-                    auto comp = [&](int q) -> T {   // q = 2: scalar
-                        if (q == 2) return xs[m + j] * pv;
-                        const int mj = m + q;
-                        if (mj < -j || mj > j) return (T)0;
-                        return lc[(q + 1) * nj + m + j] * xs[mj + j] * pv;
-                    };
-                    if ((slot & 1) == 0) { re = comp(2); im = comp(0); }
-                    else { re = comp(-1); im = comp(1); }
-                }
-            }
-            C v;
-            v.x = re;
-            v.y = im;
-            bufA[(size_t)f * Phi + k] = v;
-        }
-        __syncthreads();
-        // ---- 2. longitude synthesis (exp(+i m phi))
-        C* syn = fft_batch<T, C>(bufA, bufB, nsyn, Phi, rad, bd.nrad, tw, true);
-        C* zb = syn == bufA ? bufB : bufA;
-        // ---- 3. pointwise products on the full circle
-        const int nrp = nr * pairs;
-        for (int e = threadIdx.x; e < nrp * Phi; e += blockDim.x) {
-            const int k = e % Phi;
-            const int rp = e / Phi;
-            const int kk = k == 0 ? 0 : Phi - k;
-            if (!cross) {
-                // each slot already holds one Hermitian signal
-                zb[(size_t)rp * Phi + k] = cmul(syn[((size_t)rp * 2) * Phi + k], syn[((size_t)rp * 2 + 1) * Phi + k]);
-            } else {
-                C f[8];   // f1 s, f1 q0, f1 q-1, f1 q+1, f2 s, f2 q0, f2 q-1, f2 q+1
-                for (int s = 0; s < 4; ++s) {
-                    const C F = syn[((size_t)rp * 4 + s) * Phi + k], Fr = syn[((size_t)rp * 4 + s) * Phi + kk];
-                    f[2 * s].x = (F.x + Fr.x) * (T)0.5; f[2 * s].y = (F.y - Fr.y) * (T)0.5;
-                    f[2 * s + 1].x = (F.y + Fr.y) * (T)0.5; f[2 * s + 1].y = (Fr.x - F.x) * (T)0.5;
-                }
-                const C a_s = f[0], a0 = f[1], am = f[2], ap = f[3];
-                const C b_s = f[4], b0 = f[5], bm = f[6], bp = f[7];
-                // ccg[(q1+1)*3 + q2+1] = C^{1, q1+q2}_{1 q1 1 q2}
-                const C gs = cmul(a_s, b_s);
-                const C gp = cadd(cscale(cmul(ap, b0), ccg[2 * 3 + 1]), cscale(cmul(a0, bp), ccg[1 * 3 + 2]));
-                const C g0 = cadd(cadd(cscale(cmul(ap, bm), ccg[2 * 3 + 0]), cscale(cmul(a0, b0), ccg[1 * 3 + 1])),
-                                  cscale(cmul(am, bp), ccg[0 * 3 + 2]));
-                const C gm = cadd(cscale(cmul(a0, bm), ccg[1 * 3 + 0]), cscale(cmul(am, b0), ccg[0 * 3 + 1]));
-                C z1, z2;   // z1 = gs + i g0, z2 = g-1 + i g+1
-                z1.x = gs.x - g0.y; z1.y = gs.y + g0.x;
-                z2.x = gm.x - gp.y; z2.y = gm.y + gp.x;
-                zb[((size_t)rp * 2 + 0) * Phi + k] = z1;
-                zb[((size_t)rp * 2 + 1) * Phi + k] = z2;
-            }
-        }
-        __syncthreads();
-        // ---- 4. longitude analysis (exp(-i m phi)); real spectra in re / im
-        C* spec = fft_batch<T, C>(zb, syn, nrp * nz, Phi, rad, bd.nrad, tw, false);
-        // ---- 5. Legendre projection of the chunk's rings, accumulated
-        for (int e = threadIdx.x; e < pairs * ncomp * nel; e += blockDim.x) {
-            const int el = e % nel;
-            const int pc = e / nel;
-            const int c = pc % ncomp;
-            const int p = pc / ncomp;
-            const int n = acc_row(el, d);
-            const int l3 = d + 2 * n;
-            const int m = el - acc_rowoff(n, d) - l3;
-            const int am = m < 0 ? -m : m;
-            const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
-            const int km = m < 0 ? m + Phi : m;
-            const int lidx = l3 * (l3 + 1) / 2 + am;
-            T s = 0;
-            for (int r = 0; r < nr; ++r) {
-                const int ring = r0 + r;
-                const C G = spec[((size_t)(r * pairs + p) * nz + (c >> 1)) * Phi + km];
-                const T g = (c & 1) ? G.y : G.x;
-                s += wt[ring] * pbar[(size_t)ring * bd.pbar_stride + lidx] * g;
-            }
-            acc[e] += s * sg * twopi_over_phi;
-        }
-        __syncthreads();
-    }
-
-    // ---- recombination, 1/K, contiguous store of the block
     const int nblk = n1 * n2;
     const T* kinv = tb.kinv + bd.kinv_off;
-    for (int e = threadIdx.x; e < np * nblk; e += blockDim.x) {
-        const int p = e / nblk;
-        const int o = e - p * nblk;
+    for (int e = tid; e < np * nblk; e += kThreads) {
+        const int p = e / nblk, o = e - p * nblk;
         int j3 = (int)sqrtf((float)(o + d * d));
         while (j3 * j3 - d * d > o) --j3;
         while ((j3 + 1) * (j3 + 1) - d * d <= o) ++j3;
         const int m3 = o - (j3 * j3 - d * d) - j3;
+        const T* bp = bbuf + (size_t)p * ncomp * nel;
         T z;
         if (((J + j3) & 1) == 0) {
-            z = acc[(p * ncomp + 0) * nel + acc_rowoff((j3 - d) / 2, d) + j3 + m3];
+            z = bp[acc_rowoff((j3 - d) / 2, d) + j3 + m3];
         } else {
             const int l3 = j3 - 1;
-            const int rowoff = acc_rowoff((l3 - d) / 2, d);
-            const T* rc = tb.rcg + 3 * j3 * j3;
+            const int roff = acc_rowoff((l3 - d) / 2, d) + l3;
+            const T* rc = tb.rcg + 3 * j3 * j3 + m3 + j3;
+            const int nj3 = 2 * j3 + 1;
             z = 0;
-            // component slots: 1 -> q = 0, 2 -> q = -1, 3 -> q = +1
-            const int slot_of_q[3] = {2, 1, 3};
-            for (int q = -1; q <= 1; ++q) {
-                const int m = m3 - q;
-                if (m < -l3 || m > l3) continue;
-                z += rc[(q + 1) * (2 * j3 + 1) + m3 + j3] *
-                     acc[(p * ncomp + slot_of_q[q + 1]) * nel + rowoff + l3 + m];
-            }
+            // components: 1 -> q = 0, 2 -> q = -1, 3 -> q = +1
+            if (m3 + 1 <= l3) z += rc[0] * bp[2 * nel + roff + m3 + 1];
+            if (m3 >= -l3 && m3 <= l3) z += rc[nj3] * bp[1 * nel + roff + m3];
+            if (m3 - 1 >= -l3) z += rc[2 * nj3] * bp[3 * nel + roff + m3 - 1];
         }
         out[(p0 + p) * nout + bd.out_off + o] = z * kinv[j3 - d];
     }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads, 2) void block_kernel(Tables<T> tb, const int32_t* __restrict__ list,
+                                                         LaunchMap map, const T* __restrict__ x1,
+                                                         const T* __restrict__ x2, T* __restrict__ out, int64_t N,
+                                                         int L) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int64_t wg = blockIdx.x;
+    int cls = 0;
+    while (cls + 1 < map.ncls && wg >= map.cum[cls + 1]) ++cls;
+    const int64_t ntiles = map.ntiles[cls];
+    const int64_t local = wg - map.cum[cls];
+    const int bi = (int)(local / ntiles);
+    const int64_t tile = local - (int64_t)bi * ntiles;
+    const BlockDesc bd = tb.blocks[list[map.list_off[cls] + bi]];
+    const int64_t p0 = tile * bd.pairs;
+    const int np = (int)((N - p0) < bd.pairs ? (N - p0) : bd.pairs);
+
+#define CGTP_CASE(PHI, A_, B_) \
+    case PHI: block_body<T, A_, B_>(tb, bd, p0, np, x1, x2, out, L, smem); break;
+    switch (bd.Phi) {
+        CGTP_CASE(1, 1, 1)
+        CGTP_CASE(2, 2, 1)
+        CGTP_CASE(3, 3, 1)
+        CGTP_CASE(4, 2, 2)
+        CGTP_CASE(6, 3, 2)
+        CGTP_CASE(8, 4, 2)
+        CGTP_CASE(9, 3, 3)
+        CGTP_CASE(12, 4, 3)
+        CGTP_CASE(16, 4, 4)
+        CGTP_CASE(18, 6, 3)
+        CGTP_CASE(24, 6, 4)
+        CGTP_CASE(27, 9, 3)
+        CGTP_CASE(32, 8, 4)
+        CGTP_CASE(36, 6, 6)
+        CGTP_CASE(48, 8, 6)
+        CGTP_CASE(54, 9, 6)
+        CGTP_CASE(64, 8, 8)
+        CGTP_CASE(72, 9, 8)
+        CGTP_CASE(81, 9, 9)
+        CGTP_CASE(96, 12, 8)
+        CGTP_CASE(108, 12, 9)
+        CGTP_CASE(128, 16, 8)
+        CGTP_CASE(144, 12, 12)
+        default: break;
+    }
+#undef CGTP_CASE
 }
 
 template <typename T>
@@ -334,6 +570,11 @@ int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int l
     const int64_t grid = map.cum[map.ncls];
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)block_kernel<T>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        if (e != hipSuccess) return (int)e;
+    }
     hipLaunchKernelGGL(block_kernel<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb, list,
                        map, x1, x2, out, N, L);
     return (int)hipGetLastError();

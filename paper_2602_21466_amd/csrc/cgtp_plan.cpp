@@ -223,16 +223,7 @@ int smallest_2a3b(int n) {
     return m;
 }
 
-// Radix-4 stages first, then radix 2, then radix 3.
-int radices(int n, int* rad) {
-    int k = 0;
-    while (n % 4 == 0) { rad[k++] = 4; n /= 4; }
-    while (n % 2 == 0) { rad[k++] = 2; n /= 2; }
-    while (n % 3 == 0) { rad[k++] = 3; n /= 3; }
-    return k;
-}
-
-constexpr int kMaxPhi = 512;
+constexpr int kMaxPhi = 144;
 
 int check_grid(int L, const cgtp_grid* g) {
     if (g->dtype != CGTP_FP32 && g->dtype != CGTP_FP64) return CGTP_EDTYPE;
@@ -245,7 +236,8 @@ int check_grid(int L, const cgtp_grid* g) {
     }
     if (g->n_phi > 0) {
         if (g->n_phi < 4 * L + 1) return CGTP_EGRID;
-        if (!is_2a3b(g->n_phi) || g->n_phi > kMaxPhi) return CGTP_EUNSUP;
+        int a, b;
+        if (!cgtp::fft_factors(g->n_phi, &a, &b) || g->n_phi > kMaxPhi) return CGTP_EUNSUP;
     }
     return CGTP_OK;
 }
@@ -307,26 +299,48 @@ struct cgtp_plan_s {
     int lds_bytes = 0;
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
+    double cross_cg = 0;
 };
 
 namespace {
 
 template <typename T>
 struct HostTables {
-    std::vector<T> pbar, wt, tw, lcg, rcg, ccg, kinv;
+    std::vector<T> pbar, wtab, tw, lcg, rcg, kinv;
 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-template <typename T>
-int lds_for(const BlockDesc& b, int pairs, int chunk) {
+int align16h(int v) { return (v + 15) & ~15; }
+
+// Accumulator tiles of a block with the given pairs per work-group.
+int block_tiles(const BlockDesc& b, int pairs) {
     const bool cross = b.kind == cgtp::kBlockCross;
-    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
-    size_t bytes = sizeof(T) * (size_t)pairs * (2 * b.j1 + 1 + 2 * b.j2 + 1);
-    bytes += sizeof(T) * (size_t)pairs * ncomp * acc_entries(b.d, b.J);
-    bytes = align_up(bytes, 16);
-    bytes += 2 * sizeof(T) * 2 * (size_t)chunk * pairs * nslot * b.Phi;
-    return (int)bytes;
+    cgtp::TileGeom g{(b.J - b.d) / 2 + 1, cross ? 4 : 1, pairs};
+    int n = 0;
+    for (int mp = 0; mp <= b.J; ++mp) n += g.nrt(mp, b.d) * g.nct(mp);
+    return n;
+}
+
+// Dynamic LDS of one work-group; mirrors the kernel's make_layout.
+template <typename T>
+int lds_for(const BlockDesc& b, int pairs, int ntiles) {
+    const int sz = (int)sizeof(T), csz = 2 * sz;
+    const bool cross = b.kind == cgtp::kBlockCross;
+    const int nslot = cross ? 4 : 2, nz = cross ? 2 : 1, ncomp = cross ? 4 : 1;
+    const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
+    int o = 0;
+    o = align16h(o + sz * pairs * (n1 + n2));
+    o = align16h(o + sz * 3 * (n1 + n2));
+    o = align16h(o + sz * cgtp::kRingGroup * (b.j1 + 1 + b.j2 + 1));
+    o = align16h(o + csz * b.Phi);
+    o = align16h(o + 4 * ntiles);
+    const int stage_cols = ((2 * ncomp * pairs + 15) / 16) * 16;
+    const int stage = o;
+    o = align16h(o + sz * cgtp::kRingGroup * (b.J + 1) * stage_cols);
+    o += csz * cgtp::kRingGroup * pairs * (nslot + nz) * b.Phi;
+    const int end_phase = stage + sz * pairs * ncomp * acc_entries(b.d, b.J);
+    return std::max(o, end_phase);
 }
 
 template <typename T>
@@ -335,6 +349,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
     const cgtp_grid& g = p->grid;
     // ---- grids: one Legendre table per distinct node count
     std::map<int, int> grid_lmax;          // n_theta -> largest degree needed
+    std::map<int, int> grid_lmax_out;
     std::map<int, int> phi_set;            // Phi -> twiddle offset
     for (int j1 = 0; j1 <= L; ++j1)
         for (int j2 = 0; j2 <= L; ++j2) {
@@ -343,21 +358,25 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             grid_lmax[nt] = std::max(grid_lmax[nt], j1 + j2);
             phi_set[np] = 0;
         }
-    std::map<int, int> grid_pbar_off, grid_wt_off, grid_stride;
+    std::map<int, int> grid_pbar_off, grid_wtab_off, grid_stride;
     for (auto& kv : grid_lmax) {
         const int nt = kv.first, lmax = kv.second, R = nt / 2;
         std::vector<long double> x, w;
         gauss_legendre(nt, x, w);
         const int stride = (lmax + 1) * (lmax + 2) / 2;
         grid_pbar_off[nt] = (int)h.pbar.size();
-        grid_wt_off[nt] = (int)h.wt.size();
+        grid_wtab_off[nt] = (int)h.wtab.size();
         grid_stride[nt] = stride;
-        std::vector<long double> row(stride);
+        std::vector<long double> rows((size_t)R * stride);
         for (int i = 0; i < R; ++i) {
-            legendre(lmax, x[i], row.data());
-            for (int e = 0; e < stride; ++e) h.pbar.push_back((T)row[e]);
-            h.wt.push_back((T)(2.0L * w[i]));   // north and south rings folded
+            legendre(lmax, x[i], rows.data() + (size_t)i * stride);
+            for (int e = 0; e < stride; ++e) h.pbar.push_back((T)rows[(size_t)i * stride + e]);
         }
+        // MFMA weights: [m'][ring][l - m'] = 2 w_r P^{m'}_l(x_r) (north and south folded)
+        for (int mp = 0; mp <= lmax; ++mp)
+            for (int i = 0; i < R; ++i)
+                for (int l = mp; l <= lmax; ++l)
+                    h.wtab.push_back((T)(2.0L * w[i] * rows[(size_t)i * stride + l * (l + 1) / 2 + mp]));
         p->max_theta = std::max(p->max_theta, nt);
     }
     for (auto& kv : phi_set) {
@@ -381,9 +400,16 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
         for (int q = -1; q <= 1; ++q)
             for (int m3 = -j3; m3 <= j3; ++m3)
                 h.rcg[3 * j3 * j3 + (q + 1) * (2 * j3 + 1) + m3 + j3] = (T)cg_vec(j3 - 1, m3 - q, q, j3, m3);
-    h.ccg.assign(9, (T)0);
+    // The kernel forms the cross product as c * (antisymmetric combination) with
+    // c = C^{1,1}_{1,1,1,0}; check the coupling table has that structure.
+    const long double c = cg_vec(1, 1, 0, 1, 1);
     for (int q1 = -1; q1 <= 1; ++q1)
-        for (int q2 = -1; q2 <= 1; ++q2) h.ccg[(q1 + 1) * 3 + q2 + 1] = (T)cg_vec(1, q1, q2, 1, q1 + q2);
+        for (int q2 = -1; q2 <= 1; ++q2) {
+            if (std::abs(q1 + q2) > 1) continue;
+            const long double want = q1 == q2 ? 0.0L : (q1 > q2 ? c : -c);
+            if (fabsl(cg_vec(1, q1, q2, 1, q1 + q2) - want) > 1e-15L) return CGTP_EINVAL;
+        }
+    p->cross_cg = (double)c;
     // ---- blocks
     double min_abs_K = 1e300, flops = 0;
     blocks.clear();
@@ -396,11 +422,12 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.R = nt / 2;
             b.Phi = np;
             b.kind = (j1 > 0 && j2 > 0) ? cgtp::kBlockCross : cgtp::kBlockScalar;
-            b.nrad = radices(np, b.rad);
+            if (!cgtp::fft_factors(np, &b.A, &b.B)) return CGTP_EUNSUP;
             b.tw_off = phi_set[np];
             b.pbar_off = grid_pbar_off[nt];
             b.pbar_stride = grid_stride[nt];
-            b.wt_off = grid_wt_off[nt];
+            b.wtab_off = grid_wtab_off[nt];
+            b.lmax = grid_lmax[nt];
             b.kinv_off = (int)h.kinv.size();
             for (int j3 = b.d; j3 <= b.J; ++j3) {
                 long double K;
@@ -413,18 +440,17 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             }
             b.out_off = path_offset(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
-            // LDS: all rings in one pass if possible, then as many pairs as fit
-            int chunk = b.R;
-            while (chunk > 1 && lds_for<T>(b, 1, chunk) > cgtp::kLdsBudget) --chunk;
-            if (lds_for<T>(b, 1, chunk) > cgtp::kLdsBudget) return CGTP_EUNSUP;
-            int pairs = 1;
-            const int nslot = b.kind == cgtp::kBlockCross ? 4 : 2;
-            while (pairs < 32 && lds_for<T>(b, 2 * pairs, chunk) <= cgtp::kLdsBudget &&
-                   chunk * pairs * nslot * b.Phi < 4096)
-                pairs *= 2;
-            b.chunk = chunk;
+            // pairs per work-group: as many as the accumulator registers and LDS allow
+            const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
+            int pairs = 0;
+            for (int P = cgtp::kMaxPairs; P >= 1; P /= 2) {
+                const int nt_ = block_tiles(b, P);
+                if (nt_ <= max_tiles && lds_for<T>(b, P, nt_) <= cgtp::kLdsBudget) { pairs = P; break; }
+            }
+            if (pairs == 0) return CGTP_EUNSUP;
             b.pairs = pairs;
-            b.lds_bytes = lds_for<T>(b, pairs, chunk);
+            b.ntiles = block_tiles(b, pairs);
+            b.lds_bytes = lds_for<T>(b, pairs, b.ntiles);
             p->lds_bytes = std::max(p->lds_bytes, b.lds_bytes);
             blocks.push_back(b);
         }
@@ -452,22 +478,23 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
 template <typename T>
 int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTables<T>& h,
            const std::vector<int32_t>& list, cgtp::Tables<T>* tb) {
-    const std::vector<T>* parts[] = {&h.pbar, &h.wt, &h.tw, &h.lcg, &h.rcg, &h.ccg, &h.kinv};
-    size_t offs[9];
+    const std::vector<T>* parts[] = {&h.pbar, &h.wtab, &h.tw, &h.lcg, &h.rcg, &h.kinv};
+    constexpr int kParts = 6;
+    size_t offs[kParts + 2];
     size_t total = 0;
-    for (int i = 0; i < 7; ++i) {
+    for (int i = 0; i < kParts; ++i) {
         offs[i] = total;
         total = align_up(total + parts[i]->size() * sizeof(T), 256);
     }
-    offs[7] = total;
+    offs[kParts] = total;
     total = align_up(total + blocks.size() * sizeof(BlockDesc), 256);
-    offs[8] = total;
+    offs[kParts + 1] = total;
     total = align_up(total + list.size() * sizeof(int32_t), 256);
     std::vector<char> host(total, 0);
-    for (int i = 0; i < 7; ++i)
+    for (int i = 0; i < kParts; ++i)
         if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
-    std::memcpy(host.data() + offs[7], blocks.data(), blocks.size() * sizeof(BlockDesc));
-    std::memcpy(host.data() + offs[8], list.data(), list.size() * sizeof(int32_t));
+    std::memcpy(host.data() + offs[kParts], blocks.data(), blocks.size() * sizeof(BlockDesc));
+    std::memcpy(host.data() + offs[kParts + 1], list.data(), list.size() * sizeof(int32_t));
     hipError_t e = hipMalloc(&p->dmem, total);
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;
@@ -484,14 +511,14 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     p->dbytes = total;
     char* base = (char*)p->dmem;
     tb->pbar = (const T*)(base + offs[0]);
-    tb->wt = (const T*)(base + offs[1]);
+    tb->wtab = (const T*)(base + offs[1]);
     tb->tw = (const T*)(base + offs[2]);
     tb->lcg = (const T*)(base + offs[3]);
     tb->rcg = (const T*)(base + offs[4]);
-    tb->ccg = (const T*)(base + offs[5]);
-    tb->kinv = (const T*)(base + offs[6]);
-    tb->blocks = (const BlockDesc*)(base + offs[7]);
-    p->d_list = (const int32_t*)(base + offs[8]);
+    tb->kinv = (const T*)(base + offs[5]);
+    tb->cross_cg = (T)p->cross_cg;
+    tb->blocks = (const BlockDesc*)(base + offs[kParts]);
+    p->d_list = (const int32_t*)(base + offs[kParts + 1]);
     return CGTP_OK;
 }
 
