@@ -134,7 +134,7 @@ def main():
     main_res = time_workload(w, args.steps, args.warmup)
     log("  %.4f ms/step, %.4g pairs/s" % (main_res["ms_per_step"], main_res["value"]))
     secondary = []
-    if args.secondary:
+    if args.secondary and args.secondary != "none":
         for name in args.secondary.split(","):
             w2 = by_name[name]
             log("timing %s" % w2.name)

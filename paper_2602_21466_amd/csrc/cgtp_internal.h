@@ -8,16 +8,16 @@
 
 namespace cgtp {
 
-constexpr int kThreads = 256;      // work-group size of the block kernel (4 wave64s)
+constexpr int kThreads = 512;      // work-group size of the block kernel (8 wave64s, one per CU)
 constexpr int kWaves = kThreads / 64;
-constexpr int kRingGroup = 4;      // rings per pass: the K depth of one 16x16x4 MFMA
-constexpr int kLdsBudget = 80 * 1024;
+constexpr int kRingGroup = 8;      // rings per pass: two K = 4 steps of a 16x16x4 MFMA
+constexpr int kLdsBudget = 156 * 1024;
 constexpr int kMaxPairs = 16;
 
 // MFMA accumulator tiles (16 x 16) each wave may hold, per precision.
 template <typename T> struct MaxTiles;
-template <> struct MaxTiles<float> { static constexpr int value = 28; };
-template <> struct MaxTiles<double> { static constexpr int value = 12; };
+template <> struct MaxTiles<float> { static constexpr int value = 14; };
+template <> struct MaxTiles<double> { static constexpr int value = 6; };
 
 // Product kinds per path (mirrors cgtp_path_norm's *kind).
 enum PathKind : int32_t { kSS = 0, kCross = 1, kSV = 2, kDot = 3 };
@@ -51,9 +51,23 @@ struct alignas(16) BlockDesc {
     int32_t pbar_stride;       // Legendre entries per ring: (lmax+1)(lmax+2)/2
     int32_t wtab_off;          // offset of the grid's MFMA weight table (elements)
     int32_t lmax;              // largest degree of the grid's tables
-    int32_t kinv_off;          // offset of 1/K for j3 = d..J
-    int32_t pad0, pad1;
+    int32_t coef_off;          // offset of the block's output coefficients (3 per output)
+    int32_t tdesc_off;         // offset of the block's MFMA tile descriptors
+    int32_t lg_pairs;          // log2(pairs)
+    int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
+    int32_t sc;                // staged columns: 2 ncomp pairs rounded up to 16
+    int32_t pad0;
     int64_t out_off;           // offset of the block inside one pair's output
+};
+
+// One 16x16 accumulator tile of the Legendre projection, in the order the
+// waves take them (wave w owns tiles w, w + 4, ...).
+//   a_off: weight-table offset of (|m|, ring 0, first row l3_0) within the grid's table
+//   rs_nv: ring stride of the weight table | (valid rows of the tile << 16)
+//   b_off: staged-spectrum offset of (ring 0, first column, |m|)
+//   code:  |m| << 16 | row tile << 8 | column tile
+struct alignas(16) TileDesc {
+    int32_t a_off, rs_nv, b_off, code;
 };
 
 // Device tables, one allocation per plan; offsets in elements of T.
@@ -63,23 +77,26 @@ template <typename T>
 struct Tables {
     const T* pbar;      // [grid][ring][l (l+1)/2 + m]
     const T* wtab;      // see above
-    const T* tw;        // complex pairs [Phi][2]: exp(-2 pi i k / Phi)
+    const T* tw;        // per Phi, complex pairs in pass layout: [t < A][k2 < B+1] = exp(-2 pi i t k2 / Phi)
     const T* lcg;       // [j][q+1][m + j] = C^{j, m+q}_{j, m, 1, q}
-    const T* rcg;       // [j3][q+1][m3 + j3] = C^{j3, m3}_{j3-1, m3-q, 1, q}
-    const T* kinv;      // per block, j3 = d..J: 1 / K
+    const T* coef;      // per block and output (j3, m3): three recombination weights times 1/K
+    const TileDesc* tdesc;
     T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
     const BlockDesc* blocks;
 };
 
 // Blocks grouped by pairs-per-work-group.  One launch covers every class:
-// work-groups [cum[c], cum[c+1]) belong to class c, ntiles[c] consecutive
-// work-groups per block, heaviest classes first.
+// work-groups [cum[c], cum[c+1]) belong to class c, wpb[c] consecutive
+// work-groups per block, heaviest classes first; each work-group walks tpw[c]
+// consecutive tiles of pairs of its block.
 constexpr int kMaxClasses = 8;
 struct LaunchMap {
     int32_t ncls;
     int32_t pairs[kMaxClasses];
     int32_t list_off[kMaxClasses];
-    int64_t ntiles[kMaxClasses];
+    int32_t tpw[kMaxClasses];       // pair tiles per work-group
+    int64_t ntiles[kMaxClasses];    // pair tiles per block: ceil(N / pairs)
+    int64_t wpb[kMaxClasses];       // work-groups per block: ceil(ntiles / tpw)
     int64_t cum[kMaxClasses + 1];
 };
 
@@ -90,7 +107,7 @@ inline bool fft_factors(int phi, int* A, int* B) {
                                  {8, 4, 2},    {9, 3, 3},    {12, 4, 3},   {16, 4, 4},   {18, 6, 3},
                                  {24, 6, 4},   {27, 9, 3},   {32, 8, 4},   {36, 6, 6},   {48, 8, 6},
                                  {54, 9, 6},   {64, 8, 8},   {72, 9, 8},   {81, 9, 9},   {96, 12, 8},
-                                 {108, 12, 9}, {128, 16, 8}, {144, 12, 12}};
+                                 {108, 12, 9}, {128, 8, 16}, {144, 12, 12}};
     for (const auto& r : tab)
         if (r[0] == phi) {
             *A = r[1];

@@ -24,6 +24,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
 
 #include "cgtp_internal.h"
@@ -176,30 +177,53 @@ template <> __device__ __forceinline__ int acc_row<double>(int rq, int q) { retu
 
 __device__ __forceinline__ int acc_rowoff(int n, int d) { return 2 * n * n + (2 * d - 1) * n; }
 
+__device__ __forceinline__ int64_t rfl64(int64_t v) {
+    const int lo = __builtin_amdgcn_readfirstlane((int)(v & 0xffffffff));
+    const int hi = __builtin_amdgcn_readfirstlane((int)(v >> 32));
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
+    BlockDesc b;
+    const int32_t* src = reinterpret_cast<const int32_t*>(&g);
+    int32_t* dst = reinterpret_cast<int32_t*>(&b);
+#pragma unroll
+    for (int k = 0; k < (int)(offsetof(BlockDesc, out_off) / 4); ++k) dst[k] = __builtin_amdgcn_readfirstlane(src[k]);
+    b.out_off = rfl64(g.out_off);
+    return b;
+}
+
 // ---------------------------------------------------------------- LDS layout
+//
+// A longitude transform lives in "pass layout": A rows of B + 1 complex
+// entries (one pad per row), element k = k2 + B k1 at k1 (B + 1) + k2.  The
+// first pass writes rows, the second reads and rewrites columns in place, and
+// the padding keeps both access patterns free of bank conflicts.  The staged
+// spectra are [ring][column][|m|] with an odd |m| stride for the same reason.
 
 struct Layout {
-    int xs, lc, pst, twl, tiles, stage, fbuf, bbuf;   // byte offsets
-    int stage_cols;                                    // padded columns of one staged |m|
-    int fper;                                          // transforms per (ring, pair): nslot + nz
+    int xs, lc, pst, tw2, stage, fbuf, bbuf;   // byte offsets
+    int per_rp;                               // complex entries per (ring, pair)
 };
 
 __device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
 
-template <typename T>
-__device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, int nz, int ncomp) {
+// Block-level data first (couplings, Legendre rows of every ring, twiddles),
+// then the tile's inputs, then the per-ring working set; the end phase reuses
+// the working set for one pair's accumulators at a time.
+template <typename T, int A, int B>
+__device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     using C = typename Cplx<T>::type;
+    constexpr int FS = A * (B + 1);
     Layout l;
     const int P = b.pairs, n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     int o = 0;
-    l.xs = o; o = align16(o + (int)sizeof(T) * P * (n1 + n2));
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
-    l.pst = o; o = align16(o + (int)sizeof(T) * kRingGroup * (b.j1 + 1 + b.j2 + 1));
-    l.twl = o; o = align16(o + (int)sizeof(C) * b.Phi);
-    l.tiles = o; o = align16(o + 4 * b.ntiles);
-    l.stage_cols = ((2 * ncomp * P + 15) / 16) * 16;
-    l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * (b.J + 1) * l.stage_cols);
-    l.fper = nslot + nz;
+    l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
+    l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
+    l.xs = o; o = align16(o + (int)sizeof(T) * P * (n1 + n2));
+    l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
+    l.per_rp = nslot * FS;
     l.fbuf = o;
     l.bbuf = l.stage;
     return l;
@@ -208,38 +232,70 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, int
 // ---------------------------------------------------------------- the block body
 
 template <typename T, int A, int B>
-__device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0, int np, const T* __restrict__ x1,
-                           const T* __restrict__ x2, T* __restrict__ out, int L, unsigned char* smem) {
+__device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* __restrict__ tdesc,
+                                           const BlockDesc& bd, int64_t pt0, int64_t pt1, int64_t N,
+                                           const T* __restrict__ x1, const T* __restrict__ x2,
+                                           T* __restrict__ out, int L, unsigned char* smem) {
     using C = typename Cplx<T>::type;
     using Acc = typename Cplx<T>::acc4;
     constexpr int Phi = A * B;
     constexpr int H = Phi / 2 + 1;
+    constexpr int BP = B + 1;          // padded row of the pass layout
+    constexpr int FS = A * BP;         // padded transform
     constexpr int MT = MaxTiles<T>::value;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int j1 = bd.j1, j2 = bd.j2, J = bd.J, d = bd.d, R = bd.R, P = bd.pairs;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int j1 = bd.j1, j2 = bd.j2, J = bd.J, d = bd.d, R = bd.R, P = bd.pairs, lgP = bd.lg_pairs;
     const bool cross = bd.kind == kBlockCross;
-    const int nslot = cross ? 4 : 2;   // synthesis transforms per (ring, pair)
-    const int nz = cross ? 2 : 1;      // analysis transforms per (ring, pair)
+    const int lgS = cross ? 2 : 1;     // nslot = 4 or 2 synthesis transforms per (ring, pair)
+    const int lgZ = cross ? 1 : 0;     // nz = 2 or 1 analysis transforms per (ring, pair)
+    const int nslot = 1 << lgS, nz = 1 << lgZ;
     const int ncomp = cross ? 4 : 1;   // projected components
     const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
     const int nrows = (J - d) / 2 + 1;
     const int nel = nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
+    const int sm = bd.sm, sc = bd.sc;
     const TileGeom geo{nrows, ncomp, P};
 
-    const Layout ly = make_layout<T>(bd, nslot, nz, ncomp);
-    T* xs = reinterpret_cast<T*>(smem + ly.xs);          // [P][n1] then [P][n2]
+    const Layout ly = make_layout<T, A, B>(bd, nslot);
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
-    T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1]
-    C* twl = reinterpret_cast<C*>(smem + ly.twl);        // exp(-2 pi i k / Phi)
-    int* tiles = reinterpret_cast<int*>(smem + ly.tiles);
-    T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][|m|][stage_cols]
-    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [ring][pair][fper][Phi]
-    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [comp][nel], end phase only
+    T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
+    C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
+    T* xs = reinterpret_cast<T*>(smem + ly.xs);          // [P][n1] then [P][n2]
+    T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
+    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
+    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nel], end phase only
+    const TileDesc* __restrict__ td = tdesc + bd.tdesc_off;
+    const T* coef = tb.coef + bd.coef_off;
 
-    // ---- set-up: inputs of the tile, coupling rows, twiddles, tile table, zeroed staging
+    // ---- block-level set-up: couplings, Legendre rows of every ring, twiddles
+    for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
+    for (int e = tid; e < 3 * n2; e += kThreads) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
+    {
+        const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
+        for (int e = tid; e < FS; e += kThreads) tw2[e] = tw[e];
+    }
+    const int npr = j1 + 1 + j2 + 1;
+    for (int e = tid; e < R * npr; e += kThreads) {
+        const int r = e / npr, q = e - r * npr;
+        const T* prow = tb.pbar + bd.pbar_off + (size_t)r * bd.pbar_stride;
+        pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
+    }
+
+    const T* wtab = tb.wtab + bd.wtab_off;
+    const T cc = tb.cross_cg;
+    // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
+    // unpacking two packed signals, and the cross product's coupling constant
+    const T sc_s = (T)(6.283185307179586476925286766559 / Phi) * (cross ? (T)0.25 : (T)1);
+    const T sc_v = sc_s * cc;
+
+    for (int64_t pt = pt0; pt < pt1; ++pt) {
+    const int64_t p0 = pt * P;
+    const int np = (int)((N - p0) < P ? (N - p0) : P);
+    // ---- inputs of the tile (rows past N read as zero), zeroed staging
     for (int e = tid; e < P * n1; e += kThreads) {
         const int p = e / n1, m = e - p * n1;
         xs[e] = p < np ? x1[(p0 + p) * nin + j1 * j1 + m] : (T)0;
@@ -248,73 +304,48 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
         const int p = e / n2, m = e - p * n2;
         xs[P * n1 + e] = p < np ? x2[(p0 + p) * nin + j2 * j2 + m] : (T)0;
     }
-    for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
-    for (int e = tid; e < 3 * n2; e += kThreads) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
-    {
-        const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
-        for (int e = tid; e < Phi; e += kThreads) twl[e] = tw[e];
-    }
-    for (int e = tid; e < kRingGroup * (J + 1) * ly.stage_cols; e += kThreads) stage[e] = (T)0;
-    if (tid == 0) {
-        int u = 0;
-        for (int mp = 0; mp <= J; ++mp)
-            for (int rt = 0; rt < geo.nrt(mp, d); ++rt)
-                for (int ct = 0; ct < geo.nct(mp); ++ct) tiles[u++] = (mp << 16) | (rt << 8) | ct;
-    }
+    for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
 
     Acc acc[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) acc[s] = Acc(0);
-
-    const T* wtab = tb.wtab + bd.wtab_off;
-    const int lmax = bd.lmax;
-    const T cc = tb.cross_cg;
-    // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
-    // unpacking two packed signals, and the cross product's coupling constant
-    const T sc_s = (T)(6.283185307179586476925286766559 / Phi) * (cross ? (T)0.25 : (T)1);
-    const T sc_v = sc_s * cc;
+    __syncthreads();
 
     for (int rg0 = 0; rg0 < R; rg0 += kRingGroup) {
         const int nrg = (R - rg0) < kRingGroup ? (R - rg0) : kRingGroup;
-        // P^m_j rows of both degrees for the group's rings
-        for (int e = tid; e < nrg * (j1 + 1 + j2 + 1); e += kThreads) {
-            const int r = e / (j1 + 1 + j2 + 1), q = e - r * (j1 + 1 + j2 + 1);
-            const T* prow = tb.pbar + bd.pbar_off + (size_t)(rg0 + r) * bd.pbar_stride;
-            pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
-        }
-        __syncthreads();
 
-        // ---- 1. lift + synthesis pass 1: task (ring, pair, slot, t)
+        // ---- 1. lift + synthesis pass 1: task ((ring, pair, slot), t) -> row t
         {
-            const int ntask = nrg * P * nslot * A;
+            const int ntask = (nrg << (lgP + lgS)) * A;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int t = task % A;
-                int rest = task / A;
-                const int s = rest % nslot;
-                rest /= nslot;
-                const int p = rest % P, r = rest / P;
+                const int f = task / A;
+                const int s = f & (nslot - 1);
+                const int rp = f >> lgS;
+                const int p = rp & (P - 1), r = rp >> lgP;
                 const bool first = cross ? (s < 2) : (s == 0);
                 const int j = first ? j1 : j2;
                 const int nj = 2 * j + 1;
                 const T* xv = first ? xs + p * n1 : xs + P * n1 + p * n2;
                 const T* lcj = first ? lc : lc + 3 * n1;
-                const T* pr = pst + r * (j1 + 1 + j2 + 1) + (first ? 0 : j1 + 1);
+                const T* pr = pst + (rg0 + r) * npr + (first ? 0 : j1 + 1);
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {
                     const int n = t + A * n2i;
-                    const int m = n <= j ? n : (n >= Phi - j ? n - Phi : 1 << 20);
+                    const int m = n <= j ? n : n - Phi;
                     T re = 0, im = 0;
-                    if (m != (1 << 20)) {
+                    if (n <= j || n >= Phi - j) {
                         const int am = m < 0 ? -m : m;
                         T pv = pr[am];
                         if (m < 0 && (am & 1)) pv = -pv;
+                        const T xp = xv[m + j] * pv;
                         if (!cross) {
-                            re = xv[m + j] * pv;
+                            re = xp;
                         } else if ((s & 1) == 0) {
                             // scalar lift (real part) and the q = 0 vector lift (imaginary part)
-                            re = xv[m + j] * pv;
-                            im = lcj[nj + m + j] * xv[m + j] * pv;
+                            re = xp;
+                            im = lcj[nj + m + j] * xp;
                         } else {
                             // q = -1 (real part) and q = +1 (imaginary part) vector lifts
                             if (m - 1 >= -j) re = lcj[m + j] * xv[m - 1 + j] * pv;
@@ -324,47 +355,49 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
                     v[n2i] = cmk<C>(re, im);
                 }
                 Dft<B, true, C>::run(v);
-                C* f = fbuf + ((size_t)(r * P + p) * ly.fper + s) * Phi;
+                C* row = fbuf + (size_t)rp * ly.per_rp + (size_t)s * FS + t * BP;
+                const C* twr = tw2 + t * BP;
 #pragma unroll
-                for (int k2 = 0; k2 < B; ++k2) f[k2 + B * t] = k2 == 0 ? v[k2] : cmulc(v[k2], twl[t * k2]);
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], twr[k2]);
             }
         }
         __syncthreads();
-        // ---- 2. synthesis pass 2 (in place): task (ring, pair, slot, k2)
+        // ---- 2. synthesis pass 2 (in place): task ((ring, pair, slot), column k2)
         {
-            const int ntask = nrg * P * nslot * B;
+            const int ntask = (nrg << (lgP + lgS)) * B;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int k2 = task % B;
                 const int f = task / B;
-                const int s = f % nslot, rp = f / nslot;
-                C* fb = fbuf + ((size_t)rp * ly.fper + s) * Phi;
+                C* fb = fbuf + (size_t)(f >> lgS) * ly.per_rp + (size_t)(f & (nslot - 1)) * FS + k2;
                 C u[A];
 #pragma unroll
-                for (int t = 0; t < A; ++t) u[t] = fb[k2 + B * t];
+                for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
                 Dft<A, true, C>::run(u);
 #pragma unroll
-                for (int k1 = 0; k1 < A; ++k1) fb[k2 + B * k1] = u[k1];
+                for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
             }
         }
         __syncthreads();
         // ---- 3. pointwise products on half the circle, mirrored
         {
-            const int ntask = nrg * P * H;
+            const int ntask = (nrg << lgP) * H;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int n = task % H, rp = task / H;
                 const int kk = n == 0 ? 0 : Phi - n;
-                C* fb = fbuf + (size_t)rp * ly.fper * Phi;
-                C* zb = fb + (size_t)nslot * Phi;
+                const int pn = n + n / B, pk = kk + kk / B;   // pass-layout positions
+                // the products overwrite the second input's transforms: positions
+                // n and -n are read and written by this task only
+                C* fb = fbuf + (size_t)rp * ly.per_rp;
                 if (!cross) {
-                    const C g = cmul(fb[n], fb[Phi + n]);
-                    zb[n] = g;
-                    zb[kk] = cconj(g);
+                    const C g = cmul(fb[pn], fb[FS + pn]);
+                    fb[FS + pn] = g;
+                    fb[FS + pk] = cconj(g);
                 } else {
                     // unpacked (times 2): fA = F(n) + conj F(-n), fB = -i (F(n) - conj F(-n))
                     C f[8];
 #pragma unroll
                     for (int s = 0; s < 4; ++s) {
-                        const C Fn = fb[s * Phi + n], Fk = fb[s * Phi + kk];
+                        const C Fn = fb[s * FS + pn], Fk = fb[s * FS + pk];
                         f[2 * s] = cmk<C>(Fn.x + Fk.x, Fn.y - Fk.y);
                         f[2 * s + 1] = cmk<C>(Fn.y + Fk.y, Fk.x - Fn.x);
                     }
@@ -376,48 +409,54 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
                     const C g0 = csub(cmul(ap, bm), cmul(am, bp));
                     const C gm = csub(cmul(a0, bm), cmul(am, b0));
                     // z1 = gs + i g0, z2 = g-1 + i g+1; at -n the conjugated signals
-                    zb[n] = cmk<C>(gs.x - g0.y, gs.y + g0.x);
-                    zb[Phi + n] = cmk<C>(gm.x - gp.y, gm.y + gp.x);
+                    C* z1 = fb + 2 * FS;
+                    C* z2 = fb + 3 * FS;
+                    z1[pn] = cmk<C>(gs.x - g0.y, gs.y + g0.x);
+                    z2[pn] = cmk<C>(gm.x - gp.y, gm.y + gp.x);
                     if (kk != n) {
-                        zb[kk] = cmk<C>(gs.x + g0.y, g0.x - gs.y);
-                        zb[Phi + kk] = cmk<C>(gm.x + gp.y, gp.x - gm.y);
+                        z1[pk] = cmk<C>(gs.x + g0.y, g0.x - gs.y);
+                        z2[pk] = cmk<C>(gm.x + gp.y, gp.x - gm.y);
                     }
                 }
             }
         }
         __syncthreads();
-        // ---- 4a. analysis pass 1: task (ring, pair, z, t); result into slot z
+        // ---- 4a. analysis pass 1: task ((ring, pair, z), t); rows into slot z
         {
-            const int ntask = nrg * P * nz * A;
+            const int ntask = (nrg << (lgP + lgZ)) * A;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int t = task % A;
                 const int f = task / A;
-                const int z = f % nz, rp = f / nz;
-                const C* zb = fbuf + ((size_t)rp * ly.fper + nslot + z) * Phi;
+                const int z = f & (nz - 1), rp = f >> lgZ;
+                const C* zb = fbuf + (size_t)rp * ly.per_rp + (size_t)(nslot - nz + z) * FS;
                 C v[B];
 #pragma unroll
-                for (int n2i = 0; n2i < B; ++n2i) v[n2i] = zb[t + A * n2i];
+                for (int n2i = 0; n2i < B; ++n2i) {
+                    const int n = t + A * n2i;
+                    v[n2i] = zb[n + n / B];
+                }
                 Dft<B, false, C>::run(v);
-                C* yb = fbuf + ((size_t)rp * ly.fper + z) * Phi;
+                C* row = fbuf + (size_t)rp * ly.per_rp + (size_t)z * FS + t * BP;
+                const C* twr = tw2 + t * BP;
 #pragma unroll
-                for (int k2 = 0; k2 < B; ++k2) yb[k2 + B * t] = k2 == 0 ? v[k2] : cmul(v[k2], twl[t * k2]);
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], twr[k2]);
             }
         }
         __syncthreads();
         // ---- 4b. analysis pass 2 and staging of |m| <= J, scaled
         {
-            const int ntask = nrg * P * nz * B;
+            const int ntask = (nrg << (lgP + lgZ)) * B;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int k2 = task % B;
                 const int f = task / B;
-                const int z = f % nz, rp = f / nz;
-                const int p = rp % P, r = rp / P;
-                const C* yb = fbuf + ((size_t)rp * ly.fper + z) * Phi;
+                const int z = f & (nz - 1), rp = f >> lgZ;
+                const int p = rp & (P - 1), r = rp >> lgP;
+                const C* yb = fbuf + (size_t)rp * ly.per_rp + (size_t)z * FS + k2;
                 C u[A];
 #pragma unroll
-                for (int t = 0; t < A; ++t) u[t] = yb[k2 + B * t];
+                for (int t = 0; t < A; ++t) u[t] = yb[t * BP];
                 Dft<A, false, C>::run(u);
-                T* st = stage + (size_t)r * (J + 1) * ly.stage_cols;
+                T* st = stage + (size_t)r * sc * sm;
 #pragma unroll
                 for (int k1 = 0; k1 < A; ++k1) {
                     const int k = k2 + B * k1;
@@ -428,11 +467,11 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
                     const T flip = (sg && (mp & 1)) ? (T)-1 : (T)1;   // P^{-m} = (-1)^m P^m
                     const int cbase = sg * ncomp * P;
                     if (!cross) {
-                        st[mp * ly.stage_cols + cbase + p] = u[k1].x * sc_s * flip;
+                        st[(cbase + p) * sm + mp] = u[k1].x * sc_s * flip;
                     } else {
                         const int c0 = 2 * z, c1 = 2 * z + 1;
-                        st[mp * ly.stage_cols + cbase + c0 * P + p] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
-                        st[mp * ly.stage_cols + cbase + c1 * P + p] = u[k1].y * sc_v * flip;
+                        st[(cbase + c0 * P + p) * sm + mp] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
+                        st[(cbase + c1 * P + p) * sm + mp] = u[k1].y * sc_v * flip;
                     }
                 }
             }
@@ -441,22 +480,24 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
         // ---- 5. Legendre projection on MFMA, accumulated over ring groups
         {
             const int i = lane & 15, kq = lane >> 4;
-            const int ring = rg0 + kq;
 #pragma unroll
-            for (int s = 0; s < MT; ++s) {
-                const int u = wave + kWaves * s;
-                if (u < bd.ntiles) {
-                    const int code = __builtin_amdgcn_readfirstlane(tiles[u]);   // wave-uniform
-                    const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
-                    const int l3 = d + 2 * (geo.tmin(mp, d) + 16 * rt + i);
-                    T a = 0;
-                    if (ring < R && l3 <= J) {
-                        const int moff = R * (mp * (lmax + 1) - mp * (mp - 1) / 2);
-                        a = wtab[moff + ring * (lmax - mp + 1) + (l3 - mp)];
-                    }
-                    const T bv = stage[((size_t)kq * (J + 1) + mp) * ly.stage_cols + 16 * ct + i];
-                    acc[s] = mfma16(a, bv, acc[s]);
+            for (int h = 0; h < kRingGroup / 4; ++h) {
+                const int ring = rg0 + 4 * h + kq;
+                const T* stk = stage + (size_t)(4 * h + kq) * sc * sm + i * sm;
+                // descriptors and operands of all this wave's tiles first (branch-free,
+                // tile index clamped), so their latencies overlap; then the MFMAs
+                T av[MT], bv[MT];
+#pragma unroll
+                for (int s = 0; s < MT; ++s) {
+                    const int u = min(wave + kWaves * s, bd.ntiles - 1);
+                    const TileDesc t = td[u];   // wave-uniform: scalar loads
+                    const bool ok = wave + kWaves * s < bd.ntiles && ring < R && i < (t.rs_nv >> 16);
+                    av[s] = ok ? wtab[t.a_off + ring * (t.rs_nv & 0xffff) + 2 * i] : (T)0;
+                    bv[s] = stk[t.b_off];
                 }
+#pragma unroll
+                for (int s = 0; s < MT; ++s)
+                    if (wave + kWaves * s < bd.ntiles) acc[s] = mfma16(av[s], bv[s], acc[s]);
             }
         }
         __syncthreads();
@@ -469,13 +510,13 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
         for (int s = 0; s < MT; ++s) {
             const int u = wave + kWaves * s;
             if (u < bd.ntiles) {
-                const int code = __builtin_amdgcn_readfirstlane(tiles[u]);   // wave-uniform
+                const int code = td[u].code;   // wave-uniform
                 const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
                 const int col = 16 * ct + col_in;
-                const int p = col % P;
+                const int p = col & (P - 1);
                 if (col < geo.ncols(mp) && p < np) {
                     const int sg = col / (ncomp * P);
-                    const int comp = (col / P) % ncomp;
+                    const int comp = (col >> lgP) % ncomp;
                     const int m = sg ? -mp : mp;
                     T* dst = bbuf + (size_t)(p * ncomp + comp) * nel;
 #pragma unroll
@@ -490,51 +531,53 @@ __device__ void block_body(const Tables<T>& tb, const BlockDesc& bd, int64_t p0,
     }
     __syncthreads();
     const int nblk = n1 * n2;
-    const T* kinv = tb.kinv + bd.kinv_off;
     for (int e = tid; e < np * nblk; e += kThreads) {
         const int p = e / nblk, o = e - p * nblk;
         int j3 = (int)sqrtf((float)(o + d * d));
         while (j3 * j3 - d * d > o) --j3;
         while ((j3 + 1) * (j3 + 1) - d * d <= o) ++j3;
         const int m3 = o - (j3 * j3 - d * d) - j3;
+        const T* cf = coef + 3 * o;
         const T* bp = bbuf + (size_t)p * ncomp * nel;
         T z;
         if (((J + j3) & 1) == 0) {
-            z = bp[acc_rowoff((j3 - d) / 2, d) + j3 + m3];
+            z = cf[0] * bp[acc_rowoff((j3 - d) / 2, d) + j3 + m3];
         } else {
             const int l3 = j3 - 1;
             const int roff = acc_rowoff((l3 - d) / 2, d) + l3;
-            const T* rc = tb.rcg + 3 * j3 * j3 + m3 + j3;
-            const int nj3 = 2 * j3 + 1;
             z = 0;
             // components: 1 -> q = 0, 2 -> q = -1, 3 -> q = +1
-            if (m3 + 1 <= l3) z += rc[0] * bp[2 * nel + roff + m3 + 1];
-            if (m3 >= -l3 && m3 <= l3) z += rc[nj3] * bp[1 * nel + roff + m3];
-            if (m3 - 1 >= -l3) z += rc[2 * nj3] * bp[3 * nel + roff + m3 - 1];
+            if (m3 + 1 <= l3) z += cf[0] * bp[2 * nel + roff + m3 + 1];
+            if (m3 >= -l3 && m3 <= l3) z += cf[1] * bp[1 * nel + roff + m3];
+            if (m3 - 1 >= -l3) z += cf[2] * bp[3 * nel + roff + m3 - 1];
         }
-        out[(p0 + p) * nout + bd.out_off + o] = z * kinv[j3 - d];
+        out[(p0 + p) * nout + bd.out_off + o] = z;
     }
+    __syncthreads();
+    }   // pair tiles
 }
 
 template <typename T>
-__global__ __launch_bounds__(kThreads, 2) void block_kernel(Tables<T> tb, const int32_t* __restrict__ list,
-                                                         LaunchMap map, const T* __restrict__ x1,
-                                                         const T* __restrict__ x2, T* __restrict__ out, int64_t N,
-                                                         int L) {
+__global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const BlockDesc* __restrict__ blocks,
+                                                            const TileDesc* __restrict__ tdesc,
+                                                            const int32_t* __restrict__ list, LaunchMap map,
+                                                            const T* __restrict__ x1, const T* __restrict__ x2,
+                                                            T* __restrict__ out, int64_t N, int L) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int64_t wg = blockIdx.x;
     int cls = 0;
     while (cls + 1 < map.ncls && wg >= map.cum[cls + 1]) ++cls;
-    const int64_t ntiles = map.ntiles[cls];
+    const int64_t wpb = map.wpb[cls];
     const int64_t local = wg - map.cum[cls];
-    const int bi = (int)(local / ntiles);
-    const int64_t tile = local - (int64_t)bi * ntiles;
-    const BlockDesc bd = tb.blocks[list[map.list_off[cls] + bi]];
-    const int64_t p0 = tile * bd.pairs;
-    const int np = (int)((N - p0) < bd.pairs ? (N - p0) : bd.pairs);
+    const int bi = (int)(local / wpb);
+    const int64_t g = local - (int64_t)bi * wpb;
+    // every descriptor field is wave-uniform: keep it in scalar registers
+    const BlockDesc bd = uniform_desc(blocks[list[map.list_off[cls] + bi]]);
+    const int64_t pt0 = g * map.tpw[cls];
+    const int64_t pt1 = (pt0 + map.tpw[cls]) < map.ntiles[cls] ? (pt0 + map.tpw[cls]) : map.ntiles[cls];
 
 #define CGTP_CASE(PHI, A_, B_) \
-    case PHI: block_body<T, A_, B_>(tb, bd, p0, np, x1, x2, out, L, smem); break;
+    case PHI: block_body<T, A_, B_>(tb, tdesc, bd, pt0, pt1, N, x1, x2, out, L, smem); break;
     switch (bd.Phi) {
         CGTP_CASE(1, 1, 1)
         CGTP_CASE(2, 2, 1)
@@ -557,7 +600,7 @@ __global__ __launch_bounds__(kThreads, 2) void block_kernel(Tables<T> tb, const 
         CGTP_CASE(81, 9, 9)
         CGTP_CASE(96, 12, 8)
         CGTP_CASE(108, 12, 9)
-        CGTP_CASE(128, 16, 8)
+        CGTP_CASE(128, 8, 16)
         CGTP_CASE(144, 12, 12)
         default: break;
     }
@@ -575,8 +618,8 @@ int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int l
                                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return (int)e;
     }
-    hipLaunchKernelGGL(block_kernel<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb, list,
-                       map, x1, x2, out, N, L);
+    hipLaunchKernelGGL(block_kernel<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb,
+                       tb.blocks, tb.tdesc, list, map, x1, x2, out, N, L);
     return (int)hipGetLastError();
 }
 

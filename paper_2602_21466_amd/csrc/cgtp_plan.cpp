@@ -306,7 +306,8 @@ namespace {
 
 template <typename T>
 struct HostTables {
-    std::vector<T> pbar, wtab, tw, lcg, rcg, kinv;
+    std::vector<T> pbar, wtab, tw, lcg, coef;
+    std::vector<cgtp::TileDesc> tdesc;
 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -324,21 +325,21 @@ int block_tiles(const BlockDesc& b, int pairs) {
 
 // Dynamic LDS of one work-group; mirrors the kernel's make_layout.
 template <typename T>
-int lds_for(const BlockDesc& b, int pairs, int ntiles) {
+int lds_for(const BlockDesc& b, int pairs) {
     const int sz = (int)sizeof(T), csz = 2 * sz;
     const bool cross = b.kind == cgtp::kBlockCross;
-    const int nslot = cross ? 4 : 2, nz = cross ? 2 : 1, ncomp = cross ? 4 : 1;
+    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
     const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
+    const int FS = b.A * (b.B + 1);
     int o = 0;
-    o = align16h(o + sz * pairs * (n1 + n2));
     o = align16h(o + sz * 3 * (n1 + n2));
-    o = align16h(o + sz * cgtp::kRingGroup * (b.j1 + 1 + b.j2 + 1));
-    o = align16h(o + csz * b.Phi);
-    o = align16h(o + 4 * ntiles);
-    const int stage_cols = ((2 * ncomp * pairs + 15) / 16) * 16;
+    o = align16h(o + sz * b.R * (b.j1 + 1 + b.j2 + 1));
+    o = align16h(o + csz * FS);
+    o = align16h(o + sz * pairs * (n1 + n2));
     const int stage = o;
-    o = align16h(o + sz * cgtp::kRingGroup * (b.J + 1) * stage_cols);
-    o += csz * cgtp::kRingGroup * pairs * (nslot + nz) * b.Phi;
+    const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
+    o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
+    o += csz * cgtp::kRingGroup * pairs * nslot * FS;
     const int end_phase = stage + sz * pairs * ncomp * acc_entries(b.d, b.J);
     return std::max(o, end_phase);
 }
@@ -381,12 +382,16 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
     }
     for (auto& kv : phi_set) {
         const int n = kv.first;
+        int A, B;
+        if (!cgtp::fft_factors(n, &A, &B)) return CGTP_EUNSUP;
         kv.second = (int)(h.tw.size() / 2);
-        for (int k = 0; k < n; ++k) {
-            long double a = -2.0L * kPi * k / n;
-            h.tw.push_back((T)cosl(a));
-            h.tw.push_back((T)sinl(a));
-        }
+        // pass layout: [t < A][k2 < B + 1] = exp(-2 pi i t k2 / n), pad entry zero
+        for (int t = 0; t < A; ++t)
+            for (int k2 = 0; k2 <= B; ++k2) {
+                const long double a = -2.0L * kPi * (long double)((t * k2) % n) / n;
+                h.tw.push_back(k2 < B ? (T)cosl(a) : (T)0);
+                h.tw.push_back(k2 < B ? (T)sinl(a) : (T)0);
+            }
         p->max_phi = std::max(p->max_phi, n);
     }
     // ---- Clebsch-Gordan tables
@@ -395,11 +400,6 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
         for (int q = -1; q <= 1; ++q)
             for (int m = -j; m <= j; ++m)
                 h.lcg[3 * j * j + (q + 1) * (2 * j + 1) + m + j] = (T)cg_vec(j, m, q, j, m + q);
-    h.rcg.assign(3 * (size_t)(2 * L + 1) * (2 * L + 1), (T)0);
-    for (int j3 = 1; j3 <= 2 * L; ++j3)
-        for (int q = -1; q <= 1; ++q)
-            for (int m3 = -j3; m3 <= j3; ++m3)
-                h.rcg[3 * j3 * j3 + (q + 1) * (2 * j3 + 1) + m3 + j3] = (T)cg_vec(j3 - 1, m3 - q, q, j3, m3);
     // The kernel forms the cross product as c * (antisymmetric combination) with
     // c = C^{1,1}_{1,1,1,0}; check the coupling table has that structure.
     const long double c = cg_vec(1, 1, 0, 1, 1);
@@ -428,7 +428,9 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.pbar_stride = grid_stride[nt];
             b.wtab_off = grid_wtab_off[nt];
             b.lmax = grid_lmax[nt];
-            b.kinv_off = (int)h.kinv.size();
+            // output coefficients: 1/K for scalar-scalar paths; for cross paths the
+            // recombination weights C^{j3 m3}_{j3-1, m3-q, 1, q} (q = -1, 0, +1) times 1/K
+            b.coef_off = (int)h.coef.size();
             for (int j3 = b.d; j3 <= b.J; ++j3) {
                 long double K;
                 int kind;
@@ -436,7 +438,16 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                 const int want = ((b.J + j3) & 1) ? cgtp::kCross : cgtp::kSS;
                 if (kind != want || fabsl(K) < kMinAbsK) return CGTP_EUNSUP;
                 min_abs_K = std::min(min_abs_K, (double)fabsl(K));
-                h.kinv.push_back((T)(1.0L / K));
+                const long double kinv = 1.0L / K;
+                for (int m3 = -j3; m3 <= j3; ++m3) {
+                    if (kind == cgtp::kSS) {
+                        h.coef.push_back((T)kinv);
+                        h.coef.push_back((T)0);
+                        h.coef.push_back((T)0);
+                    } else {
+                        for (int q = -1; q <= 1; ++q) h.coef.push_back((T)(kinv * cg_vec(j3 - 1, m3 - q, q, j3, m3)));
+                    }
+                }
             }
             b.out_off = path_offset(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
@@ -444,13 +455,36 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
             int pairs = 0;
             for (int P = cgtp::kMaxPairs; P >= 1; P /= 2) {
-                const int nt_ = block_tiles(b, P);
-                if (nt_ <= max_tiles && lds_for<T>(b, P, nt_) <= cgtp::kLdsBudget) { pairs = P; break; }
+                if (block_tiles(b, P) <= max_tiles && lds_for<T>(b, P) <= cgtp::kLdsBudget) { pairs = P; break; }
             }
             if (pairs == 0) return CGTP_EUNSUP;
             b.pairs = pairs;
+            b.lg_pairs = 0;
+            while ((1 << b.lg_pairs) < pairs) ++b.lg_pairs;
             b.ntiles = block_tiles(b, pairs);
-            b.lds_bytes = lds_for<T>(b, pairs, b.ntiles);
+            b.lds_bytes = lds_for<T>(b, pairs);
+            const int ncomp = b.kind == cgtp::kBlockCross ? 4 : 1;
+            b.sc = ((2 * ncomp * pairs + 15) / 16) * 16;
+            b.sm = (b.J + 1) | 1;
+            // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
+            b.tdesc_off = (int)h.tdesc.size();
+            {
+                cgtp::TileGeom geo{(b.J - b.d) / 2 + 1, ncomp, pairs};
+                for (int mp = 0; mp <= b.J; ++mp)
+                    for (int rt = 0; rt < geo.nrt(mp, b.d); ++rt)
+                        for (int ct = 0; ct < geo.nct(mp); ++ct) {
+                            const int row0 = geo.tmin(mp, b.d) + 16 * rt;
+                            const int l30 = b.d + 2 * row0;
+                            const int nv = std::min(16, geo.nrows - row0);
+                            const int moff = b.R * (mp * (b.lmax + 1) - mp * (mp - 1) / 2);
+                            cgtp::TileDesc t;
+                            t.a_off = moff + (l30 - mp);
+                            t.rs_nv = (b.lmax - mp + 1) | (nv << 16);
+                            t.b_off = 16 * ct * b.sm + mp;
+                            t.code = (mp << 16) | (rt << 8) | ct;
+                            h.tdesc.push_back(t);
+                        }
+            }
             p->lds_bytes = std::max(p->lds_bytes, b.lds_bytes);
             blocks.push_back(b);
         }
@@ -478,8 +512,8 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
 template <typename T>
 int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTables<T>& h,
            const std::vector<int32_t>& list, cgtp::Tables<T>* tb) {
-    const std::vector<T>* parts[] = {&h.pbar, &h.wtab, &h.tw, &h.lcg, &h.rcg, &h.kinv};
-    constexpr int kParts = 6;
+    const std::vector<T>* parts[] = {&h.pbar, &h.wtab, &h.tw, &h.lcg, &h.coef};
+    constexpr int kParts = 5;
     size_t offs[kParts + 2];
     size_t total = 0;
     for (int i = 0; i < kParts; ++i) {
@@ -490,7 +524,11 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     total = align_up(total + blocks.size() * sizeof(BlockDesc), 256);
     offs[kParts + 1] = total;
     total = align_up(total + list.size() * sizeof(int32_t), 256);
+    const size_t tdesc_off = total;
+    total = align_up(total + h.tdesc.size() * sizeof(cgtp::TileDesc), 256);
     std::vector<char> host(total, 0);
+    if (!h.tdesc.empty())
+        std::memcpy(host.data() + tdesc_off, h.tdesc.data(), h.tdesc.size() * sizeof(cgtp::TileDesc));
     for (int i = 0; i < kParts; ++i)
         if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
     std::memcpy(host.data() + offs[kParts], blocks.data(), blocks.size() * sizeof(BlockDesc));
@@ -514,10 +552,10 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->wtab = (const T*)(base + offs[1]);
     tb->tw = (const T*)(base + offs[2]);
     tb->lcg = (const T*)(base + offs[3]);
-    tb->rcg = (const T*)(base + offs[4]);
-    tb->kinv = (const T*)(base + offs[5]);
+    tb->coef = (const T*)(base + offs[4]);
     tb->cross_cg = (T)p->cross_cg;
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
+    tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
     return CGTP_OK;
 }
@@ -684,12 +722,20 @@ int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, in
     cgtp::LaunchMap map{};
     map.ncls = (int32_t)plan->classes.size();
     map.cum[0] = 0;
+    // pair tiles per work-group: enough work-groups to fill the device several
+    // times over, the rest walked in a loop so block-level set-up is amortised
+    int64_t total_tiles = 0;
+    for (const auto& cl : plan->classes) total_tiles += (N + cl.pairs - 1) / cl.pairs * cl.count;
+    const int64_t target_wgs = 16384;
+    int tpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, total_tiles / target_wgs));
     for (int c = 0; c < map.ncls; ++c) {
         const auto& cl = plan->classes[c];
         map.pairs[c] = cl.pairs;
         map.list_off[c] = cl.off;
+        map.tpw[c] = tpw;
         map.ntiles[c] = (N + cl.pairs - 1) / cl.pairs;
-        map.cum[c + 1] = map.cum[c] + map.ntiles[c] * cl.count;
+        map.wpb[c] = (map.ntiles[c] + tpw - 1) / tpw;
+        map.cum[c + 1] = map.cum[c] + map.wpb[c] * cl.count;
     }
     int err;
     if (plan->grid.dtype == CGTP_FP32)
