@@ -51,7 +51,7 @@ struct alignas(16) BlockDesc {
     int32_t pbar_stride;       // Legendre entries per ring: (lmax+1)(lmax+2)/2
     int32_t wtab_off;          // offset of the grid's MFMA weight table (elements)
     int32_t lmax;              // largest degree of the grid's tables
-    int32_t coef_off;          // offset of the block's output coefficients (3 per output)
+    int32_t coef_off;          // offset of the block's output coefficients (4 per output)
     int32_t tdesc_off;         // offset of the block's MFMA tile descriptors
     int32_t lg_pairs;          // log2(pairs)
     int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
@@ -79,7 +79,7 @@ struct Tables {
     const T* wtab;      // see above
     const T* tw;        // per Phi, complex pairs in pass layout: [t < A][k2 < B+1] = exp(-2 pi i t k2 / Phi)
     const T* lcg;       // [j][q+1][m + j] = C^{j, m+q}_{j, m, 1, q}
-    const T* coef;      // per block and output (j3, m3): three recombination weights times 1/K
+    const T* coef;      // per block and output (j3, m3): recombination weights times 1/K, and the source index
     const TileDesc* tdesc;
     T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
     const BlockDesc* blocks;

@@ -202,15 +202,15 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // spectra are [ring][column][|m|] with an odd |m| stride for the same reason.
 
 struct Layout {
-    int xs, lc, pst, tw2, stage, fbuf, bbuf;   // byte offsets
-    int per_rp;                               // complex entries per (ring, pair)
+    int lc, pst, tw2, stab, lc2, stage, fbuf, bbuf;   // byte offsets
+    int per_rp;                                      // complex entries per (ring, pair)
 };
 
 __device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
 
-// Block-level data first (couplings, Legendre rows of every ring, twiddles),
-// then the tile's inputs, then the per-ring working set; the end phase reuses
-// the working set for one pair's accumulators at a time.
+// Block-level data first (couplings, Legendre rows of every ring, twiddles,
+// staging map), then the tile's lifted coefficients, then the per-ring
+// working set; the end phase reuses the working set for the accumulators.
 template <typename T, int A, int B>
 __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     using C = typename Cplx<T>::type;
@@ -221,7 +221,8 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
     l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
-    l.xs = o; o = align16(o + (int)sizeof(T) * P * (n1 + n2));
+    l.stab = o; o = align16(o + 4 * A * B);
+    l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
     l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
     l.per_rp = nslot * FS;
     l.fbuf = o;
@@ -264,12 +265,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
     T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
-    T* xs = reinterpret_cast<T*>(smem + ly.xs);          // [P][n1] then [P][n2]
+    int* stab = reinterpret_cast<int*>(smem + ly.stab);  // longitude k -> staged offset | sign, or -1
+    C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
     T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nel], end phase only
     const TileDesc* __restrict__ td = tdesc + bd.tdesc_off;
-    const T* coef = tb.coef + bd.coef_off;
+    using Coef4 = typename Cplx<T>::acc4;
+    const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef + bd.coef_off);
 
     // ---- block-level set-up: couplings, Legendre rows of every ring, twiddles
     for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
@@ -285,6 +288,18 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
     }
 
+    // staging map: orders |m| <= J of the analysis spectrum, with the sign of
+    // P^{-m} = (-1)^m P^m folded in for negative m
+    for (int k = tid; k < Phi; k += kThreads) {
+        int code = -1;
+        if (k <= J) code = k;
+        else if (k >= Phi - J) {
+            const int mp = Phi - k;
+            code = (ncomp * P * sm + mp) | ((mp & 1) << 30);
+        }
+        stab[k] = code;
+    }
+
     const T* wtab = tb.wtab + bd.wtab_off;
     const T cc = tb.cross_cg;
     // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
@@ -295,14 +310,28 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
     const int np = (int)((N - p0) < P ? (N - p0) : P);
-    // ---- inputs of the tile (rows past N read as zero), zeroed staging
-    for (int e = tid; e < P * n1; e += kThreads) {
-        const int p = e / n1, m = e - p * n1;
-        xs[e] = p < np ? x1[(p0 + p) * nin + j1 * j1 + m] : (T)0;
-    }
-    for (int e = tid; e < P * n2; e += kThreads) {
-        const int p = e / n2, m = e - p * n2;
-        xs[P * n1 + e] = p < np ? x2[(p0 + p) * nin + j2 * j2 + m] : (T)0;
+    // ---- ring-independent lifted coefficients of the tile (rows past N are zero):
+    //   series pair 0: (x_m, C^{j, m}_{j, m, 1, 0} x_m)            scalar and q = 0
+    //   series pair 1: (C^{j,m-1}_{j,m,1,-1} x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1})   q = -1, +1
+    // for orbital order m; scalar blocks use (x_m, 0) only.
+    for (int e = tid; e < P * (n1 + n2); e += kThreads) {
+        const int p = e / (n1 + n2), q = e - p * (n1 + n2);
+        const bool first = q < n1;
+        const int j = first ? j1 : j2, nj = 2 * j + 1, mj = first ? q : q - n1;   // mj = m + j
+        const T* xg = first ? x1 : x2;
+        const int64_t row = (p0 + p) * nin + j * j;
+        const bool ok = p < np;
+        const T xm = ok ? xg[row + mj] : (T)0;
+        const T* lcj = first ? lc : lc + 3 * n1;
+        C* dst = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1);
+        if (!cross) {
+            dst[mj] = cmk<C>(xm, (T)0);
+        } else {
+            const T xlo = (ok && mj >= 1) ? xg[row + mj - 1] : (T)0;
+            const T xhi = (ok && mj + 1 < nj) ? xg[row + mj + 1] : (T)0;
+            dst[mj] = cmk<C>(xm, lcj[nj + mj] * xm);
+            dst[nj + mj] = cmk<C>(lcj[mj] * xlo, lcj[2 * nj + mj] * xhi);
+        }
     }
     for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
 
@@ -326,33 +355,21 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const bool first = cross ? (s < 2) : (s == 0);
                 const int j = first ? j1 : j2;
                 const int nj = 2 * j + 1;
-                const T* xv = first ? xs + p * n1 : xs + P * n1 + p * n2;
-                const T* lcj = first ? lc : lc + 3 * n1;
+                const C* cv = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1) + (cross ? (s & 1) * nj : 0) + j;
                 const T* pr = pst + (rg0 + r) * npr + (first ? 0 : j1 + 1);
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {
                     const int n = t + A * n2i;
                     const int m = n <= j ? n : n - Phi;
-                    T re = 0, im = 0;
+                    C val = cmk<C>((T)0, (T)0);
                     if (n <= j || n >= Phi - j) {
                         const int am = m < 0 ? -m : m;
-                        T pv = pr[am];
-                        if (m < 0 && (am & 1)) pv = -pv;
-                        const T xp = xv[m + j] * pv;
-                        if (!cross) {
-                            re = xp;
-                        } else if ((s & 1) == 0) {
-                            // scalar lift (real part) and the q = 0 vector lift (imaginary part)
-                            re = xp;
-                            im = lcj[nj + m + j] * xp;
-                        } else {
-                            // q = -1 (real part) and q = +1 (imaginary part) vector lifts
-                            if (m - 1 >= -j) re = lcj[m + j] * xv[m - 1 + j] * pv;
-                            if (m + 1 <= j) im = lcj[2 * nj + m + j] * xv[m + 1 + j] * pv;
-                        }
+                        const T pv = (m < 0 && (am & 1)) ? -pr[am] : pr[am];
+                        const C c = cv[m];
+                        val = cmk<C>(c.x * pv, c.y * pv);
                     }
-                    v[n2i] = cmk<C>(re, im);
+                    v[n2i] = val;
                 }
                 Dft<B, true, C>::run(v);
                 C* row = fbuf + (size_t)rp * ly.per_rp + (size_t)s * FS + t * BP;
@@ -456,22 +473,19 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = yb[t * BP];
                 Dft<A, false, C>::run(u);
-                T* st = stage + (size_t)r * sc * sm;
+                T* st = stage + (size_t)r * sc * sm + (size_t)p * sm;
 #pragma unroll
                 for (int k1 = 0; k1 < A; ++k1) {
-                    const int k = k2 + B * k1;
-                    int mp, sg;
-                    if (k <= J) { mp = k; sg = 0; }
-                    else if (k >= Phi - J) { mp = Phi - k; sg = 1; }
-                    else continue;
-                    const T flip = (sg && (mp & 1)) ? (T)-1 : (T)1;   // P^{-m} = (-1)^m P^m
-                    const int cbase = sg * ncomp * P;
+                    const int code = stab[k2 + B * k1];
+                    if (code < 0) continue;
+                    const int off = code & 0x3fffffff;
+                    const T flip = (code >> 30) ? (T)-1 : (T)1;
                     if (!cross) {
-                        st[(cbase + p) * sm + mp] = u[k1].x * sc_s * flip;
+                        st[off] = u[k1].x * sc_s * flip;
                     } else {
                         const int c0 = 2 * z, c1 = 2 * z + 1;
-                        st[(cbase + c0 * P + p) * sm + mp] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
-                        st[(cbase + c1 * P + p) * sm + mp] = u[k1].y * sc_v * flip;
+                        st[c0 * P * sm + off] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
+                        st[c1 * P * sm + off] = u[k1].y * sc_v * flip;
                     }
                 }
             }
@@ -530,28 +544,22 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         }
     }
     __syncthreads();
+    // output o of the block: (w0, w1, w2, idx); idx < 0 marks a scalar-scalar
+    // path whose accumulator entry is -idx - 1, else e = idx - 1 is the entry of
+    // (j3 - 1, m3) and the q = -1, 0, +1 terms sit at e + 1, e, e - 1 of
+    // components 2, 1, 3 (out-of-range terms carry zero weight)
     const int nblk = n1 * n2;
-    for (int e = tid; e < np * nblk; e += kThreads) {
-        const int p = e / nblk, o = e - p * nblk;
-        int j3 = (int)sqrtf((float)(o + d * d));
-        while (j3 * j3 - d * d > o) --j3;
-        while ((j3 + 1) * (j3 + 1) - d * d <= o) ++j3;
-        const int m3 = o - (j3 * j3 - d * d) - j3;
-        const T* cf = coef + 3 * o;
+    for (int p = 0; p < np; ++p) {
         const T* bp = bbuf + (size_t)p * ncomp * nel;
-        T z;
-        if (((J + j3) & 1) == 0) {
-            z = cf[0] * bp[acc_rowoff((j3 - d) / 2, d) + j3 + m3];
-        } else {
-            const int l3 = j3 - 1;
-            const int roff = acc_rowoff((l3 - d) / 2, d) + l3;
-            z = 0;
-            // components: 1 -> q = 0, 2 -> q = -1, 3 -> q = +1
-            if (m3 + 1 <= l3) z += cf[0] * bp[2 * nel + roff + m3 + 1];
-            if (m3 >= -l3 && m3 <= l3) z += cf[1] * bp[1 * nel + roff + m3];
-            if (m3 - 1 >= -l3) z += cf[2] * bp[3 * nel + roff + m3 - 1];
+        T* op = out + (p0 + p) * nout + bd.out_off;
+        for (int o = tid; o < nblk; o += kThreads) {
+            const Coef4 cf = coef4[o];
+            const int idx = (int)cf.w;
+            T z;
+            if (idx < 0) z = cf.x * bp[-idx - 1];
+            else z = cf.x * bp[2 * nel + idx] + cf.y * bp[nel + idx - 1] + cf.z * bp[3 * nel + idx - 2];
+            op[o] = z;
         }
-        out[(p0 + p) * nout + bd.out_off + o] = z;
     }
     __syncthreads();
     }   // pair tiles

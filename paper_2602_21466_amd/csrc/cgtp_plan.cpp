@@ -255,6 +255,9 @@ int64_t path_offset(int L, int l1, int l2, int l3) {
            (int64_t)(l1 - l2) * (l1 - l2);
 }
 
+// Offset of row n (l3 = d + 2n) in a block's Legendre accumulator.
+inline int acc_rowoff_h(int n, int d) { return 2 * n * n + (2 * d - 1) * n; }
+
 // Rows l3 = d, d+2, ..., J of a block's Legendre accumulator; entries per component.
 inline int acc_entries(int d, int J) {
     const int nrows = (J - d) / 2 + 1;
@@ -335,7 +338,8 @@ int lds_for(const BlockDesc& b, int pairs) {
     o = align16h(o + sz * 3 * (n1 + n2));
     o = align16h(o + sz * b.R * (b.j1 + 1 + b.j2 + 1));
     o = align16h(o + csz * FS);
-    o = align16h(o + sz * pairs * (n1 + n2));
+    o = align16h(o + 4 * b.A * b.B);
+    o = align16h(o + csz * pairs * 2 * (n1 + n2));
     const int stage = o;
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
     o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
@@ -428,8 +432,9 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.pbar_stride = grid_stride[nt];
             b.wtab_off = grid_wtab_off[nt];
             b.lmax = grid_lmax[nt];
-            // output coefficients: 1/K for scalar-scalar paths; for cross paths the
-            // recombination weights C^{j3 m3}_{j3-1, m3-q, 1, q} (q = -1, 0, +1) times 1/K
+            // per output (j3, m3): (w0, w1, w2, idx) with 1/K folded in.  Scalar-scalar
+            // paths: w0 = 1/K and idx = -(accumulator entry) - 1.  Cross paths:
+            // w_{q+1} = C^{j3 m3}_{j3-1, m3-q, 1, q} / K and idx = 1 + the entry of (j3 - 1, m3).
             b.coef_off = (int)h.coef.size();
             for (int j3 = b.d; j3 <= b.J; ++j3) {
                 long double K;
@@ -441,11 +446,16 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                 const long double kinv = 1.0L / K;
                 for (int m3 = -j3; m3 <= j3; ++m3) {
                     if (kind == cgtp::kSS) {
+                        const int e = acc_rowoff_h((j3 - b.d) / 2, b.d) + j3 + m3;
                         h.coef.push_back((T)kinv);
                         h.coef.push_back((T)0);
                         h.coef.push_back((T)0);
+                        h.coef.push_back((T)(-e - 1));
                     } else {
-                        for (int q = -1; q <= 1; ++q) h.coef.push_back((T)(kinv * cg_vec(j3 - 1, m3 - q, q, j3, m3)));
+                        const int l3 = j3 - 1;
+                        for (int q = -1; q <= 1; ++q) h.coef.push_back((T)(kinv * cg_vec(l3, m3 - q, q, j3, m3)));
+                        // shifted by one: the q = 0 source of m3 = -(l3 + 1) sits at -1
+                        h.coef.push_back((T)(acc_rowoff_h((l3 - b.d) / 2, b.d) + l3 + m3 + 1));
                     }
                 }
             }
