@@ -8,6 +8,7 @@ N = 8192 is reported beside it.  Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -21,6 +22,27 @@ METRIC = "full-CGTP pairs/sec at L=16 and L=32 + % of HBM/MFMA roofline"
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (and dense fp32 MFMA) peak
 PEAK_FP64_TFLOPS = 78.6
 PEAK_HBM_GBS = 8000.0
+
+
+# HBM traffic of the block kernel from rocprofv3 counter runs (FETCH_SIZE and
+# WRITE_SIZE, KiB per dispatch, median over dispatches), each scaled by the
+# ratio of known bytes to the same counter over a plain device copy
+# (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
+# change, the figures no longer describe the kernel and traffic is null.
+MEASURED_TRAFFIC = {
+    "326a3125df9bb819": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 256478.8, "fetch_scale": 1.999956, "write_kib": 4774018.1, "write_scale": 1.0},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 197578.0, "fetch_scale": 1.999956, "write_kib": 2739429.2, "write_scale": 1.0},
+    },
+}
+
+
+def kernel_digest():
+    h = hashlib.sha256()
+    for name in ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h"):
+        with open(os.path.join(ROOT, "paper_2602_21466_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def log(msg):
@@ -76,11 +98,37 @@ def roofline(res):
     t = res["avg_launch_ms"] / 1e3
     achieved = flops / t / 1e12
     peak = PEAK_FP32_TFLOPS if res["dtype"] == "fp32" else PEAK_FP64_TFLOPS
-    hbm = res["plan"]["bytes_per_pair"] * res["N"] / t / 1e9
+    compulsory = res["plan"]["bytes_per_pair"] * res["N"]
+    hbm = compulsory / t / 1e9
+    m = MEASURED_TRAFFIC.get(kernel_digest(), {}).get(res["workload"])
+    traffic = None
+    if m is not None:
+        traffic = int(m["fetch_kib"] * 1024 * m["fetch_scale"] + m["write_kib"] * 1024 * m["write_scale"])
     return {"bound": "alu", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
-            "flops_per_launch": flops, "hbm_gbs_compulsory": round(hbm, 1),
-            "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4)}
+            "frac": round(achieved / peak, 4), "traffic": traffic,
+            "flops_per_launch": flops, "compulsory_bytes_per_launch": int(compulsory),
+            "hbm_gbs_compulsory": round(hbm, 1), "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4),
+            "avg_launch_ms": round(res["avg_launch_ms"], 4), "kernel_digest": kernel_digest()}
+
+
+def copy_probe(nbytes, reps=10):
+    """Plain device-to-device copy of nbytes: the calibration for the HBM counters."""
+    import torch
+
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    print(json.dumps({"copy_probe_bytes": nbytes, "read_kib": nbytes / 1024, "write_kib": nbytes / 1024,
+                      "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}), flush=True)
 
 
 def cpu_baseline(w, budget_s):
@@ -116,6 +164,8 @@ def main():
     ap.add_argument("--secondary", default="cgtp_L16_N8192_fp32")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only; --gpus %d is not supported "
@@ -128,6 +178,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     by_name = {w.name: w for w in cgtp_inputs.WORKLOADS}
     w = by_name[args.workload]
     log("timing %s: %d warmup, %d steps" % (w.name, args.warmup, args.steps))
