@@ -53,8 +53,12 @@ enum cgtp_cover {
        projected on the l3 - 1 vector harmonics (Section 5.1). */
     CGTP_COVER_DEFAULT = 0,
     /* even: dot product of the toroidal lifts; odd: scalar x1 times toroidal
-       x2.  Paths whose dot-product factor vanishes by accident, or that have a
-       degree-0 input, fall back to the scalar-scalar product. */
+       x2.  Blocks (l1, l2) with a degree-0 input use the scalar-scalar
+       product.  A block in which the dot-product factor of some even path
+       vanishes by accident (l1(l1+1) + l2(l2+1) = l3(l3+1), e.g. (3, 5, 6))
+       uses the scalar-scalar product for all its even paths; likewise the
+       cross product for its odd paths if a scalar-vector factor vanishes.
+       Same result as the default cover up to rounding. */
     CGTP_COVER_ALTERNATE = 1
 };
 
@@ -122,7 +126,8 @@ int64_t cgtp_path_offset(int32_t L, int32_t l1, int32_t l2, int32_t l3);
  * the recovered paths, the algorithmic flops per pair of the method (every
  * block on its minimal exact grid: lifts, longitude transforms at
  * 2.5 n log2 n flops per Hermitian transform of n points, pointwise products,
- * Legendre projection, recombination), and the compulsory HBM bytes per pair
+ * Legendre projection, recombination; the default cover's products whatever
+ * the plan's cover), and the compulsory HBM bytes per pair
  * (inputs read once, output written once).  Any pointer may be NULL.
  */
 int cgtp_plan_query(cgtp_plan_t plan, int32_t *n_theta, int32_t *n_phi, double *min_abs_K,
@@ -140,7 +145,8 @@ int cgtp_last_hip_error(void);
  * Per-path normalisation K of Theorem 4.2 for the product the given cover uses
  * on path (j1, j2, j3): raw projection = K * z.  *kind receives 0 for the
  * scalar-scalar product, 1 for the cross product, 2 for scalar-vector, 3 for
- * the dot product.  Returns CGTP_EINVAL if (j1, j2, j3) violates the triangle
+ * the dot product (the alternate cover's fall-backs are per block, as
+ * described at CGTP_COVER_ALTERNATE).  Returns CGTP_EINVAL if (j1, j2, j3) violates the triangle
  * rule or any degree is negative.
  */
 int cgtp_path_norm(int32_t j1, int32_t j2, int32_t j3, int32_t cover, double *K, int32_t *kind);

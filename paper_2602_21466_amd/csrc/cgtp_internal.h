@@ -25,7 +25,14 @@ enum PathKind : int32_t { kSS = 0, kCross = 1, kSV = 2, kDot = 3 };
 // Which lifts and products a block needs.
 enum BlockKind : int32_t {
     kBlockScalar = 0,   // only scalar-scalar paths (a degree-0 input)
-    kBlockCross = 1,    // scalar-scalar (even paths) + cross (odd paths)
+    kBlockCross = 1,    // scalar and toroidal lifts of both inputs; four projected components
+};
+
+// Products of a kBlockCross block (BlockDesc::products); zero bits give the
+// default cover's scalar-scalar (even paths) and cross (odd paths) products.
+enum BlockProducts : int32_t {
+    kEvenDot = 1,   // even paths: dot product of the toroidal lifts
+    kOddSV = 2,     // odd paths: scalar lift of x1 times toroidal lift of x2
 };
 
 // One (j1, j2) block: one irrep-signal tensor product on its own grid.
@@ -56,7 +63,7 @@ struct alignas(16) BlockDesc {
     int32_t lg_pairs;          // log2(pairs)
     int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
     int32_t sc;                // staged columns: 2 ncomp pairs rounded up to 16
-    int32_t pad0;
+    int32_t products;          // BlockProducts bits
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
@@ -82,6 +89,7 @@ struct Tables {
     const T* coef;      // per block and output (j3, m3): recombination weights times 1/K, and the source index
     const TileDesc* tdesc;
     T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
+    T dot_cg;           // C^{0,0}_{1,1,1,-1}: the dot product's coupling constant
     const BlockDesc* blocks;
 };
 

@@ -301,11 +301,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     }
 
     const T* wtab = tb.wtab + bd.wtab_off;
-    const T cc = tb.cross_cg;
+    const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
     // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
     // unpacking two packed signals, and the cross product's coupling constant
     const T sc_s = (T)(6.283185307179586476925286766559 / Phi) * (cross ? (T)0.25 : (T)1);
-    const T sc_v = sc_s * cc;
+    // component 0 (even paths): scalar-scalar, or the dot product's coupling
+    // constant; components 1..3 (odd paths): the cross product's, or none for
+    // scalar-vector
+    const T sc_v = sc_s * (odd_sv ? (T)1 : tb.cross_cg);
+    const T sc_e = sc_s * (even_dot ? tb.dot_cg : (T)1);
 
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
@@ -420,11 +424,23 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     }
                     const C as = f[0], a0 = f[1], am = f[2], ap = f[3];
                     const C bs = f[4], b0 = f[5], bm = f[6], bp = f[7];
-                    const C gs = cmul(as, bs);
-                    // antisymmetric 1 (x) 1 -> 1 coupling, constant applied at staging
-                    const C gp = csub(cmul(ap, b0), cmul(a0, bp));
-                    const C g0 = csub(cmul(ap, bm), cmul(am, bp));
-                    const C gm = csub(cmul(a0, bm), cmul(am, b0));
+                    C gs, gp, g0, gm;
+                    if (even_dot) {
+                        // C^{0 0}_{1 q 1 -q} is c (+1, -1, +1) for q = 1, 0, -1; c applied at staging
+                        gs = cadd(csub(cmul(ap, bm), cmul(a0, b0)), cmul(am, bp));
+                    } else {
+                        gs = cmul(as, bs);
+                    }
+                    if (odd_sv) {
+                        gp = cmul(as, bp);
+                        g0 = cmul(as, b0);
+                        gm = cmul(as, bm);
+                    } else {
+                        // antisymmetric 1 (x) 1 -> 1 coupling, constant applied at staging
+                        gp = csub(cmul(ap, b0), cmul(a0, bp));
+                        g0 = csub(cmul(ap, bm), cmul(am, bp));
+                        gm = csub(cmul(a0, bm), cmul(am, b0));
+                    }
                     // z1 = gs + i g0, z2 = g-1 + i g+1; at -n the conjugated signals
                     C* z1 = fb + 2 * FS;
                     C* z2 = fb + 3 * FS;
@@ -484,7 +500,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                         st[off] = u[k1].x * sc_s * flip;
                     } else {
                         const int c0 = 2 * z, c1 = 2 * z + 1;
-                        st[c0 * P * sm + off] = u[k1].x * (c0 == 0 ? sc_s : sc_v) * flip;
+                        st[c0 * P * sm + off] = u[k1].x * (c0 == 0 ? sc_e : sc_v) * flip;
                         st[c1 * P * sm + off] = u[k1].y * sc_v * flip;
                     }
                 }

@@ -135,17 +135,40 @@ long double gen_gaunt_K(int j1, int l1, int s1, int j2, int l2, int s2, int j3, 
 constexpr long double kMinAbsK = 1e-3L;
 
 // Chooses the product for path (j1, j2, j3) and returns its K.
+// Products the alternate cover uses in block (j1, j2), both inputs of degree
+// >= 1: the dot product for even paths unless its factor vanishes by accident
+// on one of the block's even paths, and scalar x1 times toroidal x2 for odd
+// paths unless its factor vanishes on one of the odd paths.  A block that falls
+// back uses the default product for all paths of that parity, so every block
+// needs one product per parity.
+void alt_block_products(int j1, int j2, bool* even_dot, bool* odd_sv) {
+    *even_dot = true;
+    *odd_sv = true;
+    for (int j3 = std::abs(j1 - j2); j3 <= j1 + j2; ++j3) {
+        if (((j1 + j2 + j3) & 1) == 0) {
+            if (fabsl(gen_gaunt_K(j1, j1, 1, j2, j2, 1, j3, j3, 0)) < kMinAbsK) *even_dot = false;
+        } else {
+            if (fabsl(gen_gaunt_K(j1, j1, 0, j2, j2, 1, j3, j3 - 1, 1)) < kMinAbsK) *odd_sv = false;
+        }
+    }
+}
+
 int path_norm(int j1, int j2, int j3, int cover, long double* K, int* kind) {
     if (!triangle(j1, j2, j3)) return CGTP_EINVAL;
     const bool even = ((j1 + j2 + j3) & 1) == 0;
     const bool vec_ok = j1 > 0 && j2 > 0;  // a degree-0 input has no toroidal lift
     if (cover == CGTP_COVER_ALTERNATE && vec_ok) {
-        if (even) {
-            long double k = gen_gaunt_K(j1, j1, 1, j2, j2, 1, j3, j3, 0);
-            if (fabsl(k) >= kMinAbsK) { *K = k; *kind = cgtp::kDot; return CGTP_OK; }
-        } else {
-            long double k = gen_gaunt_K(j1, j1, 0, j2, j2, 1, j3, j3 - 1, 1);
-            if (fabsl(k) >= kMinAbsK) { *K = k; *kind = cgtp::kSV; return CGTP_OK; }
+        bool even_dot, odd_sv;
+        alt_block_products(j1, j2, &even_dot, &odd_sv);
+        if (even && even_dot) {
+            *K = gen_gaunt_K(j1, j1, 1, j2, j2, 1, j3, j3, 0);
+            *kind = cgtp::kDot;
+            return CGTP_OK;
+        }
+        if (!even && odd_sv) {
+            *K = gen_gaunt_K(j1, j1, 0, j2, j2, 1, j3, j3 - 1, 1);
+            *kind = cgtp::kSV;
+            return CGTP_OK;
         }
     }
     if (even) {
@@ -302,7 +325,7 @@ struct cgtp_plan_s {
     int lds_bytes = 0;
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
-    double cross_cg = 0;
+    double cross_cg = 0, dot_cg = 0;
 };
 
 namespace {
@@ -414,6 +437,11 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             if (fabsl(cg_vec(1, q1, q2, 1, q1 + q2) - want) > 1e-15L) return CGTP_EINVAL;
         }
     p->cross_cg = (double)c;
+    // the dot product as d * (a+ b- - a0 b0 + a- b+) with d = C^{0,0}_{1,1,1,-1}
+    const long double dc = cg_vec(1, 1, -1, 0, 0);
+    for (int q = -1; q <= 1; ++q)
+        if (fabsl(cg_vec(1, q, -q, 0, 0) - (q == 0 ? -dc : dc)) > 1e-15L) return CGTP_EINVAL;
+    p->dot_cg = (double)dc;
     // ---- blocks
     double min_abs_K = 1e300, flops = 0;
     blocks.clear();
@@ -426,6 +454,12 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.R = nt / 2;
             b.Phi = np;
             b.kind = (j1 > 0 && j2 > 0) ? cgtp::kBlockCross : cgtp::kBlockScalar;
+            b.products = 0;
+            if (b.kind == cgtp::kBlockCross && g.cover == CGTP_COVER_ALTERNATE) {
+                bool even_dot, odd_sv;
+                alt_block_products(j1, j2, &even_dot, &odd_sv);
+                b.products = (even_dot ? cgtp::kEvenDot : 0) | (odd_sv ? cgtp::kOddSV : 0);
+            }
             if (!cgtp::fft_factors(np, &b.A, &b.B)) return CGTP_EUNSUP;
             b.tw_off = phi_set[np];
             b.pbar_off = grid_pbar_off[nt];
@@ -439,13 +473,15 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             for (int j3 = b.d; j3 <= b.J; ++j3) {
                 long double K;
                 int kind;
-                if (path_norm(j1, j2, j3, CGTP_COVER_DEFAULT, &K, &kind) != CGTP_OK) return CGTP_EINVAL;
-                const int want = ((b.J + j3) & 1) ? cgtp::kCross : cgtp::kSS;
+                if (path_norm(j1, j2, j3, g.cover, &K, &kind) != CGTP_OK) return CGTP_EINVAL;
+                const bool odd = (b.J + j3) & 1;
+                const int want = odd ? ((b.products & cgtp::kOddSV) ? cgtp::kSV : cgtp::kCross)
+                                     : ((b.products & cgtp::kEvenDot) ? cgtp::kDot : cgtp::kSS);
                 if (kind != want || fabsl(K) < kMinAbsK) return CGTP_EUNSUP;
                 min_abs_K = std::min(min_abs_K, (double)fabsl(K));
                 const long double kinv = 1.0L / K;
                 for (int m3 = -j3; m3 <= j3; ++m3) {
-                    if (kind == cgtp::kSS) {
+                    if (!odd) {
                         const int e = acc_rowoff_h((j3 - b.d) / 2, b.d) + j3 + m3;
                         h.coef.push_back((T)kinv);
                         h.coef.push_back((T)0);
@@ -564,6 +600,7 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->lcg = (const T*)(base + offs[3]);
     tb->coef = (const T*)(base + offs[4]);
     tb->cross_cg = (T)p->cross_cg;
+    tb->dot_cg = (T)p->dot_cg;
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
@@ -666,7 +703,6 @@ int cgtp_plan(int32_t L, const cgtp_grid* grid, cgtp_plan_t* plan_out) {
     cgtp_grid g = grid ? *grid : cgtp_grid{0, 0, CGTP_FP32, CGTP_COVER_DEFAULT};
     int rc = check_grid(L, &g);
     if (rc != CGTP_OK) return rc;
-    if (g.cover != CGTP_COVER_DEFAULT) return CGTP_EUNSUP;
     cgtp_plan_s* p = new (std::nothrow) cgtp_plan_s();
     if (!p) return CGTP_ENOMEM;
     p->L = L;

@@ -140,6 +140,21 @@ def test_small_parity(L, N, dtype):
     check_against_oracle(L, x1, x2, out.double().cpu().numpy(), dtype)
 
 
+@pytest.mark.parametrize("L,N,dtype", [(2, 17, "fp64"), (5, 33, "fp64"), (6, 300, "fp32"), (12, 19, "fp32")])
+def test_alternate_cover_parity(L, N, dtype):
+    """Dot and scalar-vector products (with the per-block fall-backs; L >= 5 holds block
+    (3, 5)) reach the same CGTP as the oracle, and agree with the default cover."""
+    _torch()
+    x1, x2 = wl.draw(L, N, dtype, seed=1000 + L)
+    _, _, _, out_alt = run_gpu(L, x1, x2, dtype, cover=1)
+    alt = out_alt.double().cpu().numpy()
+    check_against_oracle(L, x1, x2, alt, dtype)
+    _, _, _, out_dflt = run_gpu(L, x1, x2, dtype)
+    err, path = per_path_rel_err(L, alt, out_dflt.double().cpu().numpy())
+    print("alternate vs default cover: worst per-path rel L2 %.3e at %s" % (err, path), flush=True)
+    assert err <= 2 * TOL[dtype], (err, path)
+
+
 def test_zero_pairs_launches_nothing():
     torch = _torch()
     lib = _lib()

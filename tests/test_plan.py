@@ -198,13 +198,27 @@ def test_alternate_cover_falls_back_on_accidental_zeros():
     assert kind == 2
 
 
-def test_block_grid_is_minimal_exact():
-    for L in (2, 16, 32):
-        for j1, j2 in [(0, 0), (L, L), (1, L), (L // 2, L // 3)]:
-            nt, nph = lib.cgtp_block_grid(L, j1, j2)
-            J = j1 + j2
-            assert nt % 2 == 0 and 2 * nt - 1 >= 2 * J and 2 * (nt - 2) - 1 < 2 * J
-            assert nph >= 2 * J + 1
+def test_alternate_cover_fall_back_is_per_block():
+    """Each block uses one product per parity: blocks holding an exact zero of the dot factor
+    (j1(j1+1) + j2(j2+1) = j3(j3+1), even sum) fall back to scalar-scalar for all their even
+    paths, the others use the dot product throughout; odd paths use scalar-vector."""
+    for j3 in range(2, 9):
+        K, kind = lib.cgtp_path_norm(3, 5, j3, 1)
+        assert kind == (0 if j3 % 2 == 0 else 2)
+    zeros = {(a, b, c) for a in range(1, 33) for b in range(1, 33) for c in range(abs(a - b), a + b + 1)
+             if (a + b + c) % 2 == 0 and a * (a + 1) + b * (b + 1) == c * (c + 1)}
+    assert (3, 5, 6) in zeros and (5, 3, 6) in zeros
+    for a in range(1, 33):
+        for b in range(1, 33):
+            even_kinds, odd_kinds = set(), set()
+            for c in range(abs(a - b), a + b + 1):
+                K, kind = lib.cgtp_path_norm(a, b, c, 1)
+                (even_kinds if (a + b + c) % 2 == 0 else odd_kinds).add(kind)
+                assert abs(K) >= 1e-3
+            assert len(even_kinds) == 1 and even_kinds <= {0, 3}
+            if any((a, b, c) in zeros for c in range(abs(a - b), a + b + 1)):
+                assert even_kinds == {0}
+            assert odd_kinds <= {2}               # no scalar-vector zero up to L = 32
 
 
 @pytest.mark.parametrize("L", [0, 1, 2, 4])
@@ -213,6 +227,14 @@ def test_method_model_matches_oracle(L, cover, rng):
     x1 = rng.standard_normal((3, (L + 1) ** 2))
     x2 = rng.standard_normal((3, (L + 1) ** 2))
     np.testing.assert_allclose(model_cgtp(L, x1, x2, cover), oracle.cgtp(L, x1, x2), atol=1e-12)
+
+
+def test_method_model_alternate_cover_with_fall_back_block(rng):
+    """L = 5 holds block (3, 5), whose even paths fall back to scalar-scalar."""
+    L = 5
+    x1 = rng.standard_normal((2, (L + 1) ** 2))
+    x2 = rng.standard_normal((2, (L + 1) ** 2))
+    np.testing.assert_allclose(model_cgtp(L, x1, x2, 1), oracle.cgtp(L, x1, x2), atol=1e-12)
 
 
 def test_method_model_on_a_global_grid(rng):
