@@ -56,7 +56,7 @@ struct alignas(16) BlockDesc {
     int32_t tw_off;            // offset of the Phi-point twiddle table (complex entries)
     int32_t pbar_off;          // offset of the grid's Legendre table (elements)
     int32_t pbar_stride;       // Legendre entries per ring: (lmax+1)(lmax+2)/2
-    int32_t wtab_off;          // offset of the grid's MFMA weight table (elements)
+    int32_t wtab_off;          // offset of the MFMA weights of the grid, parity of J (elements)
     int32_t lmax;              // largest degree of the grid's tables
     int32_t coef_off;          // offset of the block's output coefficients (4 per output)
     int32_t tdesc_off;         // offset of the block's MFMA tile descriptors
@@ -64,13 +64,18 @@ struct alignas(16) BlockDesc {
     int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
     int32_t sc;                // staged columns: 2 ncomp pairs rounded up to 16
     int32_t products;          // BlockProducts bits
+    int32_t rpad;              // rings of the weight table: R rounded up to the ring group
+    int32_t wrow;              // entries per ring row of the weight table
+    int32_t pad1;
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
 // One 16x16 accumulator tile of the Legendre projection, in the order the
 // waves take them (wave w owns tiles w, w + 4, ...).
-//   a_off: weight-table offset of (|m|, ring 0, first row l3_0) within the grid's table
-//   rs_nv: ring stride of the weight table | (valid rows of the tile << 16)
+//   a_off: offset of (|m|, ring 0, first row l3_0) in the block's weight table
+//          ([|m|][ring][row], wrow rows per ring; rows past the tile's last
+//          valid one are read but their results are discarded)
+//   rs_nv: valid rows of the tile << 16
 //   b_off: staged-spectrum offset of (ring 0, first column, |m|)
 //   code:  |m| << 16 | row tile << 8 | column tile
 struct alignas(16) TileDesc {
@@ -90,6 +95,7 @@ struct Tables {
     const TileDesc* tdesc;
     T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
     T dot_cg;           // C^{0,0}_{1,1,1,-1}: the dot product's coupling constant
+    int32_t wtab_len;   // elements of wtab
     const BlockDesc* blocks;
 };
 

@@ -159,6 +159,19 @@ template <bool INV, typename C> struct Dft<9, INV, C> { __device__ static void r
 template <bool INV, typename C> struct Dft<12, INV, C> { __device__ static void run(C* x) { dft_ct<4, 3, INV>(x); } };
 template <bool INV, typename C> struct Dft<16, INV, C> { __device__ static void run(C* x) { dft_ct<4, 4, INV>(x); } };
 
+// ---------------------------------------------------------------- buffer loads
+
+// Fourth dword of a raw buffer resource on gfx9-family GPUs (32-bit data format).
+constexpr int kBufferFlags = 0x00020000;
+
+template <typename T> __device__ __forceinline__ T buffer_load(__amdgpu_buffer_rsrc_t r, int voff, int soff);
+template <> __device__ __forceinline__ float buffer_load<float>(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+template <> __device__ __forceinline__ double buffer_load<double>(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+
 // ---------------------------------------------------------------- MFMA
 
 __device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c) {
@@ -202,7 +215,7 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // spectra are [ring][column][|m|] with an odd |m| stride for the same reason.
 
 struct Layout {
-    int lc, pst, tw2, stab, lc2, stage, fbuf, bbuf;   // byte offsets
+    int lc, pst, tw2, stab, tdl, lc2, stage, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
 };
 
@@ -222,6 +235,7 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.stab = o; o = align16(o + 4 * A * B);
+    l.tdl = o; o = align16(o + 8 * b.ntiles);
     l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
     l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
     l.per_rp = nslot * FS;
@@ -266,6 +280,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     int* stab = reinterpret_cast<int*>(smem + ly.stab);  // longitude k -> staged offset | sign, or -1
+    int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
     C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
@@ -288,6 +303,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
     }
 
+    for (int u = tid; u < bd.ntiles; u += kThreads) {
+        const TileDesc t = td[u];
+        tdl[u] = make_int2(t.a_off * (int)sizeof(T), t.b_off * (int)sizeof(T));
+    }
+
     // staging map: orders |m| <= J of the analysis spectrum, with the sign of
     // P^{-m} = (-1)^m P^m folded in for negative m
     for (int k = tid; k < Phi; k += kThreads) {
@@ -300,7 +320,12 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         stab[k] = code;
     }
 
-    const T* wtab = tb.wtab + bd.wtab_off;
+    // MFMA operands: the block's weight table as a buffer resource (reads past it
+    // return zero), and this lane's byte offsets of row / column i, ring kq
+    const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
+    const int lane_a = ((lane >> 4) * bd.wrow + (lane & 15)) * (int)sizeof(T);
+    const int lane_b = ((lane >> 4) * sc * sm + (lane & 15) * sm) * (int)sizeof(T);
     const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
     // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
     // unpacking two packed signals, and the cross product's coupling constant
@@ -507,23 +532,23 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         __syncthreads();
-        // ---- 5. Legendre projection on MFMA, accumulated over ring groups
+        // ---- 5. Legendre projection on MFMA, accumulated over ring groups.  Lane
+        // (i, kq) feeds row i / column i of ring 4 h + kq: its weight sits at
+        // a_off + ring wrow + i of the block's table (a buffer load whose ring
+        // offset is scalar), its staged value at b_off + (ring, column i).
         {
-            const int i = lane & 15, kq = lane >> 4;
 #pragma unroll
             for (int h = 0; h < kRingGroup / 4; ++h) {
-                const int ring = rg0 + 4 * h + kq;
-                const T* stk = stage + (size_t)(4 * h + kq) * sc * sm + i * sm;
-                // descriptors and operands of all this wave's tiles first (branch-free,
-                // tile index clamped), so their latencies overlap; then the MFMAs
+                const int soff = (rg0 + 4 * h) * bd.wrow * (int)sizeof(T);
+                const int bofs = lane_b + h * 4 * sc * sm * (int)sizeof(T);
+                int2 dsc[MT];
+#pragma unroll
+                for (int s = 0; s < MT; ++s) dsc[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)];
                 T av[MT], bv[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) {
-                    const int u = min(wave + kWaves * s, bd.ntiles - 1);
-                    const TileDesc t = td[u];   // wave-uniform: scalar loads
-                    const bool ok = wave + kWaves * s < bd.ntiles && ring < R && i < (t.rs_nv >> 16);
-                    av[s] = ok ? wtab[t.a_off + ring * (t.rs_nv & 0xffff) + 2 * i] : (T)0;
-                    bv[s] = stk[t.b_off];
+                    av[s] = buffer_load<T>(wrsrc, dsc[s].x + lane_a, soff);
+                    bv[s] = *reinterpret_cast<const T*>(smem + ly.stage + bofs + dsc[s].y);
                 }
 #pragma unroll
                 for (int s = 0; s < MT; ++s)

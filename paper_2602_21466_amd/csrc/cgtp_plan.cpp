@@ -287,6 +287,11 @@ inline int acc_entries(int d, int J) {
     return nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
 }
 
+// MFMA weight table geometry: rings padded to whole ring groups; entries per
+// ring row (degrees l = par, par + 2, ..., <= lmax).
+inline int wtab_rpad(int R) { return (R + cgtp::kRingGroup - 1) / cgtp::kRingGroup * cgtp::kRingGroup; }
+inline int wtab_rowlen(int lmax, int par) { return lmax >= par ? (lmax - par) / 2 + 1 : 1; }
+
 // Algorithmic flops of one block on its minimal exact grid (default cover).
 double block_flops(int j1, int j2) {
     const int J = j1 + j2, d = std::abs(j1 - j2);
@@ -362,6 +367,7 @@ int lds_for(const BlockDesc& b, int pairs) {
     o = align16h(o + sz * b.R * (b.j1 + 1 + b.j2 + 1));
     o = align16h(o + csz * FS);
     o = align16h(o + 4 * b.A * b.B);
+    o = align16h(o + 8 * block_tiles(b, pairs));
     o = align16h(o + csz * pairs * 2 * (n1 + n2));
     const int stage = o;
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
@@ -387,6 +393,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             phi_set[np] = 0;
         }
     std::map<int, int> grid_pbar_off, grid_wtab_off, grid_stride;
+    std::map<int, std::array<int, 2>> grid_wtab_par;
     for (auto& kv : grid_lmax) {
         const int nt = kv.first, lmax = kv.second, R = nt / 2;
         std::vector<long double> x, w;
@@ -400,11 +407,24 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             legendre(lmax, x[i], rows.data() + (size_t)i * stride);
             for (int e = 0; e < stride; ++e) h.pbar.push_back((T)rows[(size_t)i * stride + e]);
         }
-        // MFMA weights: [m'][ring][l - m'] = 2 w_r P^{m'}_l(x_r) (north and south folded)
-        for (int mp = 0; mp <= lmax; ++mp)
-            for (int i = 0; i < R; ++i)
-                for (int l = mp; l <= lmax; ++l)
-                    h.wtab.push_back((T)(2.0L * w[i] * rows[(size_t)i * stride + l * (l + 1) / 2 + mp]));
+        // MFMA weights, per parity of l: [m'][ring][t] = 2 w_r P^{m'}_l(x_r) for
+        // l = par + 2t <= lmax (north and south folded; zero for l < m'), rings
+        // padded with zeros to whole ring groups, so a tile's 16 rows are
+        // contiguous; 16 zero entries close each parity.
+        const int rpad = wtab_rpad(R);
+        for (int par = 0; par < 2; ++par) {
+            const int rl = wtab_rowlen(lmax, par);
+            grid_wtab_par[nt][par] = (int)h.wtab.size() - grid_wtab_off[nt];
+            for (int mp = 0; mp <= lmax; ++mp)
+                for (int i = 0; i < rpad; ++i)
+                    for (int t = 0; t < rl; ++t) {
+                        const int l = par + 2 * t;
+                        h.wtab.push_back((i < R && l >= mp && l <= lmax)
+                                             ? (T)(2.0L * w[i] * rows[(size_t)i * stride + l * (l + 1) / 2 + mp])
+                                             : (T)0);
+                    }
+            h.wtab.insert(h.wtab.end(), (size_t)16, (T)0);
+        }
         p->max_theta = std::max(p->max_theta, nt);
     }
     for (auto& kv : phi_set) {
@@ -464,8 +484,10 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.tw_off = phi_set[np];
             b.pbar_off = grid_pbar_off[nt];
             b.pbar_stride = grid_stride[nt];
-            b.wtab_off = grid_wtab_off[nt];
             b.lmax = grid_lmax[nt];
+            b.rpad = wtab_rpad(b.R);
+            b.wrow = wtab_rowlen(b.lmax, b.J & 1);
+            b.wtab_off = grid_wtab_off[nt] + grid_wtab_par[nt][b.J & 1];
             // per output (j3, m3): (w0, w1, w2, idx) with 1/K folded in.  Scalar-scalar
             // paths: w0 = 1/K and idx = -(accumulator entry) - 1.  Cross paths:
             // w_{q+1} = C^{j3 m3}_{j3-1, m3-q, 1, q} / K and idx = 1 + the entry of (j3 - 1, m3).
@@ -522,10 +544,10 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                             const int row0 = geo.tmin(mp, b.d) + 16 * rt;
                             const int l30 = b.d + 2 * row0;
                             const int nv = std::min(16, geo.nrows - row0);
-                            const int moff = b.R * (mp * (b.lmax + 1) - mp * (mp - 1) / 2);
+                            const int par = b.J & 1;
                             cgtp::TileDesc t;
-                            t.a_off = moff + (l30 - mp);
-                            t.rs_nv = (b.lmax - mp + 1) | (nv << 16);
+                            t.a_off = mp * b.rpad * b.wrow + (l30 - par) / 2;
+                            t.rs_nv = nv << 16;
                             t.b_off = 16 * ct * b.sm + mp;
                             t.code = (mp << 16) | (rt << 8) | ct;
                             h.tdesc.push_back(t);
@@ -601,6 +623,7 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->coef = (const T*)(base + offs[4]);
     tb->cross_cg = (T)p->cross_cg;
     tb->dot_cg = (T)p->dot_cg;
+    tb->wtab_len = (int32_t)h.wtab.size();
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
