@@ -28,6 +28,12 @@ enum BlockKind : int32_t {
     kBlockCross = 1,    // scalar and toroidal lifts of both inputs; four projected components
 };
 
+// Where the Legendre projection reads the analysis spectra.
+enum BlockMode : int32_t {
+    kModeStaged = 0,   // staged as [ring][column][|m|] (any number of column tiles)
+    kModeGather = 1,   // in place in the transforms (one column tile: ncomp * pairs <= 8)
+};
+
 // Products of a kBlockCross block (BlockDesc::products); zero bits give the
 // default cover's scalar-scalar (even paths) and cross (odd paths) products.
 enum BlockProducts : int32_t {
@@ -66,7 +72,7 @@ struct alignas(16) BlockDesc {
     int32_t products;          // BlockProducts bits
     int32_t rpad;              // rings of the weight table: R rounded up to the ring group
     int32_t wrow;              // entries per ring row of the weight table
-    int32_t pad1;
+    int32_t mode;              // BlockMode: where the projection reads its spectra
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
@@ -76,7 +82,9 @@ struct alignas(16) BlockDesc {
 //          ([|m|][ring][row], wrow rows per ring; rows past the tile's last
 //          valid one are read but their results are discarded)
 //   rs_nv: valid rows of the tile << 16
-//   b_off: staged-spectrum offset of (ring 0, first column, |m|)
+//   b_off: staging mode: staged-spectrum offset of (ring 0, first column, |m|);
+//          gather mode: element offsets of longitudes +|m| (bits 0..15) and
+//          -|m| (bits 16..31) in a transform's pass layout
 //   code:  |m| << 16 | row tile << 8 | column tile
 struct alignas(16) TileDesc {
     int32_t a_off, rs_nv, b_off, code;

@@ -211,12 +211,17 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // A longitude transform lives in "pass layout": A rows of B + 1 complex
 // entries (one pad per row), element k = k2 + B k1 at k1 (B + 1) + k2.  The
 // first pass writes rows, the second reads and rewrites columns in place, and
-// the padding keeps both access patterns free of bank conflicts.  The staged
-// spectra are [ring][column][|m|] with an odd |m| stride for the same reason.
+// the padding keeps both access patterns free of bank conflicts.  Rings are
+// kRingSkew complex entries further apart than their transforms need, which
+// spreads the rings of one MFMA operand over the banks.  The staged spectra
+// (staging mode only) are [ring][column][|m|] with an odd |m| stride.
+
+constexpr int kRingSkew = 8;
 
 struct Layout {
-    int lc, pst, tw2, stab, tdl, lc2, stage, fbuf, bbuf;   // byte offsets
+    int lc, pst, tw2, stab, tdl, tdc, lc2, stage, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
+    int per_r;                                       // complex entries per ring
 };
 
 __device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
@@ -236,9 +241,12 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.stab = o; o = align16(o + 4 * A * B);
     l.tdl = o; o = align16(o + 8 * b.ntiles);
+    l.tdc = o; o = align16(o + 4 * b.ntiles);
     l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
-    l.stage = o; o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
+    l.stage = o;
+    if (b.mode == kModeStaged) o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
     l.per_rp = nslot * FS;
+    l.per_r = P * l.per_rp + kRingSkew;
     l.fbuf = o;
     l.bbuf = l.stage;
     return l;
@@ -281,10 +289,17 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     int* stab = reinterpret_cast<int*>(smem + ly.stab);  // longitude k -> staged offset | sign, or -1
     int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
+    int* tdc = reinterpret_cast<int*>(smem + ly.tdc);    // per MFMA tile: its code
+
     C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
     T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nel], end phase only
+    const bool gather = bd.mode == kModeGather;
+    // transforms of (ring, pair) rp = ring * P + pair
+    auto rpbuf = [&](int rp) -> C* {
+        return fbuf + (size_t)(rp >> lgP) * ly.per_r + (size_t)(rp & (P - 1)) * ly.per_rp;
+    };
     const TileDesc* __restrict__ td = tdesc + bd.tdesc_off;
     using Coef4 = typename Cplx<T>::acc4;
     const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef + bd.coef_off);
@@ -305,27 +320,39 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
         const TileDesc t = td[u];
-        tdl[u] = make_int2(t.a_off * (int)sizeof(T), t.b_off * (int)sizeof(T));
+        tdl[u] = make_int2(t.a_off * (int)sizeof(T), gather ? t.b_off : t.b_off * (int)sizeof(T));
+        tdc[u] = t.code;
     }
 
-    // staging map: orders |m| <= J of the analysis spectrum, with the sign of
-    // P^{-m} = (-1)^m P^m folded in for negative m
-    for (int k = tid; k < Phi; k += kThreads) {
-        int code = -1;
-        if (k <= J) code = k;
-        else if (k >= Phi - J) {
-            const int mp = Phi - k;
-            code = (ncomp * P * sm + mp) | ((mp & 1) << 30);
+    // staging map (staging mode): longitude index k -> offset of order |m| <= J
+    // among the staged columns of its sign, or -1
+    if (!gather)
+        for (int k = tid; k < Phi; k += kThreads) {
+            int off = -1;
+            if (k <= J) off = k;
+            else if (k >= Phi - J) off = ncomp * P * sm + (Phi - k);
+            stab[k] = off;
         }
-        stab[k] = code;
-    }
 
     // MFMA operands: the block's weight table as a buffer resource (reads past it
     // return zero), and this lane's byte offsets of row / column i, ring kq
     const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
     const int lane_a = ((lane >> 4) * bd.wrow + (lane & 15)) * (int)sizeof(T);
-    const int lane_b = ((lane >> 4) * sc * sm + (lane & 15) * sm) * (int)sizeof(T);
+    // B operand: staging mode reads (ring kq, column i) of the staged spectra;
+    // gather mode reads the in-place analysis output of column i = (sign,
+    // component, pair) at the tile's longitude position of +|m| or -|m|
+    // (columns past the last read column 0; their results are discarded)
+    const int lgC = lgP + (cross ? 2 : 0);   // log2(ncomp * pairs): columns per sign
+    int lane_b, lane_sg = 0;
+    if (!gather) {
+        lane_b = ((lane >> 4) * sc * sm + (lane & 15) * sm) * (int)sizeof(T);
+    } else {
+        const int col = (lane & 15) < (2 << lgC) ? (lane & 15) : 0;
+        const int comp = (col >> lgP) & (ncomp - 1), p = col & (P - 1);
+        lane_sg = col >> lgC;
+        lane_b = (((lane >> 4) * ly.per_r + p * ly.per_rp + (comp >> 1) * FS) * 2 + (comp & 1)) * (int)sizeof(T);
+    }
     const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
     // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
     // unpacking two packed signals, and the cross product's coupling constant
@@ -335,6 +362,13 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // scalar-vector
     const T sc_v = sc_s * (odd_sv ? (T)1 : tb.cross_cg);
     const T sc_e = sc_s * (even_dot ? tb.dot_cg : (T)1);
+
+    // gather mode: rings past the last one of the grid are read by the projection
+    // (with zero weight); give them finite contents once
+    if (gather) {
+        T* fz = reinterpret_cast<T*>(fbuf);
+        for (int e = tid; e < kRingGroup * ly.per_r * 2; e += kThreads) fz[e] = (T)0;
+    }
 
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
@@ -362,7 +396,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             dst[nj + mj] = cmk<C>(lcj[mj] * xlo, lcj[2 * nj + mj] * xhi);
         }
     }
-    for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
+    if (!gather)
+        for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
 
     Acc acc[MT];
 #pragma unroll
@@ -401,7 +436,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     v[n2i] = val;
                 }
                 Dft<B, true, C>::run(v);
-                C* row = fbuf + (size_t)rp * ly.per_rp + (size_t)s * FS + t * BP;
+                C* row = rpbuf(rp) + (size_t)s * FS + t * BP;
                 const C* twr = tw2 + t * BP;
 #pragma unroll
                 for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], twr[k2]);
@@ -414,7 +449,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             for (int task = tid; task < ntask; task += kThreads) {
                 const int k2 = task % B;
                 const int f = task / B;
-                C* fb = fbuf + (size_t)(f >> lgS) * ly.per_rp + (size_t)(f & (nslot - 1)) * FS + k2;
+                C* fb = rpbuf(f >> lgS) + (size_t)(f & (nslot - 1)) * FS + k2;
                 C u[A];
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
@@ -433,7 +468,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int pn = n + n / B, pk = kk + kk / B;   // pass-layout positions
                 // the products overwrite the second input's transforms: positions
                 // n and -n are read and written by this task only
-                C* fb = fbuf + (size_t)rp * ly.per_rp;
+                C* fb = rpbuf(rp);
                 if (!cross) {
                     const C g = cmul(fb[pn], fb[FS + pn]);
                     fb[FS + pn] = g;
@@ -486,7 +521,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int t = task % A;
                 const int f = task / A;
                 const int z = f & (nz - 1), rp = f >> lgZ;
-                const C* zb = fbuf + (size_t)rp * ly.per_rp + (size_t)(nslot - nz + z) * FS;
+                const C* zb = rpbuf(rp) + (size_t)(nslot - nz + z) * FS;
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {
@@ -494,14 +529,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     v[n2i] = zb[n + n / B];
                 }
                 Dft<B, false, C>::run(v);
-                C* row = fbuf + (size_t)rp * ly.per_rp + (size_t)z * FS + t * BP;
+                C* row = rpbuf(rp) + (size_t)z * FS + t * BP;
                 const C* twr = tw2 + t * BP;
 #pragma unroll
                 for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], twr[k2]);
             }
         }
         __syncthreads();
-        // ---- 4b. analysis pass 2 and staging of |m| <= J, scaled
+        // ---- 4b. analysis pass 2: in place (gather mode) or staged as |m| <= J
         {
             const int ntask = (nrg << (lgP + lgZ)) * B;
             for (int task = tid; task < ntask; task += kThreads) {
@@ -509,24 +544,26 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int f = task / B;
                 const int z = f & (nz - 1), rp = f >> lgZ;
                 const int p = rp & (P - 1), r = rp >> lgP;
-                const C* yb = fbuf + (size_t)rp * ly.per_rp + (size_t)z * FS + k2;
+                C* yb = rpbuf(rp) + (size_t)z * FS + k2;
                 C u[A];
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = yb[t * BP];
                 Dft<A, false, C>::run(u);
-                T* st = stage + (size_t)r * sc * sm + (size_t)p * sm;
+                if (gather) {
 #pragma unroll
-                for (int k1 = 0; k1 < A; ++k1) {
-                    const int code = stab[k2 + B * k1];
-                    if (code < 0) continue;
-                    const int off = code & 0x3fffffff;
-                    const T flip = (code >> 30) ? (T)-1 : (T)1;
-                    if (!cross) {
-                        st[off] = u[k1].x * sc_s * flip;
-                    } else {
-                        const int c0 = 2 * z, c1 = 2 * z + 1;
-                        st[c0 * P * sm + off] = u[k1].x * (c0 == 0 ? sc_e : sc_v) * flip;
-                        st[c1 * P * sm + off] = u[k1].y * sc_v * flip;
+                    for (int k1 = 0; k1 < A; ++k1) yb[k1 * BP] = u[k1];
+                } else {
+                    T* st = stage + (size_t)r * sc * sm + (size_t)p * sm;
+#pragma unroll
+                    for (int k1 = 0; k1 < A; ++k1) {
+                        const int off = stab[k2 + B * k1];
+                        if (off < 0) continue;
+                        if (!cross) {
+                            st[off] = u[k1].x;
+                        } else {
+                            st[2 * z * P * sm + off] = u[k1].x;
+                            st[(2 * z + 1) * P * sm + off] = u[k1].y;
+                        }
                     }
                 }
             }
@@ -535,12 +572,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         // ---- 5. Legendre projection on MFMA, accumulated over ring groups.  Lane
         // (i, kq) feeds row i / column i of ring 4 h + kq: its weight sits at
         // a_off + ring wrow + i of the block's table (a buffer load whose ring
-        // offset is scalar), its staged value at b_off + (ring, column i).
+        // offset is scalar), its spectrum value at the lane's B offset plus the
+        // tile's.
         {
 #pragma unroll
             for (int h = 0; h < kRingGroup / 4; ++h) {
                 const int soff = (rg0 + 4 * h) * bd.wrow * (int)sizeof(T);
-                const int bofs = lane_b + h * 4 * sc * sm * (int)sizeof(T);
+                const int bofs = gather ? ly.fbuf + lane_b + h * 4 * ly.per_r * (int)sizeof(C)
+                                        : ly.stage + lane_b + h * 4 * sc * sm * (int)sizeof(T);
                 int2 dsc[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) dsc[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)];
@@ -548,7 +587,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 #pragma unroll
                 for (int s = 0; s < MT; ++s) {
                     av[s] = buffer_load<T>(wrsrc, dsc[s].x + lane_a, soff);
-                    bv[s] = *reinterpret_cast<const T*>(smem + ly.stage + bofs + dsc[s].y);
+                    // staging mode: b_off in bytes; gather mode: the element offsets of
+                    // +|m| (low half) and -|m| (high half) in a transform
+                    const int bo = gather ? (lane_sg ? (dsc[s].y >> 16) : (dsc[s].y & 0xffff)) * (int)sizeof(T)
+                                          : dsc[s].y;
+                    bv[s] = *reinterpret_cast<const T*>(smem + bofs + bo);
                 }
 #pragma unroll
                 for (int s = 0; s < MT; ++s)
@@ -561,24 +604,30 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // ---- accumulators of every pair -> LDS once, then recombination, 1/K, contiguous store
     {
         const int col_in = lane & 15, rq = lane >> 4;
+        int codes[MT];
+#pragma unroll
+        for (int s = 0; s < MT; ++s) codes[s] = tdc[min(wave + kWaves * s, bd.ntiles - 1)];
 #pragma unroll
         for (int s = 0; s < MT; ++s) {
-            const int u = wave + kWaves * s;
-            if (u < bd.ntiles) {
-                const int code = td[u].code;   // wave-uniform
+            if (wave + kWaves * s < bd.ntiles) {
+                const int code = codes[s];
                 const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
                 const int col = 16 * ct + col_in;
                 const int p = col & (P - 1);
-                if (col < geo.ncols(mp) && p < np) {
-                    const int sg = col / (ncomp * P);
-                    const int comp = (col >> lgP) % ncomp;
-                    const int m = sg ? -mp : mp;
-                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nel;
+                const int ncol = (mp == 0 ? 1 : 2) << lgC;
+                if (col < ncol && p < np) {
+                    const int sg = col >> lgC;
+                    const int comp = (col >> lgP) & (ncomp - 1);
+                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nel + (sg ? -mp : mp);
+                    // longitude quadrature and unpacking scale with the product's
+                    // coupling constant, and P^{-m} = (-1)^m P^m for negative m
+                    const T f = (comp == 0 ? sc_e : sc_v) * ((sg && (mp & 1)) ? (T)-1 : (T)1);
+                    const int tr0 = geo.tmin(mp, d) + 16 * rt;
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const int tr = geo.tmin(mp, d) + 16 * rt + acc_row<T>(rq, q);
+                        const int tr = tr0 + acc_row<T>(rq, q);
                         const int l3 = d + 2 * tr;
-                        if (l3 <= J) dst[acc_rowoff(tr, d) + l3 + m] = acc[s][q];
+                        if (l3 <= J) dst[acc_rowoff(tr, d) + l3] = acc[s][q] * f;
                     }
                 }
             }
@@ -588,18 +637,32 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // output o of the block: (w0, w1, w2, idx); idx < 0 marks a scalar-scalar
     // path whose accumulator entry is -idx - 1, else e = idx - 1 is the entry of
     // (j3 - 1, m3) and the q = -1, 0, +1 terms sit at e + 1, e, e - 1 of
-    // components 2, 1, 3 (out-of-range terms carry zero weight)
-    const int nblk = n1 * n2;
-    for (int p = 0; p < np; ++p) {
-        const T* bp = bbuf + (size_t)p * ncomp * nel;
-        T* op = out + (p0 + p) * nout + bd.out_off;
-        for (int o = tid; o < nblk; o += kThreads) {
-            const Coef4 cf = coef4[o];
-            const int idx = (int)cf.w;
-            T z;
-            if (idx < 0) z = cf.x * bp[-idx - 1];
-            else z = cf.x * bp[2 * nel + idx] + cf.y * bp[nel + idx - 1] + cf.z * bp[3 * nel + idx - 2];
-            op[o] = z;
+    // components 2, 1, 3 (out-of-range terms carry zero weight).  Each
+    // coefficient is read once and applied to every pair of the tile.
+    {
+        const int nblk = n1 * n2;
+        T* ob = out + p0 * nout + bd.out_off;
+        for (int o0 = tid; o0 < nblk; o0 += 2 * kThreads) {
+            Coef4 cf[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) cf[k] = coef4[min(o0 + k * kThreads, nblk - 1)];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int o = o0 + k * kThreads;
+                if (o < nblk) {
+                    const int idx = (int)cf[k].w;
+                    const bool ss = idx < 0;
+                    const int e0 = ss ? -idx - 1 : 2 * nel + idx;
+                    const int e1 = ss ? 0 : nel + idx - 1;
+                    const int e2 = ss ? 0 : 3 * nel + idx - 2;
+                    for (int p = 0; p < np; ++p) {
+                        const T* bp = bbuf + (size_t)p * ncomp * nel;
+                        T z = cf[k].x * bp[e0];
+                        if (!ss) z += cf[k].y * bp[e1] + cf[k].z * bp[e2];
+                        ob[(size_t)p * nout + o] = z;
+                    }
+                }
+            }
         }
     }
     __syncthreads();

@@ -356,7 +356,7 @@ int block_tiles(const BlockDesc& b, int pairs) {
 
 // Dynamic LDS of one work-group; mirrors the kernel's make_layout.
 template <typename T>
-int lds_for(const BlockDesc& b, int pairs) {
+int lds_for(const BlockDesc& b, int pairs, int mode) {
     const int sz = (int)sizeof(T), csz = 2 * sz;
     const bool cross = b.kind == cgtp::kBlockCross;
     const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
@@ -368,11 +368,12 @@ int lds_for(const BlockDesc& b, int pairs) {
     o = align16h(o + csz * FS);
     o = align16h(o + 4 * b.A * b.B);
     o = align16h(o + 8 * block_tiles(b, pairs));
+    o = align16h(o + 4 * block_tiles(b, pairs));
     o = align16h(o + csz * pairs * 2 * (n1 + n2));
     const int stage = o;
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
-    o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
-    o += csz * cgtp::kRingGroup * pairs * nslot * FS;
+    if (mode == cgtp::kModeStaged) o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
+    o += csz * cgtp::kRingGroup * (pairs * nslot * FS + 8);   // 8: the ring skew
     const int end_phase = stage + sz * pairs * ncomp * acc_entries(b.d, b.J);
     return std::max(o, end_phase);
 }
@@ -521,17 +522,25 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             flops += block_flops(j1, j2);
             // pairs per work-group: as many as the accumulator registers and LDS allow
             const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
-            int pairs = 0;
-            for (int P = cgtp::kMaxPairs; P >= 1; P /= 2) {
-                if (block_tiles(b, P) <= max_tiles && lds_for<T>(b, P) <= cgtp::kLdsBudget) { pairs = P; break; }
-            }
-            if (pairs == 0) return CGTP_EUNSUP;
+            // and whether the projection reads the transforms in place (one MFMA
+            // column tile; no staging buffer) or staged spectra (any number)
+            const int ncomp = b.kind == cgtp::kBlockCross ? 4 : 1;
+            auto fits = [&](int P, int mode) {
+                return block_tiles(b, P) <= max_tiles && lds_for<T>(b, P, mode) <= cgtp::kLdsBudget;
+            };
+            int p_gather = 0, p_staged = 0;
+            for (int P = cgtp::kMaxPairs; P >= 1 && !p_gather; P /= 2)
+                if (ncomp * P <= 8 && fits(P, cgtp::kModeGather)) p_gather = P;
+            for (int P = cgtp::kMaxPairs; P >= 1 && !p_staged; P /= 2)
+                if (fits(P, cgtp::kModeStaged)) p_staged = P;
+            if (p_gather == 0 && p_staged == 0) return CGTP_EUNSUP;
+            b.mode = p_gather >= p_staged ? cgtp::kModeGather : cgtp::kModeStaged;
+            const int pairs = b.mode == cgtp::kModeGather ? p_gather : p_staged;
             b.pairs = pairs;
             b.lg_pairs = 0;
             while ((1 << b.lg_pairs) < pairs) ++b.lg_pairs;
             b.ntiles = block_tiles(b, pairs);
-            b.lds_bytes = lds_for<T>(b, pairs);
-            const int ncomp = b.kind == cgtp::kBlockCross ? 4 : 1;
+            b.lds_bytes = lds_for<T>(b, pairs, b.mode);
             b.sc = ((2 * ncomp * pairs + 15) / 16) * 16;
             b.sm = (b.J + 1) | 1;
             // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
@@ -548,7 +557,13 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                             cgtp::TileDesc t;
                             t.a_off = mp * b.rpad * b.wrow + (l30 - par) / 2;
                             t.rs_nv = nv << 16;
-                            t.b_off = 16 * ct * b.sm + mp;
+                            if (b.mode == cgtp::kModeStaged) {
+                                t.b_off = 16 * ct * b.sm + mp;
+                            } else {
+                                // pass-layout positions k + k / B of longitudes +|m| and -|m|
+                                const int kn = (b.Phi - mp) % b.Phi;
+                                t.b_off = 2 * (mp + mp / b.B) | (2 * (kn + kn / b.B)) << 16;
+                            }
                             t.code = (mp << 16) | (rt << 8) | ct;
                             h.tdesc.push_back(t);
                         }
