@@ -387,13 +387,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         const T xm = ok ? xg[row + mj] : (T)0;
         const T* lcj = first ? lc : lc + 3 * n1;
         C* dst = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1);
+        // P^{-m} = (-1)^m P^m: the sign of negative odd orbital orders goes here
+        const T sg = (mj < j && ((j - mj) & 1)) ? (T)-1 : (T)1;
         if (!cross) {
-            dst[mj] = cmk<C>(xm, (T)0);
+            dst[mj] = cmk<C>(sg * xm, (T)0);
         } else {
             const T xlo = (ok && mj >= 1) ? xg[row + mj - 1] : (T)0;
             const T xhi = (ok && mj + 1 < nj) ? xg[row + mj + 1] : (T)0;
-            dst[mj] = cmk<C>(xm, lcj[nj + mj] * xm);
-            dst[nj + mj] = cmk<C>(lcj[mj] * xlo, lcj[2 * nj + mj] * xhi);
+            dst[mj] = cmk<C>(sg * xm, sg * lcj[nj + mj] * xm);
+            dst[nj + mj] = cmk<C>(sg * lcj[mj] * xlo, sg * lcj[2 * nj + mj] * xhi);
         }
     }
     if (!gather)
@@ -406,6 +408,19 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 
     for (int rg0 = 0; rg0 < R; rg0 += kRingGroup) {
         const int nrg = (R - rg0) < kRingGroup ? (R - rg0) : kRingGroup;
+        // the group's MFMA weights (operand A) are fetched now and land while the
+        // transforms run
+        T apre[kRingGroup / 4][MT];
+        {
+            int ax[MT];
+#pragma unroll
+            for (int s = 0; s < MT; ++s) ax[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)].x + lane_a;
+#pragma unroll
+            for (int h = 0; h < kRingGroup / 4; ++h)
+#pragma unroll
+                for (int s = 0; s < MT; ++s)
+                    apre[h][s] = buffer_load<T>(wrsrc, ax[s], (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
+        }
 
         // ---- 1. lift + synthesis pass 1: task ((ring, pair, slot), t) -> row t
         {
@@ -421,25 +436,26 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int nj = 2 * j + 1;
                 const C* cv = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1) + (cross ? (s & 1) * nj : 0) + j;
                 const T* pr = pst + (rg0 + r) * npr + (first ? 0 : j1 + 1);
+                // orders outside -j..j read order 0 and are zeroed
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {
                     const int n = t + A * n2i;
-                    const int m = n <= j ? n : n - Phi;
-                    C val = cmk<C>((T)0, (T)0);
-                    if (n <= j || n >= Phi - j) {
-                        const int am = m < 0 ? -m : m;
-                        const T pv = (m < 0 && (am & 1)) ? -pr[am] : pr[am];
-                        const C c = cv[m];
-                        val = cmk<C>(c.x * pv, c.y * pv);
-                    }
-                    v[n2i] = val;
+                    const bool ok = n <= j || n >= Phi - j;
+                    const int m = ok ? (n <= j ? n : n - Phi) : 0;
+                    const T pv = ok ? pr[m < 0 ? -m : m] : (T)0;
+                    const C c = cv[m];
+                    v[n2i] = cmk<C>(c.x * pv, c.y * pv);
                 }
                 Dft<B, true, C>::run(v);
                 C* row = rpbuf(rp) + (size_t)s * FS + t * BP;
+                // all twiddles first: the row stores may not be moved above them
                 const C* twr = tw2 + t * BP;
+                C w[B];
 #pragma unroll
-                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], twr[k2]);
+                for (int k2 = 1; k2 < B; ++k2) w[k2] = twr[k2];
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], w[k2]);
             }
         }
         __syncthreads();
@@ -531,8 +547,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 Dft<B, false, C>::run(v);
                 C* row = rpbuf(rp) + (size_t)z * FS + t * BP;
                 const C* twr = tw2 + t * BP;
+                C w[B];
 #pragma unroll
-                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], twr[k2]);
+                for (int k2 = 1; k2 < B; ++k2) w[k2] = twr[k2];
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], w[k2]);
             }
         }
         __syncthreads();
@@ -577,16 +596,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         {
 #pragma unroll
             for (int h = 0; h < kRingGroup / 4; ++h) {
-                const int soff = (rg0 + 4 * h) * bd.wrow * (int)sizeof(T);
                 const int bofs = gather ? ly.fbuf + lane_b + h * 4 * ly.per_r * (int)sizeof(C)
                                         : ly.stage + lane_b + h * 4 * sc * sm * (int)sizeof(T);
                 int2 dsc[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) dsc[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)];
-                T av[MT], bv[MT];
+                T bv[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) {
-                    av[s] = buffer_load<T>(wrsrc, dsc[s].x + lane_a, soff);
                     // staging mode: b_off in bytes; gather mode: the element offsets of
                     // +|m| (low half) and -|m| (high half) in a transform
                     const int bo = gather ? (lane_sg ? (dsc[s].y >> 16) : (dsc[s].y & 0xffff)) * (int)sizeof(T)
@@ -595,7 +612,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 }
 #pragma unroll
                 for (int s = 0; s < MT; ++s)
-                    if (wave + kWaves * s < bd.ntiles) acc[s] = mfma16(av[s], bv[s], acc[s]);
+                    if (wave + kWaves * s < bd.ntiles) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);
             }
         }
         __syncthreads();
