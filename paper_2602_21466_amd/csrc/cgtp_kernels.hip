@@ -252,6 +252,10 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     return l;
 }
 
+// Orders a wave's own LDS accesses: every store issued before is complete and
+// visible to the wave's later loads (no other wave is involved).
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // ---------------------------------------------------------------- the block body
 
 template <typename T, int A, int B>
@@ -422,14 +426,20 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     apre[h][s] = buffer_load<T>(wrsrc, ax[s], (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
         }
 
-        // ---- 1. lift + synthesis pass 1: task ((ring, pair, slot), t) -> row t
+        // Phases 1 to 4 work on (ring, pair) units; wave w owns units w, w + kWaves,
+        // ... and takes each of them through synthesis, products and analysis, so
+        // between these phases only its own LDS accesses need ordering.
+        const int nunit = nrg << lgP;
+        const int uw = nunit > wave ? (nunit - 1 - wave) / kWaves + 1 : 0;   // units of this wave
+
+        // ---- 1. lift + synthesis pass 1: task ((unit, slot), t) -> row t
         {
-            const int ntask = (nrg << (lgP + lgS)) * A;
-            for (int task = tid; task < ntask; task += kThreads) {
+            const int ntask = (uw << lgS) * A;
+            for (int task = lane; task < ntask; task += 64) {
                 const int t = task % A;
                 const int f = task / A;
                 const int s = f & (nslot - 1);
-                const int rp = f >> lgS;
+                const int rp = wave + kWaves * (f >> lgS);
                 const int p = rp & (P - 1), r = rp >> lgP;
                 const bool first = cross ? (s < 2) : (s == 0);
                 const int j = first ? j1 : j2;
@@ -458,14 +468,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], w[k2]);
             }
         }
-        __syncthreads();
-        // ---- 2. synthesis pass 2 (in place): task ((ring, pair, slot), column k2)
+        wave_lds_sync();
+        // ---- 2. synthesis pass 2 (in place): task ((unit, slot), column k2)
         {
-            const int ntask = (nrg << (lgP + lgS)) * B;
-            for (int task = tid; task < ntask; task += kThreads) {
+            const int ntask = (uw << lgS) * B;
+            for (int task = lane; task < ntask; task += 64) {
                 const int k2 = task % B;
                 const int f = task / B;
-                C* fb = rpbuf(f >> lgS) + (size_t)(f & (nslot - 1)) * FS + k2;
+                C* fb = rpbuf(wave + kWaves * (f >> lgS)) + (size_t)(f & (nslot - 1)) * FS + k2;
                 C u[A];
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
@@ -474,12 +484,12 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
             }
         }
-        __syncthreads();
+        wave_lds_sync();
         // ---- 3. pointwise products on half the circle, mirrored
         {
-            const int ntask = (nrg << lgP) * H;
-            for (int task = tid; task < ntask; task += kThreads) {
-                const int n = task % H, rp = task / H;
+            const int ntask = uw * H;
+            for (int task = lane; task < ntask; task += 64) {
+                const int n = task % H, rp = wave + kWaves * (task / H);
                 const int kk = n == 0 ? 0 : Phi - n;
                 const int pn = n + n / B, pk = kk + kk / B;   // pass-layout positions
                 // the products overwrite the second input's transforms: positions
@@ -529,14 +539,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 }
             }
         }
-        __syncthreads();
-        // ---- 4a. analysis pass 1: task ((ring, pair, z), t); rows into slot z
+        wave_lds_sync();
+        // ---- 4a. analysis pass 1: task ((unit, z), t); rows into slot z
         {
-            const int ntask = (nrg << (lgP + lgZ)) * A;
-            for (int task = tid; task < ntask; task += kThreads) {
+            const int ntask = (uw << lgZ) * A;
+            for (int task = lane; task < ntask; task += 64) {
                 const int t = task % A;
                 const int f = task / A;
-                const int z = f & (nz - 1), rp = f >> lgZ;
+                const int z = f & (nz - 1), rp = wave + kWaves * (f >> lgZ);
                 const C* zb = rpbuf(rp) + (size_t)(nslot - nz + z) * FS;
                 C v[B];
 #pragma unroll
@@ -554,14 +564,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], w[k2]);
             }
         }
-        __syncthreads();
+        wave_lds_sync();
         // ---- 4b. analysis pass 2: in place (gather mode) or staged as |m| <= J
         {
-            const int ntask = (nrg << (lgP + lgZ)) * B;
-            for (int task = tid; task < ntask; task += kThreads) {
+            const int ntask = (uw << lgZ) * B;
+            for (int task = lane; task < ntask; task += 64) {
                 const int k2 = task % B;
                 const int f = task / B;
-                const int z = f & (nz - 1), rp = f >> lgZ;
+                const int z = f & (nz - 1), rp = wave + kWaves * (f >> lgZ);
                 const int p = rp & (P - 1), r = rp >> lgP;
                 C* yb = rpbuf(rp) + (size_t)z * FS + k2;
                 C u[A];
