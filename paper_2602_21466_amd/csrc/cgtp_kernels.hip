@@ -256,6 +256,12 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
 // visible to the wave's later loads (no other wave is involved).
 __device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Work-group barrier for LDS only.  The block kernel's waves never exchange data
+// through global memory (they read inputs and tables and write disjoint
+// outputs), so a barrier need not wait for outstanding global loads and stores:
+// output stores drain and weight prefetches land across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ---------------------------------------------------------------- the block body
 
 template <typename T, int A, int B>
@@ -282,6 +288,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
     const int nrows = (J - d) / 2 + 1;
     const int nel = nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
+    const int nes = nel | 1;           // odd stride of the end phase's [pair][comp] rows: spreads banks
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
     const int sm = bd.sm, sc = bd.sc;
@@ -298,7 +305,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
-    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nel], end phase only
+    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nes], end phase only
     const bool gather = bd.mode == kModeGather;
     // transforms of (ring, pair) rp = ring * P + pair
     auto rpbuf = [&](int rp) -> C* {
@@ -357,6 +364,16 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         lane_sg = col >> lgC;
         lane_b = (((lane >> 4) * ly.per_r + p * ly.per_rp + (comp >> 1) * FS) * 2 + (comp & 1)) * (int)sizeof(T);
     }
+    // this wave's MFMA tiles: wave w owns w, w + kWaves, ...; per tile the LDS
+    // byte address of the lane's B operand at ring 4 h + kq, h = 0
+    const int ntw = bd.ntiles > wave ? (bd.ntiles - 1 - wave) / kWaves + 1 : 0;
+    int bx[MT];
+#pragma unroll
+    for (int s = 0; s < MT; ++s) {
+        const int bo = td[min(wave + kWaves * s, bd.ntiles - 1)].b_off;
+        bx[s] = gather ? ly.fbuf + lane_b + (lane_sg ? (bo >> 16) : (bo & 0xffff)) * (int)sizeof(T)
+                       : ly.stage + lane_b + bo * (int)sizeof(T);
+    }
     const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
     // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
     // unpacking two packed signals, and the cross product's coupling constant
@@ -408,7 +425,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     Acc acc[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) acc[s] = Acc(0);
-    __syncthreads();
+    lds_barrier();
 
     for (int rg0 = 0; rg0 < R; rg0 += kRingGroup) {
         const int nrg = (R - rg0) < kRingGroup ? (R - rg0) : kRingGroup;
@@ -416,14 +433,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         // transforms run
         T apre[kRingGroup / 4][MT];
         {
-            int ax[MT];
 #pragma unroll
-            for (int s = 0; s < MT; ++s) ax[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)].x + lane_a;
+            for (int s = 0; s < MT; ++s) {
+                if (s < ntw) {
+                    const int ax = tdl[wave + kWaves * s].x + lane_a;
 #pragma unroll
-            for (int h = 0; h < kRingGroup / 4; ++h)
-#pragma unroll
-                for (int s = 0; s < MT; ++s)
-                    apre[h][s] = buffer_load<T>(wrsrc, ax[s], (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
+                    for (int h = 0; h < kRingGroup / 4; ++h)
+                        apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
+                }
+            }
         }
 
         // Phases 1 to 4 work on (ring, pair) units; wave w owns units w, w + kWaves,
@@ -597,7 +615,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();
         // ---- 5. Legendre projection on MFMA, accumulated over ring groups.  Lane
         // (i, kq) feeds row i / column i of ring 4 h + kq: its weight sits at
         // a_off + ring wrow + i of the block's table (a buffer load whose ring
@@ -606,26 +624,17 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         {
 #pragma unroll
             for (int h = 0; h < kRingGroup / 4; ++h) {
-                const int bofs = gather ? ly.fbuf + lane_b + h * 4 * ly.per_r * (int)sizeof(C)
-                                        : ly.stage + lane_b + h * 4 * sc * sm * (int)sizeof(T);
-                int2 dsc[MT];
-#pragma unroll
-                for (int s = 0; s < MT; ++s) dsc[s] = tdl[min(wave + kWaves * s, bd.ntiles - 1)];
+                const int hofs = h * 4 * (gather ? ly.per_r * (int)sizeof(C) : sc * sm * (int)sizeof(T));
                 T bv[MT];
 #pragma unroll
-                for (int s = 0; s < MT; ++s) {
-                    // staging mode: b_off in bytes; gather mode: the element offsets of
-                    // +|m| (low half) and -|m| (high half) in a transform
-                    const int bo = gather ? (lane_sg ? (dsc[s].y >> 16) : (dsc[s].y & 0xffff)) * (int)sizeof(T)
-                                          : dsc[s].y;
-                    bv[s] = *reinterpret_cast<const T*>(smem + bofs + bo);
-                }
+                for (int s = 0; s < MT; ++s)
+                    if (s < ntw) bv[s] = *reinterpret_cast<const T*>(smem + bx[s] + hofs);
 #pragma unroll
                 for (int s = 0; s < MT; ++s)
-                    if (wave + kWaves * s < bd.ntiles) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);
+                    if (s < ntw) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
 
     // ---- accumulators of every pair -> LDS once, then recombination, 1/K, contiguous store
@@ -645,7 +654,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 if (col < ncol && p < np) {
                     const int sg = col >> lgC;
                     const int comp = (col >> lgP) & (ncomp - 1);
-                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nel + (sg ? -mp : mp);
+                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nes + (sg ? -mp : mp);
                     // longitude quadrature and unpacking scale with the product's
                     // coupling constant, and P^{-m} = (-1)^m P^m for negative m
                     const T f = (comp == 0 ? sc_e : sc_v) * ((sg && (mp & 1)) ? (T)-1 : (T)1);
@@ -660,7 +669,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     // output o of the block: (w0, w1, w2, idx); idx < 0 marks a scalar-scalar
     // path whose accumulator entry is -idx - 1, else e = idx - 1 is the entry of
     // (j3 - 1, m3) and the q = -1, 0, +1 terms sit at e + 1, e, e - 1 of
@@ -679,11 +688,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 if (o < nblk) {
                     const int idx = (int)cf[k].w;
                     const bool ss = idx < 0;
-                    const int e0 = ss ? -idx - 1 : 2 * nel + idx;
-                    const int e1 = ss ? 0 : nel + idx - 1;
-                    const int e2 = ss ? 0 : 3 * nel + idx - 2;
+                    const int e0 = ss ? -idx - 1 : 2 * nes + idx;
+                    const int e1 = ss ? 0 : nes + idx - 1;
+                    const int e2 = ss ? 0 : 3 * nes + idx - 2;
                     for (int p = 0; p < np; ++p) {
-                        const T* bp = bbuf + (size_t)p * ncomp * nel;
+                        const T* bp = bbuf + (size_t)p * ncomp * nes;
                         T z = cf[k].x * bp[e0];
                         if (!ss) z += cf[k].y * bp[e1] + cf[k].z * bp[e2];
                         ob[(size_t)p * nout + o] = z;
@@ -692,7 +701,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
     }   // pair tiles
 }
 

@@ -374,7 +374,7 @@ int lds_for(const BlockDesc& b, int pairs, int mode) {
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
     if (mode == cgtp::kModeStaged) o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
     o += csz * cgtp::kRingGroup * (pairs * nslot * FS + 8);   // 8: the ring skew
-    const int end_phase = stage + sz * pairs * ncomp * acc_entries(b.d, b.J);
+    const int end_phase = stage + sz * pairs * ncomp * (acc_entries(b.d, b.J) | 1);
     return std::max(o, end_phase);
 }
 
