@@ -659,11 +659,24 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     // coupling constant, and P^{-m} = (-1)^m P^m for negative m
                     const T f = (comp == 0 ? sc_e : sc_v) * ((sg && (mp & 1)) ? (T)-1 : (T)1);
                     const int tr0 = geo.tmin(mp, d) + 16 * rt;
+                    if constexpr (sizeof(T) == 4) {
+                        // rows tr, tr + 1, ... of this lane: entry 2 tr^2 + (2 d + 1) tr + d,
+                        // advancing by 4 tr + 2 d + 3
+                        const int tr = tr0 + 4 * rq;
+                        int e = 2 * tr * tr + (2 * d + 1) * tr + d, de = 4 * tr + 2 * d + 3;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int tr = tr0 + acc_row<T>(rq, q);
-                        const int l3 = d + 2 * tr;
-                        if (l3 <= J) dst[acc_rowoff(tr, d) + l3] = acc[s][q] * f;
+                        for (int q = 0; q < 4; ++q) {
+                            if (tr + q < nrows) dst[e] = acc[s][q] * f;
+                            e += de;
+                            de += 4;
+                        }
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int tr = tr0 + acc_row<T>(rq, q);
+                            const int l3 = d + 2 * tr;
+                            if (l3 <= J) dst[acc_rowoff(tr, d) + l3] = acc[s][q] * f;
+                        }
                     }
                 }
             }
@@ -691,11 +704,20 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     const int e0 = ss ? -idx - 1 : 2 * nes + idx;
                     const int e1 = ss ? 0 : nes + idx - 1;
                     const int e2 = ss ? 0 : 3 * nes + idx - 2;
-                    for (int p = 0; p < np; ++p) {
-                        const T* bp = bbuf + (size_t)p * ncomp * nes;
-                        T z = cf[k].x * bp[e0];
-                        if (!ss) z += cf[k].y * bp[e1] + cf[k].z * bp[e2];
-                        ob[(size_t)p * nout + o] = z;
+                    // four pairs at a time: their gathers are in flight together
+                    for (int p0 = 0; p0 < np; p0 += 4) {
+                        T v0[4], v1[4], v2[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const T* bp = bbuf + (size_t)min(p0 + u, np - 1) * ncomp * nes;
+                            v0[u] = bp[e0];
+                            v1[u] = ss ? (T)0 : bp[e1];
+                            v2[u] = ss ? (T)0 : bp[e2];
+                        }
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (p0 + u < np)
+                                ob[(size_t)(p0 + u) * nout + o] = cf[k].x * v0[u] + cf[k].y * v1[u] + cf[k].z * v2[u];
                     }
                 }
             }
