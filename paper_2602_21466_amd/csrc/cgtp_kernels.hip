@@ -219,7 +219,7 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 constexpr int kRingSkew = 8;
 
 struct Layout {
-    int lc, pst, tw2, stab, tdl, tdc, lc2, stage, fbuf, bbuf;   // byte offsets
+    int lc, pst, tw2, tdl, tdc, lc2, stage, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
     int per_r;                                       // complex entries per ring
 };
@@ -227,7 +227,7 @@ struct Layout {
 __device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
 
 // Block-level data first (couplings, Legendre rows of every ring, twiddles,
-// staging map), then the tile's lifted coefficients, then the per-ring
+// MFMA tile table), then the tile's lifted coefficients, then the per-ring
 // working set; the end phase reuses the working set for the accumulators.
 template <typename T, int A, int B>
 __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
@@ -239,7 +239,6 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
     l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
-    l.stab = o; o = align16(o + 4 * A * B);
     l.tdl = o; o = align16(o + 8 * b.ntiles);
     l.tdc = o; o = align16(o + 4 * b.ntiles);
     l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
@@ -298,7 +297,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
     T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
-    int* stab = reinterpret_cast<int*>(smem + ly.stab);  // longitude k -> staged offset | sign, or -1
     int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
     int* tdc = reinterpret_cast<int*>(smem + ly.tdc);    // per MFMA tile: its code
 
@@ -335,15 +333,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         tdc[u] = t.code;
     }
 
-    // staging map (staging mode): longitude index k -> offset of order |m| <= J
-    // among the staged columns of its sign, or -1
-    if (!gather)
-        for (int k = tid; k < Phi; k += kThreads) {
-            int off = -1;
-            if (k <= J) off = k;
-            else if (k >= Phi - J) off = ncomp * P * sm + (Phi - k);
-            stab[k] = off;
-        }
 
     // MFMA operands: the block's weight table as a buffer resource (reads past it
     // return zero), and this lane's byte offsets of row / column i, ring kq
@@ -601,10 +590,14 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     for (int k1 = 0; k1 < A; ++k1) yb[k1 * BP] = u[k1];
                 } else {
                     T* st = stage + (size_t)r * sc * sm + (size_t)p * sm;
+                    const int neg = ncomp * P * sm + Phi;   // offset of order -(Phi - k) is neg - k
 #pragma unroll
                     for (int k1 = 0; k1 < A; ++k1) {
-                        const int off = stab[k2 + B * k1];
-                        if (off < 0) continue;
+                        // longitude index k = k2 + B k1: order k if k <= J, order -(Phi - k)
+                        // if k >= Phi - J, else not needed
+                        const int k = k2 + B * k1;
+                        if (k > J && k < Phi - J) continue;
+                        const int off = k <= J ? k : neg - k;
                         if (!cross) {
                             st[off] = u[k1].x;
                         } else {

@@ -366,7 +366,6 @@ int lds_for(const BlockDesc& b, int pairs, int mode) {
     o = align16h(o + sz * 3 * (n1 + n2));
     o = align16h(o + sz * b.R * (b.j1 + 1 + b.j2 + 1));
     o = align16h(o + csz * FS);
-    o = align16h(o + 4 * b.A * b.B);
     o = align16h(o + 8 * block_tiles(b, pairs));
     o = align16h(o + 4 * block_tiles(b, pairs));
     o = align16h(o + csz * pairs * 2 * (n1 + n2));
