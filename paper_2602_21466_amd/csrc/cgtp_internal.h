@@ -64,7 +64,7 @@ struct alignas(16) BlockDesc {
     int32_t pbar_stride;       // Legendre entries per ring: (lmax+1)(lmax+2)/2
     int32_t wtab_off;          // offset of the MFMA weights of the grid, parity of J (elements)
     int32_t lmax;              // largest degree of the grid's tables
-    int32_t coef_off;          // offset of the block's output coefficients (4 per output)
+    int32_t coef_off;          // index of the block's first output in coef / coefi
     int32_t tdesc_off;         // offset of the block's MFMA tile descriptors
     int32_t lg_pairs;          // log2(pairs)
     int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
@@ -99,10 +99,9 @@ struct Tables {
     const T* wtab;      // see above
     const T* tw;        // per Phi, complex pairs in pass layout: [t < A][k2 < B+1] = exp(-2 pi i t k2 / Phi)
     const T* lcg;       // [j][q+1][m + j] = C^{j, m+q}_{j, m, 1, q}
-    const T* coef;      // per block and output (j3, m3): recombination weights times 1/K, and the source index
+    const T* coef;      // per block and output (j3, m3): up to three term weights (4 per output)
+    const int32_t* coefi;   // per block and output: end-phase entries of the terms for pair 0, single-term flag
     const TileDesc* tdesc;
-    T cross_cg;         // C^{1,1}_{1,1,1,0}: the cross product's coupling constant
-    T dot_cg;           // C^{0,0}_{1,1,1,-1}: the dot product's coupling constant
     int32_t wtab_len;   // elements of wtab
     const BlockDesc* blocks;
 };
@@ -138,6 +137,10 @@ inline bool fft_factors(int phi, int* A, int* B) {
         }
     return false;
 }
+
+// End phase: MFMA tile u of a block is dumped at u * tile_stride<T>() elements;
+// the padding keeps consecutive tiles on different LDS banks.
+template <typename T> __host__ __device__ constexpr int tile_stride() { return sizeof(T) == 4 ? 260 : 258; }
 
 // Accumulator geometry shared by host and device.
 struct TileGeom {

@@ -219,7 +219,7 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 constexpr int kRingSkew = 8;
 
 struct Layout {
-    int lc, pst, tw2, tdl, tdc, lc2, stage, fbuf, bbuf;   // byte offsets
+    int lc, pst, tw2, tdl, lc2, stage, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
     int per_r;                                       // complex entries per ring
 };
@@ -240,7 +240,6 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.tdl = o; o = align16(o + 8 * b.ntiles);
-    l.tdc = o; o = align16(o + 4 * b.ntiles);
     l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
     l.stage = o;
     if (b.mode == kModeStaged) o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
@@ -286,8 +285,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const int ncomp = cross ? 4 : 1;   // projected components
     const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
     const int nrows = (J - d) / 2 + 1;
-    const int nel = nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
-    const int nes = nel | 1;           // odd stride of the end phase's [pair][comp] rows: spreads banks
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
     const int sm = bd.sm, sc = bd.sc;
@@ -298,12 +295,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
-    int* tdc = reinterpret_cast<int*>(smem + ly.tdc);    // per MFMA tile: its code
 
     C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
-    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // [pair][comp][nes], end phase only
+    T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // MFMA tiles, end phase only
     const bool gather = bd.mode == kModeGather;
     // transforms of (ring, pair) rp = ring * P + pair
     auto rpbuf = [&](int rp) -> C* {
@@ -311,7 +307,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     };
     const TileDesc* __restrict__ td = tdesc + bd.tdesc_off;
     using Coef4 = typename Cplx<T>::acc4;
-    const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef + bd.coef_off);
+    const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef) + bd.coef_off;
+    const int4* coefi = reinterpret_cast<const int4*>(tb.coefi) + bd.coef_off;
 
     // ---- block-level set-up: couplings, Legendre rows of every ring, twiddles
     for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
@@ -330,7 +327,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
         const TileDesc t = td[u];
         tdl[u] = make_int2(t.a_off * (int)sizeof(T), gather ? t.b_off : t.b_off * (int)sizeof(T));
-        tdc[u] = t.code;
     }
 
 
@@ -364,14 +360,9 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                        : ly.stage + lane_b + bo * (int)sizeof(T);
     }
     const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
-    // staged value scale: 2 pi / Phi from the longitude quadrature, 1/4 from
-    // unpacking two packed signals, and the cross product's coupling constant
-    const T sc_s = (T)(6.283185307179586476925286766559 / Phi) * (cross ? (T)0.25 : (T)1);
-    // component 0 (even paths): scalar-scalar, or the dot product's coupling
-    // constant; components 1..3 (odd paths): the cross product's, or none for
-    // scalar-vector
-    const T sc_v = sc_s * (odd_sv ? (T)1 : tb.cross_cg);
-    const T sc_e = sc_s * (even_dot ? tb.dot_cg : (T)1);
+    // (the longitude quadrature and unpacking scales, the products' coupling
+    // constants and the sign of negative orders are folded into the output
+    // coefficients)
 
     // gather mode: rings past the last one of the grid are read by the projection
     // (with zero weight); give them finite contents once
@@ -630,89 +621,32 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         lds_barrier();
     }
 
-    // ---- accumulators of every pair -> LDS once, then recombination, 1/K, contiguous store
-    {
-        const int col_in = lane & 15, rq = lane >> 4;
-        int codes[MT];
+    // ---- accumulators -> LDS verbatim (tile u at u * tile_stride), then each
+    // output as up to three weighted entries (plan-made), contiguous stores
 #pragma unroll
-        for (int s = 0; s < MT; ++s) codes[s] = tdc[min(wave + kWaves * s, bd.ntiles - 1)];
-#pragma unroll
-        for (int s = 0; s < MT; ++s) {
-            if (wave + kWaves * s < bd.ntiles) {
-                const int code = codes[s];
-                const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
-                const int col = 16 * ct + col_in;
-                const int p = col & (P - 1);
-                const int ncol = (mp == 0 ? 1 : 2) << lgC;
-                if (col < ncol && p < np) {
-                    const int sg = col >> lgC;
-                    const int comp = (col >> lgP) & (ncomp - 1);
-                    T* dst = bbuf + (size_t)(p * ncomp + comp) * nes + (sg ? -mp : mp);
-                    // longitude quadrature and unpacking scale with the product's
-                    // coupling constant, and P^{-m} = (-1)^m P^m for negative m
-                    const T f = (comp == 0 ? sc_e : sc_v) * ((sg && (mp & 1)) ? (T)-1 : (T)1);
-                    const int tr0 = geo.tmin(mp, d) + 16 * rt;
-                    if constexpr (sizeof(T) == 4) {
-                        // rows tr, tr + 1, ... of this lane: entry 2 tr^2 + (2 d + 1) tr + d,
-                        // advancing by 4 tr + 2 d + 3
-                        const int tr = tr0 + 4 * rq;
-                        int e = 2 * tr * tr + (2 * d + 1) * tr + d, de = 4 * tr + 2 * d + 3;
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            if (tr + q < nrows) dst[e] = acc[s][q] * f;
-                            e += de;
-                            de += 4;
-                        }
-                    } else {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int tr = tr0 + acc_row<T>(rq, q);
-                            const int l3 = d + 2 * tr;
-                            if (l3 <= J) dst[acc_rowoff(tr, d) + l3] = acc[s][q] * f;
-                        }
-                    }
-                }
-            }
-        }
-    }
+    for (int s = 0; s < MT; ++s)
+        if (s < ntw) *reinterpret_cast<Acc*>(bbuf + (size_t)(wave + kWaves * s) * tile_stride<T>() + lane * 4) = acc[s];
     lds_barrier();
-    // output o of the block: (w0, w1, w2, idx); idx < 0 marks a scalar-scalar
-    // path whose accumulator entry is -idx - 1, else e = idx - 1 is the entry of
-    // (j3 - 1, m3) and the q = -1, 0, +1 terms sit at e + 1, e, e - 1 of
-    // components 2, 1, 3 (out-of-range terms carry zero weight).  Each
-    // coefficient is read once and applied to every pair of the tile.
     {
         const int nblk = n1 * n2;
         T* ob = out + p0 * nout + bd.out_off;
-        for (int o0 = tid; o0 < nblk; o0 += 2 * kThreads) {
-            Coef4 cf[2];
+        for (int o = tid; o < nblk; o += kThreads) {
+            const Coef4 cf = coef4[o];
+            const int4 ix = coefi[o];
+            const bool one = ix.w != 0;   // scalar-scalar or dot path: one term
+            // four pairs at a time (pair p's entries are 4 p further on)
+            for (int p0 = 0; p0 < np; p0 += 4) {
+                T v0[4], v1[4], v2[4];
 #pragma unroll
-            for (int k = 0; k < 2; ++k) cf[k] = coef4[min(o0 + k * kThreads, nblk - 1)];
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                const int o = o0 + k * kThreads;
-                if (o < nblk) {
-                    const int idx = (int)cf[k].w;
-                    const bool ss = idx < 0;
-                    const int e0 = ss ? -idx - 1 : 2 * nes + idx;
-                    const int e1 = ss ? 0 : nes + idx - 1;
-                    const int e2 = ss ? 0 : 3 * nes + idx - 2;
-                    // four pairs at a time: their gathers are in flight together
-                    for (int p0 = 0; p0 < np; p0 += 4) {
-                        T v0[4], v1[4], v2[4];
-#pragma unroll
-                        for (int u = 0; u < 4; ++u) {
-                            const T* bp = bbuf + (size_t)min(p0 + u, np - 1) * ncomp * nes;
-                            v0[u] = bp[e0];
-                            v1[u] = ss ? (T)0 : bp[e1];
-                            v2[u] = ss ? (T)0 : bp[e2];
-                        }
-#pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            if (p0 + u < np)
-                                ob[(size_t)(p0 + u) * nout + o] = cf[k].x * v0[u] + cf[k].y * v1[u] + cf[k].z * v2[u];
-                    }
+                for (int u = 0; u < 4; ++u) {
+                    const int po = 4 * min(p0 + u, np - 1);
+                    v0[u] = bbuf[ix.x + po];
+                    v1[u] = one ? (T)0 : bbuf[ix.y + po];
+                    v2[u] = one ? (T)0 : bbuf[ix.z + po];
                 }
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (p0 + u < np) ob[(size_t)(p0 + u) * nout + o] = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
             }
         }
     }

@@ -338,6 +338,7 @@ namespace {
 template <typename T>
 struct HostTables {
     std::vector<T> pbar, wtab, tw, lcg, coef;
+    std::vector<int32_t> coefi;
     std::vector<cgtp::TileDesc> tdesc;
 };
 
@@ -373,7 +374,7 @@ int lds_for(const BlockDesc& b, int pairs, int mode) {
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
     if (mode == cgtp::kModeStaged) o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
     o += csz * cgtp::kRingGroup * (pairs * nslot * FS + 8);   // 8: the ring skew
-    const int end_phase = stage + sz * pairs * ncomp * (acc_entries(b.d, b.J) | 1);
+    const int end_phase = stage + sz * block_tiles(b, pairs) * cgtp::tile_stride<T>();
     return std::max(o, end_phase);
 }
 
@@ -488,10 +489,8 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.rpad = wtab_rpad(b.R);
             b.wrow = wtab_rowlen(b.lmax, b.J & 1);
             b.wtab_off = grid_wtab_off[nt] + grid_wtab_par[nt][b.J & 1];
-            // per output (j3, m3): (w0, w1, w2, idx) with 1/K folded in.  Scalar-scalar
-            // paths: w0 = 1/K and idx = -(accumulator entry) - 1.  Cross paths:
-            // w_{q+1} = C^{j3 m3}_{j3-1, m3-q, 1, q} / K and idx = 1 + the entry of (j3 - 1, m3).
-            b.coef_off = (int)h.coef.size();
+            // 1/K of every path of the block (Theorem 4.2 for the cover's products)
+            std::vector<long double> kinv(b.J + 1, 0.0L);
             for (int j3 = b.d; j3 <= b.J; ++j3) {
                 long double K;
                 int kind;
@@ -501,21 +500,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                                      : ((b.products & cgtp::kEvenDot) ? cgtp::kDot : cgtp::kSS);
                 if (kind != want || fabsl(K) < kMinAbsK) return CGTP_EUNSUP;
                 min_abs_K = std::min(min_abs_K, (double)fabsl(K));
-                const long double kinv = 1.0L / K;
-                for (int m3 = -j3; m3 <= j3; ++m3) {
-                    if (!odd) {
-                        const int e = acc_rowoff_h((j3 - b.d) / 2, b.d) + j3 + m3;
-                        h.coef.push_back((T)kinv);
-                        h.coef.push_back((T)0);
-                        h.coef.push_back((T)0);
-                        h.coef.push_back((T)(-e - 1));
-                    } else {
-                        const int l3 = j3 - 1;
-                        for (int q = -1; q <= 1; ++q) h.coef.push_back((T)(kinv * cg_vec(l3, m3 - q, q, j3, m3)));
-                        // shifted by one: the q = 0 source of m3 = -(l3 + 1) sits at -1
-                        h.coef.push_back((T)(acc_rowoff_h((l3 - b.d) / 2, b.d) + l3 + m3 + 1));
-                    }
-                }
+                kinv[j3] = 1.0L / K;
             }
             b.out_off = path_offset(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
@@ -567,6 +552,71 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                             h.tdesc.push_back(t);
                         }
             }
+            // Output coefficients.  The end phase dumps MFMA tile u of the block
+            // verbatim at u * kTileStride; entry (row r, column c) of a tile sits at
+            // lane * 4 + q with the accumulator layout of the MFMA, and the columns of
+            // the pairs of one (sign, component) are consecutive, so pair p adds 4 p.
+            // Per output: up to three (weight, entry of pair 0) terms; the weights
+            // carry 1/K, the recombination coefficient, the longitude quadrature and
+            // unpacking scale, the product's coupling constant and (-1)^m for m < 0.
+            b.coef_off = (int)(h.coef.size() / 4);
+            {
+                cgtp::TileGeom geo{(b.J - b.d) / 2 + 1, ncomp, pairs};
+                const bool cross = b.kind == cgtp::kBlockCross;
+                const long double sc_s = 2.0L * kPi / b.Phi * (cross ? 0.25L : 1.0L);
+                const long double sc_v = sc_s * ((b.products & cgtp::kOddSV) ? 1.0L : (long double)p->cross_cg);
+                const long double sc_e = sc_s * ((b.products & cgtp::kEvenDot) ? (long double)p->dot_cg : 1.0L);
+                // tile index of (|m|, row tile, column tile), in enumeration order
+                std::vector<int> first_of_m(b.J + 2, 0);
+                for (int mp = 0; mp <= b.J; ++mp)
+                    first_of_m[mp + 1] = first_of_m[mp] + geo.nrt(mp, b.d) * geo.nct(mp);
+                auto entry = [&](int comp, int m, int tr, long double* f) {
+                    const int mp = std::abs(m), sg = m < 0 ? 1 : 0;
+                    const int row = tr - geo.tmin(mp, b.d), rt = row / 16, r = row % 16;
+                    const int col = sg * ncomp * pairs + comp * pairs, ct = col / 16, ci = col % 16;
+                    const int u = first_of_m[mp] + rt * geo.nct(mp) + ct;
+                    const int lin = sizeof(T) == 4 ? (ci + 16 * (r >> 2)) * 4 + (r & 3)
+                                                   : (ci + 16 * (r & 3)) * 4 + (r >> 2);
+                    *f = (comp == 0 ? sc_e : sc_v) * ((sg && (mp & 1)) ? -1.0L : 1.0L);
+                    return u * cgtp::tile_stride<T>() + lin;
+                };
+                for (int j3 = b.d; j3 <= b.J; ++j3) {
+                    const bool odd = (b.J + j3) & 1;
+                    for (int m3 = -j3; m3 <= j3; ++m3) {
+                        long double f;
+                        if (!odd) {
+                            const int e = entry(0, m3, (j3 - b.d) / 2, &f);
+                            h.coef.push_back((T)(kinv[j3] * f));
+                            h.coef.push_back((T)0);
+                            h.coef.push_back((T)0);
+                            h.coef.push_back((T)0);
+                            h.coefi.insert(h.coefi.end(), {e, e, e, 1});
+                        } else {
+                            // q = -1, 0, +1 from components 2, 1, 3 at (j3 - 1, m3 - q)
+                            const int l3 = j3 - 1, tr = (l3 - b.d) / 2;
+                            const int comp_of_q[3] = {2, 1, 3};
+                            long double w[3];
+                            int e[3], valid = -1;
+                            for (int k = 0; k < 3; ++k) {
+                                const int q = k - 1, m = m3 - q;
+                                w[k] = 0.0L;
+                                e[k] = -1;
+                                if (std::abs(m) <= l3) {
+                                    e[k] = entry(comp_of_q[k], m, tr, &f);
+                                    w[k] = kinv[j3] * cg_vec(l3, m, q, j3, m3) * f;
+                                    valid = e[k];
+                                }
+                            }
+                            for (int k = 0; k < 3; ++k) {
+                                if (e[k] < 0) e[k] = valid;   // zero weight; any entry of the block
+                                h.coef.push_back((T)w[k]);
+                            }
+                            h.coef.push_back((T)0);
+                            h.coefi.insert(h.coefi.end(), {e[0], e[1], e[2], 0});
+                        }
+                    }
+                }
+            }
             p->lds_bytes = std::max(p->lds_bytes, b.lds_bytes);
             blocks.push_back(b);
         }
@@ -608,9 +658,12 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     total = align_up(total + list.size() * sizeof(int32_t), 256);
     const size_t tdesc_off = total;
     total = align_up(total + h.tdesc.size() * sizeof(cgtp::TileDesc), 256);
+    const size_t coefi_off = total;
+    total = align_up(total + h.coefi.size() * sizeof(int32_t), 256);
     std::vector<char> host(total, 0);
     if (!h.tdesc.empty())
         std::memcpy(host.data() + tdesc_off, h.tdesc.data(), h.tdesc.size() * sizeof(cgtp::TileDesc));
+    if (!h.coefi.empty()) std::memcpy(host.data() + coefi_off, h.coefi.data(), h.coefi.size() * sizeof(int32_t));
     for (int i = 0; i < kParts; ++i)
         if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
     std::memcpy(host.data() + offs[kParts], blocks.data(), blocks.size() * sizeof(BlockDesc));
@@ -635,8 +688,7 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->tw = (const T*)(base + offs[2]);
     tb->lcg = (const T*)(base + offs[3]);
     tb->coef = (const T*)(base + offs[4]);
-    tb->cross_cg = (T)p->cross_cg;
-    tb->dot_cg = (T)p->dot_cg;
+    tb->coefi = (const int32_t*)(base + coefi_off);
     tb->wtab_len = (int32_t)h.wtab.size();
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
