@@ -352,10 +352,13 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // this wave's MFMA tiles: wave w owns w, w + kWaves, ...; per tile the LDS
     // byte address of the lane's B operand at ring 4 h + kq, h = 0
     const int ntw = bd.ntiles > wave ? (bd.ntiles - 1 - wave) / kWaves + 1 : 0;
+    // the tile whose operands slot s loads: the wave's own, or for slots past its
+    // last tile (and waves without tiles) a tile of the block, never out of range
+    auto tile_of = [&](int s) { return min(wave + kWaves * min(s, max(ntw - 1, 0)), bd.ntiles - 1); };
     int bx[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) {
-        const int bo = td[min(wave + kWaves * s, bd.ntiles - 1)].b_off;
+        const int bo = td[tile_of(s)].b_off;
         bx[s] = gather ? ly.fbuf + lane_b + (lane_sg ? (bo >> 16) : (bo & 0xffff)) * (int)sizeof(T)
                        : ly.stage + lane_b + bo * (int)sizeof(T);
     }
@@ -416,7 +419,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 #pragma unroll
             for (int s = 0; s < MT; ++s) {
                 if (s < ntw) {
-                    const int ax = tdl[wave + kWaves * s].x + lane_a;
+                    const int ax = tdl[tile_of(s)].x + lane_a;
 #pragma unroll
                     for (int h = 0; h < kRingGroup / 4; ++h)
                         apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
@@ -611,8 +614,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int hofs = h * 4 * (gather ? ly.per_r * (int)sizeof(C) : sc * sm * (int)sizeof(T));
                 T bv[MT];
 #pragma unroll
-                for (int s = 0; s < MT; ++s)
-                    if (s < ntw) bv[s] = *reinterpret_cast<const T*>(smem + bx[s] + hofs);
+                for (int s = 0; s < MT; ++s) bv[s] = *reinterpret_cast<const T*>(smem + bx[s] + hofs);
 #pragma unroll
                 for (int s = 0; s < MT; ++s)
                     if (s < ntw) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);

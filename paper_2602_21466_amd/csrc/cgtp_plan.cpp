@@ -564,8 +564,9 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                 cgtp::TileGeom geo{(b.J - b.d) / 2 + 1, ncomp, pairs};
                 const bool cross = b.kind == cgtp::kBlockCross;
                 const long double sc_s = 2.0L * kPi / b.Phi * (cross ? 0.25L : 1.0L);
-                const long double sc_v = sc_s * ((b.products & cgtp::kOddSV) ? 1.0L : (long double)p->cross_cg);
-                const long double sc_e = sc_s * ((b.products & cgtp::kEvenDot) ? (long double)p->dot_cg : 1.0L);
+                // coupling constants C^{1,1}_{1,1,1,0} (cross) and C^{0,0}_{1,1,1,-1} (dot)
+                const long double sc_v = sc_s * ((b.products & cgtp::kOddSV) ? 1.0L : cg_vec(1, 1, 0, 1, 1));
+                const long double sc_e = sc_s * ((b.products & cgtp::kEvenDot) ? cg_vec(1, 1, -1, 0, 0) : 1.0L);
                 // tile index of (|m|, row tile, column tile), in enumeration order
                 std::vector<int> first_of_m(b.J + 2, 0);
                 for (int mp = 0; mp <= b.J; ++mp)
