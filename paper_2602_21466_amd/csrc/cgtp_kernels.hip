@@ -615,9 +615,12 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 T bv[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) bv[s] = *reinterpret_cast<const T*>(smem + bx[s] + hofs);
+                // a quad of rings wholly past the grid's last ring adds nothing
+                if (h == 0 || rg0 + 4 < R) {
 #pragma unroll
-                for (int s = 0; s < MT; ++s)
-                    if (s < ntw) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);
+                    for (int s = 0; s < MT; ++s)
+                        if (s < ntw) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);
+                }
             }
         }
         lds_barrier();
