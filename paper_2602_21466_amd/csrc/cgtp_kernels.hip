@@ -219,7 +219,7 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 constexpr int kRingSkew = 8;
 
 struct Layout {
-    int lc, pst, tw2, tdl, lc2, stage, fbuf, bbuf;   // byte offsets
+    int lc, prn, tw2, tdl, cvn, stage, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
     int per_r;                                       // complex entries per ring
 };
@@ -237,10 +237,10 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     const int P = b.pairs, n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     int o = 0;
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
-    l.pst = o; o = align16(o + (int)sizeof(T) * b.R * (b.j1 + 1 + b.j2 + 1));
+    l.prn = o; o = align16(o + (int)sizeof(T) * b.R * 2 * A * B);
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.tdl = o; o = align16(o + 8 * b.ntiles);
-    l.lc2 = o; o = align16(o + (int)sizeof(C) * P * 2 * (n1 + n2));
+    l.cvn = o; o = align16(o + (int)sizeof(C) * P * nslot * A * B);
     l.stage = o;
     if (b.mode == kModeStaged) o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
     l.per_rp = nslot * FS;
@@ -292,11 +292,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 
     const Layout ly = make_layout<T, A, B>(bd, nslot);
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
-    T* pst = reinterpret_cast<T*>(smem + ly.pst);        // [ring][j1+1] then [ring][j2+1], all rings
+    T* prn = reinterpret_cast<T*>(smem + ly.prn);        // [ring][input][longitude n]: P_j^|m(n)|, zero for |m| > j
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
 
-    C* lc2 = reinterpret_cast<C*>(smem + ly.lc2);        // per pair: lifted coefficients, two series each
+    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [pair][slot][longitude n]: lifted coefficients, two series
     T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
     T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // MFMA tiles, end phase only
@@ -317,11 +317,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
         for (int e = tid; e < FS; e += kThreads) tw2[e] = tw[e];
     }
-    const int npr = j1 + 1 + j2 + 1;
-    for (int e = tid; e < R * npr; e += kThreads) {
-        const int r = e / npr, q = e - r * npr;
-        const T* prow = tb.pbar + bd.pbar_off + (size_t)r * bd.pbar_stride;
-        pst[e] = q <= j1 ? prow[j1 * (j1 + 1) / 2 + q] : prow[j2 * (j2 + 1) / 2 + (q - j1 - 1)];
+    // Legendre rows of every ring in longitude order: entry n of (ring, input j)
+    // is P_j^|m| at the order m = n or n - Phi that longitude index n carries in
+    // the synthesis, zero for |m| > j (Phi > 2 j, so n <= Phi / 2 gives m = n)
+    for (int e = tid; e < R * 2 * Phi; e += kThreads) {
+        const int ri = e / Phi, n = e - ri * Phi;
+        const int j = (ri & 1) ? j2 : j1;
+        const int m = n <= Phi / 2 ? n : n - Phi, am = m < 0 ? -m : m;
+        const T* prow = tb.pbar + bd.pbar_off + (size_t)(ri >> 1) * bd.pbar_stride;
+        prn[e] = am <= j ? prow[j * (j + 1) / 2 + am] : (T)0;
     }
 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
@@ -377,30 +381,35 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
     const int np = (int)((N - p0) < P ? (N - p0) : P);
-    // ---- ring-independent lifted coefficients of the tile (rows past N are zero):
-    //   series pair 0: (x_m, C^{j, m}_{j, m, 1, 0} x_m)            scalar and q = 0
-    //   series pair 1: (C^{j,m-1}_{j,m,1,-1} x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1})   q = -1, +1
-    // for orbital order m; scalar blocks use (x_m, 0) only.
-    for (int e = tid; e < P * (n1 + n2); e += kThreads) {
-        const int p = e / (n1 + n2), q = e - p * (n1 + n2);
-        const bool first = q < n1;
-        const int j = first ? j1 : j2, nj = 2 * j + 1, mj = first ? q : q - n1;   // mj = m + j
-        const T* xg = first ? x1 : x2;
-        const int64_t row = (p0 + p) * nin + j * j;
-        const bool ok = p < np;
-        const T xm = ok ? xg[row + mj] : (T)0;
-        const T* lcj = first ? lc : lc + 3 * n1;
-        C* dst = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1);
-        // P^{-m} = (-1)^m P^m: the sign of negative odd orbital orders goes here
-        const T sg = (mj < j && ((j - mj) & 1)) ? (T)-1 : (T)1;
-        if (!cross) {
-            dst[mj] = cmk<C>(sg * xm, (T)0);
-        } else {
-            const T xlo = (ok && mj >= 1) ? xg[row + mj - 1] : (T)0;
-            const T xhi = (ok && mj + 1 < nj) ? xg[row + mj + 1] : (T)0;
-            dst[mj] = cmk<C>(sg * xm, sg * lcj[nj + mj] * xm);
-            dst[nj + mj] = cmk<C>(sg * lcj[mj] * xlo, sg * lcj[2 * nj + mj] * xhi);
+    // ---- ring-independent lifted coefficients of the tile in longitude order
+    // (zero for |m| > j and for rows past N), per slot:
+    //   even slot: (x_m, C^{j, m}_{j, m, 1, 0} x_m)                          scalar and q = 0
+    //   odd slot:  (C^{j,m-1}_{j,m,1,-1} x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1})   q = -1, +1
+    // for orbital order m, times (-1)^m for negative m (P^{-m} = (-1)^m P^m);
+    // scalar blocks use (x_m, 0) only.
+    for (int e = tid; e < (P << lgS) * Phi; e += kThreads) {
+        const int ps = e / Phi, n = e - ps * Phi;
+        const int p = ps >> lgS, s = ps & (nslot - 1);
+        const bool first = cross ? (s < 2) : (s == 0);
+        const int j = first ? j1 : j2, nj = 2 * j + 1;
+        const int m = n <= Phi / 2 ? n : n - Phi, am = m < 0 ? -m : m;
+        C val = cmk<C>((T)0, (T)0);
+        if (am <= j && p < np) {
+            const int mj = m + j;
+            const T* xg = first ? x1 : x2;
+            const int64_t row = (p0 + p) * nin + j * j;
+            const T* lcj = first ? lc : lc + 3 * n1;
+            const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
+            if (!cross || (s & 1) == 0) {
+                const T xm = sg * xg[row + mj];
+                val = cmk<C>(xm, cross ? lcj[nj + mj] * xm : (T)0);
+            } else {
+                const T xlo = mj >= 1 ? xg[row + mj - 1] : (T)0;
+                const T xhi = mj + 1 < nj ? xg[row + mj + 1] : (T)0;
+                val = cmk<C>(sg * lcj[mj] * xlo, sg * lcj[2 * nj + mj] * xhi);
+            }
         }
+        cvn[e] = val;
     }
     if (!gather)
         for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
@@ -443,19 +452,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const int rp = wave + kWaves * (f >> lgS);
                 const int p = rp & (P - 1), r = rp >> lgP;
                 const bool first = cross ? (s < 2) : (s == 0);
-                const int j = first ? j1 : j2;
-                const int nj = 2 * j + 1;
-                const C* cv = lc2 + (size_t)p * 2 * (n1 + n2) + (first ? 0 : 2 * n1) + (cross ? (s & 1) * nj : 0) + j;
-                const T* pr = pst + (rg0 + r) * npr + (first ? 0 : j1 + 1);
-                // orders outside -j..j read order 0 and are zeroed
+                // inputs n = t + A n2i: both factors in longitude order, read at
+                // constant offsets from the task's first element
+                const C* cv = cvn + (size_t)((p << lgS) + s) * Phi + t;
+                const T* pr = prn + (size_t)(((rg0 + r) << 1) + (first ? 0 : 1)) * Phi + t;
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {
-                    const int n = t + A * n2i;
-                    const bool ok = n <= j || n >= Phi - j;
-                    const int m = ok ? (n <= j ? n : n - Phi) : 0;
-                    const T pv = ok ? pr[m < 0 ? -m : m] : (T)0;
-                    const C c = cv[m];
+                    const C c = cv[A * n2i];
+                    const T pv = pr[A * n2i];
                     v[n2i] = cmk<C>(c.x * pv, c.y * pv);
                 }
                 Dft<B, true, C>::run(v);

@@ -365,11 +365,10 @@ int lds_for(const BlockDesc& b, int pairs, int mode) {
     const int FS = b.A * (b.B + 1);
     int o = 0;
     o = align16h(o + sz * 3 * (n1 + n2));
-    o = align16h(o + sz * b.R * (b.j1 + 1 + b.j2 + 1));
+    o = align16h(o + sz * b.R * 2 * b.Phi);
     o = align16h(o + csz * FS);
     o = align16h(o + 8 * block_tiles(b, pairs));
-    o = align16h(o + 4 * block_tiles(b, pairs));
-    o = align16h(o + csz * pairs * 2 * (n1 + n2));
+    o = align16h(o + csz * pairs * nslot * b.Phi);
     const int stage = o;
     const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
     if (mode == cgtp::kModeStaged) o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
