@@ -8,7 +8,7 @@
 
 namespace cgtp {
 
-constexpr int kThreads = 512;      // work-group size of the block kernel (8 wave64s, one per CU)
+constexpr int kThreads = 768;      // work-group size of the block kernel (12 wave64s, one per CU)
 constexpr int kWaves = kThreads / 64;
 constexpr int kRingGroup = 8;      // rings per pass: two K = 4 steps of a 16x16x4 MFMA
 constexpr int kLdsBudget = 156 * 1024;
@@ -16,8 +16,8 @@ constexpr int kMaxPairs = 16;
 
 // MFMA accumulator tiles (16 x 16) each wave may hold, per precision.
 template <typename T> struct MaxTiles;
-template <> struct MaxTiles<float> { static constexpr int value = 14; };
-template <> struct MaxTiles<double> { static constexpr int value = 6; };
+template <> struct MaxTiles<float> { static constexpr int value = 10; };
+template <> struct MaxTiles<double> { static constexpr int value = 4; };
 
 // Product kinds per path (mirrors cgtp_path_norm's *kind).
 enum PathKind : int32_t { kSS = 0, kCross = 1, kSV = 2, kDot = 3 };
