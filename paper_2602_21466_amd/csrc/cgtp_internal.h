@@ -128,7 +128,7 @@ inline bool fft_factors(int phi, int* A, int* B) {
                                  {8, 4, 2},    {9, 3, 3},    {12, 4, 3},   {16, 4, 4},   {18, 6, 3},
                                  {24, 6, 4},   {27, 9, 3},   {32, 8, 4},   {36, 6, 6},   {48, 8, 6},
                                  {54, 9, 6},   {64, 8, 8},   {72, 9, 8},   {81, 9, 9},   {96, 12, 8},
-                                 {108, 12, 9}, {128, 8, 16}, {144, 12, 12}};
+                                 {108, 12, 9}, {128, 16, 8}, {144, 12, 12}};
     for (const auto& r : tab)
         if (r[0] == phi) {
             *A = r[1];

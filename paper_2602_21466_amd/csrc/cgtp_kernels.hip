@@ -707,7 +707,7 @@ __global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const 
         CGTP_CASE(81, 9, 9)
         CGTP_CASE(96, 12, 8)
         CGTP_CASE(108, 12, 9)
-        CGTP_CASE(128, 8, 16)
+        CGTP_CASE(128, 16, 8)
         CGTP_CASE(144, 12, 12)
         default: break;
     }
