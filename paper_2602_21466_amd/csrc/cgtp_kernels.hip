@@ -421,21 +421,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 
     for (int rg0 = 0; rg0 < R; rg0 += kRingGroup) {
         const int nrg = (R - rg0) < kRingGroup ? (R - rg0) : kRingGroup;
-        // the group's MFMA weights (operand A) are fetched now and land while the
-        // transforms run
-        T apre[kRingGroup / 4][MT];
-        {
-#pragma unroll
-            for (int s = 0; s < MT; ++s) {
-                if (s < ntw) {
-                    const int ax = tdl[tile_of(s)].x + lane_a;
-#pragma unroll
-                    for (int h = 0; h < kRingGroup / 4; ++h)
-                        apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
-                }
-            }
-        }
-
         // Phases 1 to 4 work on (ring, pair) units; wave w owns units w, w + kWaves,
         // ... and takes each of them through synthesis, products and analysis, so
         // between these phases only its own LDS accesses need ordering.
@@ -571,6 +556,19 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         wave_lds_sync();
+        // the group's MFMA weights (operand A) are fetched now and land during the
+        // last transform pass (fetched earlier they would hold registers through
+        // the register peak of the row passes)
+        T apre[kRingGroup / 4][MT];
+#pragma unroll
+        for (int s = 0; s < MT; ++s) {
+            if (s < ntw) {
+                const int ax = tdl[tile_of(s)].x + lane_a;
+#pragma unroll
+                for (int h = 0; h < kRingGroup / 4; ++h)
+                    apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
+            }
+        }
         // ---- 4b. analysis pass 2: in place (gather mode) or staged as |m| <= J
         {
             const int ntask = (uw << lgZ) * B;
