@@ -30,9 +30,9 @@ PEAK_HBM_GBS = 8000.0
 # (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "a423c83f7e88baf5": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 343956.0, "fetch_scale": 1.999956, "write_kib": 4773997.5, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 202966.0, "fetch_scale": 1.999956, "write_kib": 2739396.2, "write_scale": 1.000000},
+    "61e61073754f0f9b": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 344781.2, "fetch_scale": 1.999956, "write_kib": 4936443.3, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 203985.7, "fetch_scale": 1.999956, "write_kib": 2742202.7, "write_scale": 1.000000},
     },
 }
 
