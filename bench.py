@@ -108,7 +108,8 @@ def roofline(res):
             "frac": round(achieved / peak, 4), "traffic": traffic,
             "flops_per_launch": flops, "compulsory_bytes_per_launch": int(compulsory),
             "hbm_gbs_compulsory": round(hbm, 1), "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4),
-            "avg_launch_ms": round(res["avg_launch_ms"], 4), "kernel_digest": kernel_digest()}
+            "avg_launch_ms": round(res["avg_launch_ms"], 4), "median_launch_ms": round(res["median_launch_ms"], 4),
+            "kernel_digest": kernel_digest()}
 
 
 def copy_probe(nbytes, reps=10):
@@ -131,7 +132,18 @@ def copy_probe(nbytes, reps=10):
                       "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}), flush=True)
 
 
-def cpu_baseline(w, budget_s):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, budget_s, budget_1t_s=5.0):
     import numpy as np
 
     import cgtp_inputs
@@ -149,10 +161,20 @@ def cpu_baseline(w, budget_s):
     t0 = time.perf_counter()
     oracle.cgtp(w.L, a[:k], b[:k])
     dt = time.perf_counter() - t0
-    return {"value": round(k / dt, 4), "unit": "pairs/s", "cores": oracle.max_threads(), "kind": "oracle",
+    cores = oracle.max_threads()
+    # one thread, on a smaller sample (the thread count persists, so this runs last)
+    t0 = time.perf_counter()
+    oracle.cgtp(w.L, a[:1], b[:1], threads=1)
+    t1s = max(time.perf_counter() - t0, 1e-6)
+    k1 = int(max(1, min(w.N, budget_1t_s / t1s)))
+    t0 = time.perf_counter()
+    oracle.cgtp(w.L, a[:k1], b[:k1], threads=1)
+    dt1 = time.perf_counter() - t0
+    return {"value": round(k / dt, 4), "unit": "pairs/s", "cores": cores, "kind": "oracle",
             "sample": "first %d of the %d pairs of %s (naive O(L^6) fp64 oracle, OpenMP over pairs x l1; "
                       "coefficient table built beforehand in %.2f s, not timed)" % (k, w.N, w.name, table_s),
-            "seconds": round(dt, 2)}
+            "seconds": round(dt, 2), "value_1_thread": round(k1 / dt1, 4), "sample_1_thread": "first %d pairs" % k1,
+            "host_cpu": cpu_model(), "host_threads": os.cpu_count()}
 
 
 def main():
