@@ -90,9 +90,10 @@ typedef struct cgtp_plan_s *cgtp_plan_t;
  * normalised associated Legendre tables, Clebsch-Gordan tables for the lifts
  * and the recombination, and 1/K for every path (Theorem 4.2), uploaded to
  * device memory the plan owns.  grid == NULL takes every default.
- * Returns CGTP_EINVAL (L < 0, plan_out NULL), CGTP_EUNSUP (L > CGTP_MAX_L),
- * CGTP_EDTYPE, CGTP_EGRID, CGTP_ENOMEM or CGTP_EHIP; *plan_out is set only on
- * success.  Not timed work: call once per (L, grid).
+ * Returns CGTP_EINVAL (L < 0, plan_out NULL), CGTP_EUNSUP (L > CGTP_MAX_L,
+ * or a block whose projection accumulators do not fit one work-group: fp64
+ * plans support L <= 19), CGTP_EDTYPE, CGTP_EGRID, CGTP_ENOMEM or CGTP_EHIP;
+ * *plan_out is set only on success.  Not timed work: call once per (L, grid).
  */
 int cgtp_plan(int32_t L, const cgtp_grid *grid, cgtp_plan_t *plan_out);
 

@@ -155,6 +155,27 @@ def test_alternate_cover_parity(L, N, dtype):
     assert err <= 2 * TOL[dtype], (err, path)
 
 
+def test_fp64_size_limit():
+    """fp64 plans hold fewer accumulator tiles per work-group: the largest degree that
+    fits plans and passes parity; one more is refused cleanly with CGTP_EUNSUP."""
+    _torch()
+    lib = _lib()
+    largest = None
+    for L in range(16, 33):
+        try:
+            plan = lib.Plan(L, dtype="fp64")
+        except lib.CgtpError as e:
+            assert e.code == lib.CGTP_EUNSUP, e.code
+            break
+        plan.close()
+        largest = L
+    print("largest fp64 degree: %s" % largest, flush=True)
+    assert largest is not None and largest >= 19
+    x1, x2 = wl.draw(largest, 3, "fp64", seed=1000 + largest)
+    _, _, _, out = run_gpu(largest, x1, x2, "fp64")
+    check_against_oracle(largest, x1, x2, out.double().cpu().numpy(), "fp64")
+
+
 def test_zero_pairs_launches_nothing():
     torch = _torch()
     lib = _lib()
