@@ -106,7 +106,8 @@ int cgtp_plan(int32_t L, const cgtp_grid *grid, cgtp_plan_t *plan_out);
  * this call allocates nothing.  x1 == x2 is allowed; out overlapping an input
  * is CGTP_EINVAL.  N == 0 returns CGTP_OK with no launch.  Launch failures
  * return CGTP_EHIP; faults during execution surface when the caller
- * synchronises.  A plan may be used from several streams at once.
+ * synchronises.  A plan may be used from several streams at once.  The
+ * current device must be the one the plan was built on (else CGTP_EINVAL).
  */
 int cgtp_forward(cgtp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N,
                  void *hip_stream);

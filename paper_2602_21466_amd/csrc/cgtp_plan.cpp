@@ -854,6 +854,14 @@ int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, in
     if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
     const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
     if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin)) return CGTP_EINVAL;
+    // the plan's tables live on the device current when it was built
+    int dev = -1;
+    const hipError_t de = hipGetDevice(&dev);
+    if (de != hipSuccess) {
+        g_last_hip_error = (int)de;
+        return CGTP_EHIP;
+    }
+    if (dev != plan->device) return CGTP_EINVAL;
     cgtp::LaunchMap map{};
     map.ncls = (int32_t)plan->classes.size();
     map.cum[0] = 0;
