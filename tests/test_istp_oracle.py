@@ -1,0 +1,181 @@
+"""Pins for the MIMO irrep-signal product oracle (no GPU needed).
+
+The oracle (``oracle.istp``) works on coefficients.  These tests tie it to
+things computed another way:
+* direct quadrature, on an exact sphere grid, of products of scipy's
+  spherical harmonics and of tensor harmonics built from them with sympy's
+  exact Clebsch-Gordan values (Definition 4.1);
+* Theorem 4.2 with sympy's 9j symbol;
+* a closed form for a constant first input;
+* rotation equivariance with Wigner matrices fitted from scipy's harmonics;
+* the vector selection rule of Theorem 5.1.
+A wrong sign, index or operand order in any of the oracle's three steps
+fails the quadrature tests.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle.istp as oi
+from test_oracle import _quadrature_grid, _sph_harm, _wigner_D
+from test_plan import _tsh
+
+
+def _sympy_cg(j1, m1, j2, m2, j, m):
+    from sympy.physics.wigner import clebsch_gordan
+    return float(clebsch_gordan(j1, j2, j, m1, m2, m))
+
+
+def test_layout():
+    for L in range(5):
+        labels = oi.vector_labels(L)
+        offs = [oi.vector_offset(j, l) for j, l in labels]
+        sizes = [2 * j + 1 for j, l in labels]
+        assert offs == list(np.cumsum([0] + sizes[:-1]))
+        assert sum(sizes) == oi.vector_size(L) == 3 * (L + 1) ** 2
+    with pytest.raises(ValueError):
+        oi.vector_offset(0, 0)
+    with pytest.raises(ValueError):
+        oi.vector_offset(3, 1)
+
+
+def test_gaunt_product_against_quadrature(rng):
+    """z[l3, m3] = integral of f1 f2 conj(Y_l3^m3) for f_i = sum x_i Y (scipy harmonics, exact grid)."""
+    L = 3
+    x1 = rng.standard_normal(oi.gaunt_size(L))
+    x2 = rng.standard_normal(oi.gaunt_size(L))
+    z = oi.gaunt_tp(L, x1, x2)[0]
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+    Y = {(l, m): _sph_harm(l, m, T, P) for l in range(2 * L + 1) for m in range(-l, l + 1)}
+    f1 = sum(x1[l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
+    f2 = sum(x2[l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
+    want = np.array([(W * f1 * f2 * np.conj(Y[l, m])).sum() for l in range(2 * L + 1) for m in range(-l, l + 1)])
+    assert np.abs(want.imag).max() < 1e-12
+    np.testing.assert_allclose(z, want.real, atol=1e-12)
+
+
+def _vector_signal(L, x, T, P):
+    """Spherical components q = -1, 0, +1 of sum_{j,l,m} x^(j,l)_m Y^{l,1}_{j,m} on the grid."""
+    f = [np.zeros(T.shape, complex) for _ in range(3)]
+    for j, l in oi.vector_labels(L):
+        o = oi.vector_offset(j, l)
+        for m in range(-j, j + 1):
+            comps = _tsh(l, 1, j, m, T, P)
+            for k in range(3):
+                f[k] = f[k] + x[o + j + m] * comps[k]
+    return f
+
+
+@pytest.mark.parametrize("L", [1, 2])
+def test_vector_product_against_quadrature(L, rng):
+    """Every output against the integral of conj(Y^{l3,1}_{j3,m3}) . (f1 (x) f2)^(1) (Definition 4.1, Section 4.3)."""
+    x1 = rng.standard_normal(oi.vector_size(L))
+    x2 = rng.standard_normal(oi.vector_size(L))
+    z = oi.vector_tp(L, x1, x2)[0]
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+    f1 = _vector_signal(L, x1, T, P)
+    f2 = _vector_signal(L, x2, T, P)
+    g = []
+    for q in (-1, 0, 1):
+        acc = np.zeros(T.shape, complex)
+        for q1 in (-1, 0, 1):
+            q2 = q - q1
+            if abs(q2) <= 1:
+                acc = acc + _sympy_cg(1, q1, 1, q2, 1, q) * f1[q1 + 1] * f2[q2 + 1]
+        g.append(acc)
+    want = np.zeros(oi.vector_size(2 * L), complex)
+    for j3, l3 in oi.vector_labels(2 * L):
+        o = oi.vector_offset(j3, l3)
+        for m3 in range(-j3, j3 + 1):
+            basis = _tsh(l3, 1, j3, m3, T, P)
+            want[o + j3 + m3] = sum((W * g[k] * np.conj(basis[k])).sum() for k in range(3))
+    assert np.abs(want.imag).max() < 1e-12
+    np.testing.assert_allclose(z, want.real, atol=1e-12)
+
+
+def test_vector_product_theorem_4_2(rng):
+    """Output label (j3, l3) = sum over input labels of K (x1^(j1,l1) (x) x2^(j2,l2))^(j3), K from Theorem 4.2 (sympy 9j)."""
+    from sympy.physics.wigner import wigner_9j
+    L = 2
+    x1 = rng.standard_normal(oi.vector_size(L))
+    x2 = rng.standard_normal(oi.vector_size(L))
+    z = oi.vector_tp(L, x1, x2)[0]
+    want = np.zeros_like(z)
+    for j1, l1 in oi.vector_labels(L):
+        for j2, l2 in oi.vector_labels(L):
+            for j3, l3 in oi.vector_labels(2 * L):
+                if not (abs(j1 - j2) <= j3 <= j1 + j2 and abs(l1 - l2) <= l3 <= l1 + l2) or (l1 + l2 + l3) & 1:
+                    continue
+                c0 = _sympy_cg(l1, 0, l2, 0, l3, 0)
+                nj = float(wigner_9j(j1, l1, 1, j2, l2, 1, j3, l3, 1, prec=30))
+                K = math.sqrt((2 * j1 + 1) * (2 * j2 + 1) * (2 * l1 + 1) * (2 * l2 + 1) * 3 / (4 * math.pi)) * nj * c0
+                if K == 0.0:
+                    continue
+                a = x1[oi.vector_offset(j1, l1):][: 2 * j1 + 1]
+                b = x2[oi.vector_offset(j2, l2):][: 2 * j2 + 1]
+                o = oi.vector_offset(j3, l3)
+                for m3 in range(-j3, j3 + 1):
+                    s = sum(_sympy_cg(j1, m1, j2, m3 - m1, j3, m3) * a[j1 + m1] * b[j2 + m3 - m1]
+                            for m1 in range(-j1, j1 + 1) if abs(m3 - m1) <= j2)
+                    want[o + j3 + m3] += K * s
+    np.testing.assert_allclose(z, want, atol=1e-12)
+
+
+def test_gaunt_product_constant_input(rng):
+    """f1 = c Y_0^0 = c / sqrt(4 pi) constant: z = c x2 / sqrt(4 pi) up to degree L, zero above."""
+    L = 4
+    x1 = np.zeros(oi.gaunt_size(L))
+    x1[0] = 1.7
+    x2 = rng.standard_normal(oi.gaunt_size(L))
+    z = oi.gaunt_tp(L, x1, x2)[0]
+    np.testing.assert_allclose(z[: (L + 1) ** 2], 1.7 / math.sqrt(4 * math.pi) * x2, atol=1e-14)
+    np.testing.assert_allclose(z[(L + 1) ** 2:], 0.0, atol=1e-14)
+
+
+def _complex(fn, L, x1, x2):
+    """A bilinear real product applied to complex inputs."""
+    rr = fn(L, x1.real, x2.real)
+    ii = fn(L, x1.imag, x2.imag)
+    ri = fn(L, x1.real, x2.imag)
+    ir = fn(L, x1.imag, x2.real)
+    return (rr - ii) + 1j * (ri + ir)
+
+
+def test_vector_product_rotation_equivariance(rng):
+    """Rotating both inputs (label (j, l) by D^j) rotates each output label (j3, l3) by D^{j3}."""
+    from scipy.spatial.transform import Rotation
+    L = 2
+    R = Rotation.random(random_state=int(rng.integers(1 << 30)))
+    D = {j: _wigner_D(j, R, rng) for j in range(2 * L + 2)}
+
+    def rot(x, Lx):
+        y = np.array(x, dtype=complex)
+        for j, l in oi.vector_labels(Lx):
+            o = oi.vector_offset(j, l)
+            y[..., o: o + 2 * j + 1] = x[..., o: o + 2 * j + 1] @ D[j].T
+        return y
+
+    x1 = rng.standard_normal((2, oi.vector_size(L))).astype(complex)
+    x2 = rng.standard_normal((2, oi.vector_size(L))).astype(complex)
+    z = _complex(oi.vector_tp, L, x1, x2)
+    zr = _complex(oi.vector_tp, L, rot(x1, L), rot(x2, L))
+    np.testing.assert_allclose(zr, rot(z, 2 * L), atol=1e-10)
+
+
+def test_vector_selection_rule():
+    """Theorem 5.1 for labels (1,1) x (1,1): (j3, l3) = (2, 2) vanishes by rule 5, (1, 1), (2, 1), (0, 1) by rule 4."""
+    L = 1
+    x = np.zeros(oi.vector_size(L))
+    o = oi.vector_offset(1, 1)
+    rng = np.random.default_rng(5)
+    x[o: o + 3] = rng.standard_normal(3)
+    y = np.zeros(oi.vector_size(L))
+    y[o: o + 3] = rng.standard_normal(3)
+    z = oi.vector_tp(L, x, y)[0]
+    for j3, l3, zero in [(2, 2, True), (1, 1, True), (2, 1, True), (0, 1, True), (1, 2, False), (1, 0, False)]:
+        blk = z[oi.vector_offset(j3, l3):][: 2 * j3 + 1]
+        if zero:
+            np.testing.assert_allclose(blk, 0.0, atol=1e-14)
+        else:
+            assert np.abs(blk).max() > 1e-3, (j3, l3)
