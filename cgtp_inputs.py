@@ -74,6 +74,57 @@ def draw(L: int, N: int, dtype: str = "fp32", scaled: bool = False, seed: int | 
     return x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype))
 
 
+def draw_rows(ncols: int, N: int, dtype: str = "fp32", seed: int = 0):
+    """Returns (x1, x2) as CPU torch tensors [N, ncols]: iid N(0, 1) in float64, then cast."""
+    import torch
+    g = torch.Generator("cpu").manual_seed(seed)
+    x1 = torch.randn(N, ncols, dtype=torch.float64, generator=g)
+    x2 = torch.randn(N, ncols, dtype=torch.float64, generator=g)
+    return x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype))
+
+
+# Multiple-input, multiple-output signal products: spin 0 (Gaunt) rows hold
+# (L+1)^2 values, spin 1 (vector) rows 3 (L+1)^2; same recipe as above
+# (seed L + 100 spin), checked on a seeded subsample of pairs.
+@dataclass(frozen=True)
+class IstpWorkload:
+    name: str
+    L: int
+    spin: int
+    N: int
+    dtype: str
+    check_pairs: int
+
+    @property
+    def seed(self) -> int:
+        return self.L + 100 * self.spin
+
+    @property
+    def n_coeffs(self) -> int:
+        return (2 * self.spin + 1) * (self.L + 1) ** 2
+
+    @property
+    def n_outputs(self) -> int:
+        return (2 * self.spin + 1) * (2 * self.L + 1) ** 2
+
+
+ISTP_WORKLOADS = [
+    IstpWorkload("vstp_L32_N16384_fp32", 32, 1, 16_384, "fp32", 4),
+    IstpWorkload("gtp_L32_N65536_fp32", 32, 0, 65_536, "fp32", 8),
+    IstpWorkload("vstp_L16_N65536_fp32", 16, 1, 65_536, "fp32", 16),
+]
+
+
+def istp_inputs(w: IstpWorkload):
+    return draw_rows(w.n_coeffs, w.N, w.dtype, w.seed)
+
+
+def istp_check_indices(w: IstpWorkload):
+    import torch
+    g = torch.Generator("cpu").manual_seed(w.seed + 1)
+    return torch.sort(torch.randperm(w.N, generator=g)[: w.check_pairs]).values
+
+
 def workload_inputs(w: Workload):
     return draw(w.L, w.N, w.dtype, w.scaled, w.seed)
 

@@ -1,0 +1,128 @@
+/*
+ * istp.h: C ABI of the multiple-input, multiple-output irrep-signal tensor
+ * products (arXiv 2602.21466, Section 4.3 and Appendix D) on MI355X (gfx950).
+ *
+ * Two products of two feature rows x1, x2, each the (s, s, s) case of the
+ * irrep-signal tensor product with every input irrep lifted into one signal
+ * and every output irrep read back from the one pointwise product:
+ *
+ *   ISTP_GAUNT  (s = 0, the Gaunt tensor product, Section 3.3).  A row holds
+ *               one copy of each degree l = 0..L at index l^2 + l + m
+ *               ((L+1)^2 values).  The output row holds degrees 0..2L at
+ *               l^2 + l + m ((2L+1)^2 values): the integral over the sphere
+ *               of f1 f2 conj(Y_l^m) with f_i = sum_lm x_i[l^2+l+m] Y_l^m.
+ *
+ *   ISTP_VECTOR (s = 1, the vector signal tensor product, Section 5).  A row
+ *               holds the coefficients of the tensor harmonics Y^{l,1}_{j,m}
+ *               of Definition 4.1 for the labels (j, l), l = 0..L,
+ *               j = l-1, l, l+1 (j >= 0; for l = 0 only j = 1), ordered by l,
+ *               then j, then m = -j..j: label (j, l) starts at
+ *               istp_label_offset(1, j, l) = 3 l^2 + {0, 2l-1, 4l}[j-l+1]
+ *               (3 (L+1)^2 values).  The output row holds the coefficients, in
+ *               the same basis and order up to l = 2L (3 (2L+1)^2 values), of
+ *               the 1 (x) 1 -> 1 coupled pointwise product
+ *               g_q = sum C^{1 q}_{1 q1 1 q2} f1_q1 f2_q2 of the two vector
+ *               signals f_i = sum x_i^{(j,l)}_m Y^{l,1}_{j,m}.
+ *
+ * Basis: complex spherical harmonics with the Condon-Shortley phase; inputs
+ * and outputs are real.  By Theorem 4.2 each output label (j3, l3) of the
+ * vector product is a sum over input label pairs of K times the CGTP path
+ * (x1^{(j1,l1)} (x) x2^{(j2,l2)})^{(j3)}.
+ *
+ * The result is computed the paper's way on an exact grid: lift (Legendre
+ * synthesis on MFMA, then longitude FFTs), pointwise product, longitude FFTs,
+ * Legendre projection on MFMA, recombination.  Grid: n_theta = 2L + 2
+ * Gauss-Legendre rings, n_phi = smallest 2^a 3^b >= 4L + 1 longitudes, exact
+ * for every output.
+ *
+ * Status codes are those of cgtp.h (CGTP_OK, CGTP_EINVAL, ...), and
+ * cgtp_strerror / cgtp_last_hip_error apply.
+ */
+#ifndef ISTP_H
+#define ISTP_H
+
+#include <stdint.h>
+
+#include "cgtp.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct istp_plan_s *istp_plan_t;
+
+enum { ISTP_GAUNT = 0, ISTP_VECTOR = 1 };
+
+/* Largest L: the projection accumulators must fit the register file. */
+#define ISTP_MAX_L_FP32 33
+#define ISTP_MAX_L_FP64 12
+
+/*
+ * Builds the grid, the MFMA weight tables and the recombination table on the
+ * current HIP device and uploads them (device memory owned by the plan).
+ *   L     >= 0 (CGTP_EINVAL below; CGTP_EUNSUP above the limits above)
+ *   spin  ISTP_GAUNT or ISTP_VECTOR (else CGTP_EINVAL)
+ *   dtype CGTP_FP32 or CGTP_FP64 (else CGTP_EDTYPE)
+ * Returns CGTP_ENOMEM / CGTP_EHIP on allocation or copy failure; *plan_out is
+ * written only on success.
+ */
+int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t *plan_out);
+
+/*
+ * out[n, :] = product of x1[n, :] and x2[n, :] for n < N.
+ *   x1, x2: device arrays [N, istp_num_inputs(L, spin)], row-major, of the
+ *           plan's dtype; out: device array [N, istp_num_outputs(L, spin)].
+ *   All three 16-byte aligned; out must not overlap x1 or x2 (x1 == x2 is
+ *   allowed); the current device must be the plan's.  Else CGTP_EINVAL.
+ *   N == 0 returns CGTP_OK without a launch; N < 0 is CGTP_EINVAL.
+ * Runs asynchronously on hip_stream (NULL: the default stream) and allocates
+ * nothing; execution errors surface at the caller's next synchronisation.
+ */
+int istp_forward(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N,
+                 void *hip_stream);
+
+/* Frees the plan's device tables.  NULL is a no-op. */
+int istp_destroy(istp_plan_t plan);
+
+/* Values per input row: (L+1)^2 (spin 0), 3 (L+1)^2 (spin 1); -1 if invalid. */
+int64_t istp_num_inputs(int32_t L, int32_t spin);
+
+/* Values per output row: (2L+1)^2 (spin 0), 3 (2L+1)^2 (spin 1); -1 if invalid. */
+int64_t istp_num_outputs(int32_t L, int32_t spin);
+
+/*
+ * First value of irrep label (j, l) in a row: spin 0 needs j == l and gives
+ * l^2; spin 1 gives 3 l^2 + {0, 2l-1, 4l}[j-l+1].  -1 if not a label.
+ */
+int64_t istp_label_offset(int32_t spin, int32_t j, int32_t l);
+
+/*
+ * Plan facts: grid sizes, pairs per work-group, and the model counts per
+ * pair.  flops_per_pair counts the method's arithmetic on the exact grid (one
+ * complex FFT = 5 n log2 n): Legendre synthesis 2 per (l, m) per input
+ * component per ring pair; 2 C complex FFTs per ring pair (north and south in
+ * one transform); the products on the half circle (6 per complex multiply,
+ * 2 per complex add); C complex FFTs per ring pair back; Legendre projection
+ * 2 per (l3, m) per component per ring pair; recombination 2 per term.
+ * bytes_per_pair = (2 inputs + 1 output) values in HBM.  Any pointer may be
+ * NULL.
+ */
+int istp_plan_query(istp_plan_t plan, int32_t *n_theta, int32_t *n_phi, int32_t *pairs_per_group,
+                    double *flops_per_pair, double *bytes_per_pair);
+
+/*
+ * Host-only: the geometry a plan for (L, spin, dtype) would use, without a
+ * device.  Writes 24 int32 values to desc_out: L, 2L, spin, components, north
+ * rings R, ring pairs per group G, n_phi, its factors A and B, pairs per
+ * work-group, values per input and output row, lift and projection MFMA
+ * tiles, lift operand elements, end-phase elements per pair, lift and
+ * projection weight-table elements, projection row length, LDS bytes per
+ * work-group, 3 zeros.  Status codes as istp_plan.
+ */
+int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t *desc_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISTP_H */

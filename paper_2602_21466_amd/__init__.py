@@ -1,13 +1,15 @@
 """Python binding of the MI355X CGTP library (libcgtp.so): argument marshalling only.
 
-Every step of the tensor product runs in the HIP kernels behind the C ABI
-declared in ``include/cgtp.h``; this module passes raw device pointers and a
-HIP stream through ctypes.  PyTorch is used for device memory and streams.
+Every step of the tensor products runs in the HIP kernels behind the C ABI
+declared in ``include/cgtp.h`` (full CGTP) and ``include/istp.h`` (the MIMO
+Gaunt and vector signal products); this module passes raw device pointers and
+a HIP stream through ctypes.  PyTorch is used for device memory and streams.
 There is no CPU fallback: if the shared library is missing or the GPU is
 absent, the calls raise.
 
-The functions carry the C names (``cgtp_plan``, ``cgtp_forward``, ...);
-``Plan`` is a small convenience wrapper around them.
+The functions carry the C names (``cgtp_plan``, ``cgtp_forward``,
+``istp_plan``, ...); ``Plan`` and ``IstpPlan`` are small convenience wrappers
+around them.
 """
 from __future__ import annotations
 
@@ -23,6 +25,10 @@ CGTP_FP32, CGTP_FP64 = 0, 1
 CGTP_COVER_DEFAULT, CGTP_COVER_ALTERNATE = 0, 1
 CGTP_MAX_L = 32
 KIND_NAMES = {0: "scalar-scalar", 1: "cross", 2: "scalar-vector", 3: "dot"}
+ISTP_GAUNT, ISTP_VECTOR = 0, 1
+ISTP_MAX_L = {"fp32": 33, "fp64": 12}
+ISTP_DESC_FIELDS = ("L", "Lo", "spin", "C", "R", "G", "Phi", "A", "B", "pairs", "nin", "nout", "n_lift", "n_proj",
+                    "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes")
 
 _lib = None
 
@@ -67,6 +73,14 @@ def _load():
         "cgtp_legendre": (ctypes.c_int, [i32, ctypes.c_double, vp]),
         "cgtp_block_grid": (ctypes.c_int, [i32, ctypes.POINTER(cgtp_grid), i32, i32,
                                            ctypes.POINTER(i32), ctypes.POINTER(i32)]),
+        "istp_plan": (ctypes.c_int, [i32, i32, i32, ctypes.POINTER(vp)]),
+        "istp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
+        "istp_destroy": (ctypes.c_int, [vp]),
+        "istp_num_inputs": (i64, [i32, i32]),
+        "istp_num_outputs": (i64, [i32, i32]),
+        "istp_label_offset": (i64, [i32, i32, i32]),
+        "istp_plan_query": (ctypes.c_int, [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32), dp, dp]),
+        "istp_plan_describe": (ctypes.c_int, [i32, i32, i32, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -80,7 +94,9 @@ def exported_symbols():
     """Names of the C ABI entry points this binding expects."""
     return ["cgtp_plan", "cgtp_forward", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
-            "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid"]
+            "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
+            "istp_plan", "istp_forward", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
+            "istp_plan_query", "istp_plan_describe"]
 
 
 def _check(rc: int, where: str):
@@ -171,6 +187,55 @@ def cgtp_block_grid(L: int, l1: int, l2: int, grid: cgtp_grid | None = None):
     return nt.value, nph.value
 
 
+def _dtype_code(dtype) -> int:
+    return {"fp32": CGTP_FP32, "fp64": CGTP_FP64}.get(dtype, dtype)
+
+
+def istp_plan(L: int, spin: int, dtype="fp32") -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    rc = _load().istp_plan(int(L), int(spin), int(_dtype_code(dtype)), ctypes.byref(h))
+    _check(rc, "istp_plan(L=%d, spin=%d)" % (L, spin))
+    return h
+
+
+def istp_forward(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, stream_ptr: int | None) -> None:
+    rc = _load().istp_forward(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(out_ptr),
+                              int(N), ctypes.c_void_p(stream_ptr) if stream_ptr else None)
+    _check(rc, "istp_forward")
+
+
+def istp_destroy(plan) -> None:
+    _check(_load().istp_destroy(plan), "istp_destroy")
+
+
+def istp_num_inputs(L: int, spin: int) -> int:
+    return int(_load().istp_num_inputs(int(L), int(spin)))
+
+
+def istp_num_outputs(L: int, spin: int) -> int:
+    return int(_load().istp_num_outputs(int(L), int(spin)))
+
+
+def istp_label_offset(spin: int, j: int, l: int) -> int:
+    return int(_load().istp_label_offset(int(spin), int(j), int(l)))
+
+
+def istp_plan_query(plan) -> dict:
+    nt, nph, pp = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    fl, by = ctypes.c_double(), ctypes.c_double()
+    _check(_load().istp_plan_query(plan, ctypes.byref(nt), ctypes.byref(nph), ctypes.byref(pp), ctypes.byref(fl),
+                                   ctypes.byref(by)), "istp_plan_query")
+    return {"n_theta": nt.value, "n_phi": nph.value, "pairs_per_group": pp.value,
+            "flops_per_pair": fl.value, "bytes_per_pair": by.value}
+
+
+def istp_plan_describe(L: int, spin: int, dtype="fp32") -> dict:
+    out = np.zeros(24, dtype=np.int32)
+    _check(_load().istp_plan_describe(int(L), int(spin), int(_dtype_code(dtype)), out.ctypes.data),
+           "istp_plan_describe")
+    return dict(zip(ISTP_DESC_FIELDS, (int(v) for v in out)))
+
+
 # ---------------------------------------------------------------- convenience
 
 class Plan:
@@ -206,6 +271,47 @@ class Plan:
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:
             cgtp_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class IstpPlan:
+    """Owns an istp plan (spin 0: Gaunt product, spin 1: vector product); forward() takes CUDA (HIP) tensors."""
+
+    def __init__(self, L: int, spin: int, dtype: str = "fp32"):
+        self.L, self.spin, self.dtype = int(L), int(spin), dtype
+        self._h = istp_plan(self.L, self.spin, dtype)
+        self.nin = istp_num_inputs(self.L, self.spin)
+        self.nout = istp_num_outputs(self.L, self.spin)
+
+    def query(self) -> dict:
+        return istp_plan_query(self._h)
+
+    def forward(self, x1, x2, out=None, stream=None):
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        for t in (x1, x2):
+            if not t.is_cuda or t.dtype != tdt or t.dim() != 2 or t.shape[1] != self.nin or not t.is_contiguous():
+                raise ValueError("inputs must be contiguous %s CUDA tensors [N, %d]" % (tdt, self.nin))
+        if x1.shape[0] != x2.shape[0]:
+            raise ValueError("x1 and x2 must hold the same number of pairs")
+        N = x1.shape[0]
+        if out is None:
+            out = torch.empty((N, self.nout), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, self.nout):
+            raise ValueError("out must be a contiguous %s tensor [N, %d]" % (tdt, self.nout))
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        istp_forward(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, s.cuda_stream)
+        return out
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            istp_destroy(self._h)
             self._h = None
 
     def __del__(self):

@@ -1,4 +1,4 @@
-"""Compiles the HIP library (libcgtp.so) in-tree for gfx950 with hipcc."""
+"""Compiles the HIP library (libcgtp.so: full CGTP and the MIMO signal products) in-tree for gfx950 with hipcc."""
 from __future__ import annotations
 
 import os
@@ -7,7 +7,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libcgtp.so")
-SOURCES = [os.path.join(HERE, "csrc", "cgtp_plan.cpp"), os.path.join(HERE, "csrc", "cgtp_kernels.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in
+           ("cgtp_plan.cpp", "cgtp_kernels.hip", "istp_plan.cpp", "istp_kernels.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed FP32 instructions are switched off for all device code.

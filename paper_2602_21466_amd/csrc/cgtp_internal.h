@@ -154,6 +154,9 @@ struct TileGeom {
     __host__ __device__ int nct(int mp) const { return (ncols(mp) + 15) / 16; }
 };
 
+// Records the HIP code behind a CGTP_EHIP status (cgtp_last_hip_error reads it).
+void set_last_hip_error(int code);
+
 // Launches the block kernel over the whole map; returns a hipError_t value.
 int launch_blocks_f32(const Tables<float>& tb, const int32_t* block_list, const LaunchMap& map,
                       int lds_bytes, const float* x1, const float* x2, float* out, int64_t N,

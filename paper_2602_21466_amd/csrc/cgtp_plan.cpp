@@ -278,15 +278,6 @@ int64_t path_offset(int L, int l1, int l2, int l3) {
            (int64_t)(l1 - l2) * (l1 - l2);
 }
 
-// Offset of row n (l3 = d + 2n) in a block's Legendre accumulator.
-inline int acc_rowoff_h(int n, int d) { return 2 * n * n + (2 * d - 1) * n; }
-
-// Rows l3 = d, d+2, ..., J of a block's Legendre accumulator; entries per component.
-inline int acc_entries(int d, int J) {
-    const int nrows = (J - d) / 2 + 1;
-    return nrows * (2 * d + 1) + 2 * nrows * (nrows - 1);
-}
-
 // MFMA weight table geometry: rings padded to whole ring groups; entries per
 // ring row (degrees l = par, par + 2, ..., <= lmax).
 inline int wtab_rpad(int R) { return (R + cgtp::kRingGroup - 1) / cgtp::kRingGroup * cgtp::kRingGroup; }
@@ -702,6 +693,10 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 }  // namespace
+
+namespace cgtp {
+void set_last_hip_error(int code) { g_last_hip_error = code; }
+}  // namespace cgtp
 
 // ====================================================================== C ABI
 

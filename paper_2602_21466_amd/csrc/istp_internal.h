@@ -1,0 +1,115 @@
+// Internal layout shared by the host plan (istp_plan.cpp) and the kernel
+// (istp_kernels.hip) of the multiple-input, multiple-output irrep-signal
+// tensor products.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace istp {
+
+constexpr int kThreads = 768;   // work-group size (12 wave64s, one work-group per CU)
+constexpr int kWaves = kThreads / 64;
+constexpr int kLdsBudget = 156 * 1024;
+constexpr int kMaxLiftSteps = 9;   // K = 4 steps of the lift over l = |m|..L (L + 1 <= 36)
+
+// Projection accumulator tiles (16 x 16) a wave may hold, per precision.
+template <typename T> struct MaxTiles;
+template <> struct MaxTiles<float> { static constexpr int value = 18; };
+template <> struct MaxTiles<double> { static constexpr int value = 6; };
+
+// One plan: inputs of degree <= L lifted to spin-S signals, the pointwise
+// product projected on degrees <= Lo = 2 L.
+//
+// Grid: n_theta = 2 R Gauss-Legendre rings (R north rings, the south ones
+// their mirror images), Phi = A * B equispaced longitudes.  A work-group takes
+// `pairs` pairs through `G` north/south ring pairs at a time.
+//
+// Per ring pair and pair, every signal (input i, spin component c) is one
+// complex transform carrying the north ring in its real and the south ring in
+// its imaginary part; the C product components are packed the same way.
+struct alignas(16) IstpDesc {
+    int32_t L, Lo, spin, C;      // C = 2 spin + 1 components
+    int32_t R, G, Phi, A, B;     // rings, ring pairs per group, longitudes = A * B
+    int32_t pairs, nin, nout;    // pairs per work-group, values per input / output row
+    int32_t n_lift, n_proj;      // lift / projection MFMA tiles
+    int32_t acoef_len;           // elements of the lift coefficient operand in LDS
+    int32_t hc_len;              // elements of the end-phase spectra of one pair
+    int32_t lw_len, pw_len;      // elements of the lift / projection weight tables
+    int32_t wrow;                // projection weight entries per ring (row tiles * 16)
+    int32_t lds_bytes;
+    int32_t pad[3];
+};
+
+// Lift tile: spectra of order +-am of 16 rows (ring, l - am parity) x 16
+// columns (sign of m, input, component, pair) over K = l - am.
+//   acoef: LDS element offset of (am, k = 0, column 16 ct) in the coefficient operand
+//   cstride: elements per k row of that operand
+//   lw: offset of (am, ring 0, k = 0) in the lift weights; kp entries per ring
+//   ncol: valid columns of the order (all tiles of it); steps: K / 4
+struct alignas(16) LiftTile {
+    int32_t am, ct, acoef, cstride, lw, kp, ncol, steps;
+};
+
+// Projection tile: rows l3 = am + par + 2 (16 rt + i), K = rings, columns
+// (sign of m, component, pair); its weights start at `a` (ring 0, row 16 rt).
+struct alignas(16) ProjTile {
+    int32_t am, par, rt, a;
+};
+
+// Device tables, one allocation per plan.
+template <typename T>
+struct IstpTables {
+    const T* lw;          // [am][ring < rpad][k < kp(am)]: P_{am+k}^{am}(x_ring), zero past L or R
+    const T* pw;          // [am][par][ring < rpad][row < wrow]: w_ring P_{am+par+2 row}^{am}(x_ring), zero past Lo or R
+    const T* tw;          // [t < A][k2 < B + 1]: exp(-2 pi i t k2 / Phi), pass layout
+    const T* liftcg;      // [l][j - l + 1][q + 1][ml + l]: C^{j, ml+q}_{l, ml, 1, q} (spin 1)
+    const T* coef;        // per output: three term weights and a pad (4 per output)
+    const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), pad
+    const int4* amd;      // per order am <= L: (coefficient operand offset, its k row stride, kp, columns)
+    const LiftTile* lift;
+    const ProjTile* proj;
+    const IstpDesc* desc;
+};
+
+// LDS of one work-group (byte offsets): twiddles at 0; the lift coefficient
+// operand; then G * P (ring pair, pair) units of 2 C transforms each, `unit`
+// complex entries apart (kUnitSkew entries of padding spread the units over
+// the banks).  The end phase puts the spectra of every pair at `hc`, over the
+// coefficient operand and the units.
+constexpr int kUnitSkew = 8;
+struct IstpLayout {
+    int acoef, fbuf, hc;   // byte offsets
+    int unit;              // complex entries per unit
+    int bytes;             // total
+};
+__host__ __device__ inline int istp_align16(int v) { return (v + 15) & ~15; }
+template <typename T>
+__host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, int P, int acoef_len, int hc_len) {
+    const int FS = A * (B + 1), cs = 2 * (int)sizeof(T);
+    IstpLayout l;
+    l.unit = 2 * C * FS + kUnitSkew;
+    l.acoef = istp_align16(FS * cs);
+    l.fbuf = istp_align16(l.acoef + acoef_len * (int)sizeof(T));
+    l.hc = l.acoef;
+    const int main_end = l.fbuf + G * P * l.unit * cs;
+    const int end_end = l.hc + P * hc_len * (int)sizeof(T);
+    l.bytes = main_end > end_end ? main_end : end_end;
+    return l;
+}
+
+// Lift coefficient operand: k rows of an order am are `cstride` elements apart,
+// 16 per column tile plus 16 when the tile count is even (rows k and k + 1 of
+// one MFMA operand then fall on opposite bank halves).
+__host__ __device__ inline int istp_cstride(int ncol) {
+    const int nct = (ncol + 15) / 16;
+    return 16 * nct + ((nct & 1) ? 0 : 16);
+}
+
+int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
+                    int64_t N, void* stream);
+int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                    double* out, int64_t N, void* stream);
+
+}  // namespace istp

@@ -1,0 +1,421 @@
+// Device side of the multiple-input, multiple-output irrep-signal tensor
+// products (the (0,0,0) Gaunt product and the (1,1,1) vector product,
+// Section 4.3, Appendix D).  One work-group takes a tile of pairs through the
+// whole product, in LDS and registers only.
+//
+// Per pair tile:
+//   0. the input rows become scalar-harmonic coefficients of each spin
+//      component (Definition 4.1: a[q][l][ml] = sum_j C^{j,ml+q}_{l,ml,1,q}
+//      x^(j,l)_{ml+q}), stored as the B operand of the lift;
+// then for each group of G north/south ring pairs:
+//   1. lift on MFMA: per order am, a [16 rows (ring, parity of l - am)] x
+//      [K = l] x [16 columns (sign of m, input, component, pair)] product with
+//      P_l^am(x_ring) as the A operand; even and odd parts give the north and
+//      south rings (P_l^m(-x) = (-1)^(l+m) P_l^m(x)), stored as one complex
+//      transform input (north + i south) in the first pass's layout;
+//   2. longitude synthesis, two in-register passes, in place;
+//   3. pointwise products on half the circle: the north and south signals are
+//      unpacked from each transform, multiplied (scalar product, or the
+//      1 (x) 1 -> 1 coupling), and packed back as (north + i south);
+//   4. longitude analysis, two passes;
+//   5. Legendre projection on MFMA: per order am and parity, [rows l3] x
+//      [4 rings] x [sign, component, pair], with w_ring P_l3^am(x_ring) as the
+//      A operand and north +- south of each spectrum as the B operand,
+//      accumulated in registers over all ring groups.
+// Then the accumulators go to LDS, each output is recombined from up to three
+// spectra (C^{j3,m3}_{l3,m3-q,1,q} for the vector product, with the
+// longitude quadrature, unpacking and coupling constants and the sign of
+// negative orders folded into the plan's weights), and stored contiguously.
+//
+// All quantities use the complex spherical basis with Condon-Shortley phase.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "device_common.h"
+#include "istp_internal.h"
+
+namespace istp {
+namespace {
+
+using namespace ::cgtp::dev;
+
+// Lift rows: MFMA row i carries ring ring(i) and the parity par(i) of l - am,
+// chosen so that a lane's four accumulator elements hold (even, odd) for two
+// rings (f32 rows are 4 (lane / 16) + v, f64 rows lane / 16 + 4 v).
+template <typename T> __device__ __forceinline__ void lift_row(int i, int& ring, int& par);
+template <> __device__ __forceinline__ void lift_row<float>(int i, int& ring, int& par) {
+    ring = i >> 1;
+    par = i & 1;
+}
+template <> __device__ __forceinline__ void lift_row<double>(int i, int& ring, int& par) {
+    ring = (i & 3) + 4 * (i >> 3);
+    par = (i >> 2) & 1;
+}
+// ring of accumulator elements 2 h (even) and 2 h + 1 (odd) of quarter q
+template <typename T> __device__ __forceinline__ int lift_ring(int q, int h);
+template <> __device__ __forceinline__ int lift_ring<float>(int q, int h) { return 2 * q + h; }
+template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { return q + 4 * h; }
+
+// Step 0: the B operand of the lift for one pair tile (zero for pairs past N,
+// rows past L and padding columns).  Column order: sign of m (+ first), input,
+// component, pair; negative orders carry (-1)^am (P^{-m} = (-1)^m P^m).
+template <typename T, int S>
+__device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
+                                                   const T* __restrict__ x1, const T* __restrict__ x2, T* acoef) {
+    constexpr int NC = 2 * S + 1;
+    const int L = d.L, P = d.pairs, nin = d.nin;
+    const int per_sign = 2 * NC * P;
+    for (int am = 0; am <= L; ++am) {
+        const int4 ad = tb.amd[am];   // (offset, k stride, k rows, columns)
+        const int total = ad.z * ad.y;
+        for (int e = threadIdx.x; e < total; e += kThreads) {
+            const int k = e / ad.y, col = e - k * ad.y;
+            const int l = am + k;
+            T v = (T)0;
+            if (l <= L && col < ad.w) {
+                const int sg = col / per_sign, rem = col - sg * per_sign;
+                const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
+                if (p < np) {
+                    const int m = sg ? -am : am;
+                    const T* x = (in ? x2 : x1) + (p0 + p) * (int64_t)nin;
+                    if (S == 0) {
+                        v = x[l * l + l + m];
+                    } else {
+                        const int q = c - 1, mj = m + q;
+                        const T* cg = tb.liftcg + 9 * l * l + m + l;
+#pragma unroll
+                        for (int jj = 0; jj < 3; ++jj) {
+                            const int j = l - 1 + jj;
+                            if (j < 0 || j + l < 1 || mj < -j || mj > j) continue;
+                            const int off = 3 * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
+                            v += cg[(jj * 3 + c) * (2 * l + 1)] * x[off + j + mj];
+                        }
+                    }
+                    if (sg && (am & 1)) v = -v;
+                }
+            }
+            acoef[ad.x + e] = v;
+        }
+    }
+}
+
+template <typename T, int A, int B, int S>
+__device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
+                                          const T* __restrict__ x1, const T* __restrict__ x2, T* __restrict__ out,
+                                          unsigned char* smem) {
+    using C2 = typename Cplx<T>::type;
+    using Acc = typename Cplx<T>::acc4;
+    constexpr int Phi = A * B;
+    constexpr int H = Phi / 2 + 1;
+    constexpr int BP = B + 1;
+    constexpr int FS = A * BP;
+    constexpr int NC = 2 * S + 1;   // spin components
+    constexpr int NS = 2 * NC;      // synthesis transforms per unit
+    constexpr int MT = MaxTiles<T>::value;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 15, kq = lane >> 4;
+    const int L = d.L, Lo = d.Lo, R = d.R, G = d.G, P = d.pairs;
+    const int U = G * P;
+    const IstpLayout ly = istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len);
+    C2* tw2 = reinterpret_cast<C2*>(smem);
+    T* acoef = reinterpret_cast<T*>(smem + ly.acoef);
+    C2* fbuf = reinterpret_cast<C2*>(smem + ly.fbuf);
+    T* hc = reinterpret_cast<T*>(smem + ly.hc);
+    auto ubuf = [&](int u) -> C2* { return fbuf + (size_t)u * ly.unit; };
+
+    for (int e = tid; e < FS; e += kThreads) tw2[e] = reinterpret_cast<const C2*>(tb.tw)[e];
+    build_coefficients<T, S>(tb, d, p0, np, x1, x2, acoef);
+
+    // projection tiles of this wave: w, w + kWaves, ...  A lane's B operand is
+    // column li (sign, component, pair; past the last column: column 0, whose
+    // duplicate results are discarded) of ring kq of a ring quad; per tile
+    // only the order's longitude position changes (order 0 has no negative
+    // column: those lanes read position 0).
+    const int ntw = d.n_proj > wave ? (d.n_proj - 1 - wave) / kWaves + 1 : 0;
+    const int col_l = li < 2 * NC * P ? li : 0;
+    const int sg_l = col_l / (NC * P), c_l = (col_l / P) % NC, p_l = col_l % P;
+    const int b_lane = ly.fbuf + (int)sizeof(C2) * ((kq * P + p_l) * ly.unit + c_l * FS);
+    const int a_lane = kq * d.wrow + li;
+    Acc acc[MT];
+#pragma unroll
+    for (int s = 0; s < MT; ++s) acc[s] = Acc(0);
+    lds_barrier();
+
+    for (int rg0 = 0; rg0 < R; rg0 += G) {
+        // ---- 1. lift on MFMA
+        for (int ti = wave; ti < d.n_lift; ti += kWaves) {
+            const LiftTile lt = tb.lift[ti];
+            int ring, par;
+            lift_row<T>(li, ring, par);
+            const bool rowok = ring < G && rg0 + ring < R;
+            const T* lwr = tb.lw + lt.lw + (size_t)(rg0 + (rowok ? ring : 0)) * lt.kp;
+            T a[kMaxLiftSteps];
+#pragma unroll
+            for (int s = 0; s < kMaxLiftSteps; ++s) {
+                const int k = 4 * s + kq;
+                a[s] = (s < lt.steps && rowok && (k & 1) == par) ? lwr[k] : (T)0;
+            }
+            Acc da = Acc(0);
+            const T* bb = acoef + lt.acoef + kq * lt.cstride + li;
+#pragma unroll
+            for (int s = 0; s < kMaxLiftSteps; ++s)
+                if (s < lt.steps) da = mfma16(a[s], bb[4 * s * lt.cstride], da);
+            const int col = 16 * lt.ct + li;
+            if (col < lt.ncol) {
+                const int per_sign = 2 * NC * P;
+                const int sg = col / per_sign, rem = col - sg * per_sign;
+                const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
+                const int n = sg ? Phi - lt.am : lt.am;
+                C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int r = lift_ring<T>(kq, h);
+                    if (r < G) dst[(size_t)r * P * ly.unit] = cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
+                }
+            }
+        }
+        lds_barrier();
+        // ---- 2. synthesis: pass 1 on rows (orders |m| > L are zero), pass 2 on columns
+        {
+            const int ntask = U * NS * A;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int t = task % A, f = task / A;
+                C2* row = ubuf(f / NS) + (f % NS) * FS + t * BP;
+                C2 v[B];
+#pragma unroll
+                for (int n2i = 0; n2i < B; ++n2i) {
+                    const int n = t + A * n2i;
+                    const int am = n <= Phi - n ? n : Phi - n;
+                    v[n2i] = am <= L ? row[n2i] : cmk<C2>((T)0, (T)0);
+                }
+                Dft<B, true, C2>::run(v);
+                const C2* twr = tw2 + t * BP;
+                C2 w[B];
+#pragma unroll
+                for (int k2 = 1; k2 < B; ++k2) w[k2] = twr[k2];
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmulc(v[k2], w[k2]);
+            }
+        }
+        lds_barrier();
+        {
+            const int ntask = U * NS * B;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int k2 = task % B, f = task / B;
+                C2* fb = ubuf(f / NS) + (f % NS) * FS + k2;
+                C2 u[A];
+#pragma unroll
+                for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
+                Dft<A, true, C2>::run(u);
+#pragma unroll
+                for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+            }
+        }
+        lds_barrier();
+        // ---- 3. products on half the circle; the product of component c goes to
+        // slot NC + c (positions n and -n are read and written by one task)
+        {
+            const int ntask = U * H;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int n = task % H;
+                C2* fb = ubuf(task / H);
+                const int kk = n == 0 ? 0 : Phi - n;
+                const int pn = n + n / B, pk = kk + kk / B;
+                // unpacked (times 2): north = F(n) + conj F(-n), south = -i (F(n) - conj F(-n))
+                C2 fn[NS], fs[NS];
+#pragma unroll
+                for (int s = 0; s < NS; ++s) {
+                    const C2 Fn = fb[s * FS + pn], Fk = fb[s * FS + pk];
+                    fn[s] = cmk<C2>(Fn.x + Fk.x, Fn.y - Fk.y);
+                    fs[s] = cmk<C2>(Fn.y + Fk.y, Fk.x - Fn.x);
+                }
+                C2 gn[NC], gs[NC];
+                if (S == 0) {
+                    gn[0] = cmul(fn[0], fn[1]);
+                    gs[0] = cmul(fs[0], fs[1]);
+                } else {
+                    // antisymmetric 1 (x) 1 -> 1 coupling of components q = -1, 0, +1
+                    // (slots c = q + 1 of input 0, then of input 1); its constant is in the plan's weights
+#pragma unroll
+                    for (int hs = 0; hs < 2; ++hs) {
+                        const C2* a = hs ? fs : fn;
+                        const C2* b = a + NC;
+                        C2* g = hs ? gs : gn;
+                        g[2] = csub(cmul(a[2], b[1]), cmul(a[1], b[2]));
+                        g[1] = csub(cmul(a[2], b[0]), cmul(a[0], b[2]));
+                        g[0] = csub(cmul(a[1], b[0]), cmul(a[0], b[1]));
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < NC; ++c) {
+                    C2* z = fb + (NC + c) * FS;
+                    z[pn] = cmk<C2>(gn[c].x - gs[c].y, gn[c].y + gs[c].x);
+                    if (kk != n) z[pk] = cmk<C2>(gn[c].x + gs[c].y, gs[c].x - gn[c].y);
+                }
+            }
+        }
+        lds_barrier();
+        // ---- 4. analysis: pass 1 reads slot NC + z and writes rows of slot z, pass 2 in place
+        {
+            const int ntask = U * NC * A;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int t = task % A, f = task / A;
+                const int z = f % NC;
+                C2* ub = ubuf(f / NC);
+                const C2* zb = ub + (NC + z) * FS;
+                C2 v[B];
+#pragma unroll
+                for (int n2i = 0; n2i < B; ++n2i) {
+                    const int n = t + A * n2i;
+                    v[n2i] = zb[n + n / B];
+                }
+                Dft<B, false, C2>::run(v);
+                C2* row = ub + z * FS + t * BP;
+                const C2* twr = tw2 + t * BP;
+                C2 w[B];
+#pragma unroll
+                for (int k2 = 1; k2 < B; ++k2) w[k2] = twr[k2];
+#pragma unroll
+                for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[k2] : cmul(v[k2], w[k2]);
+            }
+        }
+        lds_barrier();
+        {
+            const int ntask = U * NC * B;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int k2 = task % B, f = task / B;
+                C2* fb = ubuf(f / NC) + (f % NC) * FS + k2;
+                C2 u[A];
+#pragma unroll
+                for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
+                Dft<A, false, C2>::run(u);
+#pragma unroll
+                for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+            }
+        }
+        lds_barrier();
+        // ---- 5. Legendre projection on MFMA, four rings per step
+        for (int h = 0; h < G / 4; ++h) {
+            if (rg0 + 4 * h >= R) break;
+            const int ringofs = (rg0 + 4 * h) * d.wrow;
+            const int hofs = h * 4 * P * ly.unit * (int)sizeof(C2);
+            T av[MT];
+#pragma unroll
+            for (int s = 0; s < MT; ++s) av[s] = s < ntw ? tb.pw[tb.proj[wave + kWaves * s].a + ringofs + a_lane] : (T)0;
+#pragma unroll
+            for (int s = 0; s < MT; ++s) {
+                if (s < ntw) {
+                    const ProjTile pt = tb.proj[wave + kWaves * s];
+                    const int k = sg_l ? (pt.am ? Phi - pt.am : 0) : pt.am;
+                    const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
+                    acc[s] = mfma16(av[s], pt.par ? zv.x - zv.y : zv.x + zv.y, acc[s]);
+                }
+            }
+        }
+        lds_barrier();
+    }
+
+    // ---- spectra of every pair to LDS: [pair][component][l3^2 + l3 + m]
+    const int no = (Lo + 1) * (Lo + 1);
+#pragma unroll
+    for (int s = 0; s < MT; ++s) {
+        if (s < ntw) {
+            const ProjTile pt = tb.proj[wave + kWaves * s];
+            const int ncp = (pt.am ? 2 : 1) * NC * P;
+            if (li < ncp) {
+                const int sg = li / (NC * P), c = (li / P) % NC, p = li % P;
+                const int m = sg ? -pt.am : pt.am;
+                T* hp = hc + (size_t)(p * NC + c) * no + m;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int l3 = pt.am + pt.par + 2 * (acc_row<T>(kq, v) + 16 * pt.rt);
+                    if (l3 <= Lo) hp[l3 * l3 + l3] = acc[s][v];
+                }
+            }
+        }
+    }
+    lds_barrier();
+    // ---- recombination and contiguous stores
+    {
+        const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
+        const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
+        const int nout = d.nout, hs = NC * no;
+        for (int o = tid; o < nout; o += kThreads) {
+            const Acc cf = cf4[o];
+            const int4 ix = ci4[o];
+            for (int p = 0; p < np; ++p) {
+                const T* hp = hc + (size_t)p * hs;
+                T v = cf.x * hp[ix.x];
+                if (S == 1) v += cf.y * hp[ix.y] + cf.z * hp[ix.z];
+                out[(p0 + p) * (int64_t)nout + o] = v;
+            }
+        }
+    }
+}
+
+template <typename T, int S>
+__global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, IstpDesc d, const T* __restrict__ x1,
+                                                           const T* __restrict__ x2, T* __restrict__ out, int64_t N) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int64_t p0 = (int64_t)blockIdx.x * d.pairs;
+    const int np = (int)((N - p0) < d.pairs ? (N - p0) : d.pairs);
+#define ISTP_CASE(PHI, A_, B_)                                                        \
+    case PHI:                                                                         \
+        if constexpr (sizeof(T) == 4 || PHI <= 54)                                    \
+            istp_body<T, A_, B_, S>(tb, d, p0, np, x1, x2, out, smem);                \
+        break;
+    switch (d.Phi) {
+        ISTP_CASE(1, 1, 1)
+        ISTP_CASE(6, 3, 2)
+        ISTP_CASE(9, 3, 3)
+        ISTP_CASE(16, 4, 4)
+        ISTP_CASE(18, 6, 3)
+        ISTP_CASE(24, 6, 4)
+        ISTP_CASE(27, 9, 3)
+        ISTP_CASE(32, 8, 4)
+        ISTP_CASE(36, 6, 6)
+        ISTP_CASE(48, 8, 6)
+        ISTP_CASE(54, 9, 6)
+        ISTP_CASE(64, 8, 8)
+        ISTP_CASE(72, 9, 8)
+        ISTP_CASE(81, 9, 9)
+        ISTP_CASE(96, 12, 8)
+        ISTP_CASE(108, 12, 9)
+        ISTP_CASE(128, 16, 8)
+        ISTP_CASE(144, 12, 12)
+        default: break;
+    }
+#undef ISTP_CASE
+}
+
+template <typename T>
+int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2, T* out, int64_t N, void* stream) {
+    const int64_t grid = (N + d.pairs - 1) / d.pairs;
+    if (grid <= 0) return 0;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    auto kern = d.spin ? istp_kernel<T, 1> : istp_kernel<T, 0>;
+    if (d.lds_bytes > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
+        if (e != hipSuccess) return (int)e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), d.lds_bytes, (hipStream_t)stream, tb, d, x1, x2,
+                       out, N);
+    return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
+                    int64_t N, void* stream) {
+    return launch<float>(tb, d, x1, x2, out, N, stream);
+}
+int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                    double* out, int64_t N, void* stream) {
+    return launch<double>(tb, d, x1, x2, out, N, stream);
+}
+
+}  // namespace istp

@@ -1,0 +1,151 @@
+"""GPU parity of the MIMO Gaunt (spin 0) and vector (spin 1) signal products
+against the fp64 CPU oracle, through the C ABI of include/istp.h.
+
+Bar: per-output-label relative L2 error (over every checked pair and
+component of the label) <= 1e-4 for fp32 and <= 1e-10 for fp64.  A label
+whose reference is exactly zero (a selection rule) is held to the scale of a
+typical label.  The full-size workloads run in the benchmark's launch
+configuration and are compared on a seeded subsample of pairs.
+"""
+
+import numpy as np
+import pytest
+
+import cgtp_inputs as wl
+import oracle.istp as oi
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "fp64": 1e-10}
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _lib():
+    import paper_2602_21466_amd as lib
+    return lib
+
+
+def _labels(L, spin):
+    """Label id of every column of a row with degrees <= L, and the (j, l) list."""
+    if spin == 0:
+        labels = [(l, l) for l in range(L + 1)]
+        sizes = [2 * l + 1 for l in range(L + 1)]
+    else:
+        labels = oi.vector_labels(L)
+        sizes = [2 * j + 1 for j, l in labels]
+    return np.repeat(np.arange(len(labels)), sizes), labels
+
+
+def per_label_rel_err(L_out, spin, got, ref):
+    lid, labels = _labels(L_out, spin)
+    num = np.bincount(lid, weights=((got - ref) ** 2).sum(0), minlength=len(labels))
+    den = np.bincount(lid, weights=(ref ** 2).sum(0), minlength=len(labels))
+    typical = np.median(den[den > 0]) if (den > 0).any() else 1.0
+    rel = np.sqrt(num / np.where(den > 1e-20 * typical, den, typical))
+    worst = int(np.argmax(rel))
+    return float(rel[worst]), labels[worst]
+
+
+def reference(L, spin, x1, x2):
+    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+    return fn(L, np.asarray(x1, dtype=np.float64), np.asarray(x2, dtype=np.float64))
+
+
+def run_gpu(L, spin, x1, x2, dtype):
+    torch = _torch()
+    plan = _lib().IstpPlan(L, spin, dtype)
+    a, b = x1.to("cuda"), x2.to("cuda")
+    out = plan.forward(a, b)
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy()
+
+
+CASES = [(0, 0, 5, "fp32"), (0, 1, 5, "fp64"), (1, 0, 17, "fp64"), (1, 1, 9, "fp32"), (2, 1, 64, "fp64"),
+         (2, 0, 64, "fp32"), (3, 1, 33, "fp32"), (4, 0, 100, "fp32"), (5, 1, 19, "fp64"), (6, 1, 21, "fp32"),
+         (8, 0, 37, "fp64"), (8, 1, 40, "fp32"), (12, 1, 7, "fp64"), (12, 0, 9, "fp32")]
+
+
+@pytest.mark.parametrize("L,spin,N,dtype", CASES)
+def test_parity_small(L, spin, N, dtype):
+    """Every pair, ragged N (not a multiple of the pairs per work-group)."""
+    x1, x2 = wl.draw_rows((2 * spin + 1) * (L + 1) ** 2, N, dtype, seed=1000 + 10 * L + spin)
+    got = run_gpu(L, spin, x1, x2, dtype)
+    ref = reference(L, spin, x1, x2)
+    err, lab = per_label_rel_err(2 * L, spin, got, ref)
+    print("L=%d spin=%d N=%d %s worst label %s rel err %.3e" % (L, spin, N, dtype, lab, err))
+    assert err <= TOL[dtype], (lab, err)
+
+
+@pytest.mark.parametrize("w", wl.ISTP_WORKLOADS, ids=lambda w: w.name)
+def test_parity_workloads(w):
+    """Full-size workloads in the benchmark's launch configuration, on a seeded subsample of pairs."""
+    x1, x2 = wl.istp_inputs(w)
+    got = run_gpu(w.L, w.spin, x1, x2, w.dtype)
+    idx = wl.istp_check_indices(w).numpy()
+    ref = reference(w.L, w.spin, x1[idx], x2[idx])
+    err, lab = per_label_rel_err(2 * w.L, w.spin, got[idx], ref)
+    print("%s worst label %s rel err %.3e" % (w.name, lab, err))
+    assert err <= TOL[w.dtype], (lab, err)
+    assert np.isfinite(got).all()
+
+
+def test_same_input_twice_and_symmetry():
+    """x1 == x2 (one buffer) is allowed; the Gaunt product is symmetric, the vector one antisymmetric."""
+    torch = _torch()
+    L = 6
+    for spin, sign in ((0, 1.0), (1, -1.0)):
+        x1, x2 = wl.draw_rows((2 * spin + 1) * (L + 1) ** 2, 11, "fp64", seed=77 + spin)
+        plan = _lib().IstpPlan(L, spin, "fp64")
+        a, b = x1.cuda(), x2.cuda()
+        ab, ba, aa = plan.forward(a, b), plan.forward(b, a), plan.forward(a, a)
+        torch.cuda.synchronize()
+        scale = np.abs(ab.cpu().numpy()).max()
+        np.testing.assert_allclose(ba.cpu().numpy(), sign * ab.cpu().numpy(), atol=1e-12 * scale)
+        # x1 (x) x1: the Gaunt product against the oracle, the vector product vanishes
+        np.testing.assert_allclose(aa.cpu().numpy(), reference(L, spin, x1, x1), atol=1e-12 * scale)
+        if spin == 1:
+            assert np.abs(aa.cpu().numpy()).max() < 1e-12 * scale
+
+
+def test_empty_and_errors():
+    torch = _torch()
+    lib = _lib()
+    plan = lib.IstpPlan(3, 1, "fp32")
+    nin, nout = plan.nin, plan.nout
+    x = torch.zeros((4, nin), device="cuda")
+    out = torch.zeros((4, nout), device="cuda")
+    lib.istp_forward(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), 0, None)   # N == 0: no launch
+    with pytest.raises(lib.CgtpError) as e:
+        lib.istp_forward(plan._h, x.data_ptr() + 4, x.data_ptr(), out.data_ptr(), 4, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:
+        lib.istp_forward(plan._h, x.data_ptr(), x.data_ptr(), x.data_ptr(), 1, None)   # out overlaps x1
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:
+        lib.istp_forward(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), -1, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    for L, spin, dtype, code in [(34, 0, "fp32", lib.CGTP_EUNSUP), (13, 1, "fp64", lib.CGTP_EUNSUP),
+                                 (-1, 0, "fp32", lib.CGTP_EINVAL), (2, 2, "fp32", lib.CGTP_EINVAL),
+                                 (2, 0, 7, lib.CGTP_EDTYPE)]:
+        with pytest.raises(lib.CgtpError) as e:
+            lib.istp_plan(L, spin, dtype)
+        assert e.value.code == code
+    q = plan.query()
+    assert q["n_theta"] == 8 and q["n_phi"] == 16 and q["pairs_per_group"] >= 1
+    torch.cuda.synchronize()
+
+
+def test_largest_sizes():
+    """The largest L of each precision (fp32 at L = 33 on a few pairs, fp64 at L = 12)."""
+    for L, spin, N, dtype in ((33, 1, 2, "fp32"), (33, 0, 3, "fp32"), (12, 1, 3, "fp64")):
+        x1, x2 = wl.draw_rows((2 * spin + 1) * (L + 1) ** 2, N, dtype, seed=500 + L + spin)
+        got = run_gpu(L, spin, x1, x2, dtype)
+        err, lab = per_label_rel_err(2 * L, spin, got, reference(L, spin, x1, x2))
+        print("L=%d spin=%d %s worst %s %.3e" % (L, spin, dtype, lab, err))
+        assert err <= TOL[dtype], (lab, err)
