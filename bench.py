@@ -3,7 +3,9 @@
 One step = one cgtp_forward over the whole batch (every (l1, l2) block of every
 pair: lift, products, lower, per-path recovery), inputs already resident in
 HBM.  The headline workload is L = 32, N = 1024 pairs, fp32; L = 16,
-N = 8192 is reported beside it.  Prints ONE JSON line.
+N = 8192 is reported beside it.  The multiple-input, multiple-output Gaunt
+and vector signal products (istp_forward) are timed after it, each with its
+own roofline and oracle baseline, under "istp".  Prints ONE JSON line.
 """
 from __future__ import annotations
 
@@ -37,9 +39,15 @@ MEASURED_TRAFFIC = {
 }
 
 
-def kernel_digest():
+DIGEST_SOURCES = {
+    "cgtp": ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
+    "istp": ("istp_kernels.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
+}
+
+
+def kernel_digest(kind="cgtp"):
     h = hashlib.sha256()
-    for name in ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h"):
+    for name in DIGEST_SOURCES[kind]:
         with open(os.path.join(ROOT, "paper_2602_21466_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -49,20 +57,13 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def time_workload(w, steps, warmup):
+def _time_launches(forward, N, steps, warmup):
+    """Times `steps` launches of forward(stream) after `warmup`: HIP events on the launch stream."""
     import torch
 
-    import cgtp_inputs
-    import paper_2602_21466_amd as lib
-
-    x1, x2 = cgtp_inputs.workload_inputs(w)
-    plan = lib.Plan(w.L, dtype=w.dtype)
-    q = plan.query()
-    a, b = x1.cuda(), x2.cuda()
-    out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
-        plan.forward(a, b, out, stream)
+        forward(stream)
     torch.cuda.synchronize()
     # per-launch events on the launch stream bracket exactly one kernel each
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
@@ -73,20 +74,48 @@ def time_workload(w, steps, warmup):
     t_start.record(stream)
     for i in range(steps):
         ev[i][0].record(stream)
-        plan.forward(a, b, out, stream)
+        forward(stream)
         ev[i][1].record(stream)
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_end)
     launch_ms = sorted(s.elapsed_time(e) for s, e in ev)
-    avg_launch_ms = sum(launch_ms) / len(launch_ms)
-    res = {
-        "workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype,
-        "ms_per_step": total_ms / steps, "value": w.N * steps / (total_ms / 1e3),
-        "avg_launch_ms": avg_launch_ms, "median_launch_ms": launch_ms[len(launch_ms) // 2],
-        "wall_s": wall, "plan": q,
-    }
+    return {"ms_per_step": total_ms / steps, "value": N * steps / (total_ms / 1e3),
+            "avg_launch_ms": sum(launch_ms) / len(launch_ms), "median_launch_ms": launch_ms[len(launch_ms) // 2],
+            "wall_s": wall}
+
+
+def time_workload(w, steps, warmup):
+    import torch
+
+    import cgtp_inputs
+    import paper_2602_21466_amd as lib
+
+    x1, x2 = cgtp_inputs.workload_inputs(w)
+    plan = lib.Plan(w.L, dtype=w.dtype)
+    a, b = x1.cuda(), x2.cuda()
+    out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
+    res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": plan.query(), "kind": "cgtp"}
+    res.update(_time_launches(lambda st: plan.forward(a, b, out, st), w.N, steps, warmup))
+    plan.close()
+    del out, a, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def time_istp(w, steps, warmup):
+    import torch
+
+    import cgtp_inputs
+    import paper_2602_21466_amd as lib
+
+    x1, x2 = cgtp_inputs.istp_inputs(w)
+    plan = lib.IstpPlan(w.L, w.spin, w.dtype)
+    a, b = x1.cuda(), x2.cuda()
+    out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
+    res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": plan.query(), "kind": "istp"}
+    res.update(_time_launches(lambda st: plan.forward(a, b, out, st), w.N, steps, warmup))
     plan.close()
     del out, a, b
     torch.cuda.empty_cache()
@@ -100,7 +129,8 @@ def roofline(res):
     peak = PEAK_FP32_TFLOPS if res["dtype"] == "fp32" else PEAK_FP64_TFLOPS
     compulsory = res["plan"]["bytes_per_pair"] * res["N"]
     hbm = compulsory / t / 1e9
-    m = MEASURED_TRAFFIC.get(kernel_digest(), {}).get(res["workload"])
+    digest = kernel_digest(res["kind"])
+    m = MEASURED_TRAFFIC.get(digest, {}).get(res["workload"])
     traffic = None
     if m is not None:
         traffic = int(m["fetch_kib"] * 1024 * m["fetch_scale"] + m["write_kib"] * 1024 * m["write_scale"])
@@ -109,7 +139,7 @@ def roofline(res):
             "flops_per_launch": flops, "compulsory_bytes_per_launch": int(compulsory),
             "hbm_gbs_compulsory": round(hbm, 1), "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4),
             "avg_launch_ms": round(res["avg_launch_ms"], 4), "median_launch_ms": round(res["median_launch_ms"], 4),
-            "kernel_digest": kernel_digest()}
+            "kernel_digest": digest}
 
 
 def copy_probe(nbytes, reps=10):
@@ -177,14 +207,41 @@ def cpu_baseline(w, budget_s, budget_1t_s=5.0):
             "host_cpu": cpu_model(), "host_threads": os.cpu_count()}
 
 
+def cpu_baseline_istp(w, budget_s):
+    import cgtp_inputs
+    import oracle
+    import oracle.istp as oi
+
+    x1, x2 = cgtp_inputs.istp_inputs(w)
+    a = x1.double().numpy()
+    b = x2.double().numpy()
+    fn = oi.gaunt_tp if w.spin == 0 else oi.vector_tp
+    fn(w.L, a[:1], b[:1])                    # coefficient table of the CGTP oracle it builds on
+    t0 = time.perf_counter()
+    fn(w.L, a[:1], b[:1])
+    t1 = max(time.perf_counter() - t0, 1e-6)
+    k = int(max(1, min(w.N, budget_s / t1)))
+    t0 = time.perf_counter()
+    fn(w.L, a[:k], b[:k])
+    dt = time.perf_counter() - t0
+    return {"value": round(k / dt, 4), "unit": "pairs/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": "first %d of the %d pairs of %s (coefficient-space fp64 oracle on the naive CGTP oracle)"
+                      % (k, w.N, w.name), "seconds": round(dt, 2)}
+
+
 def main():
+    import cgtp_inputs
+
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="cgtp_L32_N1024_fp32")
     ap.add_argument("--secondary", default="cgtp_L16_N8192_fp32")
+    ap.add_argument("--istp", default=",".join(x.name for x in cgtp_inputs.ISTP_WORKLOADS),
+                    help="comma-separated signal-product workloads, or 'none'")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--istp-cpu-seconds", type=float, default=4.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (HBM counter calibration)")
@@ -196,7 +253,6 @@ def main():
 
     import torch
 
-    import cgtp_inputs
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
@@ -217,6 +273,16 @@ def main():
             log("  %.4f ms/step, %.4g pairs/s" % (r2["ms_per_step"], r2["value"]))
             secondary.append({"workload": r2["workload"], "value": round(r2["value"], 1), "unit": "pairs/s",
                               "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)})
+    istp = []
+    if args.istp and args.istp != "none":
+        by_istp = {x.name: x for x in cgtp_inputs.ISTP_WORKLOADS}
+        for name in args.istp.split(","):
+            wi = by_istp[name]
+            log("timing %s" % wi.name)
+            ri = time_istp(wi, args.steps, args.warmup)
+            log("  %.4f ms/step, %.4g pairs/s" % (ri["ms_per_step"], ri["value"]))
+            istp.append({"workload": wi.name, "value": round(ri["value"], 1), "unit": "pairs/s",
+                         "ms_per_step": round(ri["ms_per_step"], 4), "roofline": roofline(ri)})
     line = {
         "metric": METRIC, "value": round(main_res["value"], 1), "unit": "pairs/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(main_res["ms_per_step"], 4),
@@ -226,10 +292,15 @@ def main():
                    "grid": "per-block minimal exact Gauss-Legendre x FFT", "cover": "scalar-scalar + cross"},
         "roofline": roofline(main_res),
         "secondary": secondary,
+        "istp": istp,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        for entry in istp:
+            wi = {x.name: x for x in cgtp_inputs.ISTP_WORKLOADS}[entry["workload"]]
+            log("timing the CPU oracle on %s (budget %.0f s)" % (wi.name, args.istp_cpu_seconds))
+            entry["cpu_baseline"] = cpu_baseline_istp(wi, args.istp_cpu_seconds)
     print(json.dumps(line), flush=True)
 
 

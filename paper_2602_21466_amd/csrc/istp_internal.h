@@ -67,35 +67,46 @@ struct IstpTables {
     const T* liftcg;      // [l][j - l + 1][q + 1][ml + l]: C^{j, ml+q}_{l, ml, 1, q} (spin 1)
     const T* coef;        // per output: three term weights and a pad (4 per output)
     const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), pad
-    const int4* amd;      // per order am <= L: (coefficient operand offset, its k row stride, kp, columns)
     const LiftTile* lift;
     const ProjTile* proj;
     const IstpDesc* desc;
 };
 
-// LDS of one work-group (byte offsets): twiddles at 0; the lift coefficient
-// operand; then G * P (ring pair, pair) units of 2 C transforms each, `unit`
+// LDS of one work-group (byte offsets): twiddles at 0; one packed word per
+// projection tile (ptab); the lift coefficient operand; then G * P (ring pair, pair) units of 2 C transforms each, `unit`
 // complex entries apart (kUnitSkew entries of padding spread the units over
-// the banks).  The end phase puts the spectra of every pair at `hc`, over the
-// coefficient operand and the units.
+// the banks).  Before the first lift the tile's input rows and the lift
+// couplings are staged at the units (stage_len elements).  The end phase puts
+// the spectra of every pair at `hc`, over the coefficient operand and the units.
 constexpr int kUnitSkew = 8;
+constexpr int kStageLoads = 24;         // staged elements per thread (one batch of loads)
+constexpr int kLiftTilesPerWave = 1;    // lift tiles whose weights a wave loads in one batch
 struct IstpLayout {
-    int acoef, fbuf, hc;   // byte offsets
+    int ptab, acoef, fbuf, hc;   // byte offsets
     int unit;              // complex entries per unit
     int bytes;             // total
 };
 __host__ __device__ inline int istp_align16(int v) { return (v + 15) & ~15; }
+// staged elements: both inputs of every pair (rounded to 4), then C^{j,ml+q}_{l,ml,1,q} (spin 1)
+__host__ __device__ inline int istp_stage_x(int P, int nin) { return (2 * P * nin + 3) & ~3; }
+__host__ __device__ inline int istp_stage_len(int P, int nin, int L, int spin) {
+    return istp_stage_x(P, nin) + (spin ? 9 * (L + 1) * (L + 1) : 0);
+}
 template <typename T>
-__host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, int P, int acoef_len, int hc_len) {
+__host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, int P, int acoef_len, int hc_len,
+                                                  int stage_len, int n_proj) {
     const int FS = A * (B + 1), cs = 2 * (int)sizeof(T);
     IstpLayout l;
     l.unit = 2 * C * FS + kUnitSkew;
-    l.acoef = istp_align16(FS * cs);
+    l.ptab = istp_align16(FS * cs);
+    l.acoef = istp_align16(l.ptab + 4 * n_proj);
     l.fbuf = istp_align16(l.acoef + acoef_len * (int)sizeof(T));
     l.hc = l.acoef;
     const int main_end = l.fbuf + G * P * l.unit * cs;
     const int end_end = l.hc + P * hc_len * (int)sizeof(T);
+    const int stage_end = l.fbuf + stage_len * (int)sizeof(T);
     l.bytes = main_end > end_end ? main_end : end_end;
+    if (stage_end > l.bytes) l.bytes = stage_end;
     return l;
 }
 

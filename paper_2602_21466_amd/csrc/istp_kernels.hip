@@ -59,45 +59,76 @@ template <> __device__ __forceinline__ int lift_ring<float>(int q, int h) { retu
 template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { return q + 4 * h; }
 
 // Step 0: the B operand of the lift for one pair tile (zero for pairs past N,
-// rows past L and padding columns).  Column order: sign of m (+ first), input,
+// rows past L and padding columns).  The tile's input rows and the lift
+// couplings are first staged in LDS with one batch of loads per thread; then
+// every entry is formed from LDS.  Column order: sign of m (+ first), input,
 // component, pair; negative orders carry (-1)^am (P^{-m} = (-1)^m P^m).
+// Order am's rows start at the sum over lower orders of kp * cstride.
 template <typename T, int S>
 __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
-                                                   const T* __restrict__ x1, const T* __restrict__ x2, T* acoef) {
+                                                   const T* __restrict__ x1, const T* __restrict__ x2, T* acoef,
+                                                   T* stage) {
     constexpr int NC = 2 * S + 1;
     const int L = d.L, P = d.pairs, nin = d.nin;
+    const int nx = 2 * P * nin, nxa = istp_stage_x(P, nin);
+    const int ncg = S ? 9 * (L + 1) * (L + 1) : 0;
+    {
+        T v[kStageLoads];
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+            const int e = threadIdx.x + u * kThreads;
+            v[u] = (T)0;
+            if (e < nx) {
+                const int r = e / nin, c = e - r * nin;
+                const int in = r / P, p = r - in * P;
+                if (p < np) v[u] = (in ? x2 : x1)[(p0 + p) * (int64_t)nin + c];
+            } else if (e - nx < ncg) {
+                v[u] = tb.liftcg[e - nx];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+            const int e = threadIdx.x + u * kThreads;
+            if (e < nx) stage[e] = v[u];
+            else if (e - nx < ncg) stage[nxa + e - nx] = v[u];
+        }
+    }
+    lds_barrier();
+    const T* cgs = stage + nxa;
     const int per_sign = 2 * NC * P;
+    int off = 0;
     for (int am = 0; am <= L; ++am) {
-        const int4 ad = tb.amd[am];   // (offset, k stride, k rows, columns)
-        const int total = ad.z * ad.y;
+        const int kp = (L - am + 4) / 4 * 4;
+        const int ncol = (am ? 2 : 1) * per_sign;
+        const int cs = istp_cstride(ncol);
+        const int total = kp * cs;
         for (int e = threadIdx.x; e < total; e += kThreads) {
-            const int k = e / ad.y, col = e - k * ad.y;
+            const int k = e / cs, col = e - k * cs;
             const int l = am + k;
             T v = (T)0;
-            if (l <= L && col < ad.w) {
+            if (l <= L && col < ncol) {
                 const int sg = col / per_sign, rem = col - sg * per_sign;
                 const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
-                if (p < np) {
-                    const int m = sg ? -am : am;
-                    const T* x = (in ? x2 : x1) + (p0 + p) * (int64_t)nin;
-                    if (S == 0) {
-                        v = x[l * l + l + m];
-                    } else {
-                        const int q = c - 1, mj = m + q;
-                        const T* cg = tb.liftcg + 9 * l * l + m + l;
+                const int m = sg ? -am : am;
+                const T* x = stage + (in * P + p) * nin;
+                if (S == 0) {
+                    v = x[l * l + l + m];
+                } else {
+                    const int q = c - 1, mj = m + q;
+                    const T* cg = cgs + 9 * l * l + m + l;
 #pragma unroll
-                        for (int jj = 0; jj < 3; ++jj) {
-                            const int j = l - 1 + jj;
-                            if (j < 0 || j + l < 1 || mj < -j || mj > j) continue;
-                            const int off = 3 * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
-                            v += cg[(jj * 3 + c) * (2 * l + 1)] * x[off + j + mj];
-                        }
+                    for (int jj = 0; jj < 3; ++jj) {
+                        const int j = l - 1 + jj;
+                        if (j < 0 || j + l < 1 || mj < -j || mj > j) continue;
+                        const int lo = 3 * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
+                        v += cg[(jj * 3 + c) * (2 * l + 1)] * x[lo + j + mj];
                     }
-                    if (sg && (am & 1)) v = -v;
                 }
+                if (sg && (am & 1)) v = -v;
             }
-            acoef[ad.x + e] = v;
+            acoef[off + e] = v;
         }
+        off += total;
     }
 }
 
@@ -120,61 +151,92 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     const int li = lane & 15, kq = lane >> 4;
     const int L = d.L, Lo = d.Lo, R = d.R, G = d.G, P = d.pairs;
     const int U = G * P;
-    const IstpLayout ly = istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len);
+    const IstpLayout ly =
+        istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len, istp_stage_len(P, d.nin, L, S), d.n_proj);
     C2* tw2 = reinterpret_cast<C2*>(smem);
+    int* ptab = reinterpret_cast<int*>(smem + ly.ptab);
     T* acoef = reinterpret_cast<T*>(smem + ly.acoef);
     C2* fbuf = reinterpret_cast<C2*>(smem + ly.fbuf);
     T* hc = reinterpret_cast<T*>(smem + ly.hc);
     auto ubuf = [&](int u) -> C2* { return fbuf + (size_t)u * ly.unit; };
 
     for (int e = tid; e < FS; e += kThreads) tw2[e] = reinterpret_cast<const C2*>(tb.tw)[e];
-    build_coefficients<T, S>(tb, d, p0, np, x1, x2, acoef);
+    for (int e = tid; e < d.n_proj; e += kThreads) {
+        const ProjTile pt = tb.proj[e];
+        ptab[e] = pt.a | (pt.am << 20) | (pt.par << 27);
+    }
+    build_coefficients<T, S>(tb, d, p0, np, x1, x2, acoef, reinterpret_cast<T*>(fbuf));
 
     // projection tiles of this wave: w, w + kWaves, ...  A lane's B operand is
     // column li (sign, component, pair; past the last column: column 0, whose
     // duplicate results are discarded) of ring kq of a ring quad; per tile
     // only the order's longitude position changes (order 0 has no negative
-    // column: those lanes read position 0).
+    // column: those lanes read position 0).  Each tile's (weight offset |
+    // am << 20 | parity << 27) is in ptab.
     const int ntw = d.n_proj > wave ? (d.n_proj - 1 - wave) / kWaves + 1 : 0;
     const int col_l = li < 2 * NC * P ? li : 0;
     const int sg_l = col_l / (NC * P), c_l = (col_l / P) % NC, p_l = col_l % P;
     const int b_lane = ly.fbuf + (int)sizeof(C2) * ((kq * P + p_l) * ly.unit + c_l * FS);
-    const int a_lane = kq * d.wrow + li;
+    const int a_lane = (kq * d.wrow + li) * (int)sizeof(T);
+    // weight tables as buffer resources: reads past the end return zero
+    const __amdgpu_buffer_rsrc_t pw_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)tb.pw, (short)0, d.pw_len * (int)sizeof(T), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t lw_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)tb.lw, (short)0, d.lw_len * (int)sizeof(T), kBufferFlags);
     Acc acc[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) acc[s] = Acc(0);
     lds_barrier();
 
     for (int rg0 = 0; rg0 < R; rg0 += G) {
-        // ---- 1. lift on MFMA
-        for (int ti = wave; ti < d.n_lift; ti += kWaves) {
-            const LiftTile lt = tb.lift[ti];
+        // ---- 1. lift on MFMA: a wave's tiles in batches of kLiftTilesPerWave, the
+        // weights of a batch loaded at once
+        {
             int ring, par;
             lift_row<T>(li, ring, par);
             const bool rowok = ring < G && rg0 + ring < R;
-            const T* lwr = tb.lw + lt.lw + (size_t)(rg0 + (rowok ? ring : 0)) * lt.kp;
-            T a[kMaxLiftSteps];
+            for (int tb0 = wave; tb0 < d.n_lift; tb0 += kWaves * kLiftTilesPerWave) {
+                T a[kLiftTilesPerWave][kMaxLiftSteps];
 #pragma unroll
-            for (int s = 0; s < kMaxLiftSteps; ++s) {
-                const int k = 4 * s + kq;
-                a[s] = (s < lt.steps && rowok && (k & 1) == par) ? lwr[k] : (T)0;
-            }
-            Acc da = Acc(0);
-            const T* bb = acoef + lt.acoef + kq * lt.cstride + li;
+                for (int t = 0; t < kLiftTilesPerWave; ++t) {
+                    const int ti = tb0 + kWaves * t;
+                    if (ti < d.n_lift) {
+                        const LiftTile lt = tb.lift[ti];
+                        const int voff = ((rg0 + ring) * lt.kp + kq) * (int)sizeof(T);
 #pragma unroll
-            for (int s = 0; s < kMaxLiftSteps; ++s)
-                if (s < lt.steps) da = mfma16(a[s], bb[4 * s * lt.cstride], da);
-            const int col = 16 * lt.ct + li;
-            if (col < lt.ncol) {
-                const int per_sign = 2 * NC * P;
-                const int sg = col / per_sign, rem = col - sg * per_sign;
-                const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
-                const int n = sg ? Phi - lt.am : lt.am;
-                C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+                        for (int s = 0; s < kMaxLiftSteps; ++s) {
+                            const int k = 4 * s + kq;
+                            a[t][s] = (s < lt.steps && rowok && (k & 1) == par)
+                                          ? buffer_load<T>(lw_rsrc, voff + 4 * s * (int)sizeof(T), lt.lw * (int)sizeof(T))
+                                          : (T)0;
+                        }
+                    }
+                }
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int r = lift_ring<T>(kq, h);
-                    if (r < G) dst[(size_t)r * P * ly.unit] = cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
+                for (int t = 0; t < kLiftTilesPerWave; ++t) {
+                    const int ti = tb0 + kWaves * t;
+                    if (ti >= d.n_lift) break;
+                    const LiftTile lt = tb.lift[ti];
+                    Acc da = Acc(0);
+                    const T* bb = acoef + lt.acoef + kq * lt.cstride + li;
+#pragma unroll
+                    for (int s = 0; s < kMaxLiftSteps; ++s)
+                        if (s < lt.steps) da = mfma16(a[t][s], bb[4 * s * lt.cstride], da);
+                    const int col = 16 * lt.ct + li;
+                    if (col < lt.ncol) {
+                        const int per_sign = 2 * NC * P;
+                        const int sg = col / per_sign, rem = col - sg * per_sign;
+                        const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
+                        const int n = sg ? Phi - lt.am : lt.am;
+                        C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const int r = lift_ring<T>(kq, h);
+                            if (r < G)
+                                dst[(size_t)r * P * ly.unit] =
+                                    cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
+                        }
+                    }
                 }
             }
         }
@@ -298,23 +360,33 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
             }
         }
         lds_barrier();
-        // ---- 5. Legendre projection on MFMA, four rings per step
+        // ---- 5. Legendre projection on MFMA, four rings per step: the step's
+        // weights (buffer loads) and spectra (LDS) are all requested before the
+        // products issue
         for (int h = 0; h < G / 4; ++h) {
             if (rg0 + 4 * h >= R) break;
-            const int ringofs = (rg0 + 4 * h) * d.wrow;
             const int hofs = h * 4 * P * ly.unit * (int)sizeof(C2);
+            const int ringofs = (rg0 + 4 * h) * d.wrow;
+            int tw[MT];
+#pragma unroll
+            for (int s = 0; s < MT; ++s) tw[s] = s < ntw ? __builtin_amdgcn_readfirstlane(ptab[wave + kWaves * s]) : 0;
             T av[MT];
 #pragma unroll
-            for (int s = 0; s < MT; ++s) av[s] = s < ntw ? tb.pw[tb.proj[wave + kWaves * s].a + ringofs + a_lane] : (T)0;
+            for (int s = 0; s < MT; ++s)
+                av[s] = s < ntw ? buffer_load<T>(pw_rsrc, a_lane, ((tw[s] & 0xfffff) + ringofs) * (int)sizeof(T)) : (T)0;
+            T bv[MT];
 #pragma unroll
             for (int s = 0; s < MT; ++s) {
                 if (s < ntw) {
-                    const ProjTile pt = tb.proj[wave + kWaves * s];
-                    const int k = sg_l ? (pt.am ? Phi - pt.am : 0) : pt.am;
+                    const int am = (tw[s] >> 20) & 127;
+                    const int k = sg_l ? (am ? Phi - am : 0) : am;
                     const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
-                    acc[s] = mfma16(av[s], pt.par ? zv.x - zv.y : zv.x + zv.y, acc[s]);
+                    bv[s] = (tw[s] >> 27) ? zv.x - zv.y : zv.x + zv.y;
                 }
             }
+#pragma unroll
+            for (int s = 0; s < MT; ++s)
+                if (s < ntw) acc[s] = mfma16(av[s], bv[s], acc[s]);
         }
         lds_barrier();
     }
@@ -344,14 +416,25 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
         const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
         const int nout = d.nout, hs = NC * no;
-        for (int o = tid; o < nout; o += kThreads) {
-            const Acc cf = cf4[o];
-            const int4 ix = ci4[o];
-            for (int p = 0; p < np; ++p) {
-                const T* hp = hc + (size_t)p * hs;
-                T v = cf.x * hp[ix.x];
-                if (S == 1) v += cf.y * hp[ix.y] + cf.z * hp[ix.z];
-                out[(p0 + p) * (int64_t)nout + o] = v;
+        for (int o0 = tid; o0 < nout; o0 += 4 * kThreads) {
+            Acc cf[4];
+            int4 ix[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int o = min(o0 + u * kThreads, nout - 1);
+                cf[u] = cf4[o];
+                ix[u] = ci4[o];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int o = o0 + u * kThreads;
+                if (o >= nout) break;
+                for (int p = 0; p < np; ++p) {
+                    const T* hp = hc + (size_t)p * hs;
+                    T v = cf[u].x * hp[ix[u].x];
+                    if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
+                    out[(p0 + p) * (int64_t)nout + o] = v;
+                }
             }
         }
     }

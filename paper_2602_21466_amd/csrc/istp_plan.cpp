@@ -81,7 +81,6 @@ template <typename T>
 struct Host {
     std::vector<T> lw, pw, tw, liftcg, coef;
     std::vector<int32_t> coefi;
-    std::vector<int32_t> amd;   // 4 per order
     std::vector<istp::LiftTile> lift;
     std::vector<istp::ProjTile> proj;
 };
@@ -104,10 +103,15 @@ int build(istp_plan_s* p, Host<T>& h) {
     // MFMA tile; ties go to larger G (fuller lift rows).
     const int hc_len = NC * (Lo + 1) * (Lo + 1);
     int bestP = 0, bestG = 0, bestBytes = 0;
+    const int nin = (int)row_size(L, S);
     for (int P : {8, 4, 2, 1}) {
         if (2 * NC * P > 16) continue;
+        // inputs and couplings are staged with one batch of loads per thread
+        const int stage = 2 * P * nin + (S ? 9 * (L + 1) * (L + 1) : 0);
+        if (stage > istp::kStageLoads * istp::kThreads) continue;
         for (int G : {8, 4}) {
-            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(L, NC, P), hc_len);
+            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(L, NC, P), hc_len,
+                                                             istp::istp_stage_len(P, nin, L, S), nproj);
             if (ly.bytes > istp::kLdsBudget) continue;
             if (P * G > bestP * bestG || (P * G == bestP * bestG && G > bestG)) {
                 bestP = P;
@@ -176,7 +180,6 @@ int build(istp_plan_s* p, Host<T>& h) {
     int aoff = 0;
     for (int am = 0; am <= L; ++am) {
         const int kp = lift_kp(L, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
-        h.amd.insert(h.amd.end(), {aoff, cs, kp, ncol});
         for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
             h.lift.push_back(istp::LiftTile{am, ct, aoff + 16 * ct, cs, lw_off[am], kp, ncol, kp / 4});
         aoff += kp * cs;
@@ -186,6 +189,9 @@ int build(istp_plan_s* p, Host<T>& h) {
         for (int par = 0; par < 2; ++par)
             for (int rt = 0; rt < (proj_rows(Lo, am, par) + 15) / 16; ++rt)
                 h.proj.push_back(istp::ProjTile{am, par, rt, ((am * 2 + par) * rpad) * wrow + 16 * rt});
+
+    // the kernel packs (weight offset, am, parity) of a projection tile in one word
+    if ((int64_t)h.pw.size() >= (1 << 20) || Lo >= 128) return CGTP_EUNSUP;
 
     // recombination: the raw spectrum of (l3, m) is 4 Phi / (2 pi) times the
     // projection of the product's scalar-harmonic coefficient (doubled unpacked
@@ -279,7 +285,6 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         {h.liftcg.data(), h.liftcg.size() * sizeof(T), 0},
         {h.coef.data(), h.coef.size() * sizeof(T), 0},
         {h.coefi.data(), h.coefi.size() * sizeof(int32_t), 0},
-        {h.amd.data(), h.amd.size() * sizeof(int32_t), 0},
         {h.lift.data(), h.lift.size() * sizeof(istp::LiftTile), 0},
         {h.proj.data(), h.proj.size() * sizeof(istp::ProjTile), 0},
         {&p->desc, sizeof(istp::IstpDesc), 0},
@@ -313,10 +318,9 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->liftcg = (const T*)(base + parts[3].off);
     tb->coef = (const T*)(base + parts[4].off);
     tb->coefi = (const int32_t*)(base + parts[5].off);
-    tb->amd = (const int4*)(base + parts[6].off);
-    tb->lift = (const istp::LiftTile*)(base + parts[7].off);
-    tb->proj = (const istp::ProjTile*)(base + parts[8].off);
-    tb->desc = (const istp::IstpDesc*)(base + parts[9].off);
+    tb->lift = (const istp::LiftTile*)(base + parts[6].off);
+    tb->proj = (const istp::ProjTile*)(base + parts[7].off);
+    tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
     return CGTP_OK;
 }
 
