@@ -9,15 +9,15 @@
 
 namespace istp {
 
-constexpr int kThreads = 768;   // work-group size (12 wave64s, one work-group per CU)
+constexpr int kThreads = 1024;   // work-group size (16 wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
 constexpr int kLdsBudget = 156 * 1024;
 constexpr int kMaxLiftSteps = 9;   // K = 4 steps of the lift over l = |m|..L (L + 1 <= 36)
 
 // Projection accumulator tiles (16 x 16) a wave may hold, per precision.
 template <typename T> struct MaxTiles;
-template <> struct MaxTiles<float> { static constexpr int value = 18; };
-template <> struct MaxTiles<double> { static constexpr int value = 6; };
+template <> struct MaxTiles<float> { static constexpr int value = 13; };
+template <> struct MaxTiles<double> { static constexpr int value = 4; };
 
 // One plan: inputs of degree <= L lifted to spin-S signals, the pointwise
 // product projected on degrees <= Lo = 2 L.
@@ -79,7 +79,7 @@ struct IstpTables {
 // couplings are staged at the units (stage_len elements).  The end phase puts
 // the spectra of every pair at `hc`, over the coefficient operand and the units.
 constexpr int kUnitSkew = 8;
-constexpr int kStageLoads = 24;         // staged elements per thread (one batch of loads)
+constexpr int kStageLoads = 18;         // staged elements per thread (one batch of loads)
 constexpr int kLiftTilesPerWave = 1;    // lift tiles whose weights a wave loads in one batch
 struct IstpLayout {
     int ptab, acoef, fbuf, hc;   // byte offsets

@@ -374,19 +374,15 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
 #pragma unroll
             for (int s = 0; s < MT; ++s)
                 av[s] = s < ntw ? buffer_load<T>(pw_rsrc, a_lane, ((tw[s] & 0xfffff) + ringofs) * (int)sizeof(T)) : (T)0;
-            T bv[MT];
 #pragma unroll
             for (int s = 0; s < MT; ++s) {
                 if (s < ntw) {
                     const int am = (tw[s] >> 20) & 127;
                     const int k = sg_l ? (am ? Phi - am : 0) : am;
                     const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
-                    bv[s] = (tw[s] >> 27) ? zv.x - zv.y : zv.x + zv.y;
+                    acc[s] = mfma16(av[s], (tw[s] >> 27) ? zv.x - zv.y : zv.x + zv.y, acc[s]);
                 }
             }
-#pragma unroll
-            for (int s = 0; s < MT; ++s)
-                if (s < ntw) acc[s] = mfma16(av[s], bv[s], acc[s]);
         }
         lds_barrier();
     }
