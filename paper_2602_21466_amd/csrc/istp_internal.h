@@ -31,7 +31,7 @@ template <> struct MaxTiles<double> { static constexpr int value = 4; };
 // its imaginary part; the C product components are packed the same way.
 struct alignas(16) IstpDesc {
     int32_t L, Lo, spin, C;      // C = 2 spin + 1 components
-    int32_t R, G, Phi, A, B;     // rings, ring pairs per group, longitudes = A * B
+    int32_t R, G, Phi, A, B;     // rings, ring pairs per group (a multiple of 4), longitudes = A * B
     int32_t pairs, nin, nout;    // pairs per work-group, values per input / output row
     int32_t n_lift, n_proj;      // lift / projection MFMA tiles
     int32_t acoef_len;           // elements of the lift coefficient operand in LDS
@@ -42,14 +42,15 @@ struct alignas(16) IstpDesc {
     int32_t pad[3];
 };
 
-// Lift tile: spectra of order +-am of 16 rows (ring, l - am parity) x 16
-// columns (sign of m, input, component, pair) over K = l - am.
+// Lift tile: spectra of order +-am of 16 rows (ring, l - am parity; rings
+// 8 rb .. 8 rb + 7 of the group) x 16 columns (sign of m, input, component,
+// pair) over K = l - am.
 //   acoef: LDS element offset of (am, k = 0, column 16 ct) in the coefficient operand
 //   cstride: elements per k row of that operand
 //   lw: offset of (am, ring 0, k = 0) in the lift weights; kp entries per ring
 //   ncol: valid columns of the order (all tiles of it); steps: K / 4
 struct alignas(16) LiftTile {
-    int32_t am, ct, acoef, cstride, lw, kp, ncol, steps;
+    int32_t am, ct, acoef, cstride, lw, kp, ncol, steps, rb;
 };
 
 // Projection tile: rows l3 = am + par + 2 (16 rt + i), K = rings, columns

@@ -150,7 +150,6 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, kq = lane >> 4;
     const int L = d.L, Lo = d.Lo, R = d.R, G = d.G, P = d.pairs;
-    const int U = G * P;
     const IstpLayout ly =
         istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len, istp_stage_len(P, d.nin, L, S), d.n_proj);
     C2* tw2 = reinterpret_cast<C2*>(smem);
@@ -189,12 +188,15 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     lds_barrier();
 
     for (int rg0 = 0; rg0 < R; rg0 += G) {
+        // the transform phases take the units of the ring quads the projection
+        // reads: whole quads up to the grid's last ring (the group's other units
+        // are never read)
+        const int Uq = min(G, (R - rg0 + 3) & ~3) * P;
         // ---- 1. lift on MFMA: a wave's tiles in batches of kLiftTilesPerWave, the
         // weights of a batch loaded at once
         {
-            int ring, par;
-            lift_row<T>(li, ring, par);
-            const bool rowok = ring < G && rg0 + ring < R;
+            int ring0, par;
+            lift_row<T>(li, ring0, par);
             for (int tb0 = wave; tb0 < d.n_lift; tb0 += kWaves * kLiftTilesPerWave) {
                 T a[kLiftTilesPerWave][kMaxLiftSteps];
 #pragma unroll
@@ -202,6 +204,8 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     const int ti = tb0 + kWaves * t;
                     if (ti < d.n_lift) {
                         const LiftTile lt = tb.lift[ti];
+                        const int ring = 8 * lt.rb + ring0;
+                        const bool rowok = ring < G && rg0 + ring < R;
                         const int voff = ((rg0 + ring) * lt.kp + kq) * (int)sizeof(T);
 #pragma unroll
                         for (int s = 0; s < kMaxLiftSteps; ++s) {
@@ -231,7 +235,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                         C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
-                            const int r = lift_ring<T>(kq, h);
+                            const int r = 8 * lt.rb + lift_ring<T>(kq, h);
                             if (r < G)
                                 dst[(size_t)r * P * ly.unit] =
                                     cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
@@ -243,7 +247,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         lds_barrier();
         // ---- 2. synthesis: pass 1 on rows (orders |m| > L are zero), pass 2 on columns
         {
-            const int ntask = U * NS * A;
+            const int ntask = Uq * NS * A;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int t = task % A, f = task / A;
                 C2* row = ubuf(f / NS) + (f % NS) * FS + t * BP;
@@ -265,7 +269,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         }
         lds_barrier();
         {
-            const int ntask = U * NS * B;
+            const int ntask = Uq * NS * B;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int k2 = task % B, f = task / B;
                 C2* fb = ubuf(f / NS) + (f % NS) * FS + k2;
@@ -281,7 +285,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         // ---- 3. products on half the circle; the product of component c goes to
         // slot NC + c (positions n and -n are read and written by one task)
         {
-            const int ntask = U * H;
+            const int ntask = Uq * H;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int n = task % H;
                 C2* fb = ubuf(task / H);
@@ -323,7 +327,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         lds_barrier();
         // ---- 4. analysis: pass 1 reads slot NC + z and writes rows of slot z, pass 2 in place
         {
-            const int ntask = U * NC * A;
+            const int ntask = Uq * NC * A;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int t = task % A, f = task / A;
                 const int z = f % NC;
@@ -347,7 +351,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         }
         lds_barrier();
         {
-            const int ntask = U * NC * B;
+            const int ntask = Uq * NC * B;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int k2 = task % B, f = task / B;
                 C2* fb = ubuf(f / NC) + (f % NC) * FS + k2;

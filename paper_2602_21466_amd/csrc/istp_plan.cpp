@@ -98,9 +98,11 @@ int build(istp_plan_s* p, Host<T>& h) {
         for (int par = 0; par < 2; ++par) nproj += (proj_rows(Lo, am, par) + 15) / 16;
     if (nproj > istp::MaxTiles<T>::value * istp::kWaves) return CGTP_EUNSUP;
 
-    // Pairs per work-group and ring pairs per group: the most units (G P) that
-    // fit in LDS, with the projection's columns (sign, component, pair) on one
-    // MFMA tile; ties go to larger G (fuller lift rows).
+    // Pairs per work-group and ring pairs per group: the most pairs that fit in
+    // LDS with the projection's columns (sign, component, pair) on one MFMA tile
+    // (each pair more fills more of the lift's and the projection's columns),
+    // then the most ring pairs (more units fill more of the work-group's
+    // threads in the transform phases and take fewer passes over the rings).
     const int hc_len = NC * (Lo + 1) * (Lo + 1);
     int bestP = 0, bestG = 0, bestBytes = 0;
     const int nin = (int)row_size(L, S);
@@ -109,11 +111,11 @@ int build(istp_plan_s* p, Host<T>& h) {
         // inputs and couplings are staged with one batch of loads per thread
         const int stage = 2 * P * nin + (S ? 9 * (L + 1) * (L + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
-        for (int G : {8, 4}) {
+        for (int G : {16, 12, 8, 4}) {
             const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(L, NC, P), hc_len,
                                                              istp::istp_stage_len(P, nin, L, S), nproj);
             if (ly.bytes > istp::kLdsBudget) continue;
-            if (P * G > bestP * bestG || (P * G == bestP * bestG && G > bestG)) {
+            if (P > bestP || (P == bestP && G > bestG)) {
                 bestP = P;
                 bestG = G;
                 bestBytes = ly.bytes;
@@ -180,8 +182,9 @@ int build(istp_plan_s* p, Host<T>& h) {
     int aoff = 0;
     for (int am = 0; am <= L; ++am) {
         const int kp = lift_kp(L, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
-        for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
-            h.lift.push_back(istp::LiftTile{am, ct, aoff + 16 * ct, cs, lw_off[am], kp, ncol, kp / 4});
+        for (int rb = 0; rb < (G + 7) / 8; ++rb)
+            for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
+                h.lift.push_back(istp::LiftTile{am, ct, aoff + 16 * ct, cs, lw_off[am], kp, ncol, kp / 4, rb});
         aoff += kp * cs;
     }
     // projection tiles

@@ -60,7 +60,7 @@ def test_istp_plan_geometry(dtype):
             assert d["R"] == L + 1 and d["Phi"] >= 4 * L + 1 and d["A"] * d["B"] == d["Phi"]
             assert d["lds_bytes"] <= 156 * 1024
             assert d["n_proj"] <= 16 * mt
-            assert 2 * d["C"] * d["pairs"] <= 16 and d["G"] in (4, 8)
+            assert 2 * d["C"] * d["pairs"] <= 16 and d["G"] in (4, 8, 12, 16)
             assert d["hc_len"] == d["C"] * (2 * L + 1) ** 2
             assert d["nin"] == lib.istp_num_inputs(L, spin) and d["nout"] == lib.istp_num_outputs(L, spin)
             assert d["pairs"] * d["hc_len"] * esz + 16 <= d["lds_bytes"] + 16
