@@ -117,7 +117,7 @@ int istp_plan_query(istp_plan_t plan, int32_t *n_theta, int32_t *n_phi, int32_t 
  * work-group, values per input and output row, lift and projection MFMA
  * tiles, lift operand elements, end-phase elements per pair, lift and
  * projection weight-table elements, projection row length, LDS bytes per
- * work-group, 3 zeros.  Status codes as istp_plan.
+ * work-group, lift operand columns, 2 zeros.  Status codes as istp_plan.
  */
 int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t *desc_out);
 

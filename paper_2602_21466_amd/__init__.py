@@ -28,7 +28,7 @@ KIND_NAMES = {0: "scalar-scalar", 1: "cross", 2: "scalar-vector", 3: "dot"}
 ISTP_GAUNT, ISTP_VECTOR = 0, 1
 ISTP_MAX_L = {"fp32": 33, "fp64": 12}
 ISTP_DESC_FIELDS = ("L", "Lo", "spin", "C", "R", "G", "Phi", "A", "B", "pairs", "nin", "nout", "n_lift", "n_proj",
-                    "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes")
+                    "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes", "n_bcol")
 
 _lib = None
 

@@ -39,7 +39,8 @@ struct alignas(16) IstpDesc {
     int32_t lw_len, pw_len;      // elements of the lift / projection weight tables
     int32_t wrow;                // projection weight entries per ring (row tiles * 16)
     int32_t lds_bytes;
-    int32_t pad[3];
+    int32_t n_bcol;              // columns of the lift coefficient operand over all orders
+    int32_t pad[2];
 };
 
 // Lift tile: spectra of order +-am of 16 rows (ring, l - am parity; rings
@@ -70,6 +71,7 @@ struct IstpTables {
     const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), pad
     const LiftTile* lift;
     const ProjTile* proj;
+    const int2* bcol;     // per operand column: (am | column << 8, element offset of (am, k = 0, column))
     const IstpDesc* desc;
 };
 

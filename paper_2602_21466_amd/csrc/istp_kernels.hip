@@ -61,9 +61,10 @@ template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { ret
 // Step 0: the B operand of the lift for one pair tile (zero for pairs past N,
 // rows past L and padding columns).  The tile's input rows and the lift
 // couplings are first staged in LDS with one batch of loads per thread; then
-// every entry is formed from LDS.  Column order: sign of m (+ first), input,
-// component, pair; negative orders carry (-1)^am (P^{-m} = (-1)^m P^m).
-// Order am's rows start at the sum over lower orders of kp * cstride.
+// every entry is formed from LDS, one thread per operand column (the plan's
+// column table gives its order and offset; padding columns are zero).  Column
+// order: sign of m (+ first), input, component, pair; negative orders carry
+// (-1)^am (P^{-m} = (-1)^m P^m).
 template <typename T, int S>
 __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                                    const T* __restrict__ x1, const T* __restrict__ x2, T* acoef,
@@ -94,23 +95,29 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         }
     }
     lds_barrier();
+    // one thread per operand column (order am, column col), all of its k rows
     const T* cgs = stage + nxa;
     const int per_sign = 2 * NC * P;
-    int off = 0;
-    for (int am = 0; am <= L; ++am) {
+    for (int ci = threadIdx.x; ci < d.n_bcol; ci += kThreads) {
+        const int2 bc = tb.bcol[ci];
+        const int am = bc.x & 255, col = bc.x >> 8;
+        const int ncol = (am ? 2 : 1) * per_sign, cs = istp_cstride(ncol);
         const int kp = (L - am + 4) / 4 * 4;
-        const int ncol = (am ? 2 : 1) * per_sign;
-        const int cs = istp_cstride(ncol);
-        const int total = kp * cs;
-        for (int e = threadIdx.x; e < total; e += kThreads) {
-            const int k = e / cs, col = e - k * cs;
+        T* dst = acoef + bc.y;
+        if (col >= ncol) {
+            for (int k = 0; k < kp; ++k) dst[k * cs] = (T)0;
+            continue;
+        }
+        const int sg = col / per_sign, rem = col - sg * per_sign;
+        const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
+        const int m = sg ? -am : am;
+        const T sign = (sg && (am & 1)) ? (T)-1 : (T)1;
+        const T* x = stage + (in * P + p) * nin;
+#pragma unroll 4
+        for (int k = 0; k < kp; ++k) {
             const int l = am + k;
             T v = (T)0;
-            if (l <= L && col < ncol) {
-                const int sg = col / per_sign, rem = col - sg * per_sign;
-                const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
-                const int m = sg ? -am : am;
-                const T* x = stage + (in * P + p) * nin;
+            if (l <= L) {
                 if (S == 0) {
                     v = x[l * l + l + m];
                 } else {
@@ -124,11 +131,9 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
                         v += cg[(jj * 3 + c) * (2 * l + 1)] * x[lo + j + mj];
                     }
                 }
-                if (sg && (am & 1)) v = -v;
             }
-            acoef[off + e] = v;
+            dst[k * cs] = sign * v;
         }
-        off += total;
     }
 }
 

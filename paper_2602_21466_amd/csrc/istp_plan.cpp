@@ -83,6 +83,7 @@ struct Host {
     std::vector<int32_t> coefi;
     std::vector<istp::LiftTile> lift;
     std::vector<istp::ProjTile> proj;
+    std::vector<int32_t> bcol;   // 2 per operand column
 };
 
 template <typename T>
@@ -182,6 +183,7 @@ int build(istp_plan_s* p, Host<T>& h) {
     int aoff = 0;
     for (int am = 0; am <= L; ++am) {
         const int kp = lift_kp(L, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
+        for (int col = 0; col < cs; ++col) h.bcol.insert(h.bcol.end(), {am | (col << 8), aoff + col});
         for (int rb = 0; rb < (G + 7) / 8; ++rb)
             for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
                 h.lift.push_back(istp::LiftTile{am, ct, aoff + 16 * ct, cs, lw_off[am], kp, ncol, kp / 4, rb});
@@ -261,6 +263,7 @@ int build(istp_plan_s* p, Host<T>& h) {
     d.pw_len = (int32_t)h.pw.size();
     d.wrow = wrow;
     d.lds_bytes = bestBytes;
+    d.n_bcol = (int32_t)(h.bcol.size() / 2);
     p->n_theta = nt;
     p->n_phi = Phi;
 
@@ -291,6 +294,7 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         {h.lift.data(), h.lift.size() * sizeof(istp::LiftTile), 0},
         {h.proj.data(), h.proj.size() * sizeof(istp::ProjTile), 0},
         {&p->desc, sizeof(istp::IstpDesc), 0},
+        {h.bcol.data(), h.bcol.size() * sizeof(int32_t), 0},
     };
     size_t total = 0;
     for (auto& pt : parts) {
@@ -324,6 +328,7 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->lift = (const istp::LiftTile*)(base + parts[6].off);
     tb->proj = (const istp::ProjTile*)(base + parts[7].off);
     tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
+    tb->bcol = (const int2*)(base + parts[9].off);
     return CGTP_OK;
 }
 
