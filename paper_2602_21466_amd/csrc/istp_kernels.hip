@@ -95,17 +95,22 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         }
     }
     lds_barrier();
-    // one thread per operand column (order am, column col), all of its k rows
+    // per operand column (order am, column col): its k rows
     const T* cgs = stage + nxa;
     const int per_sign = 2 * NC * P;
-    for (int ci = threadIdx.x; ci < d.n_bcol; ci += kThreads) {
+    // each column's k rows in chunks of 8, so that every thread takes part
+    const int nchunk = (L + 8) / 8;
+    for (int it = threadIdx.x; it < d.n_bcol * nchunk; it += kThreads) {
+        const int ci = it % d.n_bcol, k0 = 8 * (it / d.n_bcol);
         const int2 bc = tb.bcol[ci];
         const int am = bc.x & 255, col = bc.x >> 8;
         const int ncol = (am ? 2 : 1) * per_sign, cs = istp_cstride(ncol);
         const int kp = (L - am + 4) / 4 * 4;
+        if (k0 >= kp) continue;
+        const int k1 = min(k0 + 8, kp);
         T* dst = acoef + bc.y;
         if (col >= ncol) {
-            for (int k = 0; k < kp; ++k) dst[k * cs] = (T)0;
+            for (int k = k0; k < k1; ++k) dst[k * cs] = (T)0;
             continue;
         }
         const int sg = col / per_sign, rem = col - sg * per_sign;
@@ -114,7 +119,7 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         const T sign = (sg && (am & 1)) ? (T)-1 : (T)1;
         const T* x = stage + (in * P + p) * nin;
 #pragma unroll 4
-        for (int k = 0; k < kp; ++k) {
+        for (int k = k0; k < k1; ++k) {
             const int l = am + k;
             T v = (T)0;
             if (l <= L) {
