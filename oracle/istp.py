@@ -33,6 +33,12 @@ signal, every output irrep read back from one product):
       3. z^(j3,l3)_{m3} = sum_q C^{j3 m3}_{l3, m3-q, 1, q} b[q][l3][m3-q]
          (coefficients in the orthonormal basis of Definition 4.1).
 
+``product_vjp`` gives the gradients of sum(g * z) w.r.t. both inputs by the
+plain definition of a bilinear map's derivatives.
+
+Both products take separate degree bounds for the two inputs and the output
+(L, L2, Lo; by default L2 = L and Lo = L + L2).
+
 Row layout of the vector product: labels ordered by l, then j = l-1, l, l+1
 (for l = 0 only j = 1), components m = -j..j; label (j, l) starts at
 3 l^2 + {0, 2l - 1, 4l}[j - l + 1].
@@ -85,21 +91,27 @@ def _rows(x, n):
     return a
 
 
-def gaunt_tp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
-    """(0,0,0) product (Section 3.3).  x1, x2: [N, (L+1)^2] real; returns [N, (2L+1)^2]."""
-    a = _rows(x1, gaunt_size(L))
-    b = _rows(x2, gaunt_size(L))
-    if a.shape != b.shape:
-        raise ValueError("inputs must have the same shape")
-    z = _cgtp(L, a, b, threads)
-    out = np.zeros((a.shape[0], (2 * L + 1) ** 2))
-    for l1 in range(L + 1):
-        for l2 in range(L + 1):
-            for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+def gaunt_tp(L: int, x1, x2, threads: int = 0, L2: int | None = None, Lo: int | None = None) -> np.ndarray:
+    """(0,0,0) product (Section 3.3).  x1: [N, (L+1)^2], x2: [N, (L2+1)^2] real (L2 = L by default);
+    returns the degrees 0..Lo (default L + L2): [N, (Lo+1)^2]."""
+    L1 = L
+    L2 = L1 if L2 is None else L2
+    Lo = L1 + L2 if Lo is None else Lo
+    a = _rows(x1, gaunt_size(L1))
+    b = _rows(x2, gaunt_size(L2))
+    if a.shape[0] != b.shape[0]:
+        raise ValueError("inputs must hold the same number of rows")
+    Lm = max(L1, L2)
+    pad = lambda v, l: np.concatenate([v, np.zeros((v.shape[0], gaunt_size(Lm) - gaunt_size(l)))], axis=1)
+    z = _cgtp(Lm, pad(a, L1), pad(b, L2), threads)
+    out = np.zeros((a.shape[0], (Lo + 1) ** 2))
+    for l1 in range(L1 + 1):
+        for l2 in range(L2 + 1):
+            for l3 in range(abs(l1 - l2), min(l1 + l2, Lo) + 1):
                 if (l1 + l2 + l3) & 1:
                     continue   # C^{l3 0}_{l1 0 l2 0} vanishes
                 g = math.sqrt((2 * l1 + 1) * (2 * l2 + 1) / (4 * math.pi * (2 * l3 + 1))) * _cg(l1, 0, l2, 0, l3, 0)
-                off = _path_offset(L, l1, l2, l3)
+                off = _path_offset(Lm, l1, l2, l3)
                 out[:, l3 * l3: (l3 + 1) ** 2] += g * z[:, off: off + 2 * l3 + 1]
     return out
 
@@ -118,14 +130,17 @@ def vector_components(L: int, x) -> np.ndarray:
     return a
 
 
-def vector_tp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
-    """(1,1,1) product (Section 5).  x1, x2: [N, 3 (L+1)^2] real; returns [N, 3 (2L+1)^2]."""
-    a1 = vector_components(L, x1)
-    a2 = vector_components(L, x2)
-    if a1.shape != a2.shape:
-        raise ValueError("inputs must have the same shape")
+def vector_tp(L: int, x1, x2, threads: int = 0, L2: int | None = None, Lo: int | None = None) -> np.ndarray:
+    """(1,1,1) product (Section 5).  x1: [N, 3 (L+1)^2], x2: [N, 3 (L2+1)^2] real (L2 = L by default);
+    returns the labels up to l = Lo (default L + L2): [N, 3 (Lo+1)^2]."""
+    L1 = L
+    L2 = L1 if L2 is None else L2
+    Lo = L1 + L2 if Lo is None else Lo
+    a1 = vector_components(L1, x1)
+    a2 = vector_components(L2, x2)
+    if a1.shape[0] != a2.shape[0]:
+        raise ValueError("inputs must hold the same number of rows")
     n = a1.shape[0]
-    Lo = 2 * L
     b = np.zeros((n, 3, (Lo + 1) ** 2))
     for q1 in (-1, 0, 1):
         for q2 in (-1, 0, 1):
@@ -135,7 +150,7 @@ def vector_tp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
             c = _cg(1, q1, 1, q2, 1, q)
             if c == 0.0:
                 continue
-            b[:, q + 1] += c * gaunt_tp(L, a1[:, q1 + 1], a2[:, q2 + 1], threads)
+            b[:, q + 1] += c * gaunt_tp(L1, a1[:, q1 + 1], a2[:, q2 + 1], threads, L2=L2, Lo=Lo)
     out = np.zeros((n, vector_size(Lo)))
     for j3, l3 in vector_labels(Lo):
         o = vector_offset(j3, l3)
@@ -145,3 +160,24 @@ def vector_tp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
                 if abs(ml) <= l3:
                     out[:, o + j3 + m3] += _cg(l3, ml, 1, q, j3, m3) * b[:, q + 1, l3 * l3 + l3 + ml]
     return out
+
+
+def product_vjp(spin: int, L: int, x1, x2, g, threads: int = 0):
+    """Gradients of sum(g * z(x1, x2)) w.r.t. x1 and x2 for the spin-0 or spin-1 product above, by the
+    plain definition: z is bilinear, so d/dx1[b] = sum_a g_a z_a(e_b, x2) and d/dx2[b] = sum_a g_a z_a(x1, e_b),
+    with z evaluated by ``gaunt_tp`` / ``vector_tp`` on unit rows (one pair at a time).
+    x1, x2: [N, n_in]; g: [N, n_out]; returns (grad_x1, grad_x2), each [N, n_in]."""
+    fn = gaunt_tp if spin == 0 else vector_tp
+    size = gaunt_size if spin == 0 else vector_size
+    a = _rows(x1, size(L))
+    b = _rows(x2, size(L))
+    gg = _rows(g, size(2 * L))
+    eye = np.eye(size(L))
+    g1 = np.zeros_like(a)
+    g2 = np.zeros_like(b)
+    for n in range(a.shape[0]):
+        j1 = fn(L, eye, np.repeat(b[n:n + 1], size(L), 0), threads)   # row k: z(e_k, x2)
+        j2 = fn(L, np.repeat(a[n:n + 1], size(L), 0), eye, threads)   # row k: z(x1, e_k)
+        g1[n] = j1 @ gg[n]
+        g2[n] = j2 @ gg[n]
+    return g1, g2

@@ -179,3 +179,60 @@ def test_vector_selection_rule():
             np.testing.assert_allclose(blk, 0.0, atol=1e-14)
         else:
             assert np.abs(blk).max() > 1e-3, (j3, l3)
+
+
+def _reverse(spin, L, x):
+    """x~[(j,l), m] = (-1)^(m + j - l + spin) x[(j,l), -m] (time reversal of the coefficients)."""
+    y = np.zeros_like(x)
+    labels = [(l, l) for l in range(L + 1)] if spin == 0 else oi.vector_labels(L)
+    off = (lambda j, l: l * l) if spin == 0 else oi.vector_offset
+    for j, l in labels:
+        o = off(j, l)
+        for m in range(-j, j + 1):
+            y[..., o + j + m] = (-1) ** ((m + j - l + spin) % 2) * x[..., o + j - m]
+    return y
+
+
+@pytest.mark.parametrize("spin", [0, 1])
+def test_vjp_against_time_reversed_product(spin, rng):
+    """The gradients equal +-P(g, reversed other input): a degree-2L by degree-L product projected on degrees <= L,
+    the adjoint of the integral of three harmonics (the vector product changes sign under the swap of its inputs)."""
+    L = 2
+    size = oi.gaunt_size if spin == 0 else oi.vector_size
+    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+    x1 = rng.standard_normal((2, size(L)))
+    x2 = rng.standard_normal((2, size(L)))
+    g = rng.standard_normal((2, size(2 * L)))
+    g1, g2 = oi.product_vjp(spin, L, x1, x2, g)
+    np.testing.assert_allclose(g1, fn(2 * L, g, _reverse(spin, L, x2), L2=L, Lo=L), atol=1e-12)
+    sign = 1.0 if spin == 0 else -1.0
+    np.testing.assert_allclose(g2, sign * fn(2 * L, g, _reverse(spin, L, x1), L2=L, Lo=L), atol=1e-12)
+
+
+@pytest.mark.parametrize("spin", [0, 1])
+def test_vjp_euler_identity(spin, rng):
+    """Bilinearity: <g, z(x1, x2)> = <grad_x1, x1> = <grad_x2, x2>."""
+    L = 3
+    size = oi.gaunt_size if spin == 0 else oi.vector_size
+    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+    x1 = rng.standard_normal((3, size(L)))
+    x2 = rng.standard_normal((3, size(L)))
+    g = rng.standard_normal((3, size(2 * L)))
+    g1, g2 = oi.product_vjp(spin, L, x1, x2, g)
+    want = (g * fn(L, x1, x2)).sum(1)
+    np.testing.assert_allclose((g1 * x1).sum(1), want, rtol=1e-12)
+    np.testing.assert_allclose((g2 * x2).sum(1), want, rtol=1e-12)
+
+
+def test_unequal_bounds_against_quadrature(rng):
+    """The Gaunt product with degree bounds (3, 1) -> 2 against direct quadrature of scipy's harmonics."""
+    L1, L2, Lo = 3, 1, 2
+    x1 = rng.standard_normal(oi.gaunt_size(L1))
+    x2 = rng.standard_normal(oi.gaunt_size(L2))
+    z = oi.gaunt_tp(L1, x1, x2, L2=L2, Lo=Lo)[0]
+    T, P, W = _quadrature_grid(8, 16)
+    Y = {(l, m): _sph_harm(l, m, T, P) for l in range(L1 + 1) for m in range(-l, l + 1)}
+    f1 = sum(x1[l * l + l + m] * Y[l, m] for l in range(L1 + 1) for m in range(-l, l + 1))
+    f2 = sum(x2[l * l + l + m] * Y[l, m] for l in range(L2 + 1) for m in range(-l, l + 1))
+    want = np.array([(W * f1 * f2 * np.conj(Y[l, m])).sum() for l in range(Lo + 1) for m in range(-l, l + 1)])
+    np.testing.assert_allclose(z, want.real, atol=1e-12)
