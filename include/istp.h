@@ -111,13 +111,46 @@ int istp_plan_query(istp_plan_t plan, int32_t *n_theta, int32_t *n_phi, int32_t 
                     double *flops_per_pair, double *bytes_per_pair);
 
 /*
+ * Gradients (vector-Jacobian product) of istp_forward: with g = dLoss/dout
+ * ([N, istp_num_outputs], real),
+ *   grad_x1[n, :] = dLoss/dx1[n, :],  grad_x2[n, :] = dLoss/dx2[n, :].
+ * The product is bilinear, so each is again a signal product, the adjoint of
+ * the forward pipeline: by the symmetry of the integral of three harmonics,
+ *   grad_x1 = P(g, x2~),  grad_x2 = +-P(g, x1~)  (- for the vector product,
+ *   which is antisymmetric),
+ * where P is the same kind of product of a degree-2L and a degree-L signal
+ * projected on degrees <= L (the same exact grid), and x~ is the input
+ * time-reversed: x~[(j,l), m] = (-1)^(m + j - l + s) x[(j,l), -m].
+ *   x1, x2, grad_x1, grad_x2: [N, istp_num_inputs]; grad_out: [N,
+ *   istp_num_outputs]; all 16-byte aligned device arrays of the plan's dtype.
+ *   Either gradient pointer may be NULL (not computed), not both.  A gradient
+ *   may not overlap any input or the other gradient (CGTP_EINVAL).
+ * CGTP_EUNSUP when the plan's gradient product is outside the kernel's limits
+ * (the degree-2L lift's LDS and register budget; istp_backward_query says).
+ * Asynchronous on hip_stream; allocates nothing.
+ */
+int istp_backward(istp_plan_t plan, const void *x1, const void *x2, const void *grad_out, void *grad_x1,
+                  void *grad_x2, int64_t N, void *hip_stream);
+
+/*
+ * The gradient product's facts: pairs per work-group, and the model counts
+ * per pair of both gradients (two launches; the counting rules of
+ * istp_plan_query).  CGTP_EUNSUP when the plan has no gradient product.
+ */
+int istp_backward_query(istp_plan_t plan, int32_t *pairs_per_group, double *flops_per_pair,
+                        double *bytes_per_pair);
+
+/*
  * Host-only: the geometry a plan for (L, spin, dtype) would use, without a
- * device.  Writes 24 int32 values to desc_out: L, 2L, spin, components, north
- * rings R, ring pairs per group G, n_phi, its factors A and B, pairs per
- * work-group, values per input and output row, lift and projection MFMA
- * tiles, lift operand elements, end-phase elements per pair, lift and
- * projection weight-table elements, projection row length, LDS bytes per
- * work-group, lift operand columns, 2 zeros.  Status codes as istp_plan.
+ * device.  Writes 48 int32 values to desc_out: the forward product's
+ * descriptor, then the gradient product's (all zero when outside the
+ * kernel's limits).  Each descriptor: first and second input degree bounds,
+ * output degree bound, spin, components, north rings R, ring pairs per group
+ * G, n_phi, its factors A and B, pairs per work-group, values per first
+ * input, second input and output row, lift and projection MFMA tiles, lift
+ * operand elements, end-phase elements per pair, lift and projection
+ * weight-table elements, projection row length, LDS bytes per work-group,
+ * lift operand columns, flags.  Status codes as istp_plan.
  */
 int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t *desc_out);
 

@@ -27,8 +27,9 @@ CGTP_MAX_L = 32
 KIND_NAMES = {0: "scalar-scalar", 1: "cross", 2: "scalar-vector", 3: "dot"}
 ISTP_GAUNT, ISTP_VECTOR = 0, 1
 ISTP_MAX_L = {"fp32": 33, "fp64": 12}
-ISTP_DESC_FIELDS = ("L", "Lo", "spin", "C", "R", "G", "Phi", "A", "B", "pairs", "nin", "nout", "n_lift", "n_proj",
-                    "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes", "n_bcol")
+ISTP_DESC_FIELDS = ("L", "L2", "Lo", "spin", "C", "R", "G", "Phi", "A", "B", "pairs", "nin", "nin2", "nout",
+                    "n_lift", "n_proj", "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes", "n_bcol",
+                    "flags")
 
 _lib = None
 
@@ -81,6 +82,8 @@ def _load():
         "istp_label_offset": (i64, [i32, i32, i32]),
         "istp_plan_query": (ctypes.c_int, [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32), dp, dp]),
         "istp_plan_describe": (ctypes.c_int, [i32, i32, i32, vp]),
+        "istp_backward": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp]),
+        "istp_backward_query": (ctypes.c_int, [vp, ctypes.POINTER(i32), dp, dp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -96,7 +99,7 @@ def exported_symbols():
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
-            "istp_plan_query", "istp_plan_describe"]
+            "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
 
 def _check(rc: int, where: str):
@@ -230,10 +233,28 @@ def istp_plan_query(plan) -> dict:
 
 
 def istp_plan_describe(L: int, spin: int, dtype="fp32") -> dict:
-    out = np.zeros(24, dtype=np.int32)
+    """Forward product's geometry; its gradient product's under "backward" (None outside the limits)."""
+    out = np.zeros(48, dtype=np.int32)
     _check(_load().istp_plan_describe(int(L), int(spin), int(_dtype_code(dtype)), out.ctypes.data),
            "istp_plan_describe")
-    return dict(zip(ISTP_DESC_FIELDS, (int(v) for v in out)))
+    d = dict(zip(ISTP_DESC_FIELDS, (int(v) for v in out[:24])))
+    d["backward"] = dict(zip(ISTP_DESC_FIELDS, (int(v) for v in out[24:]))) if out[24:].any() else None
+    return d
+
+
+def istp_backward(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int | None, gx2_ptr: int | None, N: int,
+                  stream_ptr: int | None) -> None:
+    vp = ctypes.c_void_p
+    rc = _load().istp_backward(plan, vp(x1_ptr), vp(x2_ptr), vp(g_ptr), vp(gx1_ptr) if gx1_ptr else None,
+                               vp(gx2_ptr) if gx2_ptr else None, int(N), vp(stream_ptr) if stream_ptr else None)
+    _check(rc, "istp_backward")
+
+
+def istp_backward_query(plan) -> dict:
+    pp, fl, by = ctypes.c_int32(), ctypes.c_double(), ctypes.c_double()
+    _check(_load().istp_backward_query(plan, ctypes.byref(pp), ctypes.byref(fl), ctypes.byref(by)),
+           "istp_backward_query")
+    return {"pairs_per_group": pp.value, "flops_per_pair": fl.value, "bytes_per_pair": by.value}
 
 
 # ---------------------------------------------------------------- convenience
@@ -308,6 +329,27 @@ class IstpPlan:
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         istp_forward(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, s.cuda_stream)
         return out
+
+    def backward_query(self) -> dict:
+        return istp_backward_query(self._h)
+
+    def backward(self, x1, x2, grad_out, need_x1=True, need_x2=True, stream=None):
+        """(grad_x1, grad_x2) for grad_out = dLoss/dout; a gradient not asked for is None."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        N = x1.shape[0]
+        for t, n in ((x1, self.nin), (x2, self.nin), (grad_out, self.nout)):
+            if (not t.is_cuda or t.dtype != tdt or t.dim() != 2 or t.shape[0] != N or t.shape[1] != n
+                    or not t.is_contiguous()):
+                raise ValueError("backward takes contiguous %s CUDA tensors x1, x2 [N, %d] and grad_out [N, %d]"
+                                 % (tdt, self.nin, self.nout))
+        g1 = torch.empty_like(x1) if need_x1 else None
+        g2 = torch.empty_like(x2) if need_x2 else None
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        istp_backward(self._h, x1.data_ptr(), x2.data_ptr(), grad_out.data_ptr(),
+                      g1.data_ptr() if g1 is not None else None, g2.data_ptr() if g2 is not None else None, N,
+                      s.cuda_stream)
+        return g1, g2
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -18,12 +18,25 @@ FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
 
 
 def build(force: bool = True, extra=None) -> str:
+    """Compiles every source to an object in parallel (one hipcc each), then links the library."""
     if not force and os.path.exists(LIB):
         return LIB
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + list(extra or []) + SOURCES + ["-o", tmp]
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    tag = ".tmp%d" % os.getpid()
+    objs = [os.path.join(HERE, "csrc", os.path.basename(src) + tag + ".o") for src in SOURCES]
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    procs = [subprocess.Popen([HIPCC] + compile_flags + list(extra or []) + ["-c", src, "-o", obj])
+             for src, obj in zip(SOURCES, objs)]
+    failed = [src for src, p in zip(SOURCES, procs) if p.wait() != 0]
+    try:
+        if failed:
+            raise subprocess.CalledProcessError(1, "hipcc", "failed: %s" % ", ".join(failed))
+        tmp = LIB + tag
+        subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", tmp], check=True)
+        os.replace(tmp, LIB)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
     return LIB
 
 

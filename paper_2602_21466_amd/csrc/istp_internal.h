@@ -12,15 +12,16 @@ namespace istp {
 constexpr int kThreads = 1024;   // work-group size (16 wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
 constexpr int kLdsBudget = 156 * 1024;
-constexpr int kMaxLiftSteps = 9;   // K = 4 steps of the lift over l = |m|..L (L + 1 <= 36)
+constexpr int kMaxLiftSteps = 9;   // K = 4 lift steps whose weights a wave loads at once
 
 // Projection accumulator tiles (16 x 16) a wave may hold, per precision.
 template <typename T> struct MaxTiles;
 template <> struct MaxTiles<float> { static constexpr int value = 13; };
 template <> struct MaxTiles<double> { static constexpr int value = 4; };
 
-// One plan: inputs of degree <= L lifted to spin-S signals, the pointwise
-// product projected on degrees <= Lo = 2 L.
+// One product: a first input of degree <= L and a second of degree <= L2
+// lifted to spin-S signals, the pointwise product projected on degrees <= Lo
+// (the forward product: L2 = L, Lo = 2 L).
 //
 // Grid: n_theta = 2 R Gauss-Legendre rings (R north rings, the south ones
 // their mirror images), Phi = A * B equispaced longitudes.  A work-group takes
@@ -29,10 +30,14 @@ template <> struct MaxTiles<double> { static constexpr int value = 4; };
 // Per ring pair and pair, every signal (input i, spin component c) is one
 // complex transform carrying the north ring in its real and the south ring in
 // its imaginary part; the C product components are packed the same way.
+enum IstpFlags : int32_t {
+    kReverseSecond = 1,   // the second input enters time-reversed: x[(j,l), m] -> (-1)^(m+j-l+S) x[(j,l), -m]
+    kNegate = 2,          // outputs are negated
+};
 struct alignas(16) IstpDesc {
-    int32_t L, Lo, spin, C;      // C = 2 spin + 1 components
+    int32_t L, L2, Lo, spin, C;  // input degree bounds, output bound, spin, C = 2 spin + 1 components
     int32_t R, G, Phi, A, B;     // rings, ring pairs per group (a multiple of 4), longitudes = A * B
-    int32_t pairs, nin, nout;    // pairs per work-group, values per input / output row
+    int32_t pairs, nin, nin2, nout;   // pairs per work-group, values per input row (first, second), output row
     int32_t n_lift, n_proj;      // lift / projection MFMA tiles
     int32_t acoef_len;           // elements of the lift coefficient operand in LDS
     int32_t hc_len;              // elements of the end-phase spectra of one pair
@@ -40,7 +45,7 @@ struct alignas(16) IstpDesc {
     int32_t wrow;                // projection weight entries per ring (row tiles * 16)
     int32_t lds_bytes;
     int32_t n_bcol;              // columns of the lift coefficient operand over all orders
-    int32_t pad[2];
+    int32_t flags;               // IstpFlags
 };
 
 // Lift tile: spectra of order +-am of 16 rows (ring, l - am parity; rings
@@ -63,10 +68,10 @@ struct alignas(16) ProjTile {
 // Device tables, one allocation per plan.
 template <typename T>
 struct IstpTables {
-    const T* lw;          // [am][ring < rpad][k < kp(am)]: P_{am+k}^{am}(x_ring), zero past L or R
+    const T* lw;          // [am][ring < rpad][k < kp(am)]: P_{am+k}^{am}(x_ring), zero past max(L, L2) or R
     const T* pw;          // [am][par][ring < rpad][row < wrow]: w_ring P_{am+par+2 row}^{am}(x_ring), zero past Lo or R
     const T* tw;          // [t < A][k2 < B + 1]: exp(-2 pi i t k2 / Phi), pass layout
-    const T* liftcg;      // [l][j - l + 1][q + 1][ml + l]: C^{j, ml+q}_{l, ml, 1, q} (spin 1)
+    const T* liftcg;      // [l][j - l + 1][q + 1][ml + l]: C^{j, ml+q}_{l, ml, 1, q} (spin 1), l <= max(L, L2)
     const T* coef;        // per output: three term weights and a pad (4 per output)
     const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), pad
     const LiftTile* lift;
@@ -83,17 +88,17 @@ struct IstpTables {
 // the spectra of every pair at `hc`, over the coefficient operand and the units.
 constexpr int kUnitSkew = 8;
 constexpr int kStageLoads = 18;         // staged elements per thread (one batch of loads)
-constexpr int kLiftTilesPerWave = 1;    // lift tiles whose weights a wave loads in one batch
 struct IstpLayout {
     int ptab, acoef, fbuf, hc;   // byte offsets
     int unit;              // complex entries per unit
     int bytes;             // total
 };
 __host__ __device__ inline int istp_align16(int v) { return (v + 15) & ~15; }
-// staged elements: both inputs of every pair (rounded to 4), then C^{j,ml+q}_{l,ml,1,q} (spin 1)
-__host__ __device__ inline int istp_stage_x(int P, int nin) { return (2 * P * nin + 3) & ~3; }
-__host__ __device__ inline int istp_stage_len(int P, int nin, int L, int spin) {
-    return istp_stage_x(P, nin) + (spin ? 9 * (L + 1) * (L + 1) : 0);
+// staged elements: both inputs of every pair (rounded to 4), then C^{j,ml+q}_{l,ml,1,q}
+// up to the larger input degree Lm (spin 1)
+__host__ __device__ inline int istp_stage_x(int P, int nin, int nin2) { return (P * (nin + nin2) + 3) & ~3; }
+__host__ __device__ inline int istp_stage_len(int P, int nin, int nin2, int Lm, int spin) {
+    return istp_stage_x(P, nin, nin2) + (spin ? 9 * (Lm + 1) * (Lm + 1) : 0);
 }
 template <typename T>
 __host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, int P, int acoef_len, int hc_len,

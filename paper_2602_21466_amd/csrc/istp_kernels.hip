@@ -58,31 +58,66 @@ template <typename T> __device__ __forceinline__ int lift_ring(int q, int h);
 template <> __device__ __forceinline__ int lift_ring<float>(int q, int h) { return 2 * q + h; }
 template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { return q + 4 * h; }
 
+// Time reversal of a row: value c of the reversed row is (-1)^(m+j-l+S) times
+// value src of the row, for the label (j, l) and order m that c holds.
+template <int S>
+__device__ __forceinline__ void reverse_index(int c, int* src, bool* neg) {
+    if (S == 0) {   // c = l^2 + l + m
+        int l = (int)sqrtf((float)c);
+        while ((l + 1) * (l + 1) <= c) ++l;
+        while (l * l > c) --l;
+        const int m = c - l * l - l;
+        *src = l * l + l - m;
+        *neg = m & 1;
+    } else {        // label (j, l) of c starts at 3 l^2 + {0, 2l - 1, 4l}[j - l + 1]
+        int l = (int)sqrtf((float)c / 3.0f);
+        while (3 * (l + 1) * (l + 1) <= c) ++l;
+        while (3 * l * l > c) --l;
+        const int r = c - 3 * l * l;
+        const int jj = r < 2 * l - 1 ? 0 : (r < 4 * l ? 1 : 2);
+        const int lo = jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l);
+        const int j = l - 1 + jj, m = r - lo - j;
+        *src = 3 * l * l + lo + j - m;
+        *neg = (m + jj) & 1;
+    }
+}
+
 // Step 0: the B operand of the lift for one pair tile (zero for pairs past N,
-// rows past L and padding columns).  The tile's input rows and the lift
-// couplings are first staged in LDS with one batch of loads per thread; then
-// every entry is formed from LDS, one thread per operand column (the plan's
-// column table gives its order and offset; padding columns are zero).  Column
-// order: sign of m (+ first), input, component, pair; negative orders carry
-// (-1)^am (P^{-m} = (-1)^m P^m).
+// rows past an input's degree bound and padding columns).  The tile's input
+// rows and the lift couplings are first staged in LDS with one batch of loads
+// per thread; then every entry is formed from LDS, per operand column (the
+// plan's column table gives its order and offset; padding columns are zero).
+// Column order: sign of m (+ first), input, component, pair; negative orders
+// carry (-1)^am (P^{-m} = (-1)^m P^m).  With kReverseSecond the second input
+// is staged time-reversed, x[(j,l), m] -> (-1)^(m+j-l+S) x[(j,l), -m].
 template <typename T, int S>
 __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                                    const T* __restrict__ x1, const T* __restrict__ x2, T* acoef,
                                                    T* stage) {
     constexpr int NC = 2 * S + 1;
-    const int L = d.L, P = d.pairs, nin = d.nin;
-    const int nx = 2 * P * nin, nxa = istp_stage_x(P, nin);
-    const int ncg = S ? 9 * (L + 1) * (L + 1) : 0;
+    const int P = d.pairs, nin = d.nin, nin2 = d.nin2;
+    const int Lm = d.L > d.L2 ? d.L : d.L2;
+    const int nx1 = P * nin, nx = nx1 + P * nin2, nxa = istp_stage_x(P, nin, nin2);
+    const int ncg = S ? 9 * (Lm + 1) * (Lm + 1) : 0;
+    const bool rev2 = d.flags & kReverseSecond;
     {
         T v[kStageLoads];
 #pragma unroll
         for (int u = 0; u < kStageLoads; ++u) {
             const int e = threadIdx.x + u * kThreads;
             v[u] = (T)0;
-            if (e < nx) {
-                const int r = e / nin, c = e - r * nin;
-                const int in = r / P, p = r - in * P;
-                if (p < np) v[u] = (in ? x2 : x1)[(p0 + p) * (int64_t)nin + c];
+            if (e < nx1) {
+                const int p = e / nin, c = e - p * nin;
+                if (p < np) v[u] = x1[(p0 + p) * (int64_t)nin + c];
+            } else if (e < nx) {
+                const int p = (e - nx1) / nin2, c = e - nx1 - p * nin2;
+                int src = c;
+                bool neg = false;
+                if (rev2) reverse_index<S>(c, &src, &neg);
+                if (p < np) {
+                    const T xv = x2[(p0 + p) * (int64_t)nin2 + src];
+                    v[u] = neg ? -xv : xv;
+                }
             } else if (e - nx < ncg) {
                 v[u] = tb.liftcg[e - nx];
             }
@@ -95,17 +130,16 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         }
     }
     lds_barrier();
-    // per operand column (order am, column col): its k rows
+    // per operand column (order am, column col): its k rows, in chunks of 8
     const T* cgs = stage + nxa;
     const int per_sign = 2 * NC * P;
-    // each column's k rows in chunks of 8, so that every thread takes part
-    const int nchunk = (L + 8) / 8;
+    const int nchunk = (Lm + 8) / 8;
     for (int it = threadIdx.x; it < d.n_bcol * nchunk; it += kThreads) {
         const int ci = it % d.n_bcol, k0 = 8 * (it / d.n_bcol);
         const int2 bc = tb.bcol[ci];
         const int am = bc.x & 255, col = bc.x >> 8;
         const int ncol = (am ? 2 : 1) * per_sign, cs = istp_cstride(ncol);
-        const int kp = (L - am + 4) / 4 * 4;
+        const int kp = (Lm - am + 4) / 4 * 4;
         if (k0 >= kp) continue;
         const int k1 = min(k0 + 8, kp);
         T* dst = acoef + bc.y;
@@ -117,12 +151,13 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
         const int m = sg ? -am : am;
         const T sign = (sg && (am & 1)) ? (T)-1 : (T)1;
-        const T* x = stage + (in * P + p) * nin;
+        const int Lin = in ? d.L2 : d.L;
+        const T* x = in ? stage + nx1 + p * nin2 : stage + p * nin;
 #pragma unroll 4
         for (int k = k0; k < k1; ++k) {
             const int l = am + k;
             T v = (T)0;
-            if (l <= L) {
+            if (l <= Lin) {
                 if (S == 0) {
                     v = x[l * l + l + m];
                 } else {
@@ -142,7 +177,7 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
     }
 }
 
-template <typename T, int A, int B, int S>
+template <typename T, int A, int B, int S, bool LONG>
 __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                           const T* __restrict__ x1, const T* __restrict__ x2, T* __restrict__ out,
                                           unsigned char* smem) {
@@ -159,9 +194,10 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, kq = lane >> 4;
-    const int L = d.L, Lo = d.Lo, R = d.R, G = d.G, P = d.pairs;
+    const int Lo = d.Lo, R = d.R, G = d.G, P = d.pairs;
+    const int Lm = d.L > d.L2 ? d.L : d.L2;   // largest input degree
     const IstpLayout ly =
-        istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len, istp_stage_len(P, d.nin, L, S), d.n_proj);
+        istp_layout<T>(A, B, NC, G, P, d.acoef_len, d.hc_len, istp_stage_len(P, d.nin, d.nin2, Lm, S), d.n_proj);
     C2* tw2 = reinterpret_cast<C2*>(smem);
     int* ptab = reinterpret_cast<int*>(smem + ly.ptab);
     T* acoef = reinterpret_cast<T*>(smem + ly.acoef);
@@ -202,60 +238,65 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         // reads: whole quads up to the grid's last ring (the group's other units
         // are never read)
         const int Uq = min(G, (R - rg0 + 3) & ~3) * P;
-        // ---- 1. lift on MFMA: a wave's tiles in batches of kLiftTilesPerWave, the
-        // weights of a batch loaded at once
+        // ---- 1. lift on MFMA: per tile, K in batches of kMaxLiftSteps steps whose
+        // weights are loaded at once
         {
             int ring0, par;
             lift_row<T>(li, ring0, par);
-            for (int tb0 = wave; tb0 < d.n_lift; tb0 += kWaves * kLiftTilesPerWave) {
-                T a[kLiftTilesPerWave][kMaxLiftSteps];
+            for (int ti = wave; ti < d.n_lift; ti += kWaves) {
+                const LiftTile lt = tb.lift[ti];
+                const int ring = 8 * lt.rb + ring0;
+                const bool rowok = ring < G && rg0 + ring < R;
+                const int voff = ((rg0 + ring) * lt.kp + kq) * (int)sizeof(T);
+                const T* bb = acoef + lt.acoef + kq * lt.cstride + li;
+                Acc da = Acc(0);
+                T a[kMaxLiftSteps];
+                if constexpr (!LONG) {
+                    // K <= 4 kMaxLiftSteps (every forward product): one batch of weights
 #pragma unroll
-                for (int t = 0; t < kLiftTilesPerWave; ++t) {
-                    const int ti = tb0 + kWaves * t;
-                    if (ti < d.n_lift) {
-                        const LiftTile lt = tb.lift[ti];
-                        const int ring = 8 * lt.rb + ring0;
-                        const bool rowok = ring < G && rg0 + ring < R;
-                        const int voff = ((rg0 + ring) * lt.kp + kq) * (int)sizeof(T);
-#pragma unroll
-                        for (int s = 0; s < kMaxLiftSteps; ++s) {
-                            const int k = 4 * s + kq;
-                            a[t][s] = (s < lt.steps && rowok && (k & 1) == par)
-                                          ? buffer_load<T>(lw_rsrc, voff + 4 * s * (int)sizeof(T), lt.lw * (int)sizeof(T))
-                                          : (T)0;
-                        }
+                    for (int s = 0; s < kMaxLiftSteps; ++s) {
+                        const int k = 4 * s + kq;
+                        a[s] = (s < lt.steps && rowok && (k & 1) == par)
+                                   ? buffer_load<T>(lw_rsrc, voff + 4 * s * (int)sizeof(T), lt.lw * (int)sizeof(T))
+                                   : (T)0;
                     }
-                }
-#pragma unroll
-                for (int t = 0; t < kLiftTilesPerWave; ++t) {
-                    const int ti = tb0 + kWaves * t;
-                    if (ti >= d.n_lift) break;
-                    const LiftTile lt = tb.lift[ti];
-                    Acc da = Acc(0);
-                    const T* bb = acoef + lt.acoef + kq * lt.cstride + li;
 #pragma unroll
                     for (int s = 0; s < kMaxLiftSteps; ++s)
-                        if (s < lt.steps) da = mfma16(a[t][s], bb[4 * s * lt.cstride], da);
-                    const int col = 16 * lt.ct + li;
-                    if (col < lt.ncol) {
-                        const int per_sign = 2 * NC * P;
-                        const int sg = col / per_sign, rem = col - sg * per_sign;
-                        const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
-                        const int n = sg ? Phi - lt.am : lt.am;
-                        C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+                        if (s < lt.steps) da = mfma16(a[s], bb[4 * s * lt.cstride], da);
+                } else {
+                    // the gradient product's degree-2L lift: K in batches
+                    for (int s0 = 0; s0 < lt.steps; s0 += kMaxLiftSteps) {
 #pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            const int r = 8 * lt.rb + lift_ring<T>(kq, h);
-                            if (r < G)
-                                dst[(size_t)r * P * ly.unit] =
-                                    cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
+                        for (int s = 0; s < kMaxLiftSteps; ++s) {
+                            const int k = 4 * (s0 + s) + kq;
+                            a[s] = (s0 + s < lt.steps && rowok && (k & 1) == par)
+                                       ? buffer_load<T>(lw_rsrc, voff + 4 * (s0 + s) * (int)sizeof(T),
+                                                        lt.lw * (int)sizeof(T))
+                                       : (T)0;
                         }
+#pragma unroll
+                        for (int s = 0; s < kMaxLiftSteps; ++s)
+                            if (s0 + s < lt.steps) da = mfma16(a[s], bb[4 * (s0 + s) * lt.cstride], da);
+                    }
+                }
+                const int col = 16 * lt.ct + li;
+                if (col < lt.ncol) {
+                    const int per_sign = 2 * NC * P;
+                    const int sg = col / per_sign, rem = col - sg * per_sign;
+                    const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
+                    const int n = sg ? Phi - lt.am : lt.am;
+                    C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int r = 8 * lt.rb + lift_ring<T>(kq, h);
+                        if (r < G)
+                            dst[(size_t)r * P * ly.unit] = cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
                     }
                 }
             }
         }
         lds_barrier();
-        // ---- 2. synthesis: pass 1 on rows (orders |m| > L are zero), pass 2 on columns
+        // ---- 2. synthesis: pass 1 on rows (orders |m| > Lm are zero), pass 2 on columns
         {
             const int ntask = Uq * NS * A;
             for (int task = tid; task < ntask; task += kThreads) {
@@ -266,7 +307,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                 for (int n2i = 0; n2i < B; ++n2i) {
                     const int n = t + A * n2i;
                     const int am = n <= Phi - n ? n : Phi - n;
-                    v[n2i] = am <= L ? row[n2i] : cmk<C2>((T)0, (T)0);
+                    v[n2i] = am <= Lm ? row[n2i] : cmk<C2>((T)0, (T)0);
                 }
                 Dft<B, true, C2>::run(v);
                 const C2* twr = tw2 + t * BP;
@@ -443,6 +484,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     const T* hp = hc + (size_t)p * hs;
                     T v = cf[u].x * hp[ix[u].x];
                     if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
+                    if (d.flags & kNegate) v = -v;
                     out[(p0 + p) * (int64_t)nout + o] = v;
                 }
             }
@@ -450,16 +492,19 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     }
 }
 
-template <typename T, int S>
+// LONG: lifts of more than 4 kMaxLiftSteps degrees (only the gradient
+// product's degree-2L input, fp32, Phi >= 72); a kernel of its own, so that
+// the forward kernels keep their register allocation.
+template <typename T, int S, bool LONG>
 __global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, IstpDesc d, const T* __restrict__ x1,
                                                            const T* __restrict__ x2, T* __restrict__ out, int64_t N) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int64_t p0 = (int64_t)blockIdx.x * d.pairs;
     const int np = (int)((N - p0) < d.pairs ? (N - p0) : d.pairs);
-#define ISTP_CASE(PHI, A_, B_)                                                        \
-    case PHI:                                                                         \
-        if constexpr (sizeof(T) == 4 || PHI <= 54)                                    \
-            istp_body<T, A_, B_, S>(tb, d, p0, np, x1, x2, out, smem);                \
+#define ISTP_CASE(PHI, A_, B_)                                                                      \
+    case PHI:                                                                                       \
+        if constexpr ((sizeof(T) == 4 || PHI <= 54) && (!LONG || (sizeof(T) == 4 && PHI >= 72)))    \
+            istp_body<T, A_, B_, S, LONG>(tb, d, p0, np, x1, x2, out, smem);                        \
         break;
     switch (d.Phi) {
         ISTP_CASE(1, 1, 1)
@@ -490,7 +535,12 @@ int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2,
     const int64_t grid = (N + d.pairs - 1) / d.pairs;
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
-    auto kern = d.spin ? istp_kernel<T, 1> : istp_kernel<T, 0>;
+    const int Lm = d.L > d.L2 ? d.L : d.L2;
+    const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
+    if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
+    void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t);
+    if (long_lift) kern = d.spin ? istp_kernel<T, 1, true> : istp_kernel<T, 0, true>;
+    else kern = d.spin ? istp_kernel<T, 1, false> : istp_kernel<T, 0, false>;
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;

@@ -18,15 +18,23 @@
 #include "cgtp_internal.h"
 #include "istp_internal.h"
 
-struct istp_plan_s {
-    int L = 0, spin = 0, dtype = 0, device = 0;
+// One product's descriptor and device tables.
+struct istp_prod {
     istp::IstpDesc desc{};
     void* dmem = nullptr;
-    size_t dbytes = 0;
     istp::IstpTables<float> tf{};
     istp::IstpTables<double> td{};
     int n_theta = 0, n_phi = 0;
     double flops_per_pair = 0, bytes_per_pair = 0;
+    bool ok = false;
+};
+
+// A plan holds the forward product (degrees L, L -> 2L) and, when it fits the
+// kernel's limits, the product its gradients use (degrees 2L, L -> L, second
+// input time-reversed).
+struct istp_plan_s {
+    int L = 0, spin = 0, dtype = 0, device = 0;
+    istp_prod fwd, bwd;
 };
 
 namespace {
@@ -86,13 +94,21 @@ struct Host {
     std::vector<int32_t> bcol;   // 2 per operand column
 };
 
+// Tables of the product of a degree-L1 and a degree-L2 input projected on
+// degrees <= Lo.  The grid is exact for every integrand: Gauss-Legendre with
+// n_theta >= (L1 + L2 + Lo + 1) / 2 nodes (even), Phi >= L1 + L2 + Lo + 1.
 template <typename T>
-int build(istp_plan_s* p, Host<T>& h) {
-    const int L = p->L, S = p->spin, NC = 2 * S + 1, Lo = 2 * L;
-    const int nt = 2 * L + 2, R = L + 1;
-    const int Phi = smallest_2a3b(4 * L + 1);
+int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
+    const int NC = 2 * S + 1, Lm = std::max(L1, L2);
+    const int D = L1 + L2 + Lo;
+    const int nmin = (D + 2) / 2;
+    const int nt = nmin + (nmin & 1), R = nt / 2;
+    const int Phi = smallest_2a3b(D + 1);
     int A = 0, B = 0;
     if (!cgtp::fft_factors(Phi, &A, &B)) return CGTP_EUNSUP;
+    if (Lm + 1 > 255) return CGTP_EUNSUP;   // the column table packs am in 8 bits
+    // lifts longer than 4 istp::kMaxLiftSteps degrees run in a kernel built for fp32, Phi >= 72
+    if (Lm + 1 > 4 * istp::kMaxLiftSteps && (sizeof(T) != 4 || Phi < 72)) return CGTP_EUNSUP;
 
     int nproj = 0;
     for (int am = 0; am <= Lo; ++am)
@@ -105,16 +121,16 @@ int build(istp_plan_s* p, Host<T>& h) {
     // then the most ring pairs (more units fill more of the work-group's
     // threads in the transform phases and take fewer passes over the rings).
     const int hc_len = NC * (Lo + 1) * (Lo + 1);
+    const int nin = (int)row_size(L1, S), nin2 = (int)row_size(L2, S);
     int bestP = 0, bestG = 0, bestBytes = 0;
-    const int nin = (int)row_size(L, S);
     for (int P : {8, 4, 2, 1}) {
         if (2 * NC * P > 16) continue;
         // inputs and couplings are staged with one batch of loads per thread
-        const int stage = 2 * P * nin + (S ? 9 * (L + 1) * (L + 1) : 0);
+        const int stage = P * (nin + nin2) + (S ? 9 * (Lm + 1) * (Lm + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
         for (int G : {16, 12, 8, 4}) {
-            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(L, NC, P), hc_len,
-                                                             istp::istp_stage_len(P, nin, L, S), nproj);
+            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(Lm, NC, P), hc_len,
+                                                             istp::istp_stage_len(P, nin, nin2, Lm, S), nproj);
             if (ly.bytes > istp::kLdsBudget) continue;
             if (P > bestP || (P == bestP && G > bestG)) {
                 bestP = P;
@@ -126,7 +142,8 @@ int build(istp_plan_s* p, Host<T>& h) {
     if (bestP == 0) return CGTP_EUNSUP;
     const int P = bestP, G = bestG;
     const int rpad = (R + G - 1) / G * G;
-    const int wrow = 16 * ((L + 1 + 15) / 16);   // most rows: am = 0, even parity, L + 1 of them
+    const int wrow = 16 * ((Lo / 2 + 1 + 15) / 16);   // most rows: am = 0, even parity
+    const int Lp = std::max(Lm, Lo);                   // Legendre table degree
 
     std::vector<double> xs(nt), ws(nt);
     if (cgtp_gauss_legendre(nt, xs.data(), ws.data()) != CGTP_OK) return CGTP_EINVAL;
@@ -134,20 +151,20 @@ int build(istp_plan_s* p, Host<T>& h) {
     std::vector<std::vector<double>> plm(R);
     for (int r = 0; r < R; ++r) {
         if (!(xs[r] > 0.0)) return CGTP_EINVAL;
-        plm[r].assign((Lo + 1) * (Lo + 2) / 2, 0.0);
-        cgtp_legendre(Lo, xs[r], plm[r].data());
+        plm[r].assign((Lp + 1) * (Lp + 2) / 2, 0.0);
+        cgtp_legendre(Lp, xs[r], plm[r].data());
     }
     auto pbar = [&](int r, int l, int m) { return plm[r][l * (l + 1) / 2 + m]; };
 
     // lift weights [am][ring][k]: P_{am+k}^{am}(x_ring)
-    std::vector<int> lw_off(L + 1);
-    for (int am = 0; am <= L; ++am) {
+    std::vector<int> lw_off(Lm + 1);
+    for (int am = 0; am <= Lm; ++am) {
         lw_off[am] = (int)h.lw.size();
-        const int kp = lift_kp(L, am);
+        const int kp = lift_kp(Lm, am);
         for (int r = 0; r < rpad; ++r)
             for (int k = 0; k < kp; ++k) {
                 const int l = am + k;
-                h.lw.push_back(r < R && l <= L ? (T)pbar(r, l, am) : (T)0);
+                h.lw.push_back(r < R && l <= Lm ? (T)pbar(r, l, am) : (T)0);
             }
     }
     // projection weights [am][par][ring][row]: w_ring P_{am+par+2 row}^{am}(x_ring)
@@ -168,9 +185,9 @@ int build(istp_plan_s* p, Host<T>& h) {
             h.tw[2 * (t * (B + 1) + k2) + 1] = (T)sinl(ang);
         }
     // lift couplings C^{j, ml+q}_{l, ml, 1, q}, j = l - 1, l, l + 1
-    h.liftcg.assign((size_t)9 * (L + 1) * (L + 1), (T)0);
+    h.liftcg.assign((size_t)9 * (Lm + 1) * (Lm + 1), (T)0);
     if (S == ISTP_VECTOR)
-        for (int l = 0; l <= L; ++l)
+        for (int l = 0; l <= Lm; ++l)
             for (int jj = 0; jj < 3; ++jj)
                 for (int c = 0; c < 3; ++c)
                     for (int ml = -l; ml <= l; ++ml) {
@@ -181,8 +198,8 @@ int build(istp_plan_s* p, Host<T>& h) {
                     }
     // coefficient operand geometry and lift tiles
     int aoff = 0;
-    for (int am = 0; am <= L; ++am) {
-        const int kp = lift_kp(L, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
+    for (int am = 0; am <= Lm; ++am) {
+        const int kp = lift_kp(Lm, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
         for (int col = 0; col < cs; ++col) h.bcol.insert(h.bcol.end(), {am | (col << 8), aoff + col});
         for (int rb = 0; rb < (G + 7) / 8; ++rb)
             for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
@@ -242,8 +259,9 @@ int build(istp_plan_s* p, Host<T>& h) {
             }
     }
 
-    istp::IstpDesc& d = p->desc;
-    d.L = L;
+    istp::IstpDesc& d = pr->desc;
+    d.L = L1;
+    d.L2 = L2;
     d.Lo = Lo;
     d.spin = S;
     d.C = NC;
@@ -253,7 +271,8 @@ int build(istp_plan_s* p, Host<T>& h) {
     d.A = A;
     d.B = B;
     d.pairs = P;
-    d.nin = (int32_t)row_size(L, S);
+    d.nin = nin;
+    d.nin2 = nin2;
     d.nout = (int32_t)nout;
     d.n_lift = (int32_t)h.lift.size();
     d.n_proj = (int32_t)h.proj.size();
@@ -264,25 +283,26 @@ int build(istp_plan_s* p, Host<T>& h) {
     d.wrow = wrow;
     d.lds_bytes = bestBytes;
     d.n_bcol = (int32_t)(h.bcol.size() / 2);
-    p->n_theta = nt;
-    p->n_phi = Phi;
+    d.flags = flags;
+    pr->n_theta = nt;
+    pr->n_phi = Phi;
 
     // model counts per pair (what include/istp.h documents)
-    const double fl_lift = 2.0 * 2 * NC * R * (double)(L + 1) * (L + 1);
+    const double fl_lift = 2.0 * NC * R * ((double)(L1 + 1) * (L1 + 1) + (double)(L2 + 1) * (L2 + 1));
     const double fl_syn = 2.0 * NC * R * fft_flops(Phi);
     const double fl_prod = (double)R * (Phi / 2 + 1) * 2 * (S == ISTP_GAUNT ? 6.0 : 6 * 6.0 + 3 * 2.0);
     const double fl_ana = (double)NC * R * fft_flops(Phi);
     const double fl_proj = 2.0 * NC * R * (double)no;
     const double fl_rec = S == ISTP_GAUNT ? 0.0 : 2.0 * 3 * (double)nout;
-    p->flops_per_pair = fl_lift + fl_syn + fl_prod + fl_ana + fl_proj + fl_rec;
-    p->bytes_per_pair = (double)(2 * d.nin + d.nout) * sizeof(T);
+    pr->flops_per_pair = fl_lift + fl_syn + fl_prod + fl_ana + fl_proj + fl_rec;
+    pr->bytes_per_pair = (double)(d.nin + d.nin2 + d.nout) * sizeof(T);
     return CGTP_OK;
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 template <typename T>
-int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
+int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     struct Part { const void* src; size_t bytes; size_t off; };
     Part parts[] = {
         {h.lw.data(), h.lw.size() * sizeof(T), 0},
@@ -317,7 +337,6 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         p->dmem = nullptr;
         return CGTP_EHIP;
     }
-    p->dbytes = total;
     char* base = (char*)p->dmem;
     tb->lw = (const T*)(base + parts[0].off);
     tb->pw = (const T*)(base + parts[1].off);
@@ -329,7 +348,58 @@ int upload(istp_plan_s* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->proj = (const istp::ProjTile*)(base + parts[7].off);
     tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
     tb->bcol = (const int2*)(base + parts[9].off);
+    p->ok = true;
     return CGTP_OK;
+}
+
+template <typename T> istp::IstpTables<T>* tables_of(istp_prod* pr);
+template <> istp::IstpTables<float>* tables_of<float>(istp_prod* pr) { return &pr->tf; }
+template <> istp::IstpTables<double>* tables_of<double>(istp_prod* pr) { return &pr->td; }
+
+// Builds and uploads one product; a product outside the kernel's limits is
+// left unbuilt (CGTP_EUNSUP) without an allocation.
+template <typename T>
+int make_prod(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, bool upload_tables) {
+    Host<T> h;
+    const int rc = build<T>(L1, L2, Lo, S, flags, pr, h);
+    if (rc != CGTP_OK || !upload_tables) return rc;
+    return upload<T>(pr, h, tables_of<T>(pr));
+}
+
+void free_prod(istp_prod* pr, int* rc) {
+    if (pr->dmem) {
+        const hipError_t e = hipFree(pr->dmem);
+        if (e != hipSuccess) {
+            cgtp::set_last_hip_error((int)e);
+            *rc = CGTP_EHIP;
+        }
+        pr->dmem = nullptr;
+    }
+}
+
+int launch_prod(const istp_plan_s* plan, const istp_prod& pr, int flags, const void* a, const void* b, void* out,
+                int64_t N, void* stream) {
+    istp::IstpDesc d = pr.desc;
+    d.flags = flags;
+    const int err = plan->dtype == CGTP_FP32
+                        ? istp::launch_istp_f32(pr.tf, d, (const float*)a, (const float*)b, (float*)out, N, stream)
+                        : istp::launch_istp_f64(pr.td, d, (const double*)a, (const double*)b, (double*)out, N,
+                                                stream);
+    if (err != 0) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
+
+int current_device_is(int device) {
+    int dev = -1;
+    const hipError_t de = hipGetDevice(&dev);
+    if (de != hipSuccess) {
+        cgtp::set_last_hip_error((int)de);
+        return CGTP_EHIP;
+    }
+    return dev == device ? CGTP_OK : CGTP_EINVAL;
 }
 
 }  // namespace
@@ -342,10 +412,17 @@ int64_t istp_num_outputs(int32_t L, int32_t spin) { return L < 0 ? -1 : row_size
 
 int64_t istp_label_offset(int32_t spin, int32_t j, int32_t l) { return label_offset(spin, j, l); }
 
-int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
-    if (!plan_out || L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return CGTP_EINVAL;
+static int check_plan_args(int32_t L, int32_t spin, int32_t dtype) {
+    if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return CGTP_EINVAL;
     if (dtype != CGTP_FP32 && dtype != CGTP_FP64) return CGTP_EDTYPE;
     if (L > (dtype == CGTP_FP32 ? ISTP_MAX_L_FP32 : ISTP_MAX_L_FP64)) return CGTP_EUNSUP;
+    return CGTP_OK;
+}
+
+int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
+    if (!plan_out) return CGTP_EINVAL;
+    int rc = check_plan_args(L, spin, dtype);
+    if (rc != CGTP_OK) return rc;
     istp_plan_s* p = new (std::nothrow) istp_plan_s();
     if (!p) return CGTP_ENOMEM;
     p->L = L;
@@ -357,17 +434,19 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
         delete p;
         return CGTP_EHIP;
     }
-    int rc;
-    if (dtype == CGTP_FP32) {
-        Host<float> h;
-        rc = build<float>(p, h);
-        if (rc == CGTP_OK) rc = upload<float>(p, h, &p->tf);
-    } else {
-        Host<double> h;
-        rc = build<double>(p, h);
-        if (rc == CGTP_OK) rc = upload<double>(p, h, &p->td);
+    rc = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, 0, &p->fwd, true)
+                            : make_prod<double>(L, L, 2 * L, spin, 0, &p->fwd, true);
+    if (rc == CGTP_OK) {
+        // the gradients' product; outside the kernel's limits it stays unbuilt
+        const int rb = dtype == CGTP_FP32
+                           ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true)
+                           : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true);
+        if (rb != CGTP_OK && rb != CGTP_EUNSUP) rc = rb;
     }
     if (rc != CGTP_OK) {
+        int ignored = CGTP_OK;
+        free_prod(&p->fwd, &ignored);
+        free_prod(&p->bwd, &ignored);
         delete p;
         return rc;
     }
@@ -376,37 +455,28 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
 }
 
 int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t* desc_out) {
-    if (!desc_out || L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return CGTP_EINVAL;
-    if (dtype != CGTP_FP32 && dtype != CGTP_FP64) return CGTP_EDTYPE;
-    if (L > (dtype == CGTP_FP32 ? ISTP_MAX_L_FP32 : ISTP_MAX_L_FP64)) return CGTP_EUNSUP;
-    istp_plan_s p;
-    p.L = L;
-    p.spin = spin;
-    p.dtype = dtype;
-    int rc;
-    if (dtype == CGTP_FP32) {
-        Host<float> h;
-        rc = build<float>(&p, h);
-    } else {
-        Host<double> h;
-        rc = build<double>(&p, h);
-    }
+    if (!desc_out) return CGTP_EINVAL;
+    int rc = check_plan_args(L, spin, dtype);
+    if (rc != CGTP_OK) return rc;
+    istp_prod pr, pb;
+    rc = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, 0, &pr, false)
+                            : make_prod<double>(L, L, 2 * L, spin, 0, &pr, false);
     if (rc != CGTP_OK) return rc;
     static_assert(sizeof(istp::IstpDesc) == 24 * sizeof(int32_t), "descriptor layout");
-    std::memcpy(desc_out, &p.desc, sizeof(istp::IstpDesc));
+    std::memcpy(desc_out, &pr.desc, sizeof(istp::IstpDesc));
+    // the gradients' product follows when it is within the kernel's limits
+    rc = dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false)
+                            : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false);
+    if (rc == CGTP_OK) std::memcpy(desc_out + 24, &pb.desc, sizeof(istp::IstpDesc));
+    else std::memset(desc_out + 24, 0, sizeof(istp::IstpDesc));
     return CGTP_OK;
 }
 
 int istp_destroy(istp_plan_t plan) {
     if (!plan) return CGTP_OK;
     int rc = CGTP_OK;
-    if (plan->dmem) {
-        hipError_t e = hipFree(plan->dmem);
-        if (e != hipSuccess) {
-            cgtp::set_last_hip_error((int)e);
-            rc = CGTP_EHIP;
-        }
-    }
+    free_prod(&plan->fwd, &rc);
+    free_prod(&plan->bwd, &rc);
     delete plan;
     return rc;
 }
@@ -414,11 +484,22 @@ int istp_destroy(istp_plan_t plan) {
 int istp_plan_query(istp_plan_t plan, int32_t* n_theta, int32_t* n_phi, int32_t* pairs_per_group,
                     double* flops_per_pair, double* bytes_per_pair) {
     if (!plan) return CGTP_EINVAL;
-    if (n_theta) *n_theta = plan->n_theta;
-    if (n_phi) *n_phi = plan->n_phi;
-    if (pairs_per_group) *pairs_per_group = plan->desc.pairs;
-    if (flops_per_pair) *flops_per_pair = plan->flops_per_pair;
-    if (bytes_per_pair) *bytes_per_pair = plan->bytes_per_pair;
+    if (n_theta) *n_theta = plan->fwd.n_theta;
+    if (n_phi) *n_phi = plan->fwd.n_phi;
+    if (pairs_per_group) *pairs_per_group = plan->fwd.desc.pairs;
+    if (flops_per_pair) *flops_per_pair = plan->fwd.flops_per_pair;
+    if (bytes_per_pair) *bytes_per_pair = plan->fwd.bytes_per_pair;
+    return CGTP_OK;
+}
+
+int istp_backward_query(istp_plan_t plan, int32_t* pairs_per_group, double* flops_per_pair,
+                        double* bytes_per_pair) {
+    if (!plan) return CGTP_EINVAL;
+    if (!plan->bwd.ok) return CGTP_EUNSUP;
+    if (pairs_per_group) *pairs_per_group = plan->bwd.desc.pairs;
+    // both gradients: two launches of the gradients' product
+    if (flops_per_pair) *flops_per_pair = 2 * plan->bwd.flops_per_pair;
+    if (bytes_per_pair) *bytes_per_pair = 2 * plan->bwd.bytes_per_pair;
     return CGTP_OK;
 }
 
@@ -428,27 +509,45 @@ int istp_forward(istp_plan_t plan, const void* x1, const void* x2, void* out, in
     if (!x1 || !x2 || !out) return CGTP_EINVAL;
     if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
-    const size_t nin = (size_t)plan->desc.nin, nout = (size_t)plan->desc.nout;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
     const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
     if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin)) return CGTP_EINVAL;
-    int dev = -1;
-    const hipError_t de = hipGetDevice(&dev);
-    if (de != hipSuccess) {
-        cgtp::set_last_hip_error((int)de);
-        return CGTP_EHIP;
+    const int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    return launch_prod(plan, plan->fwd, 0, x1, x2, out, N, hip_stream);
+}
+
+int istp_backward(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
+                  void* grad_x2, int64_t N, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (!plan->bwd.ok) return CGTP_EUNSUP;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2)) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)grad_out | (uintptr_t)grad_x1 | (uintptr_t)grad_x2) & 15)
+        return CGTP_EINVAL;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    const void* reads[3] = {x1, x2, grad_out};
+    const size_t rlen[3] = {bin, bin, bout};
+    void* writes[2] = {grad_x1, grad_x2};
+    for (void* w : writes) {
+        if (!w) continue;
+        for (int i = 0; i < 3; ++i)
+            if (overlaps(w, bin, reads[i], rlen[i])) return CGTP_EINVAL;
     }
-    if (dev != plan->device) return CGTP_EINVAL;
-    const int err = plan->dtype == CGTP_FP32
-                        ? istp::launch_istp_f32(plan->tf, plan->desc, (const float*)x1, (const float*)x2,
-                                                (float*)out, N, hip_stream)
-                        : istp::launch_istp_f64(plan->td, plan->desc, (const double*)x1, (const double*)x2,
-                                                (double*)out, N, hip_stream);
-    if (err != 0) {
-        cgtp::set_last_hip_error(err);
-        return CGTP_EHIP;
-    }
-    return CGTP_OK;
+    if (grad_x1 && grad_x2 && overlaps(grad_x1, bin, grad_x2, bin)) return CGTP_EINVAL;
+    int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    // d/dx1 <g, z(x1, x2)> = P(g, reversed x2); for x2 the roles swap, and the
+    // vector product changes sign under the swap
+    if (grad_x1) rc = launch_prod(plan, plan->bwd, istp::kReverseSecond, grad_out, x2, grad_x1, N, hip_stream);
+    if (rc == CGTP_OK && grad_x2)
+        rc = launch_prod(plan, plan->bwd, istp::kReverseSecond | (plan->spin == ISTP_VECTOR ? istp::kNegate : 0),
+                         grad_out, x1, grad_x2, N, hip_stream);
+    return rc;
 }
 
 }  // extern "C"

@@ -149,3 +149,85 @@ def test_largest_sizes():
         err, lab = per_label_rel_err(2 * L, spin, got, reference(L, spin, x1, x2))
         print("L=%d spin=%d %s worst %s %.3e" % (L, spin, dtype, lab, err))
         assert err <= TOL[dtype], (lab, err)
+
+
+# ---------------------------------------------------------------- gradients
+
+BACKWARD_CASES = [(1, 0, 5, "fp64"), (2, 1, 7, "fp64"), (3, 0, 9, "fp32"), (4, 1, 6, "fp32"), (6, 1, 5, "fp64"),
+                  (8, 0, 4, "fp32"), (5, 0, 3, "fp64"), (7, 1, 3, "fp32")]
+
+
+def run_backward(L, spin, x1, x2, g, dtype):
+    torch = _torch()
+    plan = _lib().IstpPlan(L, spin, dtype)
+    a, b, gg = x1.to("cuda"), x2.to("cuda"), g.to("cuda")
+    g1, g2 = plan.backward(a, b, gg)
+    torch.cuda.synchronize()
+    return g1.cpu().double().numpy(), g2.cpu().double().numpy()
+
+
+@pytest.mark.parametrize("L,spin,N,dtype", BACKWARD_CASES)
+def test_backward_small(L, spin, N, dtype):
+    """Both gradients against the oracle's derivative of the bilinear map, every pair."""
+    nin, nout = (2 * spin + 1) * (L + 1) ** 2, (2 * spin + 1) * (2 * L + 1) ** 2
+    x1, x2 = wl.draw_rows(nin, N, dtype, seed=2000 + 10 * L + spin)
+    g, _ = wl.draw_rows(nout, N, dtype, seed=3000 + 10 * L + spin)
+    got1, got2 = run_backward(L, spin, x1, x2, g, dtype)
+    ref1, ref2 = oi.product_vjp(spin, L, x1.double().numpy(), x2.double().numpy(), g.double().numpy())
+    e1, l1 = per_label_rel_err(L, spin, got1, ref1)
+    e2, l2 = per_label_rel_err(L, spin, got2, ref2)
+    print("backward L=%d spin=%d N=%d %s worst labels %s %.3e, %s %.3e" % (L, spin, N, dtype, l1, e1, l2, e2))
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (l1, e1, l2, e2)
+
+
+@pytest.mark.parametrize("L,spin", [(18, 1), (31, 0), (16, 1)])
+def test_backward_largest(L, spin):
+    """The largest fp32 gradient products: <g, z(x1, x2)> = <grad_x1, x1> = <grad_x2, x2> with the GPU forward,
+    and (where the oracle's degree range allows) the time-reversed product of the oracle on one pair."""
+    torch = _torch()
+    nin, nout = (2 * spin + 1) * (L + 1) ** 2, (2 * spin + 1) * (2 * L + 1) ** 2
+    x1, x2 = wl.draw_rows(nin, 6, "fp32", seed=4000 + L)
+    g, _ = wl.draw_rows(nout, 6, "fp32", seed=4100 + L)
+    plan = _lib().IstpPlan(L, spin, "fp32")
+    a, b, gg = x1.cuda(), x2.cuda(), g.cuda()
+    z = plan.forward(a, b)
+    g1, g2 = plan.backward(a, b, gg)
+    torch.cuda.synchronize()
+    z, g1, g2 = (t.double().cpu().numpy() for t in (z, g1, g2))
+    want = (g.double().numpy() * z).sum(1)
+    scale = np.abs(g.double().numpy()).sum(1) * np.abs(z).max(1)
+    assert np.all(np.abs((g1 * x1.double().numpy()).sum(1) - want) <= 1e-5 * scale)
+    assert np.all(np.abs((g2 * x2.double().numpy()).sum(1) - want) <= 1e-5 * scale)
+    if 2 * L <= 36:
+        fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+        from test_istp_oracle import _reverse
+        ref1 = fn(2 * L, g[:1].double().numpy(), _reverse(spin, L, x2[:1].double().numpy()), L2=L, Lo=L)
+        e1, lab = per_label_rel_err(L, spin, g1[:1], ref1)
+        print("backward L=%d spin=%d worst label %s rel err %.3e" % (L, spin, lab, e1))
+        assert e1 <= TOL["fp32"], (lab, e1)
+
+
+def test_backward_errors():
+    torch = _torch()
+    lib = _lib()
+    plan = lib.IstpPlan(3, 1, "fp32")
+    x = torch.zeros((4, plan.nin), device="cuda")
+    g = torch.zeros((4, plan.nout), device="cuda")
+    gx = torch.zeros((4, plan.nin), device="cuda")
+    lib.istp_backward(plan._h, x.data_ptr(), x.data_ptr(), g.data_ptr(), gx.data_ptr(), None, 0, None)
+    with pytest.raises(lib.CgtpError) as e:   # no gradient asked for
+        lib.istp_backward(plan._h, x.data_ptr(), x.data_ptr(), g.data_ptr(), None, None, 4, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:   # a gradient over an input
+        lib.istp_backward(plan._h, x.data_ptr(), x.data_ptr(), g.data_ptr(), x.data_ptr(), None, 4, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:   # the two gradients overlap
+        lib.istp_backward(plan._h, x.data_ptr(), x.data_ptr(), g.data_ptr(), gx.data_ptr(), gx.data_ptr(), 4, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    big = lib.IstpPlan(24, 1, "fp32")   # forward only: the degree-48 lift does not fit
+    with pytest.raises(lib.CgtpError) as e:
+        big.backward_query()
+    assert e.value.code == lib.CGTP_EUNSUP
+    q = plan.backward_query()
+    assert q["flops_per_pair"] > 0 and q["pairs_per_group"] >= 1
+    torch.cuda.synchronize()
