@@ -5,7 +5,8 @@ pair: lift, products, lower, per-path recovery), inputs already resident in
 HBM.  The headline workload is L = 32, N = 1024 pairs, fp32; L = 16,
 N = 8192 is reported beside it.  The multiple-input, multiple-output Gaunt
 and vector signal products (istp_forward) are timed after it, each with its
-own roofline and oracle baseline, under "istp".  Prints ONE JSON line.
+own roofline and oracle baseline, under "istp" (with the gradients,
+istp_backward, where the plan supports them).  Prints ONE JSON line.
 """
 from __future__ import annotations
 
@@ -33,13 +34,14 @@ PEAK_HBM_GBS = 8000.0
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
     "707686cb0dab3812": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 344839.9, "fetch_scale": 1.999956, "write_kib": 4938811.7, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 203731.7, "fetch_scale": 1.999956, "write_kib": 2742205.0, "write_scale": 1.000000},
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 345284.1, "fetch_scale": 1.999956, "write_kib": 4938434.0, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 203652.3, "fetch_scale": 1.999956, "write_kib": 2742194.3, "write_scale": 1.000000},
     },
-    "06ff40e7d5cbde86": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 296684.2, "fetch_scale": 1.999956, "write_kib": 811650.4, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 401054.0, "fetch_scale": 1.999956, "write_kib": 1084204.4, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 228024.4, "fetch_scale": 1.999956, "write_kib": 872600.2, "write_scale": 1.000000},
+    "545058b994e012ad": {
+        "vstp_L32_N16384_fp32": {"fetch_kib": 297877.1, "fetch_scale": 1.999956, "write_kib": 811651.5, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 403875.2, "fetch_scale": 1.999956, "write_kib": 1084122.9, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227619.7, "fetch_scale": 1.999956, "write_kib": 837122.6, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1076461.6, "fetch_scale": 1.999956, "write_kib": 447488.0, "write_scale": 1.000000},
     },
 }
 
@@ -121,6 +123,21 @@ def time_istp(w, steps, warmup):
     out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
     res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": plan.query(), "kind": "istp"}
     res.update(_time_launches(lambda st: plan.forward(a, b, out, st), w.N, steps, warmup))
+    # both gradients (two launches of the adjoint product), where the plan has it
+    try:
+        bq = plan.backward_query()
+    except lib.CgtpError:
+        bq = None
+    if bq is not None:
+        g = torch.randn(out.shape, generator=torch.Generator("cpu").manual_seed(w.seed + 2),
+                        dtype=torch.float64).to(out.dtype).cuda()
+        g1, g2 = torch.empty_like(a), torch.empty_like(b)
+        bwd = {"workload": w.name + ":backward", "L": w.L, "N": w.N, "dtype": w.dtype, "plan": bq, "kind": "istp"}
+        bwd.update(_time_launches(lambda st: lib.istp_backward(plan._h, a.data_ptr(), b.data_ptr(), g.data_ptr(),
+                                                               g1.data_ptr(), g2.data_ptr(), w.N, st.cuda_stream),
+                                  w.N, steps, warmup))
+        res["backward"] = bwd
+        del g, g1, g2
     plan.close()
     del out, a, b
     torch.cuda.empty_cache()
@@ -286,8 +303,14 @@ def main():
             log("timing %s" % wi.name)
             ri = time_istp(wi, args.steps, args.warmup)
             log("  %.4f ms/step, %.4g pairs/s" % (ri["ms_per_step"], ri["value"]))
-            istp.append({"workload": wi.name, "value": round(ri["value"], 1), "unit": "pairs/s",
-                         "ms_per_step": round(ri["ms_per_step"], 4), "roofline": roofline(ri)})
+            entry = {"workload": wi.name, "value": round(ri["value"], 1), "unit": "pairs/s",
+                     "ms_per_step": round(ri["ms_per_step"], 4), "roofline": roofline(ri)}
+            if "backward" in ri:
+                rb = ri["backward"]
+                log("  backward (both gradients) %.4f ms/step, %.4g pairs/s" % (rb["ms_per_step"], rb["value"]))
+                entry["backward"] = {"value": round(rb["value"], 1), "unit": "pairs/s",
+                                     "ms_per_step": round(rb["ms_per_step"], 4), "roofline": roofline(rb)}
+            istp.append(entry)
     line = {
         "metric": METRIC, "value": round(main_res["value"], 1), "unit": "pairs/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(main_res["ms_per_step"], 4),
