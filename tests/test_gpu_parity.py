@@ -238,3 +238,44 @@ def test_forward_rejects_overlap_and_misalignment():
     with pytest.raises(lib.CgtpError) as e:
         lib.cgtp_forward(plan._h, x.data_ptr() + 4, x.data_ptr(), buf.data_ptr() + 4 * 200, 1, None)
     assert e.value.code == lib.CGTP_EINVAL
+
+
+def _exchange_index(L):
+    """Column of path (l2, l1, l3) for every column of path (l1, l2, l3), and the sign (-1)^(l1+l2-l3)."""
+    n = (L + 1) ** 4
+    idx = np.empty(n, dtype=np.int64)
+    sign = np.empty(n)
+    for l1 in range(L + 1):
+        for l2 in range(L + 1):
+            for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+                a = oracle.path_offset(L, l1, l2, l3)
+                b = oracle.path_offset(L, l2, l1, l3)
+                idx[a:a + 2 * l3 + 1] = np.arange(b, b + 2 * l3 + 1)
+                sign[a:a + 2 * l3 + 1] = (-1.0) ** ((l1 + l2 - l3) % 2)
+    return idx, sign
+
+
+def test_exchange_symmetry_full_workload():
+    """Every pair of the L = 8 workload: z^(l2,l1,l3)(x2, x1) = (-1)^(l1+l2-l3) z^(l1,l2,l3)(x1, x2) (CG symmetry),
+    per-path relative L2 <= 1e-4; and the alternate cover (dot / scalar-vector products) agrees with the default."""
+    torch = _torch()
+    w = wl.BY_L[8]
+    x1, x2 = wl.workload_inputs(w)
+    lib = _lib()
+    plan = lib.Plan(w.L, dtype=w.dtype)
+    alt = lib.Plan(w.L, dtype=w.dtype, cover=lib.CGTP_COVER_ALTERNATE)
+    a, b = x1.cuda(), x2.cuda()
+    z = plan.forward(a, b)
+    zs = plan.forward(b, a)
+    idx, sign = _exchange_index(w.L)
+    zs = zs[:, torch.as_tensor(idx, device="cuda")] * torch.as_tensor(sign, device="cuda", dtype=zs.dtype)
+    pid, paths = path_ids(w.L)
+    pid_t = torch.as_tensor(pid, device="cuda")
+    for other, what in ((zs, "exchange"), (alt.forward(a, b), "alternate cover")):
+        num = torch.zeros(len(paths), device="cuda", dtype=torch.float64).index_add_(
+            0, pid_t, ((other - z).double() ** 2).sum(0))
+        den = torch.zeros(len(paths), device="cuda", dtype=torch.float64).index_add_(0, pid_t, (z.double() ** 2).sum(0))
+        rel = (num / den.clamp_min(1e-30)).sqrt().max().item()
+        print("%s: worst per-path relative L2 %.3e over %d pairs" % (what, rel, w.N), flush=True)
+        assert rel <= 1e-4, what
+    torch.cuda.synchronize()
