@@ -119,11 +119,13 @@ __host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, in
 }
 
 // Lift coefficient operand: k rows of an order am are `cstride` elements apart,
-// 16 per column tile plus 16 when the tile count is even (rows k and k + 1 of
-// one MFMA operand then fall on opposite bank halves).
+// 16 per column tile.  (Padding the stride to an odd number of 16-element
+// halves would keep rows k and k + 1 of one MFMA operand on opposite bank
+// halves, but the space it takes costs more pairs per work-group than the
+// conflicts it saves.)
 __host__ __device__ inline int istp_cstride(int ncol) {
     const int nct = (ncol + 15) / 16;
-    return 16 * nct + ((nct & 1) ? 0 : 16);
+    return 16 * nct;
 }
 
 int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
