@@ -49,6 +49,8 @@ MEASURED_TRAFFIC = {
 DIGEST_SOURCES = {
     "cgtp": ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "istp": ("istp_kernels.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
+    "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
+                 "device_common.h"),
 }
 
 
@@ -140,6 +142,34 @@ def time_istp(w, steps, warmup):
         del g, g1, g2
     plan.close()
     del out, a, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def time_channels(w, steps, warmup):
+    """Channel-wise CGTP with path weights: N pairs x C channels = N C rows per launch."""
+    import torch
+
+    import cgtp_inputs
+    import paper_2602_21466_amd as lib
+
+    x1, x2, wt = cgtp_inputs.channel_inputs(w.L, w.N, w.C, w.x2_shared, w.weights, w.dtype, w.seed)
+    plan = lib.Plan(w.L, dtype=w.dtype)
+    a, b = x1.cuda(), x2.cuda()
+    wc = wt.cuda() if wt is not None else None
+    rows = w.N * w.C
+    nout = (w.L + 1) ** 4
+    out = torch.empty((w.N, w.C, nout), dtype=a.dtype, device="cuda")
+    q = dict(plan.query())
+    # compulsory bytes per row: x1 row, the x2 row (shared by C rows), weights, output row
+    esz = a.element_size()
+    nin = (w.L + 1) ** 2
+    wbytes = 0 if wc is None else wc.numel() * esz / rows
+    q["bytes_per_pair"] = esz * (nin * (1 + (1 / w.C if w.x2_shared else 1)) + nout) + wbytes
+    res = {"workload": w.name, "L": w.L, "N": rows, "dtype": w.dtype, "plan": q, "kind": "channels"}
+    res.update(_time_launches(lambda st: plan.forward_weighted(a, b, wc, out, st), rows, steps, warmup))
+    plan.close()
+    del out, a, b, wc
     torch.cuda.empty_cache()
     return res
 
@@ -262,6 +292,8 @@ def main():
     ap.add_argument("--secondary", default="cgtp_L16_N8192_fp32")
     ap.add_argument("--istp", default=",".join(x.name for x in cgtp_inputs.ISTP_WORKLOADS),
                     help="comma-separated signal-product workloads, or 'none'")
+    ap.add_argument("--channels", default=",".join(x.name for x in cgtp_inputs.CHANNEL_WORKLOADS),
+                    help="comma-separated channel-wise (path-weighted) CGTP workloads, or 'none'")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--istp-cpu-seconds", type=float, default=4.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -295,6 +327,18 @@ def main():
             log("  %.4f ms/step, %.4g pairs/s" % (r2["ms_per_step"], r2["value"]))
             secondary.append({"workload": r2["workload"], "value": round(r2["value"], 1), "unit": "pairs/s",
                               "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)})
+    channels = []
+    if args.channels and args.channels != "none":
+        by_ch = {x.name: x for x in cgtp_inputs.CHANNEL_WORKLOADS}
+        for name in args.channels.split(","):
+            wc = by_ch[name]
+            log("timing %s" % wc.name)
+            rc = time_channels(wc, args.steps, args.warmup)
+            log("  %.4f ms/step, %.4g rows/s" % (rc["ms_per_step"], rc["value"]))
+            channels.append({"workload": wc.name, "value": round(rc["value"], 1), "unit": "rows/s",
+                             "rows": rc["N"], "pairs": wc.N, "channels": wc.C, "x2_shared": wc.x2_shared,
+                             "weights": wc.weights, "ms_per_step": round(rc["ms_per_step"], 4),
+                             "roofline": roofline(rc)})
     istp = []
     if args.istp and args.istp != "none":
         by_istp = {x.name: x for x in cgtp_inputs.ISTP_WORKLOADS}
@@ -320,6 +364,7 @@ def main():
                    "grid": "per-block minimal exact Gauss-Legendre x FFT", "cover": "scalar-scalar + cross"},
         "roofline": roofline(main_res),
         "secondary": secondary,
+        "channels": channels,
         "istp": istp,
     }
     if not args.no_cpu_baseline:

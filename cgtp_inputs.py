@@ -83,6 +83,64 @@ def draw_rows(ncols: int, N: int, dtype: str = "fp32", seed: int = 0):
     return x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype))
 
 
+# Channel-wise CGTP with path weights: x1 [N, C, (L+1)^2]; x2 [N, (L+1)^2]
+# when shared by the channels of a pair, else [N, C, (L+1)^2]; weights
+# [C, P] (one row per channel) or [N, C, P] (per pair), P = number of paths.
+# Same recipe (iid N(0, 1) in float64, then cast), seed L + 200; x1, then x2,
+# then the weights are drawn from one generator.
+def num_paths(L: int) -> int:
+    """Paths (l1, l2, l3) of degree L: sum over l1, l2 of 2 min(l1, l2) + 1."""
+    return (L + 1) * (2 * L * L + 4 * L + 3) // 3
+
+
+@dataclass(frozen=True)
+class ChannelWorkload:
+    name: str
+    L: int
+    N: int                # pairs
+    C: int                # channels
+    x2_shared: bool
+    weights: str          # "none" | "channel" | "pair"
+    dtype: str
+    check_rows: int       # 0: every (pair, channel) row; else a seeded subsample of rows
+
+    @property
+    def seed(self) -> int:
+        return self.L + 200
+
+
+def channel_inputs(L: int, N: int, C: int, x2_shared: bool, weights: str, dtype: str = "fp32", seed: int = 0):
+    """(x1, x2, w) as CPU torch tensors; w is None for weights == "none"."""
+    import torch
+    g = torch.Generator("cpu").manual_seed(seed)
+    nin = (L + 1) ** 2
+    x1 = torch.randn(N, C, nin, dtype=torch.float64, generator=g)
+    x2 = torch.randn(*((N, nin) if x2_shared else (N, C, nin)), dtype=torch.float64, generator=g)
+    w = None
+    if weights != "none":
+        shape = (C, num_paths(L)) if weights == "channel" else (N, C, num_paths(L))
+        w = torch.randn(*shape, dtype=torch.float64, generator=g).to(torch_dtype(dtype))
+    return x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype)), w
+
+
+def channel_check_rows(wk: ChannelWorkload):
+    """Sorted (pair, channel) row indices checked against the oracle."""
+    import torch
+    rows = wk.N * wk.C
+    if not wk.check_rows or wk.check_rows >= rows:
+        return list(range(rows))
+    g = torch.Generator("cpu").manual_seed(wk.seed + 1)
+    return sorted(torch.randperm(rows, generator=g)[: wk.check_rows].tolist())
+
+
+# A message-passing layer at the headline degree: 512 pairs (edges) of 16
+# channels, the second input (the edge's harmonics) shared by the channels,
+# one weight per path and channel.  8192 rows, as many as the L = 16 workload.
+CHANNEL_WORKLOADS = [
+    ChannelWorkload("cgtp_L16_N512_C16_fp32_x2shared_weighted", 16, 512, 16, True, "channel", "fp32", 8),
+]
+
+
 # Multiple-input, multiple-output signal products: spin 0 (Gaunt) rows hold
 # (L+1)^2 values, spin 1 (vector) rows 3 (L+1)^2; same recipe as above
 # (seed L + 100 spin), checked on a seeded subsample of pairs.

@@ -112,6 +112,51 @@ int cgtp_plan(int32_t L, const cgtp_grid *grid, cgtp_plan_t *plan_out);
 int cgtp_forward(cgtp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N,
                  void *hip_stream);
 
+/*
+ * Multiplicity channels and path weights.  A network layer carries C copies
+ * (channels) of every irrep; the method is applied to each channel, and the
+ * output of every path is scaled by a weight, the per-irrep linear maps
+ * around the tensor product that the expressivity count of Appendix E
+ * allows (Schur's lemma leaves one scalar per path).
+ *   channels:          C >= 1.
+ *   x2_shared:         0: x2 is [N, C, (L+1)^2], channel c of pair n meets
+ *                      channel c of x1; 1: x2 is [N, (L+1)^2], row n meets
+ *                      every channel of pair n (e.g. spherical harmonics of
+ *                      an edge direction).
+ *   weights_per_pair:  0: weights [C, P], shared by all pairs (a layer's
+ *                      parameters); 1: weights [N, C, P] (per-pair weights,
+ *                      e.g. from a radial network).  P = cgtp_num_paths(L).
+ *   reserved:          must be 0.
+ */
+typedef struct {
+    int32_t channels;
+    int32_t x2_shared;
+    int32_t weights_per_pair;
+    int32_t reserved;
+} cgtp_channels;
+
+/*
+ * Channel-wise CGTP with path weights, asynchronously on hip_stream.
+ *   out[n, c, cgtp_path_offset(L, l1, l2, l3) + l3 + m3]
+ *     = w[(n,) c, cgtp_path_index(L, l1, l2, l3)] * z^(l1,l2,l3)_m3(x1[n, c], x2[n, c] or x2[n])
+ * x1: [N, C, (L+1)^2]; out: [N, C, (L+1)^4]; x2 and weights as described at
+ * cgtp_channels; all device arrays of the plan's dtype, row-major and
+ * contiguous; x1, x2 and out 16-byte aligned, weights element-aligned.
+ * weights == NULL means every weight is 1; ch == NULL means one channel,
+ * x2 not shared.  CGTP_EINVAL for a bad channel description, out overlapping
+ * any input, or sizes whose byte count overflows.  Otherwise as cgtp_forward
+ * (which equals this call with C = 1 and no weights).
+ */
+int cgtp_forward_weighted(cgtp_plan_t plan, const void *x1, const void *x2, const void *weights, void *out,
+                          int64_t N, const cgtp_channels *ch, void *hip_stream);
+
+/* Number of paths of degree L: sum over l1, l2 <= L of 2 min(l1, l2) + 1; -1 for L < 0. */
+int64_t cgtp_num_paths(int32_t L);
+
+/* Index of path (l1, l2, l3) in the (l1, l2, l3) order of all paths of degree L
+   (the layout of a weight row); -1 if it is not a path. */
+int64_t cgtp_path_index(int32_t L, int32_t l1, int32_t l2, int32_t l3);
+
 /* Frees the plan's device tables.  NULL is a no-op. */
 int cgtp_destroy(cgtp_plan_t plan);
 

@@ -48,6 +48,11 @@ class cgtp_grid(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("cover", ctypes.c_int32)]
 
 
+class cgtp_channels(ctypes.Structure):
+    _fields_ = [("channels", ctypes.c_int32), ("x2_shared", ctypes.c_int32),
+                ("weights_per_pair", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 def _load():
     global _lib
     if _lib is not None:
@@ -60,6 +65,9 @@ def _load():
     sig = {
         "cgtp_plan": (ctypes.c_int, [i32, ctypes.POINTER(cgtp_grid), ctypes.POINTER(vp)]),
         "cgtp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
+        "cgtp_forward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, ctypes.POINTER(cgtp_channels), vp]),
+        "cgtp_num_paths": (i64, [i32]),
+        "cgtp_path_index": (i64, [i32, i32, i32, i32]),
         "cgtp_destroy": (ctypes.c_int, [vp]),
         "cgtp_num_outputs": (i64, [i32]),
         "cgtp_path_offset": (i64, [i32, i32, i32, i32]),
@@ -95,7 +103,7 @@ def _load():
 
 def exported_symbols():
     """Names of the C ABI entry points this binding expects."""
-    return ["cgtp_plan", "cgtp_forward", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
+    return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
@@ -129,6 +137,24 @@ def cgtp_forward(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, stream_pt
     rc = _load().cgtp_forward(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(out_ptr),
                               int(N), ctypes.c_void_p(stream_ptr) if stream_ptr else None)
     _check(rc, "cgtp_forward")
+
+
+def cgtp_forward_weighted(plan, x1_ptr: int, x2_ptr: int, w_ptr: int | None, out_ptr: int, N: int,
+                          channels: int = 1, x2_shared: bool = False, weights_per_pair: bool = False,
+                          stream_ptr: int | None = None) -> None:
+    ch = cgtp_channels(int(channels), int(bool(x2_shared)), int(bool(weights_per_pair)), 0)
+    rc = _load().cgtp_forward_weighted(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr),
+                                       ctypes.c_void_p(w_ptr) if w_ptr else None, ctypes.c_void_p(out_ptr),
+                                       int(N), ctypes.byref(ch), ctypes.c_void_p(stream_ptr) if stream_ptr else None)
+    _check(rc, "cgtp_forward_weighted")
+
+
+def cgtp_num_paths(L: int) -> int:
+    return int(_load().cgtp_num_paths(int(L)))
+
+
+def cgtp_path_index(L: int, l1: int, l2: int, l3: int) -> int:
+    return int(_load().cgtp_path_index(int(L), int(l1), int(l2), int(l3)))
 
 
 def cgtp_destroy(plan) -> None:
@@ -287,6 +313,33 @@ class Plan:
             raise ValueError("out must be a contiguous %s tensor [N, (L+1)^4]" % tdt)
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         cgtp_forward(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, s.cuda_stream)
+        return out
+
+    def forward_weighted(self, x1, x2, weights=None, out=None, stream=None):
+        """x1: [N, C, (L+1)^2]; x2: [N, C, (L+1)^2] or [N, (L+1)^2] (shared by the channels);
+        weights: None, [C, P] or [N, C, P] with P = cgtp_num_paths(L).  Returns [N, C, (L+1)^4]."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        nin, npaths = (self.L + 1) ** 2, cgtp_num_paths(self.L)
+        if not x1.is_cuda or x1.dtype != tdt or x1.dim() != 3 or x1.shape[2] != nin or not x1.is_contiguous():
+            raise ValueError("x1 must be a contiguous %s CUDA tensor [N, C, %d]" % (tdt, nin))
+        N, C = x1.shape[0], x1.shape[1]
+        if x2.dtype != tdt or not x2.is_cuda or not x2.is_contiguous() or tuple(x2.shape) not in ((N, C, nin), (N, nin)):
+            raise ValueError("x2 must be a contiguous %s CUDA tensor [N, C, %d] or [N, %d]" % (tdt, nin, nin))
+        shared = x2.dim() == 2
+        per_pair = False
+        if weights is not None:
+            if weights.dtype != tdt or not weights.is_cuda or not weights.is_contiguous() or \
+                    tuple(weights.shape) not in ((C, npaths), (N, C, npaths)):
+                raise ValueError("weights must be a contiguous %s CUDA tensor [C, %d] or [N, C, %d]" % (tdt, npaths, npaths))
+            per_pair = weights.dim() == 3
+        if out is None:
+            out = torch.empty((N, C, cgtp_num_outputs(self.L)), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, C, cgtp_num_outputs(self.L)):
+            raise ValueError("out must be a contiguous %s tensor [N, C, (L+1)^4]" % tdt)
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        cgtp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), weights.data_ptr() if weights is not None else None,
+                              out.data_ptr(), N, C, shared, per_pair, s.cuda_stream)
         return out
 
     def close(self):

@@ -73,6 +73,7 @@ struct alignas(16) BlockDesc {
     int32_t rpad;              // rings of the weight table: R rounded up to the ring group
     int32_t wrow;              // entries per ring row of the weight table
     int32_t mode;              // BlockMode: where the projection reads its spectra
+    int32_t path_off;          // index of path (j1, j2, |j1 - j2|) in the (l1, l2, l3) order of all paths
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
@@ -100,7 +101,8 @@ struct Tables {
     const T* tw;        // per Phi, complex pairs in pass layout: [t < A][k2 < B+1] = exp(-2 pi i t k2 / Phi)
     const T* lcg;       // [j][q+1][m + j] = C^{j, m+q}_{j, m, 1, q}
     const T* coef;      // per block and output (j3, m3): up to three term weights (4 per output)
-    const int32_t* coefi;   // per block and output: end-phase entries of the terms for pair 0, single-term flag
+    const int32_t* coefi;   // per block and output: end-phase entries of the terms for pair 0; bit 0 of the
+                            // fourth word flags a single term, the bits above it hold j3 - |j1 - j2|
     const TileDesc* tdesc;
     int32_t wtab_len;   // elements of wtab
     const BlockDesc* blocks;
@@ -158,11 +160,31 @@ struct TileGeom {
 void set_last_hip_error(int code);
 
 // Launches the block kernel over the whole map; returns a hipError_t value.
+// Multiplicity channels and path weights of a launch.  The N rows of x1 and
+// out are (pair, channel) rows, channel fastest.  x2 holds one row per row of
+// x1, or with kX2Shared one row per pair (row r / channels).  With w set, path
+// (l1, l2, l3) of row r is scaled by w[k * npaths + path], k = r
+// (kWeightsPerRow) or r mod channels.
+enum ChanFlags : int32_t { kX2Shared = 1, kWeightsPerRow = 2 };
+template <typename T>
+struct ChanArgs {
+    const T* w;        // NULL: unweighted
+    int32_t channels;  // >= 1
+    int32_t flags;     // ChanFlags
+    int32_t npaths;
+};
+
 int launch_blocks_f32(const Tables<float>& tb, const int32_t* block_list, const LaunchMap& map,
                       int lds_bytes, const float* x1, const float* x2, float* out, int64_t N,
                       int L, void* stream);
 int launch_blocks_f64(const Tables<double>& tb, const int32_t* block_list, const LaunchMap& map,
                       int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
                       int L, void* stream);
+int launch_blocks_channels_f32(const Tables<float>& tb, const int32_t* block_list, const LaunchMap& map,
+                               int lds_bytes, const float* x1, const float* x2, float* out, int64_t N,
+                               int L, const ChanArgs<float>& ch, void* stream);
+int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* block_list, const LaunchMap& map,
+                               int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
+                               int L, const ChanArgs<double>& ch, void* stream);
 
 }  // namespace cgtp

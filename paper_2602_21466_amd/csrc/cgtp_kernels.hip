@@ -30,6 +30,15 @@
 #include "cgtp_internal.h"
 #include "device_common.h"
 
+// This file builds the plain kernel (block_kernel); with CGTP_CHANNEL_KERNELS
+// set to 1 it builds the channel-wise, path-weighted one instead
+// (block_kernel_channels, cgtp_kernels_channels.hip).  The plain kernel carries
+// none of the channel bookkeeping, which would cost it registers in the ring
+// loop.
+#ifndef CGTP_CHANNEL_KERNELS
+#define CGTP_CHANNEL_KERNELS 0
+#endif
+
 namespace cgtp {
 namespace {
 
@@ -91,11 +100,12 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
 
 // ---------------------------------------------------------------- the block body
 
-template <typename T, int A, int B>
+template <typename T, int A, int B, bool CH>
 __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* __restrict__ tdesc,
                                            const BlockDesc& bd, int64_t pt0, int64_t pt1, int64_t N,
                                            const T* __restrict__ x1, const T* __restrict__ x2,
-                                           T* __restrict__ out, int L, unsigned char* smem) {
+                                           T* __restrict__ out, int L, const ChanArgs<T>& ch,
+                                           unsigned char* smem) {
     using C = typename Cplx<T>::type;
     using Acc = typename Cplx<T>::acc4;
     constexpr int Phi = A * B;
@@ -205,9 +215,18 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         for (int e = tid; e < kRingGroup * ly.per_r * 2; e += kThreads) fz[e] = (T)0;
     }
 
+    const bool x2s = CH && (ch.flags & kX2Shared);
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
     const int np = (int)((N - p0) < P ? (N - p0) : P);
+    // channel of the tile's first row and the pair it belongs to (rows are
+    // (pair, channel), channel fastest)
+    int64_t n0 = p0;
+    int c0 = 0;
+    if constexpr (CH) {
+        n0 = p0 / ch.channels;
+        c0 = (int)(p0 - n0 * ch.channels);
+    }
     // ---- ring-independent lifted coefficients of the tile in longitude order
     // (zero for |m| > j and for rows past N), per slot:
     //   even slot: (x_m, C^{j, m}_{j, m, 1, 0} x_m)                          scalar and q = 0
@@ -224,7 +243,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         if (am <= j && p < np) {
             const int mj = m + j;
             const T* xg = first ? x1 : x2;
-            const int64_t row = (p0 + p) * nin + j * j;
+            const int64_t xr = (first || !x2s) ? p0 + p : n0 + (c0 + p) / ch.channels;
+            const int64_t row = xr * nin + j * j;
             const T* lcj = first ? lc : lc + 3 * n1;
             const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
             if (!cross || (s & 1) == 0) {
@@ -461,6 +481,19 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 #pragma unroll
     for (int s = 0; s < MT; ++s)
         if (s < ntw) *reinterpret_cast<Acc*>(bbuf + (size_t)(wave + kWaves * s) * tile_stride<T>() + lane * 4) = acc[s];
+    // path weights of the tile's rows, [row][path of the block], staged over the
+    // lifted coefficients (no longer needed for this tile; they hold at least
+    // pairs * (2 (j1 + j2) + 1) >= rows * paths entries)
+    T* wl = reinterpret_cast<T*>(cvn);
+    const int nbp = J - bd.d + 1;   // paths of the block
+    if constexpr (CH) {
+        if (ch.w)
+            for (int e = tid; e < np * nbp; e += kThreads) {
+                const int p = e / nbp, q = e - p * nbp;
+                const int64_t k = (ch.flags & kWeightsPerRow) ? p0 + p : (int64_t)((c0 + p) % ch.channels);
+                wl[e] = ch.w[k * ch.npaths + bd.path_off + q];
+            }
+    }
     lds_barrier();
     {
         const int nblk = n1 * n2;
@@ -468,20 +501,31 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         for (int o = tid; o < nblk; o += kThreads) {
             const Coef4 cf = coef4[o];
             const int4 ix = coefi[o];
-            const bool one = ix.w != 0;   // scalar-scalar or dot path: one term
-            // four pairs at a time (pair p's entries are 4 p further on)
-            for (int p0 = 0; p0 < np; p0 += 4) {
+            const bool one = ix.w & 1;   // scalar-scalar or dot path: one term
+            // four rows at a time (row p's entries are 4 p further on)
+            for (int pb = 0; pb < np; pb += 4) {
                 T v0[4], v1[4], v2[4];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    const int po = 4 * min(p0 + u, np - 1);
+                    const int po = 4 * min(pb + u, np - 1);
                     v0[u] = bbuf[ix.x + po];
                     v1[u] = one ? (T)0 : bbuf[ix.y + po];
                     v2[u] = one ? (T)0 : bbuf[ix.z + po];
                 }
+                if constexpr (!CH) {
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (p0 + u < np) ob[(size_t)(p0 + u) * nout + o] = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
+                    for (int u = 0; u < 4; ++u)
+                        if (pb + u < np)
+                            ob[(size_t)(pb + u) * nout + o] = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
+                } else {
+                    const T* wq = wl + (ix.w >> 1);   // weight of this output's path, row pb + u at nbp (pb + u)
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (pb + u < np) {
+                            const T z = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
+                            ob[(size_t)(pb + u) * nout + o] = ch.w ? wq[(pb + u) * nbp] * z : z;
+                        }
+                }
             }
         }
     }
@@ -489,12 +533,13 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     }   // pair tiles
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const BlockDesc* __restrict__ blocks,
-                                                            const TileDesc* __restrict__ tdesc,
-                                                            const int32_t* __restrict__ list, LaunchMap map,
-                                                            const T* __restrict__ x1, const T* __restrict__ x2,
-                                                            T* __restrict__ out, int64_t N, int L) {
+// Work-group -> (class, block, pair tiles) and the block body for its grid.
+template <typename T, bool CH>
+__device__ __forceinline__ void run_blocks(const Tables<T>& tb, const BlockDesc* __restrict__ blocks,
+                                           const TileDesc* __restrict__ tdesc, const int32_t* __restrict__ list,
+                                           const LaunchMap& map, const T* __restrict__ x1,
+                                           const T* __restrict__ x2, T* __restrict__ out, int64_t N, int L,
+                                           const ChanArgs<T>& ch) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int64_t wg = blockIdx.x;
     int cls = 0;
@@ -509,7 +554,7 @@ __global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const 
     const int64_t pt1 = (pt0 + map.tpw[cls]) < map.ntiles[cls] ? (pt0 + map.tpw[cls]) : map.ntiles[cls];
 
 #define CGTP_CASE(PHI, A_, B_) \
-    case PHI: block_body<T, A_, B_>(tb, tdesc, bd, pt0, pt1, N, x1, x2, out, L, smem); break;
+    case PHI: block_body<T, A_, B_, CH>(tb, tdesc, bd, pt0, pt1, N, x1, x2, out, L, ch, smem); break;
     switch (bd.Phi) {
         CGTP_CASE(1, 1, 1)
         CGTP_CASE(2, 2, 1)
@@ -539,31 +584,73 @@ __global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const 
 #undef CGTP_CASE
 }
 
+#if !CGTP_CHANNEL_KERNELS
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const BlockDesc* __restrict__ blocks,
+                                                            const TileDesc* __restrict__ tdesc,
+                                                            const int32_t* __restrict__ list, LaunchMap map,
+                                                            const T* __restrict__ x1, const T* __restrict__ x2,
+                                                            T* __restrict__ out, int64_t N, int L) {
+    run_blocks<T, false>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ChanArgs<T>{nullptr, 1, 0, 0});
+}
+#else
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void block_kernel_channels(
+        Tables<T> tb, const BlockDesc* __restrict__ blocks, const TileDesc* __restrict__ tdesc,
+        const int32_t* __restrict__ list, LaunchMap map, const T* __restrict__ x1, const T* __restrict__ x2,
+        T* __restrict__ out, int64_t N, int L, ChanArgs<T> ch) {
+    run_blocks<T, true>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ch);
+}
+#endif
+
 template <typename T>
 int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int lds, const T* x1, const T* x2,
-           T* out, int64_t N, int L, void* stream) {
+           T* out, int64_t N, int L, const ChanArgs<T>& ch, void* stream) {
     const int64_t grid = map.cum[map.ncls];
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+#if !CGTP_CHANNEL_KERNELS
+    const void* kern = (const void*)block_kernel<T>;
+#else
+    const void* kern = (const void*)block_kernel_channels<T>;
+#endif
     if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)block_kernel<T>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return (int)e;
     }
+#if !CGTP_CHANNEL_KERNELS
+    (void)ch;
     hipLaunchKernelGGL(block_kernel<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb,
                        tb.blocks, tb.tdesc, list, map, x1, x2, out, N, L);
+#else
+    hipLaunchKernelGGL(block_kernel_channels<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream,
+                       tb, tb.blocks, tb.tdesc, list, map, x1, x2, out, N, L, ch);
+#endif
     return (int)hipGetLastError();
 }
 
 }  // namespace
 
+#if !CGTP_CHANNEL_KERNELS
 int launch_blocks_f32(const Tables<float>& tb, const int32_t* list, const LaunchMap& map, int lds, const float* x1,
                       const float* x2, float* out, int64_t N, int L, void* stream) {
-    return launch<float>(tb, list, map, lds, x1, x2, out, N, L, stream);
+    return launch<float>(tb, list, map, lds, x1, x2, out, N, L, ChanArgs<float>{nullptr, 1, 0, 0}, stream);
 }
 int launch_blocks_f64(const Tables<double>& tb, const int32_t* list, const LaunchMap& map, int lds, const double* x1,
                       const double* x2, double* out, int64_t N, int L, void* stream) {
-    return launch<double>(tb, list, map, lds, x1, x2, out, N, L, stream);
+    return launch<double>(tb, list, map, lds, x1, x2, out, N, L, ChanArgs<double>{nullptr, 1, 0, 0}, stream);
 }
+#else
+int launch_blocks_channels_f32(const Tables<float>& tb, const int32_t* list, const LaunchMap& map, int lds,
+                               const float* x1, const float* x2, float* out, int64_t N, int L,
+                               const ChanArgs<float>& ch, void* stream) {
+    return launch<float>(tb, list, map, lds, x1, x2, out, N, L, ch, stream);
+}
+int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* list, const LaunchMap& map, int lds,
+                               const double* x1, const double* x2, double* out, int64_t N, int L,
+                               const ChanArgs<double>& ch, void* stream) {
+    return launch<double>(tb, list, map, lds, x1, x2, out, N, L, ch, stream);
+}
+#endif
 
 }  // namespace cgtp

@@ -278,6 +278,20 @@ int64_t path_offset(int L, int l1, int l2, int l3) {
            (int64_t)(l1 - l2) * (l1 - l2);
 }
 
+// Index of path (l1, l2, l3) when all paths of degree L are listed in (l1, l2,
+// l3) order (block (a, b) holds the 2 min(a, b) + 1 paths l3 = |a - b|..a + b);
+// -1 if it is not a path.  path_index(L, L + 1, 0, 1) is the number of paths.
+int64_t path_index(int L, int l1, int l2, int l3) {
+    const bool end = L >= 0 && l1 == L + 1 && l2 == 0 && l3 == 1;
+    if (!end && path_offset(L, l1, l2, l3) < 0) return -1;
+    int64_t k = 0;
+    for (int a = 0; a < l1; ++a)
+        for (int b = 0; b <= L; ++b) k += 2 * std::min(a, b) + 1;
+    if (end) return k;
+    for (int b = 0; b < l2; ++b) k += 2 * std::min(l1, b) + 1;
+    return k + l3 - std::abs(l1 - l2);
+}
+
 // MFMA weight table geometry: rings padded to whole ring groups; entries per
 // ring row (degrees l = par, par + 2, ..., <= lmax).
 inline int wtab_rpad(int R) { return (R + cgtp::kRingGroup - 1) / cgtp::kRingGroup * cgtp::kRingGroup; }
@@ -493,6 +507,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                 kinv[j3] = 1.0L / K;
             }
             b.out_off = path_offset(L, j1, j2, b.d);
+            b.path_off = (int32_t)path_index(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
             // pairs per work-group: as many as the accumulator registers and LDS allow
             const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
@@ -581,7 +596,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                             h.coef.push_back((T)0);
                             h.coef.push_back((T)0);
                             h.coef.push_back((T)0);
-                            h.coefi.insert(h.coefi.end(), {e, e, e, 1});
+                            h.coefi.insert(h.coefi.end(), {e, e, e, 1 | (j3 - b.d) << 1});
                         } else {
                             // q = -1, 0, +1 from components 2, 1, 3 at (j3 - 1, m3 - q)
                             const int l3 = j3 - 1, tr = (l3 - b.d) / 2;
@@ -603,7 +618,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                                 h.coef.push_back((T)w[k]);
                             }
                             h.coef.push_back((T)0);
-                            h.coefi.insert(h.coefi.end(), {e[0], e[1], e[2], 0});
+                            h.coefi.insert(h.coefi.end(), {e[0], e[1], e[2], (j3 - b.d) << 1});
                         }
                     }
                 }
@@ -838,17 +853,26 @@ int cgtp_plan_query(cgtp_plan_t plan, int32_t* n_theta, int32_t* n_phi, double* 
     return CGTP_OK;
 }
 
-int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* hip_stream) {
-    if (!plan || N < 0) return CGTP_EINVAL;
-    if (N == 0) return CGTP_OK;
-    if (!x1 || !x2 || !out) return CGTP_EINVAL;
-    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// Shared by both forward entry points: N rows (pair, channel), x2 with one row
+// per row or per pair, optional path weights.
+int forward_rows(cgtp_plan_t plan, const void* x1, const void* x2, const void* w, void* out, int64_t N,
+                 int32_t channels, int32_t flags, void* hip_stream) {
     const int L = plan->L;
     const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)(L + 1) * (L + 1), nout = (size_t)cgtp_num_outputs(L);
+    const int64_t npaths = path_index(L, L + 1, 0, 1);
     if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
-    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
-    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin)) return CGTP_EINVAL;
+    const int64_t n2 = (flags & cgtp::kX2Shared) ? N / channels : N;
+    const int64_t nw = (flags & cgtp::kWeightsPerRow) ? N : channels;
+    if (w && (uint64_t)nw > (uint64_t)(INT64_MAX / (npaths * (int64_t)esz))) return CGTP_EINVAL;
+    const size_t bin = (size_t)N * nin * esz, bin2 = (size_t)n2 * nin * esz, bout = (size_t)N * nout * esz;
+    const size_t bw = w ? (size_t)nw * npaths * esz : 0;
+    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin2) || (w && overlaps(out, bout, w, bw)))
+        return CGTP_EINVAL;
     // the plan's tables live on the device current when it was built
     int dev = -1;
     const hipError_t de = hipGetDevice(&dev);
@@ -875,18 +899,64 @@ int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, in
         map.wpb[c] = (map.ntiles[c] + tpw - 1) / tpw;
         map.cum[c + 1] = map.cum[c] + map.wpb[c] * cl.count;
     }
+    // one channel, no sharing, no weights: the plain kernel
+    const bool plain = channels == 1 && flags == 0 && !w;
     int err;
-    if (plan->grid.dtype == CGTP_FP32)
-        err = cgtp::launch_blocks_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
-                                      (const float*)x2, (float*)out, N, L, hip_stream);
-    else
-        err = cgtp::launch_blocks_f64(plan->td, plan->d_list, map, plan->lds_bytes, (const double*)x1,
-                                      (const double*)x2, (double*)out, N, L, hip_stream);
+    if (plan->grid.dtype == CGTP_FP32) {
+        const cgtp::ChanArgs<float> ch{(const float*)w, channels, flags, (int32_t)npaths};
+        err = plain ? cgtp::launch_blocks_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
+                                              (const float*)x2, (float*)out, N, L, hip_stream)
+                    : cgtp::launch_blocks_channels_f32(plan->tf, plan->d_list, map, plan->lds_bytes,
+                                                       (const float*)x1, (const float*)x2, (float*)out, N, L, ch,
+                                                       hip_stream);
+    } else {
+        const cgtp::ChanArgs<double> ch{(const double*)w, channels, flags, (int32_t)npaths};
+        err = plain ? cgtp::launch_blocks_f64(plan->td, plan->d_list, map, plan->lds_bytes, (const double*)x1,
+                                              (const double*)x2, (double*)out, N, L, hip_stream)
+                    : cgtp::launch_blocks_channels_f64(plan->td, plan->d_list, map, plan->lds_bytes,
+                                                       (const double*)x1, (const double*)x2, (double*)out, N, L,
+                                                       ch, hip_stream);
+    }
     if (err != 0) {
         g_last_hip_error = err;
         return CGTP_EHIP;
     }
     return CGTP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cgtp_forward(cgtp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+    return forward_rows(plan, x1, x2, nullptr, out, N, 1, 0, hip_stream);
+}
+
+int cgtp_forward_weighted(cgtp_plan_t plan, const void* x1, const void* x2, const void* weights, void* out,
+                          int64_t N, const cgtp_channels* ch, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    const int32_t C = ch ? ch->channels : 1;
+    if (C < 1 || (ch && ((ch->x2_shared & ~1) || (ch->weights_per_pair & ~1) || ch->reserved))) return CGTP_EINVAL;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+    const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    if ((uintptr_t)weights & (esz - 1)) return CGTP_EINVAL;
+    if (N > INT64_MAX / C) return CGTP_EINVAL;
+    const int32_t flags = (ch && ch->x2_shared ? cgtp::kX2Shared : 0) |
+                          (ch && ch->weights_per_pair ? cgtp::kWeightsPerRow : 0);
+    return forward_rows(plan, x1, x2, weights, out, N * C, C, flags, hip_stream);
+}
+
+int64_t cgtp_num_paths(int32_t L) { return L < 0 ? -1 : path_index(L, L + 1, 0, 1); }
+
+int64_t cgtp_path_index(int32_t L, int32_t l1, int32_t l2, int32_t l3) {
+    if (L >= 0 && l1 == L + 1) return -1;
+    return path_index(L, l1, l2, l3);
 }
 
 }  // extern "C"
