@@ -33,15 +33,18 @@ PEAK_HBM_GBS = 8000.0
 # (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "707686cb0dab3812": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 345013.1, "fetch_scale": 1.999956, "write_kib": 4939527.3, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 204376.0, "fetch_scale": 1.999956, "write_kib": 2742165.3, "write_scale": 1.000000},
+    "eb1538a138bbb0e1": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 344444.9, "fetch_scale": 1.999956, "write_kib": 4942925.1, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 204032.4, "fetch_scale": 1.999956, "write_kib": 2742207.3, "write_scale": 1.000000},
+    },
+    "04c961e1dcae9b1a": {
+        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118920.5, "fetch_scale": 1.999956, "write_kib": 2829100.8, "write_scale": 1.000000},
     },
     "fad6b244a8d81cac": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 293133.8, "fetch_scale": 1.999956, "write_kib": 811652.9, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 404077.2, "fetch_scale": 1.999956, "write_kib": 1084126.0, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 227635.9, "fetch_scale": 1.999956, "write_kib": 837122.6, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068380.9, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
+        "vstp_L32_N16384_fp32": {"fetch_kib": 295004.2, "fetch_scale": 1.999956, "write_kib": 811652.9, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 403820.8, "fetch_scale": 1.999956, "write_kib": 1084121.8, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227603.4, "fetch_scale": 1.999956, "write_kib": 837123.0, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068410.0, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
     },
 }
 
