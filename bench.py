@@ -54,6 +54,8 @@ DIGEST_SOURCES = {
     "istp": ("istp_kernels.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
+    "istp_channels": ("istp_kernels.hip", "istp_kernels_channels.hip", "istp_plan.cpp", "istp_internal.h",
+                      "device_common.h"),
 }
 
 
@@ -173,6 +175,32 @@ def time_channels(w, steps, warmup):
     res.update(_time_launches(lambda st: plan.forward_weighted(a, b, wc, out, st), rows, steps, warmup))
     plan.close()
     del out, a, b, wc
+    torch.cuda.empty_cache()
+    return res
+
+
+def time_istp_channels(w, steps, warmup):
+    """Channel-wise signal product with label weights: N pairs x C channels = N C rows per launch."""
+    import torch
+
+    import cgtp_inputs
+    import paper_2602_21466_amd as lib
+
+    x1, x2, w1, w2, wo = cgtp_inputs.istp_channel_inputs(w.spin, w.L, w.N, w.C, w.x2_shared, w.weights, w.dtype,
+                                                          w.seed)
+    plan = lib.IstpPlan(w.L, w.spin, w.dtype)
+    a, b = x1.cuda(), x2.cuda()
+    ws = [None if t is None else t.cuda() for t in (w1, w2, wo)]
+    rows = w.N * w.C
+    out = torch.empty((w.N, w.C, plan.nout), dtype=a.dtype, device="cuda")
+    q = dict(plan.query())
+    esz = a.element_size()
+    wbytes = sum(t.numel() for t in ws if t is not None) * esz / rows
+    q["bytes_per_pair"] = esz * (plan.nin * (1 + (1 / w.C if w.x2_shared else 1)) + plan.nout) + wbytes
+    res = {"workload": w.name, "L": w.L, "N": rows, "dtype": w.dtype, "plan": q, "kind": "istp_channels"}
+    res.update(_time_launches(lambda st: plan.forward_weighted(a, b, *ws, out=out, stream=st), rows, steps, warmup))
+    plan.close()
+    del out, a, b, ws
     torch.cuda.empty_cache()
     return res
 
@@ -297,6 +325,8 @@ def main():
                     help="comma-separated signal-product workloads, or 'none'")
     ap.add_argument("--channels", default=",".join(x.name for x in cgtp_inputs.CHANNEL_WORKLOADS),
                     help="comma-separated channel-wise (path-weighted) CGTP workloads, or 'none'")
+    ap.add_argument("--istp-channels", default=",".join(x.name for x in cgtp_inputs.ISTP_CHANNEL_WORKLOADS),
+                    help="comma-separated channel-wise (label-weighted) signal-product workloads, or 'none'")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--istp-cpu-seconds", type=float, default=4.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -358,6 +388,17 @@ def main():
                 entry["backward"] = {"value": round(rb["value"], 1), "unit": "pairs/s",
                                      "ms_per_step": round(rb["ms_per_step"], 4), "roofline": roofline(rb)}
             istp.append(entry)
+    if args.istp_channels and args.istp_channels != "none":
+        by_ic = {x.name: x for x in cgtp_inputs.ISTP_CHANNEL_WORKLOADS}
+        for name in args.istp_channels.split(","):
+            wc = by_ic[name]
+            log("timing %s" % wc.name)
+            rc = time_istp_channels(wc, args.steps, args.warmup)
+            log("  %.4f ms/step, %.4g rows/s" % (rc["ms_per_step"], rc["value"]))
+            istp.append({"workload": wc.name, "value": round(rc["value"], 1), "unit": "rows/s",
+                         "rows": rc["N"], "pairs": wc.N, "channels": wc.C, "x2_shared": wc.x2_shared,
+                         "weights": wc.weights, "ms_per_step": round(rc["ms_per_step"], 4),
+                         "roofline": roofline(rc)})
     line = {
         "metric": METRIC, "value": round(main_res["value"], 1), "unit": "pairs/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(main_res["ms_per_step"], 4),
@@ -374,7 +415,9 @@ def main():
         # the signal-product baselines first: the CGTP baseline's one-thread leg
         # leaves the oracle's thread count at one
         for entry in istp:
-            wi = {x.name: x for x in cgtp_inputs.ISTP_WORKLOADS}[entry["workload"]]
+            wi = {x.name: x for x in cgtp_inputs.ISTP_WORKLOADS}.get(entry["workload"])
+            if wi is None:
+                continue   # channel workloads: the row products' baseline stands for them
             log("timing the CPU oracle on %s (budget %.0f s)" % (wi.name, args.istp_cpu_seconds))
             entry["cpu_baseline"] = cpu_baseline_istp(wi, args.istp_cpu_seconds)
         log("timing the CPU oracle (budget %.0f s)" % args.cpu_seconds)

@@ -194,3 +194,64 @@ def check_indices(w: Workload):
         return torch.arange(w.N)
     g = torch.Generator("cpu").manual_seed(w.seed + 1)
     return torch.sort(torch.randperm(w.N, generator=g)[: w.check_pairs]).values
+
+
+# Channel-wise signal products with label weights: x1 [N, C, n_in]; x2
+# [N, n_in] when shared by the channels, else [N, C, n_in]; weights w1, w2
+# [C, n_lab(L)], wo [C, n_lab(2L)] (per channel) or [N, C, ...] (per pair),
+# n_lab = L + 1 (spin 0) or 3 L + 1 (spin 1) irrep labels per row.  Same
+# recipe (iid N(0, 1) in float64, then cast), seed L + 300 + spin; x1, x2,
+# w1, w2, wo drawn in that order from one generator.
+def istp_num_labels(L: int, spin: int) -> int:
+    return L + 1 if spin == 0 else 3 * L + 1
+
+
+@dataclass(frozen=True)
+class IstpChannelWorkload:
+    name: str
+    L: int
+    spin: int
+    N: int                # pairs
+    C: int                # channels
+    x2_shared: bool
+    weights: str          # "none" | "channel" | "pair"
+    dtype: str
+    check_rows: int       # 0: every row; else a seeded subsample of (pair, channel) rows
+
+    @property
+    def seed(self) -> int:
+        return self.L + 300 + self.spin
+
+
+def istp_channel_inputs(spin: int, L: int, N: int, C: int, x2_shared: bool, weights: str, dtype: str = "fp32",
+                        seed: int = 0):
+    """(x1, x2, w1, w2, wo) as CPU torch tensors; the weights are None for weights == "none"."""
+    import torch
+    g = torch.Generator("cpu").manual_seed(seed)
+    nin = (2 * spin + 1) * (L + 1) ** 2
+    x1 = torch.randn(N, C, nin, dtype=torch.float64, generator=g)
+    x2 = torch.randn(*((N, nin) if x2_shared else (N, C, nin)), dtype=torch.float64, generator=g)
+    ws = [None, None, None]
+    if weights != "none":
+        lead = (C,) if weights == "channel" else (N, C)
+        for k, Lx in enumerate((L, L, 2 * L)):
+            ws[k] = torch.randn(*lead, istp_num_labels(Lx, spin), dtype=torch.float64, generator=g).to(torch_dtype(dtype))
+    return (x1.to(torch_dtype(dtype)), x2.to(torch_dtype(dtype))) + tuple(ws)
+
+
+def istp_channel_check_rows(wk: IstpChannelWorkload):
+    import torch
+    rows = wk.N * wk.C
+    if not wk.check_rows or wk.check_rows >= rows:
+        return list(range(rows))
+    g = torch.Generator("cpu").manual_seed(wk.seed + 1)
+    return sorted(torch.randperm(rows, generator=g)[: wk.check_rows].tolist())
+
+
+# The vector product as a message-passing layer at L = 16: 4096 pairs (edges)
+# x 16 channels = 65536 rows, as many as the L = 16 row workload; x2 (the
+# edge's harmonics) shared by the channels, per-channel label weights.
+ISTP_CHANNEL_WORKLOADS = [
+    IstpChannelWorkload("vstp_L16_N4096_C16_fp32_x2shared_weighted", 16, 1, 4096, 16, True, "channel", "fp32", 16),
+]
+

@@ -84,6 +84,50 @@ int istp_forward(istp_plan_t plan, const void *x1, const void *x2, void *out, in
 /* Frees the plan's device tables.  NULL is a no-op. */
 int istp_destroy(istp_plan_t plan);
 
+/*
+ * Multiplicity channels and label weights (the layer around the product).
+ * A layer holds C channels of the input feature; equivariant linear maps
+ * before and after the product can only scale each irrep label (Schur's
+ * lemma; the degrees-of-freedom count of Appendix E), so each channel's
+ * product is
+ *   out[n, c] = wo[c] . P(w1[c] . x1[n, c], w2[c] . x2[n, c] or x2[n])
+ * with "w . x" scaling every column of label k by w[k].
+ *   channels:         C >= 1.
+ *   x2_shared:        0: x2 is [N, C, n_in]; 1: x2 is [N, n_in], row n met by
+ *                     every channel of pair n.
+ *   weights_per_pair: 0: weight rows per channel, w1 / w2 [C, istp_num_labels(L)],
+ *                     wo [C, istp_num_labels(2L)]; 1: per (pair, channel),
+ *                     [N, C, ...].
+ *   reserved:         must be 0.
+ */
+typedef struct {
+    int32_t channels;
+    int32_t x2_shared;
+    int32_t weights_per_pair;
+    int32_t reserved;
+} istp_channels;
+
+/*
+ * Channel-wise forward product with label weights, asynchronously on
+ * hip_stream.  x1: [N, C, istp_num_inputs(L, spin)]; out: [N, C,
+ * istp_num_outputs(L, spin)]; x2 and the weights as described at
+ * istp_channels; device arrays of the plan's dtype, row-major, contiguous;
+ * x1, x2 and out 16-byte aligned, weights element-aligned.  Any of w1, w2,
+ * wo may be NULL (all ones); ch == NULL means one channel, x2 not shared.
+ * Label k of a weight row is the one istp_label_index returns.  CGTP_EINVAL
+ * for a bad channel description, out overlapping any input, or byte counts
+ * that overflow; otherwise as istp_forward.
+ */
+int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, const void *w1, const void *w2,
+                          const void *wo, void *out, int64_t N, const istp_channels *ch, void *hip_stream);
+
+/* Irrep labels in a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1); -1 if invalid. */
+int64_t istp_num_labels(int32_t L, int32_t spin);
+
+/* Position of label (j, l) in a weight row: l (spin 0, j == l); 2 l - 1 + j (spin 1,
+   the row order of the labels); -1 if it is not a label. */
+int64_t istp_label_index(int32_t spin, int32_t j, int32_t l);
+
 /* Values per input row: (L+1)^2 (spin 0), 3 (L+1)^2 (spin 1); -1 if invalid. */
 int64_t istp_num_inputs(int32_t L, int32_t spin);
 

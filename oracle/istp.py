@@ -34,7 +34,9 @@ signal, every output irrep read back from one product):
          (coefficients in the orthonormal basis of Definition 4.1).
 
 ``product_vjp`` gives the gradients of sum(g * z) w.r.t. both inputs by the
-plain definition of a bilinear map's derivatives.
+plain definition of a bilinear map's derivatives.  ``channel_product`` is the
+layer around a product: C channels, the second input per channel or shared,
+and one weight per (channel, irrep label) on each input and on the output.
 
 Both products take separate degree bounds for the two inputs and the output
 (L, L2, Lo; by default L2 = L and Lo = L + L2).
@@ -181,3 +183,64 @@ def product_vjp(spin: int, L: int, x1, x2, g, threads: int = 0):
         g1[n] = j1 @ gg[n]
         g2[n] = j2 @ gg[n]
     return g1, g2
+
+
+# ---------------------------------------------------------------- channels and label weights
+#
+# A layer holds C channels of the input feature.  Equivariant linear maps
+# before and after the product can only scale each irrep label (Schur's
+# lemma; the degrees-of-freedom count of Appendix E), so per pair n and
+# channel c:
+#
+#     out[n, c] = wo[c] . P(w1[c] . x1[n, c], w2[c] . y)
+#
+# with y = x2[n, c], or x2[n] when the second input is shared by the
+# channels, P the product above and "w . x" scaling every column of label k
+# by w[k].  Weight rows list the labels in row order: degree l for spin 0,
+# (j, l) as ``vector_labels`` gives them for spin 1.
+
+def labels(spin: int, L: int):
+    """(j, l) of every label of a row of degree bound L, in row order."""
+    return [(l, l) for l in range(L + 1)] if spin == 0 else vector_labels(L)
+
+
+def column_labels(spin: int, L: int) -> np.ndarray:
+    """Label index (position in ``labels``) of every column of a row."""
+    if spin == 0:
+        return np.concatenate([np.full(2 * l + 1, l) for l in range(L + 1)])
+    out = np.empty(vector_size(L), dtype=np.int64)
+    for k, (j, l) in enumerate(vector_labels(L)):
+        o = vector_offset(j, l)
+        out[o: o + 2 * j + 1] = k
+    return out
+
+
+def channel_product(spin: int, L: int, x1, x2, w1=None, w2=None, wo=None, threads: int = 0) -> np.ndarray:
+    """x1: [N, C, n_in]; x2: [N, C, n_in] or [N, n_in]; w1, w2: None, [C, n_lab(L)] or [N, C, n_lab(L)];
+    wo: None, [C, n_lab(2L)] or [N, C, n_lab(2L)].  Returns [N, C, n_out] in fp64."""
+    fn = gaunt_tp if spin == 0 else vector_tp
+    size = gaunt_size if spin == 0 else vector_size
+    nin = size(L)
+    a = np.asarray(x1, dtype=np.float64)
+    if a.ndim != 3 or a.shape[2] != nin:
+        raise ValueError("x1 must be [N, C, %d]" % nin)
+    n, c = a.shape[:2]
+    b = np.asarray(x2, dtype=np.float64)
+    if b.shape == (n, nin):
+        b = np.repeat(b[:, None, :], c, axis=1)
+    elif b.shape != (n, c, nin):
+        raise ValueError("x2 must be [N, C, %d] or [N, %d]" % (nin, nin))
+
+    def scale(x, w, Lx):
+        if w is None:
+            return x
+        nl = len(labels(spin, Lx))
+        wt = np.asarray(w, dtype=np.float64)
+        if wt.shape == (c, nl):
+            wt = np.broadcast_to(wt, (n, c, nl))
+        elif wt.shape != (n, c, nl):
+            raise ValueError("weights must be [C, %d] or [N, C, %d]" % (nl, nl))
+        return x * wt[:, :, column_labels(spin, Lx)]
+
+    z = fn(L, scale(a, w1, L).reshape(n * c, nin), scale(b, w2, L).reshape(n * c, nin), threads)
+    return scale(z.reshape(n, c, -1), wo, 2 * L)

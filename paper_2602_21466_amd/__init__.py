@@ -84,6 +84,9 @@ def _load():
                                            ctypes.POINTER(i32), ctypes.POINTER(i32)]),
         "istp_plan": (ctypes.c_int, [i32, i32, i32, ctypes.POINTER(vp)]),
         "istp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
+        "istp_forward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, i64, ctypes.POINTER(cgtp_channels), vp]),
+        "istp_num_labels": (i64, [i32, i32]),
+        "istp_label_index": (i64, [i32, i32, i32]),
         "istp_destroy": (ctypes.c_int, [vp]),
         "istp_num_inputs": (i64, [i32, i32]),
         "istp_num_outputs": (i64, [i32, i32]),
@@ -106,7 +109,7 @@ def exported_symbols():
     return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
-            "istp_plan", "istp_forward", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
+            "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
             "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
 
@@ -249,6 +252,26 @@ def istp_label_offset(spin: int, j: int, l: int) -> int:
     return int(_load().istp_label_offset(int(spin), int(j), int(l)))
 
 
+def istp_num_labels(L: int, spin: int) -> int:
+    return int(_load().istp_num_labels(int(L), int(spin)))
+
+
+def istp_label_index(spin: int, j: int, l: int) -> int:
+    return int(_load().istp_label_index(int(spin), int(j), int(l)))
+
+
+def istp_forward_weighted(plan, x1_ptr: int, x2_ptr: int, w1_ptr, w2_ptr, wo_ptr, out_ptr: int, N: int,
+                          channels: int = 1, x2_shared: bool = False, weights_per_pair: bool = False,
+                          stream_ptr: int | None = None) -> None:
+    # istp_channels has the layout of cgtp_channels
+    ch = cgtp_channels(int(channels), int(bool(x2_shared)), int(bool(weights_per_pair)), 0)
+    vpn = lambda p: ctypes.c_void_p(p) if p else None
+    rc = _load().istp_forward_weighted(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), vpn(w1_ptr),
+                                       vpn(w2_ptr), vpn(wo_ptr), ctypes.c_void_p(out_ptr), int(N), ctypes.byref(ch),
+                                       vpn(stream_ptr))
+    _check(rc, "istp_forward_weighted")
+
+
 def istp_plan_query(plan) -> dict:
     nt, nph, pp = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     fl, by = ctypes.c_double(), ctypes.c_double()
@@ -381,6 +404,38 @@ class IstpPlan:
             raise ValueError("out must be a contiguous %s tensor [N, %d]" % (tdt, self.nout))
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         istp_forward(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, s.cuda_stream)
+        return out
+
+    def forward_weighted(self, x1, x2, w1=None, w2=None, wo=None, out=None, stream=None):
+        """x1: [N, C, nin]; x2: [N, C, nin] or [N, nin] (shared by the channels); w1, w2: None, [C, nl] or
+        [N, C, nl] with nl = istp_num_labels(L, spin); wo: None, [C, nlo] or [N, C, nlo] with
+        nlo = istp_num_labels(2L, spin).  Returns [N, C, nout]."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        if not x1.is_cuda or x1.dtype != tdt or x1.dim() != 3 or x1.shape[2] != self.nin or not x1.is_contiguous():
+            raise ValueError("x1 must be a contiguous %s CUDA tensor [N, C, %d]" % (tdt, self.nin))
+        N, C = x1.shape[0], x1.shape[1]
+        if x2.dtype != tdt or not x2.is_cuda or not x2.is_contiguous() or \
+                tuple(x2.shape) not in ((N, C, self.nin), (N, self.nin)):
+            raise ValueError("x2 must be a contiguous %s CUDA tensor [N, C, %d] or [N, %d]" % (tdt, self.nin, self.nin))
+        nl, nlo = istp_num_labels(self.L, self.spin), istp_num_labels(2 * self.L, self.spin)
+        given = [w for w in (w1, w2, wo) if w is not None]
+        per_pair = bool(given) and given[0].dim() == 3
+        for w, n in ((w1, nl), (w2, nl), (wo, nlo)):
+            if w is None:
+                continue
+            want = (N, C, n) if per_pair else (C, n)
+            if w.dtype != tdt or not w.is_cuda or not w.is_contiguous() or tuple(w.shape) != want:
+                raise ValueError("weights must be contiguous %s CUDA tensors %s (all per channel or all per pair)"
+                                 % (tdt, want))
+        if out is None:
+            out = torch.empty((N, C, self.nout), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, C, self.nout):
+            raise ValueError("out must be a contiguous %s tensor [N, C, %d]" % (tdt, self.nout))
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        ptr = lambda w: w.data_ptr() if w is not None else None
+        istp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), ptr(w1), ptr(w2), ptr(wo), out.data_ptr(), N,
+                              C, x2.dim() == 2, per_pair, s.cuda_stream)
         return out
 
     def backward_query(self) -> dict:

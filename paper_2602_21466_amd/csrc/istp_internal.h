@@ -78,6 +78,22 @@ struct IstpTables {
     const ProjTile* proj;
     const int2* bcol;     // per operand column: (am | column << 8, element offset of (am, k = 0, column))
     const IstpDesc* desc;
+    const int32_t* lab;   // label index of every column: input 1 [nin], input 2 [nin2], output [nout]
+};
+
+// Multiplicity channels and label weights of a launch (the channel-wise
+// kernels only).  Rows of x1 and out are (pair, channel), channel fastest; x2
+// has one row per row, or with kChanX2Shared one per pair (row / channels).
+// Weight rows k = the row (kChanPerRow) or its channel: w1[k nl1 + label] scales
+// input 1, w2[k nl2 + label] input 2, wo[k nlo + label] the output; NULL: 1.
+enum IstpChanFlags : int32_t { kChanX2Shared = 1, kChanPerRow = 2 };
+template <typename T>
+struct IstpChan {
+    const T* w1;
+    const T* w2;
+    const T* wo;
+    int32_t channels, flags;
+    int32_t nl1, nl2, nlo;
 };
 
 // LDS of one work-group (byte offsets): twiddles at 0; one packed word per
@@ -132,5 +148,9 @@ int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float*
                     int64_t N, void* stream);
 int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
                     double* out, int64_t N, void* stream);
+int launch_istp_channels_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                             float* out, int64_t N, const IstpChan<float>& ch, void* stream);
+int launch_istp_channels_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                             double* out, int64_t N, const IstpChan<double>& ch, void* stream);
 
 }  // namespace istp

@@ -36,6 +36,14 @@
 #include "device_common.h"
 #include "istp_internal.h"
 
+// This file builds the plain kernels (istp_kernel); with ISTP_CHANNEL_KERNELS
+// set to 1 it builds the channel-wise, label-weighted forward kernels instead
+// (istp_kernel_channels, istp_kernels_channels.hip), so that the plain ones
+// carry none of the channel bookkeeping.
+#ifndef ISTP_CHANNEL_KERNELS
+#define ISTP_CHANNEL_KERNELS 0
+#endif
+
 namespace istp {
 namespace {
 
@@ -90,10 +98,16 @@ __device__ __forceinline__ void reverse_index(int c, int* src, bool* neg) {
 // Column order: sign of m (+ first), input, component, pair; negative orders
 // carry (-1)^am (P^{-m} = (-1)^m P^m).  With kReverseSecond the second input
 // is staged time-reversed, x[(j,l), m] -> (-1)^(m+j-l+S) x[(j,l), -m].
-template <typename T, int S>
+// Channel bookkeeping of a work-group: its first row is channel c0 of pair n0.
+struct ChanPos {
+    int64_t n0;
+    int c0;
+};
+
+template <typename T, int S, bool CH>
 __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                                    const T* __restrict__ x1, const T* __restrict__ x2, T* acoef,
-                                                   T* stage) {
+                                                   T* stage, const IstpChan<T>& ch, ChanPos cp) {
     constexpr int NC = 2 * S + 1;
     const int P = d.pairs, nin = d.nin, nin2 = d.nin2;
     const int Lm = d.L > d.L2 ? d.L : d.L2;
@@ -108,14 +122,33 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
             v[u] = (T)0;
             if (e < nx1) {
                 const int p = e / nin, c = e - p * nin;
-                if (p < np) v[u] = x1[(p0 + p) * (int64_t)nin + c];
+                if (p < np) {
+                    T xv = x1[(p0 + p) * (int64_t)nin + c];
+                    if constexpr (CH) {
+                        if (ch.w1) {
+                            const int64_t k = (ch.flags & kChanPerRow) ? p0 + p : (cp.c0 + p) % ch.channels;
+                            xv *= ch.w1[k * ch.nl1 + tb.lab[c]];
+                        }
+                    }
+                    v[u] = xv;
+                }
             } else if (e < nx) {
                 const int p = (e - nx1) / nin2, c = e - nx1 - p * nin2;
                 int src = c;
                 bool neg = false;
                 if (rev2) reverse_index<S>(c, &src, &neg);
                 if (p < np) {
-                    const T xv = x2[(p0 + p) * (int64_t)nin2 + src];
+                    int64_t r2 = p0 + p;
+                    if constexpr (CH) {
+                        if (ch.flags & kChanX2Shared) r2 = cp.n0 + (cp.c0 + p) / ch.channels;
+                    }
+                    T xv = x2[r2 * (int64_t)nin2 + src];
+                    if constexpr (CH) {
+                        if (ch.w2) {
+                            const int64_t k = (ch.flags & kChanPerRow) ? p0 + p : (cp.c0 + p) % ch.channels;
+                            xv *= ch.w2[k * ch.nl2 + tb.lab[nin + src]];
+                        }
+                    }
                     v[u] = neg ? -xv : xv;
                 }
             } else if (e - nx < ncg) {
@@ -177,10 +210,10 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
     }
 }
 
-template <typename T, int A, int B, int S, bool LONG>
+template <typename T, int A, int B, int S, bool LONG, bool CH>
 __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                           const T* __restrict__ x1, const T* __restrict__ x2, T* __restrict__ out,
-                                          unsigned char* smem) {
+                                          const IstpChan<T>& ch, unsigned char* smem) {
     using C2 = typename Cplx<T>::type;
     using Acc = typename Cplx<T>::acc4;
     constexpr int Phi = A * B;
@@ -210,7 +243,12 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         const ProjTile pt = tb.proj[e];
         ptab[e] = pt.a | (pt.am << 20) | (pt.par << 27);
     }
-    build_coefficients<T, S>(tb, d, p0, np, x1, x2, acoef, reinterpret_cast<T*>(fbuf));
+    ChanPos cp{p0, 0};
+    if constexpr (CH) {
+        cp.n0 = p0 / ch.channels;
+        cp.c0 = (int)(p0 - cp.n0 * ch.channels);
+    }
+    build_coefficients<T, S, CH>(tb, d, p0, np, x1, x2, acoef, reinterpret_cast<T*>(fbuf), ch, cp);
 
     // projection tiles of this wave: w, w + kWaves, ...  A lane's B operand is
     // column li (sign, component, pair; past the last column: column 0, whose
@@ -480,12 +518,29 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
             for (int u = 0; u < 4; ++u) {
                 const int o = o0 + u * kThreads;
                 if (o >= nout) break;
-                for (int p = 0; p < np; ++p) {
-                    const T* hp = hc + (size_t)p * hs;
-                    T v = cf[u].x * hp[ix[u].x];
-                    if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
-                    if (d.flags & kNegate) v = -v;
-                    out[(p0 + p) * (int64_t)nout + o] = v;
+                if constexpr (!CH) {
+                    for (int p = 0; p < np; ++p) {
+                        const T* hp = hc + (size_t)p * hs;
+                        T v = cf[u].x * hp[ix[u].x];
+                        if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
+                        if (d.flags & kNegate) v = -v;
+                        out[(p0 + p) * (int64_t)nout + o] = v;
+                    }
+                } else {
+                    // output label weight of row p: row k of wo, k = the row or its channel
+                    const int lo = ch.wo ? tb.lab[d.nin + d.nin2 + o] : 0;
+                    int cc = cp.c0;
+                    for (int p = 0; p < np; ++p) {
+                        const T* hp = hc + (size_t)p * hs;
+                        T v = cf[u].x * hp[ix[u].x];
+                        if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
+                        if (ch.wo) {
+                            const int64_t k = (ch.flags & kChanPerRow) ? p0 + p : cc;
+                            v *= ch.wo[k * ch.nlo + lo];
+                        }
+                        cc = cc + 1 == ch.channels ? 0 : cc + 1;
+                        out[(p0 + p) * (int64_t)nout + o] = v;
+                    }
                 }
             }
         }
@@ -495,16 +550,17 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
 // LONG: lifts of more than 4 kMaxLiftSteps degrees (only the gradient
 // product's degree-2L input, fp32, Phi >= 72); a kernel of its own, so that
 // the forward kernels keep their register allocation.
-template <typename T, int S, bool LONG>
-__global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, IstpDesc d, const T* __restrict__ x1,
-                                                           const T* __restrict__ x2, T* __restrict__ out, int64_t N) {
+template <typename T, int S, bool LONG, bool CH>
+__device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc& d, const T* __restrict__ x1,
+                                         const T* __restrict__ x2, T* __restrict__ out, int64_t N,
+                                         const IstpChan<T>& ch) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int64_t p0 = (int64_t)blockIdx.x * d.pairs;
     const int np = (int)((N - p0) < d.pairs ? (N - p0) : d.pairs);
 #define ISTP_CASE(PHI, A_, B_)                                                                      \
     case PHI:                                                                                       \
         if constexpr ((sizeof(T) == 4 || PHI <= 54) && (!LONG || (sizeof(T) == 4 && PHI >= 72)))    \
-            istp_body<T, A_, B_, S, LONG>(tb, d, p0, np, x1, x2, out, smem);                        \
+            istp_body<T, A_, B_, S, LONG, CH>(tb, d, p0, np, x1, x2, out, ch, smem);                \
         break;
     switch (d.Phi) {
         ISTP_CASE(1, 1, 1)
@@ -530,6 +586,13 @@ __global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, Ist
 #undef ISTP_CASE
 }
 
+#if !ISTP_CHANNEL_KERNELS
+template <typename T, int S, bool LONG>
+__global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, IstpDesc d, const T* __restrict__ x1,
+                                                           const T* __restrict__ x2, T* __restrict__ out, int64_t N) {
+    run_istp<T, S, LONG, false>(tb, d, x1, x2, out, N, IstpChan<T>{nullptr, nullptr, nullptr, 1, 0, 0, 0, 0});
+}
+
 template <typename T>
 int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2, T* out, int64_t N, void* stream) {
     const int64_t grid = (N + d.pairs - 1) / d.pairs;
@@ -549,9 +612,39 @@ int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2,
                        out, N);
     return (int)hipGetLastError();
 }
+#else
+// forward products only (input degrees <= 32: no long lifts)
+template <typename T, int S>
+__global__ __launch_bounds__(kThreads, 1) void istp_kernel_channels(IstpTables<T> tb, IstpDesc d,
+                                                                    const T* __restrict__ x1,
+                                                                    const T* __restrict__ x2, T* __restrict__ out,
+                                                                    int64_t N, IstpChan<T> ch) {
+    run_istp<T, S, false, true>(tb, d, x1, x2, out, N, ch);
+}
+
+template <typename T>
+int launch_channels(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2, T* out, int64_t N,
+                    const IstpChan<T>& ch, void* stream) {
+    const int64_t grid = (N + d.pairs - 1) / d.pairs;
+    if (grid <= 0) return 0;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    const int Lm = d.L > d.L2 ? d.L : d.L2;
+    if (Lm + 1 > 4 * kMaxLiftSteps || ch.channels < 1) return (int)hipErrorInvalidConfiguration;
+    void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t, IstpChan<T>) =
+        d.spin ? istp_kernel_channels<T, 1> : istp_kernel_channels<T, 0>;
+    if (d.lds_bytes > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
+        if (e != hipSuccess) return (int)e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), d.lds_bytes, (hipStream_t)stream, tb, d, x1, x2,
+                       out, N, ch);
+    return (int)hipGetLastError();
+}
+#endif
 
 }  // namespace
 
+#if !ISTP_CHANNEL_KERNELS
 int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
                     int64_t N, void* stream) {
     return launch<float>(tb, d, x1, x2, out, N, stream);
@@ -560,5 +653,15 @@ int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const doubl
                     double* out, int64_t N, void* stream) {
     return launch<double>(tb, d, x1, x2, out, N, stream);
 }
+#else
+int launch_istp_channels_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                             float* out, int64_t N, const IstpChan<float>& ch, void* stream) {
+    return launch_channels<float>(tb, d, x1, x2, out, N, ch, stream);
+}
+int launch_istp_channels_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                             double* out, int64_t N, const IstpChan<double>& ch, void* stream) {
+    return launch_channels<double>(tb, d, x1, x2, out, N, ch, stream);
+}
+#endif
 
 }  // namespace istp

@@ -49,6 +49,28 @@ int64_t label_offset(int spin, int j, int l) {
     return 3LL * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
 }
 
+// Position of label (j, l) in a row of label weights: l for spin 0; for spin 1
+// the labels in row order (l, then j = l - 1, l, l + 1), i.e. 2 l - 1 + j.
+int64_t label_index(int spin, int j, int l) {
+    if (label_offset(spin, j, l) < 0) return -1;
+    return spin == ISTP_GAUNT ? l : 2LL * l - 1 + j;
+}
+
+// Labels of a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1).
+int64_t num_labels(int L, int spin) {
+    if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return -1;
+    return spin == ISTP_GAUNT ? L + 1 : 3LL * L + 1;
+}
+
+// Label index of every column of a row of degree bound L, appended to v.
+void append_column_labels(int L, int spin, std::vector<int32_t>& v) {
+    for (int l = 0; l <= L; ++l)
+        for (int j = l - 1; j <= l + 1; ++j) {
+            if (label_offset(spin, j, l) < 0) continue;
+            for (int m = -j; m <= j; ++m) v.push_back((int32_t)label_index(spin, j, l));
+        }
+}
+
 int64_t row_size(int L, int spin) {
     if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return -1;
     return (int64_t)(2 * spin + 1) * (L + 1) * (L + 1);
@@ -92,6 +114,7 @@ struct Host {
     std::vector<istp::LiftTile> lift;
     std::vector<istp::ProjTile> proj;
     std::vector<int32_t> bcol;   // 2 per operand column
+    std::vector<int32_t> lab;    // label index of every column: input 1, input 2, output
 };
 
 // Tables of the product of a degree-L1 and a degree-L2 input projected on
@@ -284,6 +307,9 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     d.lds_bytes = bestBytes;
     d.n_bcol = (int32_t)(h.bcol.size() / 2);
     d.flags = flags;
+    append_column_labels(L1, S, h.lab);
+    append_column_labels(L2, S, h.lab);
+    append_column_labels(Lo, S, h.lab);
     pr->n_theta = nt;
     pr->n_phi = Phi;
 
@@ -315,6 +341,7 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         {h.proj.data(), h.proj.size() * sizeof(istp::ProjTile), 0},
         {&p->desc, sizeof(istp::IstpDesc), 0},
         {h.bcol.data(), h.bcol.size() * sizeof(int32_t), 0},
+        {h.lab.data(), h.lab.size() * sizeof(int32_t), 0},
     };
     size_t total = 0;
     for (auto& pt : parts) {
@@ -348,6 +375,7 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->proj = (const istp::ProjTile*)(base + parts[7].off);
     tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
     tb->bcol = (const int2*)(base + parts[9].off);
+    tb->lab = (const int32_t*)(base + parts[10].off);
     p->ok = true;
     return CGTP_OK;
 }
@@ -411,6 +439,10 @@ int64_t istp_num_inputs(int32_t L, int32_t spin) { return row_size(L, spin); }
 int64_t istp_num_outputs(int32_t L, int32_t spin) { return L < 0 ? -1 : row_size(2 * L, spin); }
 
 int64_t istp_label_offset(int32_t spin, int32_t j, int32_t l) { return label_offset(spin, j, l); }
+
+int64_t istp_label_index(int32_t spin, int32_t j, int32_t l) { return label_index(spin, j, l); }
+
+int64_t istp_num_labels(int32_t L, int32_t spin) { return num_labels(L, spin); }
 
 static int check_plan_args(int32_t L, int32_t spin, int32_t dtype) {
     if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return CGTP_EINVAL;
@@ -516,6 +548,53 @@ int istp_forward(istp_plan_t plan, const void* x1, const void* x2, void* out, in
     const int rc = current_device_is(plan->device);
     if (rc != CGTP_OK) return rc;
     return launch_prod(plan, plan->fwd, 0, x1, x2, out, N, hip_stream);
+}
+
+int istp_forward_weighted(istp_plan_t plan, const void* x1, const void* x2, const void* w1, const void* w2,
+                          const void* wo, void* out, int64_t N, const istp_channels* ch, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    const int32_t C = ch ? ch->channels : 1;
+    if (C < 1 || (ch && ((ch->x2_shared & ~1) || (ch->weights_per_pair & ~1) || ch->reserved))) return CGTP_EINVAL;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    if (((uintptr_t)w1 | (uintptr_t)w2 | (uintptr_t)wo) & (esz - 1)) return CGTP_EINVAL;
+    const bool shared = ch && ch->x2_shared, per_row = ch && ch->weights_per_pair;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    const int64_t nl = num_labels(plan->L, plan->spin), nlo = num_labels(2 * plan->L, plan->spin);
+    if (N > INT64_MAX / C) return CGTP_EINVAL;
+    const int64_t rows = N * C;
+    if ((uint64_t)rows > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
+    const int64_t wrows = per_row ? rows : C;
+    const size_t bin = (size_t)rows * nin * esz, bin2 = (size_t)(shared ? N : rows) * nin * esz;
+    const size_t bout = (size_t)rows * nout * esz;
+    const size_t bw = (size_t)wrows * nl * esz, bwo = (size_t)wrows * nlo * esz;
+    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin2) || (w1 && overlaps(out, bout, w1, bw)) ||
+        (w2 && overlaps(out, bout, w2, bw)) || (wo && overlaps(out, bout, wo, bwo)))
+        return CGTP_EINVAL;
+    const int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    istp::IstpDesc d = plan->fwd.desc;
+    d.flags = 0;
+    const int32_t flags = (shared ? istp::kChanX2Shared : 0) | (per_row ? istp::kChanPerRow : 0);
+    int err;
+    if (plan->dtype == CGTP_FP32) {
+        const istp::IstpChan<float> c{(const float*)w1, (const float*)w2, (const float*)wo, C, flags,
+                                      (int32_t)nl, (int32_t)nl, (int32_t)nlo};
+        err = istp::launch_istp_channels_f32(plan->fwd.tf, d, (const float*)x1, (const float*)x2, (float*)out, rows,
+                                             c, hip_stream);
+    } else {
+        const istp::IstpChan<double> c{(const double*)w1, (const double*)w2, (const double*)wo, C, flags,
+                                       (int32_t)nl, (int32_t)nl, (int32_t)nlo};
+        err = istp::launch_istp_channels_f64(plan->fwd.td, d, (const double*)x1, (const double*)x2, (double*)out,
+                                             rows, c, hip_stream);
+    }
+    if (err != 0) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
 }
 
 int istp_backward(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
