@@ -33,7 +33,8 @@ signal, every output irrep read back from one product):
       3. z^(j3,l3)_{m3} = sum_q C^{j3 m3}_{l3, m3-q, 1, q} b[q][l3][m3-q]
          (coefficients in the orthonormal basis of Definition 4.1).
 
-``product_vjp`` gives the gradients of sum(g * z) w.r.t. both inputs by the
+``spin_tp`` is the same product for any spin s (s = 2: tensor spherical
+harmonics of rank 2).  ``product_vjp`` gives the gradients of sum(g * z) w.r.t. both inputs by the
 plain definition of a bilinear map's derivatives.  ``channel_product`` is the
 layer around a product: C channels, the second input per channel or shared,
 and one weight per (channel, irrep label) on each input and on the output.
@@ -164,6 +165,78 @@ def vector_tp(L: int, x1, x2, threads: int = 0, L2: int | None = None, Lo: int |
     return out
 
 
+# ---------------------------------------------------------------- any spin s
+#
+# The (s, s, s) product for any s (the general irrep-signal tensor product of
+# Section 4.3 with tensor spherical harmonics of spin s, Definition 4.1): labels
+# (j, l), l = 0..L, |l - s| <= j <= l + s, (2 s + 1)(L + 1)^2 numbers per row
+# (label (j, l) at (2 s + 1) l^2 + j^2 - (l - s)^2); the same three steps as
+# ``vector_tp`` with spin s in place of 1:
+#
+#     a[q][l][ml] = sum_j C^{j, ml+q}_{l, ml, s, q} x^(j,l)_{ml+q},   q = -s..s
+#     b[q] = sum_{q1+q2=q} C^{s q}_{s q1 s q2} gaunt_tp(a1[q1], a2[q2])
+#     z^(j3,l3)_{m3} = sum_q C^{j3 m3}_{l3, m3-q, s, q} b[q][l3][m3-q]
+
+def spin_labels(s: int, L: int):
+    """(j, l) labels of a spin-s row, in row order (l, then j ascending)."""
+    return [(j, l) for l in range(L + 1) for j in range(abs(l - s), l + s + 1)]
+
+
+def spin_offset(s: int, j: int, l: int) -> int:
+    if l < 0 or not (abs(l - s) <= j <= l + s):
+        raise ValueError("(%d, %d) is not a spin-%d label" % (j, l, s))
+    return (2 * s + 1) * l * l + j * j - (l - s) ** 2
+
+
+def spin_size(s: int, L: int) -> int:
+    return (2 * s + 1) * (L + 1) ** 2
+
+
+def spin_components(s: int, L: int, x) -> np.ndarray:
+    """[N, 2 s + 1 (q = -s..s), (L+1)^2] scalar-harmonic coefficients of the spin-s signal."""
+    x = _rows(x, spin_size(s, L))
+    a = np.zeros((x.shape[0], 2 * s + 1, (L + 1) ** 2))
+    for j, l in spin_labels(s, L):
+        o = spin_offset(s, j, l)
+        for q in range(-s, s + 1):
+            for ml in range(-l, l + 1):
+                mj = ml + q
+                if abs(mj) <= j:
+                    a[:, q + s, l * l + l + ml] += _cg(l, ml, s, q, j, mj) * x[:, o + j + mj]
+    return a
+
+
+def spin_tp(s: int, L: int, x1, x2, threads: int = 0, L2: int | None = None, Lo: int | None = None) -> np.ndarray:
+    """(s, s, s) product: x1 [N, (2s+1)(L+1)^2], x2 [N, (2s+1)(L2+1)^2]; returns labels up to l = Lo (default L + L2)."""
+    L1 = L
+    L2 = L1 if L2 is None else L2
+    Lo = L1 + L2 if Lo is None else Lo
+    a1 = spin_components(s, L1, x1)
+    a2 = spin_components(s, L2, x2)
+    if a1.shape[0] != a2.shape[0]:
+        raise ValueError("inputs must hold the same number of rows")
+    n = a1.shape[0]
+    b = np.zeros((n, 2 * s + 1, (Lo + 1) ** 2))
+    for q1 in range(-s, s + 1):
+        for q2 in range(-s, s + 1):
+            q = q1 + q2
+            if abs(q) > s:
+                continue
+            c = _cg(s, q1, s, q2, s, q)
+            if c == 0.0:
+                continue
+            b[:, q + s] += c * gaunt_tp(L1, a1[:, q1 + s], a2[:, q2 + s], threads, L2=L2, Lo=Lo)
+    out = np.zeros((n, spin_size(s, Lo)))
+    for j3, l3 in spin_labels(s, Lo):
+        o = spin_offset(s, j3, l3)
+        for m3 in range(-j3, j3 + 1):
+            for q in range(-s, s + 1):
+                ml = m3 - q
+                if abs(ml) <= l3:
+                    out[:, o + j3 + m3] += _cg(l3, ml, s, q, j3, m3) * b[:, q + s, l3 * l3 + l3 + ml]
+    return out
+
+
 def product_vjp(spin: int, L: int, x1, x2, g, threads: int = 0):
     """Gradients of sum(g * z(x1, x2)) w.r.t. x1 and x2 for the spin-0 or spin-1 product above, by the
     plain definition: z is bilinear, so d/dx1[b] = sum_a g_a z_a(e_b, x2) and d/dx2[b] = sum_a g_a z_a(x1, e_b),
@@ -201,16 +274,16 @@ def product_vjp(spin: int, L: int, x1, x2, g, threads: int = 0):
 
 def labels(spin: int, L: int):
     """(j, l) of every label of a row of degree bound L, in row order."""
-    return [(l, l) for l in range(L + 1)] if spin == 0 else vector_labels(L)
+    return [(l, l) for l in range(L + 1)] if spin == 0 else (vector_labels(L) if spin == 1 else spin_labels(spin, L))
 
 
 def column_labels(spin: int, L: int) -> np.ndarray:
     """Label index (position in ``labels``) of every column of a row."""
     if spin == 0:
         return np.concatenate([np.full(2 * l + 1, l) for l in range(L + 1)])
-    out = np.empty(vector_size(L), dtype=np.int64)
-    for k, (j, l) in enumerate(vector_labels(L)):
-        o = vector_offset(j, l)
+    out = np.empty(spin_size(spin, L), dtype=np.int64)
+    for k, (j, l) in enumerate(labels(spin, L)):
+        o = spin_offset(spin, j, l)
         out[o: o + 2 * j + 1] = k
     return out
 
@@ -218,9 +291,8 @@ def column_labels(spin: int, L: int) -> np.ndarray:
 def channel_product(spin: int, L: int, x1, x2, w1=None, w2=None, wo=None, threads: int = 0) -> np.ndarray:
     """x1: [N, C, n_in]; x2: [N, C, n_in] or [N, n_in]; w1, w2: None, [C, n_lab(L)] or [N, C, n_lab(L)];
     wo: None, [C, n_lab(2L)] or [N, C, n_lab(2L)].  Returns [N, C, n_out] in fp64."""
-    fn = gaunt_tp if spin == 0 else vector_tp
-    size = gaunt_size if spin == 0 else vector_size
-    nin = size(L)
+    fn = gaunt_tp if spin == 0 else (vector_tp if spin == 1 else (lambda *a_, **k_: spin_tp(spin, *a_, **k_)))
+    nin = spin_size(spin, L)
     a = np.asarray(x1, dtype=np.float64)
     if a.ndim != 3 or a.shape[2] != nin:
         raise ValueError("x1 must be [N, C, %d]" % nin)

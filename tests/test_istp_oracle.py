@@ -236,3 +236,79 @@ def test_unequal_bounds_against_quadrature(rng):
     f2 = sum(x2[l * l + l + m] * Y[l, m] for l in range(L2 + 1) for m in range(-l, l + 1))
     want = np.array([(W * f1 * f2 * np.conj(Y[l, m])).sum() for l in range(Lo + 1) for m in range(-l, l + 1)])
     np.testing.assert_allclose(z, want.real, atol=1e-12)
+
+
+# ---------------------------------------------------------------- spin 2
+
+def test_spin_layout_and_spin_one():
+    """Spin-s rows: labels tile the row; at s = 1 the general product is the vector product."""
+    for s in (1, 2, 3):
+        for L in range(4):
+            labs = oi.spin_labels(s, L)
+            offs = [oi.spin_offset(s, j, l) for j, l in labs]
+            sizes = [2 * j + 1 for j, l in labs]
+            assert offs == list(np.cumsum([0] + sizes[:-1])) and sum(sizes) == oi.spin_size(s, L)
+    assert oi.spin_labels(1, 3) == oi.vector_labels(3)
+    rng = np.random.default_rng(4)
+    x1, x2 = rng.standard_normal((2, 2, oi.vector_size(2)))
+    np.testing.assert_allclose(oi.spin_tp(1, 2, x1, x2), oi.vector_tp(2, x1, x2), atol=1e-14)
+
+
+def test_spin_two_product_against_quadrature(rng):
+    """Every output against the integral of conj(Y^{l3,2}_{j3,m3}) . (f1 (x) f2)^(2) on an exact grid
+    (tensor harmonics of Definition 4.1 from scipy's harmonics and sympy's CG)."""
+    L, s = 1, 2
+    x1 = rng.standard_normal(oi.spin_size(s, L))
+    x2 = rng.standard_normal(oi.spin_size(s, L))
+    z = oi.spin_tp(s, L, x1, x2)[0]
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+
+    def signal(x):
+        f = [np.zeros(T.shape, complex) for _ in range(2 * s + 1)]
+        for j, l in oi.spin_labels(s, L):
+            o = oi.spin_offset(s, j, l)
+            for m in range(-j, j + 1):
+                comps = _tsh(l, s, j, m, T, P)
+                for k in range(2 * s + 1):
+                    f[k] = f[k] + x[o + j + m] * comps[k]
+        return f
+
+    f1, f2 = signal(x1), signal(x2)
+    g = []
+    for q in range(-s, s + 1):
+        acc = np.zeros(T.shape, complex)
+        for q1 in range(-s, s + 1):
+            q2 = q - q1
+            if abs(q2) <= s:
+                acc = acc + _sympy_cg(s, q1, s, q2, s, q) * f1[q1 + s] * f2[q2 + s]
+        g.append(acc)
+    want = np.zeros(oi.spin_size(s, 2 * L), complex)
+    for j3, l3 in oi.spin_labels(s, 2 * L):
+        o = oi.spin_offset(s, j3, l3)
+        for m3 in range(-j3, j3 + 1):
+            basis = _tsh(l3, s, j3, m3, T, P)
+            want[o + j3 + m3] = sum((W * g[k] * np.conj(basis[k])).sum() for k in range(2 * s + 1))
+    assert np.abs(want.imag).max() < 1e-12
+    np.testing.assert_allclose(z, want.real, atol=1e-12)
+
+
+def test_spin_two_rotation_equivariance(rng):
+    """Rotating both inputs (label (j, l) by D^j) rotates each output label (j3, l3) by D^{j3}."""
+    from scipy.spatial.transform import Rotation
+    L, s = 2, 2
+    R = Rotation.random(random_state=int(rng.integers(1 << 30)))
+    D = {j: _wigner_D(j, R, rng) for j in range(2 * L + s + 1)}
+
+    def rot(x, Lx):
+        y = np.array(x, dtype=complex)
+        for j, l in oi.spin_labels(s, Lx):
+            o = oi.spin_offset(s, j, l)
+            y[..., o: o + 2 * j + 1] = x[..., o: o + 2 * j + 1] @ D[j].T
+        return y
+
+    x1 = rng.standard_normal((2, oi.spin_size(s, L))).astype(complex)
+    x2 = rng.standard_normal((2, oi.spin_size(s, L))).astype(complex)
+    f = lambda L_, a, b: oi.spin_tp(s, L_, a, b)
+    z = _complex(f, L, x1, x2)
+    zr = _complex(f, L, rot(x1, L), rot(x2, L))
+    np.testing.assert_allclose(zr, rot(z, 2 * L), atol=1e-10)
