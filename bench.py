@@ -301,7 +301,7 @@ def cpu_baseline_istp(w, budget_s):
     x1, x2 = cgtp_inputs.istp_inputs(w)
     a = x1.double().numpy()
     b = x2.double().numpy()
-    fn = oi.gaunt_tp if w.spin == 0 else oi.vector_tp
+    fn = oi.gaunt_tp if w.spin == 0 else (oi.vector_tp if w.spin == 1 else (lambda L, x, y: oi.spin_tp(2, L, x, y)))
     fn(w.L, a[:1], b[:1])                    # coefficient table of the CGTP oracle it builds on
     t0 = time.perf_counter()
     fn(w.L, a[:1], b[:1])

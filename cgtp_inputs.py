@@ -170,6 +170,8 @@ ISTP_WORKLOADS = [
     IstpWorkload("vstp_L32_N16384_fp32", 32, 1, 16_384, "fp32", 4),
     IstpWorkload("gtp_L32_N65536_fp32", 32, 0, 65_536, "fp32", 8),
     IstpWorkload("vstp_L16_N65536_fp32", 16, 1, 65_536, "fp32", 16),
+    # the rank-2 tensor-harmonic product (spin 2) at L = 16
+    IstpWorkload("tstp_L16_N16384_fp32", 16, 2, 16_384, "fp32", 4),
 ]
 
 
@@ -199,11 +201,12 @@ def check_indices(w: Workload):
 # Channel-wise signal products with label weights: x1 [N, C, n_in]; x2
 # [N, n_in] when shared by the channels, else [N, C, n_in]; weights w1, w2
 # [C, n_lab(L)], wo [C, n_lab(2L)] (per channel) or [N, C, ...] (per pair),
-# n_lab = L + 1 (spin 0) or 3 L + 1 (spin 1) irrep labels per row.  Same
+# n_lab irrep labels per row (L + 1, 3 L + 1 or 5 L - 1 for spin 0, 1, 2).  Same
 # recipe (iid N(0, 1) in float64, then cast), seed L + 300 + spin; x1, x2,
 # w1, w2, wo drawn in that order from one generator.
 def istp_num_labels(L: int, spin: int) -> int:
-    return L + 1 if spin == 0 else 3 * L + 1
+    """Irrep labels (j, l), l <= L, |l - spin| <= j <= l + spin, of a row."""
+    return sum(2 * min(l, spin) + 1 for l in range(L + 1))
 
 
 @dataclass(frozen=True)

@@ -24,6 +24,16 @@
  *               g_q = sum C^{1 q}_{1 q1 1 q2} f1_q1 f2_q2 of the two vector
  *               signals f_i = sum x_i^{(j,l)}_m Y^{l,1}_{j,m}.
  *
+ *   ISTP_TENSOR (s = 2, the general irrep-signal product of Section 4.3 with
+ *               rank-2 tensor harmonics Y^{l,2}_{j,m}, Definition 4.1).  Labels
+ *               (j, l), l = 0..L, j = |l-2|..l+2, ordered by l, then j, then
+ *               m: label (j, l) starts at istp_label_offset(2, j, l) =
+ *               5 l^2 + j^2 - (l-2)^2 (5 (L+1)^2 values).  The output holds the
+ *               2 (x) 2 -> 2 coupled pointwise product
+ *               g_q = sum C^{2 q}_{2 q1 2 q2} f1_q1 f2_q2 in the same basis up
+ *               to l = 2L (5 (2L+1)^2 values).  Forward only: istp_backward
+ *               returns CGTP_EUNSUP for these plans.
+ *
  * Basis: complex spherical harmonics with the Condon-Shortley phase; inputs
  * and outputs are real.  By Theorem 4.2 each output label (j3, l3) of the
  * vector product is a sum over input label pairs of K times the CGTP path
@@ -51,17 +61,20 @@ extern "C" {
 
 typedef struct istp_plan_s *istp_plan_t;
 
-enum { ISTP_GAUNT = 0, ISTP_VECTOR = 1 };
+enum { ISTP_GAUNT = 0, ISTP_VECTOR = 1, ISTP_TENSOR = 2 };
 
 /* Largest L: the projection accumulators must fit the register file. */
 #define ISTP_MAX_L_FP32 33
 #define ISTP_MAX_L_FP64 12
+/* spin 2 (ISTP_TENSOR) bounds: staging its rows and rank-2 couplings */
+#define ISTP_TENSOR_MAX_L_FP32 20
+#define ISTP_TENSOR_MAX_L_FP64 12
 
 /*
  * Builds the grid, the MFMA weight tables and the recombination table on the
  * current HIP device and uploads them (device memory owned by the plan).
  *   L     >= 0 (CGTP_EINVAL below; CGTP_EUNSUP above the limits above)
- *   spin  ISTP_GAUNT or ISTP_VECTOR (else CGTP_EINVAL)
+ *   spin  ISTP_GAUNT, ISTP_VECTOR or ISTP_TENSOR (else CGTP_EINVAL)
  *   dtype CGTP_FP32 or CGTP_FP64 (else CGTP_EDTYPE)
  * Returns CGTP_ENOMEM / CGTP_EHIP on allocation or copy failure; *plan_out is
  * written only on success.

@@ -25,8 +25,9 @@ CGTP_FP32, CGTP_FP64 = 0, 1
 CGTP_COVER_DEFAULT, CGTP_COVER_ALTERNATE = 0, 1
 CGTP_MAX_L = 32
 KIND_NAMES = {0: "scalar-scalar", 1: "cross", 2: "scalar-vector", 3: "dot"}
-ISTP_GAUNT, ISTP_VECTOR = 0, 1
+ISTP_GAUNT, ISTP_VECTOR, ISTP_TENSOR = 0, 1, 2
 ISTP_MAX_L = {"fp32": 33, "fp64": 12}
+ISTP_TENSOR_MAX_L = {"fp32": 20, "fp64": 12}
 ISTP_DESC_FIELDS = ("L", "L2", "Lo", "spin", "C", "R", "G", "Phi", "A", "B", "pairs", "nin", "nin2", "nout",
                     "n_lift", "n_proj", "acoef_len", "hc_len", "lw_len", "pw_len", "wrow", "lds_bytes", "n_bcol",
                     "flags")

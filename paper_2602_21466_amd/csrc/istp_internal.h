@@ -71,14 +71,15 @@ struct IstpTables {
     const T* lw;          // [am][ring < rpad][k < kp(am)]: P_{am+k}^{am}(x_ring), zero past max(L, L2) or R
     const T* pw;          // [am][par][ring < rpad][row < wrow]: w_ring P_{am+par+2 row}^{am}(x_ring), zero past Lo or R
     const T* tw;          // [t < A][k2 < B + 1]: exp(-2 pi i t k2 / Phi), pass layout
-    const T* liftcg;      // [l][j - l + 1][q + 1][ml + l]: C^{j, ml+q}_{l, ml, 1, q} (spin 1), l <= max(L, L2)
-    const T* coef;        // per output: three term weights and a pad (4 per output)
-    const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), pad
+    const T* liftcg;      // [l][j - l + s][q + s][ml + l]: C^{j, ml+q}_{l, ml, s, q} (spin s > 0), l <= max(L, L2)
+    const T* coef;        // per output: term weights, 4 (spin 0, 1: three terms and a pad) or 8 (spin 2: five terms)
+    const int32_t* coefi; // per output: end-phase spectrum index of each term (pair 0), as coef
     const LiftTile* lift;
     const ProjTile* proj;
     const int2* bcol;     // per operand column: (am | column << 8, element offset of (am, k = 0, column))
     const IstpDesc* desc;
     const int32_t* lab;   // label index of every column: input 1 [nin], input 2 [nin2], output [nout]
+    const T* pk;          // spin 2: C^{2, q1+q2}_{2 q1 2 q2} at [q1 + 2][q2 + 2] (25 entries)
 };
 
 // Multiplicity channels and label weights of a launch (the channel-wise
@@ -110,11 +111,11 @@ struct IstpLayout {
     int bytes;             // total
 };
 __host__ __device__ inline int istp_align16(int v) { return (v + 15) & ~15; }
-// staged elements: both inputs of every pair (rounded to 4), then C^{j,ml+q}_{l,ml,1,q}
-// up to the larger input degree Lm (spin 1)
+// staged elements: both inputs of every pair (rounded to 4), then C^{j,ml+q}_{l,ml,s,q}
+// up to the larger input degree Lm (spin s > 0)
 __host__ __device__ inline int istp_stage_x(int P, int nin, int nin2) { return (P * (nin + nin2) + 3) & ~3; }
 __host__ __device__ inline int istp_stage_len(int P, int nin, int nin2, int Lm, int spin) {
-    return istp_stage_x(P, nin, nin2) + (spin ? 9 * (Lm + 1) * (Lm + 1) : 0);
+    return istp_stage_x(P, nin, nin2) + (spin ? (2 * spin + 1) * (2 * spin + 1) * (Lm + 1) * (Lm + 1) : 0);
 }
 template <typename T>
 __host__ __device__ inline IstpLayout istp_layout(int A, int B, int C, int G, int P, int acoef_len, int hc_len,

@@ -70,6 +70,11 @@ template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { ret
 // value src of the row, for the label (j, l) and order m that c holds.
 template <int S>
 __device__ __forceinline__ void reverse_index(int c, int* src, bool* neg) {
+    if constexpr (S == 2) {   // spin 2 has no gradient product: never staged reversed
+        *src = c;
+        *neg = false;
+        return;
+    }
     if (S == 0) {   // c = l^2 + l + m
         int l = (int)sqrtf((float)c);
         while ((l + 1) * (l + 1) <= c) ++l;
@@ -112,7 +117,7 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
     const int P = d.pairs, nin = d.nin, nin2 = d.nin2;
     const int Lm = d.L > d.L2 ? d.L : d.L2;
     const int nx1 = P * nin, nx = nx1 + P * nin2, nxa = istp_stage_x(P, nin, nin2);
-    const int ncg = S ? 9 * (Lm + 1) * (Lm + 1) : 0;
+    const int ncg = S ? NC * NC * (Lm + 1) * (Lm + 1) : 0;
     const bool rev2 = d.flags & kReverseSecond;
     {
         T v[kStageLoads];
@@ -193,6 +198,17 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
             if (l <= Lin) {
                 if (S == 0) {
                     v = x[l * l + l + m];
+                } else if constexpr (S == 2) {
+                    // labels j = |l - 2| .. l + 2; label (j, l) starts at 5 l^2 + j^2 - (l - 2)^2
+                    const int q = c - 2, mj = m + q, jmin = l >= 2 ? l - 2 : 2 - l;
+                    const T* cg = cgs + 25 * l * l + m + l;
+#pragma unroll
+                    for (int jj = 0; jj < 5; ++jj) {
+                        const int j = l - 2 + jj;
+                        if (j < jmin || mj < -j || mj > j) continue;
+                        const int lo = 5 * l * l + j * j - (l - 2) * (l - 2);
+                        v += cg[(jj * 5 + c) * (2 * l + 1)] * x[lo + j + mj];
+                    }
                 } else {
                     const int q = c - 1, mj = m + q;
                     const T* cg = cgs + 9 * l * l + m + l;
@@ -374,6 +390,12 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         // ---- 3. products on half the circle; the product of component c goes to
         // slot NC + c (positions n and -n are read and written by one task)
         {
+            // spin 2: the coupling constants C^{2, q1+q2}_{2 q1 2 q2}, [q1 + 2][q2 + 2]
+            T kc[S == 2 ? 25 : 1];
+            if constexpr (S == 2) {
+#pragma unroll
+                for (int k = 0; k < 25; ++k) kc[k] = tb.pk[k];
+            }
             const int ntask = Uq * H;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int n = task % H;
@@ -392,6 +414,28 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                 if (S == 0) {
                     gn[0] = cmul(fn[0], fn[1]);
                     gs[0] = cmul(fs[0], fs[1]);
+                } else if constexpr (S == 2) {
+                    // 2 (x) 2 -> 2 coupling of components q = -2..2 (slots c = q + 2 of input 0, then of
+                    // input 1): g_q = sum over q1 + q2 = q of C^{2 q}_{2 q1 2 q2} a_q1 b_q2
+#pragma unroll
+                    for (int hs = 0; hs < 2; ++hs) {
+                        const C2* a = hs ? fs : fn;
+                        const C2* b = a + NC;
+                        C2* g = hs ? gs : gn;
+#pragma unroll
+                        for (int q = -2; q <= 2; ++q) {
+                            C2 acc = cmk<C2>((T)0, (T)0);
+#pragma unroll
+                            for (int q1 = -2; q1 <= 2; ++q1) {
+                                const int q2 = q - q1;
+                                if (q2 < -2 || q2 > 2) continue;
+                                const C2 ab = cmul(a[q1 + 2], b[q2 + 2]);
+                                const T k = kc[(q1 + 2) * 5 + q2 + 2];
+                                acc = cmk<C2>(acc.x + k * ab.x, acc.y + k * ab.y);
+                            }
+                            g[q + 2] = acc;
+                        }
+                    }
                 } else {
                     // antisymmetric 1 (x) 1 -> 1 coupling of components q = -1, 0, +1
                     // (slots c = q + 1 of input 0, then of input 1); its constant is in the plan's weights
@@ -501,7 +545,30 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     }
     lds_barrier();
     // ---- recombination and contiguous stores
-    {
+    if constexpr (S == 2) {
+        // five terms per output: weights and end-phase entries in two words each
+        const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
+        const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
+        const int nout = d.nout, hs = NC * no;
+        for (int o = tid; o < nout; o += kThreads) {
+            const Acc ca = cf4[2 * o], cb = cf4[2 * o + 1];
+            const int4 ia = ci4[2 * o], ib = ci4[2 * o + 1];
+            int cc = cp.c0;
+            const int lo = (CH && ch.wo) ? tb.lab[d.nin + d.nin2 + o] : 0;
+            for (int p = 0; p < np; ++p) {
+                const T* hp = hc + (size_t)p * hs;
+                T v = ca.x * hp[ia.x] + ca.y * hp[ia.y] + ca.z * hp[ia.z] + ca.w * hp[ia.w] + cb.x * hp[ib.x];
+                if constexpr (CH) {
+                    if (ch.wo) {
+                        const int64_t k = (ch.flags & kChanPerRow) ? p0 + p : cc;
+                        v *= ch.wo[k * ch.nlo + lo];
+                    }
+                    cc = cc + 1 == ch.channels ? 0 : cc + 1;
+                }
+                out[(p0 + p) * (int64_t)nout + o] = v;
+            }
+        }
+    } else {
         const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
         const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
         const int nout = d.nout, hs = NC * no;
@@ -602,8 +669,9 @@ int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2,
     const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
     if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
     void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t);
+    if (long_lift && d.spin == 2) return (int)hipErrorInvalidConfiguration;
     if (long_lift) kern = d.spin ? istp_kernel<T, 1, true> : istp_kernel<T, 0, true>;
-    else kern = d.spin ? istp_kernel<T, 1, false> : istp_kernel<T, 0, false>;
+    else kern = d.spin == 2 ? istp_kernel<T, 2, false> : (d.spin ? istp_kernel<T, 1, false> : istp_kernel<T, 0, false>);
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;
@@ -631,7 +699,7 @@ int launch_channels(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, con
     const int Lm = d.L > d.L2 ? d.L : d.L2;
     if (Lm + 1 > 4 * kMaxLiftSteps || ch.channels < 1) return (int)hipErrorInvalidConfiguration;
     void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t, IstpChan<T>) =
-        d.spin ? istp_kernel_channels<T, 1> : istp_kernel_channels<T, 0>;
+        d.spin == 2 ? istp_kernel_channels<T, 2> : (d.spin ? istp_kernel_channels<T, 1> : istp_kernel_channels<T, 0>);
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;

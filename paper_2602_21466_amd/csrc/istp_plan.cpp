@@ -44,6 +44,10 @@ const double kPi = 3.14159265358979323846264338327950288;
 int64_t label_offset(int spin, int j, int l) {
     if (l < 0 || j < 0) return -1;
     if (spin == ISTP_GAUNT) return j == l ? (int64_t)l * l : -1;
+    if (spin == ISTP_TENSOR) {   // j = |l - 2| .. l + 2 at 5 l^2 + j^2 - (l - 2)^2
+        if (j < std::abs(l - 2) || j > l + 2) return -1;
+        return 5LL * l * l + (int64_t)j * j - (int64_t)(l - 2) * (l - 2);
+    }
     if (spin != ISTP_VECTOR || std::abs(j - l) > 1 || j + l < 1) return -1;
     const int jj = j - l + 1;
     return 3LL * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
@@ -53,26 +57,33 @@ int64_t label_offset(int spin, int j, int l) {
 // the labels in row order (l, then j = l - 1, l, l + 1), i.e. 2 l - 1 + j.
 int64_t label_index(int spin, int j, int l) {
     if (label_offset(spin, j, l) < 0) return -1;
+    if (spin == ISTP_TENSOR) {   // 2 min(l', 2) + 1 labels at each degree l' < l
+        int64_t k = 0;
+        for (int lp = 0; lp < l; ++lp) k += 2 * std::min(lp, 2) + 1;
+        return k + j - std::abs(l - 2);
+    }
     return spin == ISTP_GAUNT ? l : 2LL * l - 1 + j;
 }
 
-// Labels of a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1).
+// Labels of a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1),
+// 5 L - 1 (spin 2, L >= 1; 1 at L = 0).
 int64_t num_labels(int L, int spin) {
-    if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return -1;
+    if (L < 0 || spin < ISTP_GAUNT || spin > ISTP_TENSOR) return -1;
+    if (spin == ISTP_TENSOR) return L == 0 ? 1 : 5LL * L - 1;
     return spin == ISTP_GAUNT ? L + 1 : 3LL * L + 1;
 }
 
 // Label index of every column of a row of degree bound L, appended to v.
 void append_column_labels(int L, int spin, std::vector<int32_t>& v) {
     for (int l = 0; l <= L; ++l)
-        for (int j = l - 1; j <= l + 1; ++j) {
+        for (int j = l - spin; j <= l + spin; ++j) {
             if (label_offset(spin, j, l) < 0) continue;
             for (int m = -j; m <= j; ++m) v.push_back((int32_t)label_index(spin, j, l));
         }
 }
 
 int64_t row_size(int L, int spin) {
-    if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return -1;
+    if (L < 0 || spin < ISTP_GAUNT || spin > ISTP_TENSOR) return -1;
     return (int64_t)(2 * spin + 1) * (L + 1) * (L + 1);
 }
 
@@ -100,6 +111,26 @@ int acoef_len(int L, int NC, int P) {
     return n;
 }
 
+// C^{j m}_{j1 m1 j2 m2} (Condon-Shortley phase) by Racah's single-sum formula,
+// in long double with log-factorials; 0 outside the selection rules.
+long double cg_racah(int j1, int m1, int j2, int m2, int j, int m) {
+    if (m1 + m2 != m || std::abs(m1) > j1 || std::abs(m2) > j2 || std::abs(m) > j) return 0.0L;
+    if (j < std::abs(j1 - j2) || j > j1 + j2) return 0.0L;
+    auto lf = [](int n) { return lgammal((long double)n + 1.0L); };
+    const long double pre = 0.5L * (logl(2.0L * j + 1.0L) + lf(j1 + j2 - j) + lf(j1 - j2 + j) + lf(-j1 + j2 + j) -
+                                    lf(j1 + j2 + j + 1) + lf(j1 + m1) + lf(j1 - m1) + lf(j2 + m2) + lf(j2 - m2) +
+                                    lf(j + m) + lf(j - m));
+    const int kmin = std::max({0, j2 - j - m1, j1 - j + m2});
+    const int kmax = std::min({j1 + j2 - j, j1 - m1, j2 + m2});
+    long double sum = 0.0L;
+    for (int k = kmin; k <= kmax; ++k) {
+        const long double t = expl(pre - lf(k) - lf(j1 + j2 - j - k) - lf(j1 - m1 - k) - lf(j2 + m2 - k) -
+                                   lf(j - j2 + m1 + k) - lf(j - j1 - m2 + k));
+        sum += (k & 1) ? -t : t;
+    }
+    return sum;
+}
+
 double fft_flops(int n) { return n > 1 ? 5.0 * n * std::log2((double)n) : 0.0; }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -115,6 +146,7 @@ struct Host {
     std::vector<istp::ProjTile> proj;
     std::vector<int32_t> bcol;   // 2 per operand column
     std::vector<int32_t> lab;    // label index of every column: input 1, input 2, output
+    std::vector<T> pk;           // spin 2: pointwise coupling constants
 };
 
 // Tables of the product of a degree-L1 and a degree-L2 input projected on
@@ -149,7 +181,7 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     for (int P : {8, 4, 2, 1}) {
         if (2 * NC * P > 16) continue;
         // inputs and couplings are staged with one batch of loads per thread
-        const int stage = P * (nin + nin2) + (S ? 9 * (Lm + 1) * (Lm + 1) : 0);
+        const int stage = P * (nin + nin2) + (S ? NC * NC * (Lm + 1) * (Lm + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
         for (int G : {16, 12, 8, 4}) {
             const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(Lm, NC, P), hc_len,
@@ -207,8 +239,24 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
             h.tw[2 * (t * (B + 1) + k2)] = (T)cosl(ang);
             h.tw[2 * (t * (B + 1) + k2) + 1] = (T)sinl(ang);
         }
-    // lift couplings C^{j, ml+q}_{l, ml, 1, q}, j = l - 1, l, l + 1
-    h.liftcg.assign((size_t)9 * (Lm + 1) * (Lm + 1), (T)0);
+    // lift couplings C^{j, ml+q}_{l, ml, s, q}, j = l - s .. l + s
+    h.liftcg.assign((size_t)NC * NC * (Lm + 1) * (Lm + 1), (T)0);
+    if (S == ISTP_TENSOR)
+        for (int l = 0; l <= Lm; ++l)
+            for (int jj = 0; jj < 5; ++jj)
+                for (int c = 0; c < 5; ++c)
+                    for (int ml = -l; ml <= l; ++ml) {
+                        const int j = l - 2 + jj, q = c - 2;
+                        if (j < std::abs(l - 2) || std::abs(ml + q) > j) continue;
+                        h.liftcg[(size_t)25 * l * l + (jj * 5 + c) * (2 * l + 1) + ml + l] =
+                            (T)cg_racah(l, ml, 2, q, j, ml + q);
+                    }
+    // spin 2: the pointwise coupling C^{2, q1+q2}_{2 q1 2 q2}
+    h.pk.assign(25, (T)0);
+    if (S == ISTP_TENSOR)
+        for (int q1 = -2; q1 <= 2; ++q1)
+            for (int q2 = -2; q2 <= 2; ++q2)
+                if (std::abs(q1 + q2) <= 2) h.pk[(q1 + 2) * 5 + q2 + 2] = (T)cg_racah(2, q1, 2, q2, 2, q1 + q2);
     if (S == ISTP_VECTOR)
         for (int l = 0; l <= Lm; ++l)
             for (int jj = 0; jj < 3; ++jj)
@@ -248,7 +296,26 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     const int64_t nout = row_size(Lo, S);
     h.coef.assign(4 * nout, (T)0);
     h.coefi.assign(4 * nout, 0);
-    if (S == ISTP_GAUNT) {
+    if (S == ISTP_TENSOR) {
+        // five terms per output (two words of four): q = -2..2 at (l3, m3 - q);
+        // the coupling constants are applied in the kernel's product
+        h.coef.assign(8 * nout, (T)0);
+        h.coefi.assign(8 * nout, 0);
+        for (int l3 = 0; l3 <= Lo; ++l3)
+            for (int j3 = std::abs(l3 - 2); j3 <= l3 + 2; ++j3) {
+                const int64_t off = label_offset(ISTP_TENSOR, j3, l3);
+                for (int m3 = -j3; m3 <= j3; ++m3) {
+                    const int64_t o = off + j3 + m3;
+                    for (int q = -2; q <= 2; ++q) {
+                        const int ml = m3 - q;
+                        h.coefi[8 * o + q + 2] = (int32_t)(l3 * l3 + l3);   // any entry; zero weight
+                        if (std::abs(ml) > l3) continue;
+                        h.coef[8 * o + q + 2] = (T)(cg_racah(l3, ml, 2, q, j3, m3) * scale * sgn(ml));
+                        h.coefi[8 * o + q + 2] = (q + 2) * no + l3 * l3 + l3 + ml;
+                    }
+                }
+            }
+    } else if (S == ISTP_GAUNT) {
         for (int l3 = 0; l3 <= Lo; ++l3)
             for (int m3 = -l3; m3 <= l3; ++m3) {
                 const int o = l3 * l3 + l3 + m3;
@@ -316,10 +383,14 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     // model counts per pair (what include/istp.h documents)
     const double fl_lift = 2.0 * NC * R * ((double)(L1 + 1) * (L1 + 1) + (double)(L2 + 1) * (L2 + 1));
     const double fl_syn = 2.0 * NC * R * fft_flops(Phi);
-    const double fl_prod = (double)R * (Phi / 2 + 1) * 2 * (S == ISTP_GAUNT ? 6.0 : 6 * 6.0 + 3 * 2.0);
+    // products per point and hemisphere: one complex product (spin 0); six
+    // products and three differences (spin 1); nineteen products, each scaled by
+    // a real constant, summed into five components (spin 2)
+    const double pp = S == ISTP_GAUNT ? 6.0 : (S == ISTP_VECTOR ? 6 * 6.0 + 3 * 2.0 : 19 * 8.0 + 14 * 2.0);
+    const double fl_prod = (double)R * (Phi / 2 + 1) * 2 * pp;
     const double fl_ana = (double)NC * R * fft_flops(Phi);
     const double fl_proj = 2.0 * NC * R * (double)no;
-    const double fl_rec = S == ISTP_GAUNT ? 0.0 : 2.0 * 3 * (double)nout;
+    const double fl_rec = S == ISTP_GAUNT ? 0.0 : 2.0 * NC * (double)nout;
     pr->flops_per_pair = fl_lift + fl_syn + fl_prod + fl_ana + fl_proj + fl_rec;
     pr->bytes_per_pair = (double)(d.nin + d.nin2 + d.nout) * sizeof(T);
     return CGTP_OK;
@@ -342,6 +413,7 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         {&p->desc, sizeof(istp::IstpDesc), 0},
         {h.bcol.data(), h.bcol.size() * sizeof(int32_t), 0},
         {h.lab.data(), h.lab.size() * sizeof(int32_t), 0},
+        {h.pk.data(), h.pk.size() * sizeof(T), 0},
     };
     size_t total = 0;
     for (auto& pt : parts) {
@@ -376,6 +448,7 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
     tb->bcol = (const int2*)(base + parts[9].off);
     tb->lab = (const int32_t*)(base + parts[10].off);
+    tb->pk = (const T*)(base + parts[11].off);
     p->ok = true;
     return CGTP_OK;
 }
@@ -445,8 +518,10 @@ int64_t istp_label_index(int32_t spin, int32_t j, int32_t l) { return label_inde
 int64_t istp_num_labels(int32_t L, int32_t spin) { return num_labels(L, spin); }
 
 static int check_plan_args(int32_t L, int32_t spin, int32_t dtype) {
-    if (L < 0 || (spin != ISTP_GAUNT && spin != ISTP_VECTOR)) return CGTP_EINVAL;
+    if (L < 0 || spin < ISTP_GAUNT || spin > ISTP_TENSOR) return CGTP_EINVAL;
     if (dtype != CGTP_FP32 && dtype != CGTP_FP64) return CGTP_EDTYPE;
+    if (spin == ISTP_TENSOR && L > (dtype == CGTP_FP32 ? ISTP_TENSOR_MAX_L_FP32 : ISTP_TENSOR_MAX_L_FP64))
+        return CGTP_EUNSUP;
     if (L > (dtype == CGTP_FP32 ? ISTP_MAX_L_FP32 : ISTP_MAX_L_FP64)) return CGTP_EUNSUP;
     return CGTP_OK;
 }
@@ -468,8 +543,9 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
     }
     rc = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, 0, &p->fwd, true)
                             : make_prod<double>(L, L, 2 * L, spin, 0, &p->fwd, true);
-    if (rc == CGTP_OK) {
+    if (rc == CGTP_OK && spin != ISTP_TENSOR) {
         // the gradients' product; outside the kernel's limits it stays unbuilt
+        // (and for spin 2, which has no gradient product)
         const int rb = dtype == CGTP_FP32
                            ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true)
                            : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true);
@@ -497,7 +573,8 @@ int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t* desc_out
     static_assert(sizeof(istp::IstpDesc) == 24 * sizeof(int32_t), "descriptor layout");
     std::memcpy(desc_out, &pr.desc, sizeof(istp::IstpDesc));
     // the gradients' product follows when it is within the kernel's limits
-    rc = dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false)
+    rc = spin == ISTP_TENSOR ? CGTP_EUNSUP
+         : dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false)
                             : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false);
     if (rc == CGTP_OK) std::memcpy(desc_out + 24, &pb.desc, sizeof(istp::IstpDesc));
     else std::memset(desc_out + 24, 0, sizeof(istp::IstpDesc));

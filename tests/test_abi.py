@@ -44,9 +44,17 @@ def test_istp_row_layouts_match_the_oracle():
             assert lib.istp_label_offset(1, j, l) == oi.vector_offset(j, l)
         for l in range(L + 1):
             assert lib.istp_label_offset(0, l, l) == l * l
+    for L in range(6):
+        assert lib.istp_num_inputs(L, 2) == oi.spin_size(2, L)
+        assert lib.istp_num_outputs(L, 2) == oi.spin_size(2, 2 * L)
+        assert lib.istp_num_labels(L, 2) == len(oi.spin_labels(2, L))
+        for k, (j, l) in enumerate(oi.spin_labels(2, L)):
+            assert lib.istp_label_offset(2, j, l) == oi.spin_offset(2, j, l)
+            assert lib.istp_label_index(2, j, l) == k
     assert lib.istp_label_offset(1, 0, 0) == -1 and lib.istp_label_offset(1, 3, 1) == -1
     assert lib.istp_label_offset(0, 1, 2) == -1 and lib.istp_num_inputs(-1, 0) == -1
-    assert lib.istp_num_inputs(3, 2) == -1
+    assert lib.istp_label_offset(2, 1, 0) == -1 and lib.istp_label_offset(2, 0, 1) == -1
+    assert lib.istp_num_inputs(3, 3) == -1
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "fp64"])
@@ -54,8 +62,9 @@ def test_istp_plan_geometry(dtype):
     """Every supported plan fits LDS and the accumulator budget; the grid is the exact one."""
     esz = 4 if dtype == "fp32" else 8
     mt = 13 if dtype == "fp32" else 4
-    for spin in (0, 1):
-        for L in range(lib.ISTP_MAX_L[dtype] + 1):
+    for spin in (0, 1, 2):
+        lmax = (lib.ISTP_TENSOR_MAX_L if spin == 2 else lib.ISTP_MAX_L)[dtype]
+        for L in range(lmax + 1):
             d = lib.istp_plan_describe(L, spin, dtype)
             assert d["R"] == L + 1 and d["Phi"] >= 4 * L + 1 and d["A"] * d["B"] == d["Phi"]
             assert d["lds_bytes"] <= 156 * 1024
@@ -65,4 +74,4 @@ def test_istp_plan_geometry(dtype):
             assert d["nin"] == lib.istp_num_inputs(L, spin) and d["nout"] == lib.istp_num_outputs(L, spin)
             assert d["pairs"] * d["hc_len"] * esz + 16 <= d["lds_bytes"] + 16
         with pytest.raises(lib.CgtpError):
-            lib.istp_plan_describe(lib.ISTP_MAX_L[dtype] + 1, spin, dtype)
+            lib.istp_plan_describe(lmax + 1, spin, dtype)

@@ -23,6 +23,8 @@ CASES = [
     (1, 8, 5, 7, True, "channel", "fp32"),
     (0, 3, 5, 3, True, "channel", "fp64"),
     (1, 2, 4, 6, False, "pair", "fp64"),
+    (2, 3, 5, 3, True, "channel", "fp32"),
+    (2, 2, 3, 2, False, "pair", "fp64"),
 ]
 
 

@@ -37,7 +37,7 @@ def _labels(L, spin):
         labels = [(l, l) for l in range(L + 1)]
         sizes = [2 * l + 1 for l in range(L + 1)]
     else:
-        labels = oi.vector_labels(L)
+        labels = oi.vector_labels(L) if spin == 1 else oi.spin_labels(spin, L)
         sizes = [2 * j + 1 for j, l in labels]
     return np.repeat(np.arange(len(labels)), sizes), labels
 
@@ -53,8 +53,10 @@ def per_label_rel_err(L_out, spin, got, ref):
 
 
 def reference(L, spin, x1, x2):
-    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
-    return fn(L, np.asarray(x1, dtype=np.float64), np.asarray(x2, dtype=np.float64))
+    a, b = np.asarray(x1, dtype=np.float64), np.asarray(x2, dtype=np.float64)
+    if spin == 2:
+        return oi.spin_tp(2, L, a, b)
+    return (oi.gaunt_tp if spin == 0 else oi.vector_tp)(L, a, b)
 
 
 def run_gpu(L, spin, x1, x2, dtype):
@@ -68,7 +70,10 @@ def run_gpu(L, spin, x1, x2, dtype):
 
 CASES = [(0, 0, 5, "fp32"), (0, 1, 5, "fp64"), (1, 0, 17, "fp64"), (1, 1, 9, "fp32"), (2, 1, 64, "fp64"),
          (2, 0, 64, "fp32"), (3, 1, 33, "fp32"), (4, 0, 100, "fp32"), (5, 1, 19, "fp64"), (6, 1, 21, "fp32"),
-         (8, 0, 37, "fp64"), (8, 1, 40, "fp32"), (12, 1, 7, "fp64"), (12, 0, 9, "fp32")]
+         (8, 0, 37, "fp64"), (8, 1, 40, "fp32"), (12, 1, 7, "fp64"), (12, 0, 9, "fp32"),
+         # spin 2 (rank-2 tensor harmonics): one pair per work-group
+         (0, 2, 5, "fp32"), (1, 2, 7, "fp32"), (2, 2, 9, "fp64"), (3, 2, 11, "fp32"), (5, 2, 6, "fp32"),
+         (6, 2, 4, "fp64"), (8, 2, 3, "fp32")]
 
 
 @pytest.mark.parametrize("L,spin,N,dtype", CASES)
@@ -99,7 +104,7 @@ def test_same_input_twice_and_symmetry():
     """x1 == x2 (one buffer) is allowed; the Gaunt product is symmetric, the vector one antisymmetric."""
     torch = _torch()
     L = 6
-    for spin, sign in ((0, 1.0), (1, -1.0)):
+    for spin, sign in ((0, 1.0), (1, -1.0), (2, 1.0)):
         x1, x2 = wl.draw_rows((2 * spin + 1) * (L + 1) ** 2, 11, "fp64", seed=77 + spin)
         plan = _lib().IstpPlan(L, spin, "fp64")
         a, b = x1.cuda(), x2.cuda()
@@ -131,7 +136,8 @@ def test_empty_and_errors():
         lib.istp_forward(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), -1, None)
     assert e.value.code == lib.CGTP_EINVAL
     for L, spin, dtype, code in [(34, 0, "fp32", lib.CGTP_EUNSUP), (13, 1, "fp64", lib.CGTP_EUNSUP),
-                                 (-1, 0, "fp32", lib.CGTP_EINVAL), (2, 2, "fp32", lib.CGTP_EINVAL),
+                                 (21, 2, "fp32", lib.CGTP_EUNSUP), (13, 2, "fp64", lib.CGTP_EUNSUP),
+                                 (-1, 0, "fp32", lib.CGTP_EINVAL), (2, 3, "fp32", lib.CGTP_EINVAL),
                                  (2, 0, 7, lib.CGTP_EDTYPE)]:
         with pytest.raises(lib.CgtpError) as e:
             lib.istp_plan(L, spin, dtype)
@@ -143,7 +149,8 @@ def test_empty_and_errors():
 
 def test_largest_sizes():
     """The largest L of each precision (fp32 at L = 33 on a few pairs, fp64 at L = 12)."""
-    for L, spin, N, dtype in ((33, 1, 2, "fp32"), (33, 0, 3, "fp32"), (12, 1, 3, "fp64")):
+    for L, spin, N, dtype in ((33, 1, 2, "fp32"), (33, 0, 3, "fp32"), (12, 1, 3, "fp64"), (20, 2, 2, "fp32"),
+                              (12, 2, 2, "fp64")):
         x1, x2 = wl.draw_rows((2 * spin + 1) * (L + 1) ** 2, N, dtype, seed=500 + L + spin)
         got = run_gpu(L, spin, x1, x2, dtype)
         err, lab = per_label_rel_err(2 * L, spin, got, reference(L, spin, x1, x2))
@@ -231,3 +238,18 @@ def test_backward_errors():
     q = plan.backward_query()
     assert q["flops_per_pair"] > 0 and q["pairs_per_group"] >= 1
     torch.cuda.synchronize()
+
+
+def test_spin_two_has_no_gradients():
+    """Spin-2 plans are forward only: istp_backward reports CGTP_EUNSUP and launches nothing."""
+    torch = _torch()
+    lib = _lib()
+    plan = lib.IstpPlan(3, 2, "fp32")
+    x = torch.zeros((2, plan.nin), device="cuda")
+    g = torch.zeros((2, plan.nout), device="cuda")
+    gx = torch.zeros((2, plan.nin), device="cuda")
+    with pytest.raises(lib.CgtpError) as e:
+        lib.istp_backward(plan._h, x.data_ptr(), x.data_ptr(), g.data_ptr(), gx.data_ptr(), None, 2, None)
+    assert e.value.code == lib.CGTP_EUNSUP
+    torch.cuda.synchronize()
+
