@@ -18,6 +18,12 @@ constexpr int kMaxLiftSteps = 9;   // K = 4 lift steps whose weights a wave load
 template <typename T> struct MaxTiles;
 template <> struct MaxTiles<float> { static constexpr int value = 13; };
 template <> struct MaxTiles<double> { static constexpr int value = 4; };
+// Spin 2 holds its products' ten components in registers: at most 7 tiles a
+// wave (its projections need at most 98 tiles, L <= 20).
+template <typename T>
+__host__ __device__ constexpr int max_tiles(int S) {
+    return S == 2 && MaxTiles<T>::value > 7 ? 7 : MaxTiles<T>::value;
+}
 
 // One product: a first input of degree <= L and a second of degree <= L2
 // lifted to spin-S signals, the pointwise product projected on degrees <= Lo
@@ -79,7 +85,6 @@ struct IstpTables {
     const int2* bcol;     // per operand column: (am | column << 8, element offset of (am, k = 0, column))
     const IstpDesc* desc;
     const int32_t* lab;   // label index of every column: input 1 [nin], input 2 [nin2], output [nout]
-    const T* pk;          // spin 2: C^{2, q1+q2}_{2 q1 2 q2} at [q1 + 2][q2 + 2] (25 entries)
 };
 
 // Multiplicity channels and label weights of a launch (the channel-wise
@@ -149,6 +154,16 @@ int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float*
                     int64_t N, void* stream);
 int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
                     double* out, int64_t N, void* stream);
+int launch_istp_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                           float* out, int64_t N, void* stream);
+int launch_istp_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                           double* out, int64_t N, void* stream);
+int launch_istp_channels_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1,
+                                    const float* x2, float* out, int64_t N, const IstpChan<float>& ch,
+                                    void* stream);
+int launch_istp_channels_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1,
+                                    const double* x2, double* out, int64_t N, const IstpChan<double>& ch,
+                                    void* stream);
 int launch_istp_channels_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
                              float* out, int64_t N, const IstpChan<float>& ch, void* stream);
 int launch_istp_channels_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,

@@ -43,6 +43,12 @@
 #ifndef ISTP_CHANNEL_KERNELS
 #define ISTP_CHANNEL_KERNELS 0
 #endif
+// With ISTP_TENSOR_KERNELS set to 1 the same two kinds are built for spin 2
+// only (istp_kernels_tensor.hip, istp_kernels_channels_tensor.hip): a
+// translation unit of its own compiles in parallel with the others.
+#ifndef ISTP_TENSOR_KERNELS
+#define ISTP_TENSOR_KERNELS 0
+#endif
 
 namespace istp {
 namespace {
@@ -238,7 +244,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     constexpr int FS = A * BP;
     constexpr int NC = 2 * S + 1;   // spin components
     constexpr int NS = 2 * NC;      // synthesis transforms per unit
-    constexpr int MT = MaxTiles<T>::value;
+    constexpr int MT = max_tiles<T>(S);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -390,12 +396,6 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         // ---- 3. products on half the circle; the product of component c goes to
         // slot NC + c (positions n and -n are read and written by one task)
         {
-            // spin 2: the coupling constants C^{2, q1+q2}_{2 q1 2 q2}, [q1 + 2][q2 + 2]
-            T kc[S == 2 ? 25 : 1];
-            if constexpr (S == 2) {
-#pragma unroll
-                for (int k = 0; k < 25; ++k) kc[k] = tb.pk[k];
-            }
             const int ntask = Uq * H;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int n = task % H;
@@ -403,6 +403,40 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                 const int kk = n == 0 ? 0 : Phi - n;
                 const int pn = n + n / B, pk = kk + kk / B;
                 // unpacked (times 2): north = F(n) + conj F(-n), south = -i (F(n) - conj F(-n))
+                C2 gn[NC], gs[NC];
+                if constexpr (S == 2) {
+                    // 2 (x) 2 -> 2 coupling of components q = -2..2 (slots c = q + 2 of input 0, then of
+                    // input 1), one hemisphere at a time (its ten unpacked components only).
+                    // C^{2 q}_{2 q1 2 q2} is +-1, +-2 or +-sqrt(6) times 1 / sqrt(14); the common factor
+                    // is in the plan's recombination weights (which checks this pattern)
+                    const T r6 = (T)2.449489742783178098197284;   // sqrt(6)
+#pragma unroll
+                    for (int hs = 0; hs < 2; ++hs) {
+                        C2 f[NS];
+#pragma unroll
+                        for (int s2 = 0; s2 < NS; ++s2) {
+                            const C2 Fn = fb[s2 * FS + pn], Fk = fb[s2 * FS + pk];
+                            f[s2] = hs ? cmk<C2>(Fn.y + Fk.y, Fk.x - Fn.x) : cmk<C2>(Fn.x + Fk.x, Fn.y - Fk.y);
+                        }
+                        const C2* a = f;        // a[q + 2]
+                        const C2* b = f + NC;   // b[q + 2]
+                        C2* g = hs ? gs : gn;
+                        auto lin = [](T u, C2 x, T v, C2 y) { return cmk<C2>(u * x.x + v * y.x, u * x.y + v * y.y); };
+                        // q = +2: 2 (a0 b2 + a2 b0) - sqrt6 a1 b1
+                        g[4] = lin((T)2, cadd(cmul(a[2], b[4]), cmul(a[4], b[2])), -r6, cmul(a[3], b[3]));
+                        // q = +1: sqrt6 (a-1 b2 + a2 b-1) - (a0 b1 + a1 b0)
+                        g[3] = lin(r6, cadd(cmul(a[1], b[4]), cmul(a[4], b[1])), (T)-1,
+                                   cadd(cmul(a[2], b[3]), cmul(a[3], b[2])));
+                        // q = 0: 2 (a-2 b2 + a2 b-2) + (a-1 b1 + a1 b-1) - 2 a0 b0
+                        g[2] = cadd(lin((T)2, cadd(cmul(a[0], b[4]), cmul(a[4], b[0])), (T)-2, cmul(a[2], b[2])),
+                                    cadd(cmul(a[1], b[3]), cmul(a[3], b[1])));
+                        // q = -1: sqrt6 (a-2 b1 + a1 b-2) - (a-1 b0 + a0 b-1)
+                        g[1] = lin(r6, cadd(cmul(a[0], b[3]), cmul(a[3], b[0])), (T)-1,
+                                   cadd(cmul(a[1], b[2]), cmul(a[2], b[1])));
+                        // q = -2: 2 (a-2 b0 + a0 b-2) - sqrt6 a-1 b-1
+                        g[0] = lin((T)2, cadd(cmul(a[0], b[2]), cmul(a[2], b[0])), -r6, cmul(a[1], b[1]));
+                    }
+                } else {
                 C2 fn[NS], fs[NS];
 #pragma unroll
                 for (int s = 0; s < NS; ++s) {
@@ -410,32 +444,9 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     fn[s] = cmk<C2>(Fn.x + Fk.x, Fn.y - Fk.y);
                     fs[s] = cmk<C2>(Fn.y + Fk.y, Fk.x - Fn.x);
                 }
-                C2 gn[NC], gs[NC];
                 if (S == 0) {
                     gn[0] = cmul(fn[0], fn[1]);
                     gs[0] = cmul(fs[0], fs[1]);
-                } else if constexpr (S == 2) {
-                    // 2 (x) 2 -> 2 coupling of components q = -2..2 (slots c = q + 2 of input 0, then of
-                    // input 1): g_q = sum over q1 + q2 = q of C^{2 q}_{2 q1 2 q2} a_q1 b_q2
-#pragma unroll
-                    for (int hs = 0; hs < 2; ++hs) {
-                        const C2* a = hs ? fs : fn;
-                        const C2* b = a + NC;
-                        C2* g = hs ? gs : gn;
-#pragma unroll
-                        for (int q = -2; q <= 2; ++q) {
-                            C2 acc = cmk<C2>((T)0, (T)0);
-#pragma unroll
-                            for (int q1 = -2; q1 <= 2; ++q1) {
-                                const int q2 = q - q1;
-                                if (q2 < -2 || q2 > 2) continue;
-                                const C2 ab = cmul(a[q1 + 2], b[q2 + 2]);
-                                const T k = kc[(q1 + 2) * 5 + q2 + 2];
-                                acc = cmk<C2>(acc.x + k * ab.x, acc.y + k * ab.y);
-                            }
-                            g[q + 2] = acc;
-                        }
-                    }
                 } else {
                     // antisymmetric 1 (x) 1 -> 1 coupling of components q = -1, 0, +1
                     // (slots c = q + 1 of input 0, then of input 1); its constant is in the plan's weights
@@ -448,6 +459,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                         g[1] = csub(cmul(a[2], b[0]), cmul(a[0], b[2]));
                         g[0] = csub(cmul(a[1], b[0]), cmul(a[0], b[1]));
                     }
+                }
                 }
 #pragma unroll
                 for (int c = 0; c < NC; ++c) {
@@ -626,7 +638,8 @@ __device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc
     const int np = (int)((N - p0) < d.pairs ? (N - p0) : d.pairs);
 #define ISTP_CASE(PHI, A_, B_)                                                                      \
     case PHI:                                                                                       \
-        if constexpr ((sizeof(T) == 4 || PHI <= 54) && (!LONG || (sizeof(T) == 4 && PHI >= 72)))    \
+        if constexpr ((sizeof(T) == 4 || PHI <= 54) && (!LONG || (sizeof(T) == 4 && PHI >= 72)) &&  \
+                      (S != 2 || PHI <= 81))                                                        \
             istp_body<T, A_, B_, S, LONG, CH>(tb, d, p0, np, x1, x2, out, ch, smem);                \
         break;
     switch (d.Phi) {
@@ -669,9 +682,14 @@ int launch(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2,
     const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
     if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
     void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t);
-    if (long_lift && d.spin == 2) return (int)hipErrorInvalidConfiguration;
+#if !ISTP_TENSOR_KERNELS
+    if (d.spin != 0 && d.spin != 1) return (int)hipErrorInvalidConfiguration;
     if (long_lift) kern = d.spin ? istp_kernel<T, 1, true> : istp_kernel<T, 0, true>;
-    else kern = d.spin == 2 ? istp_kernel<T, 2, false> : (d.spin ? istp_kernel<T, 1, false> : istp_kernel<T, 0, false>);
+    else kern = d.spin ? istp_kernel<T, 1, false> : istp_kernel<T, 0, false>;
+#else
+    if (d.spin != 2 || long_lift || d.Phi > 81) return (int)hipErrorInvalidConfiguration;
+    kern = istp_kernel<T, 2, false>;
+#endif
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;
@@ -698,8 +716,14 @@ int launch_channels(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, con
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     const int Lm = d.L > d.L2 ? d.L : d.L2;
     if (Lm + 1 > 4 * kMaxLiftSteps || ch.channels < 1) return (int)hipErrorInvalidConfiguration;
-    void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t, IstpChan<T>) =
-        d.spin == 2 ? istp_kernel_channels<T, 2> : (d.spin ? istp_kernel_channels<T, 1> : istp_kernel_channels<T, 0>);
+    void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t, IstpChan<T>);
+#if !ISTP_TENSOR_KERNELS
+    if (d.spin != 0 && d.spin != 1) return (int)hipErrorInvalidConfiguration;
+    kern = d.spin ? istp_kernel_channels<T, 1> : istp_kernel_channels<T, 0>;
+#else
+    if (d.spin != 2 || d.Phi > 81) return (int)hipErrorInvalidConfiguration;
+    kern = istp_kernel_channels<T, 2>;
+#endif
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;
@@ -712,7 +736,10 @@ int launch_channels(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, con
 
 }  // namespace
 
-#if !ISTP_CHANNEL_KERNELS
+// Exported launchers: spins 0 and 1 from istp_kernels.hip and
+// istp_kernels_channels.hip; spin 2 from istp_kernels_tensor.hip and
+// istp_kernels_channels_tensor.hip.
+#if !ISTP_CHANNEL_KERNELS && !ISTP_TENSOR_KERNELS
 int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
                     int64_t N, void* stream) {
     return launch<float>(tb, d, x1, x2, out, N, stream);
@@ -721,13 +748,33 @@ int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const doubl
                     double* out, int64_t N, void* stream) {
     return launch<double>(tb, d, x1, x2, out, N, stream);
 }
-#else
+#elif !ISTP_CHANNEL_KERNELS
+int launch_istp_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                           float* out, int64_t N, void* stream) {
+    return launch<float>(tb, d, x1, x2, out, N, stream);
+}
+int launch_istp_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                           double* out, int64_t N, void* stream) {
+    return launch<double>(tb, d, x1, x2, out, N, stream);
+}
+#elif !ISTP_TENSOR_KERNELS
 int launch_istp_channels_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
                              float* out, int64_t N, const IstpChan<float>& ch, void* stream) {
     return launch_channels<float>(tb, d, x1, x2, out, N, ch, stream);
 }
 int launch_istp_channels_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
                              double* out, int64_t N, const IstpChan<double>& ch, void* stream) {
+    return launch_channels<double>(tb, d, x1, x2, out, N, ch, stream);
+}
+#else
+int launch_istp_channels_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1,
+                                    const float* x2, float* out, int64_t N, const IstpChan<float>& ch,
+                                    void* stream) {
+    return launch_channels<float>(tb, d, x1, x2, out, N, ch, stream);
+}
+int launch_istp_channels_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1,
+                                    const double* x2, double* out, int64_t N, const IstpChan<double>& ch,
+                                    void* stream) {
     return launch_channels<double>(tb, d, x1, x2, out, N, ch, stream);
 }
 #endif

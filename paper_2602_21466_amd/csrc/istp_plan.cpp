@@ -146,7 +146,6 @@ struct Host {
     std::vector<istp::ProjTile> proj;
     std::vector<int32_t> bcol;   // 2 per operand column
     std::vector<int32_t> lab;    // label index of every column: input 1, input 2, output
-    std::vector<T> pk;           // spin 2: pointwise coupling constants
 };
 
 // Tables of the product of a degree-L1 and a degree-L2 input projected on
@@ -164,11 +163,13 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     if (Lm + 1 > 255) return CGTP_EUNSUP;   // the column table packs am in 8 bits
     // lifts longer than 4 istp::kMaxLiftSteps degrees run in a kernel built for fp32, Phi >= 72
     if (Lm + 1 > 4 * istp::kMaxLiftSteps && (sizeof(T) != 4 || Phi < 72)) return CGTP_EUNSUP;
+    // spin 2 is built for grids of at most 81 longitudes (L <= 20 forward) and short lifts
+    if (S == ISTP_TENSOR && (Phi > 81 || Lm + 1 > 4 * istp::kMaxLiftSteps)) return CGTP_EUNSUP;
 
     int nproj = 0;
     for (int am = 0; am <= Lo; ++am)
         for (int par = 0; par < 2; ++par) nproj += (proj_rows(Lo, am, par) + 15) / 16;
-    if (nproj > istp::MaxTiles<T>::value * istp::kWaves) return CGTP_EUNSUP;
+    if (nproj > istp::max_tiles<T>(S) * istp::kWaves) return CGTP_EUNSUP;
 
     // Pairs per work-group and ring pairs per group: the most pairs that fit in
     // LDS with the projection's columns (sign, component, pair) on one MFMA tile
@@ -251,12 +252,7 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
                         h.liftcg[(size_t)25 * l * l + (jj * 5 + c) * (2 * l + 1) + ml + l] =
                             (T)cg_racah(l, ml, 2, q, j, ml + q);
                     }
-    // spin 2: the pointwise coupling C^{2, q1+q2}_{2 q1 2 q2}
-    h.pk.assign(25, (T)0);
-    if (S == ISTP_TENSOR)
-        for (int q1 = -2; q1 <= 2; ++q1)
-            for (int q2 = -2; q2 <= 2; ++q2)
-                if (std::abs(q1 + q2) <= 2) h.pk[(q1 + 2) * 5 + q2 + 2] = (T)cg_racah(2, q1, 2, q2, 2, q1 + q2);
+
     if (S == ISTP_VECTOR)
         for (int l = 0; l <= Lm; ++l)
             for (int jj = 0; jj < 3; ++jj)
@@ -297,8 +293,22 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     h.coef.assign(4 * nout, (T)0);
     h.coefi.assign(4 * nout, 0);
     if (S == ISTP_TENSOR) {
-        // five terms per output (two words of four): q = -2..2 at (l3, m3 - q);
-        // the coupling constants are applied in the kernel's product
+        // five terms per output (two words of four): q = -2..2 at (l3, m3 - q).
+        // The kernel forms the 2 (x) 2 -> 2 products with C^{2 q}_{2 q1 2 q2}
+        // in units of c2 = 1 / sqrt(14) (+-1, +-2, +-sqrt(6)); c2 is applied here.
+        const long double c2 = 1.0L / sqrtl(14.0L), r6 = sqrtl(6.0L);
+        for (int q1 = -2; q1 <= 2; ++q1)
+            for (int q2 = -2; q2 <= 2; ++q2) {
+                const int q = q1 + q2;
+                if (std::abs(q) > 2) continue;
+                // the kernel's weight of a_q1 b_q2 in g_q
+                long double w;
+                const int lo = std::min(std::abs(q1), std::abs(q2)), hi = std::max(std::abs(q1), std::abs(q2));
+                if (q == 0) w = q1 == 0 ? -2.0L : (std::abs(q1) == 2 ? 2.0L : 1.0L);
+                else if (std::abs(q) == 2) w = (q1 == q2) ? -r6 : 2.0L;
+                else w = (lo == 1 && hi == 2) ? r6 : -1.0L;
+                if (fabsl(cg_racah(2, q1, 2, q2, 2, q) - w * c2) > 1e-15L) return CGTP_EINVAL;
+            }
         h.coef.assign(8 * nout, (T)0);
         h.coefi.assign(8 * nout, 0);
         for (int l3 = 0; l3 <= Lo; ++l3)
@@ -310,7 +320,7 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
                         const int ml = m3 - q;
                         h.coefi[8 * o + q + 2] = (int32_t)(l3 * l3 + l3);   // any entry; zero weight
                         if (std::abs(ml) > l3) continue;
-                        h.coef[8 * o + q + 2] = (T)(cg_racah(l3, ml, 2, q, j3, m3) * scale * sgn(ml));
+                        h.coef[8 * o + q + 2] = (T)(cg_racah(l3, ml, 2, q, j3, m3) * c2 * scale * sgn(ml));
                         h.coefi[8 * o + q + 2] = (q + 2) * no + l3 * l3 + l3 + ml;
                     }
                 }
@@ -413,7 +423,6 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
         {&p->desc, sizeof(istp::IstpDesc), 0},
         {h.bcol.data(), h.bcol.size() * sizeof(int32_t), 0},
         {h.lab.data(), h.lab.size() * sizeof(int32_t), 0},
-        {h.pk.data(), h.pk.size() * sizeof(T), 0},
     };
     size_t total = 0;
     for (auto& pt : parts) {
@@ -448,7 +457,6 @@ int upload(istp_prod* p, const Host<T>& h, istp::IstpTables<T>* tb) {
     tb->desc = (const istp::IstpDesc*)(base + parts[8].off);
     tb->bcol = (const int2*)(base + parts[9].off);
     tb->lab = (const int32_t*)(base + parts[10].off);
-    tb->pk = (const T*)(base + parts[11].off);
     p->ok = true;
     return CGTP_OK;
 }
@@ -482,10 +490,13 @@ int launch_prod(const istp_plan_s* plan, const istp_prod& pr, int flags, const v
                 int64_t N, void* stream) {
     istp::IstpDesc d = pr.desc;
     d.flags = flags;
-    const int err = plan->dtype == CGTP_FP32
-                        ? istp::launch_istp_f32(pr.tf, d, (const float*)a, (const float*)b, (float*)out, N, stream)
-                        : istp::launch_istp_f64(pr.td, d, (const double*)a, (const double*)b, (double*)out, N,
-                                                stream);
+    const bool t2 = d.spin == ISTP_TENSOR;
+    const int err =
+        plan->dtype == CGTP_FP32
+            ? (t2 ? istp::launch_istp_tensor_f32 : istp::launch_istp_f32)(pr.tf, d, (const float*)a, (const float*)b,
+                                                                          (float*)out, N, stream)
+            : (t2 ? istp::launch_istp_tensor_f64 : istp::launch_istp_f64)(pr.td, d, (const double*)a,
+                                                                          (const double*)b, (double*)out, N, stream);
     if (err != 0) {
         cgtp::set_last_hip_error(err);
         return CGTP_EHIP;
@@ -659,13 +670,13 @@ int istp_forward_weighted(istp_plan_t plan, const void* x1, const void* x2, cons
     if (plan->dtype == CGTP_FP32) {
         const istp::IstpChan<float> c{(const float*)w1, (const float*)w2, (const float*)wo, C, flags,
                                       (int32_t)nl, (int32_t)nl, (int32_t)nlo};
-        err = istp::launch_istp_channels_f32(plan->fwd.tf, d, (const float*)x1, (const float*)x2, (float*)out, rows,
-                                             c, hip_stream);
+        err = (plan->spin == ISTP_TENSOR ? istp::launch_istp_channels_tensor_f32 : istp::launch_istp_channels_f32)(
+            plan->fwd.tf, d, (const float*)x1, (const float*)x2, (float*)out, rows, c, hip_stream);
     } else {
         const istp::IstpChan<double> c{(const double*)w1, (const double*)w2, (const double*)wo, C, flags,
                                        (int32_t)nl, (int32_t)nl, (int32_t)nlo};
-        err = istp::launch_istp_channels_f64(plan->fwd.td, d, (const double*)x1, (const double*)x2, (double*)out,
-                                             rows, c, hip_stream);
+        err = (plan->spin == ISTP_TENSOR ? istp::launch_istp_channels_tensor_f64 : istp::launch_istp_channels_f64)(
+            plan->fwd.td, d, (const double*)x1, (const double*)x2, (double*)out, rows, c, hip_stream);
     }
     if (err != 0) {
         cgtp::set_last_hip_error(err);
