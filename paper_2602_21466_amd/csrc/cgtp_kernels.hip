@@ -157,12 +157,21 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // Legendre rows of every ring in longitude order: entry n of (ring, input j)
     // is P_j^|m| at the order m = n or n - Phi that longitude index n carries in
     // the synthesis, zero for |m| > j (Phi > 2 j, so n <= Phi / 2 gives m = n)
-    for (int e = tid; e < R * 2 * Phi; e += kThreads) {
-        const int ri = e / Phi, n = e - ri * Phi;
-        const int j = (ri & 1) ? j2 : j1;
-        const int m = n <= Phi / 2 ? n : n - Phi, am = m < 0 ? -m : m;
-        const T* prow = tb.pbar + bd.pbar_off + (size_t)(ri >> 1) * bd.pbar_stride;
-        prn[e] = am <= j ? prow[j * (j + 1) / 2 + am] : (T)0;
+    // (four entries per thread at a time: their loads are in flight together)
+    for (int e0 = tid; e0 < R * 2 * Phi; e0 += 4 * kThreads) {
+        T v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * kThreads;
+            const int ri = e / Phi, n = e - ri * Phi;
+            const int j = (ri & 1) ? j2 : j1;
+            const int m = n <= Phi / 2 ? n : n - Phi, am = m < 0 ? -m : m;
+            const T* prow = tb.pbar + bd.pbar_off + (size_t)(ri >> 1) * bd.pbar_stride;
+            v[u] = (e < R * 2 * Phi && am <= j) ? prow[j * (j + 1) / 2 + am] : (T)0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (e0 + u * kThreads < R * 2 * Phi) prn[e0 + u * kThreads] = v[u];
     }
 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
@@ -498,9 +507,20 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     {
         const int nblk = n1 * n2;
         T* ob = out + p0 * nout + bd.out_off;
+        // the next output's coefficients are loaded while this one is stored
+        Coef4 cfn{};
+        int4 ixn{};
+        if (tid < nblk) {
+            cfn = coef4[tid];
+            ixn = coefi[tid];
+        }
         for (int o = tid; o < nblk; o += kThreads) {
-            const Coef4 cf = coef4[o];
-            const int4 ix = coefi[o];
+            const Coef4 cf = cfn;
+            const int4 ix = ixn;
+            if (o + kThreads < nblk) {
+                cfn = coef4[o + kThreads];
+                ixn = coefi[o + kThreads];
+            }
             const bool one = ix.w & 1;   // scalar-scalar or dot path: one term
             // four rows at a time (row p's entries are 4 p further on)
             for (int pb = 0; pb < np; pb += 4) {
