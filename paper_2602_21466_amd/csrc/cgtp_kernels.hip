@@ -223,6 +223,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         T* fz = reinterpret_cast<T*>(fbuf);
         for (int e = tid; e < kRingGroup * ly.per_r * 2; e += kThreads) fz[e] = (T)0;
     }
+    // the couplings (lc) are read by other waves in the first tile's lift fill
+    lds_barrier();
 
     const bool x2s = CH && (ch.flags & kX2Shared);
     for (int64_t pt = pt0; pt < pt1; ++pt) {
