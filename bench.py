@@ -33,22 +33,22 @@ PEAK_HBM_GBS = 8000.0
 # (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "d17bc428c7c1620e": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 346603.5, "fetch_scale": 1.999956, "write_kib": 4920391.2, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 203101.4, "fetch_scale": 1.999956, "write_kib": 2740647.2, "write_scale": 1.000000},
+    "11760e4f080b1fea": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 432209.5, "fetch_scale": 1.999956, "write_kib": 4871641.2, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 206265.0, "fetch_scale": 1.999956, "write_kib": 2739751.3, "write_scale": 1.000000},
     },
-    "07ff4a6792eb4483": {
-        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 116520.5, "fetch_scale": 1.999956, "write_kib": 2741448.1, "write_scale": 1.000000},
+    "98b2595f487717ca": {
+        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118418.4, "fetch_scale": 1.999956, "write_kib": 2739754.7, "write_scale": 1.000000},
     },
     "4829bf158776de88": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 302326.6, "fetch_scale": 1.999956, "write_kib": 811653.2, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 404543.9, "fetch_scale": 1.999956, "write_kib": 1084120.5, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 227655.4, "fetch_scale": 1.999956, "write_kib": 837122.7, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068438.8, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
-        "tstp_L16_N16384_fp32": {"fetch_kib": 97021.6, "fetch_scale": 1.999956, "write_kib": 348928.0, "write_scale": 1.000000},
+        "vstp_L32_N16384_fp32": {"fetch_kib": 295863.6, "fetch_scale": 1.999956, "write_kib": 811653.6, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 404629.5, "fetch_scale": 1.999956, "write_kib": 1084122.8, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227654.3, "fetch_scale": 1.999956, "write_kib": 837122.4, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068388.4, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
+        "tstp_L16_N16384_fp32": {"fetch_kib": 97021.5, "fetch_scale": 1.999956, "write_kib": 348928.0, "write_scale": 1.000000},
     },
     "667ed8390a21448f": {
-        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170409.2, "fetch_scale": 1.999956, "write_kib": 837126.8, "write_scale": 1.000000},
+        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170364.4, "fetch_scale": 1.999956, "write_kib": 837125.8, "write_scale": 1.000000},
     },
 }
 

@@ -889,7 +889,8 @@ int forward_rows(cgtp_plan_t plan, const void* x1, const void* x2, const void* w
     int64_t total_tiles = 0;
     for (const auto& cl : plan->classes) total_tiles += (N + cl.pairs - 1) / cl.pairs * cl.count;
     const int64_t target_wgs = 16384;
-    int tpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, total_tiles / target_wgs));
+    // (at most 16: same-process A/B against 8, 32 and 64 at L = 32 and 16)
+    int tpw = (int)std::max<int64_t>(1, std::min<int64_t>(16, total_tiles / target_wgs));
     for (int c = 0; c < map.ncls; ++c) {
         const auto& cl = plan->classes[c];
         map.pairs[c] = cl.pairs;
