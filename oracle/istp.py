@@ -316,3 +316,51 @@ def channel_product(spin: int, L: int, x1, x2, w1=None, w2=None, wo=None, thread
 
     z = fn(L, scale(a, w1, L).reshape(n * c, nin), scale(b, w2, L).reshape(n * c, nin), threads)
     return scale(z.reshape(n, c, -1), wo, 2 * L)
+
+
+# ---------------------------------------------------------------- real spherical harmonics
+#
+# Real harmonics with the Condon-Shortley phase carried over from Y_l^m:
+#     Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m      (m > 0)
+#     Y^R_{l,0} = Y_l^0
+#     Y^R_{l,m} = sqrt(2) (-1)^m Im Y_l^{|m|}  (m < 0)
+# (index l^2 + l + m, as for the complex basis).  A real function
+# f = sum r_lm Y^R_lm has complex coefficients c = to_complex(r), and the
+# real-basis Gaunt product is the complex-basis one on c, read back in the real
+# basis; the complex-basis product is bilinear with real coefficients, so it
+# applies to complex inputs part by part.
+
+def to_complex(L: int, r) -> np.ndarray:
+    """Complex-basis coefficients [N, (L+1)^2] of the real-basis rows r."""
+    r = _rows(r, gaunt_size(L))
+    c = np.zeros(r.shape, dtype=complex)
+    s = 1.0 / math.sqrt(2.0)
+    for l in range(L + 1):
+        o = l * l + l
+        c[:, o] = r[:, o]
+        for m in range(1, l + 1):
+            c[:, o + m] = (-1) ** m * s * (r[:, o + m] - 1j * r[:, o - m])
+            c[:, o - m] = s * (r[:, o + m] + 1j * r[:, o - m])
+    return c
+
+
+def to_real(L: int, c) -> np.ndarray:
+    """Real-basis coefficients of a real function from its complex-basis coefficients [N, (L+1)^2]."""
+    c = np.atleast_2d(np.asarray(c, dtype=complex))
+    r = np.zeros(c.shape)
+    s = math.sqrt(2.0)
+    for l in range(L + 1):
+        o = l * l + l
+        r[:, o] = c[:, o].real
+        for m in range(1, l + 1):
+            r[:, o + m] = s * c[:, o - m].real
+            r[:, o - m] = s * c[:, o - m].imag
+    return r
+
+
+def gaunt_tp_real(L: int, r1, r2, threads: int = 0) -> np.ndarray:
+    """Gaunt product of real-basis rows: degrees 0..L in, 0..2L out, all in the real basis."""
+    c1, c2 = to_complex(L, r1), to_complex(L, r2)
+    f = lambda a, b: gaunt_tp(L, a, b, threads)
+    z = (f(c1.real, c2.real) - f(c1.imag, c2.imag)) + 1j * (f(c1.real, c2.imag) + f(c1.imag, c2.real))
+    return to_real(2 * L, z)

@@ -312,3 +312,40 @@ def test_spin_two_rotation_equivariance(rng):
     z = _complex(f, L, x1, x2)
     zr = _complex(f, L, rot(x1, L), rot(x2, L))
     np.testing.assert_allclose(zr, rot(z, 2 * L), atol=1e-10)
+
+
+# ---------------------------------------------------------------- real basis
+
+def _real_sph_harm(l, m, T, P):
+    """Real harmonic with the Condon-Shortley phase, built from scipy's complex harmonic."""
+    y = _sph_harm(l, abs(m), T, P)
+    if m > 0:
+        return math.sqrt(2.0) * (-1) ** m * y.real
+    if m < 0:
+        return math.sqrt(2.0) * (-1) ** m * y.imag
+    return y.real
+
+
+def test_real_basis_round_trip(rng):
+    """to_real(to_complex(r)) = r, and the complex coefficients of a real function are Hermitian."""
+    L = 4
+    r = rng.standard_normal((3, oi.gaunt_size(L)))
+    c = oi.to_complex(L, r)
+    np.testing.assert_allclose(oi.to_real(L, c), r, atol=1e-14)
+    for l in range(L + 1):
+        for m in range(1, l + 1):
+            np.testing.assert_allclose(c[:, l * l + l - m], (-1) ** m * np.conj(c[:, l * l + l + m]), atol=1e-14)
+
+
+def test_real_gaunt_product_against_quadrature(rng):
+    """z[l3, m3] = integral of f1 f2 Y^R_{l3 m3} for f_i = sum r_i Y^R (scipy harmonics, exact grid)."""
+    L = 3
+    r1 = rng.standard_normal(oi.gaunt_size(L))
+    r2 = rng.standard_normal(oi.gaunt_size(L))
+    z = oi.gaunt_tp_real(L, r1, r2)[0]
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+    Y = {(l, m): _real_sph_harm(l, m, T, P) for l in range(2 * L + 1) for m in range(-l, l + 1)}
+    f1 = sum(r1[l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
+    f2 = sum(r2[l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
+    want = np.array([(W * f1 * f2 * Y[l, m]).sum() for l in range(2 * L + 1) for m in range(-l, l + 1)])
+    np.testing.assert_allclose(z, want, atol=1e-12)
