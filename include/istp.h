@@ -134,6 +134,27 @@ typedef struct {
 int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, const void *w1, const void *w2,
                           const void *wo, void *out, int64_t N, const istp_channels *ch, void *hip_stream);
 
+/*
+ * The Gaunt product in the real spherical-harmonic basis (spin 0 plans only):
+ * real harmonics with the Condon-Shortley phase carried over,
+ *   Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m (m > 0), Y_l^0 (m = 0),
+ *               sqrt(2) (-1)^m Im Y_l^{|m|} (m < 0),
+ * index l^2 + l + m.  x1, x2: [N, (L+1)^2] real-basis rows; out: [N, (2L+1)^2]
+ * the real-basis coefficients of the integral of f1 f2 Y^R_{l3 m3}.  The
+ * inputs are converted to the real and imaginary parts of their complex
+ * coefficients, the four products of those parts run on the plan's kernel, and
+ * the result is read back in the real basis: four products' work.
+ * workspace: caller-owned device memory of istp_real_workspace_bytes(plan, N)
+ * bytes or more, 256-byte aligned, not overlapping the other buffers (its
+ * contents are scratch).  CGTP_EUNSUP for spin 1 or 2 plans; otherwise as
+ * istp_forward.
+ */
+int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
+                      int64_t workspace_bytes, void *hip_stream);
+
+/* Workspace bytes istp_forward_real needs for N pairs; -1 for spin 1 or 2 plans or N < 0. */
+int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
+
 /* Irrep labels in a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1); -1 if invalid. */
 int64_t istp_num_labels(int32_t L, int32_t spin);
 

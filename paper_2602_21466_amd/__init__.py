@@ -87,6 +87,8 @@ def _load():
         "istp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
         "istp_forward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, i64, ctypes.POINTER(cgtp_channels), vp]),
         "istp_num_labels": (i64, [i32, i32]),
+        "istp_forward_real": (ctypes.c_int, [vp, vp, vp, vp, i64, vp, i64, vp]),
+        "istp_real_workspace_bytes": (i64, [vp, i64]),
         "istp_label_index": (i64, [i32, i32, i32]),
         "istp_destroy": (ctypes.c_int, [vp]),
         "istp_num_inputs": (i64, [i32, i32]),
@@ -110,7 +112,8 @@ def exported_symbols():
     return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
-            "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
+            "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index",
+            "istp_forward_real", "istp_real_workspace_bytes", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
             "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
 
@@ -251,6 +254,18 @@ def istp_num_outputs(L: int, spin: int) -> int:
 
 def istp_label_offset(spin: int, j: int, l: int) -> int:
     return int(_load().istp_label_offset(int(spin), int(j), int(l)))
+
+
+def istp_forward_real(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, ws_ptr: int, ws_bytes: int,
+                      stream_ptr: int | None = None) -> None:
+    rc = _load().istp_forward_real(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(out_ptr),
+                                   int(N), ctypes.c_void_p(ws_ptr) if ws_ptr else None, int(ws_bytes),
+                                   ctypes.c_void_p(stream_ptr) if stream_ptr else None)
+    _check(rc, "istp_forward_real")
+
+
+def istp_real_workspace_bytes(plan, N: int) -> int:
+    return int(_load().istp_real_workspace_bytes(plan, int(N)))
 
 
 def istp_num_labels(L: int, spin: int) -> int:
@@ -437,6 +452,32 @@ class IstpPlan:
         ptr = lambda w: w.data_ptr() if w is not None else None
         istp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), ptr(w1), ptr(w2), ptr(wo), out.data_ptr(), N,
                               C, x2.dim() == 2, per_pair, s.cuda_stream)
+        return out
+
+    def forward_real(self, x1, x2, out=None, workspace=None, stream=None):
+        """Gaunt product in the real spherical-harmonic basis (spin 0 plans): x1, x2 [N, (L+1)^2] real-basis rows;
+        returns [N, (2L+1)^2].  The workspace (a uint8 CUDA tensor of istp_real_workspace_bytes bytes) is
+        allocated here when not given."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        for t in (x1, x2):
+            if not t.is_cuda or t.dtype != tdt or t.dim() != 2 or t.shape[1] != self.nin or not t.is_contiguous():
+                raise ValueError("inputs must be contiguous %s CUDA tensors [N, %d]" % (tdt, self.nin))
+        if x1.shape[0] != x2.shape[0]:
+            raise ValueError("x1 and x2 must hold the same number of pairs")
+        N = x1.shape[0]
+        need = istp_real_workspace_bytes(self._h, N)
+        if need < 0:
+            raise CgtpError(CGTP_EUNSUP, "forward_real (spin %d)" % self.spin)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        if out is None:
+            out = torch.empty((N, self.nout), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, self.nout):
+            raise ValueError("out must be a contiguous %s tensor [N, %d]" % (tdt, self.nout))
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        istp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, workspace.data_ptr(),
+                          workspace.numel(), s.cuda_stream)
         return out
 
     def backward_query(self) -> dict:

@@ -685,6 +685,80 @@ int istp_forward_weighted(istp_plan_t plan, const void* x1, const void* x2, cons
     return CGTP_OK;
 }
 
+// Real-basis Gaunt product: workspace of four converted inputs and three
+// products (the fourth product lands in out), each 256-byte aligned.
+static size_t real_part_bytes(size_t n) { return (n + 255) / 256 * 256; }
+
+int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
+    if (!plan || N < 0 || plan->spin != ISTP_GAUNT) return -1;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(nout * esz))) return -1;
+    return (int64_t)(4 * real_part_bytes((size_t)N * nin * esz) + 3 * real_part_bytes((size_t)N * nout * esz));
+}
+
+int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* workspace,
+                      int64_t workspace_bytes, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (plan->spin != ISTP_GAUNT) return CGTP_EUNSUP;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out || !workspace) return CGTP_EINVAL;
+    if ((((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) || ((uintptr_t)workspace & 255)) return CGTP_EINVAL;
+    const int64_t need = istp_real_workspace_bytes(plan, N);
+    if (need < 0 || workspace_bytes < need) return CGTP_EINVAL;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin) || overlaps(out, bout, workspace, need) ||
+        overlaps(workspace, need, x1, bin) || overlaps(workspace, need, x2, bin))
+        return CGTP_EINVAL;
+    int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    char* w = (char*)workspace;
+    const size_t pin = real_part_bytes(bin), pout = real_part_bytes(bout);
+    void* re1 = w;
+    void* im1 = w + pin;
+    void* re2 = w + 2 * pin;
+    void* im2 = w + 3 * pin;
+    void* pbb = w + 4 * pin;
+    void* pab = w + 4 * pin + pout;
+    void* pba = w + 4 * pin + 2 * pout;
+    const int Lo = 2 * plan->L;
+    int err;
+    if (plan->dtype == CGTP_FP32) {
+        err = istp::launch_real_to_complex_f32((const float*)x1, (float*)re1, (float*)im1, N, (int)nin, hip_stream);
+        if (!err)
+            err = istp::launch_real_to_complex_f32((const float*)x2, (float*)re2, (float*)im2, N, (int)nin,
+                                                   hip_stream);
+    } else {
+        err = istp::launch_real_to_complex_f64((const double*)x1, (double*)re1, (double*)im1, N, (int)nin,
+                                               hip_stream);
+        if (!err)
+            err = istp::launch_real_to_complex_f64((const double*)x2, (double*)re2, (double*)im2, N, (int)nin,
+                                                   hip_stream);
+    }
+    if (err) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    // P(a1, a2) into out, then P(b1, b2), P(a1, b2), P(b1, a2)
+    rc = launch_prod(plan, plan->fwd, 0, re1, re2, out, N, hip_stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, im1, im2, pbb, N, hip_stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, re1, im2, pab, N, hip_stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, im1, re2, pba, N, hip_stream);
+    if (rc != CGTP_OK) return rc;
+    err = plan->dtype == CGTP_FP32
+              ? istp::launch_real_from_complex_f32((float*)out, (const float*)pbb, (const float*)pab,
+                                                   (const float*)pba, N, Lo, hip_stream)
+              : istp::launch_real_from_complex_f64((double*)out, (const double*)pbb, (const double*)pab,
+                                                   (const double*)pba, N, Lo, hip_stream);
+    if (err) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
+
 int istp_backward(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
                   void* grad_x2, int64_t N, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;

@@ -253,3 +253,51 @@ def test_spin_two_has_no_gradients():
     assert e.value.code == lib.CGTP_EUNSUP
     torch.cuda.synchronize()
 
+
+
+# ---------------------------------------------------------------- real basis
+
+REAL_CASES = [(0, 5, "fp32"), (1, 7, "fp32"), (2, 9, "fp64"), (3, 11, "fp32"), (5, 6, "fp64"), (8, 13, "fp32"),
+              (16, 3, "fp32")]
+
+
+@pytest.mark.parametrize("L,N,dtype", REAL_CASES)
+def test_real_basis_gaunt(L, N, dtype):
+    """istp_forward_real against the real-basis oracle on every pair (ragged N)."""
+    torch = _torch()
+    x1, x2 = wl.draw_rows((L + 1) ** 2, N, dtype, seed=700 + L)
+    plan = _lib().IstpPlan(L, 0, dtype)
+    got = plan.forward_real(x1.cuda(), x2.cuda())
+    torch.cuda.synchronize()
+    ref = oi.gaunt_tp_real(L, x1.double().numpy(), x2.double().numpy())
+    err, lab = per_label_rel_err(2 * L, 0, got.cpu().double().numpy(), ref)
+    print("real basis L=%d N=%d %s worst label %s rel err %.3e" % (L, N, dtype, lab, err), flush=True)
+    assert err <= TOL[dtype], (lab, err)
+    plan.close()
+
+
+def test_real_basis_errors():
+    torch = _torch()
+    lib = _lib()
+    plan = lib.IstpPlan(3, 0, "fp32")
+    N = 4
+    need = lib.istp_real_workspace_bytes(plan._h, N)
+    assert need > 0 and lib.istp_real_workspace_bytes(plan._h, -1) == -1
+    x = torch.zeros((N, plan.nin), device="cuda")
+    out = torch.zeros((N, plan.nout), device="cuda")
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), 0, ws.data_ptr(), need, None)
+    with pytest.raises(lib.CgtpError) as e:   # workspace too small
+        lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, ws.data_ptr(), need - 1, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    with pytest.raises(lib.CgtpError) as e:   # workspace overlapping the output
+        lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), ws.data_ptr(), N, ws.data_ptr(), need, None)
+    assert e.value.code == lib.CGTP_EINVAL
+    vplan = lib.IstpPlan(3, 1, "fp32")
+    assert lib.istp_real_workspace_bytes(vplan._h, N) == -1
+    with pytest.raises(lib.CgtpError) as e:
+        lib.istp_forward_real(vplan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, ws.data_ptr(), need, None)
+    assert e.value.code == lib.CGTP_EUNSUP
+    torch.cuda.synchronize()
+    plan.close()
+    vplan.close()
