@@ -34,21 +34,24 @@ PEAK_HBM_GBS = 8000.0
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
     "11760e4f080b1fea": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 432209.5, "fetch_scale": 1.999956, "write_kib": 4871641.2, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 206265.0, "fetch_scale": 1.999956, "write_kib": 2739751.3, "write_scale": 1.000000},
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 386835.5, "fetch_scale": 1.999956, "write_kib": 4872244.3, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 206013.3, "fetch_scale": 1.999956, "write_kib": 2739792.7, "write_scale": 1.000000},
     },
     "98b2595f487717ca": {
-        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118418.4, "fetch_scale": 1.999956, "write_kib": 2739754.7, "write_scale": 1.000000},
+        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118357.7, "fetch_scale": 1.999956, "write_kib": 2739763.4, "write_scale": 1.000000},
     },
-    "4829bf158776de88": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 295863.6, "fetch_scale": 1.999956, "write_kib": 811653.6, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 404629.5, "fetch_scale": 1.999956, "write_kib": 1084122.8, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 227654.3, "fetch_scale": 1.999956, "write_kib": 837122.4, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068388.4, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
-        "tstp_L16_N16384_fp32": {"fetch_kib": 97021.5, "fetch_scale": 1.999956, "write_kib": 348928.0, "write_scale": 1.000000},
+    "e6e64571649e3caf": {
+        "vstp_L32_N16384_fp32": {"fetch_kib": 299232.3, "fetch_scale": 1.999956, "write_kib": 811653.6, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 404466.9, "fetch_scale": 1.999956, "write_kib": 1084134.4, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227649.3, "fetch_scale": 1.999956, "write_kib": 837123.1, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068381.1, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
+        "tstp_L16_N16384_fp32": {"fetch_kib": 97022.1, "fetch_scale": 1.999956, "write_kib": 348928.0, "write_scale": 1.000000},
     },
-    "667ed8390a21448f": {
-        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170364.4, "fetch_scale": 1.999956, "write_kib": 837125.8, "write_scale": 1.000000},
+    "6e3a7b722582dad7": {
+        "gtp_real_L16_N65536_fp32": {"fetch_kib": 304040.8, "fetch_scale": 1.999956, "write_kib": 1115136.0, "write_scale": 1.000000},
+    },
+    "57c9abda6385f69e": {
+        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170361.6, "fetch_scale": 1.999956, "write_kib": 837127.5, "write_scale": 1.000000},
     },
 }
 
@@ -58,6 +61,8 @@ DIGEST_SOURCES = {
     "istp": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
+    "istp_real": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_real.hip", "istp_plan.cpp", "istp_internal.h",
+                  "device_common.h"),
     "istp_channels": ("istp_kernels.hip", "istp_kernels_channels.hip", "istp_kernels_channels_tensor.hip",
                       "istp_plan.cpp", "istp_internal.h", "device_common.h"),
 }
@@ -181,6 +186,33 @@ def time_channels(w, steps, warmup):
     del out, a, b, wc
     torch.cuda.empty_cache()
     return res
+
+
+def time_istp_real(w, steps, warmup):
+    """Gaunt product in the real basis: two conversions and four products per step."""
+    import torch
+
+    import paper_2602_21466_amd as lib
+
+    x1, x2 = draw_rows_for(w, 400)
+    plan = lib.IstpPlan(w.L, 0, w.dtype)
+    a, b = x1.cuda(), x2.cuda()
+    out = torch.empty((w.N, plan.nout), dtype=a.dtype, device="cuda")
+    ws = torch.empty(lib.istp_real_workspace_bytes(plan._h, w.N), dtype=torch.uint8, device="cuda")
+    q = dict(plan.query())
+    # the method's work: four products; compulsory bytes: the inputs and the output once
+    q["flops_per_pair"] = 4 * q["flops_per_pair"]
+    res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": q, "kind": "istp_real"}
+    res.update(_time_launches(lambda st: plan.forward_real(a, b, out, ws, st), w.N, steps, warmup))
+    plan.close()
+    del out, a, b, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def draw_rows_for(w, seed_offset):
+    import cgtp_inputs
+    return cgtp_inputs.draw_rows(w.n_coeffs, w.N, w.dtype, w.L + seed_offset)
 
 
 def time_istp_channels(w, steps, warmup):
@@ -331,6 +363,8 @@ def main():
                     help="comma-separated channel-wise (path-weighted) CGTP workloads, or 'none'")
     ap.add_argument("--istp-channels", default=",".join(x.name for x in cgtp_inputs.ISTP_CHANNEL_WORKLOADS),
                     help="comma-separated channel-wise (label-weighted) signal-product workloads, or 'none'")
+    ap.add_argument("--istp-real", default=",".join(x.name for x in cgtp_inputs.REAL_WORKLOADS),
+                    help="comma-separated real-basis Gaunt workloads, or 'none'")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--istp-cpu-seconds", type=float, default=4.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -392,6 +426,15 @@ def main():
                 entry["backward"] = {"value": round(rb["value"], 1), "unit": "pairs/s",
                                      "ms_per_step": round(rb["ms_per_step"], 4), "roofline": roofline(rb)}
             istp.append(entry)
+    if args.istp_real and args.istp_real != "none":
+        by_re = {x.name: x for x in cgtp_inputs.REAL_WORKLOADS}
+        for name in args.istp_real.split(","):
+            wr = by_re[name]
+            log("timing %s" % wr.name)
+            rr = time_istp_real(wr, args.steps, args.warmup)
+            log("  %.4f ms/step, %.4g pairs/s" % (rr["ms_per_step"], rr["value"]))
+            istp.append({"workload": wr.name, "value": round(rr["value"], 1), "unit": "pairs/s",
+                         "basis": "real", "ms_per_step": round(rr["ms_per_step"], 4), "roofline": roofline(rr)})
     if args.istp_channels and args.istp_channels != "none":
         by_ic = {x.name: x for x in cgtp_inputs.ISTP_CHANNEL_WORKLOADS}
         for name in args.istp_channels.split(","):

@@ -258,3 +258,10 @@ ISTP_CHANNEL_WORKLOADS = [
     IstpChannelWorkload("vstp_L16_N4096_C16_fp32_x2shared_weighted", 16, 1, 4096, 16, True, "channel", "fp32", 16),
 ]
 
+
+# The Gaunt product in the real spherical-harmonic basis: rows drawn as for
+# the signal products (seed L + 400), real-basis coefficients.
+REAL_WORKLOADS = [
+    IstpWorkload("gtp_real_L16_N65536_fp32", 16, 0, 65_536, "fp32", 8),
+]
+
