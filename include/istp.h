@@ -31,8 +31,9 @@
  *               5 l^2 + j^2 - (l-2)^2 (5 (L+1)^2 values).  The output holds the
  *               2 (x) 2 -> 2 coupled pointwise product
  *               g_q = sum C^{2 q}_{2 q1 2 q2} f1_q1 f2_q2 in the same basis up
- *               to l = 2L (5 (2L+1)^2 values).  Forward only: istp_backward
- *               returns CGTP_EUNSUP for these plans.
+ *               to l = 2L (5 (2L+1)^2 values).  The coupling is symmetric;
+ *               gradients (istp_backward) exist up to L = 11 (fp32) and
+ *               L = 9 (fp64).
  *
  * Basis: complex spherical harmonics with the Condon-Shortley phase; inputs
  * and outputs are real.  By Theorem 4.2 each output label (j3, l3) of the

@@ -238,12 +238,12 @@ def spin_tp(s: int, L: int, x1, x2, threads: int = 0, L2: int | None = None, Lo:
 
 
 def product_vjp(spin: int, L: int, x1, x2, g, threads: int = 0):
-    """Gradients of sum(g * z(x1, x2)) w.r.t. x1 and x2 for the spin-0 or spin-1 product above, by the
+    """Gradients of sum(g * z(x1, x2)) w.r.t. x1 and x2 for the spin-0, 1 or 2 product above, by the
     plain definition: z is bilinear, so d/dx1[b] = sum_a g_a z_a(e_b, x2) and d/dx2[b] = sum_a g_a z_a(x1, e_b),
     with z evaluated by ``gaunt_tp`` / ``vector_tp`` on unit rows (one pair at a time).
     x1, x2: [N, n_in]; g: [N, n_out]; returns (grad_x1, grad_x2), each [N, n_in]."""
-    fn = gaunt_tp if spin == 0 else vector_tp
-    size = gaunt_size if spin == 0 else vector_size
+    fn = gaunt_tp if spin == 0 else (vector_tp if spin == 1 else (lambda *a_, **k_: spin_tp(spin, *a_, **k_)))
+    size = lambda Lx: spin_size(spin, Lx)
     a = _rows(x1, size(L))
     b = _rows(x2, size(L))
     gg = _rows(g, size(2 * L))

@@ -76,9 +76,16 @@ template <> __device__ __forceinline__ int lift_ring<double>(int q, int h) { ret
 // value src of the row, for the label (j, l) and order m that c holds.
 template <int S>
 __device__ __forceinline__ void reverse_index(int c, int* src, bool* neg) {
-    if constexpr (S == 2) {   // spin 2 has no gradient product: never staged reversed
-        *src = c;
-        *neg = false;
+    if constexpr (S == 2) {   // label (j, l), j = |l - 2| .. l + 2, starts at 5 l^2 + j^2 - (l - 2)^2
+        int l = (int)sqrtf((float)c / 5.0f);
+        while (5 * (l + 1) * (l + 1) <= c) ++l;
+        while (5 * l * l > c) --l;
+        const int r = c - 5 * l * l, jmin = l >= 2 ? l - 2 : 2 - l;
+        int j = jmin;
+        while (j < l + 2 && (j + 1) * (j + 1) - jmin * jmin <= r) ++j;
+        const int lo = j * j - jmin * jmin, m = r - lo - j;
+        *src = 5 * l * l + lo + j - m;
+        *neg = (m + j - l) & 1;
         return;
     }
     if (S == 0) {   // c = l^2 + l + m

@@ -554,9 +554,8 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
     }
     rc = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, 0, &p->fwd, true)
                             : make_prod<double>(L, L, 2 * L, spin, 0, &p->fwd, true);
-    if (rc == CGTP_OK && spin != ISTP_TENSOR) {
+    if (rc == CGTP_OK) {
         // the gradients' product; outside the kernel's limits it stays unbuilt
-        // (and for spin 2, which has no gradient product)
         const int rb = dtype == CGTP_FP32
                            ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true)
                            : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true);
@@ -584,8 +583,7 @@ int istp_plan_describe(int32_t L, int32_t spin, int32_t dtype, int32_t* desc_out
     static_assert(sizeof(istp::IstpDesc) == 24 * sizeof(int32_t), "descriptor layout");
     std::memcpy(desc_out, &pr.desc, sizeof(istp::IstpDesc));
     // the gradients' product follows when it is within the kernel's limits
-    rc = spin == ISTP_TENSOR ? CGTP_EUNSUP
-         : dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false)
+    rc = dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false)
                             : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &pb, false);
     if (rc == CGTP_OK) std::memcpy(desc_out + 24, &pb.desc, sizeof(istp::IstpDesc));
     else std::memset(desc_out + 24, 0, sizeof(istp::IstpDesc));

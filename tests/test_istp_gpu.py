@@ -161,7 +161,9 @@ def test_largest_sizes():
 # ---------------------------------------------------------------- gradients
 
 BACKWARD_CASES = [(1, 0, 5, "fp64"), (2, 1, 7, "fp64"), (3, 0, 9, "fp32"), (4, 1, 6, "fp32"), (6, 1, 5, "fp64"),
-                  (8, 0, 4, "fp32"), (5, 0, 3, "fp64"), (7, 1, 3, "fp32")]
+                  (8, 0, 4, "fp32"), (5, 0, 3, "fp64"), (7, 1, 3, "fp32"),
+                  # spin 2: symmetric coupling, the same time reversal
+                  (1, 2, 5, "fp32"), (2, 2, 4, "fp64"), (4, 2, 3, "fp32"), (6, 2, 2, "fp32")]
 
 
 def run_backward(L, spin, x1, x2, g, dtype):
@@ -187,7 +189,7 @@ def test_backward_small(L, spin, N, dtype):
     assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (l1, e1, l2, e2)
 
 
-@pytest.mark.parametrize("L,spin", [(18, 1), (31, 0), (16, 1)])
+@pytest.mark.parametrize("L,spin", [(18, 1), (31, 0), (16, 1), (11, 2)])
 def test_backward_largest(L, spin):
     """The largest fp32 gradient products: <g, z(x1, x2)> = <grad_x1, x1> = <grad_x2, x2> with the GPU forward,
     and (where the oracle's degree range allows) the time-reversed product of the oracle on one pair."""
@@ -206,7 +208,7 @@ def test_backward_largest(L, spin):
     assert np.all(np.abs((g1 * x1.double().numpy()).sum(1) - want) <= 1e-5 * scale)
     assert np.all(np.abs((g2 * x2.double().numpy()).sum(1) - want) <= 1e-5 * scale)
     if 2 * L <= 36:
-        fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+        fn = {0: oi.gaunt_tp, 1: oi.vector_tp}.get(spin, lambda *a, **k: oi.spin_tp(spin, *a, **k))
         from test_istp_oracle import _reverse
         ref1 = fn(2 * L, g[:1].double().numpy(), _reverse(spin, L, x2[:1].double().numpy()), L2=L, Lo=L)
         e1, lab = per_label_rel_err(L, spin, g1[:1], ref1)
@@ -240,11 +242,13 @@ def test_backward_errors():
     torch.cuda.synchronize()
 
 
-def test_spin_two_has_no_gradients():
-    """Spin-2 plans are forward only: istp_backward reports CGTP_EUNSUP and launches nothing."""
+def test_spin_two_gradient_limit():
+    """Spin-2 gradient products exist up to L = 11 (fp32); beyond, istp_backward reports CGTP_EUNSUP and
+    launches nothing."""
     torch = _torch()
     lib = _lib()
-    plan = lib.IstpPlan(3, 2, "fp32")
+    assert lib.IstpPlan(11, 2, "fp32").backward_query()["flops_per_pair"] > 0
+    plan = lib.IstpPlan(12, 2, "fp32")
     x = torch.zeros((2, plan.nin), device="cuda")
     g = torch.zeros((2, plan.nout), device="cuda")
     gx = torch.zeros((2, plan.nin), device="cuda")

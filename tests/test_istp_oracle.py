@@ -184,8 +184,8 @@ def test_vector_selection_rule():
 def _reverse(spin, L, x):
     """x~[(j,l), m] = (-1)^(m + j - l + spin) x[(j,l), -m] (time reversal of the coefficients)."""
     y = np.zeros_like(x)
-    labels = [(l, l) for l in range(L + 1)] if spin == 0 else oi.vector_labels(L)
-    off = (lambda j, l: l * l) if spin == 0 else oi.vector_offset
+    labels = [(l, l) for l in range(L + 1)] if spin == 0 else oi.spin_labels(spin, L)
+    off = (lambda j, l: l * l) if spin == 0 else (lambda j, l: oi.spin_offset(spin, j, l))
     for j, l in labels:
         o = off(j, l)
         for m in range(-j, j + 1):
@@ -193,28 +193,33 @@ def _reverse(spin, L, x):
     return y
 
 
-@pytest.mark.parametrize("spin", [0, 1])
+def _fn(spin):
+    return {0: oi.gaunt_tp, 1: oi.vector_tp}.get(spin, lambda *a, **k: oi.spin_tp(spin, *a, **k))
+
+
+@pytest.mark.parametrize("spin", [0, 1, 2])
 def test_vjp_against_time_reversed_product(spin, rng):
     """The gradients equal +-P(g, reversed other input): a degree-2L by degree-L product projected on degrees <= L,
-    the adjoint of the integral of three harmonics (the vector product changes sign under the swap of its inputs)."""
+    the adjoint of the integral of three harmonics (the vector product changes sign under the swap of its inputs;
+    the spin-0 and spin-2 couplings are symmetric)."""
     L = 2
-    size = oi.gaunt_size if spin == 0 else oi.vector_size
-    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+    size = lambda Lx: oi.spin_size(spin, Lx)
+    fn = _fn(spin)
     x1 = rng.standard_normal((2, size(L)))
     x2 = rng.standard_normal((2, size(L)))
     g = rng.standard_normal((2, size(2 * L)))
     g1, g2 = oi.product_vjp(spin, L, x1, x2, g)
     np.testing.assert_allclose(g1, fn(2 * L, g, _reverse(spin, L, x2), L2=L, Lo=L), atol=1e-12)
-    sign = 1.0 if spin == 0 else -1.0
+    sign = -1.0 if spin == 1 else 1.0
     np.testing.assert_allclose(g2, sign * fn(2 * L, g, _reverse(spin, L, x1), L2=L, Lo=L), atol=1e-12)
 
 
-@pytest.mark.parametrize("spin", [0, 1])
+@pytest.mark.parametrize("spin", [0, 1, 2])
 def test_vjp_euler_identity(spin, rng):
     """Bilinearity: <g, z(x1, x2)> = <grad_x1, x1> = <grad_x2, x2>."""
-    L = 3
-    size = oi.gaunt_size if spin == 0 else oi.vector_size
-    fn = oi.gaunt_tp if spin == 0 else oi.vector_tp
+    L = 3 if spin < 2 else 2
+    size = lambda Lx: oi.spin_size(spin, Lx)
+    fn = _fn(spin)
     x1 = rng.standard_normal((3, size(L)))
     x2 = rng.standard_normal((3, size(L)))
     g = rng.standard_normal((3, size(2 * L)))
