@@ -156,6 +156,23 @@ int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *ou
 /* Workspace bytes istp_forward_real needs for N pairs; -1 for spin 1 or 2 plans or N < 0. */
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
 
+/*
+ * Gradients of sum(grad_out * out) for istp_forward_real, in the real basis.
+ * The integrals of three real harmonics are fully symmetric, so
+ *   grad_x1 = Q(grad_out, x2),  grad_x2 = Q(grad_out, x1),
+ * with Q the real-basis product of a degree-2L and a degree-L row projected on
+ * degrees <= L (four products on the plan's gradient grid; no time reversal).
+ * Layouts and rules as istp_backward; workspace: caller-owned, 256-byte
+ * aligned, istp_real_backward_workspace_bytes(plan, N) bytes or more, reused
+ * by the two gradients.  CGTP_EUNSUP for spin 1 or 2 plans and where the
+ * plan has no gradient product.
+ */
+int istp_backward_real(istp_plan_t plan, const void *x1, const void *x2, const void *grad_out, void *grad_x1,
+                       void *grad_x2, int64_t N, void *workspace, int64_t workspace_bytes, void *hip_stream);
+
+/* Workspace bytes istp_backward_real needs for N pairs; -1 where it does not apply. */
+int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N);
+
 /* Irrep labels in a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1); -1 if invalid. */
 int64_t istp_num_labels(int32_t L, int32_t spin);
 

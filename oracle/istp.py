@@ -364,3 +364,18 @@ def gaunt_tp_real(L: int, r1, r2, threads: int = 0) -> np.ndarray:
     f = lambda a, b: gaunt_tp(L, a, b, threads)
     z = (f(c1.real, c2.real) - f(c1.imag, c2.imag)) + 1j * (f(c1.real, c2.imag) + f(c1.imag, c2.real))
     return to_real(2 * L, z)
+
+
+def gaunt_tp_real_vjp(L: int, r1, r2, g, threads: int = 0):
+    """Gradients of sum(g * gaunt_tp_real(r1, r2)) w.r.t. r1 and r2, by the plain definition of a bilinear
+    map's derivatives (``gaunt_tp_real`` on unit rows, one pair at a time)."""
+    a = _rows(r1, gaunt_size(L))
+    b = _rows(r2, gaunt_size(L))
+    gg = _rows(g, gaunt_size(2 * L))
+    eye = np.eye(gaunt_size(L))
+    g1 = np.zeros_like(a)
+    g2 = np.zeros_like(b)
+    for n in range(a.shape[0]):
+        g1[n] = gaunt_tp_real(L, eye, np.repeat(b[n:n + 1], gaunt_size(L), 0), threads) @ gg[n]
+        g2[n] = gaunt_tp_real(L, np.repeat(a[n:n + 1], gaunt_size(L), 0), eye, threads) @ gg[n]
+    return g1, g2

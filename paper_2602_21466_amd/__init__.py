@@ -89,6 +89,8 @@ def _load():
         "istp_num_labels": (i64, [i32, i32]),
         "istp_forward_real": (ctypes.c_int, [vp, vp, vp, vp, i64, vp, i64, vp]),
         "istp_real_workspace_bytes": (i64, [vp, i64]),
+        "istp_backward_real": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
+        "istp_real_backward_workspace_bytes": (i64, [vp, i64]),
         "istp_label_index": (i64, [i32, i32, i32]),
         "istp_destroy": (ctypes.c_int, [vp]),
         "istp_num_inputs": (i64, [i32, i32]),
@@ -113,7 +115,8 @@ def exported_symbols():
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index",
-            "istp_forward_real", "istp_real_workspace_bytes", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
+            "istp_forward_real", "istp_real_workspace_bytes", "istp_backward_real",
+            "istp_real_backward_workspace_bytes", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
             "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
 
@@ -266,6 +269,18 @@ def istp_forward_real(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, ws_p
 
 def istp_real_workspace_bytes(plan, N: int) -> int:
     return int(_load().istp_real_workspace_bytes(plan, int(N)))
+
+
+def istp_backward_real(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int | None, gx2_ptr: int | None,
+                       N: int, ws_ptr: int, ws_bytes: int, stream_ptr: int | None = None) -> None:
+    vpn = lambda p: ctypes.c_void_p(p) if p else None
+    rc = _load().istp_backward_real(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(g_ptr),
+                                    vpn(gx1_ptr), vpn(gx2_ptr), int(N), vpn(ws_ptr), int(ws_bytes), vpn(stream_ptr))
+    _check(rc, "istp_backward_real")
+
+
+def istp_real_backward_workspace_bytes(plan, N: int) -> int:
+    return int(_load().istp_real_backward_workspace_bytes(plan, int(N)))
 
 
 def istp_num_labels(L: int, spin: int) -> int:
@@ -479,6 +494,21 @@ class IstpPlan:
         istp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, workspace.data_ptr(),
                           workspace.numel(), s.cuda_stream)
         return out
+
+    def backward_real(self, x1, x2, grad_out, workspace=None, stream=None):
+        """Gradients of sum(grad_out * forward_real(x1, x2)) w.r.t. x1 and x2 (real basis, spin 0 plans)."""
+        import torch
+        N = x1.shape[0]
+        need = istp_real_backward_workspace_bytes(self._h, N)
+        if need < 0:
+            raise CgtpError(CGTP_EUNSUP, "backward_real (spin %d, L %d)" % (self.spin, self.L))
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        g1, g2 = torch.empty_like(x1), torch.empty_like(x2)
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        istp_backward_real(self._h, x1.data_ptr(), x2.data_ptr(), grad_out.contiguous().data_ptr(), g1.data_ptr(),
+                           g2.data_ptr(), N, workspace.data_ptr(), workspace.numel(), s.cuda_stream)
+        return g1, g2
 
     def backward_query(self) -> dict:
         return istp_backward_query(self._h)

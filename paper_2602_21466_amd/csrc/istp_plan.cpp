@@ -757,6 +757,95 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
     return CGTP_OK;
 }
 
+// Gradients in the real basis: the real Gaunt coefficients (integrals of three
+// real harmonics) are fully symmetric, so grad_x1 = Q(g, x2) and grad_x2 =
+// Q(g, x1) with Q the real-basis product of a degree-2L and a degree-L row
+// projected on degrees <= L (the gradient product's grid, no time reversal).
+// Workspace per gradient launch: the converted upstream gradient (two rows of
+// (2L+1)^2), the converted input (two rows of (L+1)^2), three products.
+int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N) {
+    if (!plan || N < 0 || plan->spin != ISTP_GAUNT || !plan->bwd.ok) return -1;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t ng = (size_t)plan->fwd.desc.nout, nin = (size_t)plan->fwd.desc.nin;
+    if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(ng * esz))) return -1;
+    return (int64_t)(2 * real_part_bytes((size_t)N * ng * esz) + 2 * real_part_bytes((size_t)N * nin * esz) +
+                     3 * real_part_bytes((size_t)N * nin * esz));
+}
+
+static int real_bwd_one(istp_plan_t plan, const void* g, const void* x, void* grad, int64_t N, char* w,
+                        void* stream) {
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t ng = (size_t)plan->fwd.desc.nout, nin = (size_t)plan->fwd.desc.nin;
+    const size_t pg = real_part_bytes((size_t)N * ng * esz), px = real_part_bytes((size_t)N * nin * esz);
+    void* ga = w;
+    void* gb = w + pg;
+    void* xa = w + 2 * pg;
+    void* xb = w + 2 * pg + px;
+    void* pbb = w + 2 * pg + 2 * px;
+    void* pab = w + 2 * pg + 3 * px;
+    void* pba = w + 2 * pg + 4 * px;
+    int err = plan->dtype == CGTP_FP32
+                  ? istp::launch_real_to_complex_f32((const float*)g, (float*)ga, (float*)gb, N, (int)ng, stream)
+                  : istp::launch_real_to_complex_f64((const double*)g, (double*)ga, (double*)gb, N, (int)ng, stream);
+    if (!err)
+        err = plan->dtype == CGTP_FP32
+                  ? istp::launch_real_to_complex_f32((const float*)x, (float*)xa, (float*)xb, N, (int)nin, stream)
+                  : istp::launch_real_to_complex_f64((const double*)x, (double*)xa, (double*)xb, N, (int)nin,
+                                                     stream);
+    if (err) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    int rc = launch_prod(plan, plan->bwd, 0, ga, xa, grad, N, stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, gb, xb, pbb, N, stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, ga, xb, pab, N, stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, gb, xa, pba, N, stream);
+    if (rc != CGTP_OK) return rc;
+    err = plan->dtype == CGTP_FP32
+              ? istp::launch_real_from_complex_f32((float*)grad, (const float*)pbb, (const float*)pab,
+                                                   (const float*)pba, N, plan->L, stream)
+              : istp::launch_real_from_complex_f64((double*)grad, (const double*)pbb, (const double*)pab,
+                                                   (const double*)pba, N, plan->L, stream);
+    if (err) {
+        cgtp::set_last_hip_error(err);
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
+
+int istp_backward_real(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
+                       void* grad_x2, int64_t N, void* workspace, int64_t workspace_bytes, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (plan->spin != ISTP_GAUNT || !plan->bwd.ok) return CGTP_EUNSUP;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2) || !workspace) return CGTP_EINVAL;
+    if ((((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)grad_out | (uintptr_t)grad_x1 | (uintptr_t)grad_x2) & 15) ||
+        ((uintptr_t)workspace & 255))
+        return CGTP_EINVAL;
+    const int64_t need = istp_real_backward_workspace_bytes(plan, N);
+    if (need < 0 || workspace_bytes < need) return CGTP_EINVAL;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    const void* reads[4] = {x1, x2, grad_out, workspace};
+    const size_t rlen[4] = {bin, bin, bout, (size_t)need};
+    void* writes[2] = {grad_x1, grad_x2};
+    for (void* w : writes) {
+        if (!w) continue;
+        for (int i = 0; i < 4; ++i)
+            if (overlaps(w, bin, reads[i], rlen[i])) return CGTP_EINVAL;
+    }
+    if (overlaps(workspace, need, x1, bin) || overlaps(workspace, need, x2, bin) ||
+        overlaps(workspace, need, grad_out, bout))
+        return CGTP_EINVAL;
+    if (grad_x1 && grad_x2 && overlaps(grad_x1, bin, grad_x2, bin)) return CGTP_EINVAL;
+    int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    if (grad_x1) rc = real_bwd_one(plan, grad_out, x2, grad_x1, N, (char*)workspace, hip_stream);
+    if (rc == CGTP_OK && grad_x2) rc = real_bwd_one(plan, grad_out, x1, grad_x2, N, (char*)workspace, hip_stream);
+    return rc;
+}
+
 int istp_backward(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
                   void* grad_x2, int64_t N, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;

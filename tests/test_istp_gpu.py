@@ -305,3 +305,24 @@ def test_real_basis_errors():
     torch.cuda.synchronize()
     plan.close()
     vplan.close()
+
+
+@pytest.mark.parametrize("L,N,dtype", [(1, 5, "fp32"), (3, 7, "fp64"), (6, 4, "fp32"), (10, 3, "fp32")])
+def test_real_basis_gradients(L, N, dtype):
+    """istp_backward_real against the oracle's derivative of the real-basis product, every pair."""
+    torch = _torch()
+    x1, x2 = wl.draw_rows((L + 1) ** 2, N, dtype, seed=800 + L)
+    g, _ = wl.draw_rows((2 * L + 1) ** 2, N, dtype, seed=900 + L)
+    plan = _lib().IstpPlan(L, 0, dtype)
+    g1, g2 = plan.backward_real(x1.cuda(), x2.cuda(), g.cuda())
+    torch.cuda.synchronize()
+    r1, r2 = oi.gaunt_tp_real_vjp(L, x1.double().numpy(), x2.double().numpy(), g.double().numpy())
+    e1, l1 = per_label_rel_err(L, 0, g1.cpu().double().numpy(), r1)
+    e2, l2 = per_label_rel_err(L, 0, g2.cpu().double().numpy(), r2)
+    print("real-basis gradients L=%d %s worst %s %.3e, %s %.3e" % (L, dtype, l1, e1, l2, e2), flush=True)
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (l1, e1, l2, e2)
+    lib = _lib()
+    vplan = lib.IstpPlan(2, 1, dtype)
+    assert lib.istp_real_backward_workspace_bytes(vplan._h, N) == -1
+    plan.close()
+    vplan.close()

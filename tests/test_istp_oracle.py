@@ -354,3 +354,22 @@ def test_real_gaunt_product_against_quadrature(rng):
     f2 = sum(r2[l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
     want = np.array([(W * f1 * f2 * Y[l, m]).sum() for l in range(2 * L + 1) for m in range(-l, l + 1)])
     np.testing.assert_allclose(z, want, atol=1e-12)
+
+
+def test_real_gaunt_gradients(rng):
+    """Euler identity, and grad_x1[i] = integral of Y^R_i f2 f_g (f_g = sum g Y^R; scipy harmonics, exact grid)."""
+    L = 2
+    r1 = rng.standard_normal((2, oi.gaunt_size(L)))
+    r2 = rng.standard_normal((2, oi.gaunt_size(L)))
+    g = rng.standard_normal((2, oi.gaunt_size(2 * L)))
+    g1, g2 = oi.gaunt_tp_real_vjp(L, r1, r2, g)
+    want = (g * oi.gaunt_tp_real(L, r1, r2)).sum(1)
+    np.testing.assert_allclose((g1 * r1).sum(1), want, rtol=1e-12)
+    np.testing.assert_allclose((g2 * r2).sum(1), want, rtol=1e-12)
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+    Y = {(l, m): _real_sph_harm(l, m, T, P) for l in range(2 * L + 1) for m in range(-l, l + 1)}
+    for n in range(2):
+        f2 = sum(r2[n, l * l + l + m] * Y[l, m] for l in range(L + 1) for m in range(-l, l + 1))
+        fg = sum(g[n, l * l + l + m] * Y[l, m] for l in range(2 * L + 1) for m in range(-l, l + 1))
+        q = np.array([(W * Y[l, m] * f2 * fg).sum() for l in range(L + 1) for m in range(-l, l + 1)])
+        np.testing.assert_allclose(g1[n], q, atol=1e-12)
