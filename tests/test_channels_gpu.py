@@ -126,3 +126,20 @@ def test_rejects_bad_channel_arguments():
     call(N=0)   # nothing to do
     torch.cuda.synchronize()
     plan.close()
+
+
+@pytest.mark.parametrize("grid", [{"cover": 1}, {"n_theta": 12, "n_phi": 24}], ids=["alternate-cover", "global-grid"])
+def test_weighted_channels_other_plans(grid):
+    """The channel kernel on plans with the alternate product cover and with one forced global grid."""
+    torch = _torch()
+    L, N, C = 5, 6, 3
+    x1, x2, w = wl.channel_inputs(L, N, C, True, "pair", "fp32", seed=31)
+    plan = _lib().Plan(L, **grid)
+    got = plan.forward_weighted(x1.cuda(), x2.cuda(), w.cuda())
+    torch.cuda.synchronize()
+    ref = oc.cgtp_channels(L, x1.double().numpy(), x2.double().numpy(), w.double().numpy())
+    nout = (L + 1) ** 4
+    err, path = per_path_rel_err(L, got.cpu().double().numpy().reshape(N * C, nout), ref.reshape(N * C, nout))
+    print("%s worst per-path rel L2 %.3e at %s" % (grid, err, path), flush=True)
+    assert err <= TOL["fp32"], (err, path)
+    plan.close()
