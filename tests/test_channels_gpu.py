@@ -8,7 +8,7 @@ import pytest
 
 import cgtp_inputs as wl
 import oracle.channels as oc
-from test_gpu_parity import TOL, _lib, _torch, per_path_rel_err
+from test_gpu_parity import TOL, _lib, _torch, path_ids, per_path_rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -71,7 +71,7 @@ def test_weights_scale_paths_of_the_unweighted_result():
     zw = plan.forward_weighted(a, b, wc)
     z = plan.forward_weighted(a, b)
     torch.cuda.synchronize()
-    pid, _ = __import__("test_gpu_parity").path_ids(L)
+    pid, _ = path_ids(L)
     scale = wc[:, :, torch.as_tensor(pid, device="cuda")]
     torch.testing.assert_close(zw, z * scale, rtol=2e-6, atol=1e-6 * float(z.abs().max()))
     plan.close()
