@@ -173,6 +173,21 @@ int istp_backward_real(istp_plan_t plan, const void *x1, const void *x2, const v
 /* Workspace bytes istp_backward_real needs for N pairs; -1 where it does not apply. */
 int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N);
 
+/*
+ * Gradients of sum(grad_out * out) for istp_forward_weighted with x2 per
+ * channel (x2_shared must be 0: its gradient would sum over the channels,
+ * CGTP_EUNSUP).  By the chain rule through the label weights,
+ *   grad_x1 = w1 . P'(wo . grad_out, w2 . x2~),  grad_x2 = +-w2 . P'(wo . grad_out, w1 . x1~),
+ * with P' and x~ as for istp_backward; the channel kernel runs them on the
+ * gradient grid.  Layouts as istp_forward_weighted (grad_x1, grad_x2 like x1);
+ * rules as istp_backward.  CGTP_EUNSUP where the plan's gradient product needs
+ * lifts beyond 36 degrees (L > 17) or does not exist.  Gradients with respect
+ * to the weights are not computed.
+ */
+int istp_backward_weighted(istp_plan_t plan, const void *x1, const void *x2, const void *w1, const void *w2,
+                           const void *wo, const void *grad_out, void *grad_x1, void *grad_x2, int64_t N,
+                           const istp_channels *ch, void *hip_stream);
+
 /* Irrep labels in a row of degree bound L: L + 1 (spin 0), 3 L + 1 (spin 1); -1 if invalid. */
 int64_t istp_num_labels(int32_t L, int32_t spin);
 

@@ -379,3 +379,25 @@ def gaunt_tp_real_vjp(L: int, r1, r2, g, threads: int = 0):
         g1[n] = gaunt_tp_real(L, eye, np.repeat(b[n:n + 1], gaunt_size(L), 0), threads) @ gg[n]
         g2[n] = gaunt_tp_real(L, np.repeat(a[n:n + 1], gaunt_size(L), 0), eye, threads) @ gg[n]
     return g1, g2
+
+
+def channel_product_vjp(spin: int, L: int, x1, x2, g, w1=None, w2=None, wo=None, threads: int = 0):
+    """Gradients of sum(g * channel_product(x1, x2, w1, w2, wo)) w.r.t. x1 and x2 (x2 per channel, [N, C, n_in]):
+    the chain rule through the label weights around ``product_vjp``."""
+    a = np.asarray(x1, dtype=np.float64)
+    b = np.asarray(x2, dtype=np.float64)
+    gg = np.asarray(g, dtype=np.float64)
+    n, c, nin = a.shape
+
+    def col_weights(w, Lx):
+        if w is None:
+            return np.ones((n, c, spin_size(spin, Lx)))
+        wt = np.asarray(w, dtype=np.float64)
+        if wt.ndim == 2:
+            wt = np.broadcast_to(wt, (n, c, wt.shape[1]))
+        return wt[:, :, column_labels(spin, Lx)]
+
+    s1, s2, so = col_weights(w1, L), col_weights(w2, L), col_weights(wo, 2 * L)
+    r1, r2 = product_vjp(spin, L, (s1 * a).reshape(n * c, nin), (s2 * b).reshape(n * c, nin),
+                         (so * gg).reshape(n * c, -1), threads)
+    return s1 * r1.reshape(n, c, nin), s2 * r2.reshape(n, c, nin)

@@ -91,6 +91,8 @@ def _load():
         "istp_real_workspace_bytes": (i64, [vp, i64]),
         "istp_backward_real": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
         "istp_real_backward_workspace_bytes": (i64, [vp, i64]),
+        "istp_backward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64,
+                                                  ctypes.POINTER(cgtp_channels), vp]),
         "istp_label_index": (i64, [i32, i32, i32]),
         "istp_destroy": (ctypes.c_int, [vp]),
         "istp_num_inputs": (i64, [i32, i32]),
@@ -116,7 +118,7 @@ def exported_symbols():
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index",
             "istp_forward_real", "istp_real_workspace_bytes", "istp_backward_real",
-            "istp_real_backward_workspace_bytes", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
+            "istp_real_backward_workspace_bytes", "istp_backward_weighted", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
             "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
 
@@ -281,6 +283,17 @@ def istp_backward_real(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int 
 
 def istp_real_backward_workspace_bytes(plan, N: int) -> int:
     return int(_load().istp_real_backward_workspace_bytes(plan, int(N)))
+
+
+def istp_backward_weighted(plan, x1_ptr: int, x2_ptr: int, w1_ptr, w2_ptr, wo_ptr, g_ptr: int, gx1_ptr, gx2_ptr,
+                           N: int, channels: int = 1, weights_per_pair: bool = False,
+                           stream_ptr: int | None = None) -> None:
+    ch = cgtp_channels(int(channels), 0, int(bool(weights_per_pair)), 0)
+    vpn = lambda p: ctypes.c_void_p(p) if p else None
+    rc = _load().istp_backward_weighted(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), vpn(w1_ptr),
+                                        vpn(w2_ptr), vpn(wo_ptr), ctypes.c_void_p(g_ptr), vpn(gx1_ptr), vpn(gx2_ptr),
+                                        int(N), ctypes.byref(ch), vpn(stream_ptr))
+    _check(rc, "istp_backward_weighted")
 
 
 def istp_num_labels(L: int, spin: int) -> int:
@@ -494,6 +507,20 @@ class IstpPlan:
         istp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, workspace.data_ptr(),
                           workspace.numel(), s.cuda_stream)
         return out
+
+    def backward_weighted(self, x1, x2, grad_out, w1=None, w2=None, wo=None, stream=None):
+        """Gradients w.r.t. x1 [N, C, nin] and x2 [N, C, nin] of sum(grad_out * forward_weighted(x1, x2, w1, w2, wo))."""
+        import torch
+        N, C = x1.shape[0], x1.shape[1]
+        given = [w for w in (w1, w2, wo) if w is not None]
+        per_pair = bool(given) and given[0].dim() == 3
+        g1, g2 = torch.empty_like(x1), torch.empty_like(x2)
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        ptr = lambda w: w.data_ptr() if w is not None else None
+        istp_backward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), ptr(w1), ptr(w2), ptr(wo),
+                               grad_out.contiguous().data_ptr(), g1.data_ptr(), g2.data_ptr(), N, C, per_pair,
+                               s.cuda_stream)
+        return g1, g2
 
     def backward_real(self, x1, x2, grad_out, workspace=None, stream=None):
         """Gradients of sum(grad_out * forward_real(x1, x2)) w.r.t. x1 and x2 (real basis, spin 0 plans)."""

@@ -584,6 +584,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     }
                     cc = cc + 1 == ch.channels ? 0 : cc + 1;
                 }
+                if (d.flags & kNegate) v = -v;
                 out[(p0 + p) * (int64_t)nout + o] = v;
             }
         }
@@ -625,6 +626,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                             v *= ch.wo[k * ch.nlo + lo];
                         }
                         cc = cc + 1 == ch.channels ? 0 : cc + 1;
+                        if (d.flags & kNegate) v = -v;
                         out[(p0 + p) * (int64_t)nout + o] = v;
                     }
                 }

@@ -846,6 +846,72 @@ int istp_backward_real(istp_plan_t plan, const void* x1, const void* x2, const v
     return rc;
 }
 
+// Gradients of the channel-wise product out = wo . P(w1 . x1, w2 . x2) (x2 per
+// channel): grad_x1 = w1 . P'(wo . g, w2 . x2~), grad_x2 = +-w2 . P'(wo . g, w1 . x1~),
+// P' the gradient product; the channel kernel applies the three weights with
+// their roles exchanged.
+int istp_backward_weighted(istp_plan_t plan, const void* x1, const void* x2, const void* w1, const void* w2,
+                           const void* wo, const void* grad_out, void* grad_x1, void* grad_x2, int64_t N,
+                           const istp_channels* ch, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (!plan->bwd.ok || plan->bwd.desc.L + 1 > 4 * istp::kMaxLiftSteps) return CGTP_EUNSUP;
+    const int32_t C = ch ? ch->channels : 1;
+    if (C < 1 || (ch && ((ch->x2_shared & ~1) || (ch->weights_per_pair & ~1) || ch->reserved))) return CGTP_EINVAL;
+    if (ch && ch->x2_shared) return CGTP_EUNSUP;   // its gradient sums over the channels
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2)) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)grad_out | (uintptr_t)grad_x1 | (uintptr_t)grad_x2) & 15)
+        return CGTP_EINVAL;
+    const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+    if (((uintptr_t)w1 | (uintptr_t)w2 | (uintptr_t)wo) & (esz - 1)) return CGTP_EINVAL;
+    if (N > INT64_MAX / C) return CGTP_EINVAL;
+    const int64_t rows = N * C;
+    const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+    if ((uint64_t)rows > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
+    const bool per_row = ch && ch->weights_per_pair;
+    const int64_t nl = num_labels(plan->L, plan->spin), nlo = num_labels(2 * plan->L, plan->spin);
+    const int64_t wrows = per_row ? rows : C;
+    const size_t bin = (size_t)rows * nin * esz, bout = (size_t)rows * nout * esz;
+    const void* reads[6] = {x1, x2, grad_out, w1, w2, wo};
+    const size_t rlen[6] = {bin, bin, bout, (size_t)(wrows * nl) * esz, (size_t)(wrows * nl) * esz,
+                            (size_t)(wrows * nlo) * esz};
+    void* writes[2] = {grad_x1, grad_x2};
+    for (void* w : writes) {
+        if (!w) continue;
+        for (int i = 0; i < 6; ++i)
+            if (reads[i] && overlaps(w, bin, reads[i], rlen[i])) return CGTP_EINVAL;
+    }
+    if (grad_x1 && grad_x2 && overlaps(grad_x1, bin, grad_x2, bin)) return CGTP_EINVAL;
+    int rc = current_device_is(plan->device);
+    if (rc != CGTP_OK) return rc;
+    const int32_t flags = per_row ? istp::kChanPerRow : 0;
+    auto one = [&](const void* xo, const void* w_other, const void* w_self, void* grad, int extra) -> int {
+        istp::IstpDesc d = plan->bwd.desc;
+        d.flags = istp::kReverseSecond | extra;
+        int err;
+        const bool t2 = plan->spin == ISTP_TENSOR;
+        if (plan->dtype == CGTP_FP32) {
+            const istp::IstpChan<float> c{(const float*)wo, (const float*)w_other, (const float*)w_self, C, flags,
+                                          (int32_t)nlo, (int32_t)nl, (int32_t)nl};
+            err = (t2 ? istp::launch_istp_channels_tensor_f32 : istp::launch_istp_channels_f32)(
+                plan->bwd.tf, d, (const float*)grad_out, (const float*)xo, (float*)grad, rows, c, hip_stream);
+        } else {
+            const istp::IstpChan<double> c{(const double*)wo, (const double*)w_other, (const double*)w_self, C,
+                                           flags, (int32_t)nlo, (int32_t)nl, (int32_t)nl};
+            err = (t2 ? istp::launch_istp_channels_tensor_f64 : istp::launch_istp_channels_f64)(
+                plan->bwd.td, d, (const double*)grad_out, (const double*)xo, (double*)grad, rows, c, hip_stream);
+        }
+        if (err != 0) {
+            cgtp::set_last_hip_error(err);
+            return CGTP_EHIP;
+        }
+        return CGTP_OK;
+    };
+    if (grad_x1) rc = one(x2, w2, w1, grad_x1, 0);
+    if (rc == CGTP_OK && grad_x2) rc = one(x1, w1, w2, grad_x2, plan->spin == ISTP_VECTOR ? istp::kNegate : 0);
+    return rc;
+}
+
 int istp_backward(istp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
                   void* grad_x2, int64_t N, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;

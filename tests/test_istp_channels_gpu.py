@@ -124,3 +124,24 @@ def test_rejects_bad_channel_arguments():
     call(N=0)
     torch.cuda.synchronize()
     plan.close()
+
+
+@pytest.mark.parametrize("spin,L,N,C,weights,dtype", [(0, 3, 5, 3, "channel", "fp32"), (1, 4, 4, 2, "pair", "fp32"),
+                                                      (1, 2, 3, 3, "channel", "fp64"), (2, 2, 3, 2, "channel", "fp32")])
+def test_weighted_channel_gradients(spin, L, N, C, weights, dtype):
+    """istp_backward_weighted against the oracle's chain rule through the label weights (x2 per channel)."""
+    torch = _torch()
+    x1, x2, w1, w2, wo = wl.istp_channel_inputs(spin, L, N, C, False, weights, dtype, seed=40 + L + spin)
+    g = torch.randn(N, C, (2 * spin + 1) * (2 * L + 1) ** 2, generator=torch.Generator().manual_seed(50 + L),
+                    dtype=torch.float64).to(x1.dtype)
+    plan = _lib().IstpPlan(L, spin, dtype)
+    cu = lambda t: None if t is None else t.cuda()
+    g1, g2 = plan.backward_weighted(x1.cuda(), x2.cuda(), g.cuda(), cu(w1), cu(w2), cu(wo))
+    torch.cuda.synchronize()
+    d = lambda t: None if t is None else t.double().numpy()
+    r1, r2 = oi.channel_product_vjp(spin, L, d(x1), d(x2), d(g), d(w1), d(w2), d(wo))
+    e1, l1 = per_label_rel_err(L, spin, g1.cpu().double().numpy().reshape(N * C, -1), r1.reshape(N * C, -1))
+    e2, l2 = per_label_rel_err(L, spin, g2.cpu().double().numpy().reshape(N * C, -1), r2.reshape(N * C, -1))
+    print("weighted gradients spin=%d L=%d %s: %s %.3e, %s %.3e" % (spin, L, dtype, l1, e1, l2, e2), flush=True)
+    assert e1 <= TOL[dtype] and e2 <= TOL[dtype], (l1, e1, l2, e2)
+    plan.close()

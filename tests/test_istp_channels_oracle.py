@@ -96,3 +96,23 @@ def test_weighted_channels_are_equivariant(spin, rng):
     z = f(L, x1, x2)
     zr = _complex(f, L, rot(x1, L), rot(x2, L))
     np.testing.assert_allclose(zr, rot(z, 2 * L), atol=1e-10)
+
+
+@pytest.mark.parametrize("spin", [0, 1, 2])
+def test_weighted_channel_gradients_euler(spin, rng):
+    """Bilinearity of the weighted layer: <g, out> = <grad_x1, x1> = <grad_x2, x2>, per (pair, channel)."""
+    L, n, ch = 2, 2, 3
+    size = oi.spin_size(spin, L)
+    x1 = rng.standard_normal((n, ch, size))
+    x2 = rng.standard_normal((n, ch, size))
+    g = rng.standard_normal((n, ch, oi.spin_size(spin, 2 * L)))
+    w1 = rng.standard_normal((ch, len(oi.labels(spin, L))))
+    w2 = rng.standard_normal((n, ch, len(oi.labels(spin, L))))
+    wo = rng.standard_normal((ch, len(oi.labels(spin, 2 * L))))
+    # w1 and wo per channel, w2 per pair: the layer takes one layout, so the per-channel rows are repeated
+    out = oi.channel_product(spin, L, x1, x2, np.broadcast_to(w1, (n,) + w1.shape), w2,
+                             np.broadcast_to(wo, (n,) + wo.shape))
+    g1, g2 = oi.channel_product_vjp(spin, L, x1, x2, g, w1, w2, wo)
+    want = (g * out).sum(-1)
+    np.testing.assert_allclose((g1 * x1).sum(-1), want, rtol=1e-11)
+    np.testing.assert_allclose((g2 * x2).sum(-1), want, rtol=1e-11)
