@@ -2,7 +2,7 @@
  * istp.h: C ABI of the multiple-input, multiple-output irrep-signal tensor
  * products (arXiv 2602.21466, Section 4.3 and Appendix D) on MI355X (gfx950).
  *
- * Two products of two feature rows x1, x2, each the (s, s, s) case of the
+ * Three products of two feature rows x1, x2, each the (s, s, s) case of the
  * irrep-signal tensor product with every input irrep lifted into one signal
  * and every output irrep read back from the one pointwise product:
  *
