@@ -204,6 +204,23 @@ def time_istp_real(w, steps, warmup):
     q["flops_per_pair"] = 4 * q["flops_per_pair"]
     res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": q, "kind": "istp_real"}
     res.update(_time_launches(lambda st: plan.forward_real(a, b, out, ws, st), w.N, steps, warmup))
+    # both gradients in the real basis: four gradient products each, plus conversions
+    nbw = lib.istp_real_backward_workspace_bytes(plan._h, w.N)
+    if nbw > 0:
+        bq = dict(plan.backward_query())
+        bq["flops_per_pair"] = 4 * bq["flops_per_pair"]
+        g = torch.randn(out.shape, generator=torch.Generator("cpu").manual_seed(w.seed + 2),
+                        dtype=torch.float64).to(out.dtype).cuda()
+        g1, g2 = torch.empty_like(a), torch.empty_like(b)
+        wsb = torch.empty(nbw, dtype=torch.uint8, device="cuda")
+        bwd = {"workload": w.name + ":backward", "L": w.L, "N": w.N, "dtype": w.dtype, "plan": bq,
+               "kind": "istp_real"}
+        bwd.update(_time_launches(lambda st: lib.istp_backward_real(plan._h, a.data_ptr(), b.data_ptr(), g.data_ptr(),
+                                                                    g1.data_ptr(), g2.data_ptr(), w.N, wsb.data_ptr(),
+                                                                    nbw, st.cuda_stream),
+                                  w.N, steps, warmup))
+        res["backward"] = bwd
+        del g, g1, g2, wsb
     plan.close()
     del out, a, b, ws
     torch.cuda.empty_cache()
@@ -433,8 +450,14 @@ def main():
             log("timing %s" % wr.name)
             rr = time_istp_real(wr, args.steps, args.warmup)
             log("  %.4f ms/step, %.4g pairs/s" % (rr["ms_per_step"], rr["value"]))
-            istp.append({"workload": wr.name, "value": round(rr["value"], 1), "unit": "pairs/s",
-                         "basis": "real", "ms_per_step": round(rr["ms_per_step"], 4), "roofline": roofline(rr)})
+            entry = {"workload": wr.name, "value": round(rr["value"], 1), "unit": "pairs/s",
+                     "basis": "real", "ms_per_step": round(rr["ms_per_step"], 4), "roofline": roofline(rr)}
+            if "backward" in rr:
+                rb = rr["backward"]
+                log("  backward (both gradients) %.4f ms/step, %.4g pairs/s" % (rb["ms_per_step"], rb["value"]))
+                entry["backward"] = {"value": round(rb["value"], 1), "unit": "pairs/s",
+                                     "ms_per_step": round(rb["ms_per_step"], 4), "roofline": roofline(rb)}
+            istp.append(entry)
     if args.istp_channels and args.istp_channels != "none":
         by_ic = {x.name: x for x in cgtp_inputs.ISTP_CHANNEL_WORKLOADS}
         for name in args.istp_channels.split(","):
