@@ -143,8 +143,9 @@ int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, cons
  * index l^2 + l + m.  x1, x2: [N, (L+1)^2] real-basis rows; out: [N, (2L+1)^2]
  * the real-basis coefficients of the integral of f1 f2 Y^R_{l3 m3}.  The
  * inputs are converted to the real and imaginary parts of their complex
- * coefficients, the four products of those parts run on the plan's kernel, and
- * the result is read back in the real basis: four products' work.
+ * coefficients, three products of those parts run on the plan's kernel
+ * (Karatsuba's form: P(a1, a2), P(b1, b2), P(a1 + b1, a2 + b2)), and the
+ * result is read back in the real basis: three products' work.
  * workspace: caller-owned device memory of istp_real_workspace_bytes(plan, N)
  * bytes or more, 256-byte aligned, not overlapping the other buffers (its
  * contents are scratch).  CGTP_EUNSUP for spin 1 or 2 plans; otherwise as
@@ -161,7 +162,7 @@ int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
  * The integrals of three real harmonics are fully symmetric, so
  *   grad_x1 = Q(grad_out, x2),  grad_x2 = Q(grad_out, x1),
  * with Q the real-basis product of a degree-2L and a degree-L row projected on
- * degrees <= L (four products on the plan's gradient grid; no time reversal).
+ * degrees <= L (three products on the plan's gradient grid; no time reversal).
  * Layouts and rules as istp_backward; workspace: caller-owned, 256-byte
  * aligned, istp_real_backward_workspace_bytes(plan, N) bytes or more, reused
  * by the two gradients.  CGTP_EUNSUP for spin 1 or 2 plans and where the

@@ -154,12 +154,14 @@ int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float*
                     int64_t N, void* stream);
 int launch_istp_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
                     double* out, int64_t N, void* stream);
-int launch_real_to_complex_f32(const float* r, float* re, float* im, int64_t rows, int nin, void* stream);
-int launch_real_to_complex_f64(const double* r, double* re, double* im, int64_t rows, int nin, void* stream);
-int launch_real_from_complex_f32(float* out, const float* pbb, const float* pab, const float* pba, int64_t rows,
-                                 int Lo, void* stream);
-int launch_real_from_complex_f64(double* out, const double* pbb, const double* pab, const double* pba,
-                                 int64_t rows, int Lo, void* stream);
+int launch_real_to_complex_f32(const float* r, float* re, float* im, float* sum, int64_t rows, int nin,
+                               void* stream);
+int launch_real_to_complex_f64(const double* r, double* re, double* im, double* sum, int64_t rows, int nin,
+                               void* stream);
+int launch_real_from_complex_f32(float* out, const float* pbb, const float* pss, int64_t rows, int Lo,
+                                 void* stream);
+int launch_real_from_complex_f64(double* out, const double* pbb, const double* pss, int64_t rows, int Lo,
+                                 void* stream);
 int launch_istp_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
                            float* out, int64_t N, void* stream);
 int launch_istp_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,

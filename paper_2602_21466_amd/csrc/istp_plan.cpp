@@ -683,8 +683,9 @@ int istp_forward_weighted(istp_plan_t plan, const void* x1, const void* x2, cons
     return CGTP_OK;
 }
 
-// Real-basis Gaunt product: workspace of four converted inputs and three
-// products (the fourth product lands in out), each 256-byte aligned.
+// Real-basis Gaunt product: workspace of the converted inputs (real part,
+// imaginary part and their sum, for each input) and two products (the third
+// lands in out), each 256-byte aligned.
 static size_t real_part_bytes(size_t n) { return (n + 255) / 256 * 256; }
 
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
@@ -692,7 +693,7 @@ int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(nout * esz))) return -1;
-    return (int64_t)(4 * real_part_bytes((size_t)N * nin * esz) + 3 * real_part_bytes((size_t)N * nout * esz));
+    return (int64_t)(6 * real_part_bytes((size_t)N * nin * esz) + 2 * real_part_bytes((size_t)N * nout * esz));
 }
 
 int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* workspace,
@@ -716,40 +717,41 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
     const size_t pin = real_part_bytes(bin), pout = real_part_bytes(bout);
     void* re1 = w;
     void* im1 = w + pin;
-    void* re2 = w + 2 * pin;
-    void* im2 = w + 3 * pin;
-    void* pbb = w + 4 * pin;
-    void* pab = w + 4 * pin + pout;
-    void* pba = w + 4 * pin + 2 * pout;
+    void* sm1 = w + 2 * pin;
+    void* re2 = w + 3 * pin;
+    void* im2 = w + 4 * pin;
+    void* sm2 = w + 5 * pin;
+    void* pbb = w + 6 * pin;
+    void* pss = w + 6 * pin + pout;
     const int Lo = 2 * plan->L;
     int err;
     if (plan->dtype == CGTP_FP32) {
-        err = istp::launch_real_to_complex_f32((const float*)x1, (float*)re1, (float*)im1, N, (int)nin, hip_stream);
-        if (!err)
-            err = istp::launch_real_to_complex_f32((const float*)x2, (float*)re2, (float*)im2, N, (int)nin,
-                                                   hip_stream);
-    } else {
-        err = istp::launch_real_to_complex_f64((const double*)x1, (double*)re1, (double*)im1, N, (int)nin,
+        err = istp::launch_real_to_complex_f32((const float*)x1, (float*)re1, (float*)im1, (float*)sm1, N, (int)nin,
                                                hip_stream);
         if (!err)
-            err = istp::launch_real_to_complex_f64((const double*)x2, (double*)re2, (double*)im2, N, (int)nin,
-                                                   hip_stream);
+            err = istp::launch_real_to_complex_f32((const float*)x2, (float*)re2, (float*)im2, (float*)sm2, N,
+                                                   (int)nin, hip_stream);
+    } else {
+        err = istp::launch_real_to_complex_f64((const double*)x1, (double*)re1, (double*)im1, (double*)sm1, N,
+                                               (int)nin, hip_stream);
+        if (!err)
+            err = istp::launch_real_to_complex_f64((const double*)x2, (double*)re2, (double*)im2, (double*)sm2, N,
+                                                   (int)nin, hip_stream);
     }
     if (err) {
         cgtp::set_last_hip_error(err);
         return CGTP_EHIP;
     }
-    // P(a1, a2) into out, then P(b1, b2), P(a1, b2), P(b1, a2)
+    // P(a1, a2) into out, then P(b1, b2) and P(a1 + b1, a2 + b2)
     rc = launch_prod(plan, plan->fwd, 0, re1, re2, out, N, hip_stream);
     if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, im1, im2, pbb, N, hip_stream);
-    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, re1, im2, pab, N, hip_stream);
-    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, im1, re2, pba, N, hip_stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, sm1, sm2, pss, N, hip_stream);
     if (rc != CGTP_OK) return rc;
     err = plan->dtype == CGTP_FP32
-              ? istp::launch_real_from_complex_f32((float*)out, (const float*)pbb, (const float*)pab,
-                                                   (const float*)pba, N, Lo, hip_stream)
-              : istp::launch_real_from_complex_f64((double*)out, (const double*)pbb, (const double*)pab,
-                                                   (const double*)pba, N, Lo, hip_stream);
+              ? istp::launch_real_from_complex_f32((float*)out, (const float*)pbb, (const float*)pss, N, Lo,
+                                                   hip_stream)
+              : istp::launch_real_from_complex_f64((double*)out, (const double*)pbb, (const double*)pss, N, Lo,
+                                                   hip_stream);
     if (err) {
         cgtp::set_last_hip_error(err);
         return CGTP_EHIP;
@@ -761,15 +763,14 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
 // real harmonics) are fully symmetric, so grad_x1 = Q(g, x2) and grad_x2 =
 // Q(g, x1) with Q the real-basis product of a degree-2L and a degree-L row
 // projected on degrees <= L (the gradient product's grid, no time reversal).
-// Workspace per gradient launch: the converted upstream gradient (two rows of
-// (2L+1)^2), the converted input (two rows of (L+1)^2), three products.
+// Workspace per gradient: the converted upstream gradient (three rows of
+// (2L+1)^2), the converted input (three rows of (L+1)^2), two products.
 int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N) {
     if (!plan || N < 0 || plan->spin != ISTP_GAUNT || !plan->bwd.ok) return -1;
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t ng = (size_t)plan->fwd.desc.nout, nin = (size_t)plan->fwd.desc.nin;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(ng * esz))) return -1;
-    return (int64_t)(2 * real_part_bytes((size_t)N * ng * esz) + 2 * real_part_bytes((size_t)N * nin * esz) +
-                     3 * real_part_bytes((size_t)N * nin * esz));
+    return (int64_t)(3 * real_part_bytes((size_t)N * ng * esz) + 5 * real_part_bytes((size_t)N * nin * esz));
 }
 
 static int real_bwd_one(istp_plan_t plan, const void* g, const void* x, void* grad, int64_t N, char* w,
@@ -779,33 +780,36 @@ static int real_bwd_one(istp_plan_t plan, const void* g, const void* x, void* gr
     const size_t pg = real_part_bytes((size_t)N * ng * esz), px = real_part_bytes((size_t)N * nin * esz);
     void* ga = w;
     void* gb = w + pg;
-    void* xa = w + 2 * pg;
-    void* xb = w + 2 * pg + px;
-    void* pbb = w + 2 * pg + 2 * px;
-    void* pab = w + 2 * pg + 3 * px;
-    void* pba = w + 2 * pg + 4 * px;
+    void* gs = w + 2 * pg;
+    void* xa = w + 3 * pg;
+    void* xb = w + 3 * pg + px;
+    void* xs = w + 3 * pg + 2 * px;
+    void* pbb = w + 3 * pg + 3 * px;
+    void* pss = w + 3 * pg + 4 * px;
     int err = plan->dtype == CGTP_FP32
-                  ? istp::launch_real_to_complex_f32((const float*)g, (float*)ga, (float*)gb, N, (int)ng, stream)
-                  : istp::launch_real_to_complex_f64((const double*)g, (double*)ga, (double*)gb, N, (int)ng, stream);
+                  ? istp::launch_real_to_complex_f32((const float*)g, (float*)ga, (float*)gb, (float*)gs, N, (int)ng,
+                                                     stream)
+                  : istp::launch_real_to_complex_f64((const double*)g, (double*)ga, (double*)gb, (double*)gs, N,
+                                                     (int)ng, stream);
     if (!err)
         err = plan->dtype == CGTP_FP32
-                  ? istp::launch_real_to_complex_f32((const float*)x, (float*)xa, (float*)xb, N, (int)nin, stream)
-                  : istp::launch_real_to_complex_f64((const double*)x, (double*)xa, (double*)xb, N, (int)nin,
-                                                     stream);
+                  ? istp::launch_real_to_complex_f32((const float*)x, (float*)xa, (float*)xb, (float*)xs, N,
+                                                     (int)nin, stream)
+                  : istp::launch_real_to_complex_f64((const double*)x, (double*)xa, (double*)xb, (double*)xs, N,
+                                                     (int)nin, stream);
     if (err) {
         cgtp::set_last_hip_error(err);
         return CGTP_EHIP;
     }
     int rc = launch_prod(plan, plan->bwd, 0, ga, xa, grad, N, stream);
     if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, gb, xb, pbb, N, stream);
-    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, ga, xb, pab, N, stream);
-    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, gb, xa, pba, N, stream);
+    if (rc == CGTP_OK) rc = launch_prod(plan, plan->bwd, 0, gs, xs, pss, N, stream);
     if (rc != CGTP_OK) return rc;
     err = plan->dtype == CGTP_FP32
-              ? istp::launch_real_from_complex_f32((float*)grad, (const float*)pbb, (const float*)pab,
-                                                   (const float*)pba, N, plan->L, stream)
-              : istp::launch_real_from_complex_f64((double*)grad, (const double*)pbb, (const double*)pab,
-                                                   (const double*)pba, N, plan->L, stream);
+              ? istp::launch_real_from_complex_f32((float*)grad, (const float*)pbb, (const float*)pss, N, plan->L,
+                                                   stream)
+              : istp::launch_real_from_complex_f64((double*)grad, (const double*)pbb, (const double*)pss, N, plan->L,
+                                                   stream);
     if (err) {
         cgtp::set_last_hip_error(err);
         return CGTP_EHIP;

@@ -1,6 +1,6 @@
 // Real spherical-harmonic basis for the Gaunt product (spin 0): conversion of
 // real-basis rows to the real and imaginary parts of their complex-basis
-// coefficients, and of the four products of those parts back to the real
+// coefficients, and of the three products of those parts back to the real
 // basis.  With the Condon-Shortley phase carried over from Y_l^m,
 //   Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m (m > 0), Y_l^0 (m = 0),
 //               sqrt(2) (-1)^m Im Y_l^|m| (m < 0),
@@ -10,7 +10,8 @@
 // and a real function's real-basis coefficients are read back as
 //   r_{l,m} = sqrt 2 Re c_{l,-m},  r_{l,-m} = sqrt 2 Im c_{l,-m}  (m > 0),  r_{l,0} = Re c_{l,0}.
 // The product of the complex coefficients is bilinear with real weights, so
-// c3 = P(a1, a2) - P(b1, b2) + i (P(a1, b2) + P(b1, a2)) for c = a + i b.
+// for c = a + i b, with three products (Karatsuba's form):
+//   Re c3 = P(a1, a2) - P(b1, b2),  Im c3 = P(a1 + b1, a2 + b2) - P(a1, a2) - P(b1, b2).
 
 #include <hip/hip_runtime.h>
 
@@ -30,10 +31,11 @@ __device__ __forceinline__ int degree_of(int c) {   // c = l^2 + l + m
     return l;
 }
 
-// One thread per (row, column): real and imaginary parts of c at that column.
+// One thread per (row, column): real and imaginary parts of c at that column, and their sum.
 template <typename T>
 __global__ __launch_bounds__(kConvThreads) void to_complex_kernel(const T* __restrict__ r, T* __restrict__ re,
-                                                                  T* __restrict__ im, int64_t total, int nin) {
+                                                                  T* __restrict__ im, T* __restrict__ sum,
+                                                                  int64_t total, int nin) {
     const int64_t e = (int64_t)blockIdx.x * kConvThreads + threadIdx.x;
     if (e >= total) return;
     const int64_t row = e / nin;
@@ -54,15 +56,15 @@ __global__ __launch_bounds__(kConvThreads) void to_complex_kernel(const T* __res
     }
     re[e] = a;
     im[e] = b;
+    sum[e] = a + b;
 }
 
-// One thread per (row, l, k >= 0) of the output: reads the four products at
+// One thread per (row, l, k >= 0) of the output: reads the three products at
 // column (l, -k) and writes the real-basis values at (l, k) and (l, -k).  out
 // holds P(a1, a2) on entry (read and written by the same thread only).
 template <typename T>
 __global__ __launch_bounds__(kConvThreads) void from_complex_kernel(T* __restrict__ out, const T* __restrict__ pbb,
-                                                                    const T* __restrict__ pab,
-                                                                    const T* __restrict__ pba, int64_t total,
+                                                                    const T* __restrict__ pss, int64_t total,
                                                                     int Lo) {
     const int64_t e = (int64_t)blockIdx.x * kConvThreads + threadIdx.x;
     if (e >= total) return;
@@ -75,53 +77,56 @@ __global__ __launch_bounds__(kConvThreads) void from_complex_kernel(T* __restric
     const int k = t - l * (l + 1) / 2;
     const int64_t base = row * nout + l * l + l;
     const T s = (T)1.41421356237309504880168872420969808;
-    const T re = out[base - k] - pbb[base - k];
+    const T paa = out[base - k], pb = pbb[base - k];
+    const T re = paa - pb;
     if (k == 0) {
         out[base] = re;
     } else {
-        const T imv = pab[base - k] + pba[base - k];
+        const T imv = pss[base - k] - paa - pb;
         out[base + k] = s * re;
         out[base - k] = s * imv;
     }
 }
 
 template <typename T>
-int launch_to_complex(const T* r, T* re, T* im, int64_t rows, int nin, void* stream) {
+int launch_to_complex(const T* r, T* re, T* im, T* sum, int64_t rows, int nin, void* stream) {
     const int64_t total = rows * nin;
     if (total <= 0) return 0;
     const int64_t grid = (total + kConvThreads - 1) / kConvThreads;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(to_complex_kernel<T>, dim3((unsigned)grid), dim3(kConvThreads), 0, (hipStream_t)stream, r, re,
-                       im, total, nin);
+                       im, sum, total, nin);
     return (int)hipGetLastError();
 }
 
 template <typename T>
-int launch_from_complex(T* out, const T* pbb, const T* pab, const T* pba, int64_t rows, int Lo, void* stream) {
+int launch_from_complex(T* out, const T* pbb, const T* pss, int64_t rows, int Lo, void* stream) {
     const int64_t total = rows * (int64_t)((Lo + 1) * (Lo + 2) / 2);
     if (total <= 0) return 0;
     const int64_t grid = (total + kConvThreads - 1) / kConvThreads;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(from_complex_kernel<T>, dim3((unsigned)grid), dim3(kConvThreads), 0, (hipStream_t)stream, out,
-                       pbb, pab, pba, total, Lo);
+                       pbb, pss, total, Lo);
     return (int)hipGetLastError();
 }
 
 }  // namespace
 
-int launch_real_to_complex_f32(const float* r, float* re, float* im, int64_t rows, int nin, void* stream) {
-    return launch_to_complex<float>(r, re, im, rows, nin, stream);
+int launch_real_to_complex_f32(const float* r, float* re, float* im, float* sum, int64_t rows, int nin,
+                               void* stream) {
+    return launch_to_complex<float>(r, re, im, sum, rows, nin, stream);
 }
-int launch_real_to_complex_f64(const double* r, double* re, double* im, int64_t rows, int nin, void* stream) {
-    return launch_to_complex<double>(r, re, im, rows, nin, stream);
+int launch_real_to_complex_f64(const double* r, double* re, double* im, double* sum, int64_t rows, int nin,
+                               void* stream) {
+    return launch_to_complex<double>(r, re, im, sum, rows, nin, stream);
 }
-int launch_real_from_complex_f32(float* out, const float* pbb, const float* pab, const float* pba, int64_t rows,
-                                 int Lo, void* stream) {
-    return launch_from_complex<float>(out, pbb, pab, pba, rows, Lo, stream);
+int launch_real_from_complex_f32(float* out, const float* pbb, const float* pss, int64_t rows, int Lo,
+                                 void* stream) {
+    return launch_from_complex<float>(out, pbb, pss, rows, Lo, stream);
 }
-int launch_real_from_complex_f64(double* out, const double* pbb, const double* pab, const double* pba,
-                                 int64_t rows, int Lo, void* stream) {
-    return launch_from_complex<double>(out, pbb, pab, pba, rows, Lo, stream);
+int launch_real_from_complex_f64(double* out, const double* pbb, const double* pss, int64_t rows, int Lo,
+                                 void* stream) {
+    return launch_from_complex<double>(out, pbb, pss, rows, Lo, stream);
 }
 
 }  // namespace istp
