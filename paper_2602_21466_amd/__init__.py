@@ -499,6 +499,8 @@ class IstpPlan:
             raise CgtpError(CGTP_EUNSUP, "forward_real (spin %d)" % self.spin)
         if workspace is None:
             workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < need:
+            raise ValueError("workspace must be a uint8 CUDA tensor of at least %d bytes" % need)
         if out is None:
             out = torch.empty((N, self.nout), dtype=tdt, device=x1.device)
         elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, self.nout):
@@ -511,9 +513,24 @@ class IstpPlan:
     def backward_weighted(self, x1, x2, grad_out, w1=None, w2=None, wo=None, stream=None):
         """Gradients w.r.t. x1 [N, C, nin] and x2 [N, C, nin] of sum(grad_out * forward_weighted(x1, x2, w1, w2, wo))."""
         import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        if not x1.is_cuda or x1.dtype != tdt or x1.dim() != 3 or x1.shape[2] != self.nin or not x1.is_contiguous():
+            raise ValueError("x1 must be a contiguous %s CUDA tensor [N, C, %d]" % (tdt, self.nin))
         N, C = x1.shape[0], x1.shape[1]
+        for t, n, what in ((x2, self.nin, "x2"), (grad_out, self.nout, "grad_out")):
+            if not t.is_cuda or t.dtype != tdt or tuple(t.shape) != (N, C, n):
+                raise ValueError("%s must be a %s CUDA tensor [N, C, %d] (x2 per channel)" % (what, tdt, n))
+        nl, nlo = istp_num_labels(self.L, self.spin), istp_num_labels(2 * self.L, self.spin)
         given = [w for w in (w1, w2, wo) if w is not None]
         per_pair = bool(given) and given[0].dim() == 3
+        for w, n in ((w1, nl), (w2, nl), (wo, nlo)):
+            if w is None:
+                continue
+            want = (N, C, n) if per_pair else (C, n)
+            if w.dtype != tdt or not w.is_cuda or not w.is_contiguous() or tuple(w.shape) != want:
+                raise ValueError("weights must be contiguous %s CUDA tensors %s (all per channel or all per pair)"
+                                 % (tdt, want))
+        x2 = x2.contiguous()
         g1, g2 = torch.empty_like(x1), torch.empty_like(x2)
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         ptr = lambda w: w.data_ptr() if w is not None else None
@@ -525,12 +542,18 @@ class IstpPlan:
     def backward_real(self, x1, x2, grad_out, workspace=None, stream=None):
         """Gradients of sum(grad_out * forward_real(x1, x2)) w.r.t. x1 and x2 (real basis, spin 0 plans)."""
         import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
         N = x1.shape[0]
+        for t, n, what in ((x1, self.nin, "x1"), (x2, self.nin, "x2"), (grad_out, self.nout, "grad_out")):
+            if not t.is_cuda or t.dtype != tdt or tuple(t.shape) != (N, n) or not t.is_contiguous():
+                raise ValueError("%s must be a contiguous %s CUDA tensor [N, %d]" % (what, tdt, n))
         need = istp_real_backward_workspace_bytes(self._h, N)
         if need < 0:
             raise CgtpError(CGTP_EUNSUP, "backward_real (spin %d, L %d)" % (self.spin, self.L))
         if workspace is None:
             workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < need:
+            raise ValueError("workspace must be a uint8 CUDA tensor of at least %d bytes" % need)
         g1, g2 = torch.empty_like(x1), torch.empty_like(x2)
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         istp_backward_real(self._h, x1.data_ptr(), x2.data_ptr(), grad_out.contiguous().data_ptr(), g1.data_ptr(),
