@@ -8,15 +8,24 @@
 
 namespace cgtp {
 
-constexpr int kThreads = 768;      // work-group size of the block kernel (12 wave64s, one per CU)
+#ifndef CGTP_THREADS
+#define CGTP_THREADS 768
+#endif
+#ifndef CGTP_RING_GROUP
+#define CGTP_RING_GROUP 8
+#endif
+#ifndef CGTP_MAX_TILES_F32
+#define CGTP_MAX_TILES_F32 10
+#endif
+constexpr int kThreads = CGTP_THREADS;   // work-group size of the block kernel (wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
-constexpr int kRingGroup = 8;      // rings per pass: two K = 4 steps of a 16x16x4 MFMA
+constexpr int kRingGroup = CGTP_RING_GROUP;   // rings per pass: K = 4 steps of a 16x16x4 MFMA
 constexpr int kLdsBudget = 156 * 1024;
 constexpr int kMaxPairs = 16;
 
 // MFMA accumulator tiles (16 x 16) each wave may hold, per precision.
 template <typename T> struct MaxTiles;
-template <> struct MaxTiles<float> { static constexpr int value = 10; };
+template <> struct MaxTiles<float> { static constexpr int value = CGTP_MAX_TILES_F32; };
 template <> struct MaxTiles<double> { static constexpr int value = 4; };
 
 // Product kinds per path (mirrors cgtp_path_norm's *kind).
@@ -26,12 +35,6 @@ enum PathKind : int32_t { kSS = 0, kCross = 1, kSV = 2, kDot = 3 };
 enum BlockKind : int32_t {
     kBlockScalar = 0,   // only scalar-scalar paths (a degree-0 input)
     kBlockCross = 1,    // scalar and toroidal lifts of both inputs; four projected components
-};
-
-// Where the Legendre projection reads the analysis spectra.
-enum BlockMode : int32_t {
-    kModeStaged = 0,   // staged as [ring][column][|m|] (any number of column tiles)
-    kModeGather = 1,   // in place in the transforms (one column tile: ncomp * pairs <= 8)
 };
 
 // Products of a kBlockCross block (BlockDesc::products); zero bits give the
@@ -50,7 +53,8 @@ enum BlockProducts : int32_t {
 // The Legendre projection is a batch of small GEMMs, one per |m|: rows
 // l3 = d, d+2, ..., J (those >= |m|), K = rings, columns (sign of m,
 // component, pair).  It runs on 16x16x4 MFMA tiles whose accumulators stay in
-// registers across all rings.
+// registers across all rings; its B operand is read in place in the analysis
+// output.
 struct alignas(16) BlockDesc {
     int32_t j1, j2, J, d;      // d = |j1 - j2|
     int32_t R;                 // northern rings of the block's grid
@@ -67,12 +71,9 @@ struct alignas(16) BlockDesc {
     int32_t coef_off;          // index of the block's first output in coef / coefi
     int32_t tdesc_off;         // offset of the block's MFMA tile descriptors
     int32_t lg_pairs;          // log2(pairs)
-    int32_t sm;                // |m| stride of the staged spectra: (J + 1) | 1
-    int32_t sc;                // staged columns: 2 ncomp pairs rounded up to 16
     int32_t products;          // BlockProducts bits
     int32_t rpad;              // rings of the weight table: R rounded up to the ring group
     int32_t wrow;              // entries per ring row of the weight table
-    int32_t mode;              // BlockMode: where the projection reads its spectra
     int32_t path_off;          // index of path (j1, j2, |j1 - j2|) in the (l1, l2, l3) order of all paths
     int64_t out_off;           // offset of the block inside one pair's output
 };
@@ -83,9 +84,8 @@ struct alignas(16) BlockDesc {
 //          ([|m|][ring][row], wrow rows per ring; rows past the tile's last
 //          valid one are read but their results are discarded)
 //   rs_nv: valid rows of the tile << 16
-//   b_off: staging mode: staged-spectrum offset of (ring 0, first column, |m|);
-//          gather mode: element offsets of longitudes +|m| (bits 0..15) and
-//          -|m| (bits 16..31) in a transform's pass layout
+//   b_off: element offsets of longitudes +|m| (bits 0..15) and -|m| (bits
+//          16..31) in a transform's pass layout
 //   code:  |m| << 16 | row tile << 8 | column tile
 struct alignas(16) TileDesc {
     int32_t a_off, rs_nv, b_off, code;
@@ -138,6 +138,24 @@ inline bool fft_factors(int phi, int* A, int* B) {
             return true;
         }
     return false;
+}
+
+// Strides of the per-ring working set, in complex entries: one transform in
+// pass layout (slot), one (ring, pair) unit, one ring.  With fp32 they put the
+// 16 columns (sign, component, pair) of an MFMA B operand read in place, and
+// the rings of the operand, on distinct 4-byte LDS banks where the column
+// pattern allows: slot = 1, unit = 2 and ring = 2 P (mod 16) entries.
+#ifndef CGTP_PAD
+#define CGTP_PAD 1
+#endif
+__host__ __device__ constexpr int slot_stride(int A, int B) {
+    return CGTP_PAD ? A * (B + 1) + ((1 - A * (B + 1)) & 15) : A * (B + 1);
+}
+__host__ __device__ constexpr int unit_stride(int nslot, int fs) {
+    return CGTP_PAD ? nslot * fs + ((2 - nslot * fs) & 15) : nslot * fs;
+}
+__host__ __device__ constexpr int ring_stride(int pairs, int per_rp) {
+    return CGTP_PAD ? pairs * per_rp + (((pairs <= 4 ? 2 * pairs : 1) - pairs * per_rp) & 15) : pairs * per_rp + 8;
 }
 
 // End phase: MFMA tile u of a block is dumped at u * tile_stride<T>() elements;

@@ -11,8 +11,8 @@
 //   3. pointwise products on half the circle (the other half is the complex
 //      conjugate): scalar-scalar, and the 1 (x) 1 -> 1 coupling of the two
 //      toroidal fields, i.e. the cross product (Section 5.1);
-//   4. longitude analysis in two passes; each complex transform carries two
-//      real spectra; the needed orders |m| <= J are staged, scaled, in LDS;
+//   4. longitude analysis in two passes, in place; each complex transform
+//      carries two real spectra;
 //   5. Legendre projection on MFMA: per |m| a [rows l3] x [4 rings] x
 //      [sign, component, pair] product accumulated in registers, with the
 //      Gauss weights, the north-south folding and P^m_l in the A operand.
@@ -59,15 +59,12 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // A longitude transform lives in "pass layout": A rows of B + 1 complex
 // entries (one pad per row), element k = k2 + B k1 at k1 (B + 1) + k2.  The
 // first pass writes rows, the second reads and rewrites columns in place, and
-// the padding keeps both access patterns free of bank conflicts.  Rings are
-// kRingSkew complex entries further apart than their transforms need, which
-// spreads the rings of one MFMA operand over the banks.  The staged spectra
-// (staging mode only) are [ring][column][|m|] with an odd |m| stride.
-
-constexpr int kRingSkew = 8;
+// the padding keeps both access patterns free of bank conflicts.  Slots,
+// (ring, pair) units and rings are padded (slot_stride, unit_stride,
+// ring_stride) so that the MFMA operands read in place spread over the banks.
 
 struct Layout {
-    int lc, prn, tw2, tdl, cvn, stage, fbuf, bbuf;   // byte offsets
+    int lc, prn, tw2, tdl, cvn, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
     int per_r;                                       // complex entries per ring
 };
@@ -81,20 +78,19 @@ template <typename T, int A, int B>
 __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     using C = typename Cplx<T>::type;
     constexpr int FS = A * (B + 1);
+    constexpr int FSS = slot_stride(A, B);
     Layout l;
     const int P = b.pairs, n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     int o = 0;
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
     l.prn = o; o = align16(o + (int)sizeof(T) * b.R * 2 * A * B);
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
-    l.tdl = o; o = align16(o + 8 * b.ntiles);
+    l.tdl = o; o = align16(o + 4 * b.ntiles);
     l.cvn = o; o = align16(o + (int)sizeof(C) * P * nslot * A * B);
-    l.stage = o;
-    if (b.mode == kModeStaged) o = align16(o + (int)sizeof(T) * kRingGroup * b.sc * b.sm);
-    l.per_rp = nslot * FS;
-    l.per_r = P * l.per_rp + kRingSkew;
+    l.per_rp = unit_stride(nslot, FSS);
+    l.per_r = ring_stride(P, l.per_rp);
     l.fbuf = o;
-    l.bbuf = l.stage;
+    l.bbuf = l.fbuf;
     return l;
 }
 
@@ -111,7 +107,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     constexpr int Phi = A * B;
     constexpr int H = Phi / 2 + 1;
     constexpr int BP = B + 1;          // padded row of the pass layout
-    constexpr int FS = A * BP;         // padded transform
+    constexpr int FS = slot_stride(A, B);   // padded transform plus the slot padding
     constexpr int MT = MaxTiles<T>::value;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -125,19 +121,16 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
-    const int sm = bd.sm, sc = bd.sc;
 
     const Layout ly = make_layout<T, A, B>(bd, nslot);
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
     T* prn = reinterpret_cast<T*>(smem + ly.prn);        // [ring][input][longitude n]: P_j^|m(n)|, zero for |m| > j
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
-    int2* tdl = reinterpret_cast<int2*>(smem + ly.tdl);  // per MFMA tile: (weight offset, staged offset) in bytes
+    int* tdl = reinterpret_cast<int*>(smem + ly.tdl);    // per MFMA tile: weight offset in bytes
 
     C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [pair][slot][longitude n]: lifted coefficients, two series
-    T* stage = reinterpret_cast<T*>(smem + ly.stage);    // [ring][column][|m|]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
     T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // MFMA tiles, end phase only
-    const bool gather = bd.mode == kModeGather;
     // transforms of (ring, pair) rp = ring * P + pair
     auto rpbuf = [&](int rp) -> C* {
         return fbuf + (size_t)(rp >> lgP) * ly.per_r + (size_t)(rp & (P - 1)) * ly.per_rp;
@@ -152,7 +145,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     for (int e = tid; e < 3 * n2; e += kThreads) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
     {
         const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
-        for (int e = tid; e < FS; e += kThreads) tw2[e] = tw[e];
+        for (int e = tid; e < A * BP; e += kThreads) tw2[e] = tw[e];
     }
     // Legendre rows of every ring in longitude order: entry n of (ring, input j)
     // is P_j^|m| at the order m = n or n - Phi that longitude index n carries in
@@ -176,7 +169,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
         const TileDesc t = td[u];
-        tdl[u] = make_int2(t.a_off * (int)sizeof(T), gather ? t.b_off : t.b_off * (int)sizeof(T));
+        tdl[u] = t.a_off * (int)sizeof(T);
     }
 
 
@@ -185,20 +178,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
     const int lane_a = ((lane >> 4) * bd.wrow + (lane & 15)) * (int)sizeof(T);
-    // B operand: staging mode reads (ring kq, column i) of the staged spectra;
-    // gather mode reads the in-place analysis output of column i = (sign,
-    // component, pair) at the tile's longitude position of +|m| or -|m|
-    // (columns past the last read column 0; their results are discarded)
+    // B operand: the in-place analysis output of the lane's column
+    // c = 16 ct + i = (sign, component, pair) of the tile's column tile ct at
+    // the longitude position of +|m| or -|m| (columns past the last read
+    // column 0; their results are discarded)
     const int lgC = lgP + (cross ? 2 : 0);   // log2(ncomp * pairs): columns per sign
-    int lane_b, lane_sg = 0;
-    if (!gather) {
-        lane_b = ((lane >> 4) * sc * sm + (lane & 15) * sm) * (int)sizeof(T);
-    } else {
-        const int col = (lane & 15) < (2 << lgC) ? (lane & 15) : 0;
-        const int comp = (col >> lgP) & (ncomp - 1), p = col & (P - 1);
-        lane_sg = col >> lgC;
-        lane_b = (((lane >> 4) * ly.per_r + p * ly.per_rp + (comp >> 1) * FS) * 2 + (comp & 1)) * (int)sizeof(T);
-    }
     // this wave's MFMA tiles: wave w owns w, w + kWaves, ...; per tile the LDS
     // byte address of the lane's B operand at ring 4 h + kq, h = 0
     const int ntw = bd.ntiles > wave ? (bd.ntiles - 1 - wave) / kWaves + 1 : 0;
@@ -208,18 +192,24 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     int bx[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) {
-        const int bo = td[tile_of(s)].b_off;
-        bx[s] = gather ? ly.fbuf + lane_b + (lane_sg ? (bo >> 16) : (bo & 0xffff)) * (int)sizeof(T)
-                       : ly.stage + lane_b + bo * (int)sizeof(T);
+        const TileDesc t = td[tile_of(s)];
+        const int mp = t.code >> 16, ct = t.code & 0xff;
+        int c = 16 * ct + (lane & 15);
+        if (c >= ((mp == 0 ? 1 : 2) << lgC)) c = 0;
+        const int comp = (c >> lgP) & (ncomp - 1), p = c & (P - 1);
+        const int pos = (c >> lgC) ? (t.b_off >> 16) : (t.b_off & 0xffff);
+        bx[s] = ly.fbuf +
+                ((((lane >> 4) * ly.per_r + p * ly.per_rp + (comp >> 1) * FS) * 2 + (comp & 1)) + pos) *
+                    (int)sizeof(T);
     }
     const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
     // (the longitude quadrature and unpacking scales, the products' coupling
     // constants and the sign of negative orders are folded into the output
     // coefficients)
 
-    // gather mode: rings past the last one of the grid are read by the projection
-    // (with zero weight); give them finite contents once
-    if (gather) {
+    // rings past the last one of the grid are read by the projection (with zero
+    // weight); give them finite contents once
+    {
         T* fz = reinterpret_cast<T*>(fbuf);
         for (int e = tid; e < kRingGroup * ly.per_r * 2; e += kThreads) fz[e] = (T)0;
     }
@@ -269,8 +259,6 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         }
         cvn[e] = val;
     }
-    if (!gather)
-        for (int e = tid; e < kRingGroup * sc * sm; e += kThreads) stage[e] = (T)0;
 
     Acc acc[MT];
 #pragma unroll
@@ -421,46 +409,26 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 #pragma unroll
         for (int s = 0; s < MT; ++s) {
             if (s < ntw) {
-                const int ax = tdl[tile_of(s)].x + lane_a;
+                const int ax = tdl[tile_of(s)] + lane_a;
 #pragma unroll
                 for (int h = 0; h < kRingGroup / 4; ++h)
                     apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
             }
         }
-        // ---- 4b. analysis pass 2: in place (gather mode) or staged as |m| <= J
+        // ---- 4b. analysis pass 2, in place
         {
             const int ntask = (uw << lgZ) * B;
             for (int task = lane; task < ntask; task += 64) {
                 const int k2 = task % B;
                 const int f = task / B;
                 const int z = f & (nz - 1), rp = wave + kWaves * (f >> lgZ);
-                const int p = rp & (P - 1), r = rp >> lgP;
                 C* yb = rpbuf(rp) + (size_t)z * FS + k2;
                 C u[A];
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = yb[t * BP];
                 Dft<A, false, C>::run(u);
-                if (gather) {
 #pragma unroll
-                    for (int k1 = 0; k1 < A; ++k1) yb[k1 * BP] = u[k1];
-                } else {
-                    T* st = stage + (size_t)r * sc * sm + (size_t)p * sm;
-                    const int neg = ncomp * P * sm + Phi;   // offset of order -(Phi - k) is neg - k
-#pragma unroll
-                    for (int k1 = 0; k1 < A; ++k1) {
-                        // longitude index k = k2 + B k1: order k if k <= J, order -(Phi - k)
-                        // if k >= Phi - J, else not needed
-                        const int k = k2 + B * k1;
-                        if (k > J && k < Phi - J) continue;
-                        const int off = k <= J ? k : neg - k;
-                        if (!cross) {
-                            st[off] = u[k1].x;
-                        } else {
-                            st[2 * z * P * sm + off] = u[k1].x;
-                            st[(2 * z + 1) * P * sm + off] = u[k1].y;
-                        }
-                    }
-                }
+                for (int k1 = 0; k1 < A; ++k1) yb[k1 * BP] = u[k1];
             }
         }
         lds_barrier();
@@ -472,12 +440,12 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         {
 #pragma unroll
             for (int h = 0; h < kRingGroup / 4; ++h) {
-                const int hofs = h * 4 * (gather ? ly.per_r * (int)sizeof(C) : sc * sm * (int)sizeof(T));
+                const int hofs = h * 4 * ly.per_r * (int)sizeof(C);
                 T bv[MT];
 #pragma unroll
                 for (int s = 0; s < MT; ++s) bv[s] = *reinterpret_cast<const T*>(smem + bx[s] + hofs);
                 // a quad of rings wholly past the grid's last ring adds nothing
-                if (h == 0 || rg0 + 4 < R) {
+                if (h == 0 || rg0 + 4 * h < R) {
 #pragma unroll
                     for (int s = 0; s < MT; ++s)
                         if (s < ntw) acc[s] = mfma16(apre[h][s], bv[s], acc[s]);

@@ -362,23 +362,22 @@ int block_tiles(const BlockDesc& b, int pairs) {
 
 // Dynamic LDS of one work-group; mirrors the kernel's make_layout.
 template <typename T>
-int lds_for(const BlockDesc& b, int pairs, int mode) {
+int lds_for(const BlockDesc& b, int pairs) {
     const int sz = (int)sizeof(T), csz = 2 * sz;
     const bool cross = b.kind == cgtp::kBlockCross;
-    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
+    const int nslot = cross ? 4 : 2;
     const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     const int FS = b.A * (b.B + 1);
+    const int per_r = cgtp::ring_stride(pairs, cgtp::unit_stride(nslot, cgtp::slot_stride(b.A, b.B)));
     int o = 0;
     o = align16h(o + sz * 3 * (n1 + n2));
     o = align16h(o + sz * b.R * 2 * b.Phi);
     o = align16h(o + csz * FS);
-    o = align16h(o + 8 * block_tiles(b, pairs));
+    o = align16h(o + 4 * block_tiles(b, pairs));
     o = align16h(o + csz * pairs * nslot * b.Phi);
-    const int stage = o;
-    const int sc = ((2 * ncomp * pairs + 15) / 16) * 16, sm = (b.J + 1) | 1;
-    if (mode == cgtp::kModeStaged) o = align16h(o + sz * cgtp::kRingGroup * sc * sm);
-    o += csz * cgtp::kRingGroup * (pairs * nslot * FS + 8);   // 8: the ring skew
-    const int end_phase = stage + sz * block_tiles(b, pairs) * cgtp::tile_stride<T>();
+    const int fbuf = o;
+    o += csz * cgtp::kRingGroup * per_r;
+    const int end_phase = fbuf + sz * block_tiles(b, pairs) * cgtp::tile_stride<T>();
     return std::max(o, end_phase);
 }
 
@@ -511,27 +510,19 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             flops += block_flops(j1, j2);
             // pairs per work-group: as many as the accumulator registers and LDS allow
             const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
-            // and whether the projection reads the transforms in place (one MFMA
-            // column tile; no staging buffer) or staged spectra (any number)
             const int ncomp = b.kind == cgtp::kBlockCross ? 4 : 1;
-            auto fits = [&](int P, int mode) {
-                return block_tiles(b, P) <= max_tiles && lds_for<T>(b, P, mode) <= cgtp::kLdsBudget;
+            auto fits = [&](int P) {
+                return block_tiles(b, P) <= max_tiles && lds_for<T>(b, P) <= cgtp::kLdsBudget;
             };
-            int p_gather = 0, p_staged = 0;
-            for (int P = cgtp::kMaxPairs; P >= 1 && !p_gather; P /= 2)
-                if (ncomp * P <= 8 && fits(P, cgtp::kModeGather)) p_gather = P;
-            for (int P = cgtp::kMaxPairs; P >= 1 && !p_staged; P /= 2)
-                if (fits(P, cgtp::kModeStaged)) p_staged = P;
-            if (p_gather == 0 && p_staged == 0) return CGTP_EUNSUP;
-            b.mode = p_gather >= p_staged ? cgtp::kModeGather : cgtp::kModeStaged;
-            const int pairs = b.mode == cgtp::kModeGather ? p_gather : p_staged;
+            int pairs = 0;
+            for (int P = cgtp::kMaxPairs; P >= 1 && !pairs; P /= 2)
+                if (fits(P)) pairs = P;
+            if (pairs == 0) return CGTP_EUNSUP;
             b.pairs = pairs;
             b.lg_pairs = 0;
             while ((1 << b.lg_pairs) < pairs) ++b.lg_pairs;
             b.ntiles = block_tiles(b, pairs);
-            b.lds_bytes = lds_for<T>(b, pairs, b.mode);
-            b.sc = ((2 * ncomp * pairs + 15) / 16) * 16;
-            b.sm = (b.J + 1) | 1;
+            b.lds_bytes = lds_for<T>(b, pairs);
             // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
             b.tdesc_off = (int)h.tdesc.size();
             {
@@ -546,13 +537,9 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                             cgtp::TileDesc t;
                             t.a_off = mp * b.rpad * b.wrow + (l30 - par) / 2;
                             t.rs_nv = nv << 16;
-                            if (b.mode == cgtp::kModeStaged) {
-                                t.b_off = 16 * ct * b.sm + mp;
-                            } else {
-                                // pass-layout positions k + k / B of longitudes +|m| and -|m|
-                                const int kn = (b.Phi - mp) % b.Phi;
-                                t.b_off = 2 * (mp + mp / b.B) | (2 * (kn + kn / b.B)) << 16;
-                            }
+                            // pass-layout positions k + k / B of longitudes +|m| and -|m|
+                            const int kn = (b.Phi - mp) % b.Phi;
+                            t.b_off = 2 * (mp + mp / b.B) | (2 * (kn + kn / b.B)) << 16;
                             t.code = (mp << 16) | (rt << 8) | ct;
                             h.tdesc.push_back(t);
                         }
