@@ -33,9 +33,9 @@ PEAK_HBM_GBS = 8000.0
 # (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
 # change, the figures no longer describe the kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "11760e4f080b1fea": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 382938.0, "fetch_scale": 1.999956, "write_kib": 4872290.0, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 206155.6, "fetch_scale": 1.999956, "write_kib": 2739790.3, "write_scale": 1.000000},
+    "66216a927e9336b4": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 351548.9, "fetch_scale": 1.999956, "write_kib": 4812323.9, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 216943.0, "fetch_scale": 1.999956, "write_kib": 2738911.9, "write_scale": 1.000000},
     },
     "98b2595f487717ca": {
         "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118558.4, "fetch_scale": 1.999956, "write_kib": 2739759.3, "write_scale": 1.000000},
@@ -258,6 +258,30 @@ def time_istp_channels(w, steps, warmup):
     return res
 
 
+def survey_flops_per_pair(L):
+    """Algorithmic flops per pair of the full CGTP on one global exact grid
+    (n_theta = 2L + 2, Phi = 4L + 1, lifts once per input degree, FFT cost
+    2.5 Phi log2 Phi): lift, products, longitude analysis, Legendre projection
+    and recombination, summed over all (l1, l2) blocks."""
+    import math
+    R, Phi, H = L + 1, 4 * L + 1, 2 * L + 1
+    f = 2.5 * Phi * math.log2(Phi) if Phi > 1 else 0.0
+    total = 4 * R * (L + 1) ** 2 + 4 * R * (L + 1) * f
+    T = rec = 0
+    for j1 in range(L + 1):
+        for j2 in range(L + 1):
+            vec = 1 if j1 * j2 > 0 else 0
+            total += R * H * (6 + 60 * vec) + (1 + 3 * vec) * R * f
+            for j3 in range(abs(j1 - j2), j1 + j2 + 1):
+                if (j1 + j2 + j3) % 2 == 0:
+                    T += 2 * j3 + 1
+                    rec += 2 * j3 + 1
+                else:
+                    T += 3 * (2 * j3 - 1)
+                    rec += 7 * (2 * j3 + 1)
+    return total + 2 * R * T + rec
+
+
 def roofline(res):
     flops = res["plan"]["flops_per_pair"] * res["N"]
     t = res["avg_launch_ms"] / 1e3
@@ -265,17 +289,26 @@ def roofline(res):
     peak = PEAK_FP32_TFLOPS if res["dtype"] == "fp32" else PEAK_FP64_TFLOPS
     compulsory = res["plan"]["bytes_per_pair"] * res["N"]
     hbm = compulsory / t / 1e9
+    # the bound of the algorithmic work: arithmetic or HBM time at peak, whichever is longer
+    bound = "alu" if flops / (peak * 1e12) >= compulsory / (PEAK_HBM_GBS * 1e9) else "hbm"
     digest = kernel_digest(res["kind"])
     m = MEASURED_TRAFFIC.get(digest, {}).get(res["workload"])
     traffic = None
     if m is not None:
         traffic = int(m["fetch_kib"] * 1024 * m["fetch_scale"] + m["write_kib"] * 1024 * m["write_scale"])
-    return {"bound": "alu", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": traffic,
+    out = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+           "frac": round(achieved / peak, 4), "traffic": traffic,
             "flops_per_launch": flops, "compulsory_bytes_per_launch": int(compulsory),
             "hbm_gbs_compulsory": round(hbm, 1), "hbm_frac_compulsory": round(hbm / PEAK_HBM_GBS, 4),
             "avg_launch_ms": round(res["avg_launch_ms"], 4), "median_launch_ms": round(res["median_launch_ms"], 4),
             "kernel_digest": digest}
+    if res["kind"] == "cgtp":
+        # the same launch against the work of the method on one global grid
+        fs = survey_flops_per_pair(res["L"]) * res["N"]
+        out["flops_per_launch_survey_model"] = fs
+        out["achieved_survey_model"] = round(fs / t / 1e12, 3)
+        out["frac_survey_model"] = round(fs / t / 1e12 / peak, 4)
+    return out
 
 
 def copy_probe(nbytes, reps=10):

@@ -38,6 +38,9 @@
 #ifndef CGTP_CHANNEL_KERNELS
 #define CGTP_CHANNEL_KERNELS 0
 #endif
+#ifndef CGTP_APRE_AT
+#define CGTP_APRE_AT 2
+#endif
 
 namespace cgtp {
 namespace {
@@ -189,6 +192,18 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     // the tile whose operands slot s loads: the wave's own, or for slots past its
     // last tile (and waves without tiles) a tile of the block, never out of range
     auto tile_of = [&](int s) { return min(wave + kWaves * min(s, max(ntw - 1, 0)), bd.ntiles - 1); };
+    // the MFMA weights (operand A) of this wave's tiles for the ring group at rg0
+    auto prefetch_weights_at = [&](T (&ap)[kRingGroup / 4][MT], int rg) {
+#pragma unroll
+        for (int s = 0; s < MT; ++s) {
+            if (s < ntw) {
+                const int ax = tdl[tile_of(s)] + lane_a;
+#pragma unroll
+                for (int h = 0; h < kRingGroup / 4; ++h)
+                    ap[h][s] = buffer_load<T>(wrsrc, ax, (rg + 4 * h) * bd.wrow * (int)sizeof(T));
+            }
+        }
+    };
     int bx[MT];
 #pragma unroll
     for (int s = 0; s < MT; ++s) {
@@ -213,10 +228,10 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         T* fz = reinterpret_cast<T*>(fbuf);
         for (int e = tid; e < kRingGroup * ly.per_r * 2; e += kThreads) fz[e] = (T)0;
     }
+    const bool x2s = CH && (ch.flags & kX2Shared);
     // the couplings (lc) are read by other waves in the first tile's lift fill
     lds_barrier();
 
-    const bool x2s = CH && (ch.flags & kX2Shared);
     for (int64_t pt = pt0; pt < pt1; ++pt) {
     const int64_t p0 = pt * P;
     const int np = (int)((N - p0) < P ? (N - p0) : P);
@@ -271,6 +286,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         // ... and takes each of them through synthesis, products and analysis, so
         // between these phases only its own LDS accesses need ordering.
         const int nunit = nrg << lgP;
+        auto prefetch_weights = [&](T (&ap)[kRingGroup / 4][MT]) { prefetch_weights_at(ap, rg0); };
         const int uw = nunit > wave ? (nunit - 1 - wave) / kWaves + 1 : 0;   // units of this wave
 
         // ---- 1. lift + synthesis pass 1: task ((unit, slot), t) -> row t
@@ -322,6 +338,10 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         wave_lds_sync();
+#if CGTP_APRE_AT == 2
+        T apre[kRingGroup / 4][MT];
+        prefetch_weights(apre);
+#endif
         // ---- 3. pointwise products on half the circle, mirrored
         {
             const int ntask = uw * H;
@@ -377,6 +397,10 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         wave_lds_sync();
+#if CGTP_APRE_AT == 1
+        T apre[kRingGroup / 4][MT];
+        prefetch_weights(apre);
+#endif
         // ---- 4a. analysis pass 1: task ((unit, z), t); rows into slot z
         {
             const int ntask = (uw << lgZ) * A;
@@ -402,19 +426,13 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         wave_lds_sync();
+#if CGTP_APRE_AT == 0
         // the group's MFMA weights (operand A) are fetched now and land during the
         // last transform pass (fetched earlier they would hold registers through
         // the register peak of the row passes)
         T apre[kRingGroup / 4][MT];
-#pragma unroll
-        for (int s = 0; s < MT; ++s) {
-            if (s < ntw) {
-                const int ax = tdl[tile_of(s)] + lane_a;
-#pragma unroll
-                for (int h = 0; h < kRingGroup / 4; ++h)
-                    apre[h][s] = buffer_load<T>(wrsrc, ax, (rg0 + 4 * h) * bd.wrow * (int)sizeof(T));
-            }
-        }
+        prefetch_weights(apre);
+#endif
         // ---- 4b. analysis pass 2, in place
         {
             const int ntask = (uw << lgZ) * B;
@@ -476,7 +494,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     lds_barrier();
     {
         const int nblk = n1 * n2;
-        T* ob = out + p0 * nout + bd.out_off;
+        T* const ob = out + p0 * nout + bd.out_off;
         // the next output's coefficients are loaded while this one is stored
         Coef4 cfn{};
         int4 ixn{};
@@ -492,30 +510,20 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 ixn = coefi[o + kThreads];
             }
             const bool one = ix.w & 1;   // scalar-scalar or dot path: one term
-            // four rows at a time (row p's entries are 4 p further on)
-            for (int pb = 0; pb < np; pb += 4) {
-                T v0[4], v1[4], v2[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int po = 4 * min(pb + u, np - 1);
-                    v0[u] = bbuf[ix.x + po];
-                    v1[u] = one ? (T)0 : bbuf[ix.y + po];
-                    v2[u] = one ? (T)0 : bbuf[ix.z + po];
+            const T* e0 = bbuf + ix.x;    // the terms' entries for row 0; row p's are 4 p further on
+            const T* e1 = bbuf + ix.y;
+            const T* e2 = bbuf + ix.z;
+            const T* wq = wl + (ix.w >> 1);   // weight of this output's path, row p at nbp p
+            // two rows at a time; each row's store goes through a wave-uniform row pointer
+#pragma unroll 2
+            for (int p = 0; p < np; ++p) {
+                T z = cf.x * e0[4 * p];
+                if (!one) z += cf.y * e1[4 * p] + cf.z * e2[4 * p];
+                if constexpr (CH) {
+                    if (ch.w) z *= wq[p * nbp];
                 }
-                if constexpr (!CH) {
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (pb + u < np)
-                            ob[(size_t)(pb + u) * nout + o] = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
-                } else {
-                    const T* wq = wl + (ix.w >> 1);   // weight of this output's path, row pb + u at nbp (pb + u)
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (pb + u < np) {
-                            const T z = cf.x * v0[u] + cf.y * v1[u] + cf.z * v2[u];
-                            ob[(size_t)(pb + u) * nout + o] = ch.w ? wq[(pb + u) * nbp] * z : z;
-                        }
-                }
+                T* orow = ob + (int64_t)p * nout;
+                orow[o] = z;
             }
         }
     }

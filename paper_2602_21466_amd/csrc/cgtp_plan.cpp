@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -297,7 +298,9 @@ int64_t path_index(int L, int l1, int l2, int l3) {
 inline int wtab_rpad(int R) { return (R + cgtp::kRingGroup - 1) / cgtp::kRingGroup * cgtp::kRingGroup; }
 inline int wtab_rowlen(int lmax, int par) { return lmax >= par ? (lmax - par) / 2 + 1 : 1; }
 
-// Algorithmic flops of one block on its minimal exact grid (default cover).
+// Algorithmic flops of one block on its minimal exact grid (default cover),
+// without the lifts: those are counted once per input, degree and grid by
+// lift_flops, however many blocks of the grid use them.
 double block_flops(int j1, int j2) {
     const int J = j1 + j2, d = std::abs(j1 - j2);
     const double R = J / 2 + 1, Phi = 2 * J + 1, H = J + 1;
@@ -309,12 +312,20 @@ double block_flops(int j1, int j2) {
         if (((J + j3) & 1) == 0) { T += 2 * j3 + 1; rec += 2 * j3 + 1; }
         else { T += 3 * (2 * (j3 - 1) + 1); rec += 7 * (2 * j3 + 1); }
     }
-    return R * (2 * j1 + 1 + 2 * j2 + 1) * nin   // lift, latitude stage
-         + 2 * nin * R * f                       // lift, longitude synthesis
-         + R * H * (6 + (vec ? 60 : 0))          // pointwise products
+    return R * H * (6 + (vec ? 60 : 0))          // pointwise products
          + nin * R * f                           // longitude analysis
          + 2 * R * T                             // Legendre projection
          + rec;                                  // recombination and 1/K
+}
+
+// Flops of lifting one input of degree j (nin series: 1 scalar, 4 scalar +
+// vector) to a grid of R north rings that blocks up to degree Jmax share:
+// latitude stage and longitude synthesis on the minimal exact longitudes
+// 2 Jmax + 1.
+double lift_flops(int j, int R, int Jmax, int nin) {
+    const double Phi = 2 * Jmax + 1;
+    const double f = Phi > 1 ? 2.5 * Phi * std::log2(Phi) : 0.0;
+    return (double)R * (2 * j + 1) * nin + (double)nin * R * f;
 }
 
 }  // namespace
@@ -468,6 +479,8 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
     p->dot_cg = (double)dc;
     // ---- blocks
     double min_abs_K = 1e300, flops = 0;
+    // lifts: (input, degree, n_theta, Phi) -> (north rings, largest J of the grid, series)
+    std::map<std::array<int, 4>, std::array<int, 3>> lifts;
     blocks.clear();
     for (int j1 = 0; j1 <= L; ++j1)
         for (int j2 = 0; j2 <= L; ++j2) {
@@ -508,6 +521,15 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.out_off = path_offset(L, j1, j2, b.d);
             b.path_off = (int32_t)path_index(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
+            {
+                const int nin = b.kind == cgtp::kBlockCross ? 4 : 1;
+                for (int in = 0; in < 2; ++in) {
+                    auto& e = lifts[std::array<int, 4>{in, in ? j2 : j1, nt, np}];
+                    e[0] = b.R;
+                    e[1] = std::max(e[1], b.J);
+                    e[2] = std::max(e[2], nin);
+                }
+            }
             // pairs per work-group: as many as the accumulator registers and LDS allow
             const int max_tiles = cgtp::kWaves * cgtp::MaxTiles<T>::value;
             const int ncomp = b.kind == cgtp::kBlockCross ? 4 : 1;
@@ -614,6 +636,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             blocks.push_back(b);
         }
     p->min_abs_K = min_abs_K;
+    for (const auto& kv : lifts) flops += lift_flops(kv.first[1], kv.second[0], kv.second[1], kv.second[2]);
     p->flops_per_pair = flops;
     p->bytes_per_pair = (double)sizeof(T) * (2.0 * (L + 1) * (L + 1) + std::pow((double)(L + 1), 4));
     // ---- launch classes: fewest pairs (heaviest blocks) first; inside, by cost
