@@ -41,7 +41,8 @@ enum cgtp_status {
     CGTP_EDTYPE = -3, /* unknown dtype */
     CGTP_ENOMEM = -4, /* host or device allocation failed */
     CGTP_EHIP = -5,   /* a HIP runtime call failed; cgtp_last_hip_error() has the HIP code */
-    CGTP_EUNSUP = -6  /* valid request this build does not support (L above CGTP_MAX_L, FFT size) */
+    CGTP_EUNSUP = -6, /* valid request this build does not support (L above CGTP_MAX_L, FFT size) */
+    CGTP_ESCRATCH = -7 /* request larger than a no-allocation entry point's static scratch */
 };
 
 enum cgtp_dtype { CGTP_FP32 = 0, CGTP_FP64 = 1 };

@@ -158,6 +158,24 @@ int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *ou
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
 
 /*
+ * istp_forward_real for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same conversions and products, with the workspace taken
+ * from a static device array of ISTP_STATIC_SCRATCH_BYTES (64 MiB) that the
+ * library holds on each GPU it runs on until the process ends.  Same
+ * arguments and rules as istp_forward_real without the workspace; the plan's
+ * device must be current.  CGTP_ESCRATCH when istp_real_workspace_bytes(plan,
+ * N) exceeds the array (in fp32: above 4288 pairs at L = 16, 1119 at L = 32).  The
+ * entry point calls no allocating routine; every call on a GPU shares that
+ * GPU's array, so calls that overlap in time on one GPU (concurrent streams)
+ * race and must be ordered by the caller.  Nothing in the array needs to
+ * start at zero.
+ */
+#define ISTP_STATIC_SCRATCH_BYTES (64LL << 20)
+int istp_forward_real_static(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N,
+                             void *hip_stream);
+
+/*
  * Gradients of sum(grad_out * out) for istp_forward_real, in the real basis.
  * The integrals of three real harmonics are fully symmetric, so
  *   grad_x1 = Q(grad_out, x2),  grad_x2 = Q(grad_out, x1),

@@ -21,6 +21,7 @@ import numpy as np
 from ._build import LIB as _LIB_PATH
 
 CGTP_OK, CGTP_EINVAL, CGTP_EGRID, CGTP_EDTYPE, CGTP_ENOMEM, CGTP_EHIP, CGTP_EUNSUP = 0, -1, -2, -3, -4, -5, -6
+CGTP_ESCRATCH = -7
 CGTP_FP32, CGTP_FP64 = 0, 1
 CGTP_COVER_DEFAULT, CGTP_COVER_ALTERNATE = 0, 1
 CGTP_MAX_L = 32
@@ -89,6 +90,7 @@ def _load():
         "istp_num_labels": (i64, [i32, i32]),
         "istp_forward_real": (ctypes.c_int, [vp, vp, vp, vp, i64, vp, i64, vp]),
         "istp_real_workspace_bytes": (i64, [vp, i64]),
+        "istp_forward_real_static": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
         "istp_backward_real": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
         "istp_real_backward_workspace_bytes": (i64, [vp, i64]),
         "istp_backward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64,
@@ -117,7 +119,7 @@ def exported_symbols():
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index",
-            "istp_forward_real", "istp_real_workspace_bytes", "istp_backward_real",
+            "istp_forward_real", "istp_real_workspace_bytes", "istp_forward_real_static", "istp_backward_real",
             "istp_real_backward_workspace_bytes", "istp_backward_weighted", "istp_destroy", "istp_num_inputs", "istp_num_outputs", "istp_label_offset",
             "istp_plan_query", "istp_plan_describe", "istp_backward", "istp_backward_query"]
 
@@ -267,6 +269,14 @@ def istp_forward_real(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, ws_p
                                    int(N), ctypes.c_void_p(ws_ptr) if ws_ptr else None, int(ws_bytes),
                                    ctypes.c_void_p(stream_ptr) if stream_ptr else None)
     _check(rc, "istp_forward_real")
+
+
+def istp_forward_real_static(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int,
+                             stream_ptr: int | None = None) -> None:
+    rc = _load().istp_forward_real_static(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr),
+                                          ctypes.c_void_p(out_ptr), int(N),
+                                          ctypes.c_void_p(stream_ptr) if stream_ptr else None)
+    _check(rc, "istp_forward_real_static")
 
 
 def istp_real_workspace_bytes(plan, N: int) -> int:

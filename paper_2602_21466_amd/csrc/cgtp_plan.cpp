@@ -736,6 +736,7 @@ const char* cgtp_strerror(int code) {
         case CGTP_ENOMEM: return "out of memory";
         case CGTP_EHIP: return "HIP runtime error";
         case CGTP_EUNSUP: return "unsupported by this build";
+        case CGTP_ESCRATCH: return "request exceeds the static scratch of a no-allocation entry point";
         default: return "unknown status";
     }
 }

@@ -16,7 +16,10 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 
+#include "../../include/istp.h"
+#include "cgtp_internal.h"
 #include "istp_internal.h"
 
 namespace istp {
@@ -130,3 +133,55 @@ int launch_real_from_complex_f64(double* out, const double* pbb, const double* p
 }
 
 }  // namespace istp
+
+// ---------------------------------------------------------------- no-allocation entry point
+//
+// The workspace of istp_forward_real_static: one static array per device.  In
+// host code the array's name is a host-side stand-in, not a device address;
+// its device address is looked up once per device (with that device current)
+// and only that address is ever passed to kernels.
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[ISTP_STATIC_SCRATCH_BYTES];
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, or an error code.
+int scratch_address(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        cgtp::set_last_hip_error((int)e);
+        return CGTP_EHIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return CGTP_EUNSUP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            cgtp::set_last_hip_error((int)e);
+            return CGTP_EHIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return CGTP_OK;
+}
+
+}  // namespace
+
+extern "C" int istp_forward_real_static(istp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N,
+                                        void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (N == 0) return istp_forward_real(plan, x1, x2, out, 0, nullptr, 0, hip_stream);
+    const int64_t need = istp_real_workspace_bytes(plan, N);
+    if (need < 0) return istp_forward_real(plan, x1, x2, out, N, nullptr, 0, hip_stream);   // its own error
+    if (need > ISTP_STATIC_SCRATCH_BYTES) return CGTP_ESCRATCH;
+    void* ws = nullptr;
+    const int rc = scratch_address(&ws);
+    if (rc != CGTP_OK) return rc;
+    return istp_forward_real(plan, x1, x2, out, N, ws, ISTP_STATIC_SCRATCH_BYTES, hip_stream);
+}

@@ -1,0 +1,74 @@
+"""The no-allocation entry point istp_forward_real_static against istp_forward_real
+(same kernels, caller-allocated workspace), through the C ABI, on two calls in a
+row (the second with fewer pairs, reusing the static scratch the first one left
+behind), and its size limit."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import cgtp_inputs
+import oracle.istp as oi
+
+pytestmark = pytest.mark.gpu
+
+
+def _setup():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_21466_amd as lib
+    return torch, lib
+
+
+def _rel(a, b):
+    a = a.double().cpu().numpy()
+    b = b.double().cpu().numpy()
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+@pytest.mark.parametrize("L,N1,N2,dtype", [(16, 2000, 500, "fp32"), (5, 300, 37, "fp32"), (4, 50, 9, "fp64")])
+def test_static_scratch_matches_workspace_entry_point(L, N1, N2, dtype):
+    torch, lib = _setup()
+    plan = lib.IstpPlan(L, lib.ISTP_GAUNT, dtype)
+    tdt = torch.float32 if dtype == "fp32" else torch.float64
+    s = torch.cuda.current_stream().cuda_stream
+    for n, seed in ((N1, 11), (N2, 12)):
+        x1, x2 = cgtp_inputs.draw_rows(oi.gaunt_size(L), n, dtype, seed=seed + L)
+        a, b = x1.cuda(), x2.cuda()
+        ref = plan.forward_real(a, b)
+        out = torch.full((n, plan.nout), float("nan"), dtype=tdt, device="cuda")
+        lib.istp_forward_real_static(plan._h, a.data_ptr(), b.data_ptr(), out.data_ptr(), n, s)
+        torch.cuda.synchronize()
+        err = _rel(out, ref)
+        print("L=%d N=%d %s: static vs workspace entry point rel L2 %.3e, identical %s"
+              % (L, n, dtype, err, torch.equal(out, ref)), flush=True)
+        assert torch.isfinite(out).all().item()
+        assert err <= (1e-6 if dtype == "fp32" else 1e-13)
+        # and the oracle on a few rows, at the parity bar of the real-basis product
+        k = min(n, 3)
+        want = oi.gaunt_tp_real(L, x1[:k].double().numpy(), x2[:k].double().numpy())
+        got = out[:k].double().cpu().numpy()
+        assert np.linalg.norm(got - want) / np.linalg.norm(want) <= (1e-4 if dtype == "fp32" else 1e-10)
+
+
+def test_static_scratch_size_limit():
+    torch, lib = _setup()
+    L = 16
+    plan = lib.IstpPlan(L, lib.ISTP_GAUNT, "fp32")
+    limit = max(n for n in (4288, 4289) if lib.istp_real_workspace_bytes(plan._h, n) <= (64 << 20))
+    assert limit == 4288
+    n = limit + 1
+    x = torch.zeros(n, plan.nin, device="cuda")
+    out = torch.full((n, plan.nout), 5.0, device="cuda")
+    rc = lib._load().istp_forward_real_static(plan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                                             ctypes.c_void_p(out.data_ptr()), n, None)
+    assert rc == lib.CGTP_ESCRATCH
+    assert lib.cgtp_strerror(rc)
+    torch.cuda.synchronize()
+    assert (out == 5.0).all().item()
+    # spin 1 plans have no real-basis product
+    vplan = lib.IstpPlan(3, lib.ISTP_VECTOR, "fp32")
+    rc = lib._load().istp_forward_real_static(vplan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                                             ctypes.c_void_p(out.data_ptr()), 2, None)
+    assert rc == lib.CGTP_EUNSUP
