@@ -75,6 +75,7 @@ struct alignas(16) BlockDesc {
     int32_t rpad;              // rings of the weight table: R rounded up to the ring group
     int32_t wrow;              // entries per ring row of the weight table
     int32_t path_off;          // index of path (j1, j2, |j1 - j2|) in the (l1, l2, l3) order of all paths
+    int32_t x2share;           // channel kernel: LDS holds a shared second-input buffer (x2_bytes) beside the working set
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
@@ -157,6 +158,11 @@ __host__ __device__ constexpr int unit_stride(int nslot, int fs) {
 __host__ __device__ constexpr int ring_stride(int pairs, int per_rp) {
     return CGTP_PAD ? pairs * per_rp + (((pairs <= 4 ? 2 * pairs : 1) - pairs * per_rp) & 15) : pairs * per_rp + 8;
 }
+
+// Channel-wise launches with a shared second input synthesise it once per
+// ring into a buffer of its own: half the transforms of a unit, per ring of
+// the ring group (complex entries).
+__host__ __device__ constexpr int x2buf_entries(int nslot, int fs, int rings) { return rings * (nslot / 2) * fs; }
 
 // End phase: MFMA tile u of a block is dumped at u * tile_stride<T>() elements;
 // the padding keeps consecutive tiles on different LDS banks.

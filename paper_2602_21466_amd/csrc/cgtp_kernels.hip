@@ -67,7 +67,7 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // ring_stride) so that the MFMA operands read in place spread over the banks.
 
 struct Layout {
-    int lc, prn, tw2, tdl, cvn, fbuf, bbuf;   // byte offsets
+    int lc, prn, tw2, tdl, cvn, x2b, fbuf, bbuf;   // byte offsets
     int per_rp;                                      // complex entries per (ring, pair)
     int per_r;                                       // complex entries per ring
 };
@@ -78,7 +78,7 @@ __device__ __forceinline__ int align16(int v) { return (v + 15) & ~15; }
 // MFMA tile table), then the tile's lifted coefficients, then the per-ring
 // working set; the end phase reuses the working set for the accumulators.
 template <typename T, int A, int B>
-__device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
+__device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, bool x2buf) {
     using C = typename Cplx<T>::type;
     constexpr int FS = A * (B + 1);
     constexpr int FSS = slot_stride(A, B);
@@ -90,6 +90,8 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot) {
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.tdl = o; o = align16(o + 4 * b.ntiles);
     l.cvn = o; o = align16(o + (int)sizeof(C) * P * nslot * A * B);
+    l.x2b = o;
+    if (x2buf) o = align16(o + (int)sizeof(C) * x2buf_entries(nslot, FSS, kRingGroup));
     l.per_rp = unit_stride(nslot, FSS);
     l.per_r = ring_stride(P, l.per_rp);
     l.fbuf = o;
@@ -125,7 +127,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
 
-    const Layout ly = make_layout<T, A, B>(bd, nslot);
+    const Layout ly = make_layout<T, A, B>(bd, nslot, CH && bd.x2share);
+    // channel-wise launch whose rows of a tile all share one second input: its
+    // lift is synthesised once per ring, into a buffer of its own
+    const bool xsh = CH && bd.x2share && (ch.flags & kX2Shared) && ch.channels % P == 0;
+    C* x2buf = reinterpret_cast<C*>(smem + ly.x2b);      // [ring][second-input slot], pass layout
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
     T* prn = reinterpret_cast<T*>(smem + ly.prn);        // [ring][input][longitude n]: P_j^|m(n)|, zero for |m| > j
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
@@ -289,14 +295,42 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         auto prefetch_weights = [&](T (&ap)[kRingGroup / 4][MT]) { prefetch_weights_at(ap, rg0); };
         const int uw = nunit > wave ? (nunit - 1 - wave) / kWaves + 1 : 0;   // units of this wave
 
-        // ---- 1. lift + synthesis pass 1: task ((unit, slot), t) -> row t
+        // Transforms of this wave: every slot of its units or, with a shared second
+        // input, its units' first-input slots and its share of the group's
+        // second-input transforms (one per ring and slot, from pair 0's lift),
+        // dealt from the last wave down: waves with the most units come first in
+        // the unit order, so the totals even out.
+        const int lgH = lgS - 1;   // log2 of the slots per input
+        const int nx2 = xsh ? nrg << lgH : 0;
+        const int q0 = kWaves - 1 - wave;
+        const int nx2w = nx2 > q0 ? (nx2 - 1 - q0) / kWaves + 1 : 0;
+        const int ntr = xsh ? (uw << lgH) + nx2w : uw << lgS;
+        auto tr_of = [&](int f, int& rp, int& s) {
+            if (!xsh) {
+                rp = wave + kWaves * (f >> lgS);
+                s = f & (nslot - 1);
+            } else if (f < (uw << lgH)) {
+                rp = wave + kWaves * (f >> lgH);
+                s = f & ((1 << lgH) - 1);
+            } else {
+                const int q = q0 + kWaves * (f - (uw << lgH));
+                rp = (q >> lgH) << lgP;
+                s = (1 << lgH) + (q & ((1 << lgH) - 1));
+            }
+        };
+        // slot s of unit rp (the shared buffer holds the second input's slots)
+        auto slotp = [&](int rp, int s) -> C* {
+            if (xsh && s >= (1 << lgH)) return x2buf + (size_t)(((rp >> lgP) << lgH) + s - (1 << lgH)) * FS;
+            return rpbuf(rp) + (size_t)s * FS;
+        };
+        // ---- 1. lift + synthesis pass 1: task (transform, t) -> row t
         {
-            const int ntask = (uw << lgS) * A;
+            const int ntask = ntr * A;
             for (int task = lane; task < ntask; task += 64) {
                 const int t = task % A;
                 const int f = task / A;
-                const int s = f & (nslot - 1);
-                const int rp = wave + kWaves * (f >> lgS);
+                int rp, s;
+                tr_of(f, rp, s);
                 const int p = rp & (P - 1), r = rp >> lgP;
                 const bool first = cross ? (s < 2) : (s == 0);
                 // inputs n = t + A n2i: both factors in longitude order, read at
@@ -311,7 +345,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     v[n2i] = cmk<C>(c.x * pv, c.y * pv);
                 }
                 Dft<B, true, C>::run(v);
-                C* row = rpbuf(rp) + (size_t)s * FS + t * BP;
+                C* row = slotp(rp, s) + t * BP;
                 // all twiddles first: the row stores may not be moved above them
                 const C* twr = tw2 + t * BP;
                 C w[B];
@@ -322,13 +356,15 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             }
         }
         wave_lds_sync();
-        // ---- 2. synthesis pass 2 (in place): task ((unit, slot), column k2)
+        // ---- 2. synthesis pass 2 (in place): task (transform, column k2)
         {
-            const int ntask = (uw << lgS) * B;
+            const int ntask = ntr * B;
             for (int task = lane; task < ntask; task += 64) {
                 const int k2 = task % B;
                 const int f = task / B;
-                C* fb = rpbuf(wave + kWaves * (f >> lgS)) + (size_t)(f & (nslot - 1)) * FS + k2;
+                int rp, s;
+                tr_of(f, rp, s);
+                C* fb = slotp(rp, s) + k2;
                 C u[A];
 #pragma unroll
                 for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
@@ -337,7 +373,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
             }
         }
-        wave_lds_sync();
+        // the shared transforms were made by other waves
+        if (xsh)
+            lds_barrier();
+        else
+            wave_lds_sync();
 #if CGTP_APRE_AT == 2
         T apre[kRingGroup / 4][MT];
         prefetch_weights(apre);
@@ -353,7 +393,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 // n and -n are read and written by this task only
                 C* fb = rpbuf(rp);
                 if (!cross) {
-                    const C g = cmul(fb[pn], fb[FS + pn]);
+                    const C g = cmul(fb[pn], slotp(rp, 1)[pn]);
                     fb[FS + pn] = g;
                     fb[FS + pk] = cconj(g);
                 } else {
@@ -361,7 +401,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     C f[8];
 #pragma unroll
                     for (int s = 0; s < 4; ++s) {
-                        const C Fn = fb[s * FS + pn], Fk = fb[s * FS + pk];
+                        const C* fs = slotp(rp, s);
+                        const C Fn = fs[pn], Fk = fs[pk];
                         f[2 * s] = cmk<C>(Fn.x + Fk.x, Fn.y - Fk.y);
                         f[2 * s + 1] = cmk<C>(Fn.y + Fk.y, Fk.x - Fn.x);
                     }

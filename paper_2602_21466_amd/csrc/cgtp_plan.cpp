@@ -343,7 +343,8 @@ struct cgtp_plan_s {
     const int32_t* d_list = nullptr;   // block indices grouped by pairs-per-work-group
     struct Cls { int pairs; int off; int count; };
     std::vector<Cls> classes;
-    int lds_bytes = 0;
+    int lds_bytes = 0;      // dynamic LDS of the plain kernel
+    int lds_bytes_ch = 0;   // and of the channel kernel (with the shared second-input buffers)
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
     double cross_cg = 0, dot_cg = 0;
@@ -373,7 +374,7 @@ int block_tiles(const BlockDesc& b, int pairs) {
 
 // Dynamic LDS of one work-group; mirrors the kernel's make_layout.
 template <typename T>
-int lds_for(const BlockDesc& b, int pairs) {
+int lds_for(const BlockDesc& b, int pairs, bool x2buf = false) {
     const int sz = (int)sizeof(T), csz = 2 * sz;
     const bool cross = b.kind == cgtp::kBlockCross;
     const int nslot = cross ? 4 : 2;
@@ -386,6 +387,7 @@ int lds_for(const BlockDesc& b, int pairs) {
     o = align16h(o + csz * FS);
     o = align16h(o + 4 * block_tiles(b, pairs));
     o = align16h(o + csz * pairs * nslot * b.Phi);
+    if (x2buf) o = align16h(o + csz * cgtp::x2buf_entries(nslot, cgtp::slot_stride(b.A, b.B), cgtp::kRingGroup));
     const int fbuf = o;
     o += csz * cgtp::kRingGroup * per_r;
     const int end_phase = fbuf + sz * block_tiles(b, pairs) * cgtp::tile_stride<T>();
@@ -545,6 +547,10 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             while ((1 << b.lg_pairs) < pairs) ++b.lg_pairs;
             b.ntiles = block_tiles(b, pairs);
             b.lds_bytes = lds_for<T>(b, pairs);
+            // the channel kernel's shared second-input buffer, where it fits
+            const int lds_x2 = lds_for<T>(b, pairs, true);
+            b.x2share = lds_x2 <= cgtp::kLdsBudget ? 1 : 0;
+            p->lds_bytes_ch = std::max(p->lds_bytes_ch, b.x2share ? lds_x2 : b.lds_bytes);
             // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
             b.tdesc_off = (int)h.tdesc.size();
             {
@@ -918,14 +924,14 @@ int forward_rows(cgtp_plan_t plan, const void* x1, const void* x2, const void* w
         const cgtp::ChanArgs<float> ch{(const float*)w, channels, flags, (int32_t)npaths};
         err = plain ? cgtp::launch_blocks_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
                                               (const float*)x2, (float*)out, N, L, hip_stream)
-                    : cgtp::launch_blocks_channels_f32(plan->tf, plan->d_list, map, plan->lds_bytes,
+                    : cgtp::launch_blocks_channels_f32(plan->tf, plan->d_list, map, plan->lds_bytes_ch,
                                                        (const float*)x1, (const float*)x2, (float*)out, N, L, ch,
                                                        hip_stream);
     } else {
         const cgtp::ChanArgs<double> ch{(const double*)w, channels, flags, (int32_t)npaths};
         err = plain ? cgtp::launch_blocks_f64(plan->td, plan->d_list, map, plan->lds_bytes, (const double*)x1,
                                               (const double*)x2, (double*)out, N, L, hip_stream)
-                    : cgtp::launch_blocks_channels_f64(plan->td, plan->d_list, map, plan->lds_bytes,
+                    : cgtp::launch_blocks_channels_f64(plan->td, plan->d_list, map, plan->lds_bytes_ch,
                                                        (const double*)x1, (const double*)x2, (double*)out, N, L,
                                                        ch, hip_stream);
     }
