@@ -53,6 +53,8 @@ def _load():
     lib.oracle_num_outputs.argtypes = [ctypes.c_int]
     lib.oracle_path_offset.restype = ctypes.c_int64
     lib.oracle_path_offset.argtypes = [ctypes.c_int] * 4
+    lib.oracle_cgtp_backward.restype = ctypes.c_int
+    lib.oracle_cgtp_backward.argtypes = [ctypes.c_int, ctypes.c_int64] + [ctypes.c_void_p] * 5 + [ctypes.c_int]
     lib.oracle_table_build_seconds.restype = ctypes.c_double
     lib.oracle_table_build_seconds.argtypes = []
     lib.oracle_max_threads.restype = ctypes.c_int
@@ -100,6 +102,26 @@ def cgtp(L: int, x1, x2, threads: int = 0) -> np.ndarray:
     if rc != 0:
         raise RuntimeError("oracle_cgtp failed (L=%d, N=%d)" % (L, n))
     return out
+
+
+def cgtp_backward(L: int, x1, x2, g, threads: int = 0):
+    """Gradients (gx1, gx2) of sum(g * cgtp(L, x1, x2)) in fp64: the derivative of the bilinear map by its
+    definition, written out term by term (cgtp_oracle.c).  x1, x2: [N, (L+1)^2]; g: [N, (L+1)^4]."""
+    a = np.ascontiguousarray(np.asarray(x1, dtype=np.float64))
+    b = np.ascontiguousarray(np.asarray(x2, dtype=np.float64))
+    gz = np.ascontiguousarray(np.asarray(g, dtype=np.float64))
+    if a.ndim == 1:
+        a, b, gz = a[None], b[None], gz[None]
+    n = a.shape[0]
+    if a.shape != b.shape or a.shape[1] != (L + 1) ** 2 or gz.shape != (n, num_outputs(L)):
+        raise ValueError("x1, x2 must be [N, (L+1)^2] and g [N, (L+1)^4]")
+    ga = np.empty_like(a)
+    gb = np.empty_like(b)
+    rc = _load().oracle_cgtp_backward(L, n, a.ctypes.data, b.ctypes.data, gz.ctypes.data, ga.ctypes.data,
+                                      gb.ctypes.data, int(threads))
+    if rc != 0:
+        raise RuntimeError("oracle_cgtp_backward failed (L=%d, N=%d)" % (L, n))
+    return ga, gb
 
 
 def cgtp_complex(L: int, x1, x2, threads: int = 0) -> np.ndarray:

@@ -31,6 +31,9 @@
  *     * sum_k (-1)^k / [k! (j1+j2-j-k)! (j1-m1-k)! (j2+m2-k)!
  *                       (j-j2+m1+k)! (j-j1-m2+k)!]
  *
+ * The gradients of the CGTP (oracle_cgtp_backward) are the same double sum
+ * differentiated term by term by x1 and by x2.
+ *
  * Arithmetic: products are accumulated in double (fp64).
  */
 #include <math.h>
@@ -207,6 +210,57 @@ int oracle_cgtp(int L, int64_t N, const double *x1, const double *x2, double *ou
                     }
                 }
         }
+    return 0;
+}
+
+/*
+ * Gradients of the full CGTP: for an upstream gradient g = dLoss/dz of the
+ * same layout as z, the plain definition of the derivative of the bilinear
+ * map written out (each term of the double sum above, differentiated by x1
+ * and by x2):
+ *
+ *   gx1[n, l1^2+l1+m1] = sum over paths (l1, l2, l3), m2:
+ *                          C^{l3, m1+m2}_{l1 m1 l2 m2} g[n, path, m1+m2] x2[n, l2^2+l2+m2]
+ *   gx2[n, l2^2+l2+m2] = sum over paths (l1, l2, l3), m1:
+ *                          C^{l3, m1+m2}_{l1 m1 l2 m2} g[n, path, m1+m2] x1[n, l1^2+l1+m1]
+ *
+ * x1, x2, gx1, gx2: [N, (L+1)^2]; g: [N, (L+1)^4]; fp64.  Either output may
+ * be NULL.  Returns 0 on success, -1 on bad arguments or allocation failure.
+ */
+int oracle_cgtp_backward(int L, int64_t N, const double *x1, const double *x2, const double *g, double *gx1,
+                         double *gx2, int nthreads) {
+    if (L < 0 || L > ORACLE_MAX_L || N < 0) return -1;
+    if (N == 0) return 0;
+    if (!x1 || !x2 || !g) return -1;
+    if (ensure_table(L, nthreads) != 0) return -1;
+    const int64_t nin = (int64_t)(L + 1) * (L + 1);
+    const int64_t nout = oracle_num_outputs(L);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t n = 0; n < N; ++n) {
+        const double *a = x1 + n * nin;
+        const double *b = x2 + n * nin;
+        const double *gz = g + n * nout;
+        double *ga = gx1 ? gx1 + n * nin : NULL;
+        double *gb = gx2 ? gx2 + n * nin : NULL;
+        if (ga) memset(ga, 0, sizeof(double) * nin);
+        if (gb) memset(gb, 0, sizeof(double) * nin);
+        for (int l1 = 0; l1 <= L; ++l1)
+            for (int l2 = 0; l2 <= L; ++l2)
+                for (int l3 = iabs_(l1 - l2); l3 <= l1 + l2; ++l3) {
+                    const int64_t base = oracle_path_offset(L, l1, l2, l3);
+                    for (int m1 = -l1; m1 <= l1; ++m1)
+                        for (int m2 = -l2; m2 <= l2; ++m2) {
+                            const int m3 = m1 + m2;
+                            if (iabs_(m3) > l3) continue;
+                            const double c = cg_lookup(L, l1, m1, l2, m2, l3, m3) * gz[base + l3 + m3];
+                            if (ga) ga[l1 * l1 + l1 + m1] += c * b[l2 * l2 + l2 + m2];
+                            if (gb) gb[l2 * l2 + l2 + m2] += c * a[l1 * l1 + l1 + m1];
+                        }
+                }
+    }
     return 0;
 }
 
