@@ -151,6 +151,36 @@ typedef struct {
 int cgtp_forward_weighted(cgtp_plan_t plan, const void *x1, const void *x2, const void *weights, void *out,
                           int64_t N, const cgtp_channels *ch, void *hip_stream);
 
+/*
+ * Gradients of sum(grad_out * out) for cgtp_forward:
+ *   grad_x1[n, (l1, m1)] = sum over paths and m2, m3 of C^{l3 m3}_{l1 m1 l2 m2} x2[n, (l2, m2)] grad_out[n, (l1, l2, l3), m3]
+ *   grad_x2[n, (l2, m2)] = sum over paths and m1, m3 of C^{l3 m3}_{l1 m1 l2 m2} x1[n, (l1, m1)] grad_out[n, (l1, l2, l3), m3]
+ * (the CGTP is bilinear: each gradient is the transpose of a linear map).
+ * Computed by the method of the forward call run backwards, block by block
+ * (Section 4.3): the adjoint of every stage (recombination and 1/K, Legendre
+ * projection, longitude analysis, pointwise products, longitude synthesis,
+ * lift), on the same grids and with the same tables, so the result equals the
+ * double sum above up to rounding.
+ *   x1, x2, grad_x1, grad_x2: device arrays [N, (L+1)^2]; grad_out: [N,
+ *   (L+1)^4] in cgtp_forward's output layout; all of the plan's dtype,
+ *   row-major, contiguous, 16-byte aligned.  Either gradient pointer may be
+ *   NULL (not written), not both.
+ *   workspace: caller-owned device memory, 256-byte aligned, at least
+ *   cgtp_backward_workspace_bytes(plan, N) bytes (each block's contribution
+ *   to both gradients of every pair, summed afterwards in a fixed order, so
+ *   results do not depend on scheduling).  Contents on entry are ignored.
+ * CGTP_EINVAL for NULL inputs, misalignment, a short workspace, or a
+ * gradient or the workspace overlapping any other buffer; CGTP_EUNSUP when a
+ * block of the plan does not fit the gradient kernel or N (L+1)^2 exceeds
+ * 2^31 - 1.  Asynchronous on hip_stream; allocates nothing; N == 0 returns
+ * CGTP_OK with no launch.  The plan's device must be current.
+ */
+int cgtp_backward(cgtp_plan_t plan, const void *x1, const void *x2, const void *grad_out, void *grad_x1,
+                  void *grad_x2, int64_t N, void *workspace, int64_t workspace_bytes, void *hip_stream);
+
+/* Workspace bytes cgtp_backward needs for N pairs: 2 (L+1)^3 N elements; -1 for a NULL plan, N < 0 or overflow. */
+int64_t cgtp_backward_workspace_bytes(cgtp_plan_t plan, int64_t N);
+
 /* Number of paths of degree L: sum over l1, l2 <= L of 2 min(l1, l2) + 1; -1 for L < 0. */
 int64_t cgtp_num_paths(int32_t L);
 

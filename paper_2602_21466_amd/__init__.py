@@ -68,6 +68,8 @@ def _load():
         "cgtp_plan": (ctypes.c_int, [i32, ctypes.POINTER(cgtp_grid), ctypes.POINTER(vp)]),
         "cgtp_forward": (ctypes.c_int, [vp, vp, vp, vp, i64, vp]),
         "cgtp_forward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, ctypes.POINTER(cgtp_channels), vp]),
+        "cgtp_backward": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
+        "cgtp_backward_workspace_bytes": (i64, [vp, i64]),
         "cgtp_num_paths": (i64, [i32]),
         "cgtp_path_index": (i64, [i32, i32, i32, i32]),
         "cgtp_destroy": (ctypes.c_int, [vp]),
@@ -115,7 +117,8 @@ def _load():
 
 def exported_symbols():
     """Names of the C ABI entry points this binding expects."""
-    return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
+    return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_backward", "cgtp_backward_workspace_bytes",
+            "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
             "istp_plan", "istp_forward", "istp_forward_weighted", "istp_num_labels", "istp_label_index",
@@ -161,6 +164,18 @@ def cgtp_forward_weighted(plan, x1_ptr: int, x2_ptr: int, w_ptr: int | None, out
                                        ctypes.c_void_p(w_ptr) if w_ptr else None, ctypes.c_void_p(out_ptr),
                                        int(N), ctypes.byref(ch), ctypes.c_void_p(stream_ptr) if stream_ptr else None)
     _check(rc, "cgtp_forward_weighted")
+
+
+def cgtp_backward(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int | None, gx2_ptr: int | None, N: int,
+                  ws_ptr: int, ws_bytes: int, stream_ptr: int | None = None) -> None:
+    vpn = lambda p: ctypes.c_void_p(p) if p else None
+    rc = _load().cgtp_backward(plan, ctypes.c_void_p(x1_ptr), ctypes.c_void_p(x2_ptr), ctypes.c_void_p(g_ptr),
+                               vpn(gx1_ptr), vpn(gx2_ptr), int(N), vpn(ws_ptr), int(ws_bytes), vpn(stream_ptr))
+    _check(rc, "cgtp_backward")
+
+
+def cgtp_backward_workspace_bytes(plan, N: int) -> int:
+    return int(_load().cgtp_backward_workspace_bytes(plan, int(N)))
 
 
 def cgtp_num_paths(L: int) -> int:
@@ -418,6 +433,31 @@ class Plan:
         cgtp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), weights.data_ptr() if weights is not None else None,
                               out.data_ptr(), N, C, shared, per_pair, s.cuda_stream)
         return out
+
+    def backward(self, x1, x2, grad_out, need_x1=True, need_x2=True, workspace=None, stream=None):
+        """(grad_x1, grad_x2) of sum(grad_out * forward(x1, x2)); a gradient not asked for is None.
+        workspace: optional uint8 CUDA tensor of at least cgtp_backward_workspace_bytes(plan, N) bytes."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        nin, nout = (self.L + 1) ** 2, cgtp_num_outputs(self.L)
+        N = x1.shape[0]
+        for t, n, what in ((x1, nin, "x1"), (x2, nin, "x2"), (grad_out, nout, "grad_out")):
+            if not t.is_cuda or t.dtype != tdt or tuple(t.shape) != (N, n) or not t.is_contiguous():
+                raise ValueError("%s must be a contiguous %s CUDA tensor [N, %d]" % (what, tdt, n))
+        if not (need_x1 or need_x2):
+            return None, None
+        need = cgtp_backward_workspace_bytes(self._h, N)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < need:
+            raise ValueError("workspace must be a uint8 CUDA tensor of at least %d bytes" % need)
+        g1 = torch.empty_like(x1) if need_x1 else None
+        g2 = torch.empty_like(x2) if need_x2 else None
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        cgtp_backward(self._h, x1.data_ptr(), x2.data_ptr(), grad_out.data_ptr(),
+                      g1.data_ptr() if g1 is not None else None, g2.data_ptr() if g2 is not None else None, N,
+                      workspace.data_ptr(), workspace.numel(), s.cuda_stream)
+        return g1, g2
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -1,0 +1,517 @@
+// Gradients of the full CGTP: the adjoint of the block kernel's procedure
+// (Section 4.3), block by block.  The CGTP is bilinear, so for an upstream
+// gradient g of the outputs, the gradient for x1 (x2) is the transpose of the
+// linear map x1 -> z (x2 -> z) applied to g.  Every stage of the forward
+// kernel (cgtp_kernels.hip) is linear in the input it carries, and each is
+// transposed here in reverse order, with the forward plan's own tables:
+//
+//   end phase (recombination, 1/K, scales) -> g scattered onto the
+//       projection's accumulator entries with the same weights;
+//   Legendre projection (MFMA)             -> Legendre synthesis: per ring and
+//       order, the sum over l3 of the same weights times those entries;
+//   longitude analysis (forward DFT)       -> inverse DFT, conjugate twiddles;
+//   pointwise products (bilinear)          -> the incoming gradient times the
+//       conjugate of the other factor;
+//   longitude synthesis (inverse DFT)      -> forward DFT;
+//   lift (Definition 4.1, real weights)    -> the lift's weights applied to
+//       the gradient, summed over the rings.
+//
+// Transposes are taken for the real inner product of complex arrays, under
+// which a complex-linear map's adjoint is its conjugate transpose.  The
+// forward forms each product on half the circle and writes the other half as
+// its conjugate (the signals have real coefficients); the scalar blocks'
+// transpose below uses the equivalent full-circle form z(k) = F0(k) F1(k),
+// which is the same function of the inputs and so has the same gradient.
+//
+// One work-group computes one (j1, j2) block for one pair: the block's
+// contribution to the pair's gradient rows of degree j1 (x1) and j2 (x2),
+// written to a workspace; a second kernel sums the contributions over the
+// other degree in a fixed order.  The phases are work-group-wide task pools
+// separated by barriers; rings go bd.bwd_rings at a time.
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "cgtp_internal.h"
+#include "device_common.h"
+
+namespace cgtp {
+namespace {
+
+using namespace ::cgtp::dev;
+
+template <typename T, int A, int B>
+__device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& bd, int64_t n,
+                                         const T* __restrict__ x1, const T* __restrict__ x2,
+                                         const T* __restrict__ gin, T* __restrict__ wrow, int L,
+                                         unsigned char* smem) {
+    using C = typename Cplx<T>::type;
+    using Coef4 = typename Cplx<T>::acc4;
+    constexpr int Phi = A * B;
+    constexpr int H = Phi / 2 + 1;
+    constexpr int BP = B + 1;
+    constexpr int FS = slot_stride(A, B);
+    constexpr int NT = kBwdThreads;
+    const int tid = threadIdx.x;
+    const int j1 = bd.j1, j2 = bd.j2, J = bd.J, R = bd.R, d = bd.d, G = bd.bwd_rings;
+    const bool cross = bd.kind == kBlockCross;
+    const int nslot = cross ? 4 : 2;
+    const int nz = cross ? 2 : 1;          // analysis transforms
+    const int ncomp = cross ? 4 : 1;       // projected components
+    const int n1 = 2 * j1 + 1, n2 = 2 * j2 + 1;
+    const int nin = (L + 1) * (L + 1);
+    const int64_t nout = (int64_t)nin * nin;
+    const int nrows = (J - d) / 2 + 1;
+    auto tmin = [&](int mp) { return mp > d ? (mp - d + 1) / 2 : 0; };
+    auto rows_of = [&](int mp) { return nrows - tmin(mp); };
+
+    const BwdLayout ly = bwd_layout(bd, (int)sizeof(T), G);
+    T* lc = reinterpret_cast<T*>(smem + ly.lc);        // [3][n1] then [3][n2]
+    C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);      // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
+    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);      // [slot][longitude n]: the pair's lifted coefficients
+    C* cacc = reinterpret_cast<C*>(smem + ly.cacc);    // [slot][longitude n]: their gradients, summed over rings
+    T* bg = reinterpret_cast<T*>(smem + ly.bg);        // accumulator-entry gradients, compact
+    int* moff = reinterpret_cast<int*>(smem + ly.moff);
+    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);    // [ring of the group][kBwdSlots], pass layout
+    auto slot = [&](int r, int s) -> C* { return fbuf + (size_t)(r * kBwdSlots + s) * FS; };
+    const int zs0 = nslot;              // slots of the analysis gradients (spectra)
+    const int zg0 = kBwdSlots - 2;      // slots of the product gradients (circle)
+
+    // normalised P_j^|m| at the order m that longitude index nn carries in the
+    // synthesis (Phi > 2 j: nn <= Phi / 2 is m = nn), zero for |m| > j
+    auto pval = [&](int ring, int j, int nn) -> T {
+        const int m = nn <= Phi / 2 ? nn : nn - Phi, am = m < 0 ? -m : m;
+        return am <= j ? tb.pbar[bd.pbar_off + (size_t)ring * bd.pbar_stride + j * (j + 1) / 2 + am] : (T)0;
+    };
+
+    // ---- set-up: couplings, twiddles, entry offsets per |m|, cleared sums
+    for (int e = tid; e < 3 * n1; e += NT) lc[e] = tb.lcg[3 * j1 * j1 + e];
+    for (int e = tid; e < 3 * n2; e += NT) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
+    {
+        const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
+        for (int e = tid; e < A * BP; e += NT) tw2[e] = tw[e];
+    }
+    if (tid == 0) {
+        int o = 0;
+        for (int mp = 0; mp <= J; ++mp) {
+            moff[mp] = o;
+            o += rows_of(mp) * (mp == 0 ? 1 : 2) * ncomp;
+        }
+        moff[J + 1] = o;
+    }
+    for (int e = tid; e < ly.nbg; e += NT) bg[e] = (T)0;
+    for (int e = tid; e < nslot * Phi; e += NT) cacc[e] = cmk<C>((T)0, (T)0);
+    __syncthreads();
+    // ---- the pair's lifted coefficients, as the forward forms them:
+    //   even slot: (x_m, C^{j, m}_{j, m, 1, 0} x_m), odd slot: (C^{j,m-1}_{j,m,1,-1}
+    //   x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1}), times (-1)^m for negative m;
+    //   scalar blocks (x_m, 0)
+    for (int e = tid; e < nslot * Phi; e += NT) {
+        const int s = e / Phi, nn = e - s * Phi;
+        const bool first = cross ? (s < 2) : (s == 0);
+        const int j = first ? j1 : j2, nj = 2 * j + 1;
+        const int m = nn <= Phi / 2 ? nn : nn - Phi, am = m < 0 ? -m : m;
+        C val = cmk<C>((T)0, (T)0);
+        if (am <= j) {
+            const int mj = m + j;
+            const T* xrow = (first ? x1 : x2) + n * nin + j * j;
+            const T* lcj = first ? lc : lc + 3 * n1;
+            const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
+            if (!cross || (s & 1) == 0) {
+                const T xm = sg * xrow[mj];
+                val = cmk<C>(xm, cross ? lcj[nj + mj] * xm : (T)0);
+            } else {
+                const T xlo = mj >= 1 ? xrow[mj - 1] : (T)0;
+                const T xhi = mj + 1 < nj ? xrow[mj + 1] : (T)0;
+                val = cmk<C>(sg * lcj[mj] * xlo, sg * lcj[2 * nj + mj] * xhi);
+            }
+        }
+        cvn[e] = val;
+    }
+    // ---- transpose of the end phase.  Output o of the block is sum_k w_k e_k
+    // over up to three accumulator entries e_k (given for pair 0 in the forward
+    // plan's tile layout); each entry feeds one output, so its gradient is
+    // w_k g_o.  Zero-weight placeholder terms are skipped.
+    {
+        const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef) + bd.coef_off;
+        const int4* coefi = reinterpret_cast<const int4*>(tb.coefi) + bd.coef_off;
+        const TileDesc* td = tb.tdesc + bd.tdesc_off;
+        const T* grow = gin + n * nout + bd.out_off;
+        const int lgC = bd.lg_pairs + (cross ? 2 : 0);   // log2(columns per sign) of the forward tiling
+        for (int o = tid; o < n1 * n2; o += NT) {
+            const Coef4 cf = coef4[o];
+            const int4 ix = coefi[o];
+            const T gv = grow[o];
+            const T w3[3] = {cf.x, cf.y, cf.z};
+            const int e3[3] = {ix.x, ix.y, ix.z};
+            const int nterm = (ix.w & 1) ? 1 : 3;
+            for (int k = 0; k < nterm; ++k) {
+                if (w3[k] == (T)0) continue;
+                const int u = e3[k] / tile_stride<T>(), lin = e3[k] - u * tile_stride<T>();
+                // accumulator layout: lane = lin / 4 (column lane % 16, quarter lane / 16),
+                // element q = lin % 4 of the lane
+                const int lane = lin >> 2, q = lin & 3;
+                const int r = sizeof(T) == 4 ? 4 * (lane >> 4) + q : (lane >> 4) + 4 * q;
+                const int code = td[u].code;
+                const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
+                const int row = 16 * rt + r, col = 16 * ct + (lane & 15);
+                const int sg = col >> lgC, comp = (col >> bd.lg_pairs) & (ncomp - 1);
+                bg[moff[mp] + (sg * ncomp + comp) * rows_of(mp) + row] = w3[k] * gv;
+            }
+        }
+    }
+    __syncthreads();
+
+    const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
+
+    for (int rg0 = 0; rg0 < R; rg0 += G) {
+        const int nrg = (R - rg0) < G ? (R - rg0) : G;
+        // ---- 1. synthesis pass 1 of the lifts (as the forward); clear the
+        // analysis-gradient slots (orders past J stay zero)
+        for (int task = tid; task < nrg * nslot * A; task += NT) {
+            const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
+            const bool first = cross ? (s < 2) : (s == 0);
+            const int j = first ? j1 : j2;
+            const C* cv = cvn + (size_t)s * Phi + t;
+            C v[B];
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                const C c = cv[A * i];
+                const T pv = pval(rg0 + r, j, t + A * i);
+                v[i] = cmk<C>(c.x * pv, c.y * pv);
+            }
+            Dft<B, true, C>::run(v);
+            C* row = slot(r, s) + t * BP;
+            const C* twr = tw2 + t * BP;
+#pragma unroll
+            for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[0] : cmulc(v[k2], twr[k2]);
+        }
+        for (int e = tid; e < nrg * nz * FS; e += NT) {
+            const int r = e / (nz * FS), rest = e - r * nz * FS;
+            slot(r, zs0)[rest] = cmk<C>((T)0, (T)0);   // nz consecutive slots
+        }
+        __syncthreads();
+        // ---- 2. synthesis pass 2 (in place)
+        for (int task = tid; task < nrg * nslot * B; task += NT) {
+            const int k2 = task % B, f = task / B, s = f % nslot, r = f / nslot;
+            C* fb = slot(r, s) + k2;
+            C u[A];
+#pragma unroll
+            for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
+            Dft<A, true, C>::run(u);
+#pragma unroll
+            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+        }
+        // ---- 3. transpose of the projection (other slots than pass 2's): the
+        // spectrum gradient at (ring, component, signed m) is the sum over the
+        // rows l3 of the weight 2 w_r P^|m|_l3(x_r) times the entry gradient; it
+        // goes to the real (even component) or imaginary (odd) part at the
+        // pass-layout position of m
+        for (int task = tid; task < nrg * (2 * J + 1) * ncomp; task += NT) {
+            const int comp = task % ncomp, f = task / ncomp, sm = f % (2 * J + 1), r = f / (2 * J + 1);
+            const int m = sm - J, mp = m < 0 ? -m : m;
+            const int nr = rows_of(mp), t0 = tmin(mp);
+            const T* gcol = bg + moff[mp] + ((m < 0 ? ncomp : 0) + comp) * nr;
+            // weight of (|m|, ring, l3 = d + 2 (t0 + i)) at [|m|][ring][(l3 - parity of J) / 2]
+            const int w0 = (mp * bd.rpad + rg0 + r) * bd.wrow + (d + 2 * t0 - (J & 1)) / 2;
+            T acc = (T)0;
+            for (int i = 0; i < nr; ++i) acc += buffer_load<T>(wrsrc, (w0 + i) * (int)sizeof(T), 0) * gcol[i];
+            const int k = m < 0 ? Phi + m : m;
+            T* dst = reinterpret_cast<T*>(slot(r, zs0 + (comp >> 1)) + (k + k / B));
+            dst[comp & 1] = acc;
+        }
+        __syncthreads();
+        // ---- 4. transpose of analysis pass 2: inverse DFT down the columns
+        for (int task = tid; task < nrg * nz * B; task += NT) {
+            const int k2 = task % B, f = task / B, z = f % nz, r = f / nz;
+            C* fb = slot(r, zs0 + z) + k2;
+            C u[A];
+#pragma unroll
+            for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
+            Dft<A, true, C>::run(u);
+#pragma unroll
+            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+        }
+        __syncthreads();
+        // ---- 5. transpose of analysis pass 1: conjugate twiddles, inverse DFT
+        // along the row, back to the longitudes n = t + A n2 (product gradients)
+        for (int task = tid; task < nrg * nz * A; task += NT) {
+            const int t = task % A, f = task / A, z = f % nz, r = f / nz;
+            const C* row = slot(r, zs0 + z) + t * BP;
+            const C* twr = tw2 + t * BP;
+            C v[B];
+#pragma unroll
+            for (int k2 = 0; k2 < B; ++k2) v[k2] = k2 == 0 ? row[0] : cmulc(row[k2], twr[k2]);
+            Dft<B, true, C>::run(v);
+            C* zg = slot(r, zg0 + z);
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                const int nn = t + A * i;
+                zg[nn + nn / B] = v[i];
+            }
+        }
+        __syncthreads();
+        // ---- 6. transpose of the products at longitudes n and -n; the lifts'
+        // transforms are overwritten in place with their gradients
+        for (int task = tid; task < nrg * H; task += NT) {
+            const int nn = task % H, r = task / H;
+            const int kk = nn == 0 ? 0 : Phi - nn;
+            const int pn = nn + nn / B, pk = kk + kk / B;
+            const bool self = kk == nn;
+            const C* zg1 = slot(r, zg0);
+            if (!cross) {
+                C* f0 = slot(r, 0);
+                C* f1 = slot(r, 1);
+                const C a = f0[pn], b = f1[pn], za = zg1[pn];
+                f0[pn] = cmulc(za, b);
+                f1[pn] = cmulc(za, a);
+                if (!self) {
+                    const C ak = f0[pk], bk = f1[pk], zk = zg1[pk];
+                    f0[pk] = cmulc(zk, bk);
+                    f1[pk] = cmulc(zk, ak);
+                }
+                continue;
+            }
+            const C* zg2 = slot(r, zg0 + 1);
+            // the forward writes z1 = gs + i g0 at n and conj(gs) + i conj(g0) at -n
+            // (z2 likewise from g-1, g+1); transposed:
+            C ggs, gg0, ggm, ggp;
+            {
+                const C z1n = zg1[pn], z2n = zg2[pn];
+                const C z1k = self ? cmk<C>((T)0, (T)0) : cconj(zg1[pk]);
+                const C z2k = self ? cmk<C>((T)0, (T)0) : cconj(zg2[pk]);
+                ggs = cadd(z1n, z1k);
+                gg0 = mul_mi<false>(csub(z1n, z1k));
+                ggm = cadd(z2n, z2k);
+                ggp = mul_mi<false>(csub(z2n, z2k));
+            }
+            // the unpacked signals (times 2), as the forward forms them
+            C f[8];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const C* fs = slot(r, s);
+                const C Fn = fs[pn], Fk = fs[pk];
+                f[2 * s] = cmk<C>(Fn.x + Fk.x, Fn.y - Fk.y);
+                f[2 * s + 1] = cmk<C>(Fn.y + Fk.y, Fk.x - Fn.x);
+            }
+            const C as = f[0], a0 = f[1], am = f[2], ap = f[3];
+            const C bs = f[4], b0 = f[5], bm = f[6], bp = f[7];
+            const bool even_dot = bd.products & kEvenDot, odd_sv = bd.products & kOddSV;
+            C fg[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) fg[i] = cmk<C>((T)0, (T)0);
+            // the gradient of a factor of a product is the product's gradient times
+            // the conjugate of the other factor
+            if (even_dot) {   // gs = ap bm - a0 b0 + am bp
+                fg[3] = cadd(fg[3], cmulc(ggs, bm));
+                fg[6] = cadd(fg[6], cmulc(ggs, ap));
+                fg[1] = csub(fg[1], cmulc(ggs, b0));
+                fg[5] = csub(fg[5], cmulc(ggs, a0));
+                fg[2] = cadd(fg[2], cmulc(ggs, bp));
+                fg[7] = cadd(fg[7], cmulc(ggs, am));
+            } else {          // gs = as bs
+                fg[0] = cadd(fg[0], cmulc(ggs, bs));
+                fg[4] = cadd(fg[4], cmulc(ggs, as));
+            }
+            if (odd_sv) {     // g+1 = as bp, g0 = as b0, g-1 = as bm
+                fg[0] = cadd(fg[0], cadd(cadd(cmulc(ggp, bp), cmulc(gg0, b0)), cmulc(ggm, bm)));
+                fg[7] = cadd(fg[7], cmulc(ggp, as));
+                fg[5] = cadd(fg[5], cmulc(gg0, as));
+                fg[6] = cadd(fg[6], cmulc(ggm, as));
+            } else {          // g+1 = ap b0 - a0 bp, g0 = ap bm - am bp, g-1 = a0 bm - am b0
+                fg[3] = cadd(fg[3], cadd(cmulc(ggp, b0), cmulc(gg0, bm)));
+                fg[1] = cadd(fg[1], csub(cmulc(ggm, bm), cmulc(ggp, bp)));
+                fg[2] = csub(fg[2], cadd(cmulc(gg0, bp), cmulc(ggm, b0)));
+                fg[5] = cadd(fg[5], csub(cmulc(ggp, ap), cmulc(ggm, am)));
+                fg[6] = cadd(fg[6], cadd(cmulc(gg0, ap), cmulc(ggm, a0)));
+                fg[7] = csub(fg[7], cadd(cmulc(ggp, a0), cmulc(gg0, am)));
+            }
+            // transpose of the unpacking fA = F(n) + conj F(-n), fB = -i (F(n) - conj F(-n)):
+            // F(n) receives fA' + i fB', F(-n) receives conj(fA' - i fB')
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const C ga = fg[2 * s], ign = mul_mi<true>(fg[2 * s + 1]);
+                const C dn = cadd(ga, ign), dk = cconj(csub(ga, ign));
+                C* fs = slot(r, s);
+                if (self) {
+                    fs[pn] = cadd(dn, dk);
+                } else {
+                    fs[pn] = dn;
+                    fs[pk] = dk;
+                }
+            }
+        }
+        __syncthreads();
+        // ---- 7. transpose of synthesis pass 2: forward DFT down the columns
+        for (int task = tid; task < nrg * nslot * B; task += NT) {
+            const int k2 = task % B, f = task / B, s = f % nslot, r = f / nslot;
+            C* fb = slot(r, s) + k2;
+            C u[A];
+#pragma unroll
+            for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
+            Dft<A, false, C>::run(u);
+#pragma unroll
+            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+        }
+        __syncthreads();
+        // ---- 8. transpose of synthesis pass 1: twiddles, forward DFT along the
+        // row; the coefficient gradient at longitude n = t + A n2 is that times
+        // the Legendre value, kept in natural order in slot nslot + s
+        for (int task = tid; task < nrg * nslot * A; task += NT) {
+            const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
+            const bool first = cross ? (s < 2) : (s == 0);
+            const int j = first ? j1 : j2;
+            const C* row = slot(r, s) + t * BP;
+            const C* twr = tw2 + t * BP;
+            C v[B];
+#pragma unroll
+            for (int k2 = 0; k2 < B; ++k2) v[k2] = k2 == 0 ? row[0] : cmul(row[k2], twr[k2]);
+            Dft<B, false, C>::run(v);
+            C* out = slot(r, nslot + s);
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                const T pv = pval(rg0 + r, j, t + A * i);
+                out[t + A * i] = cmk<C>(v[i].x * pv, v[i].y * pv);
+            }
+        }
+        __syncthreads();
+        // ---- 9. sum over the group's rings, in ring order
+        for (int e = tid; e < nslot * Phi; e += NT) {
+            const int s = e / Phi, nn = e - s * Phi;
+            C sum = cacc[e];
+            for (int r = 0; r < nrg; ++r) sum = cadd(sum, slot(r, nslot + s)[nn]);
+            cacc[e] = sum;
+        }
+        __syncthreads();
+    }
+
+    // ---- transpose of the lift: each input component collects the gradients of
+    // the lifted coefficients it was placed in, with the same weights
+    auto at = [&](int s, int m) -> C { return cacc[s * Phi + (m < 0 ? Phi + m : m)]; };
+    auto sgn = [&](int m) -> T { return (m < 0 && ((-m) & 1)) ? (T)-1 : (T)1; };
+    for (int e = tid; e < n1 + n2; e += NT) {
+        const bool first = e < n1;
+        const int j = first ? j1 : j2, nj = 2 * j + 1, mj = first ? e : e - n1, mc = mj - j;
+        const T* lcj = first ? lc : lc + 3 * n1;
+        const int s0 = first ? 0 : (cross ? 2 : 1);   // the input's even slot
+        // even slot, order mc: (x, C0 x)
+        const C c = at(s0, mc);
+        T acc = sgn(mc) * (c.x + (cross ? lcj[nj + mj] * c.y : (T)0));
+        if (cross) {
+            // odd slot: real part of order mc + 1 holds C- x_mc, imaginary part of
+            // order mc - 1 holds C+ x_mc
+            if (mc + 1 <= j) acc += sgn(mc + 1) * lcj[mj + 1] * at(s0 + 1, mc + 1).x;
+            if (mc - 1 >= -j) acc += sgn(mc - 1) * lcj[2 * nj + mj - 1] * at(s0 + 1, mc - 1).y;
+        }
+        wrow[e] = acc;
+    }
+}
+
+// Work-group -> (block, pair); the block body for the block's longitude size.
+template <typename T>
+__global__ __launch_bounds__(kBwdThreads) void bwd_kernel(Tables<T> tb, const int32_t* __restrict__ list,
+                                                           const T* __restrict__ x1, const T* __restrict__ x2,
+                                                           const T* __restrict__ g, T* __restrict__ ws, int64_t N,
+                                                           int L) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int64_t wg = blockIdx.x;
+    const int li = (int)(wg / N);
+    const int64_t n = wg - (int64_t)li * N;
+    const BlockDesc bd = tb.blocks[list[li]];
+    T* wrow = ws + bwd_block_off(L, bd.j1, bd.j2) * N + n * (2 * (bd.j1 + bd.j2) + 2);
+#define CGTP_BCASE(PHI, A_, B_) \
+    case PHI: bwd_body<T, A_, B_>(tb, bd, n, x1, x2, g, wrow, L, smem); break;
+    switch (bd.Phi) {
+        CGTP_BCASE(1, 1, 1)
+        CGTP_BCASE(2, 2, 1)
+        CGTP_BCASE(3, 3, 1)
+        CGTP_BCASE(4, 2, 2)
+        CGTP_BCASE(6, 3, 2)
+        CGTP_BCASE(8, 4, 2)
+        CGTP_BCASE(9, 3, 3)
+        CGTP_BCASE(12, 4, 3)
+        CGTP_BCASE(16, 4, 4)
+        CGTP_BCASE(18, 6, 3)
+        CGTP_BCASE(24, 6, 4)
+        CGTP_BCASE(27, 9, 3)
+        CGTP_BCASE(32, 8, 4)
+        CGTP_BCASE(36, 6, 6)
+        CGTP_BCASE(48, 8, 6)
+        CGTP_BCASE(54, 9, 6)
+        CGTP_BCASE(64, 8, 8)
+        CGTP_BCASE(72, 9, 8)
+        CGTP_BCASE(81, 9, 9)
+        CGTP_BCASE(96, 12, 8)
+        CGTP_BCASE(108, 12, 9)
+        CGTP_BCASE(128, 16, 8)
+        CGTP_BCASE(144, 12, 12)
+        default: break;
+    }
+#undef CGTP_BCASE
+}
+
+// Sums of the blocks' contributions in a fixed order: gx1[n, (l, m)] over the
+// blocks (l, j2), gx2[n, (l, m)] over the blocks (j1, l).  One thread per
+// (input, pair, component).
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const T* __restrict__ ws, T* __restrict__ gx1,
+                                                         T* __restrict__ gx2, int64_t N, int L) {
+    const int nin = (L + 1) * (L + 1);
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= 2 * N * nin) return;
+    const int which = (int)(e / (N * nin));
+    const int64_t rest = e - (int64_t)which * N * nin;
+    const int64_t n = rest / nin;
+    const int c = (int)(rest - n * nin);
+    T* dst = which == 0 ? gx1 : gx2;
+    if (!dst) return;
+    int l = 0;
+    while ((l + 1) * (l + 1) <= c) ++l;
+    const int i = c - l * l;   // component within degree l
+    T sum = (T)0;
+    for (int o = 0; o <= L; ++o) {
+        const int j1 = which == 0 ? l : o, j2 = which == 0 ? o : l;
+        const int w = 2 * (j1 + j2) + 2;
+        sum += ws[bwd_block_off(L, j1, j2) * N + n * w + (which == 0 ? i : 2 * j1 + 1 + i)];
+    }
+    dst[n * nin + c] = sum;
+}
+
+template <typename T>
+int launch_bwd(const Tables<T>& tb, const int32_t* list, int lds, const T* x1, const T* x2, const T* g, T* gx1,
+               T* gx2, T* ws, int64_t N, int L, void* stream) {
+    const int64_t nblocks = (int64_t)(L + 1) * (L + 1);
+    const int64_t grid = nblocks * N;
+    if (grid <= 0) return 0;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)bwd_kernel<T>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        if (e != hipSuccess) return (int)e;
+    }
+    hipLaunchKernelGGL(bwd_kernel<T>, dim3((unsigned)grid), dim3(kBwdThreads), lds, (hipStream_t)stream, tb, list,
+                       x1, x2, g, ws, N, L);
+    int err = (int)hipGetLastError();
+    if (err) return err;
+    const int64_t rgrid = (2 * N * (int64_t)(L + 1) * (L + 1) + 255) / 256;
+    if (rgrid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(bwd_reduce_kernel<T>, dim3((unsigned)rgrid), dim3(256), 0, (hipStream_t)stream, ws, gx1, gx2,
+                       N, L);
+    return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_backward_f32(const Tables<float>& tb, const int32_t* list, int lds, const float* x1, const float* x2,
+                        const float* g, float* gx1, float* gx2, float* ws, int64_t N, int L, void* stream) {
+    return launch_bwd<float>(tb, list, lds, x1, x2, g, gx1, gx2, ws, N, L, stream);
+}
+int launch_backward_f64(const Tables<double>& tb, const int32_t* list, int lds, const double* x1,
+                        const double* x2, const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L,
+                        void* stream) {
+    return launch_bwd<double>(tb, list, lds, x1, x2, g, gx1, gx2, ws, N, L, stream);
+}
+
+}  // namespace cgtp

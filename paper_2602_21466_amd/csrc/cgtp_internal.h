@@ -76,6 +76,7 @@ struct alignas(16) BlockDesc {
     int32_t wrow;              // entries per ring row of the weight table
     int32_t path_off;          // index of path (j1, j2, |j1 - j2|) in the (l1, l2, l3) order of all paths
     int32_t x2share;           // channel kernel: LDS holds a shared second-input buffer (x2_bytes) beside the working set
+    int32_t bwd_rings;         // gradient kernel: rings per group (bwd_layout)
     int64_t out_off;           // offset of the block inside one pair's output
 };
 
@@ -180,6 +181,49 @@ struct TileGeom {
     __host__ __device__ int nct(int mp) const { return (ncols(mp) + 15) / 16; }
 };
 
+// ---------------------------------------------------------------- gradients
+//
+// The gradient kernel (cgtp_backward.hip) runs one work-group per (block,
+// pair).  Its LDS, in byte offsets: couplings [3][n1 + n2], twiddles in pass
+// layout, the pair's lifted coefficients and their gradients ([slot][Phi]
+// each), the accumulator-entry gradients (compact: per |m|, [column (sign,
+// component)][row]), their offsets per |m|, and per ring of a group
+// kBwdSlots transforms.
+constexpr int kBwdThreads = 256;
+constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
+struct BwdLayout {
+    int lc, tw2, cvn, cacc, bg, moff, fbuf, end;
+    int nbg;   // accumulator entries of one pair
+};
+__host__ __device__ inline int bwd_align16(int v) { return (v + 15) & ~15; }
+__host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int rings) {
+    const int csz = 2 * esz;
+    const bool cross = b.kind == kBlockCross;
+    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
+    const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
+    const int nrows = (b.J - b.d) / 2 + 1;
+    BwdLayout l;
+    l.nbg = 0;
+    for (int mp = 0; mp <= b.J; ++mp)
+        l.nbg += (nrows - (mp > b.d ? (mp - b.d + 1) / 2 : 0)) * (mp == 0 ? 1 : 2) * ncomp;
+    int o = 0;
+    l.lc = o; o = bwd_align16(o + esz * 3 * (n1 + n2));
+    l.tw2 = o; o = bwd_align16(o + csz * b.A * (b.B + 1));
+    l.cvn = o; o = bwd_align16(o + csz * nslot * b.Phi);
+    l.cacc = o; o = bwd_align16(o + csz * nslot * b.Phi);
+    l.bg = o; o = bwd_align16(o + esz * l.nbg);
+    l.moff = o; o = bwd_align16(o + 4 * (b.J + 2));
+    l.fbuf = o; o += csz * rings * kBwdSlots * slot_stride(b.A, b.B);
+    l.end = o;
+    return l;
+}
+// Offset (elements per pair) of block (j1, j2)'s gradient rows in the
+// workspace: blocks in (j1, j2) order, each [pair][n1 + n2].
+__host__ __device__ inline int64_t bwd_block_off(int L, int j1, int j2) {
+    const int64_t M = L + 1;
+    return M * j1 * j1 + (int64_t)j1 * M * M + (int64_t)(2 * j1 + 1) * j2 + (int64_t)j2 * j2;
+}
+
 // Records the HIP code behind a CGTP_EHIP status (cgtp_last_hip_error reads it).
 void set_last_hip_error(int code);
 
@@ -210,5 +254,14 @@ int launch_blocks_channels_f32(const Tables<float>& tb, const int32_t* block_lis
 int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* block_list, const LaunchMap& map,
                                int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
                                int L, const ChanArgs<double>& ch, void* stream);
+
+// Gradients: the per-block kernel over (L + 1)^2 blocks x N pairs into ws,
+// then the sums over the other degree into gx1 / gx2 (either may be NULL).
+int launch_backward_f32(const Tables<float>& tb, const int32_t* block_list, int lds_bytes, const float* x1,
+                        const float* x2, const float* g, float* gx1, float* gx2, float* ws, int64_t N, int L,
+                        void* stream);
+int launch_backward_f64(const Tables<double>& tb, const int32_t* block_list, int lds_bytes, const double* x1,
+                        const double* x2, const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L,
+                        void* stream);
 
 }  // namespace cgtp

@@ -345,6 +345,8 @@ struct cgtp_plan_s {
     std::vector<Cls> classes;
     int lds_bytes = 0;      // dynamic LDS of the plain kernel
     int lds_bytes_ch = 0;   // and of the channel kernel (with the shared second-input buffers)
+    int bwd_lds = 0;        // dynamic LDS of the gradient kernel
+    bool bwd_ok = true;     // every block fits the gradient kernel's LDS
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
     double cross_cg = 0, dot_cg = 0;
@@ -551,6 +553,12 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             const int lds_x2 = lds_for<T>(b, pairs, true);
             b.x2share = lds_x2 <= cgtp::kLdsBudget ? 1 : 0;
             p->lds_bytes_ch = std::max(p->lds_bytes_ch, b.x2share ? lds_x2 : b.lds_bytes);
+            // gradient kernel: as many rings per group (4, 2, 1) as its LDS allows
+            b.bwd_rings = 0;
+            for (int G = 4; G >= 1 && !b.bwd_rings; G /= 2)
+                if (cgtp::bwd_layout(b, (int)sizeof(T), G).end <= cgtp::kLdsBudget) b.bwd_rings = G;
+            if (b.bwd_rings == 0) p->bwd_ok = false;
+            else p->bwd_lds = std::max(p->bwd_lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings).end);
             // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
             b.tdesc_off = (int)h.tdesc.size();
             {
@@ -971,6 +979,66 @@ int cgtp_forward_weighted(cgtp_plan_t plan, const void* x1, const void* x2, cons
 }
 
 int64_t cgtp_num_paths(int32_t L) { return L < 0 ? -1 : path_index(L, L + 1, 0, 1); }
+
+int64_t cgtp_backward_workspace_bytes(cgtp_plan_t plan, int64_t N) {
+    if (!plan || N < 0) return -1;
+    const int64_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const int64_t per = 2 * (int64_t)(plan->L + 1) * (plan->L + 1) * (plan->L + 1) * esz;
+    if (N > INT64_MAX / per) return -1;
+    return N * per;
+}
+
+int cgtp_backward(cgtp_plan_t plan, const void* x1, const void* x2, const void* grad_out, void* grad_x1,
+                  void* grad_x2, int64_t N, void* workspace, int64_t workspace_bytes, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (!plan->bwd_ok) return CGTP_EUNSUP;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2) || !workspace) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)grad_out | (uintptr_t)grad_x1 | (uintptr_t)grad_x2) & 15)
+        return CGTP_EINVAL;
+    if ((uintptr_t)workspace & 255) return CGTP_EINVAL;
+    const int L = plan->L;
+    const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)(L + 1) * (L + 1), nout = (size_t)cgtp_num_outputs(L);
+    if ((uint64_t)N > (uint64_t)(INT64_MAX / (int64_t)(nout * esz))) return CGTP_EINVAL;
+    const int64_t need = cgtp_backward_workspace_bytes(plan, N);
+    if (need < 0 || workspace_bytes < need) return CGTP_EINVAL;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    const void* ins[3] = {x1, x2, grad_out};
+    const size_t insz[3] = {bin, bin, bout};
+    void* outs[3] = {grad_x1, grad_x2, workspace};
+    const size_t outsz[3] = {bin, bin, (size_t)need};
+    for (int a = 0; a < 3; ++a) {
+        if (!outs[a]) continue;
+        for (int b = 0; b < 3; ++b)
+            if (overlaps(outs[a], outsz[a], ins[b], insz[b])) return CGTP_EINVAL;
+        for (int b = a + 1; b < 3; ++b)
+            if (outs[b] && overlaps(outs[a], outsz[a], outs[b], outsz[b])) return CGTP_EINVAL;
+    }
+    int dev = -1;
+    const hipError_t de = hipGetDevice(&dev);
+    if (de != hipSuccess) {
+        g_last_hip_error = (int)de;
+        return CGTP_EHIP;
+    }
+    if (dev != plan->device) return CGTP_EINVAL;
+    // one work-group per (block, pair)
+    if ((int64_t)nin * N > 0x7fffffffLL) return CGTP_EUNSUP;
+    int err;
+    if (plan->grid.dtype == CGTP_FP32)
+        err = cgtp::launch_backward_f32(plan->tf, plan->d_list, plan->bwd_lds, (const float*)x1, (const float*)x2,
+                                        (const float*)grad_out, (float*)grad_x1, (float*)grad_x2, (float*)workspace,
+                                        N, L, hip_stream);
+    else
+        err = cgtp::launch_backward_f64(plan->td, plan->d_list, plan->bwd_lds, (const double*)x1,
+                                        (const double*)x2, (const double*)grad_out, (double*)grad_x1,
+                                        (double*)grad_x2, (double*)workspace, N, L, hip_stream);
+    if (err != 0) {
+        g_last_hip_error = err;
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
 
 int64_t cgtp_path_index(int32_t L, int32_t l1, int32_t l2, int32_t l3) {
     if (L >= 0 && l1 == L + 1) return -1;

@@ -91,3 +91,12 @@ def test_query_and_strerror_edges():
     assert lib.cgtp_strerror(12345)
     assert lib.cgtp_num_outputs(-1) < 0
     assert lib.cgtp_path_offset(3, 1, 1, 3) == -1 and lib.cgtp_path_offset(3, 4, 0, 4) == -1
+
+
+def test_backward_null_plan_and_workspace_query():
+    f = lib._load()
+    buf = ctypes.create_string_buffer(8192)
+    p = ctypes.addressof(buf)
+    v = lambda o: ctypes.c_void_p(p + o)
+    assert f.cgtp_backward(None, v(0), v(0), v(256), v(4096), v(4352), 1, v(6144), 1024, None) == lib.CGTP_EINVAL
+    assert lib.cgtp_backward_workspace_bytes(None, 10) == -1
