@@ -3,7 +3,9 @@
 One step = one cgtp_forward over the whole batch (every (l1, l2) block of every
 pair: lift, products, lower, per-path recovery), inputs already resident in
 HBM.  The headline workload is L = 32, N = 1024 pairs, fp32; L = 16,
-N = 8192 is reported beside it.  The multiple-input, multiple-output Gaunt
+N = 8192 is reported beside it, each with the time of both gradients
+(cgtp_backward: the block adjoint kernel and the fixed-order sums, timed
+together as one step) under "backward".  The multiple-input, multiple-output Gaunt
 and vector signal products (istp_forward) are timed after it, each with its
 own roofline and oracle baseline, under "istp" (with the gradients,
 istp_backward, where the plan supports them).  Prints ONE JSON line.
@@ -58,6 +60,7 @@ MEASURED_TRAFFIC = {
 
 DIGEST_SOURCES = {
     "cgtp": ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
+    "cgtp_backward": ("cgtp_backward.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "istp": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
@@ -109,7 +112,7 @@ def _time_launches(forward, N, steps, warmup):
             "wall_s": wall}
 
 
-def time_workload(w, steps, warmup):
+def time_workload(w, steps, warmup, backward=True):
     import torch
 
     import cgtp_inputs
@@ -121,8 +124,26 @@ def time_workload(w, steps, warmup):
     out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
     res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": plan.query(), "kind": "cgtp"}
     res.update(_time_launches(lambda st: plan.forward(a, b, out, st), w.N, steps, warmup))
+    if backward:
+        # both gradients (block kernel and the fixed-order sums) for a seeded grad_out
+        g = torch.randn(out.shape, generator=torch.Generator("cpu").manual_seed(w.seed + 2),
+                        dtype=torch.float64).to(out.dtype).cuda()
+        del out
+        g1, g2 = torch.empty_like(a), torch.empty_like(b)
+        need = lib.cgtp_backward_workspace_bytes(plan._h, w.N)
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        bwd = {"workload": w.name + ":backward", "L": w.L, "N": w.N, "dtype": w.dtype,
+               "plan": plan.backward_query(), "kind": "cgtp_backward"}
+        bwd.update(_time_launches(lambda st: lib.cgtp_backward(plan._h, a.data_ptr(), b.data_ptr(), g.data_ptr(),
+                                                               g1.data_ptr(), g2.data_ptr(), w.N, ws.data_ptr(),
+                                                               need, st.cuda_stream),
+                                  w.N, steps, warmup))
+        res["backward"] = bwd
+        del g, g1, g2, ws
+    else:
+        del out
     plan.close()
-    del out, a, b
+    del a, b
     torch.cuda.empty_cache()
     return res
 
@@ -311,6 +332,12 @@ def roofline(res):
     return out
 
 
+def backward_entry(rb):
+    log("  backward (both gradients) %.4f ms/step, %.4g pairs/s" % (rb["ms_per_step"], rb["value"]))
+    return {"value": round(rb["value"], 1), "unit": "pairs/s", "ms_per_step": round(rb["ms_per_step"], 4),
+            "roofline": roofline(rb)}
+
+
 def copy_probe(nbytes, reps=10):
     """Plain device-to-device copy of nbytes: the calibration for the HBM counters."""
     import torch
@@ -446,8 +473,11 @@ def main():
             log("timing %s" % w2.name)
             r2 = time_workload(w2, args.steps, args.warmup)
             log("  %.4f ms/step, %.4g pairs/s" % (r2["ms_per_step"], r2["value"]))
-            secondary.append({"workload": r2["workload"], "value": round(r2["value"], 1), "unit": "pairs/s",
-                              "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)})
+            entry = {"workload": r2["workload"], "value": round(r2["value"], 1), "unit": "pairs/s",
+                     "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)}
+            if "backward" in r2:
+                entry["backward"] = backward_entry(r2["backward"])
+            secondary.append(entry)
     channels = []
     if args.channels and args.channels != "none":
         by_ch = {x.name: x for x in cgtp_inputs.CHANNEL_WORKLOADS}
@@ -510,6 +540,7 @@ def main():
         "config": {"workload": w.name, "L": w.L, "pairs": w.N, "outputs_per_pair": w.n_outputs,
                    "grid": "per-block minimal exact Gauss-Legendre x FFT", "cover": "scalar-scalar + cross"},
         "roofline": roofline(main_res),
+        "backward": backward_entry(main_res["backward"]) if "backward" in main_res else None,
         "secondary": secondary,
         "channels": channels,
         "istp": istp,

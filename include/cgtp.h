@@ -181,6 +181,16 @@ int cgtp_backward(cgtp_plan_t plan, const void *x1, const void *x2, const void *
 /* Workspace bytes cgtp_backward needs for N pairs: 2 (L+1)^3 N elements; -1 for a NULL plan, N < 0 or overflow. */
 int64_t cgtp_backward_workspace_bytes(cgtp_plan_t plan, int64_t N);
 
+/*
+ * Model counts per pair of cgtp_backward (both gradients): the forward's
+ * algorithmic flops (cgtp_plan_query) plus the adjoint's extra work, i.e. the
+ * products' adjoint forms both factors' gradients (the products term twice)
+ * and the transposed synthesis costs what the lift does; compulsory bytes:
+ * x1, x2, grad_x1, grad_x2 and grad_out, each once.  Either pointer may be
+ * NULL.  CGTP_EINVAL for a NULL plan, CGTP_EUNSUP where cgtp_backward is.
+ */
+int cgtp_backward_query(cgtp_plan_t plan, double *flops_per_pair, double *bytes_per_pair);
+
 /* Number of paths of degree L: sum over l1, l2 <= L of 2 min(l1, l2) + 1; -1 for L < 0. */
 int64_t cgtp_num_paths(int32_t L);
 

@@ -70,6 +70,7 @@ def _load():
         "cgtp_forward_weighted": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, ctypes.POINTER(cgtp_channels), vp]),
         "cgtp_backward": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
         "cgtp_backward_workspace_bytes": (i64, [vp, i64]),
+        "cgtp_backward_query": (ctypes.c_int, [vp, dp, dp]),
         "cgtp_num_paths": (i64, [i32]),
         "cgtp_path_index": (i64, [i32, i32, i32, i32]),
         "cgtp_destroy": (ctypes.c_int, [vp]),
@@ -118,6 +119,7 @@ def _load():
 def exported_symbols():
     """Names of the C ABI entry points this binding expects."""
     return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_backward", "cgtp_backward_workspace_bytes",
+            "cgtp_backward_query",
             "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
@@ -176,6 +178,12 @@ def cgtp_backward(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int | Non
 
 def cgtp_backward_workspace_bytes(plan, N: int) -> int:
     return int(_load().cgtp_backward_workspace_bytes(plan, int(N)))
+
+
+def cgtp_backward_query(plan) -> dict:
+    fl, by = ctypes.c_double(), ctypes.c_double()
+    _check(_load().cgtp_backward_query(plan, ctypes.byref(fl), ctypes.byref(by)), "cgtp_backward_query")
+    return {"flops_per_pair": fl.value, "bytes_per_pair": by.value}
 
 
 def cgtp_num_paths(L: int) -> int:
@@ -433,6 +441,9 @@ class Plan:
         cgtp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), weights.data_ptr() if weights is not None else None,
                               out.data_ptr(), N, C, shared, per_pair, s.cuda_stream)
         return out
+
+    def backward_query(self) -> dict:
+        return cgtp_backward_query(self._h)
 
     def backward(self, x1, x2, grad_out, need_x1=True, need_x2=True, workspace=None, stream=None):
         """(grad_x1, grad_x2) of sum(grad_out * forward(x1, x2)); a gradient not asked for is None.

@@ -318,6 +318,13 @@ double block_flops(int j1, int j2) {
          + rec;                                  // recombination and 1/K
 }
 
+// Flops of a block's pointwise products (the products term of block_flops).
+double block_product_flops(int j1, int j2) {
+    const int J = j1 + j2;
+    const double R = J / 2 + 1, H = J + 1;
+    return R * H * (6 + ((j1 > 0 && j2 > 0) ? 60 : 0));
+}
+
 // Flops of lifting one input of degree j (nin series: 1 scalar, 4 scalar +
 // vector) to a grid of R north rings that blocks up to degree Jmax share:
 // latitude stage and longitude synthesis on the minimal exact longitudes
@@ -349,6 +356,7 @@ struct cgtp_plan_s {
     bool bwd_ok = true;     // every block fits the gradient kernel's LDS
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
+    double bwd_flops_per_pair = 0;
     double cross_cg = 0, dot_cg = 0;
 };
 
@@ -482,7 +490,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
         if (fabsl(cg_vec(1, q, -q, 0, 0) - (q == 0 ? -dc : dc)) > 1e-15L) return CGTP_EINVAL;
     p->dot_cg = (double)dc;
     // ---- blocks
-    double min_abs_K = 1e300, flops = 0;
+    double min_abs_K = 1e300, flops = 0, bwd_extra = 0;
     // lifts: (input, degree, n_theta, Phi) -> (north rings, largest J of the grid, series)
     std::map<std::array<int, 4>, std::array<int, 3>> lifts;
     blocks.clear();
@@ -525,6 +533,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.out_off = path_offset(L, j1, j2, b.d);
             b.path_off = (int32_t)path_index(L, j1, j2, b.d);
             flops += block_flops(j1, j2);
+            bwd_extra += block_product_flops(j1, j2);   // the products' adjoint yields both factors' gradients
             {
                 const int nin = b.kind == cgtp::kBlockCross ? 4 : 1;
                 for (int in = 0; in < 2; ++in) {
@@ -650,8 +659,13 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             blocks.push_back(b);
         }
     p->min_abs_K = min_abs_K;
-    for (const auto& kv : lifts) flops += lift_flops(kv.first[1], kv.second[0], kv.second[1], kv.second[2]);
+    double lflops = 0;
+    for (const auto& kv : lifts) lflops += lift_flops(kv.first[1], kv.second[0], kv.second[1], kv.second[2]);
+    flops += lflops;
     p->flops_per_pair = flops;
+    // gradients: the forward's work plus the adjoint's extra product term and
+    // the transposed synthesis, which costs what the lift does
+    p->bwd_flops_per_pair = flops + bwd_extra + lflops;
     p->bytes_per_pair = (double)sizeof(T) * (2.0 * (L + 1) * (L + 1) + std::pow((double)(L + 1), 4));
     // ---- launch classes: fewest pairs (heaviest blocks) first; inside, by cost
     std::map<int, std::vector<int>> by_pairs;
@@ -979,6 +993,16 @@ int cgtp_forward_weighted(cgtp_plan_t plan, const void* x1, const void* x2, cons
 }
 
 int64_t cgtp_num_paths(int32_t L) { return L < 0 ? -1 : path_index(L, L + 1, 0, 1); }
+
+int cgtp_backward_query(cgtp_plan_t plan, double* flops_per_pair, double* bytes_per_pair) {
+    if (!plan) return CGTP_EINVAL;
+    if (!plan->bwd_ok) return CGTP_EUNSUP;
+    const double esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const double nin = (double)(plan->L + 1) * (plan->L + 1);
+    if (flops_per_pair) *flops_per_pair = plan->bwd_flops_per_pair;
+    if (bytes_per_pair) *bytes_per_pair = esz * (4 * nin + nin * nin);
+    return CGTP_OK;
+}
 
 int64_t cgtp_backward_workspace_bytes(cgtp_plan_t plan, int64_t N) {
     if (!plan || N < 0) return -1;
