@@ -25,9 +25,13 @@
 //
 // One work-group computes one (j1, j2) block for one pair: the block's
 // contribution to the pair's gradient rows of degree j1 (x1) and j2 (x2),
-// written to a workspace; a second kernel sums the contributions over the
-// other degree in a fixed order.  The phases are work-group-wide task pools
-// separated by barriers; rings go bd.bwd_rings at a time.
+// written to a workspace; a last kernel sums the contributions over the other
+// degree in a fixed order.  The phases are work-group-wide task pools
+// separated by barriers; rings go bd.bwd_rings at a time.  Small blocks run
+// on 256-thread work-groups with the accumulator-entry gradients in LDS; large
+// ones on 768 threads with one column of entry gradients per thread in
+// registers (the LDS they would take limits large blocks to one work-group
+// per CU).
 
 #include <hip/hip_runtime.h>
 
@@ -42,18 +46,18 @@ namespace {
 
 using namespace ::cgtp::dev;
 
-template <typename T, int A, int B>
+template <typename T, int A, int B, bool SMALL>
 __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& bd, int64_t n,
                                          const T* __restrict__ x1, const T* __restrict__ x2,
                                          const T* __restrict__ gin, T* __restrict__ wrow, int L,
                                          unsigned char* smem) {
     using C = typename Cplx<T>::type;
-    using Coef4 = typename Cplx<T>::acc4;
     constexpr int Phi = A * B;
     constexpr int H = Phi / 2 + 1;
     constexpr int BP = B + 1;
     constexpr int FS = slot_stride(A, B);
-    constexpr int NT = kBwdThreads;
+    constexpr int NT = SMALL ? kBwdSmallThreads : kBwdThreads;
+    constexpr int MR = SMALL ? 1 : BwdMaxRows<T>::value;   // register-held rows (large variant)
     const int tid = threadIdx.x;
     const int j1 = bd.j1, j2 = bd.j2, J = bd.J, R = bd.R, d = bd.d, G = bd.bwd_rings;
     const bool cross = bd.kind == kBlockCross;
@@ -65,28 +69,23 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     const int64_t nout = (int64_t)nin * nin;
     const int nrows = (J - d) / 2 + 1;
     auto tmin = [&](int mp) { return mp > d ? (mp - d + 1) / 2 : 0; };
-    auto rows_of = [&](int mp) { return nrows - tmin(mp); };
 
     const BwdLayout ly = bwd_layout(bd, (int)sizeof(T), G);
-    T* lc = reinterpret_cast<T*>(smem + ly.lc);        // [3][n1] then [3][n2]
-    C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);      // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
-    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);      // [slot][longitude n]: the pair's lifted coefficients
-    C* cacc = reinterpret_cast<C*>(smem + ly.cacc);    // [slot][longitude n]: their gradients, summed over rings
-    T* bg = reinterpret_cast<T*>(smem + ly.bg);        // accumulator-entry gradients, compact
-    int* moff = reinterpret_cast<int*>(smem + ly.moff);
-    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);    // [ring of the group][kBwdSlots], pass layout
+    T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
+    C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
+    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [slot][longitude n]: the pair's lifted coefficients
+    C* cacc = reinterpret_cast<C*>(smem + ly.cacc);      // [slot][longitude n]: their gradients, summed over rings
+    int* rowoff = reinterpret_cast<int*>(smem + ly.rowoff);   // first weight of |m| in a ring's row
+    T* wst = reinterpret_cast<T*>(smem + ly.wst);        // [ring of the group][|m|, row]: 2 w_r P^|m|_l3(x_r)
+    T* prs = reinterpret_cast<T*>(smem + ly.prs);        // [ring of the group][input][longitude n]: P_j^|m(n)|
+    int* colb = reinterpret_cast<int*>(smem + ly.colb);  // small variant: first entry gradient of signed m
+    T* bg = reinterpret_cast<T*>(smem + ly.bg);          // small variant: [signed m][component][row]
+    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [ring of the group][kBwdSlots], pass layout
     auto slot = [&](int r, int s) -> C* { return fbuf + (size_t)(r * kBwdSlots + s) * FS; };
     const int zs0 = nslot;              // slots of the analysis gradients (spectra)
     const int zg0 = kBwdSlots - 2;      // slots of the product gradients (circle)
 
-    // normalised P_j^|m| at the order m that longitude index nn carries in the
-    // synthesis (Phi > 2 j: nn <= Phi / 2 is m = nn), zero for |m| > j
-    auto pval = [&](int ring, int j, int nn) -> T {
-        const int m = nn <= Phi / 2 ? nn : nn - Phi, am = m < 0 ? -m : m;
-        return am <= j ? tb.pbar[bd.pbar_off + (size_t)ring * bd.pbar_stride + j * (j + 1) / 2 + am] : (T)0;
-    };
-
-    // ---- set-up: couplings, twiddles, entry offsets per |m|, cleared sums
+    // ---- set-up: couplings, twiddles, weight-row offsets, cleared sums
     for (int e = tid; e < 3 * n1; e += NT) lc[e] = tb.lcg[3 * j1 * j1 + e];
     for (int e = tid; e < 3 * n2; e += NT) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
     {
@@ -96,14 +95,20 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     if (tid == 0) {
         int o = 0;
         for (int mp = 0; mp <= J; ++mp) {
-            moff[mp] = o;
-            o += rows_of(mp) * (mp == 0 ? 1 : 2) * ncomp;
+            rowoff[mp] = o;
+            o += nrows - tmin(mp);
         }
-        moff[J + 1] = o;
+        rowoff[J + 1] = o;
+        if (SMALL) {
+            o = 0;
+            for (int sm = 0; sm <= 2 * J; ++sm) {
+                colb[sm] = o;
+                o += ncomp * (nrows - tmin(sm < J ? J - sm : sm - J));
+            }
+            colb[2 * J + 1] = o;
+        }
     }
-    for (int e = tid; e < ly.nbg; e += NT) bg[e] = (T)0;
     for (int e = tid; e < nslot * Phi; e += NT) cacc[e] = cmk<C>((T)0, (T)0);
-    __syncthreads();
     // ---- the pair's lifted coefficients, as the forward forms them:
     //   even slot: (x_m, C^{j, m}_{j, m, 1, 0} x_m), odd slot: (C^{j,m-1}_{j,m,1,-1}
     //   x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1}), times (-1)^m for negative m;
@@ -117,7 +122,7 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         if (am <= j) {
             const int mj = m + j;
             const T* xrow = (first ? x1 : x2) + n * nin + j * j;
-            const T* lcj = first ? lc : lc + 3 * n1;
+            const T* lcj = first ? tb.lcg + 3 * j1 * j1 : tb.lcg + 3 * j2 * j2;
             const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
             if (!cross || (s & 1) == 0) {
                 const T xm = sg * xrow[mj];
@@ -130,57 +135,77 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         }
         cvn[e] = val;
     }
-    // ---- transpose of the end phase.  Output o of the block is sum_k w_k e_k
-    // over up to three accumulator entries e_k (given for pair 0 in the forward
-    // plan's tile layout); each entry feeds one output, so its gradient is
-    // w_k g_o.  Zero-weight placeholder terms are skipped.
-    {
-        const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef) + bd.coef_off;
-        const int4* coefi = reinterpret_cast<const int4*>(tb.coefi) + bd.coef_off;
-        const TileDesc* td = tb.tdesc + bd.tdesc_off;
-        const T* grow = gin + n * nout + bd.out_off;
-        const int lgC = bd.lg_pairs + (cross ? 2 : 0);   // log2(columns per sign) of the forward tiling
-        for (int o = tid; o < n1 * n2; o += NT) {
-            const Coef4 cf = coef4[o];
-            const int4 ix = coefi[o];
-            const T gv = grow[o];
-            const T w3[3] = {cf.x, cf.y, cf.z};
-            const int e3[3] = {ix.x, ix.y, ix.z};
-            const int nterm = (ix.w & 1) ? 1 : 3;
-            for (int k = 0; k < nterm; ++k) {
-                if (w3[k] == (T)0) continue;
-                const int u = e3[k] / tile_stride<T>(), lin = e3[k] - u * tile_stride<T>();
-                // accumulator layout: lane = lin / 4 (column lane % 16, quarter lane / 16),
-                // element q = lin % 4 of the lane
-                const int lane = lin >> 2, q = lin & 3;
-                const int r = sizeof(T) == 4 ? 4 * (lane >> 4) + q : (lane >> 4) + 4 * q;
-                const int code = td[u].code;
-                const int mp = code >> 16, rt = (code >> 8) & 0xff, ct = code & 0xff;
-                const int row = 16 * rt + r, col = 16 * ct + (lane & 15);
-                const int sg = col >> lgC, comp = (col >> bd.lg_pairs) & (ncomp - 1);
-                bg[moff[mp] + (sg * ncomp + comp) * rows_of(mp) + row] = w3[k] * gv;
-            }
+    // ---- transpose of the end phase.  Output (j3, m3) of the block is a
+    // weighted sum of accumulator entries: an even path reads component 0 at
+    // (l3 = j3, m3); an odd path reads, for q = -1, 0, +1, component 2, 1, 3 at
+    // (l3 = j3 - 1, m3 - q) with the plan's term q + 1.  Each entry thus feeds
+    // one output, and its gradient is that term's weight times the output's
+    // gradient.  Column c = (m + J) ncomp + comp holds the entries of rows
+    // l3 = d + 2 (tmin(|m|) + i), i < the rows of |m|: in LDS (small variant),
+    // or in the registers of thread c (large variant).
+    const int ncols = (2 * J + 1) * ncomp;
+    const T* coefs = tb.coef + (size_t)bd.coef_off * 4;
+    const T* grow = gin + n * nout + bd.out_off;
+    auto entry_grad = [&](int comp, int m, int l3) -> T {
+        const int q = comp == 2 ? -1 : (comp == 3 ? 1 : 0);
+        const int j3 = comp == 0 ? l3 : l3 + 1, m3 = m + q;
+        if (j3 > J) return (T)0;
+        const int o = j3 * j3 - d * d + j3 + m3;
+        return coefs[4 * o + (comp == 0 ? 0 : q + 1)] * grow[o];
+    };
+    T bgr[MR];
+    if constexpr (SMALL) {
+        __syncthreads();   // colb
+        for (int c = tid; c < ncols; c += NT) {
+            const int comp = c % ncomp, sm = c / ncomp, m = sm - J, mp = m < 0 ? -m : m;
+            const int nr = nrows - tmin(mp), l30 = d + 2 * tmin(mp);
+            T* col = bg + colb[sm] + comp * nr;
+            for (int i = 0; i < nr; ++i) col[i] = entry_grad(comp, m, l30 + 2 * i);
         }
+    } else {
+        const int c = tid;
+        const int comp = c % ncomp, m = c / ncomp - J, mp = m < 0 ? -m : m;
+        const int nr = c < ncols ? nrows - tmin(mp) : 0;
+        const int l30 = d + 2 * tmin(mp);
+#pragma unroll
+        for (int i = 0; i < MR; ++i) bgr[i] = i < nr ? entry_grad(comp, m, l30 + 2 * i) : (T)0;
     }
     __syncthreads();
 
-    const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
-
     for (int rg0 = 0; rg0 < R; rg0 += G) {
         const int nrg = (R - rg0) < G ? (R - rg0) : G;
-        // ---- 1. synthesis pass 1 of the lifts (as the forward); clear the
-        // analysis-gradient slots (orders past J stay zero)
+        // ---- 0. the group's weights and Legendre values, staged
+        for (int e = tid; e < nrg * (J + 1) * nrows; e += NT) {
+            const int i = e % nrows, f = e / nrows, mp = f % (J + 1), r = f / (J + 1);
+            const int t0 = tmin(mp);
+            if (i < nrows - t0)
+                wst[r * ly.nwr + rowoff[mp] + i] =
+                    tb.wtab[bd.wtab_off + (mp * bd.rpad + rg0 + r) * bd.wrow + (d + 2 * t0 - (J & 1)) / 2 + i];
+        }
+        for (int e = tid; e < nrg * 2 * Phi; e += NT) {
+            const int nn = e % Phi, f = e / Phi, r = f >> 1;
+            const int j = (f & 1) ? j2 : j1;
+            const int m = nn <= Phi / 2 ? nn : nn - Phi, am = m < 0 ? -m : m;
+            prs[e] = am <= j ? tb.pbar[bd.pbar_off + (size_t)(rg0 + r) * bd.pbar_stride + j * (j + 1) / 2 + am]
+                             : (T)0;
+        }
+        // the analysis-gradient slots are cleared (orders past J stay zero)
+        for (int e = tid; e < nrg * nz * FS; e += NT) {
+            const int r = e / (nz * FS), rest = e - r * nz * FS;
+            slot(r, zs0)[rest] = cmk<C>((T)0, (T)0);   // nz consecutive slots
+        }
+        __syncthreads();
+        // ---- 1. synthesis pass 1 of the lifts (as the forward)
         for (int task = tid; task < nrg * nslot * A; task += NT) {
             const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
             const bool first = cross ? (s < 2) : (s == 0);
-            const int j = first ? j1 : j2;
             const C* cv = cvn + (size_t)s * Phi + t;
+            const T* pr = prs + (size_t)(2 * r + (first ? 0 : 1)) * Phi + t;
             C v[B];
 #pragma unroll
             for (int i = 0; i < B; ++i) {
                 const C c = cv[A * i];
-                const T pv = pval(rg0 + r, j, t + A * i);
+                const T pv = pr[A * i];
                 v[i] = cmk<C>(c.x * pv, c.y * pv);
             }
             Dft<B, true, C>::run(v);
@@ -189,45 +214,37 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[0] : cmulc(v[k2], twr[k2]);
         }
-        for (int e = tid; e < nrg * nz * FS; e += NT) {
-            const int r = e / (nz * FS), rest = e - r * nz * FS;
-            slot(r, zs0)[rest] = cmk<C>((T)0, (T)0);   // nz consecutive slots
-        }
-        __syncthreads();
-        // ---- 2. synthesis pass 2 (in place)
-        for (int task = tid; task < nrg * nslot * B; task += NT) {
-            const int k2 = task % B, f = task / B, s = f % nslot, r = f / nslot;
-            C* fb = slot(r, s) + k2;
-            C u[A];
-#pragma unroll
-            for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
-            Dft<A, true, C>::run(u);
-#pragma unroll
-            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
-        }
-        // ---- 3. transpose of the projection (other slots than pass 2's): the
-        // spectrum gradient at (ring, component, signed m) is the sum over the
+        // ---- 3. transpose of the projection (other slots than the synthesis'):
+        // the spectrum gradient at (ring, component, signed m) is the sum over the
         // rows l3 of the weight 2 w_r P^|m|_l3(x_r) times the entry gradient; it
         // goes to the real (even component) or imaginary (odd) part at the
         // pass-layout position of m
-        for (int task = tid; task < nrg * (2 * J + 1) * ncomp; task += NT) {
-            const int comp = task % ncomp, f = task / ncomp, sm = f % (2 * J + 1), r = f / (2 * J + 1);
-            const int m = sm - J, mp = m < 0 ? -m : m;
-            const int nr = rows_of(mp), t0 = tmin(mp);
-            const T* gcol = bg + moff[mp] + ((m < 0 ? ncomp : 0) + comp) * nr;
-            // weight of (|m|, ring, l3 = d + 2 (t0 + i)) at [|m|][ring][(l3 - parity of J) / 2]
-            const int w0 = (mp * bd.rpad + rg0 + r) * bd.wrow + (d + 2 * t0 - (J & 1)) / 2;
-            T acc = (T)0;
-            for (int i = 0; i < nr; ++i) acc += buffer_load<T>(wrsrc, (w0 + i) * (int)sizeof(T), 0) * gcol[i];
-            const int k = m < 0 ? Phi + m : m;
-            T* dst = reinterpret_cast<T*>(slot(r, zs0 + (comp >> 1)) + (k + k / B));
-            dst[comp & 1] = acc;
+        for (int c = tid; c < ncols; c += NT) {
+            const int comp = c % ncomp, sm = c / ncomp, m = sm - J, mp = m < 0 ? -m : m;
+            const int nr = nrows - tmin(mp);
+            const int kk = m < 0 ? Phi + m : m;
+            for (int r = 0; r < nrg; ++r) {
+                const T* w = wst + r * ly.nwr + rowoff[mp];
+                T acc = (T)0;
+                if constexpr (SMALL) {
+                    const T* col = bg + colb[sm] + comp * nr;
+                    for (int i = 0; i < nr; ++i) acc += w[i] * col[i];
+                } else {
+#pragma unroll
+                    for (int i = 0; i < MR; ++i)
+                        if (i < nr) acc += w[i] * bgr[i];
+                }
+                T* dst = reinterpret_cast<T*>(slot(r, zs0 + (comp >> 1)) + (kk + kk / B));
+                dst[comp & 1] = acc;
+            }
         }
         __syncthreads();
-        // ---- 4. transpose of analysis pass 2: inverse DFT down the columns
-        for (int task = tid; task < nrg * nz * B; task += NT) {
-            const int k2 = task % B, f = task / B, z = f % nz, r = f / nz;
-            C* fb = slot(r, zs0 + z) + k2;
+        // ---- 2 and 4. synthesis pass 2 of the lifts and the transpose of analysis
+        // pass 2 of the spectrum gradients: both inverse DFTs down the columns, in
+        // place, over the consecutive slots 0 .. nslot + nz - 1
+        for (int task = tid; task < nrg * (nslot + nz) * B; task += NT) {
+            const int k2 = task % B, f = task / B, s = f % (nslot + nz), r = f / (nslot + nz);
+            C* fb = slot(r, s) + k2;
             C u[A];
 #pragma unroll
             for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
@@ -363,17 +380,17 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         for (int task = tid; task < nrg * nslot * A; task += NT) {
             const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
             const bool first = cross ? (s < 2) : (s == 0);
-            const int j = first ? j1 : j2;
             const C* row = slot(r, s) + t * BP;
             const C* twr = tw2 + t * BP;
             C v[B];
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) v[k2] = k2 == 0 ? row[0] : cmul(row[k2], twr[k2]);
             Dft<B, false, C>::run(v);
+            const T* pr = prs + (size_t)(2 * r + (first ? 0 : 1)) * Phi + t;
             C* out = slot(r, nslot + s);
 #pragma unroll
             for (int i = 0; i < B; ++i) {
-                const T pv = pval(rg0 + r, j, t + A * i);
+                const T pv = pr[A * i];
                 out[t + A * i] = cmk<C>(v[i].x * pv, v[i].y * pv);
             }
         }
@@ -411,11 +428,10 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 }
 
 // Work-group -> (block, pair); the block body for the block's longitude size.
-template <typename T>
-__global__ __launch_bounds__(kBwdThreads) void bwd_kernel(Tables<T> tb, const int32_t* __restrict__ list,
-                                                           const T* __restrict__ x1, const T* __restrict__ x2,
-                                                           const T* __restrict__ g, T* __restrict__ ws, int64_t N,
-                                                           int L) {
+template <typename T, bool SMALL>
+__global__ __launch_bounds__(SMALL ? kBwdSmallThreads : kBwdThreads) void bwd_kernel(
+        Tables<T> tb, const int32_t* __restrict__ list, const T* __restrict__ x1, const T* __restrict__ x2,
+        const T* __restrict__ g, T* __restrict__ ws, int64_t N, int L) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int64_t wg = blockIdx.x;
     const int li = (int)(wg / N);
@@ -423,7 +439,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_kernel(Tables<T> tb, const in
     const BlockDesc bd = tb.blocks[list[li]];
     T* wrow = ws + bwd_block_off(L, bd.j1, bd.j2) * N + n * (2 * (bd.j1 + bd.j2) + 2);
 #define CGTP_BCASE(PHI, A_, B_) \
-    case PHI: bwd_body<T, A_, B_>(tb, bd, n, x1, x2, g, wrow, L, smem); break;
+    case PHI: bwd_body<T, A_, B_, SMALL>(tb, bd, n, x1, x2, g, wrow, L, smem); break;
     switch (bd.Phi) {
         CGTP_BCASE(1, 1, 1)
         CGTP_BCASE(2, 2, 1)
@@ -480,22 +496,32 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const T* __restrict__ w
     dst[n * nin + c] = sum;
 }
 
-template <typename T>
-int launch_bwd(const Tables<T>& tb, const int32_t* list, int lds, const T* x1, const T* x2, const T* g, T* gx1,
-               T* gx2, T* ws, int64_t N, int L, void* stream) {
-    const int64_t nblocks = (int64_t)(L + 1) * (L + 1);
+template <typename T, bool SMALL>
+int launch_variant(const Tables<T>& tb, const int32_t* list, int64_t nblocks, int lds, const T* x1, const T* x2,
+                   const T* g, T* ws, int64_t N, int L, void* stream) {
     const int64_t grid = nblocks * N;
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)bwd_kernel<T>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        hipError_t e =
+            hipFuncSetAttribute((const void*)bwd_kernel<T, SMALL>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return (int)e;
     }
-    hipLaunchKernelGGL(bwd_kernel<T>, dim3((unsigned)grid), dim3(kBwdThreads), lds, (hipStream_t)stream, tb, list,
-                       x1, x2, g, ws, N, L);
-    int err = (int)hipGetLastError();
+    hipLaunchKernelGGL((bwd_kernel<T, SMALL>), dim3((unsigned)grid), dim3(SMALL ? kBwdSmallThreads : kBwdThreads),
+                       lds, (hipStream_t)stream, tb, list, x1, x2, g, ws, N, L);
+    return (int)hipGetLastError();
+}
+
+template <typename T>
+int launch_bwd(const Tables<T>& tb, const BwdLaunch& bl, const T* x1, const T* x2, const T* g, T* gx1, T* gx2,
+               T* ws, int64_t N, int L, void* stream) {
+    int err = launch_variant<T, true>(tb, bl.block_list, bl.nsmall, bl.lds_small, x1, x2, g, ws, N, L, stream);
+    if (err) return err;
+    err = launch_variant<T, false>(tb, bl.block_list + bl.nsmall, bl.nlarge, bl.lds_large, x1, x2, g, ws, N, L,
+                                   stream);
     if (err) return err;
     const int64_t rgrid = (2 * N * (int64_t)(L + 1) * (L + 1) + 255) / 256;
+    if (rgrid <= 0) return 0;
     if (rgrid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(bwd_reduce_kernel<T>, dim3((unsigned)rgrid), dim3(256), 0, (hipStream_t)stream, ws, gx1, gx2,
                        N, L);
@@ -504,14 +530,13 @@ int launch_bwd(const Tables<T>& tb, const int32_t* list, int lds, const T* x1, c
 
 }  // namespace
 
-int launch_backward_f32(const Tables<float>& tb, const int32_t* list, int lds, const float* x1, const float* x2,
+int launch_backward_f32(const Tables<float>& tb, const BwdLaunch& bl, const float* x1, const float* x2,
                         const float* g, float* gx1, float* gx2, float* ws, int64_t N, int L, void* stream) {
-    return launch_bwd<float>(tb, list, lds, x1, x2, g, gx1, gx2, ws, N, L, stream);
+    return launch_bwd<float>(tb, bl, x1, x2, g, gx1, gx2, ws, N, L, stream);
 }
-int launch_backward_f64(const Tables<double>& tb, const int32_t* list, int lds, const double* x1,
-                        const double* x2, const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L,
-                        void* stream) {
-    return launch_bwd<double>(tb, list, lds, x1, x2, g, gx1, gx2, ws, N, L, stream);
+int launch_backward_f64(const Tables<double>& tb, const BwdLaunch& bl, const double* x1, const double* x2,
+                        const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L, void* stream) {
+    return launch_bwd<double>(tb, bl, x1, x2, g, gx1, gx2, ws, N, L, stream);
 }
 
 }  // namespace cgtp

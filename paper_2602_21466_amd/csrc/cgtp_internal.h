@@ -184,17 +184,33 @@ struct TileGeom {
 // ---------------------------------------------------------------- gradients
 //
 // The gradient kernel (cgtp_backward.hip) runs one work-group per (block,
-// pair).  Its LDS, in byte offsets: couplings [3][n1 + n2], twiddles in pass
-// layout, the pair's lifted coefficients and their gradients ([slot][Phi]
-// each), the accumulator-entry gradients (compact: per |m|, [column (sign,
-// component)][row]), their offsets per |m|, and per ring of a group
-// kBwdSlots transforms.
-constexpr int kBwdThreads = 256;
+// pair), in two variants.  Both need the gradients of the projection's
+// accumulator entries, per column (|m|, sign, component) all its rows l3:
+//   small blocks, (2 J + 1) * components <= kBwdSmallThreads: 256 threads,
+//     entry gradients in LDS (compact, column by column);
+//   large blocks: 768 threads, one column per thread in registers.
+// LDS, in byte offsets: couplings [3][n1 + n2], twiddles in pass layout, the
+// pair's lifted coefficients and their gradients ([slot][Phi] each), the first
+// row of every |m| in a ring's weight rows, (small variant) each signed m's
+// first entry gradient and the entry gradients, then per ring group the
+// weights [ring][sum over |m| of its rows], the Legendre values
+// [ring][input][Phi] and kBwdSlots transforms per ring.
+constexpr int kBwdThreads = 768;         // large variant
+constexpr int kBwdSmallThreads = 256;    // small variant
+constexpr int kBwdSmallLds = 40 * 1024;  // small variant: ring groups sized for four work-groups per CU
 constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
+template <typename T> struct BwdMaxRows;
+template <> struct BwdMaxRows<float> { static constexpr int value = 33; };    // rows l3 of a block at L <= 32
+template <> struct BwdMaxRows<double> { static constexpr int value = 20; };   // fp64 plans stop at L = 19
 struct BwdLayout {
-    int lc, tw2, cvn, cacc, bg, moff, fbuf, end;
-    int nbg;   // accumulator entries of one pair
+    int lc, tw2, cvn, cacc, rowoff, colb, bg, wst, prs, fbuf, end;
+    int nwr;   // weights per ring: sum over |m| of the rows l3 >= |m|
+    int nbg;   // entry gradients (small variant)
 };
+__host__ __device__ inline int bwd_columns(const BlockDesc& b) {
+    return (2 * b.J + 1) * (b.kind == kBlockCross ? 4 : 1);
+}
+__host__ __device__ inline bool bwd_small(const BlockDesc& b) { return bwd_columns(b) <= kBwdSmallThreads; }
 __host__ __device__ inline int bwd_align16(int v) { return (v + 15) & ~15; }
 __host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int rings) {
     const int csz = 2 * esz;
@@ -202,17 +218,21 @@ __host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int
     const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
     const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     const int nrows = (b.J - b.d) / 2 + 1;
+    const bool small = bwd_small(b);
     BwdLayout l;
-    l.nbg = 0;
-    for (int mp = 0; mp <= b.J; ++mp)
-        l.nbg += (nrows - (mp > b.d ? (mp - b.d + 1) / 2 : 0)) * (mp == 0 ? 1 : 2) * ncomp;
+    l.nwr = 0;
+    for (int mp = 0; mp <= b.J; ++mp) l.nwr += nrows - (mp > b.d ? (mp - b.d + 1) / 2 : 0);
+    l.nbg = small ? ncomp * (2 * l.nwr - nrows) : 0;
     int o = 0;
     l.lc = o; o = bwd_align16(o + esz * 3 * (n1 + n2));
     l.tw2 = o; o = bwd_align16(o + csz * b.A * (b.B + 1));
     l.cvn = o; o = bwd_align16(o + csz * nslot * b.Phi);
     l.cacc = o; o = bwd_align16(o + csz * nslot * b.Phi);
+    l.rowoff = o; o = bwd_align16(o + 4 * (b.J + 2));
+    l.colb = o; o = bwd_align16(o + (small ? 4 * (2 * b.J + 2) : 0));
     l.bg = o; o = bwd_align16(o + esz * l.nbg);
-    l.moff = o; o = bwd_align16(o + 4 * (b.J + 2));
+    l.wst = o; o = bwd_align16(o + esz * rings * l.nwr);
+    l.prs = o; o = bwd_align16(o + esz * rings * 2 * b.Phi);
     l.fbuf = o; o += csz * rings * kBwdSlots * slot_stride(b.A, b.B);
     l.end = o;
     return l;
@@ -255,13 +275,17 @@ int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* block_li
                                int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
                                int L, const ChanArgs<double>& ch, void* stream);
 
-// Gradients: the per-block kernel over (L + 1)^2 blocks x N pairs into ws,
-// then the sums over the other degree into gx1 / gx2 (either may be NULL).
-int launch_backward_f32(const Tables<float>& tb, const int32_t* block_list, int lds_bytes, const float* x1,
-                        const float* x2, const float* g, float* gx1, float* gx2, float* ws, int64_t N, int L,
-                        void* stream);
-int launch_backward_f64(const Tables<double>& tb, const int32_t* block_list, int lds_bytes, const double* x1,
-                        const double* x2, const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L,
-                        void* stream);
+// Gradients: the per-block kernels (block_list: the nsmall small-variant
+// blocks, then the nlarge others) over their blocks x N pairs into ws, then
+// the sums over the other degree into gx1 / gx2 (either may be NULL).
+struct BwdLaunch {
+    const int32_t* block_list;
+    int32_t nsmall, nlarge;
+    int32_t lds_small, lds_large;
+};
+int launch_backward_f32(const Tables<float>& tb, const BwdLaunch& bl, const float* x1, const float* x2,
+                        const float* g, float* gx1, float* gx2, float* ws, int64_t N, int L, void* stream);
+int launch_backward_f64(const Tables<double>& tb, const BwdLaunch& bl, const double* x1, const double* x2,
+                        const double* g, double* gx1, double* gx2, double* ws, int64_t N, int L, void* stream);
 
 }  // namespace cgtp

@@ -352,8 +352,11 @@ struct cgtp_plan_s {
     std::vector<Cls> classes;
     int lds_bytes = 0;      // dynamic LDS of the plain kernel
     int lds_bytes_ch = 0;   // and of the channel kernel (with the shared second-input buffers)
-    int bwd_lds = 0;        // dynamic LDS of the gradient kernel
-    bool bwd_ok = true;     // every block fits the gradient kernel's LDS
+    int bwd_lds_small = 0, bwd_lds_large = 0;   // dynamic LDS of the gradient kernel's two variants
+    int bwd_nsmall = 0;     // blocks of the small variant: the first entries of the gradient block list
+    int bwd_list_off = 0;   // the gradient block list's offset in the uploaded block lists
+    const int32_t* d_bwd_list = nullptr;
+    bool bwd_ok = true;     // every block fits one of the gradient kernel's variants
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
     double bwd_flops_per_pair = 0;
@@ -562,12 +565,25 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             const int lds_x2 = lds_for<T>(b, pairs, true);
             b.x2share = lds_x2 <= cgtp::kLdsBudget ? 1 : 0;
             p->lds_bytes_ch = std::max(p->lds_bytes_ch, b.x2share ? lds_x2 : b.lds_bytes);
-            // gradient kernel: as many rings per group (4, 2, 1) as its LDS allows
+            // gradient kernel: the largest ring group (8, 4, 2, 1) whose LDS fits, for
+            // small blocks within kBwdSmallLds where one does
             b.bwd_rings = 0;
-            for (int G = 4; G >= 1 && !b.bwd_rings; G /= 2)
-                if (cgtp::bwd_layout(b, (int)sizeof(T), G).end <= cgtp::kLdsBudget) b.bwd_rings = G;
+            {
+                const bool small = cgtp::bwd_small(b);
+                for (int pass = small ? 0 : 1; pass < 2 && !b.bwd_rings; ++pass)
+                    for (int G = 8; G >= 1 && !b.bwd_rings; G /= 2)
+                        if (cgtp::bwd_layout(b, (int)sizeof(T), G).end <= (pass ? cgtp::kLdsBudget : cgtp::kBwdSmallLds))
+                            b.bwd_rings = G;
+                // the large variant's register-held entry gradients: one column per thread
+                if (!small && (cgtp::bwd_columns(b) > cgtp::kBwdThreads ||
+                               (b.J - b.d) / 2 + 1 > cgtp::BwdMaxRows<T>::value))
+                    b.bwd_rings = 0;
+                if (b.bwd_rings) {
+                    int& lds = small ? p->bwd_lds_small : p->bwd_lds_large;
+                    lds = std::max(lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings).end);
+                }
+            }
             if (b.bwd_rings == 0) p->bwd_ok = false;
-            else p->bwd_lds = std::max(p->bwd_lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings).end);
             // MFMA tiles in the order the waves take them: by |m|, row tile, column tile
             b.tdesc_off = (int)h.tdesc.size();
             {
@@ -682,6 +698,20 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
         p->classes.push_back({kv.first, (int)list.size(), (int)v.size()});
         list.insert(list.end(), v.begin(), v.end());
     }
+    // gradient kernel's block list, after the forward's: the small variant's
+    // blocks, then the large variant's, each heaviest first
+    p->bwd_list_off = (int)list.size();
+    std::vector<int> bs, bl;
+    for (int i = 0; i < (int)blocks.size(); ++i) (cgtp::bwd_small(blocks[i]) ? bs : bl).push_back(i);
+    auto heavier = [&](int a, int b) {
+        const BlockDesc &x = blocks[a], &y = blocks[b];
+        return (double)x.R * x.Phi * (x.J + 1) > (double)y.R * y.Phi * (y.J + 1);
+    };
+    std::stable_sort(bs.begin(), bs.end(), heavier);
+    std::stable_sort(bl.begin(), bl.end(), heavier);
+    p->bwd_nsmall = (int)bs.size();
+    list.insert(list.end(), bs.begin(), bs.end());
+    list.insert(list.end(), bl.begin(), bl.end());
     return CGTP_OK;
 }
 
@@ -737,6 +767,7 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
+    p->d_bwd_list = p->d_list + p->bwd_list_off;
     return CGTP_OK;
 }
 
@@ -1048,15 +1079,16 @@ int cgtp_backward(cgtp_plan_t plan, const void* x1, const void* x2, const void* 
     if (dev != plan->device) return CGTP_EINVAL;
     // one work-group per (block, pair)
     if ((int64_t)nin * N > 0x7fffffffLL) return CGTP_EUNSUP;
+    const int nblocks = (L + 1) * (L + 1);
+    const cgtp::BwdLaunch bl{plan->d_bwd_list, plan->bwd_nsmall, nblocks - plan->bwd_nsmall, plan->bwd_lds_small,
+                             plan->bwd_lds_large};
     int err;
     if (plan->grid.dtype == CGTP_FP32)
-        err = cgtp::launch_backward_f32(plan->tf, plan->d_list, plan->bwd_lds, (const float*)x1, (const float*)x2,
-                                        (const float*)grad_out, (float*)grad_x1, (float*)grad_x2, (float*)workspace,
-                                        N, L, hip_stream);
+        err = cgtp::launch_backward_f32(plan->tf, bl, (const float*)x1, (const float*)x2, (const float*)grad_out,
+                                        (float*)grad_x1, (float*)grad_x2, (float*)workspace, N, L, hip_stream);
     else
-        err = cgtp::launch_backward_f64(plan->td, plan->d_list, plan->bwd_lds, (const double*)x1,
-                                        (const double*)x2, (const double*)grad_out, (double*)grad_x1,
-                                        (double*)grad_x2, (double*)workspace, N, L, hip_stream);
+        err = cgtp::launch_backward_f64(plan->td, bl, (const double*)x1, (const double*)x2, (const double*)grad_out,
+                                        (double*)grad_x1, (double*)grad_x2, (double*)workspace, N, L, hip_stream);
     if (err != 0) {
         g_last_hip_error = err;
         return CGTP_EHIP;
