@@ -14,6 +14,7 @@ bilinearity: (a + ib) (x) (c + id) = a(x)c - b(x)d + i (a(x)d + b(x)c).
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import subprocess
 
@@ -133,6 +134,44 @@ def cgtp_complex(L: int, x1, x2, threads: int = 0) -> np.ndarray:
     ri = cgtp(L, x1.real, x2.imag, threads)
     ir = cgtp(L, x1.imag, x2.real, threads)
     return (rr - ii) + 1j * (ri + ir)
+
+
+def _degree_to_real(l: int, c) -> np.ndarray:
+    """Real-basis coefficients [N, 2l + 1] of a real function's degree-l complex coefficients c [N, 2l + 1]:
+    r_0 = Re c_0, r_m = sqrt(2) Re c_{-m}, r_{-m} = sqrt(2) Im c_{-m} (m > 0), for the real harmonics
+    Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m (m > 0), Y_l^0 (m = 0), sqrt(2) (-1)^m Im Y_l^|m| (m < 0)."""
+    r = np.zeros(c.shape)
+    r[:, l] = c[:, l].real
+    for m in range(1, l + 1):
+        r[:, l + m] = math.sqrt(2.0) * c[:, l - m].real
+        r[:, l - m] = math.sqrt(2.0) * c[:, l - m].imag
+    return r
+
+
+def cgtp_real(L: int, r1, r2, threads: int = 0) -> np.ndarray:
+    """Full CGTP of real-basis rows r1, r2 [N, (L+1)^2], every path read back in the real basis; [N, (L+1)^4]
+    in cgtp's layout.
+
+    The inputs' complex-basis coefficients c = to_complex(r) are Hermitian.  With real Clebsch-Gordan
+    coefficients, path (l1, l2, l3) of two Hermitian inputs is Hermitian when l1 + l2 + l3 is even and
+    anti-Hermitian when it is odd (C^{l3,-m3}_{l1,-m1,l2,-m2} = (-1)^{l1+l2-l3} C^{l3 m3}_{l1 m1 l2 m2}); the
+    even paths are read back as they are, the odd ones after multiplication by i, which makes them Hermitian
+    (and the degree-1 path (1, 1, 1) the cross product over sqrt(2) in the real basis' (y, z, x) order).
+    """
+    from .istp import to_complex
+    c1 = to_complex(L, r1)
+    c2 = to_complex(L, r2)
+    z = cgtp_complex(L, c1, c2, threads)
+    out = np.empty(z.shape)
+    for l1 in range(L + 1):
+        for l2 in range(L + 1):
+            for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+                off = path_offset(L, l1, l2, l3)
+                blk = z[:, off:off + 2 * l3 + 1]
+                if (l1 + l2 + l3) % 2:
+                    blk = 1j * blk
+                out[:, off:off + 2 * l3 + 1] = _degree_to_real(l3, blk)
+    return out
 
 
 def table_build_seconds() -> float:
