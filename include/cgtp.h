@@ -191,6 +191,32 @@ int64_t cgtp_backward_workspace_bytes(cgtp_plan_t plan, int64_t N);
  */
 int cgtp_backward_query(cgtp_plan_t plan, double *flops_per_pair, double *bytes_per_pair);
 
+/*
+ * The full CGTP in the real spherical-harmonic basis (the paper works with real
+ * signals on the sphere, Section 3.3).  Real harmonics, Condon-Shortley phase
+ * kept, index l^2 + l + m:
+ *   Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m (m > 0),  Y_l^0 (m = 0),  sqrt(2) (-1)^m Im Y_l^|m| (m < 0).
+ * x1, x2 hold real-basis coefficients [N, (L+1)^2]; out [N, (L+1)^4] in
+ * cgtp_forward's layout holds every path in the real basis: the complex-basis
+ * CGTP of the inputs' (Hermitian) complex coefficients, path by path read back
+ * in the real basis, odd l1 + l2 + l3 paths (anti-Hermitian) after a factor i.
+ * So the even paths are the real Gaunt integrals over K (Theorem 4.2 read in the
+ * real basis) and path (1, 1, 1) is the cross product over sqrt(2) in the real
+ * basis' (y, z, x) order.  Runs three cgtp_forward products (Karatsuba's form of
+ * a complex product) between two conversion kernels.
+ *   workspace: caller-owned device memory, 256-byte aligned, at least
+ *   cgtp_real_workspace_bytes(plan, N) bytes: the converted inputs and two of
+ *   the three products (the third is formed in out, then read back in place).
+ * Rules otherwise as cgtp_forward; CGTP_EINVAL also for a short, misaligned or
+ * overlapping workspace.  Allocates nothing; asynchronous on hip_stream.
+ */
+int cgtp_forward_real(cgtp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
+                      int64_t workspace_bytes, void *hip_stream);
+
+/* Workspace bytes cgtp_forward_real needs for N pairs (6 N (L+1)^2 + 2 N (L+1)^4 elements, parts 256-byte
+   aligned); -1 for a NULL plan, N < 0 or overflow. */
+int64_t cgtp_real_workspace_bytes(cgtp_plan_t plan, int64_t N);
+
 /* Number of paths of degree L: sum over l1, l2 <= L of 2 min(l1, l2) + 1; -1 for L < 0. */
 int64_t cgtp_num_paths(int32_t L);
 

@@ -71,6 +71,8 @@ def _load():
         "cgtp_backward": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, vp, i64, vp]),
         "cgtp_backward_workspace_bytes": (i64, [vp, i64]),
         "cgtp_backward_query": (ctypes.c_int, [vp, dp, dp]),
+        "cgtp_forward_real": (ctypes.c_int, [vp, vp, vp, vp, i64, vp, i64, vp]),
+        "cgtp_real_workspace_bytes": (i64, [vp, i64]),
         "cgtp_num_paths": (i64, [i32]),
         "cgtp_path_index": (i64, [i32, i32, i32, i32]),
         "cgtp_destroy": (ctypes.c_int, [vp]),
@@ -119,7 +121,7 @@ def _load():
 def exported_symbols():
     """Names of the C ABI entry points this binding expects."""
     return ["cgtp_plan", "cgtp_forward", "cgtp_forward_weighted", "cgtp_backward", "cgtp_backward_workspace_bytes",
-            "cgtp_backward_query",
+            "cgtp_backward_query", "cgtp_forward_real", "cgtp_real_workspace_bytes",
             "cgtp_num_paths", "cgtp_path_index", "cgtp_destroy", "cgtp_num_outputs", "cgtp_path_offset",
             "cgtp_plan_query", "cgtp_strerror", "cgtp_last_hip_error", "cgtp_path_norm", "cgtp_wigner_9j",
             "cgtp_cg_vector", "cgtp_cg_zero", "cgtp_gauss_legendre", "cgtp_legendre", "cgtp_block_grid",
@@ -178,6 +180,18 @@ def cgtp_backward(plan, x1_ptr: int, x2_ptr: int, g_ptr: int, gx1_ptr: int | Non
 
 def cgtp_backward_workspace_bytes(plan, N: int) -> int:
     return int(_load().cgtp_backward_workspace_bytes(plan, int(N)))
+
+
+def cgtp_forward_real(plan, x1_ptr: int, x2_ptr: int, out_ptr: int, N: int, ws_ptr: int, ws_bytes: int,
+                      stream_ptr: int | None = None) -> None:
+    vpn = lambda p: ctypes.c_void_p(p) if p else None
+    rc = _load().cgtp_forward_real(plan, vpn(x1_ptr), vpn(x2_ptr), vpn(out_ptr), int(N), vpn(ws_ptr), int(ws_bytes),
+                                   vpn(stream_ptr))
+    _check(rc, "cgtp_forward_real")
+
+
+def cgtp_real_workspace_bytes(plan, N: int) -> int:
+    return int(_load().cgtp_real_workspace_bytes(plan, int(N)))
 
 
 def cgtp_backward_query(plan) -> dict:
@@ -440,6 +454,29 @@ class Plan:
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
         cgtp_forward_weighted(self._h, x1.data_ptr(), x2.data_ptr(), weights.data_ptr() if weights is not None else None,
                               out.data_ptr(), N, C, shared, per_pair, s.cuda_stream)
+        return out
+
+    def forward_real(self, x1, x2, out=None, workspace=None, stream=None):
+        """Full CGTP of real-basis inputs [N, (L+1)^2], every path in the real basis [N, (L+1)^4]."""
+        import torch
+        tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
+        nin, nout = (self.L + 1) ** 2, cgtp_num_outputs(self.L)
+        N = x1.shape[0]
+        for t, what in ((x1, "x1"), (x2, "x2")):
+            if not t.is_cuda or t.dtype != tdt or tuple(t.shape) != (N, nin) or not t.is_contiguous():
+                raise ValueError("%s must be a contiguous %s CUDA tensor [N, %d]" % (what, tdt, nin))
+        if out is None:
+            out = torch.empty((N, nout), dtype=tdt, device=x1.device)
+        elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, nout):
+            raise ValueError("out must be a contiguous %s tensor [N, (L+1)^4]" % tdt)
+        need = cgtp_real_workspace_bytes(self._h, N)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < need:
+            raise ValueError("workspace must be a uint8 CUDA tensor of at least %d bytes" % need)
+        s = stream if stream is not None else torch.cuda.current_stream(x1.device)
+        cgtp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, workspace.data_ptr(),
+                          workspace.numel(), s.cuda_stream)
         return out
 
     def backward_query(self) -> dict:

@@ -275,6 +275,17 @@ int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* block_li
                                int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
                                int L, const ChanArgs<double>& ch, void* stream);
 
+// Real basis: real rows -> (a, b, a + b) of their complex coefficients, and
+// the three products -> real-basis paths in place (cgtp_real.hip).
+int launch_real_in_f32(const float* r1, const float* r2, float* xa1, float* xbc1, float* xa2, float* xbc2,
+                       int64_t N, int L, void* stream);
+int launch_real_in_f64(const double* r1, const double* r2, double* xa1, double* xbc1, double* xa2, double* xbc2,
+                       int64_t N, int L, void* stream);
+int launch_real_out_f32(float* out, const float* z, const int32_t* half, int64_t nhalf, int64_t N, int L,
+                        void* stream);
+int launch_real_out_f64(double* out, const double* z, const int32_t* half, int64_t nhalf, int64_t N, int L,
+                        void* stream);
+
 // Gradients: the per-block kernels (block_list: the nsmall small-variant
 // blocks, then the nlarge others) over their blocks x N pairs into ws, then
 // the sums over the other degree into gx1 / gx2 (either may be NULL).

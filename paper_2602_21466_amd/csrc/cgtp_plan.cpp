@@ -356,6 +356,8 @@ struct cgtp_plan_s {
     int bwd_nsmall = 0;     // blocks of the small variant: the first entries of the gradient block list
     int bwd_list_off = 0;   // the gradient block list's offset in the uploaded block lists
     const int32_t* d_bwd_list = nullptr;
+    const int32_t* d_rhalf = nullptr;   // real basis: HostTables::rhalf
+    int64_t nhalf = 0;
     bool bwd_ok = true;     // every block fits one of the gradient kernel's variants
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
@@ -370,6 +372,7 @@ struct HostTables {
     std::vector<T> pbar, wtab, tw, lcg, coef;
     std::vector<int32_t> coefi;
     std::vector<cgtp::TileDesc> tdesc;
+    std::vector<int32_t> rhalf;   // real basis: per path and |m3|, see real_out_kernel
 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -712,6 +715,18 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
     p->bwd_nsmall = (int)bs.size();
     list.insert(list.end(), bs.begin(), bs.end());
     list.insert(list.end(), bl.begin(), bl.end());
+    // real basis: one entry per path and |m3| <= l3: the index of m3 = 0 in a
+    // pair's row, |m3| and the parity of l1 + l2 + l3
+    h.rhalf.clear();
+    for (int l1 = 0; l1 <= L; ++l1)
+        for (int l2 = 0; l2 <= L; ++l2)
+            for (int l3 = std::abs(l1 - l2); l3 <= l1 + l2; ++l3) {
+                const int64_t base = path_offset(L, l1, l2, l3) + l3;
+                if (base >= (1 << 21)) return CGTP_EUNSUP;
+                for (int mu = 0; mu <= l3; ++mu)
+                    h.rhalf.push_back((int32_t)(base | (int64_t)mu << 21 | (int64_t)((l1 + l2 + l3) & 1) << 28));
+            }
+    p->nhalf = (int64_t)h.rhalf.size();
     return CGTP_OK;
 }
 
@@ -734,10 +749,13 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     total = align_up(total + h.tdesc.size() * sizeof(cgtp::TileDesc), 256);
     const size_t coefi_off = total;
     total = align_up(total + h.coefi.size() * sizeof(int32_t), 256);
+    const size_t rhalf_off = total;
+    total = align_up(total + h.rhalf.size() * sizeof(int32_t), 256);
     std::vector<char> host(total, 0);
     if (!h.tdesc.empty())
         std::memcpy(host.data() + tdesc_off, h.tdesc.data(), h.tdesc.size() * sizeof(cgtp::TileDesc));
     if (!h.coefi.empty()) std::memcpy(host.data() + coefi_off, h.coefi.data(), h.coefi.size() * sizeof(int32_t));
+    if (!h.rhalf.empty()) std::memcpy(host.data() + rhalf_off, h.rhalf.data(), h.rhalf.size() * sizeof(int32_t));
     for (int i = 0; i < kParts; ++i)
         if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
     std::memcpy(host.data() + offs[kParts], blocks.data(), blocks.size() * sizeof(BlockDesc));
@@ -768,6 +786,7 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
     p->d_bwd_list = p->d_list + p->bwd_list_off;
+    p->d_rhalf = (const int32_t*)(base + rhalf_off);
     return CGTP_OK;
 }
 
@@ -1024,6 +1043,90 @@ int cgtp_forward_weighted(cgtp_plan_t plan, const void* x1, const void* x2, cons
 }
 
 int64_t cgtp_num_paths(int32_t L) { return L < 0 ? -1 : path_index(L, L + 1, 0, 1); }
+
+}  // extern "C"
+
+namespace {
+
+// Workspace of cgtp_forward_real: per input the a rows [N] and the b, a + b
+// rows [2N] (each part 256-byte aligned), then the products P(b1, b2) and
+// P(a1 + b1, a2 + b2) [2N, (L+1)^4].
+struct RealWs {
+    int64_t xa1, xbc1, xa2, xbc2, z, total;
+};
+bool real_ws(const cgtp_plan_s* p, int64_t N, RealWs* w) {
+    const int64_t esz = p->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const int64_t nin = (int64_t)(p->L + 1) * (p->L + 1), nout = nin * nin;
+    if (N < 0 || N > INT64_MAX / (8 * nout * esz)) return false;
+    auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
+    w->xa1 = 0;
+    w->xbc1 = w->xa1 + al(N * nin * esz);
+    w->xa2 = w->xbc1 + al(2 * N * nin * esz);
+    w->xbc2 = w->xa2 + al(N * nin * esz);
+    w->z = w->xbc2 + al(2 * N * nin * esz);
+    w->total = w->z + 2 * N * nout * esz;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t cgtp_real_workspace_bytes(cgtp_plan_t plan, int64_t N) {
+    RealWs w;
+    if (!plan || !real_ws(plan, N, &w)) return -1;
+    return w.total;
+}
+
+int cgtp_forward_real(cgtp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* workspace,
+                      int64_t workspace_bytes, void* hip_stream) {
+    if (!plan || N < 0) return CGTP_EINVAL;
+    if (N == 0) return CGTP_OK;
+    if (!x1 || !x2 || !out || !workspace) return CGTP_EINVAL;
+    if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+    if ((uintptr_t)workspace & 255) return CGTP_EINVAL;
+    RealWs w;
+    if (!real_ws(plan, N, &w) || workspace_bytes < w.total) return CGTP_EINVAL;
+    const int L = plan->L;
+    const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
+    const size_t nin = (size_t)(L + 1) * (L + 1), nout = nin * nin;
+    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin) ||
+        overlaps(workspace, (size_t)w.total, x1, bin) || overlaps(workspace, (size_t)w.total, x2, bin) ||
+        overlaps(workspace, (size_t)w.total, out, bout))
+        return CGTP_EINVAL;
+    int dev = -1;
+    const hipError_t de = hipGetDevice(&dev);
+    if (de != hipSuccess) {
+        g_last_hip_error = (int)de;
+        return CGTP_EHIP;
+    }
+    if (dev != plan->device) return CGTP_EINVAL;
+    char* ws = (char*)workspace;
+    void *xa1 = ws + w.xa1, *xbc1 = ws + w.xbc1, *xa2 = ws + w.xa2, *xbc2 = ws + w.xbc2, *z = ws + w.z;
+    int err = plan->grid.dtype == CGTP_FP32
+                  ? cgtp::launch_real_in_f32((const float*)x1, (const float*)x2, (float*)xa1, (float*)xbc1,
+                                             (float*)xa2, (float*)xbc2, N, L, hip_stream)
+                  : cgtp::launch_real_in_f64((const double*)x1, (const double*)x2, (double*)xa1, (double*)xbc1,
+                                             (double*)xa2, (double*)xbc2, N, L, hip_stream);
+    if (err != 0) {
+        g_last_hip_error = err;
+        return CGTP_EHIP;
+    }
+    // P(a1, a2) into out; P(b1, b2) and P(a1 + b1, a2 + b2) into the workspace
+    int rc = forward_rows(plan, xa1, xa2, nullptr, out, N, 1, 0, hip_stream);
+    if (rc == CGTP_OK) rc = forward_rows(plan, xbc1, xbc2, nullptr, z, 2 * N, 1, 0, hip_stream);
+    if (rc != CGTP_OK) return rc;
+    err = plan->grid.dtype == CGTP_FP32
+              ? cgtp::launch_real_out_f32((float*)out, (const float*)z, plan->d_rhalf, plan->nhalf, N, L, hip_stream)
+              : cgtp::launch_real_out_f64((double*)out, (const double*)z, plan->d_rhalf, plan->nhalf, N, L,
+                                          hip_stream);
+    if (err != 0) {
+        g_last_hip_error = err;
+        return CGTP_EHIP;
+    }
+    return CGTP_OK;
+}
 
 int cgtp_backward_query(cgtp_plan_t plan, double* flops_per_pair, double* bytes_per_pair) {
     if (!plan) return CGTP_EINVAL;
