@@ -57,8 +57,13 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     constexpr int BP = B + 1;
     constexpr int FS = slot_stride(A, B);
     constexpr int NT = SMALL ? kBwdSmallThreads : kBwdThreads;
-    constexpr int MR = SMALL ? 1 : BwdMaxRows<T>::value;   // register-held rows (large variant)
-    const int tid = threadIdx.x;
+    constexpr int NW = NT / 64;                       // waves
+    constexpr int MPW = BwdGeom<T, SMALL>::mpw;       // |m| values per wave
+    constexpr int KS = bwd_ks<T, SMALL>(0);           // MFMA K steps (4 rows each) of the first |m|
+    using Acc = typename Cplx<T>::acc4;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 15, lk = lane >> 4;       // MFMA lane: column / A-row index, K index
     const int j1 = bd.j1, j2 = bd.j2, J = bd.J, R = bd.R, d = bd.d, G = bd.bwd_rings;
     const bool cross = bd.kind == kBlockCross;
     const int nslot = cross ? 4 : 2;
@@ -75,38 +80,18 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [slot][longitude n]: the pair's lifted coefficients
     C* cacc = reinterpret_cast<C*>(smem + ly.cacc);      // [slot][longitude n]: their gradients, summed over rings
-    int* rowoff = reinterpret_cast<int*>(smem + ly.rowoff);   // first weight of |m| in a ring's row
-    T* wst = reinterpret_cast<T*>(smem + ly.wst);        // [ring of the group][|m|, row]: 2 w_r P^|m|_l3(x_r)
     T* prs = reinterpret_cast<T*>(smem + ly.prs);        // [ring of the group][input][longitude n]: P_j^|m(n)|
-    int* colb = reinterpret_cast<int*>(smem + ly.colb);  // small variant: first entry gradient of signed m
-    T* bg = reinterpret_cast<T*>(smem + ly.bg);          // small variant: [signed m][component][row]
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [ring of the group][kBwdSlots], pass layout
     auto slot = [&](int r, int s) -> C* { return fbuf + (size_t)(r * kBwdSlots + s) * FS; };
     const int zs0 = nslot;              // slots of the analysis gradients (spectra)
     const int zg0 = kBwdSlots - 2;      // slots of the product gradients (circle)
 
-    // ---- set-up: couplings, twiddles, weight-row offsets, cleared sums
+    // ---- set-up: couplings, twiddles, cleared sums
     for (int e = tid; e < 3 * n1; e += NT) lc[e] = tb.lcg[3 * j1 * j1 + e];
     for (int e = tid; e < 3 * n2; e += NT) lc[3 * n1 + e] = tb.lcg[3 * j2 * j2 + e];
     {
         const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
         for (int e = tid; e < A * BP; e += NT) tw2[e] = tw[e];
-    }
-    if (tid == 0) {
-        int o = 0;
-        for (int mp = 0; mp <= J; ++mp) {
-            rowoff[mp] = o;
-            o += nrows - tmin(mp);
-        }
-        rowoff[J + 1] = o;
-        if (SMALL) {
-            o = 0;
-            for (int sm = 0; sm <= 2 * J; ++sm) {
-                colb[sm] = o;
-                o += ncomp * (nrows - tmin(sm < J ? J - sm : sm - J));
-            }
-            colb[2 * J + 1] = o;
-        }
     }
     for (int e = tid; e < nslot * Phi; e += NT) cacc[e] = cmk<C>((T)0, (T)0);
     // ---- the pair's lifted coefficients, as the forward forms them:
@@ -135,15 +120,14 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         }
         cvn[e] = val;
     }
-    // ---- transpose of the end phase.  Output (j3, m3) of the block is a
-    // weighted sum of accumulator entries: an even path reads component 0 at
-    // (l3 = j3, m3); an odd path reads, for q = -1, 0, +1, component 2, 1, 3 at
-    // (l3 = j3 - 1, m3 - q) with the plan's term q + 1.  Each entry thus feeds
-    // one output, and its gradient is that term's weight times the output's
-    // gradient.  Column c = (m + J) ncomp + comp holds the entries of rows
-    // l3 = d + 2 (tmin(|m|) + i), i < the rows of |m|: in LDS (small variant),
-    // or in the registers of thread c (large variant).
-    const int ncols = (2 * J + 1) * ncomp;
+    // ---- transpose of the end phase, into MFMA B operands.  Output (j3, m3) of
+    // the block is a weighted sum of accumulator entries: an even path reads
+    // component 0 at (l3 = j3, m3); an odd path reads, for q = -1, 0, +1,
+    // component 2, 1, 3 at (l3 = j3 - 1, m3 - q) with the plan's term q + 1.
+    // Each entry thus feeds one output, and its gradient is that term's weight
+    // times the output's gradient.  For |m| = wave + NW t, lane (k, j) holds the
+    // entries of rows l3 = d + 2 (tmin(|m|) + 4 s + k) in column j = (sign,
+    // component): B[t][s].
     const T* coefs = tb.coef + (size_t)bd.coef_off * 4;
     const T* grow = gin + n * nout + bd.out_off;
     auto entry_grad = [&](int comp, int m, int l3) -> T {
@@ -153,35 +137,31 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         const int o = j3 * j3 - d * d + j3 + m3;
         return coefs[4 * o + (comp == 0 ? 0 : q + 1)] * grow[o];
     };
-    T bgr[MR];
-    if constexpr (SMALL) {
-        __syncthreads();   // colb
-        for (int c = tid; c < ncols; c += NT) {
-            const int comp = c % ncomp, sm = c / ncomp, m = sm - J, mp = m < 0 ? -m : m;
-            const int nr = nrows - tmin(mp), l30 = d + 2 * tmin(mp);
-            T* col = bg + colb[sm] + comp * nr;
-            for (int i = 0; i < nr; ++i) col[i] = entry_grad(comp, m, l30 + 2 * i);
-        }
-    } else {
-        const int c = tid;
-        const int comp = c % ncomp, m = c / ncomp - J, mp = m < 0 ? -m : m;
-        const int nr = c < ncols ? nrows - tmin(mp) : 0;
-        const int l30 = d + 2 * tmin(mp);
+    // the lane's column: sign of m and component; valid for the |m| at hand
+    const int csign = cross ? li >> 2 : li, ccomp = cross ? li & 3 : 0;
+    auto col_ok = [&](int mp) { return csign < (mp == 0 ? 1 : 2) && (cross || li < 2); };
+    T bq[MPW][KS];
 #pragma unroll
-        for (int i = 0; i < MR; ++i) bgr[i] = i < nr ? entry_grad(comp, m, l30 + 2 * i) : (T)0;
+    for (int t = 0; t < MPW; ++t) {
+        const int mp = wave + NW * t;
+        const int nr = mp <= J ? nrows - tmin(mp) : 0;
+        const int l30 = d + 2 * tmin(mp);
+        const bool ok = mp <= J && col_ok(mp);
+#pragma unroll
+        for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s) {
+            const int row = 4 * s + lk;
+            bq[t][s] = (ok && row < nr) ? entry_grad(ccomp, csign ? -mp : mp, l30 + 2 * row) : (T)0;
+        }
     }
     __syncthreads();
 
+    // the block's weight table as a buffer resource (reads past it return zero)
+    const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(tb.wtab + bd.wtab_off), (short)0, (tb.wtab_len - bd.wtab_off) * (int)sizeof(T), kBufferFlags);
+
     for (int rg0 = 0; rg0 < R; rg0 += G) {
         const int nrg = (R - rg0) < G ? (R - rg0) : G;
-        // ---- 0. the group's weights and Legendre values, staged
-        for (int e = tid; e < nrg * (J + 1) * nrows; e += NT) {
-            const int i = e % nrows, f = e / nrows, mp = f % (J + 1), r = f / (J + 1);
-            const int t0 = tmin(mp);
-            if (i < nrows - t0)
-                wst[r * ly.nwr + rowoff[mp] + i] =
-                    tb.wtab[bd.wtab_off + (mp * bd.rpad + rg0 + r) * bd.wrow + (d + 2 * t0 - (J & 1)) / 2 + i];
-        }
+        // ---- 0. the group's Legendre values, staged
         for (int e = tid; e < nrg * 2 * Phi; e += NT) {
             const int nn = e % Phi, f = e / Phi, r = f >> 1;
             const int j = (f & 1) ? j2 : j1;
@@ -214,28 +194,36 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[0] : cmulc(v[k2], twr[k2]);
         }
-        // ---- 3. transpose of the projection (other slots than the synthesis'):
-        // the spectrum gradient at (ring, component, signed m) is the sum over the
-        // rows l3 of the weight 2 w_r P^|m|_l3(x_r) times the entry gradient; it
-        // goes to the real (even component) or imaginary (odd) part at the
+        // ---- 3. transpose of the projection (other slots than the synthesis'),
+        // on MFMA: per |m|, D[ring][column] = sum over rows l3 of A[ring][row] =
+        // 2 w_r P^|m|_l3(x_r) (the forward's weight table, read in place) times
+        // B[row][column] (the entry gradients); D goes to the real (even
+        // component) or imaginary (odd) part of the spectrum gradient at the
         // pass-layout position of m
-        for (int c = tid; c < ncols; c += NT) {
-            const int comp = c % ncomp, sm = c / ncomp, m = sm - J, mp = m < 0 ? -m : m;
-            const int nr = nrows - tmin(mp);
-            const int kk = m < 0 ? Phi + m : m;
-            for (int r = 0; r < nrg; ++r) {
-                const T* w = wst + r * ly.nwr + rowoff[mp];
-                T acc = (T)0;
-                if constexpr (SMALL) {
-                    const T* col = bg + colb[sm] + comp * nr;
-                    for (int i = 0; i < nr; ++i) acc += w[i] * col[i];
-                } else {
 #pragma unroll
-                    for (int i = 0; i < MR; ++i)
-                        if (i < nr) acc += w[i] * bgr[i];
+        for (int t = 0; t < MPW; ++t) {
+            const int mp = wave + NW * t;
+            if (mp <= J) {
+                const int nr = nrows - tmin(mp);
+                const int w0 = (mp * bd.rpad + rg0 + li) * bd.wrow + (d + 2 * tmin(mp) - (J & 1)) / 2 + lk;
+                Acc acc = Acc(0);
+#pragma unroll
+                for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s) {
+                    if (4 * s < nr) {
+                        const T a = (li < nrg && 4 * s + lk < nr)
+                                        ? buffer_load<T>(wrsrc, (w0 + 4 * s) * (int)sizeof(T), 0) : (T)0;
+                        acc = mfma16(a, bq[t][s], acc);
+                    }
                 }
-                T* dst = reinterpret_cast<T*>(slot(r, zs0 + (comp >> 1)) + (kk + kk / B));
-                dst[comp & 1] = acc;
+                if (col_ok(mp)) {
+                    const int k = csign ? Phi - mp : mp;
+                    const int pos = 2 * (k + k / B) + (ccomp & 1);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int r = acc_row<T>(lk, q);
+                        if (r < nrg) reinterpret_cast<T*>(slot(r, zs0 + (ccomp >> 1)))[pos] = acc[q];
+                    }
+                }
             }
         }
         __syncthreads();

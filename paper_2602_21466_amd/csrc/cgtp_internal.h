@@ -184,28 +184,36 @@ struct TileGeom {
 // ---------------------------------------------------------------- gradients
 //
 // The gradient kernel (cgtp_backward.hip) runs one work-group per (block,
-// pair), in two variants.  Both need the gradients of the projection's
-// accumulator entries, per column (|m|, sign, component) all its rows l3:
-//   small blocks, (2 J + 1) * components <= kBwdSmallThreads: 256 threads,
-//     entry gradients in LDS (compact, column by column);
-//   large blocks: 768 threads, one column per thread in registers.
-// LDS, in byte offsets: couplings [3][n1 + n2], twiddles in pass layout, the
-// pair's lifted coefficients and their gradients ([slot][Phi] each), the first
-// row of every |m| in a ring's weight rows, (small variant) each signed m's
-// first entry gradient and the entry gradients, then per ring group the
-// weights [ring][sum over |m| of its rows], the Legendre values
-// [ring][input][Phi] and kBwdSlots transforms per ring.
-constexpr int kBwdThreads = 768;         // large variant
-constexpr int kBwdSmallThreads = 256;    // small variant
-constexpr int kBwdSmallLds = 40 * 1024;  // small variant: ring groups sized for four work-groups per CU
+// pair), in two sizes: 256 threads for blocks with (2 J + 1) * components <=
+// kBwdSmallThreads, 768 for the others.  The transposed Legendre projection
+// runs on 16x16x4 MFMA per |m|: wave w owns |m| = w, w + waves, ..., and holds
+// the gradients of those accumulator entries in registers as B operands
+// (lane: rows 4 s + lane / 16, column lane % 16 = (sign, component)).  LDS, in
+// byte offsets: couplings [3][n1 + n2], twiddles in pass layout, the pair's
+// lifted coefficients and their gradients ([slot][Phi] each), then per ring
+// group the Legendre values [ring][input][Phi] and kBwdSlots transforms per
+// ring.
+constexpr int kBwdThreads = 768;         // large blocks
+constexpr int kBwdSmallThreads = 256;    // small blocks
+constexpr int kBwdSmallLds = 52 * 1024;  // small blocks: ring groups sized for three work-groups per CU
 constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
-template <typename T> struct BwdMaxRows;
-template <> struct BwdMaxRows<float> { static constexpr int value = 33; };    // rows l3 of a block at L <= 32
-template <> struct BwdMaxRows<double> { static constexpr int value = 20; };   // fp64 plans stop at L = 19
+// Register budget of the B operands: |m| values per wave (mpw) and, for the
+// t-th of them (|m| >= waves * t), K steps of 4 rows.  A block's |m| has at
+// most floor((J - |m|) / 2) + 1 <= rmax - floor(|m| / 2) rows (rmax = Jmax / 2
+// + 1), so the t-th needs at most ceil((rmax - waves * t / 2) / 4) steps.
+template <typename T, bool SMALL> struct BwdGeom;
+template <> struct BwdGeom<float, false> { static constexpr int mpw = 6, rmax = 33; };   // J <= 64
+template <> struct BwdGeom<float, true> { static constexpr int mpw = 9, rmax = 17; };    // J <= 32
+template <> struct BwdGeom<double, false> { static constexpr int mpw = 4, rmax = 20; };  // J <= 38
+template <> struct BwdGeom<double, true> { static constexpr int mpw = 9, rmax = 17; };
+template <typename T, bool SMALL>
+__host__ __device__ constexpr int bwd_ks(int t) {
+    const int nw = (SMALL ? kBwdSmallThreads : kBwdThreads) / 64;
+    const int rows = BwdGeom<T, SMALL>::rmax - nw * t / 2;
+    return rows < 1 ? 1 : (rows + 3) / 4;
+}
 struct BwdLayout {
-    int lc, tw2, cvn, cacc, rowoff, colb, bg, wst, prs, fbuf, end;
-    int nwr;   // weights per ring: sum over |m| of the rows l3 >= |m|
-    int nbg;   // entry gradients (small variant)
+    int lc, tw2, cvn, cacc, prs, fbuf, end;
 };
 __host__ __device__ inline int bwd_columns(const BlockDesc& b) {
     return (2 * b.J + 1) * (b.kind == kBlockCross ? 4 : 1);
@@ -215,28 +223,35 @@ __host__ __device__ inline int bwd_align16(int v) { return (v + 15) & ~15; }
 __host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int rings) {
     const int csz = 2 * esz;
     const bool cross = b.kind == kBlockCross;
-    const int nslot = cross ? 4 : 2, ncomp = cross ? 4 : 1;
+    const int nslot = cross ? 4 : 2;
     const int n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
-    const int nrows = (b.J - b.d) / 2 + 1;
-    const bool small = bwd_small(b);
     BwdLayout l;
-    l.nwr = 0;
-    for (int mp = 0; mp <= b.J; ++mp) l.nwr += nrows - (mp > b.d ? (mp - b.d + 1) / 2 : 0);
-    l.nbg = small ? ncomp * (2 * l.nwr - nrows) : 0;
     int o = 0;
     l.lc = o; o = bwd_align16(o + esz * 3 * (n1 + n2));
     l.tw2 = o; o = bwd_align16(o + csz * b.A * (b.B + 1));
     l.cvn = o; o = bwd_align16(o + csz * nslot * b.Phi);
     l.cacc = o; o = bwd_align16(o + csz * nslot * b.Phi);
-    l.rowoff = o; o = bwd_align16(o + 4 * (b.J + 2));
-    l.colb = o; o = bwd_align16(o + (small ? 4 * (2 * b.J + 2) : 0));
-    l.bg = o; o = bwd_align16(o + esz * l.nbg);
-    l.wst = o; o = bwd_align16(o + esz * rings * l.nwr);
     l.prs = o; o = bwd_align16(o + esz * rings * 2 * b.Phi);
     l.fbuf = o; o += csz * rings * kBwdSlots * slot_stride(b.A, b.B);
     l.end = o;
     return l;
 }
+// Whether a block fits its variant's B-operand registers.
+template <typename T>
+inline bool bwd_fits(const BlockDesc& b) {
+    const bool small = bwd_small(b);
+    const int nw = (small ? kBwdSmallThreads : kBwdThreads) / 64;
+    const int mpw = small ? BwdGeom<T, true>::mpw : BwdGeom<T, false>::mpw;
+    if (b.J + 1 > mpw * nw) return false;
+    const int nrows = (b.J - b.d) / 2 + 1;
+    for (int mp = 0; mp <= b.J; ++mp) {
+        const int rows = nrows - (mp > b.d ? (mp - b.d + 1) / 2 : 0);
+        const int ks = small ? bwd_ks<T, true>(mp / nw) : bwd_ks<T, false>(mp / nw);
+        if (rows > 4 * ks) return false;
+    }
+    return true;
+}
+
 // Offset (elements per pair) of block (j1, j2)'s gradient rows in the
 // workspace: blocks in (j1, j2) order, each [pair][n1 + n2].
 __host__ __device__ inline int64_t bwd_block_off(int L, int j1, int j2) {

@@ -577,10 +577,8 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                     for (int G = 8; G >= 1 && !b.bwd_rings; G /= 2)
                         if (cgtp::bwd_layout(b, (int)sizeof(T), G).end <= (pass ? cgtp::kLdsBudget : cgtp::kBwdSmallLds))
                             b.bwd_rings = G;
-                // the large variant's register-held entry gradients: one column per thread
-                if (!small && (cgtp::bwd_columns(b) > cgtp::kBwdThreads ||
-                               (b.J - b.d) / 2 + 1 > cgtp::BwdMaxRows<T>::value))
-                    b.bwd_rings = 0;
+                // the register-held entry gradients (B operands of the transposed projection)
+                if (!cgtp::bwd_fits<T>(b)) b.bwd_rings = 0;
                 if (b.bwd_rings) {
                     int& lds = small ? p->bwd_lds_small : p->bwd_lds_large;
                     lds = std::max(lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings).end);
