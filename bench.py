@@ -5,7 +5,8 @@ pair: lift, products, lower, per-path recovery), inputs already resident in
 HBM.  The headline workload is L = 32, N = 1024 pairs, fp32; L = 16,
 N = 8192 is reported beside it, each with the time of both gradients
 (cgtp_backward: the block adjoint kernel and the fixed-order sums, timed
-together as one step) under "backward".  The multiple-input, multiple-output Gaunt
+together as one step) under "backward" and of the real-basis CGTP
+(cgtp_forward_real, its roofline against one CGTP's model work) under "real".  The multiple-input, multiple-output Gaunt
 and vector signal products (istp_forward) are timed after it, each with its
 own roofline and oracle baseline, under "istp" (with the gradients,
 istp_backward, where the plan supports them).  Prints ONE JSON line.
@@ -61,6 +62,7 @@ MEASURED_TRAFFIC = {
 DIGEST_SOURCES = {
     "cgtp": ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "cgtp_backward": ("cgtp_backward.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
+    "cgtp_real": ("cgtp_real.hip", "cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "istp": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
@@ -140,6 +142,18 @@ def time_workload(w, steps, warmup, backward=True):
                                   w.N, steps, warmup))
         res["backward"] = bwd
         del g, g1, g2, ws
+        # the real spherical-harmonic basis (cgtp_forward_real: conversions and three products)
+        out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
+        need = lib.cgtp_real_workspace_bytes(plan._h, w.N)
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        real = {"workload": w.name + ":real", "L": w.L, "N": w.N, "dtype": w.dtype, "plan": plan.query(),
+                "kind": "cgtp_real"}
+        real.update(_time_launches(lambda st: lib.cgtp_forward_real(plan._h, a.data_ptr(), b.data_ptr(),
+                                                                    out.data_ptr(), w.N, ws.data_ptr(), need,
+                                                                    st.cuda_stream),
+                                   w.N, steps, warmup))
+        res["real"] = real
+        del out, ws
     else:
         del out
     plan.close()
@@ -338,6 +352,12 @@ def backward_entry(rb):
             "roofline": roofline(rb)}
 
 
+def real_entry(rr):
+    log("  real basis (conversions + three products) %.4f ms/step, %.4g pairs/s" % (rr["ms_per_step"], rr["value"]))
+    return {"value": round(rr["value"], 1), "unit": "pairs/s", "basis": "real",
+            "ms_per_step": round(rr["ms_per_step"], 4), "roofline": roofline(rr)}
+
+
 def copy_probe(nbytes, reps=10):
     """Plain device-to-device copy of nbytes: the calibration for the HBM counters."""
     import torch
@@ -477,6 +497,8 @@ def main():
                      "ms_per_step": round(r2["ms_per_step"], 4), "roofline": roofline(r2)}
             if "backward" in r2:
                 entry["backward"] = backward_entry(r2["backward"])
+            if "real" in r2:
+                entry["real"] = real_entry(r2["real"])
             secondary.append(entry)
     channels = []
     if args.channels and args.channels != "none":
@@ -541,6 +563,7 @@ def main():
                    "grid": "per-block minimal exact Gauss-Legendre x FFT", "cover": "scalar-scalar + cross"},
         "roofline": roofline(main_res),
         "backward": backward_entry(main_res["backward"]) if "backward" in main_res else None,
+        "real": real_entry(main_res["real"]) if "real" in main_res else None,
         "secondary": secondary,
         "channels": channels,
         "istp": istp,
