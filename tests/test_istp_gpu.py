@@ -280,6 +280,73 @@ def test_real_basis_gaunt(L, N, dtype):
     plan.close()
 
 
+def test_real_basis_bench_workload_subsample():
+    """istp_forward_real at the benchmark's size (L = 16, N = 65536) on its seeded subsample of pairs."""
+    torch = _torch()
+    w = wl.REAL_WORKLOADS[0]
+    x1, x2 = wl.istp_inputs(w)
+    plan = _lib().IstpPlan(w.L, 0, w.dtype)
+    got = plan.forward_real(x1.cuda(), x2.cuda())
+    torch.cuda.synchronize()
+    idx = wl.istp_check_indices(w).numpy()
+    ref = oi.gaunt_tp_real(w.L, x1.double().numpy()[idx], x2.double().numpy()[idx])
+    err, lab = per_label_rel_err(2 * w.L, 0, got.cpu().double().numpy()[idx], ref)
+    print("real basis %s: %d sampled pairs, worst label %s rel err %.3e" % (w.name, len(idx), lab, err), flush=True)
+    assert err <= TOL[w.dtype], (lab, err)
+    plan.close()
+
+
+def test_real_basis_largest_degree():
+    """istp_forward_real at the largest fp32 degree the plans accept, every pair."""
+    torch = _torch()
+    lib = _lib()
+    L, N = 33, 3
+    x1, x2 = wl.draw_rows((L + 1) ** 2, N, "fp32", seed=733)
+    plan = lib.IstpPlan(L, 0, "fp32")
+    got = plan.forward_real(x1.cuda(), x2.cuda())
+    torch.cuda.synchronize()
+    ref = oi.gaunt_tp_real(L, x1.double().numpy(), x2.double().numpy())
+    err, lab = per_label_rel_err(2 * L, 0, got.cpu().double().numpy(), ref)
+    print("real basis L=%d (largest fp32) worst label %s rel err %.3e" % (L, lab, err), flush=True)
+    assert err <= TOL["fp32"], (lab, err)
+    plan.close()
+
+
+def test_real_basis_gradients_largest_degree():
+    """istp_backward_real at the largest degree whose plan has the gradient product, every pair, checked
+    through directional derivatives against the forward oracle: <grad_x1, d> = <g, z(d, x2)> and
+    <grad_x2, d> = <g, z(x1, d)> for three seeded directions d (the unit-row derivative costs
+    (L + 1)^2 oracle products per pair at this degree)."""
+    torch = _torch()
+    lib = _lib()
+    L = None
+    for cand in range(33, 0, -1):
+        plan = lib.IstpPlan(cand, 0, "fp32")
+        if lib.istp_real_backward_workspace_bytes(plan._h, 2) > 0:
+            L = cand
+            break
+        plan.close()
+    assert L is not None
+    print("largest degree with real-basis gradients: L=%d" % L, flush=True)
+    N = 2
+    x1, x2 = wl.draw_rows((L + 1) ** 2, N, "fp32", seed=834)
+    g, _ = wl.draw_rows((2 * L + 1) ** 2, N, "fp32", seed=934)
+    g1, g2 = plan.backward_real(x1.cuda(), x2.cuda(), g.cuda())
+    torch.cuda.synchronize()
+    a, b, gg = x1.double().numpy(), x2.double().numpy(), g.double().numpy()
+    G1, G2 = g1.cpu().double().numpy(), g2.cpu().double().numpy()
+    rng = np.random.default_rng(L)
+    for k in range(3):
+        d = rng.standard_normal(a.shape)
+        lhs1, rhs1 = (G1 * d).sum(1), (gg * oi.gaunt_tp_real(L, d, b)).sum(1)
+        lhs2, rhs2 = (G2 * d).sum(1), (gg * oi.gaunt_tp_real(L, a, d)).sum(1)
+        e1 = float(np.abs(lhs1 - rhs1).max() / np.abs(rhs1).max())
+        e2 = float(np.abs(lhs2 - rhs2).max() / np.abs(rhs2).max())
+        print("L=%d direction %d: rel err %.3e (x1), %.3e (x2)" % (L, k, e1, e2), flush=True)
+        assert e1 <= 1e-4 and e2 <= 1e-4, (k, e1, e2)
+    plan.close()
+
+
 def test_real_basis_errors():
     torch = _torch()
     lib = _lib()
