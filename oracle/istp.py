@@ -366,6 +366,67 @@ def gaunt_tp_real(L: int, r1, r2, threads: int = 0) -> np.ndarray:
     return to_real(2 * L, z)
 
 
+# Real basis for spin-s signals.  A real spin-s field sum c^(j,l)_m Y^{l,s}_{j,m}
+# has c^(j,l)_{-m} = sigma (-1)^m conj(c^(j,l)_m) with sigma = (-1)^(l+s-j)
+# (conj Y^{l,s}_{j,m} = (-1)^(m+l+s-j) Y^{l,s}_{j,-m} with Condon-Shortley
+# phases for Y_l^m and the spherical basis vectors).  A label with sigma = +1
+# takes the scalar real basis above; one with sigma = -1 takes it for i c
+# (which is then Hermitian).  The spin-1 product of two real fields is i times
+# a real field (the 1 (x) 1 -> 1 coupling is i / sqrt 2 times the cross
+# product, up to the sign of the basis), so its output is read back after a
+# factor i, which makes the product of two constant fields their cross product
+# over sqrt 2 (times Y_0^0); spin 0 and 2 need none.
+
+def _label_sigma(s: int, j: int, l: int) -> int:
+    return -1 if (l + s - j) % 2 else 1
+
+
+def spin_to_complex(s: int, L: int, r) -> np.ndarray:
+    """Complex-basis coefficients [N, spin_size] of real-basis spin-s rows r."""
+    r = _rows(r, spin_size(s, L))
+    c = np.zeros(r.shape, dtype=complex)
+    h = 1.0 / math.sqrt(2.0)
+    for j, l in spin_labels(s, L):
+        o = spin_offset(s, j, l) + j
+        blk = np.zeros((r.shape[0], 2 * j + 1), dtype=complex)
+        blk[:, j] = r[:, o]
+        for m in range(1, j + 1):
+            blk[:, j + m] = (-1) ** m * h * (r[:, o + m] - 1j * r[:, o - m])
+            blk[:, j - m] = h * (r[:, o + m] + 1j * r[:, o - m])
+        if _label_sigma(s, j, l) < 0:
+            blk = -1j * blk
+        c[:, o - j:o + j + 1] = blk
+    return c
+
+
+def spin_to_real(s: int, L: int, c) -> np.ndarray:
+    """Real-basis coefficients of a real spin-s field from its complex-basis coefficients."""
+    c = np.atleast_2d(np.asarray(c, dtype=complex))
+    r = np.zeros(c.shape)
+    h = math.sqrt(2.0)
+    for j, l in spin_labels(s, L):
+        o = spin_offset(s, j, l) + j
+        blk = c[:, o - j:o + j + 1]
+        if _label_sigma(s, j, l) < 0:
+            blk = 1j * blk
+        r[:, o] = blk[:, j].real
+        for m in range(1, j + 1):
+            r[:, o + m] = h * blk[:, j - m].real
+            r[:, o - m] = h * blk[:, j - m].imag
+    return r
+
+
+SPIN_OUTPUT_PHASE = {0: 1.0, 1: 1j, 2: 1.0}
+
+
+def spin_tp_real(s: int, L: int, r1, r2, threads: int = 0) -> np.ndarray:
+    """(s, s, s) product of real-basis rows: labels up to l = L in, up to 2L out, all in the real basis."""
+    c1, c2 = spin_to_complex(s, L, r1), spin_to_complex(s, L, r2)
+    f = lambda a, b: spin_tp(s, L, a, b, threads)
+    z = (f(c1.real, c2.real) - f(c1.imag, c2.imag)) + 1j * (f(c1.real, c2.imag) + f(c1.imag, c2.real))
+    return spin_to_real(s, 2 * L, SPIN_OUTPUT_PHASE[s] * z)
+
+
 def gaunt_tp_real_vjp(L: int, r1, r2, g, threads: int = 0):
     """Gradients of sum(g * gaunt_tp_real(r1, r2)) w.r.t. r1 and r2, by the plain definition of a bilinear
     map's derivatives (``gaunt_tp_real`` on unit rows, one pair at a time)."""

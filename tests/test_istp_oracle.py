@@ -373,3 +373,96 @@ def test_real_gaunt_gradients(rng):
         fg = sum(g[n, l * l + l + m] * Y[l, m] for l in range(2 * L + 1) for m in range(-l, l + 1))
         q = np.array([(W * Y[l, m] * f2 * fg).sum() for l in range(L + 1) for m in range(-l, l + 1)])
         np.testing.assert_allclose(g1[n], q, atol=1e-12)
+
+
+# ---------------------------------------------------------------- real basis, spin 1 and 2
+
+def _spin_field(s, L, c, T, P):
+    """Spherical components q = -s..s on the grid of sum c^(j,l)_m Y^{l,s}_{j,m}."""
+    f = [np.zeros(T.shape, complex) for _ in range(2 * s + 1)]
+    for j, l in oi.spin_labels(s, L):
+        o = oi.spin_offset(s, j, l)
+        for m in range(-j, j + 1):
+            if c[o + j + m] == 0:
+                continue
+            comps = _tsh(l, s, j, m, T, P)
+            for k in range(2 * s + 1):
+                f[k] = f[k] + c[o + j + m] * comps[k]
+    return f
+
+
+def _real_field_violation(f, s):
+    """max |F_{-q} - (-1)^q conj(F_q)|: zero exactly for a real field in the spherical basis."""
+    return max(np.abs(f[s - q] - (-1) ** q * np.conj(f[s + q])).max() for q in range(0, s + 1))
+
+
+@pytest.mark.parametrize("s", [1, 2])
+def test_spin_real_basis_round_trip_and_real_fields(s, rng):
+    """spin_to_real inverts spin_to_complex, and real-basis rows synthesise real fields (the per-label phase
+    (-1)^(l+s-j) of the conjugation rule)."""
+    L = 2
+    r = rng.standard_normal((3, oi.spin_size(s, L)))
+    np.testing.assert_allclose(oi.spin_to_real(s, L, oi.spin_to_complex(s, L, r)), r, atol=1e-14)
+    T, P, _ = _quadrature_grid(L + 2, 2 * L + 3)
+    f = _spin_field(s, L, oi.spin_to_complex(s, L, r[0])[0], T, P)
+    assert _real_field_violation(f, s) < 1e-12
+
+
+@pytest.mark.parametrize("s", [1, 2])
+def test_spin_real_product_against_quadrature(s, rng):
+    """spin_tp_real against direct quadrature: the coupled pointwise product of the two real fields, times the
+    oracle's output phase, is a real field, and its projections on the tensor harmonics, read back in the real
+    basis, are the oracle's outputs."""
+    L = 1
+    r1 = rng.standard_normal(oi.spin_size(s, L))
+    r2 = rng.standard_normal(oi.spin_size(s, L))
+    z = oi.spin_tp_real(s, L, r1, r2)[0]
+    T, P, W = _quadrature_grid(3 * L + 2, 6 * L + 2)
+    f1 = _spin_field(s, L, oi.spin_to_complex(s, L, r1)[0], T, P)
+    f2 = _spin_field(s, L, oi.spin_to_complex(s, L, r2)[0], T, P)
+    kappa = {1: 1j, 2: 1.0}[s]   # the convention: spin 2 as coupled, spin 1 times i (sign: the cross-product test)
+    g = []
+    for q in range(-s, s + 1):
+        acc = np.zeros(T.shape, complex)
+        for q1 in range(-s, s + 1):
+            q2 = q - q1
+            if abs(q2) <= s:
+                acc = acc + _sympy_cg(s, q1, s, q2, s, q) * f1[q1 + s] * f2[q2 + s]
+        g.append(kappa * acc)
+    assert _real_field_violation(g, s) < 1e-12
+    c3 = np.zeros(oi.spin_size(s, 2 * L), complex)
+    for j3, l3 in oi.spin_labels(s, 2 * L):
+        o = oi.spin_offset(s, j3, l3)
+        for m3 in range(-j3, j3 + 1):
+            basis = _tsh(l3, s, j3, m3, T, P)
+            c3[o + j3 + m3] = sum((W * g[k] * np.conj(basis[k])).sum() for k in range(2 * s + 1))
+    np.testing.assert_allclose(z, oi.spin_to_real(s, 2 * L, c3)[0], atol=1e-12)
+
+
+def test_spin_one_real_basis_constant_fields():
+    """Label (1, 0) holds a constant field: its real basis is the Cartesian (y, z, x) components times Y_0^0,
+    and the spin-1 product of two constant fields A, B is (A x B) / sqrt 2 times Y_0^0 there."""
+    rng = np.random.default_rng(9)
+    L = 1
+    o = oi.spin_offset(1, 1, 0)
+    a = np.zeros((1, oi.spin_size(1, L)))
+    b = np.zeros_like(a)
+    A, B = rng.standard_normal(3), rng.standard_normal(3)   # (y, z, x)
+    a[0, o:o + 3], b[0, o:o + 3] = A, B
+    y00 = 1.0 / math.sqrt(4 * math.pi)
+    T, P, _ = _quadrature_grid(3, 5)
+    f = _spin_field(1, L, oi.spin_to_complex(1, L, a)[0], T, P)
+    # spherical components -> Cartesian: F = sum_q F_q e_q, e_{+-1} = -+(x +- i y) / sqrt 2, e_0 = z
+    fx = (-f[2] + f[0]) / math.sqrt(2)
+    fy = (-1j * f[2] - 1j * f[0]) / math.sqrt(2)
+    np.testing.assert_allclose(np.stack([fy, f[1], fx]).real.reshape(3, -1).mean(1), A * y00, atol=1e-12)
+    z = oi.spin_tp_real(1, L, a, b)[0]
+    cart = lambda v: np.array([v[2], v[0], v[1]])
+    cr = np.cross(cart(A), cart(B))
+    np.testing.assert_allclose(z[o:o + 3], np.array([cr[1], cr[2], cr[0]]) / math.sqrt(2) * y00, atol=1e-13)
+
+
+def test_spin_zero_real_product_is_the_real_gaunt_product(rng):
+    r1 = rng.standard_normal((2, 16))
+    r2 = rng.standard_normal((2, 16))
+    np.testing.assert_allclose(oi.spin_tp_real(0, 3, r1, r2), oi.gaunt_tp_real(3, r1, r2), atol=1e-14)
