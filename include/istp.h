@@ -136,25 +136,33 @@ int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, cons
                           const void *wo, void *out, int64_t N, const istp_channels *ch, void *hip_stream);
 
 /*
- * The Gaunt product in the real spherical-harmonic basis (spin 0 plans only):
- * real harmonics with the Condon-Shortley phase carried over,
+ * The signal products in the real spherical-harmonic basis.  Spin 0: real
+ * harmonics with the Condon-Shortley phase carried over,
  *   Y^R_{l,m} = sqrt(2) (-1)^m Re Y_l^m (m > 0), Y_l^0 (m = 0),
  *               sqrt(2) (-1)^m Im Y_l^{|m|} (m < 0),
  * index l^2 + l + m.  x1, x2: [N, (L+1)^2] real-basis rows; out: [N, (2L+1)^2]
- * the real-basis coefficients of the integral of f1 f2 Y^R_{l3 m3}.  The
- * inputs are converted to the real and imaginary parts of their complex
+ * the real-basis coefficients of the integral of f1 f2 Y^R_{l3 m3}.  Spin 1
+ * and 2 (rows in istp_forward's label layout): a real field's coefficients of
+ * label (j, l) satisfy c_{-m} = sigma (-1)^m conj(c_m), sigma = (-1)^(l+s-j)
+ * (the tensor harmonics' conjugation rule, Definition 4.1); each label with
+ * sigma = +1 takes the scalar real basis above, each with sigma = -1 the
+ * scalar real basis of i c.  The output is the real field of the coupled
+ * pointwise product (Section 4.3); for spin 1, whose coupling is i / sqrt 2
+ * times the cross product, the real basis of i times the product, so that two
+ * constant fields give their cross product over sqrt 2 (label (1, 0) holds a
+ * constant field's Cartesian (y, z, x) components times Y_0^0).  The inputs
+ * are converted to the real and imaginary parts of their complex
  * coefficients, three products of those parts run on the plan's kernel
  * (Karatsuba's form: P(a1, a2), P(b1, b2), P(a1 + b1, a2 + b2)), and the
  * result is read back in the real basis: three products' work.
  * workspace: caller-owned device memory of istp_real_workspace_bytes(plan, N)
  * bytes or more, 256-byte aligned, not overlapping the other buffers (its
- * contents are scratch).  CGTP_EUNSUP for spin 1 or 2 plans; otherwise as
- * istp_forward.
+ * contents are scratch).  Otherwise as istp_forward.
  */
 int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
                       int64_t workspace_bytes, void *hip_stream);
 
-/* Workspace bytes istp_forward_real needs for N pairs; -1 for spin 1 or 2 plans or N < 0. */
+/* Workspace bytes istp_forward_real needs for N pairs; -1 for N < 0 or overflow. */
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
 
 /*
@@ -165,7 +173,7 @@ int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
  * library holds on each GPU it runs on until the process ends.  Same
  * arguments and rules as istp_forward_real without the workspace; the plan's
  * device must be current.  CGTP_ESCRATCH when istp_real_workspace_bytes(plan,
- * N) exceeds the array (in fp32: above 4288 pairs at L = 16, 1119 at L = 32).  The
+ * N) exceeds the array (fp32 spin 0: above 4288 pairs at L = 16, 1119 at L = 32).  The
  * entry point calls no allocating routine; every call on a GPU shares that
  * GPU's array, so calls that overlap in time on one GPU (concurrent streams)
  * race and must be ordered by the caller.  Nothing in the array needs to

@@ -581,9 +581,9 @@ class IstpPlan:
         return out
 
     def forward_real(self, x1, x2, out=None, workspace=None, stream=None):
-        """Gaunt product in the real spherical-harmonic basis (spin 0 plans): x1, x2 [N, (L+1)^2] real-basis rows;
-        returns [N, (2L+1)^2].  The workspace (a uint8 CUDA tensor of istp_real_workspace_bytes bytes) is
-        allocated here when not given."""
+        """The signal product in the real spherical-harmonic basis: x1, x2 [N, nin] real-basis rows (spin 0:
+        [N, (L+1)^2]); returns [N, nout].  The workspace (a uint8 CUDA tensor of istp_real_workspace_bytes bytes)
+        is allocated here when not given."""
         import torch
         tdt = {"fp32": torch.float32, "fp64": torch.float64}[self.dtype]
         for t in (x1, x2):

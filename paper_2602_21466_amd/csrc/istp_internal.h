@@ -162,6 +162,14 @@ int launch_real_from_complex_f32(float* out, const float* pbb, const float* pss,
                                  void* stream);
 int launch_real_from_complex_f64(double* out, const double* pbb, const double* pss, int64_t rows, int Lo,
                                  void* stream);
+int launch_real_to_complex_spin_f32(const float* r, float* re, float* im, float* sum, int64_t rows, int nin, int s,
+                                    void* stream);
+int launch_real_to_complex_spin_f64(const double* r, double* re, double* im, double* sum, int64_t rows, int nin,
+                                    int s, void* stream);
+int launch_real_from_complex_spin_f32(float* out, const float* paa, const float* pbb, const float* pss,
+                                      int64_t rows, int nout, int s, void* stream);
+int launch_real_from_complex_spin_f64(double* out, const double* paa, const double* pbb, const double* pss,
+                                      int64_t rows, int nout, int s, void* stream);
 int launch_istp_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
                            float* out, int64_t N, void* stream);
 int launch_istp_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,

@@ -689,17 +689,19 @@ int istp_forward_weighted(istp_plan_t plan, const void* x1, const void* x2, cons
 static size_t real_part_bytes(size_t n) { return (n + 255) / 256 * 256; }
 
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
-    if (!plan || N < 0 || plan->spin != ISTP_GAUNT) return -1;
+    if (!plan || N < 0) return -1;
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(nout * esz))) return -1;
-    return (int64_t)(6 * real_part_bytes((size_t)N * nin * esz) + 2 * real_part_bytes((size_t)N * nout * esz));
+    // spin 0 forms the first product in out and reads it back in place; spin 1
+    // and 2 keep all three products in the workspace
+    const size_t nprod = plan->spin == ISTP_GAUNT ? 2 : 3;
+    return (int64_t)(6 * real_part_bytes((size_t)N * nin * esz) + nprod * real_part_bytes((size_t)N * nout * esz));
 }
 
 int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* workspace,
                       int64_t workspace_bytes, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;
-    if (plan->spin != ISTP_GAUNT) return CGTP_EUNSUP;
     if (N == 0) return CGTP_OK;
     if (!x1 || !x2 || !out || !workspace) return CGTP_EINVAL;
     if ((((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) || ((uintptr_t)workspace & 255)) return CGTP_EINVAL;
@@ -725,6 +727,42 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
     void* pss = w + 6 * pin + pout;
     const int Lo = 2 * plan->L;
     int err;
+    if (plan->spin != ISTP_GAUNT) {
+        // spin 1 and 2: per-label phases; the three products in the workspace
+        const int sp = plan->spin;
+        void* paa = w + 6 * pin + 2 * pout;
+        if (plan->dtype == CGTP_FP32) {
+            err = istp::launch_real_to_complex_spin_f32((const float*)x1, (float*)re1, (float*)im1, (float*)sm1, N,
+                                                        (int)nin, sp, hip_stream);
+            if (!err)
+                err = istp::launch_real_to_complex_spin_f32((const float*)x2, (float*)re2, (float*)im2, (float*)sm2,
+                                                            N, (int)nin, sp, hip_stream);
+        } else {
+            err = istp::launch_real_to_complex_spin_f64((const double*)x1, (double*)re1, (double*)im1, (double*)sm1,
+                                                        N, (int)nin, sp, hip_stream);
+            if (!err)
+                err = istp::launch_real_to_complex_spin_f64((const double*)x2, (double*)re2, (double*)im2,
+                                                            (double*)sm2, N, (int)nin, sp, hip_stream);
+        }
+        if (err) {
+            cgtp::set_last_hip_error(err);
+            return CGTP_EHIP;
+        }
+        rc = launch_prod(plan, plan->fwd, 0, re1, re2, paa, N, hip_stream);
+        if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, im1, im2, pbb, N, hip_stream);
+        if (rc == CGTP_OK) rc = launch_prod(plan, plan->fwd, 0, sm1, sm2, pss, N, hip_stream);
+        if (rc != CGTP_OK) return rc;
+        err = plan->dtype == CGTP_FP32
+                  ? istp::launch_real_from_complex_spin_f32((float*)out, (const float*)paa, (const float*)pbb,
+                                                            (const float*)pss, N, (int)nout, sp, hip_stream)
+                  : istp::launch_real_from_complex_spin_f64((double*)out, (const double*)paa, (const double*)pbb,
+                                                            (const double*)pss, N, (int)nout, sp, hip_stream);
+        if (err) {
+            cgtp::set_last_hip_error(err);
+            return CGTP_EHIP;
+        }
+        return CGTP_OK;
+    }
     if (plan->dtype == CGTP_FP32) {
         err = istp::launch_real_to_complex_f32((const float*)x1, (float*)re1, (float*)im1, (float*)sm1, N, (int)nin,
                                                hip_stream);

@@ -1,4 +1,4 @@
-// Real spherical-harmonic basis for the Gaunt product (spin 0): conversion of
+// Real spherical-harmonic basis for the signal products: conversion of
 // real-basis rows to the real and imaginary parts of their complex-basis
 // coefficients, and of the three products of those parts back to the real
 // basis.  With the Condon-Shortley phase carried over from Y_l^m,
@@ -91,6 +91,115 @@ __global__ __launch_bounds__(kConvThreads) void from_complex_kernel(T* __restric
     }
 }
 
+// ---- spin 1 and 2.  A real spin-s field sum c^(j,l)_m Y^{l,s}_{j,m} has
+// c^(j,l)_{-m} = sigma (-1)^m conj(c^(j,l)_m), sigma = (-1)^(l+s-j): a label
+// with sigma = +1 takes the scalar real basis above, one with sigma = -1 takes
+// it for i c.  The spin-1 product of two real fields is i times a real field;
+// it is read back after a factor i (spin 2 needs none).
+
+// Column c of a spin-s row -> degree l, label j, order m (labels by l, then j
+// from |l - s|; degree l starts at (2 s + 1) l^2, label j of it at j^2 - (l - s)^2).
+__device__ __forceinline__ void spin_decode(int c, int s, int& l, int& j, int& m) {
+    const int w = 2 * s + 1;
+    l = (int)sqrtf((float)c / (float)w);
+    while ((l + 1) * (l + 1) * w <= c) ++l;
+    while (l * l * w > c) --l;
+    const int e = c - w * l * l, ls = (l - s) * (l - s);
+    j = (int)sqrtf((float)(e + ls));
+    while ((j + 1) * (j + 1) - ls <= e) ++j;
+    while (j * j - ls > e) --j;
+    m = e - (j * j - ls) - j;
+}
+
+// One thread per (row, column): the label's real and imaginary parts at that
+// column (with the label's phase), and their sum.
+template <typename T>
+__global__ __launch_bounds__(kConvThreads) void to_complex_spin_kernel(const T* __restrict__ r, T* __restrict__ re,
+                                                                       T* __restrict__ im, T* __restrict__ sum,
+                                                                       int64_t total, int nin, int s) {
+    const int64_t e = (int64_t)blockIdx.x * kConvThreads + threadIdx.x;
+    if (e >= total) return;
+    const int64_t row = e / nin;
+    const int c = (int)(e - row * nin);
+    int l, j, m;
+    spin_decode(c, s, l, j, m);
+    const T* rr = r + row * nin + (c - m);   // rr[m] = r^(j,l)_m
+    const T h = (T)0.707106781186547524400844362104849039;
+    T a, b;
+    if (m == 0) {
+        a = rr[0];
+        b = (T)0;
+    } else if (m > 0) {
+        const T sg = (m & 1) ? -h : h;
+        a = sg * rr[m];
+        b = -sg * rr[-m];
+    } else {
+        a = h * rr[-m];
+        b = h * rr[m];
+    }
+    if ((l + s - j) & 1) {   // sigma = -1: c = -i (a + i b)
+        const T t = a;
+        a = b;
+        b = -t;
+    }
+    re[e] = a;
+    im[e] = b;
+    sum[e] = a + b;
+}
+
+// One thread per (row, output column): the three products at the label's
+// order -|m| give c_{-|m|} = (paa - pbb) + i (pss - paa - pbb); the label's
+// phase (and the spin-1 factor i) applied, the column's real-basis value.
+template <typename T>
+__global__ __launch_bounds__(kConvThreads) void from_complex_spin_kernel(T* __restrict__ out,
+                                                                         const T* __restrict__ paa,
+                                                                         const T* __restrict__ pbb,
+                                                                         const T* __restrict__ pss, int64_t total,
+                                                                         int nout, int s) {
+    const int64_t e = (int64_t)blockIdx.x * kConvThreads + threadIdx.x;
+    if (e >= total) return;
+    const int64_t row = e / nout;
+    const int c = (int)(e - row * nout);
+    int l, j, m;
+    spin_decode(c, s, l, j, m);
+    const int mu = m < 0 ? -m : m;
+    const int64_t at = row * nout + (c - m) - mu;
+    const T A = paa[at], Bv = pbb[at];
+    T re = A - Bv, im = pss[at] - A - Bv;
+    // quarter turns: sigma = -1 and the spin-1 factor each multiply by i
+    const int turns = (((l + s - j) & 1) ? 1 : 0) + (s == 1 ? 1 : 0);
+    for (int k = 0; k < turns; ++k) {
+        const T t = re;
+        re = -im;
+        im = t;
+    }
+    const T r2 = (T)1.41421356237309504880168872420969808;
+    out[e] = m == 0 ? re : (m > 0 ? r2 * re : r2 * im);
+}
+
+template <typename T>
+int launch_to_complex_spin(const T* r, T* re, T* im, T* sum, int64_t rows, int nin, int s, void* stream) {
+    const int64_t total = rows * nin;
+    if (total <= 0) return 0;
+    const int64_t grid = (total + kConvThreads - 1) / kConvThreads;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(to_complex_spin_kernel<T>, dim3((unsigned)grid), dim3(kConvThreads), 0, (hipStream_t)stream,
+                       r, re, im, sum, total, nin, s);
+    return (int)hipGetLastError();
+}
+
+template <typename T>
+int launch_from_complex_spin(T* out, const T* paa, const T* pbb, const T* pss, int64_t rows, int nout, int s,
+                             void* stream) {
+    const int64_t total = rows * nout;
+    if (total <= 0) return 0;
+    const int64_t grid = (total + kConvThreads - 1) / kConvThreads;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(from_complex_spin_kernel<T>, dim3((unsigned)grid), dim3(kConvThreads), 0, (hipStream_t)stream,
+                       out, paa, pbb, pss, total, nout, s);
+    return (int)hipGetLastError();
+}
+
 template <typename T>
 int launch_to_complex(const T* r, T* re, T* im, T* sum, int64_t rows, int nin, void* stream) {
     const int64_t total = rows * nin;
@@ -130,6 +239,22 @@ int launch_real_from_complex_f32(float* out, const float* pbb, const float* pss,
 int launch_real_from_complex_f64(double* out, const double* pbb, const double* pss, int64_t rows, int Lo,
                                  void* stream) {
     return launch_from_complex<double>(out, pbb, pss, rows, Lo, stream);
+}
+int launch_real_to_complex_spin_f32(const float* r, float* re, float* im, float* sum, int64_t rows, int nin, int s,
+                                    void* stream) {
+    return launch_to_complex_spin<float>(r, re, im, sum, rows, nin, s, stream);
+}
+int launch_real_to_complex_spin_f64(const double* r, double* re, double* im, double* sum, int64_t rows, int nin,
+                                    int s, void* stream) {
+    return launch_to_complex_spin<double>(r, re, im, sum, rows, nin, s, stream);
+}
+int launch_real_from_complex_spin_f32(float* out, const float* paa, const float* pbb, const float* pss,
+                                      int64_t rows, int nout, int s, void* stream) {
+    return launch_from_complex_spin<float>(out, paa, pbb, pss, rows, nout, s, stream);
+}
+int launch_real_from_complex_spin_f64(double* out, const double* paa, const double* pbb, const double* pss,
+                                      int64_t rows, int nout, int s, void* stream) {
+    return launch_from_complex_spin<double>(out, paa, pbb, pss, rows, nout, s, stream);
 }
 
 }  // namespace istp

@@ -365,13 +365,38 @@ def test_real_basis_errors():
         lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), ws.data_ptr(), N, ws.data_ptr(), need, None)
     assert e.value.code == lib.CGTP_EINVAL
     vplan = lib.IstpPlan(3, 1, "fp32")
-    assert lib.istp_real_workspace_bytes(vplan._h, N) == -1
-    with pytest.raises(lib.CgtpError) as e:
-        lib.istp_forward_real(vplan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, ws.data_ptr(), need, None)
-    assert e.value.code == lib.CGTP_EUNSUP
+    vneed = lib.istp_real_workspace_bytes(vplan._h, N)
+    assert vneed > 0
+    vx = torch.zeros((N, vplan.nin), device="cuda")
+    vout = torch.zeros((N, vplan.nout), device="cuda")
+    vws = torch.zeros(vneed, dtype=torch.uint8, device="cuda")
+    with pytest.raises(lib.CgtpError) as e:   # a spin-1 workspace too small
+        lib.istp_forward_real(vplan._h, vx.data_ptr(), vx.data_ptr(), vout.data_ptr(), N, vws.data_ptr(),
+                              vneed - 1, None)
+    assert e.value.code == lib.CGTP_EINVAL
     torch.cuda.synchronize()
     plan.close()
     vplan.close()
+
+
+SPIN_REAL_CASES = [(1, 1, 7, "fp32"), (1, 3, 9, "fp32"), (1, 8, 5, "fp32"), (1, 4, 6, "fp64"), (1, 16, 2, "fp32"),
+                   (2, 1, 5, "fp32"), (2, 3, 6, "fp32"), (2, 2, 4, "fp64"), (2, 8, 3, "fp32")]
+
+
+@pytest.mark.parametrize("spin,L,N,dtype", SPIN_REAL_CASES)
+def test_real_basis_spin_products(spin, L, N, dtype):
+    """istp_forward_real for the vector (spin 1) and rank-2 (spin 2) products against the real-basis oracle,
+    every pair (ragged N)."""
+    torch = _torch()
+    x1, x2 = wl.draw_rows(oi.spin_size(spin, L), N, dtype, seed=1000 + 10 * spin + L)
+    plan = _lib().IstpPlan(L, spin, dtype)
+    got = plan.forward_real(x1.cuda(), x2.cuda())
+    torch.cuda.synchronize()
+    ref = oi.spin_tp_real(spin, L, x1.double().numpy(), x2.double().numpy())
+    err, lab = per_label_rel_err(2 * L, spin, got.cpu().double().numpy(), ref)
+    print("real basis spin %d L=%d N=%d %s worst label %s rel err %.3e" % (spin, L, N, dtype, lab, err), flush=True)
+    assert err <= TOL[dtype], (lab, err)
+    plan.close()
 
 
 @pytest.mark.parametrize("L,N,dtype", [(1, 5, "fp32"), (3, 7, "fp64"), (6, 4, "fp32"), (10, 3, "fp32")])

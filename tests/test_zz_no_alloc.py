@@ -67,8 +67,26 @@ def test_static_scratch_size_limit():
     assert lib.cgtp_strerror(rc)
     torch.cuda.synchronize()
     assert (out == 5.0).all().item()
-    # spin 1 plans have no real-basis product
-    vplan = lib.IstpPlan(3, lib.ISTP_VECTOR, "fp32")
-    rc = lib._load().istp_forward_real_static(vplan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
-                                             ctypes.c_void_p(out.data_ptr()), 2, None)
-    assert rc == lib.CGTP_EUNSUP
+
+
+@pytest.mark.parametrize("spin,L,N1,N2", [(1, 6, 400, 41), (2, 3, 120, 7)])
+def test_static_scratch_spin_products(spin, L, N1, N2):
+    """The spin-1 and spin-2 real-basis products through the static scratch, two calls in a row."""
+    torch, lib = _setup()
+    plan = lib.IstpPlan(L, spin, "fp32")
+    s = torch.cuda.current_stream().cuda_stream
+    for n, seed in ((N1, 21), (N2, 22)):
+        x1, x2 = cgtp_inputs.draw_rows(oi.spin_size(spin, L), n, "fp32", seed=seed + L)
+        a, b = x1.cuda(), x2.cuda()
+        ref = plan.forward_real(a, b)
+        out = torch.full((n, plan.nout), float("nan"), device="cuda")
+        rc = lib._load().istp_forward_real_static(plan._h, ctypes.c_void_p(a.data_ptr()), ctypes.c_void_p(b.data_ptr()),
+                                                 ctypes.c_void_p(out.data_ptr()), n, ctypes.c_void_p(s))
+        assert rc == lib.CGTP_OK
+        torch.cuda.synchronize()
+        err = _rel(out, ref)
+        print("spin %d L=%d N=%d: static vs workspace entry point rel L2 %.3e" % (spin, L, n, err), flush=True)
+        assert torch.isfinite(out).all().item() and err <= 1e-6
+        want = oi.spin_tp_real(spin, L, x1[:2].double().numpy(), x2[:2].double().numpy())
+        got = out[:2].double().cpu().numpy()
+        assert np.linalg.norm(got - want) / np.linalg.norm(want) <= 1e-4
