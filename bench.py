@@ -224,13 +224,13 @@ def time_channels(w, steps, warmup):
 
 
 def time_istp_real(w, steps, warmup):
-    """Gaunt product in the real basis: two conversions and four products per step."""
+    """A signal product in the real basis: two conversions, three products and the read-back per step."""
     import torch
 
     import paper_2602_21466_amd as lib
 
     x1, x2 = draw_rows_for(w, 400)
-    plan = lib.IstpPlan(w.L, 0, w.dtype)
+    plan = lib.IstpPlan(w.L, w.spin, w.dtype)
     a, b = x1.cuda(), x2.cuda()
     out = torch.empty((w.N, plan.nout), dtype=a.dtype, device="cuda")
     ws = torch.empty(lib.istp_real_workspace_bytes(plan._h, w.N), dtype=torch.uint8, device="cuda")

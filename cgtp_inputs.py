@@ -263,5 +263,6 @@ ISTP_CHANNEL_WORKLOADS = [
 # the signal products (seed L + 400), real-basis coefficients.
 REAL_WORKLOADS = [
     IstpWorkload("gtp_real_L16_N65536_fp32", 16, 0, 65_536, "fp32", 8),
+    IstpWorkload("vstp_real_L16_N65536_fp32", 16, 1, 65_536, "fp32", 8),
 ]
 

@@ -51,6 +51,15 @@ int launch_real_to_complex_f32(const float*, float*, float*, float*, int64_t, in
 int launch_real_to_complex_f64(const double*, double*, double*, double*, int64_t, int, void*) { return 1; }
 int launch_real_from_complex_f32(float*, const float*, const float*, int64_t, int, void*) { return 1; }
 int launch_real_from_complex_f64(double*, const double*, const double*, int64_t, int, void*) { return 1; }
+int launch_real_to_complex_spin_f32(const float*, float*, float*, float*, int64_t, int, int, void*) { return 1; }
+int launch_real_to_complex_spin_f64(const double*, double*, double*, double*, int64_t, int, int, void*) {
+    return 1;
+}
+int launch_real_from_complex_spin_f32(float*, const float*, const float*, const float*, int64_t, int, int, void*) {
+    return 1;
+}
+int launch_real_from_complex_spin_f64(double*, const double*, const double*, const double*, int64_t, int, int,
+                                      void*) { return 1; }
 int launch_istp_tensor_f32(const IstpTables<float>&, const IstpDesc&, const float*, const float*, float*, int64_t,
                            void*) { return 1; }
 int launch_istp_tensor_f64(const IstpTables<double>&, const IstpDesc&, const double*, const double*, double*,

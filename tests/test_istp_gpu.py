@@ -280,17 +280,17 @@ def test_real_basis_gaunt(L, N, dtype):
     plan.close()
 
 
-def test_real_basis_bench_workload_subsample():
-    """istp_forward_real at the benchmark's size (L = 16, N = 65536) on its seeded subsample of pairs."""
+@pytest.mark.parametrize("w", wl.REAL_WORKLOADS, ids=lambda w: w.name)
+def test_real_basis_bench_workload_subsample(w):
+    """istp_forward_real at the benchmark's sizes (L = 16, N = 65536) on their seeded subsamples of pairs."""
     torch = _torch()
-    w = wl.REAL_WORKLOADS[0]
     x1, x2 = wl.istp_inputs(w)
-    plan = _lib().IstpPlan(w.L, 0, w.dtype)
+    plan = _lib().IstpPlan(w.L, w.spin, w.dtype)
     got = plan.forward_real(x1.cuda(), x2.cuda())
     torch.cuda.synchronize()
     idx = wl.istp_check_indices(w).numpy()
-    ref = oi.gaunt_tp_real(w.L, x1.double().numpy()[idx], x2.double().numpy()[idx])
-    err, lab = per_label_rel_err(2 * w.L, 0, got.cpu().double().numpy()[idx], ref)
+    ref = oi.spin_tp_real(w.spin, w.L, x1.double().numpy()[idx], x2.double().numpy()[idx])
+    err, lab = per_label_rel_err(2 * w.L, w.spin, got.cpu().double().numpy()[idx], ref)
     print("real basis %s: %d sampled pairs, worst label %s rel err %.3e" % (w.name, len(idx), lab, err), flush=True)
     assert err <= TOL[w.dtype], (lab, err)
     plan.close()
