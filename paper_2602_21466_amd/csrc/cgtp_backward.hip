@@ -47,9 +47,9 @@ namespace {
 using namespace ::cgtp::dev;
 
 template <typename T, int A, int B, bool SMALL>
-__device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& bd, int64_t n,
+__device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& bd, int64_t n0, int64_t N,
                                          const T* __restrict__ x1, const T* __restrict__ x2,
-                                         const T* __restrict__ gin, T* __restrict__ wrow, int L,
+                                         const T* __restrict__ gin, T* __restrict__ wbase, int L,
                                          unsigned char* smem) {
     using C = typename Cplx<T>::type;
     constexpr int Phi = A * B;
@@ -58,6 +58,7 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     constexpr int FS = slot_stride(A, B);
     constexpr int NT = SMALL ? kBwdSmallThreads : kBwdThreads;
     constexpr int NW = NT / 64;                       // waves
+    constexpr int P = SMALL ? kBwdSmallPairs : 1;     // pairs of the work-group
     constexpr int MPW = BwdGeom<T, SMALL>::mpw;       // |m| values per wave
     constexpr int KS = bwd_ks<T, SMALL>(0);           // MFMA K steps (4 rows each) of the first |m|
     using Acc = typename Cplx<T>::acc4;
@@ -73,16 +74,17 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     const int nin = (L + 1) * (L + 1);
     const int64_t nout = (int64_t)nin * nin;
     const int nrows = (J - d) / 2 + 1;
+    const int np = (int)((N - n0) < P ? (N - n0) : P);   // pairs of this work-group that exist
     auto tmin = [&](int mp) { return mp > d ? (mp - d + 1) / 2 : 0; };
 
-    const BwdLayout ly = bwd_layout(bd, (int)sizeof(T), G);
+    const BwdLayout ly = bwd_layout(bd, (int)sizeof(T), G, P);
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
-    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [slot][longitude n]: the pair's lifted coefficients
-    C* cacc = reinterpret_cast<C*>(smem + ly.cacc);      // [slot][longitude n]: their gradients, summed over rings
+    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [pair][slot][longitude n]: lifted coefficients
+    C* cacc = reinterpret_cast<C*>(smem + ly.cacc);      // [pair][slot][longitude n]: their gradients, summed over rings
     T* prs = reinterpret_cast<T*>(smem + ly.prs);        // [ring of the group][input][longitude n]: P_j^|m(n)|
-    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [ring of the group][kBwdSlots], pass layout
-    auto slot = [&](int r, int s) -> C* { return fbuf + (size_t)(r * kBwdSlots + s) * FS; };
+    C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // [unit = ring of the group * P + pair][kBwdSlots]
+    auto slot = [&](int u, int s) -> C* { return fbuf + (size_t)(u * kBwdSlots + s) * FS; };
     const int zs0 = nslot;              // slots of the analysis gradients (spectra)
     const int zg0 = kBwdSlots - 2;      // slots of the product gradients (circle)
 
@@ -93,20 +95,21 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         const C* tw = reinterpret_cast<const C*>(tb.tw) + bd.tw_off;
         for (int e = tid; e < A * BP; e += NT) tw2[e] = tw[e];
     }
-    for (int e = tid; e < nslot * Phi; e += NT) cacc[e] = cmk<C>((T)0, (T)0);
-    // ---- the pair's lifted coefficients, as the forward forms them:
+    for (int e = tid; e < P * nslot * Phi; e += NT) cacc[e] = cmk<C>((T)0, (T)0);
+    // ---- the pairs' lifted coefficients, as the forward forms them (zero for
+    // pairs past N):
     //   even slot: (x_m, C^{j, m}_{j, m, 1, 0} x_m), odd slot: (C^{j,m-1}_{j,m,1,-1}
     //   x_{m-1}, C^{j,m+1}_{j,m,1,1} x_{m+1}), times (-1)^m for negative m;
     //   scalar blocks (x_m, 0)
-    for (int e = tid; e < nslot * Phi; e += NT) {
-        const int s = e / Phi, nn = e - s * Phi;
+    for (int e = tid; e < P * nslot * Phi; e += NT) {
+        const int ps = e / Phi, nn = e - ps * Phi, pp = ps / nslot, s = ps - pp * nslot;
         const bool first = cross ? (s < 2) : (s == 0);
         const int j = first ? j1 : j2, nj = 2 * j + 1;
         const int m = nn <= Phi / 2 ? nn : nn - Phi, am = m < 0 ? -m : m;
         C val = cmk<C>((T)0, (T)0);
-        if (am <= j) {
+        if (am <= j && pp < np) {
             const int mj = m + j;
-            const T* xrow = (first ? x1 : x2) + n * nin + j * j;
+            const T* xrow = (first ? x1 : x2) + (n0 + pp) * nin + j * j;
             const T* lcj = first ? tb.lcg + 3 * j1 * j1 : tb.lcg + 3 * j2 * j2;
             const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
             if (!cross || (s & 1) == 0) {
@@ -126,10 +129,13 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     // component 2, 1, 3 at (l3 = j3 - 1, m3 - q) with the plan's term q + 1.
     // Each entry thus feeds one output, and its gradient is that term's weight
     // times the output's gradient.  For |m| = wave + NW t, lane (k, j) holds the
-    // entries of rows l3 = d + 2 (tmin(|m|) + 4 s + k) in column j = (sign,
-    // component): B[t][s].
+    // entries of rows l3 = d + 2 (tmin(|m|) + 4 s + k) in column j = (pair,
+    // sign, component): B[t][s].
     const T* coefs = tb.coef + (size_t)bd.coef_off * 4;
-    const T* grow = gin + n * nout + bd.out_off;
+    const int ncolp = 2 * ncomp;                        // columns of one pair
+    const int cpair = li / ncolp, cc = li - cpair * ncolp;
+    const int csign = cc / ncomp, ccomp = cc - csign * ncomp;
+    const T* grow = gin + (n0 + cpair) * nout + bd.out_off;
     auto entry_grad = [&](int comp, int m, int l3) -> T {
         const int q = comp == 2 ? -1 : (comp == 3 ? 1 : 0);
         const int j3 = comp == 0 ? l3 : l3 + 1, m3 = m + q;
@@ -137,16 +143,15 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         const int o = j3 * j3 - d * d + j3 + m3;
         return coefs[4 * o + (comp == 0 ? 0 : q + 1)] * grow[o];
     };
-    // the lane's column: sign of m and component; valid for the |m| at hand
-    const int csign = cross ? li >> 2 : li, ccomp = cross ? li & 3 : 0;
-    auto col_ok = [&](int mp) { return csign < (mp == 0 ? 1 : 2) && (cross || li < 2); };
+    // the lane's column exists for the |m| at hand (and its pair for this work-group)
+    auto col_ok = [&](int mp) { return cpair < P && csign < (mp == 0 ? 1 : 2); };
     T bq[MPW][KS];
 #pragma unroll
     for (int t = 0; t < MPW; ++t) {
         const int mp = wave + NW * t;
         const int nr = mp <= J ? nrows - tmin(mp) : 0;
         const int l30 = d + 2 * tmin(mp);
-        const bool ok = mp <= J && col_ok(mp);
+        const bool ok = mp <= J && col_ok(mp) && cpair < np;
 #pragma unroll
         for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s) {
             const int row = 4 * s + lk;
@@ -161,6 +166,7 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 
     for (int rg0 = 0; rg0 < R; rg0 += G) {
         const int nrg = (R - rg0) < G ? (R - rg0) : G;
+        const int nu = nrg * P;   // units (ring, pair) of the group
         // ---- 0. the group's Legendre values, staged
         for (int e = tid; e < nrg * 2 * Phi; e += NT) {
             const int nn = e % Phi, f = e / Phi, r = f >> 1;
@@ -170,16 +176,17 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
                              : (T)0;
         }
         // the analysis-gradient slots are cleared (orders past J stay zero)
-        for (int e = tid; e < nrg * nz * FS; e += NT) {
-            const int r = e / (nz * FS), rest = e - r * nz * FS;
-            slot(r, zs0)[rest] = cmk<C>((T)0, (T)0);   // nz consecutive slots
+        for (int e = tid; e < nu * nz * FS; e += NT) {
+            const int u = e / (nz * FS), rest = e - u * nz * FS;
+            slot(u, zs0)[rest] = cmk<C>((T)0, (T)0);   // nz consecutive slots
         }
         __syncthreads();
         // ---- 1. synthesis pass 1 of the lifts (as the forward)
-        for (int task = tid; task < nrg * nslot * A; task += NT) {
-            const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
+        for (int task = tid; task < nu * nslot * A; task += NT) {
+            const int t = task % A, f = task / A, s = f % nslot, u = f / nslot;
+            const int r = u / P, pp = u - r * P;
             const bool first = cross ? (s < 2) : (s == 0);
-            const C* cv = cvn + (size_t)s * Phi + t;
+            const C* cv = cvn + (size_t)(pp * nslot + s) * Phi + t;
             const T* pr = prs + (size_t)(2 * r + (first ? 0 : 1)) * Phi + t;
             C v[B];
 #pragma unroll
@@ -189,7 +196,7 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
                 v[i] = cmk<C>(c.x * pv, c.y * pv);
             }
             Dft<B, true, C>::run(v);
-            C* row = slot(r, s) + t * BP;
+            C* row = slot(u, s) + t * BP;
             const C* twr = tw2 + t * BP;
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) row[k2] = k2 == 0 ? v[0] : cmulc(v[k2], twr[k2]);
@@ -221,7 +228,8 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         const int r = acc_row<T>(lk, q);
-                        if (r < nrg) reinterpret_cast<T*>(slot(r, zs0 + (ccomp >> 1)))[pos] = acc[q];
+                        if (r < nrg)
+                            reinterpret_cast<T*>(slot(r * P + cpair, zs0 + (ccomp >> 1)))[pos] = acc[q];
                     }
                 }
             }
@@ -230,28 +238,28 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         // ---- 2 and 4. synthesis pass 2 of the lifts and the transpose of analysis
         // pass 2 of the spectrum gradients: both inverse DFTs down the columns, in
         // place, over the consecutive slots 0 .. nslot + nz - 1
-        for (int task = tid; task < nrg * (nslot + nz) * B; task += NT) {
-            const int k2 = task % B, f = task / B, s = f % (nslot + nz), r = f / (nslot + nz);
-            C* fb = slot(r, s) + k2;
-            C u[A];
+        for (int task = tid; task < nu * (nslot + nz) * B; task += NT) {
+            const int k2 = task % B, f = task / B, s = f % (nslot + nz), u = f / (nslot + nz);
+            C* fb = slot(u, s) + k2;
+            C w[A];
 #pragma unroll
-            for (int t = 0; t < A; ++t) u[t] = fb[t * BP];
-            Dft<A, true, C>::run(u);
+            for (int t = 0; t < A; ++t) w[t] = fb[t * BP];
+            Dft<A, true, C>::run(w);
 #pragma unroll
-            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = u[k1];
+            for (int k1 = 0; k1 < A; ++k1) fb[k1 * BP] = w[k1];
         }
         __syncthreads();
         // ---- 5. transpose of analysis pass 1: conjugate twiddles, inverse DFT
         // along the row, back to the longitudes n = t + A n2 (product gradients)
-        for (int task = tid; task < nrg * nz * A; task += NT) {
-            const int t = task % A, f = task / A, z = f % nz, r = f / nz;
-            const C* row = slot(r, zs0 + z) + t * BP;
+        for (int task = tid; task < nu * nz * A; task += NT) {
+            const int t = task % A, f = task / A, z = f % nz, u = f / nz;
+            const C* row = slot(u, zs0 + z) + t * BP;
             const C* twr = tw2 + t * BP;
             C v[B];
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) v[k2] = k2 == 0 ? row[0] : cmulc(row[k2], twr[k2]);
             Dft<B, true, C>::run(v);
-            C* zg = slot(r, zg0 + z);
+            C* zg = slot(u, zg0 + z);
 #pragma unroll
             for (int i = 0; i < B; ++i) {
                 const int nn = t + A * i;
@@ -261,8 +269,8 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         __syncthreads();
         // ---- 6. transpose of the products at longitudes n and -n; the lifts'
         // transforms are overwritten in place with their gradients
-        for (int task = tid; task < nrg * H; task += NT) {
-            const int nn = task % H, r = task / H;
+        for (int task = tid; task < nu * H; task += NT) {
+            const int nn = task % H, r = task / H;   // r: unit
             const int kk = nn == 0 ? 0 : Phi - nn;
             const int pn = nn + nn / B, pk = kk + kk / B;
             const bool self = kk == nn;
@@ -351,8 +359,8 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         }
         __syncthreads();
         // ---- 7. transpose of synthesis pass 2: forward DFT down the columns
-        for (int task = tid; task < nrg * nslot * B; task += NT) {
-            const int k2 = task % B, f = task / B, s = f % nslot, r = f / nslot;
+        for (int task = tid; task < nu * nslot * B; task += NT) {
+            const int k2 = task % B, f = task / B, s = f % nslot, r = f / nslot;   // r: unit
             C* fb = slot(r, s) + k2;
             C u[A];
 #pragma unroll
@@ -365,17 +373,18 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         // ---- 8. transpose of synthesis pass 1: twiddles, forward DFT along the
         // row; the coefficient gradient at longitude n = t + A n2 is that times
         // the Legendre value, kept in natural order in slot nslot + s
-        for (int task = tid; task < nrg * nslot * A; task += NT) {
-            const int t = task % A, f = task / A, s = f % nslot, r = f / nslot;
+        for (int task = tid; task < nu * nslot * A; task += NT) {
+            const int t = task % A, f = task / A, s = f % nslot, u = f / nslot;
+            const int r = u / P;
             const bool first = cross ? (s < 2) : (s == 0);
-            const C* row = slot(r, s) + t * BP;
+            const C* row = slot(u, s) + t * BP;
             const C* twr = tw2 + t * BP;
             C v[B];
 #pragma unroll
             for (int k2 = 0; k2 < B; ++k2) v[k2] = k2 == 0 ? row[0] : cmul(row[k2], twr[k2]);
             Dft<B, false, C>::run(v);
             const T* pr = prs + (size_t)(2 * r + (first ? 0 : 1)) * Phi + t;
-            C* out = slot(r, nslot + s);
+            C* out = slot(u, nslot + s);
 #pragma unroll
             for (int i = 0; i < B; ++i) {
                 const T pv = pr[A * i];
@@ -383,11 +392,11 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
             }
         }
         __syncthreads();
-        // ---- 9. sum over the group's rings, in ring order
-        for (int e = tid; e < nslot * Phi; e += NT) {
-            const int s = e / Phi, nn = e - s * Phi;
+        // ---- 9. sum over the group's rings, in ring order, per pair
+        for (int e = tid; e < P * nslot * Phi; e += NT) {
+            const int ps = e / Phi, nn = e - ps * Phi, pp = ps / nslot, s = ps - pp * nslot;
             C sum = cacc[e];
-            for (int r = 0; r < nrg; ++r) sum = cadd(sum, slot(r, nslot + s)[nn]);
+            for (int r = 0; r < nrg; ++r) sum = cadd(sum, slot(r * P + pp, nslot + s)[nn]);
             cacc[e] = sum;
         }
         __syncthreads();
@@ -395,11 +404,13 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
 
     // ---- transpose of the lift: each input component collects the gradients of
     // the lifted coefficients it was placed in, with the same weights
-    auto at = [&](int s, int m) -> C { return cacc[s * Phi + (m < 0 ? Phi + m : m)]; };
     auto sgn = [&](int m) -> T { return (m < 0 && ((-m) & 1)) ? (T)-1 : (T)1; };
-    for (int e = tid; e < n1 + n2; e += NT) {
-        const bool first = e < n1;
-        const int j = first ? j1 : j2, nj = 2 * j + 1, mj = first ? e : e - n1, mc = mj - j;
+    const int nrow = n1 + n2;
+    for (int e = tid; e < np * nrow; e += NT) {
+        const int pp = e / nrow, ee = e - pp * nrow;
+        auto at = [&](int s, int m) -> C { return cacc[(pp * nslot + s) * Phi + (m < 0 ? Phi + m : m)]; };
+        const bool first = ee < n1;
+        const int j = first ? j1 : j2, nj = 2 * j + 1, mj = first ? ee : ee - n1, mc = mj - j;
         const T* lcj = first ? lc : lc + 3 * n1;
         const int s0 = first ? 0 : (cross ? 2 : 1);   // the input's even slot
         // even slot, order mc: (x, C0 x)
@@ -411,23 +422,25 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
             if (mc + 1 <= j) acc += sgn(mc + 1) * lcj[mj + 1] * at(s0 + 1, mc + 1).x;
             if (mc - 1 >= -j) acc += sgn(mc - 1) * lcj[2 * nj + mj - 1] * at(s0 + 1, mc - 1).y;
         }
-        wrow[e] = acc;
+        wbase[(n0 + pp) * nrow + ee] = acc;
     }
 }
 
-// Work-group -> (block, pair); the block body for the block's longitude size.
+// Work-group -> (block, tile of pairs); the block body for the block's longitude size.
 template <typename T, bool SMALL>
 __global__ __launch_bounds__(SMALL ? kBwdSmallThreads : kBwdThreads) void bwd_kernel(
         Tables<T> tb, const int32_t* __restrict__ list, const T* __restrict__ x1, const T* __restrict__ x2,
         const T* __restrict__ g, T* __restrict__ ws, int64_t N, int L) {
     extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int P = SMALL ? kBwdSmallPairs : 1;
+    const int64_t ntile = (N + P - 1) / P;
     const int64_t wg = blockIdx.x;
-    const int li = (int)(wg / N);
-    const int64_t n = wg - (int64_t)li * N;
+    const int li = (int)(wg / ntile);
+    const int64_t n0 = (wg - (int64_t)li * ntile) * P;
     const BlockDesc bd = tb.blocks[list[li]];
-    T* wrow = ws + bwd_block_off(L, bd.j1, bd.j2) * N + n * (2 * (bd.j1 + bd.j2) + 2);
+    T* wbase = ws + bwd_block_off(L, bd.j1, bd.j2) * N;
 #define CGTP_BCASE(PHI, A_, B_) \
-    case PHI: bwd_body<T, A_, B_, SMALL>(tb, bd, n, x1, x2, g, wrow, L, smem); break;
+    case PHI: bwd_body<T, A_, B_, SMALL>(tb, bd, n0, N, x1, x2, g, wbase, L, smem); break;
     switch (bd.Phi) {
         CGTP_BCASE(1, 1, 1)
         CGTP_BCASE(2, 2, 1)
@@ -487,7 +500,8 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const T* __restrict__ w
 template <typename T, bool SMALL>
 int launch_variant(const Tables<T>& tb, const int32_t* list, int64_t nblocks, int lds, const T* x1, const T* x2,
                    const T* g, T* ws, int64_t N, int L, void* stream) {
-    const int64_t grid = nblocks * N;
+    constexpr int P = SMALL ? kBwdSmallPairs : 1;
+    const int64_t grid = nblocks * ((N + P - 1) / P);
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     if (lds > 64 * 1024) {

@@ -184,18 +184,20 @@ struct TileGeom {
 // ---------------------------------------------------------------- gradients
 //
 // The gradient kernel (cgtp_backward.hip) runs one work-group per (block,
-// pair), in two sizes: 256 threads for blocks with (2 J + 1) * components <=
-// kBwdSmallThreads, 768 for the others.  The transposed Legendre projection
+// tile of pairs), in two sizes: 256 threads and kBwdSmallPairs pairs for
+// blocks with (2 J + 1) * components <= kBwdSmallThreads, 768 threads and one
+// pair for the others.  The transposed Legendre projection
 // runs on 16x16x4 MFMA per |m|: wave w owns |m| = w, w + waves, ..., and holds
 // the gradients of those accumulator entries in registers as B operands
 // (lane: rows 4 s + lane / 16, column lane % 16 = (sign, component)).  LDS, in
 // byte offsets: couplings [3][n1 + n2], twiddles in pass layout, the pair's
-// lifted coefficients and their gradients ([slot][Phi] each), then per ring
-// group the Legendre values [ring][input][Phi] and kBwdSlots transforms per
-// ring.
+// lifted coefficients and their gradients ([pair][slot][Phi] each), then per
+// ring group the Legendre values [ring][input][Phi] and kBwdSlots transforms
+// per (ring, pair).
 constexpr int kBwdThreads = 768;         // large blocks
 constexpr int kBwdSmallThreads = 256;    // small blocks
 constexpr int kBwdSmallLds = 52 * 1024;  // small blocks: ring groups sized for three work-groups per CU
+constexpr int kBwdSmallPairs = 2;        // small blocks: pairs per work-group (a cross block's 8 columns each)
 constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
 // Register budget of the B operands: |m| values per wave (mpw) and, for the
 // t-th of them (|m| >= waves * t), K steps of 4 rows.  A block's |m| has at
@@ -220,7 +222,7 @@ __host__ __device__ inline int bwd_columns(const BlockDesc& b) {
 }
 __host__ __device__ inline bool bwd_small(const BlockDesc& b) { return bwd_columns(b) <= kBwdSmallThreads; }
 __host__ __device__ inline int bwd_align16(int v) { return (v + 15) & ~15; }
-__host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int rings) {
+__host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int rings, int pairs) {
     const int csz = 2 * esz;
     const bool cross = b.kind == kBlockCross;
     const int nslot = cross ? 4 : 2;
@@ -229,10 +231,10 @@ __host__ __device__ inline BwdLayout bwd_layout(const BlockDesc& b, int esz, int
     int o = 0;
     l.lc = o; o = bwd_align16(o + esz * 3 * (n1 + n2));
     l.tw2 = o; o = bwd_align16(o + csz * b.A * (b.B + 1));
-    l.cvn = o; o = bwd_align16(o + csz * nslot * b.Phi);
-    l.cacc = o; o = bwd_align16(o + csz * nslot * b.Phi);
+    l.cvn = o; o = bwd_align16(o + csz * pairs * nslot * b.Phi);
+    l.cacc = o; o = bwd_align16(o + csz * pairs * nslot * b.Phi);
     l.prs = o; o = bwd_align16(o + esz * rings * 2 * b.Phi);
-    l.fbuf = o; o += csz * rings * kBwdSlots * slot_stride(b.A, b.B);
+    l.fbuf = o; o += csz * rings * pairs * kBwdSlots * slot_stride(b.A, b.B);
     l.end = o;
     return l;
 }

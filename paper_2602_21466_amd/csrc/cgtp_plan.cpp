@@ -573,15 +573,17 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.bwd_rings = 0;
             {
                 const bool small = cgtp::bwd_small(b);
+                const int bp = small ? cgtp::kBwdSmallPairs : 1;
                 for (int pass = small ? 0 : 1; pass < 2 && !b.bwd_rings; ++pass)
                     for (int G = 8; G >= 1 && !b.bwd_rings; G /= 2)
-                        if (cgtp::bwd_layout(b, (int)sizeof(T), G).end <= (pass ? cgtp::kLdsBudget : cgtp::kBwdSmallLds))
+                        if (cgtp::bwd_layout(b, (int)sizeof(T), G, bp).end <=
+                            (pass ? cgtp::kLdsBudget : cgtp::kBwdSmallLds))
                             b.bwd_rings = G;
                 // the register-held entry gradients (B operands of the transposed projection)
                 if (!cgtp::bwd_fits<T>(b)) b.bwd_rings = 0;
                 if (b.bwd_rings) {
                     int& lds = small ? p->bwd_lds_small : p->bwd_lds_large;
-                    lds = std::max(lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings).end);
+                    lds = std::max(lds, cgtp::bwd_layout(b, (int)sizeof(T), b.bwd_rings, bp).end);
                 }
             }
             if (b.bwd_rings == 0) p->bwd_ok = false;
