@@ -58,7 +58,7 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     constexpr int FS = slot_stride(A, B);
     constexpr int NT = SMALL ? kBwdSmallThreads : kBwdThreads;
     constexpr int NW = NT / 64;                       // waves
-    constexpr int P = SMALL ? kBwdSmallPairs : 1;     // pairs of the work-group
+    constexpr int P = SMALL ? kBwdSmallPairs : kBwdLargePairs;   // pairs of the work-group
     constexpr int MPW = BwdGeom<T, SMALL>::mpw;       // |m| values per wave
     constexpr int KS = bwd_ks<T, SMALL>(0);           // MFMA K steps (4 rows each) of the first |m|
     using Acc = typename Cplx<T>::acc4;
@@ -432,7 +432,7 @@ __global__ __launch_bounds__(SMALL ? kBwdSmallThreads : kBwdThreads) void bwd_ke
         Tables<T> tb, const int32_t* __restrict__ list, const T* __restrict__ x1, const T* __restrict__ x2,
         const T* __restrict__ g, T* __restrict__ ws, int64_t N, int L) {
     extern __shared__ __align__(16) unsigned char smem[];
-    constexpr int P = SMALL ? kBwdSmallPairs : 1;
+    constexpr int P = SMALL ? kBwdSmallPairs : kBwdLargePairs;
     const int64_t ntile = (N + P - 1) / P;
     const int64_t wg = blockIdx.x;
     const int li = (int)(wg / ntile);
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const T* __restrict__ w
 template <typename T, bool SMALL>
 int launch_variant(const Tables<T>& tb, const int32_t* list, int64_t nblocks, int lds, const T* x1, const T* x2,
                    const T* g, T* ws, int64_t N, int L, void* stream) {
-    constexpr int P = SMALL ? kBwdSmallPairs : 1;
+    constexpr int P = SMALL ? kBwdSmallPairs : kBwdLargePairs;
     const int64_t grid = nblocks * ((N + P - 1) / P);
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;

@@ -198,6 +198,7 @@ constexpr int kBwdThreads = 768;         // large blocks
 constexpr int kBwdSmallThreads = 256;    // small blocks
 constexpr int kBwdSmallLds = 52 * 1024;  // small blocks: ring groups sized for three work-groups per CU
 constexpr int kBwdSmallPairs = 2;        // small blocks: pairs per work-group (a cross block's 8 columns each)
+constexpr int kBwdLargePairs = 2;        // large blocks: pairs per work-group
 constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
 // Register budget of the B operands: |m| values per wave (mpw) and, for the
 // t-th of them (|m| >= waves * t), K steps of 4 rows.  A block's |m| has at

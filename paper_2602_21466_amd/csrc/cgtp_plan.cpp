@@ -573,7 +573,7 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             b.bwd_rings = 0;
             {
                 const bool small = cgtp::bwd_small(b);
-                const int bp = small ? cgtp::kBwdSmallPairs : 1;
+                const int bp = small ? cgtp::kBwdSmallPairs : cgtp::kBwdLargePairs;
                 for (int pass = small ? 0 : 1; pass < 2 && !b.bwd_rings; ++pass)
                     for (int G = 8; G >= 1 && !b.bwd_rings; G /= 2)
                         if (cgtp::bwd_layout(b, (int)sizeof(T), G, bp).end <=
