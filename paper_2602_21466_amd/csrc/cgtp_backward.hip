@@ -128,9 +128,11 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
     // component 0 at (l3 = j3, m3); an odd path reads, for q = -1, 0, +1,
     // component 2, 1, 3 at (l3 = j3 - 1, m3 - q) with the plan's term q + 1.
     // Each entry thus feeds one output, and its gradient is that term's weight
-    // times the output's gradient.  For |m| = wave + NW t, lane (k, j) holds the
-    // entries of rows l3 = d + 2 (tmin(|m|) + 4 s + k) in column j = (pair,
-    // sign, component): B[t][s].
+    // times the output's gradient.  For |m| = wave + NW t with nr rows and
+    // ks = ceil(nr / 4) MFMA K steps, lane (k, j) holds the entries of rows
+    // l3 = d + 2 (tmin(|m|) + ks k + s) in column j = (pair, sign, component):
+    // B[t][s].  (Each lane's rows are consecutive, so its weights, operand A of
+    // the same rows, come in a few wide loads.)
     const T* coefs = tb.coef + (size_t)bd.coef_off * 4;
     const int ncolp = 2 * ncomp;                        // columns of one pair
     const int cpair = li / ncolp, cc = li - cpair * ncolp;
@@ -154,8 +156,8 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         const bool ok = mp <= J && col_ok(mp) && cpair < np;
 #pragma unroll
         for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s) {
-            const int row = 4 * s + lk;
-            bq[t][s] = (ok && row < nr) ? entry_grad(ccomp, csign ? -mp : mp, l30 + 2 * row) : (T)0;
+            const int ksm = (nr + 3) / 4, row = ksm * lk + s;
+            bq[t][s] = (ok && s < ksm && row < nr) ? entry_grad(ccomp, csign ? -mp : mp, l30 + 2 * row) : (T)0;
         }
     }
     __syncthreads();
@@ -211,17 +213,15 @@ __device__ __forceinline__ void bwd_body(const Tables<T>& tb, const BlockDesc& b
         for (int t = 0; t < MPW; ++t) {
             const int mp = wave + NW * t;
             if (mp <= J) {
-                const int nr = nrows - tmin(mp);
-                const int w0 = (mp * bd.rpad + rg0 + li) * bd.wrow + (d + 2 * tmin(mp) - (J & 1)) / 2 + lk;
+                const int nr = nrows - tmin(mp), ksm = (nr + 3) / 4;
+                const int r0 = (d + 2 * tmin(mp) - (J & 1)) / 2 + ksm * lk;   // the lane's first table row
+                T a[KS];
+                load_run(wrsrc, ((mp * bd.rpad + rg0 + li) * bd.wrow + r0) * (int)sizeof(T),
+                         li < nrg ? min(ksm, bwd_ks<T, SMALL>(t)) : 0, a);
                 Acc acc = Acc(0);
 #pragma unroll
-                for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s) {
-                    if (4 * s < nr) {
-                        const T a = (li < nrg && 4 * s + lk < nr)
-                                        ? buffer_load<T>(wrsrc, (w0 + 4 * s) * (int)sizeof(T), 0) : (T)0;
-                        acc = mfma16(a, bq[t][s], acc);
-                    }
-                }
+                for (int s = 0; s < bwd_ks<T, SMALL>(t); ++s)
+                    if (s < ksm) acc = mfma16(ksm * lk + s < nr ? a[s] : (T)0, bq[t][s], acc);
                 if (col_ok(mp)) {
                     const int k = csign ? Phi - mp : mp;
                     const int pos = 2 * (k + k / B) + (ccomp & 1);

@@ -151,6 +151,36 @@ template <> __device__ __forceinline__ double buffer_load<double>(__amdgpu_buffe
     return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
 }
 
+// The first `cnt` (<= N) elements from byte offset voff of a buffer in
+// 16-byte loads (elements past cnt up to the last load's end are loaded too;
+// the rest of out is zero).  Offsets need element alignment only.  Each load
+// is reinterpreted as a whole vector of elements before any element is taken
+// out: taking 32-bit words out of the loaded vector and reinterpreting them
+// one by one has been seen to compile into a single-word load whose value is
+// copied to all four elements.
+typedef double f64x2 __attribute__((ext_vector_type(2)));
+template <int N>
+__device__ __forceinline__ void load_run(__amdgpu_buffer_rsrc_t r, int voff, int cnt, float (&out)[N]) {
+#pragma unroll
+    for (int c = 0; c < (N + 3) / 4; ++c) {
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (4 * c < cnt) v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16 * c, 0, 0));
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (4 * c + e < N) out[4 * c + e] = v[e];
+    }
+}
+template <int N>
+__device__ __forceinline__ void load_run(__amdgpu_buffer_rsrc_t r, int voff, int cnt, double (&out)[N]) {
+#pragma unroll
+    for (int c = 0; c < (N + 1) / 2; ++c) {
+        f64x2 v = {0.0, 0.0};
+        if (2 * c < cnt) v = __builtin_bit_cast(f64x2, __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16 * c, 0, 0));
+        out[2 * c] = v[0];
+        if (2 * c + 1 < N) out[2 * c + 1] = v[1];
+    }
+}
+
 // ---------------------------------------------------------------- MFMA
 
 __device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c) {
