@@ -555,7 +555,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             const T* e1 = bbuf + ix.y;
             const T* e2 = bbuf + ix.z;
             const T* wq = wl + (ix.w >> 1);   // weight of this output's path, row p at nbp p
-            // two rows at a time; each row's store goes through a wave-uniform row pointer
+            // two rows at a time; each row's store goes through a wave-uniform row
+            // pointer, non-temporal (the outputs are not read again here)
 #pragma unroll 2
             for (int p = 0; p < np; ++p) {
                 T z = cf.x * e0[4 * p];
@@ -564,7 +565,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                     if (ch.w) z *= wq[p * nbp];
                 }
                 T* orow = ob + (int64_t)p * nout;
-                orow[o] = z;
+                __builtin_nontemporal_store(z, orow + o);
             }
         }
     }

@@ -569,6 +569,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
         const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
         const int nout = d.nout, hs = NC * no;
+        // (outputs are stored non-temporally: they are not read again here)
         for (int o = tid; o < nout; o += kThreads) {
             const Acc ca = cf4[2 * o], cb = cf4[2 * o + 1];
             const int4 ia = ci4[2 * o], ib = ci4[2 * o + 1];
@@ -585,7 +586,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     cc = cc + 1 == ch.channels ? 0 : cc + 1;
                 }
                 if (d.flags & kNegate) v = -v;
-                out[(p0 + p) * (int64_t)nout + o] = v;
+                __builtin_nontemporal_store(v, out + (p0 + p) * (int64_t)nout + o);
             }
         }
     } else {
@@ -611,7 +612,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                         T v = cf[u].x * hp[ix[u].x];
                         if (S == 1) v += cf[u].y * hp[ix[u].y] + cf[u].z * hp[ix[u].z];
                         if (d.flags & kNegate) v = -v;
-                        out[(p0 + p) * (int64_t)nout + o] = v;
+                        __builtin_nontemporal_store(v, out + (p0 + p) * (int64_t)nout + o);
                     }
                 } else {
                     // output label weight of row p: row k of wo, k = the row or its channel
@@ -627,7 +628,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                         }
                         cc = cc + 1 == ch.channels ? 0 : cc + 1;
                         if (d.flags & kNegate) v = -v;
-                        out[(p0 + p) * (int64_t)nout + o] = v;
+                        __builtin_nontemporal_store(v, out + (p0 + p) * (int64_t)nout + o);
                     }
                 }
             }
