@@ -62,7 +62,7 @@ MEASURED_TRAFFIC = {
 DIGEST_SOURCES = {
     "cgtp": ("cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "cgtp_backward": ("cgtp_backward.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
-    "cgtp_real": ("cgtp_real.hip", "cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
+    "cgtp_real": ("cgtp_kernels_real.hip", "cgtp_kernels.hip", "cgtp_plan.cpp", "cgtp_internal.h", "device_common.h"),
     "istp": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
@@ -142,7 +142,7 @@ def time_workload(w, steps, warmup, backward=True):
                                   w.N, steps, warmup))
         res["backward"] = bwd
         del g, g1, g2, ws
-        # the real spherical-harmonic basis (cgtp_forward_real: conversions and three products)
+        # the real spherical-harmonic basis (cgtp_forward_real: the block kernel's real-basis variant)
         out = torch.empty((w.N, w.n_outputs), dtype=a.dtype, device="cuda")
         need = lib.cgtp_real_workspace_bytes(plan._h, w.N)
         ws = torch.empty(need, dtype=torch.uint8, device="cuda")

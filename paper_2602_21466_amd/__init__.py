@@ -469,14 +469,9 @@ class Plan:
             out = torch.empty((N, nout), dtype=tdt, device=x1.device)
         elif out.dtype != tdt or not out.is_contiguous() or tuple(out.shape) != (N, nout):
             raise ValueError("out must be a contiguous %s tensor [N, (L+1)^4]" % tdt)
-        need = cgtp_real_workspace_bytes(self._h, N)
-        if workspace is None:
-            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x1.device)
-        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or workspace.numel() < need:
-            raise ValueError("workspace must be a uint8 CUDA tensor of at least %d bytes" % need)
+        # (the fused kernel needs no workspace: `workspace` is accepted and unused)
         s = stream if stream is not None else torch.cuda.current_stream(x1.device)
-        cgtp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, workspace.data_ptr(),
-                          workspace.numel(), s.cuda_stream)
+        cgtp_forward_real(self._h, x1.data_ptr(), x2.data_ptr(), out.data_ptr(), N, None, 0, s.cuda_stream)
         return out
 
     def backward_query(self) -> dict:

@@ -105,6 +105,8 @@ struct Tables {
     const T* coef;      // per block and output (j3, m3): up to three term weights (4 per output)
     const int32_t* coefi;   // per block and output: end-phase entries of the terms for pair 0; bit 0 of the
                             // fourth word flags a single term, the bits above it hold j3 - |j1 - j2|
+    const T* coefr;         // the same for outputs in the real basis: four term weights per output
+    const int32_t* coefir;  // and their four entries (no flags)
     const TileDesc* tdesc;
     int32_t wtab_len;   // elements of wtab
     const BlockDesc* blocks;
@@ -293,16 +295,14 @@ int launch_blocks_channels_f64(const Tables<double>& tb, const int32_t* block_li
                                int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
                                int L, const ChanArgs<double>& ch, void* stream);
 
-// Real basis: real rows -> (a, b, a + b) of their complex coefficients, and
-// the three products -> real-basis paths in place (cgtp_real.hip).
-int launch_real_in_f32(const float* r1, const float* r2, float* xa1, float* xbc1, float* xa2, float* xbc2,
-                       int64_t N, int L, void* stream);
-int launch_real_in_f64(const double* r1, const double* r2, double* xa1, double* xbc1, double* xa2, double* xbc2,
-                       int64_t N, int L, void* stream);
-int launch_real_out_f32(float* out, const float* z, const int32_t* half, int64_t nhalf, int64_t N, int L,
-                        void* stream);
-int launch_real_out_f64(double* out, const double* z, const int32_t* half, int64_t nhalf, int64_t N, int L,
-                        void* stream);
+// Real basis: the block kernel with real-basis rows in and out
+// (cgtp_kernels_real.hip), tables coefr / coefir for the end phase.
+int launch_blocks_real_f32(const Tables<float>& tb, const int32_t* block_list, const LaunchMap& map,
+                           int lds_bytes, const float* x1, const float* x2, float* out, int64_t N,
+                           int L, void* stream);
+int launch_blocks_real_f64(const Tables<double>& tb, const int32_t* block_list, const LaunchMap& map,
+                           int lds_bytes, const double* x1, const double* x2, double* out, int64_t N,
+                           int L, void* stream);
 
 // Gradients: the per-block kernels (block_list: the nsmall small-variant
 // blocks, then the nlarge others) over their blocks x N pairs into ws, then

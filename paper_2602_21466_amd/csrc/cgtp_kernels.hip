@@ -32,11 +32,16 @@
 
 // This file builds the plain kernel (block_kernel); with CGTP_CHANNEL_KERNELS
 // set to 1 it builds the channel-wise, path-weighted one instead
-// (block_kernel_channels, cgtp_kernels_channels.hip).  The plain kernel carries
-// none of the channel bookkeeping, which would cost it registers in the ring
-// loop.
+// (block_kernel_channels, cgtp_kernels_channels.hip), and with
+// CGTP_REAL_KERNELS set to 1 the one for inputs and outputs in the real
+// spherical-harmonic basis (block_kernel_real, cgtp_kernels_real.hip).  The
+// plain kernel carries none of their bookkeeping, which would cost it
+// registers in the ring loop.
 #ifndef CGTP_CHANNEL_KERNELS
 #define CGTP_CHANNEL_KERNELS 0
+#endif
+#ifndef CGTP_REAL_KERNELS
+#define CGTP_REAL_KERNELS 0
 #endif
 #ifndef CGTP_APRE_AT
 #define CGTP_APRE_AT 2
@@ -46,6 +51,8 @@ namespace cgtp {
 namespace {
 
 using namespace ::cgtp::dev;
+
+constexpr double kRsqrt2 = 0.70710678118654752440084436210485;
 
 __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
     BlockDesc b;
@@ -101,7 +108,17 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, boo
 
 // ---------------------------------------------------------------- the block body
 
-template <typename T, int A, int B, bool CH>
+// RL: real-basis rows.  A real function's complex coefficients are Hermitian,
+// c_-m = (-1)^m conj(c_m), and then (cross blocks) its scalar lift f_s is
+// real, its q = 0 lift f_0 is i times a real signal and f_-1 = conj(f_+1), so
+// one transform carries f_s + f_0 (series s_m + a0_m) and one f_+1 (series
+// a+_m); the products give the real gs, i times a real g0 and g+1 (g-1 =
+// conj(g+1)), carried as z1 = gs + g0 and z2 = g+1.  The MFMA columns are the
+// same (real and imaginary parts of z1 and z2 at +|m| and -|m|); the end
+// phase combines up to four of them per real-basis output (plan-made).
+// Blocks with a degree-0 input are a scaling, the same in either basis: they
+// run as in the complex basis.
+template <typename T, int A, int B, bool CH, bool RL>
 __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* __restrict__ tdesc,
                                            const BlockDesc& bd, int64_t pt0, int64_t pt1, int64_t N,
                                            const T* __restrict__ x1, const T* __restrict__ x2,
@@ -146,8 +163,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     };
     const TileDesc* __restrict__ td = tdesc + bd.tdesc_off;
     using Coef4 = typename Cplx<T>::acc4;
-    const Coef4* coef4 = reinterpret_cast<const Coef4*>(tb.coef) + bd.coef_off;
-    const int4* coefi = reinterpret_cast<const int4*>(tb.coefi) + bd.coef_off;
+    const Coef4* coef4 = reinterpret_cast<const Coef4*>(RL ? tb.coefr : tb.coef) + bd.coef_off;
+    const int4* coefi = reinterpret_cast<const int4*>(RL ? tb.coefir : tb.coefi) + bd.coef_off;
 
     // ---- block-level set-up: couplings, Legendre rows of every ring, twiddles
     for (int e = tid; e < 3 * n1; e += kThreads) lc[e] = tb.lcg[3 * j1 * j1 + e];
@@ -269,7 +286,28 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             const int64_t row = xr * nin + j * j;
             const T* lcj = first ? lc : lc + 3 * n1;
             const T sg = (m < 0 && (am & 1)) ? (T)-1 : (T)1;
-            if (!cross || (s & 1) == 0) {
+            if (RL && cross) {
+                // complex coefficient of order k from the real-basis row:
+                // c_0 = r_0, c_k = (-1)^k (r_k - i r_-k) / sqrt 2, c_-k = (r_k + i r_-k) / sqrt 2
+                const T* r0 = xg + row + j;
+                auto coefc = [&](int k) -> C {
+                    const int ak = k < 0 ? -k : k;
+                    if (ak > j) return cmk<C>((T)0, (T)0);
+                    if (k == 0) return cmk<C>(r0[0], (T)0);
+                    const T rp = r0[ak] * (T)kRsqrt2, rm = r0[-ak] * (T)kRsqrt2;
+                    if (k < 0) return cmk<C>(rp, rm);
+                    return (ak & 1) ? cmk<C>(-rp, rm) : cmk<C>(rp, -rm);
+                };
+                if ((s & 1) == 0) {   // f_s + f_0: (1 + C^{j,m}_{j,m,1,0}) c_m
+                    const C c = coefc(m);
+                    const T f = sg * ((T)1 + lcj[nj + mj]);
+                    val = cmk<C>(f * c.x, f * c.y);
+                } else {              // f_+1: C^{j,m+1}_{j,m,1,1} c_{m+1}
+                    const C c = coefc(m + 1);
+                    const T f = sg * lcj[2 * nj + mj];
+                    val = cmk<C>(f * c.x, f * c.y);
+                }
+            } else if (!cross || (s & 1) == 0) {
                 const T xm = sg * xg[row + mj];
                 val = cmk<C>(xm, cross ? lcj[nj + mj] * xm : (T)0);
             } else {
@@ -382,8 +420,34 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
         T apre[kRingGroup / 4][MT];
         prefetch_weights(apre);
 #endif
-        // ---- 3. pointwise products on half the circle, mirrored
-        {
+        // ---- 3. pointwise products on half the circle, mirrored (real basis: on
+        // the whole circle, in place)
+        if (RL && cross) {
+            const int ntask = uw * Phi;
+            for (int task = lane; task < ntask; task += 64) {
+                const int n = task % Phi, rp = wave + kWaves * (task / Phi);
+                const int pn = n + n / B;
+                C* fb = rpbuf(rp);
+                // as = Re T1, a0 = i al (al = Im T1), a+ = T2, a- = conj(T2); b likewise
+                const C t1a = fb[pn], ap = fb[FS + pn], t1b = fb[2 * FS + pn], bp = fb[3 * FS + pn];
+                const T al = t1a.y, be = t1b.y;
+                const T ddot = ap.x * bp.x + ap.y * bp.y;   // Re(a+ conj b+)
+                // gs: as bs, or (dot) a+ b- - a0 b0 + a- b+ = 2 Re(a+ conj b+) + al be
+                const T gs = even_dot ? (T)2 * ddot + al * be : t1a.x * t1b.x;
+                T g0, gpx, gpy;
+                if (odd_sv) {   // g+ = as b+, g0 = as b0
+                    g0 = t1a.x * be;
+                    gpx = t1a.x * bp.x;
+                    gpy = t1a.x * bp.y;
+                } else {        // g+ = a+ b0 - a0 b+ = i (be a+ - al b+), g0 = a+ b- - a- b+ = 2 i Im(a+ conj b+)
+                    g0 = (T)2 * (ap.y * bp.x - ap.x * bp.y);
+                    gpx = -(be * ap.y - al * bp.y);
+                    gpy = be * ap.x - al * bp.x;
+                }
+                fb[2 * FS + pn] = cmk<C>(gs, g0);    // z1 = gs + g0 (g0 imaginary)
+                fb[3 * FS + pn] = cmk<C>(gpx, gpy);  // z2 = g+1
+            }
+        } else {
             const int ntask = uw * H;
             for (int task = lane; task < ntask; task += 64) {
                 const int n = task % H, rp = wave + kWaves * (task / H);
@@ -550,7 +614,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 cfn = coef4[o + kThreads];
                 ixn = coefi[o + kThreads];
             }
-            const bool one = ix.w & 1;   // scalar-scalar or dot path: one term
+            const bool one = !RL && (ix.w & 1);   // scalar-scalar or dot path: one term
             const T* e0 = bbuf + ix.x;    // the terms' entries for row 0; row p's are 4 p further on
             const T* e1 = bbuf + ix.y;
             const T* e2 = bbuf + ix.z;
@@ -561,6 +625,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             for (int p = 0; p < np; ++p) {
                 T z = cf.x * e0[4 * p];
                 if (!one) z += cf.y * e1[4 * p] + cf.z * e2[4 * p];
+                if constexpr (RL) z += cf.w * bbuf[ix.w + 4 * p];   // the real basis' fourth term
                 if constexpr (CH) {
                     if (ch.w) z *= wq[p * nbp];
                 }
@@ -574,7 +639,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
 }
 
 // Work-group -> (class, block, pair tiles) and the block body for its grid.
-template <typename T, bool CH>
+template <typename T, bool CH, bool RL>
 __device__ __forceinline__ void run_blocks(const Tables<T>& tb, const BlockDesc* __restrict__ blocks,
                                            const TileDesc* __restrict__ tdesc, const int32_t* __restrict__ list,
                                            const LaunchMap& map, const T* __restrict__ x1,
@@ -594,7 +659,7 @@ __device__ __forceinline__ void run_blocks(const Tables<T>& tb, const BlockDesc*
     const int64_t pt1 = (pt0 + map.tpw[cls]) < map.ntiles[cls] ? (pt0 + map.tpw[cls]) : map.ntiles[cls];
 
 #define CGTP_CASE(PHI, A_, B_) \
-    case PHI: block_body<T, A_, B_, CH>(tb, tdesc, bd, pt0, pt1, N, x1, x2, out, L, ch, smem); break;
+    case PHI: block_body<T, A_, B_, CH, RL>(tb, tdesc, bd, pt0, pt1, N, x1, x2, out, L, ch, smem); break;
     switch (bd.Phi) {
         CGTP_CASE(1, 1, 1)
         CGTP_CASE(2, 2, 1)
@@ -624,14 +689,23 @@ __device__ __forceinline__ void run_blocks(const Tables<T>& tb, const BlockDesc*
 #undef CGTP_CASE
 }
 
-#if !CGTP_CHANNEL_KERNELS
+#if CGTP_REAL_KERNELS
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void block_kernel_real(Tables<T> tb, const BlockDesc* __restrict__ blocks,
+                                                                 const TileDesc* __restrict__ tdesc,
+                                                                 const int32_t* __restrict__ list, LaunchMap map,
+                                                                 const T* __restrict__ x1, const T* __restrict__ x2,
+                                                                 T* __restrict__ out, int64_t N, int L) {
+    run_blocks<T, false, true>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ChanArgs<T>{nullptr, 1, 0, 0});
+}
+#elif !CGTP_CHANNEL_KERNELS
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void block_kernel(Tables<T> tb, const BlockDesc* __restrict__ blocks,
                                                             const TileDesc* __restrict__ tdesc,
                                                             const int32_t* __restrict__ list, LaunchMap map,
                                                             const T* __restrict__ x1, const T* __restrict__ x2,
                                                             T* __restrict__ out, int64_t N, int L) {
-    run_blocks<T, false>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ChanArgs<T>{nullptr, 1, 0, 0});
+    run_blocks<T, false, false>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ChanArgs<T>{nullptr, 1, 0, 0});
 }
 #else
 template <typename T>
@@ -639,7 +713,7 @@ __global__ __launch_bounds__(kThreads, 1) void block_kernel_channels(
         Tables<T> tb, const BlockDesc* __restrict__ blocks, const TileDesc* __restrict__ tdesc,
         const int32_t* __restrict__ list, LaunchMap map, const T* __restrict__ x1, const T* __restrict__ x2,
         T* __restrict__ out, int64_t N, int L, ChanArgs<T> ch) {
-    run_blocks<T, true>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ch);
+    run_blocks<T, true, false>(tb, blocks, tdesc, list, map, x1, x2, out, N, L, ch);
 }
 #endif
 
@@ -649,7 +723,9 @@ int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int l
     const int64_t grid = map.cum[map.ncls];
     if (grid <= 0) return 0;
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
-#if !CGTP_CHANNEL_KERNELS
+#if CGTP_REAL_KERNELS
+    const void* kern = (const void*)block_kernel_real<T>;
+#elif !CGTP_CHANNEL_KERNELS
     const void* kern = (const void*)block_kernel<T>;
 #else
     const void* kern = (const void*)block_kernel_channels<T>;
@@ -658,7 +734,11 @@ int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int l
         hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return (int)e;
     }
-#if !CGTP_CHANNEL_KERNELS
+#if CGTP_REAL_KERNELS
+    (void)ch;
+    hipLaunchKernelGGL(block_kernel_real<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb,
+                       tb.blocks, tb.tdesc, list, map, x1, x2, out, N, L);
+#elif !CGTP_CHANNEL_KERNELS
     (void)ch;
     hipLaunchKernelGGL(block_kernel<T>, dim3((unsigned)grid), dim3(kThreads), lds, (hipStream_t)stream, tb,
                        tb.blocks, tb.tdesc, list, map, x1, x2, out, N, L);
@@ -671,7 +751,16 @@ int launch(const Tables<T>& tb, const int32_t* list, const LaunchMap& map, int l
 
 }  // namespace
 
-#if !CGTP_CHANNEL_KERNELS
+#if CGTP_REAL_KERNELS
+int launch_blocks_real_f32(const Tables<float>& tb, const int32_t* list, const LaunchMap& map, int lds,
+                           const float* x1, const float* x2, float* out, int64_t N, int L, void* stream) {
+    return launch<float>(tb, list, map, lds, x1, x2, out, N, L, ChanArgs<float>{nullptr, 1, 0, 0}, stream);
+}
+int launch_blocks_real_f64(const Tables<double>& tb, const int32_t* list, const LaunchMap& map, int lds,
+                           const double* x1, const double* x2, double* out, int64_t N, int L, void* stream) {
+    return launch<double>(tb, list, map, lds, x1, x2, out, N, L, ChanArgs<double>{nullptr, 1, 0, 0}, stream);
+}
+#elif !CGTP_CHANNEL_KERNELS
 int launch_blocks_f32(const Tables<float>& tb, const int32_t* list, const LaunchMap& map, int lds, const float* x1,
                       const float* x2, float* out, int64_t N, int L, void* stream) {
     return launch<float>(tb, list, map, lds, x1, x2, out, N, L, ChanArgs<float>{nullptr, 1, 0, 0}, stream);

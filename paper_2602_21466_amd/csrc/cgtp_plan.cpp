@@ -356,8 +356,6 @@ struct cgtp_plan_s {
     int bwd_nsmall = 0;     // blocks of the small variant: the first entries of the gradient block list
     int bwd_list_off = 0;   // the gradient block list's offset in the uploaded block lists
     const int32_t* d_bwd_list = nullptr;
-    const int32_t* d_rhalf = nullptr;   // real basis: HostTables::rhalf
-    int64_t nhalf = 0;
     bool bwd_ok = true;     // every block fits one of the gradient kernel's variants
     int max_theta = 0, max_phi = 0;
     double min_abs_K = 0, flops_per_pair = 0, bytes_per_pair = 0;
@@ -369,10 +367,9 @@ namespace {
 
 template <typename T>
 struct HostTables {
-    std::vector<T> pbar, wtab, tw, lcg, coef;
-    std::vector<int32_t> coefi;
+    std::vector<T> pbar, wtab, tw, lcg, coef, coefr;
+    std::vector<int32_t> coefi, coefir;
     std::vector<cgtp::TileDesc> tdesc;
-    std::vector<int32_t> rhalf;   // real basis: per path and |m3|, see real_out_kernel
 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -673,6 +670,105 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
                         }
                     }
                 }
+                // The same outputs in the real basis (four terms each).  Blocks with
+                // a degree-0 input scale the other input, the same in either basis:
+                // their terms are the complex basis' ones.  Cross blocks: the
+                // accumulators hold, per component c and order m, A_c[m] = the
+                // projection of Re z1, Im z1, Re z2, Im z2 with P^|m|; with the true
+                // P^m (sign (-1)^m for m < 0) they give Pi1[m] = A_0 + i A_1 and
+                // Pi2[m] = A_2 + i A_3 per row.  z1 = gs + g0 and z2 = g+ with gs
+                // real, g0 imaginary and g- = conj(g+) on the sphere, so per row
+                //   Pi[gs][m] = (Pi1[m] + (-1)^m conj Pi1[-m]) / 2,
+                //   Pi[g0][m] = (Pi1[m] - (-1)^m conj Pi1[-m]) / 2,
+                //   Pi[g+][m] = Pi2[m],  Pi[g-][m] = (-1)^m conj Pi2[-m].
+                // A path's complex output z (even: 1/K Pi[gs] at l3 = j3; odd: 1/K
+                // sum over q of C^{j3 m3}_{j3-1, m3-q, 1, q} Pi[g_q] at j3 - 1) is
+                // multiplied by i on odd paths and read in the real basis: r_0 =
+                // Re z_0, r_mu = sqrt 2 Re z_-mu, r_-mu = sqrt 2 Im z_-mu.
+                const size_t nr0 = h.coefr.size();
+                if (!cross) {
+                    for (size_t k = b.coef_off * (size_t)4; k < h.coef.size(); k += 4) {
+                        h.coefr.insert(h.coefr.end(), {h.coef[k], (T)0, (T)0, (T)0});
+                        const int32_t e0 = h.coefi[k];
+                        h.coefir.insert(h.coefir.end(), {e0, e0, e0, e0});
+                    }
+                } else {
+                    const long double sc_r = 2.0L * kPi / b.Phi;   // exact unpacking: no factor 1/4
+                    const long double sr_e = sc_r * ((b.products & cgtp::kEvenDot) ? cg_vec(1, 1, -1, 0, 0) : 1.0L);
+                    const long double sr_v = sc_r * ((b.products & cgtp::kOddSV) ? 1.0L : cg_vec(1, 1, 0, 1, 1));
+                    // linear forms over accumulator entries (entry of pair 0 -> weight)
+                    using Form = std::map<int, long double>;
+                    auto put = [&](Form& f, int comp, int m, int tr, int l, long double w) {
+                        if (std::abs(m) > l || w == 0.0L) return;
+                        long double sg;
+                        const int e = entry(comp, m, tr, &sg);
+                        sg = (m < 0 && (std::abs(m) & 1)) ? -1.0L : 1.0L;
+                        f[e] += w * sg;
+                    };
+                    auto par = [](int m) { return (std::abs(m) & 1) ? -1.0L : 1.0L; };
+                    const long double rt2 = std::sqrt(2.0L);
+                    for (int j3 = b.d; j3 <= b.J; ++j3) {
+                        const bool odd = (b.J + j3) & 1;
+                        const int l3 = odd ? j3 - 1 : j3, tr = (l3 - b.d) / 2;
+                        for (int m3 = -j3; m3 <= j3; ++m3) {
+                            const int M = -std::abs(m3);
+                            Form zr, zi;   // Re z_M, Im z_M
+                            if (!odd) {
+                                const long double k = kinv[j3] * sr_e, s = par(M);
+                                put(zr, 0, M, tr, l3, k / 2);
+                                put(zr, 0, -M, tr, l3, k * s / 2);
+                                put(zi, 1, M, tr, l3, k / 2);
+                                put(zi, 1, -M, tr, l3, -k * s / 2);
+                            } else {
+                                for (int q = -1; q <= 1; ++q) {
+                                    const int mq = M - q;
+                                    if (std::abs(mq) > l3) continue;
+                                    const long double c = kinv[j3] * sr_v * cg_vec(l3, mq, q, j3, M), s = par(mq);
+                                    if (q == 0) {
+                                        put(zr, 0, mq, tr, l3, c / 2);
+                                        put(zr, 0, -mq, tr, l3, -c * s / 2);
+                                        put(zi, 1, mq, tr, l3, c / 2);
+                                        put(zi, 1, -mq, tr, l3, c * s / 2);
+                                    } else if (q == 1) {
+                                        put(zr, 2, mq, tr, l3, c);
+                                        put(zi, 3, mq, tr, l3, c);
+                                    } else {
+                                        put(zr, 2, -mq, tr, l3, c * s);
+                                        put(zi, 3, -mq, tr, l3, -c * s);
+                                    }
+                                }
+                            }
+                            // w = z (even) or i z (odd); output Re w (m3 >= 0) or Im w (m3 < 0)
+                            const Form* f;
+                            long double sgn = 1.0L;
+                            if (!odd)
+                                f = m3 < 0 ? &zi : &zr;
+                            else if (m3 < 0)
+                                f = &zr;   // Im(i z) = Re z
+                            else {
+                                f = &zi;   // Re(i z) = -Im z
+                                sgn = -1.0L;
+                            }
+                            if (m3 != 0) sgn *= rt2;
+                            T w[4] = {(T)0, (T)0, (T)0, (T)0};
+                            int32_t ei[4] = {-1, -1, -1, -1};
+                            int nt = 0;
+                            for (const auto& kv : *f) {
+                                if (kv.second == 0.0L) continue;
+                                if (nt == 4) return CGTP_EUNSUP;   // cannot happen: at most four entries
+                                w[nt] = (T)(sgn * kv.second);
+                                ei[nt++] = kv.first;
+                            }
+                            long double unused;
+                            const int32_t any = nt ? ei[0] : entry(0, 0, 0, &unused);
+                            for (int k = 0; k < 4; ++k)
+                                if (ei[k] < 0) ei[k] = any;   // zero weight; any entry of the block
+                            h.coefr.insert(h.coefr.end(), {w[0], w[1], w[2], w[3]});
+                            h.coefir.insert(h.coefir.end(), {ei[0], ei[1], ei[2], ei[3]});
+                        }
+                    }
+                }
+                if (h.coefr.size() - nr0 != h.coef.size() - (size_t)b.coef_off * 4) return CGTP_EUNSUP;
             }
             p->lds_bytes = std::max(p->lds_bytes, b.lds_bytes);
             blocks.push_back(b);
@@ -715,26 +811,14 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
     p->bwd_nsmall = (int)bs.size();
     list.insert(list.end(), bs.begin(), bs.end());
     list.insert(list.end(), bl.begin(), bl.end());
-    // real basis: one entry per path and |m3| <= l3: the index of m3 = 0 in a
-    // pair's row, |m3| and the parity of l1 + l2 + l3
-    h.rhalf.clear();
-    for (int l1 = 0; l1 <= L; ++l1)
-        for (int l2 = 0; l2 <= L; ++l2)
-            for (int l3 = std::abs(l1 - l2); l3 <= l1 + l2; ++l3) {
-                const int64_t base = path_offset(L, l1, l2, l3) + l3;
-                if (base >= (1 << 21)) return CGTP_EUNSUP;
-                for (int mu = 0; mu <= l3; ++mu)
-                    h.rhalf.push_back((int32_t)(base | (int64_t)mu << 21 | (int64_t)((l1 + l2 + l3) & 1) << 28));
-            }
-    p->nhalf = (int64_t)h.rhalf.size();
     return CGTP_OK;
 }
 
 template <typename T>
 int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTables<T>& h,
            const std::vector<int32_t>& list, cgtp::Tables<T>* tb) {
-    const std::vector<T>* parts[] = {&h.pbar, &h.wtab, &h.tw, &h.lcg, &h.coef};
-    constexpr int kParts = 5;
+    const std::vector<T>* parts[] = {&h.pbar, &h.wtab, &h.tw, &h.lcg, &h.coef, &h.coefr};
+    constexpr int kParts = 6;
     size_t offs[kParts + 2];
     size_t total = 0;
     for (int i = 0; i < kParts; ++i) {
@@ -749,13 +833,14 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     total = align_up(total + h.tdesc.size() * sizeof(cgtp::TileDesc), 256);
     const size_t coefi_off = total;
     total = align_up(total + h.coefi.size() * sizeof(int32_t), 256);
-    const size_t rhalf_off = total;
-    total = align_up(total + h.rhalf.size() * sizeof(int32_t), 256);
+    const size_t coefir_off = total;
+    total = align_up(total + h.coefir.size() * sizeof(int32_t), 256);
     std::vector<char> host(total, 0);
     if (!h.tdesc.empty())
         std::memcpy(host.data() + tdesc_off, h.tdesc.data(), h.tdesc.size() * sizeof(cgtp::TileDesc));
     if (!h.coefi.empty()) std::memcpy(host.data() + coefi_off, h.coefi.data(), h.coefi.size() * sizeof(int32_t));
-    if (!h.rhalf.empty()) std::memcpy(host.data() + rhalf_off, h.rhalf.data(), h.rhalf.size() * sizeof(int32_t));
+    if (!h.coefir.empty())
+        std::memcpy(host.data() + coefir_off, h.coefir.data(), h.coefir.size() * sizeof(int32_t));
     for (int i = 0; i < kParts; ++i)
         if (!parts[i]->empty()) std::memcpy(host.data() + offs[i], parts[i]->data(), parts[i]->size() * sizeof(T));
     std::memcpy(host.data() + offs[kParts], blocks.data(), blocks.size() * sizeof(BlockDesc));
@@ -781,12 +866,13 @@ int upload(cgtp_plan_s* p, const std::vector<BlockDesc>& blocks, const HostTable
     tb->lcg = (const T*)(base + offs[3]);
     tb->coef = (const T*)(base + offs[4]);
     tb->coefi = (const int32_t*)(base + coefi_off);
+    tb->coefr = (const T*)(base + offs[5]);
+    tb->coefir = (const int32_t*)(base + coefir_off);
     tb->wtab_len = (int32_t)h.wtab.size();
     tb->blocks = (const BlockDesc*)(base + offs[kParts]);
     tb->tdesc = (const cgtp::TileDesc*)(base + tdesc_off);
     p->d_list = (const int32_t*)(base + offs[kParts + 1]);
     p->d_bwd_list = p->d_list + p->bwd_list_off;
-    p->d_rhalf = (const int32_t*)(base + rhalf_off);
     return CGTP_OK;
 }
 
@@ -949,7 +1035,7 @@ namespace {
 // Shared by both forward entry points: N rows (pair, channel), x2 with one row
 // per row or per pair, optional path weights.
 int forward_rows(cgtp_plan_t plan, const void* x1, const void* x2, const void* w, void* out, int64_t N,
-                 int32_t channels, int32_t flags, void* hip_stream) {
+                 int32_t channels, int32_t flags, void* hip_stream, bool real_basis = false) {
     const int L = plan->L;
     const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)(L + 1) * (L + 1), nout = (size_t)cgtp_num_outputs(L);
@@ -992,7 +1078,13 @@ int forward_rows(cgtp_plan_t plan, const void* x1, const void* x2, const void* w
     // one channel, no sharing, no weights: the plain kernel
     const bool plain = channels == 1 && flags == 0 && !w;
     int err;
-    if (plan->grid.dtype == CGTP_FP32) {
+    if (real_basis) {
+        err = plan->grid.dtype == CGTP_FP32
+                  ? cgtp::launch_blocks_real_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
+                                                 (const float*)x2, (float*)out, N, L, hip_stream)
+                  : cgtp::launch_blocks_real_f64(plan->td, plan->d_list, map, plan->lds_bytes, (const double*)x1,
+                                                 (const double*)x2, (double*)out, N, L, hip_stream);
+    } else if (plan->grid.dtype == CGTP_FP32) {
         const cgtp::ChanArgs<float> ch{(const float*)w, channels, flags, (int32_t)npaths};
         err = plain ? cgtp::launch_blocks_f32(plan->tf, plan->d_list, map, plan->lds_bytes, (const float*)x1,
                                               (const float*)x2, (float*)out, N, L, hip_stream)
@@ -1046,86 +1138,19 @@ int64_t cgtp_num_paths(int32_t L) { return L < 0 ? -1 : path_index(L, L + 1, 0, 
 
 }  // extern "C"
 
-namespace {
-
-// Workspace of cgtp_forward_real: per input the a rows [N] and the b, a + b
-// rows [2N] (each part 256-byte aligned), then the products P(b1, b2) and
-// P(a1 + b1, a2 + b2) [2N, (L+1)^4].
-struct RealWs {
-    int64_t xa1, xbc1, xa2, xbc2, z, total;
-};
-bool real_ws(const cgtp_plan_s* p, int64_t N, RealWs* w) {
-    const int64_t esz = p->grid.dtype == CGTP_FP32 ? 4 : 8;
-    const int64_t nin = (int64_t)(p->L + 1) * (p->L + 1), nout = nin * nin;
-    if (N < 0 || N > INT64_MAX / (8 * nout * esz)) return false;
-    auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
-    w->xa1 = 0;
-    w->xbc1 = w->xa1 + al(N * nin * esz);
-    w->xa2 = w->xbc1 + al(2 * N * nin * esz);
-    w->xbc2 = w->xa2 + al(N * nin * esz);
-    w->z = w->xbc2 + al(2 * N * nin * esz);
-    w->total = w->z + 2 * N * nout * esz;
-    return true;
-}
-
-}  // namespace
-
 extern "C" {
 
-int64_t cgtp_real_workspace_bytes(cgtp_plan_t plan, int64_t N) {
-    RealWs w;
-    if (!plan || !real_ws(plan, N, &w)) return -1;
-    return w.total;
-}
+// The fused kernel needs no workspace; the call keeps its workspace arguments.
+int64_t cgtp_real_workspace_bytes(cgtp_plan_t plan, int64_t N) { return (!plan || N < 0) ? -1 : 0; }
 
 int cgtp_forward_real(cgtp_plan_t plan, const void* x1, const void* x2, void* out, int64_t N, void* workspace,
                       int64_t workspace_bytes, void* hip_stream) {
-    if (!plan || N < 0) return CGTP_EINVAL;
+    (void)workspace;
+    if (!plan || N < 0 || workspace_bytes < 0) return CGTP_EINVAL;
     if (N == 0) return CGTP_OK;
-    if (!x1 || !x2 || !out || !workspace) return CGTP_EINVAL;
+    if (!x1 || !x2 || !out) return CGTP_EINVAL;
     if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
-    if ((uintptr_t)workspace & 255) return CGTP_EINVAL;
-    RealWs w;
-    if (!real_ws(plan, N, &w) || workspace_bytes < w.total) return CGTP_EINVAL;
-    const int L = plan->L;
-    const size_t esz = plan->grid.dtype == CGTP_FP32 ? 4 : 8;
-    const size_t nin = (size_t)(L + 1) * (L + 1), nout = nin * nin;
-    const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
-    if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin) ||
-        overlaps(workspace, (size_t)w.total, x1, bin) || overlaps(workspace, (size_t)w.total, x2, bin) ||
-        overlaps(workspace, (size_t)w.total, out, bout))
-        return CGTP_EINVAL;
-    int dev = -1;
-    const hipError_t de = hipGetDevice(&dev);
-    if (de != hipSuccess) {
-        g_last_hip_error = (int)de;
-        return CGTP_EHIP;
-    }
-    if (dev != plan->device) return CGTP_EINVAL;
-    char* ws = (char*)workspace;
-    void *xa1 = ws + w.xa1, *xbc1 = ws + w.xbc1, *xa2 = ws + w.xa2, *xbc2 = ws + w.xbc2, *z = ws + w.z;
-    int err = plan->grid.dtype == CGTP_FP32
-                  ? cgtp::launch_real_in_f32((const float*)x1, (const float*)x2, (float*)xa1, (float*)xbc1,
-                                             (float*)xa2, (float*)xbc2, N, L, hip_stream)
-                  : cgtp::launch_real_in_f64((const double*)x1, (const double*)x2, (double*)xa1, (double*)xbc1,
-                                             (double*)xa2, (double*)xbc2, N, L, hip_stream);
-    if (err != 0) {
-        g_last_hip_error = err;
-        return CGTP_EHIP;
-    }
-    // P(a1, a2) into out; P(b1, b2) and P(a1 + b1, a2 + b2) into the workspace
-    int rc = forward_rows(plan, xa1, xa2, nullptr, out, N, 1, 0, hip_stream);
-    if (rc == CGTP_OK) rc = forward_rows(plan, xbc1, xbc2, nullptr, z, 2 * N, 1, 0, hip_stream);
-    if (rc != CGTP_OK) return rc;
-    err = plan->grid.dtype == CGTP_FP32
-              ? cgtp::launch_real_out_f32((float*)out, (const float*)z, plan->d_rhalf, plan->nhalf, N, L, hip_stream)
-              : cgtp::launch_real_out_f64((double*)out, (const double*)z, plan->d_rhalf, plan->nhalf, N, L,
-                                          hip_stream);
-    if (err != 0) {
-        g_last_hip_error = err;
-        return CGTP_EHIP;
-    }
-    return CGTP_OK;
+    return forward_rows(plan, x1, x2, nullptr, out, N, 1, 0, hip_stream, true);
 }
 
 int cgtp_backward_query(cgtp_plan_t plan, double* flops_per_pair, double* bytes_per_pair) {

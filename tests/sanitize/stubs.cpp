@@ -29,12 +29,10 @@ int launch_blocks_channels_f32(const Tables<float>&, const int32_t*, const Launc
                                const float*, float*, int64_t, int, const ChanArgs<float>&, void*) { return 1; }
 int launch_blocks_channels_f64(const Tables<double>&, const int32_t*, const LaunchMap&, int, const double*,
                                const double*, double*, int64_t, int, const ChanArgs<double>&, void*) { return 1; }
-int launch_real_in_f32(const float*, const float*, float*, float*, float*, float*, int64_t, int, void*) { return 1; }
-int launch_real_in_f64(const double*, const double*, double*, double*, double*, double*, int64_t, int, void*) {
-    return 1;
-}
-int launch_real_out_f32(float*, const float*, const int32_t*, int64_t, int64_t, int, void*) { return 1; }
-int launch_real_out_f64(double*, const double*, const int32_t*, int64_t, int64_t, int, void*) { return 1; }
+int launch_blocks_real_f32(const Tables<float>&, const int32_t*, const LaunchMap&, int, const float*, const float*,
+                           float*, int64_t, int, void*) { return 1; }
+int launch_blocks_real_f64(const Tables<double>&, const int32_t*, const LaunchMap&, int, const double*,
+                           const double*, double*, int64_t, int, void*) { return 1; }
 int launch_backward_f32(const Tables<float>&, const BwdLaunch&, const float*, const float*, const float*, float*,
                         float*, float*, int64_t, int, void*) { return 1; }
 int launch_backward_f64(const Tables<double>&, const BwdLaunch&, const double*, const double*, const double*,

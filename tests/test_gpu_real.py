@@ -92,23 +92,31 @@ def test_real_large_subsample_and_norm_identity(L, N, rows):
     assert worst <= 1e-4
 
 
-def test_real_rejects_bad_workspace():
+def test_real_argument_errors_and_no_workspace():
+    """The fused kernel needs no workspace (0 bytes); bad pointers, misalignment, negative sizes and outputs that
+    overlap an input are rejected before anything is launched."""
     torch = _torch()
     lib = _lib()
     L, N = 3, 8
     plan = lib.Plan(L)
     f = lib._load()
+    assert lib.cgtp_real_workspace_bytes(plan._h, N) == 0
+    assert lib.cgtp_real_workspace_bytes(plan._h, -1) == -1
     x = torch.randn(N, 16, device="cuda")
+    big = torch.randn(N * 256 + 64, device="cuda")
     out = torch.full((N, 256), 7.0, device="cuda")
-    need = lib.cgtp_real_workspace_bytes(plan._h, N)
-    assert need >= (6 * N * 16 + 2 * N * 256) * 4
-    ws = torch.empty(need + 512, dtype=torch.uint8, device="cuda")
     P = lambda t, off=0: ctypes.c_void_p(t.data_ptr() + off)
-    for args in [(P(x), P(x), P(out), N, P(ws), need - 1),      # short
-                 (P(x), P(x), P(out), N, P(ws, 64), need),      # misaligned
-                 (P(x), P(x), P(out), N, None, need),           # missing
-                 (P(x), P(x), P(ws), N, P(ws), need),           # out inside the workspace
-                 (P(x), P(x), P(out), -1, P(ws), need)]:        # negative N
+    for args in [(None, P(x), P(out), N, None, 0),          # missing input
+                 (P(x), P(x), None, N, None, 0),            # missing output
+                 (P(x), P(x), P(out, 4), N, None, 0),       # misaligned output
+                 (P(x), P(x), P(out), -1, None, 0),         # negative N
+                 (P(x), P(x), P(out), N, None, -1),         # negative workspace size
+                 (P(big), P(x), P(big, 64), N, None, 0)]:   # output overlapping an input
         assert f.cgtp_forward_real(plan._h, *args, None) == lib.CGTP_EINVAL, args
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
+    # a call without workspace works (and N = 0 is a no-op)
+    assert f.cgtp_forward_real(plan._h, P(x), P(x), P(out), 0, None, 0, None) == lib.CGTP_OK
+    assert f.cgtp_forward_real(plan._h, P(x), P(x), P(out), N, None, 0, None) == lib.CGTP_OK
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out).all()) and not bool((out == 7.0).all())
