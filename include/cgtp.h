@@ -202,19 +202,19 @@ int cgtp_backward_query(cgtp_plan_t plan, double *flops_per_pair, double *bytes_
  * in the real basis, odd l1 + l2 + l3 paths (anti-Hermitian) after a factor i.
  * So the even paths are the real Gaunt integrals over K (Theorem 4.2 read in the
  * real basis) and path (1, 1, 1) is the cross product over sqrt(2) in the real
- * basis' (y, z, x) order.  Runs three cgtp_forward products (Karatsuba's form of
- * a complex product) between two conversion kernels.
- *   workspace: caller-owned device memory, 256-byte aligned, at least
- *   cgtp_real_workspace_bytes(plan, N) bytes: the converted inputs and two of
- *   the three products (the third is formed in out, then read back in place).
- * Rules otherwise as cgtp_forward; CGTP_EINVAL also for a short, misaligned or
- * overlapping workspace.  Allocates nothing; asynchronous on hip_stream.
+ * basis' (y, z, x) order.  One launch of the block kernel's real-basis
+ * variant: the inputs' Hermitian coefficients make every lifted signal real
+ * (or i times real, or a conjugate pair), so a cross block still needs two
+ * transforms per input; the end phase forms the real-basis outputs.
+ *   workspace, workspace_bytes: unused (kept for callers of an earlier version
+ *   that needed one); workspace may be NULL, workspace_bytes must be >= 0.
+ * Rules otherwise as cgtp_forward.  Allocates nothing; asynchronous on
+ * hip_stream.
  */
 int cgtp_forward_real(cgtp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
                       int64_t workspace_bytes, void *hip_stream);
 
-/* Workspace bytes cgtp_forward_real needs for N pairs (6 N (L+1)^2 + 2 N (L+1)^4 elements, parts 256-byte
-   aligned); -1 for a NULL plan, N < 0 or overflow. */
+/* Workspace bytes cgtp_forward_real needs for N pairs: 0; -1 for a NULL plan or N < 0. */
 int64_t cgtp_real_workspace_bytes(cgtp_plan_t plan, int64_t N);
 
 /* Number of paths of degree L: sum over l1, l2 <= L of 2 min(l1, l2) + 1; -1 for L < 0. */
