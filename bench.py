@@ -30,31 +30,42 @@ PEAK_FP64_TFLOPS = 78.6
 PEAK_HBM_GBS = 8000.0
 
 
-# HBM traffic of the block kernel from rocprofv3 counter runs (FETCH_SIZE and
-# WRITE_SIZE, KiB per dispatch, median over dispatches), each scaled by the
-# ratio of known bytes to the same counter over a plain device copy
-# (--copy-probe).  Keyed by a digest of the kernel and plan sources: once they
-# change, the figures no longer describe the kernel and traffic is null.
+# HBM traffic of each timed step from rocprofv3 counter runs (FETCH_SIZE and
+# WRITE_SIZE over a whole bench run, KiB summed over a step's launches, median
+# over the timed steps), each scaled by the ratio of known bytes to the same
+# counter over a plain device copy (--copy-probe).  Keyed by a digest of the
+# kernel and plan sources: once they change, the figures no longer describe the
+# kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "66216a927e9336b4": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 351548.9, "fetch_scale": 1.999956, "write_kib": 4812323.9, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 216943.0, "fetch_scale": 1.999956, "write_kib": 2738911.9, "write_scale": 1.000000},
+    "3ce5aa064a526a45": {
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 220648.2, "fetch_scale": 1.999956, "write_kib": 5701608.2, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 41325.5, "fetch_scale": 1.999956, "write_kib": 3153575.6, "write_scale": 1.000000},
     },
-    "98b2595f487717ca": {
-        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 118558.4, "fetch_scale": 1.999956, "write_kib": 2739759.3, "write_scale": 1.000000},
+    "4173d62bb601274c": {
+        "cgtp_L32_N1024_fp32:backward": {"fetch_kib": 2961072.8, "fetch_scale": 1.999956, "write_kib": 300568.0, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32:backward": {"fetch_kib": 2115042.4, "fetch_scale": 1.999956, "write_kib": 342208.0, "write_scale": 1.000000},
     },
-    "70492b96a487484c": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 302711.6, "fetch_scale": 1.999956, "write_kib": 811653.6, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 404508.9, "fetch_scale": 1.999956, "write_kib": 1084145.4, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 227652.8, "fetch_scale": 1.999956, "write_kib": 837123.1, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068437.1, "fetch_scale": 1.999956, "write_kib": 445440.0, "write_scale": 1.000000},
-        "tstp_L16_N16384_fp32": {"fetch_kib": 97086.1, "fetch_scale": 1.999956, "write_kib": 348928.0, "write_scale": 1.000000},
+    "57413782ae7a98b8": {
+        "cgtp_L32_N1024_fp32:real": {"fetch_kib": 223100.4, "fetch_scale": 1.999956, "write_kib": 5900140.5, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32:real": {"fetch_kib": 41482.0, "fetch_scale": 1.999956, "write_kib": 3286307.8, "write_scale": 1.000000},
     },
-    "1f9b11fd01348db2": {
-        "gtp_real_L16_N65536_fp32": {"fetch_kib": 228030.1, "fetch_scale": 1.999956, "write_kib": 836352.0, "write_scale": 1.000000},
+    "0cf4273a768d508c": {
+        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 30599.1, "fetch_scale": 1.999956, "write_kib": 3090072.7, "write_scale": 1.000000},
     },
-    "a371e45cd2275a5c": {
-        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170352.5, "fetch_scale": 1.999956, "write_kib": 837126.0, "write_scale": 1.000000},
+    "a46e27aaf2e902fb": {
+        "vstp_L32_N16384_fp32": {"fetch_kib": 216648.6, "fetch_scale": 1.999956, "write_kib": 986845.3, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 284794.2, "fetch_scale": 1.999956, "write_kib": 1311305.5, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227504.5, "fetch_scale": 1.999956, "write_kib": 1006590.0, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068316.0, "fetch_scale": 1.999956, "write_kib": 522849.4, "write_scale": 1.000000},
+        "tstp_L16_N16384_fp32": {"fetch_kib": 97086.0, "fetch_scale": 1.999956, "write_kib": 428103.1, "write_scale": 1.000000},
+    },
+    "a3adfc16bb75e8b2": {
+        "gtp_real_L16_N65536_fp32": {"fetch_kib": 769738.5, "fetch_scale": 1.999956, "write_kib": 1763803.6, "write_scale": 1.000000},
+        "gtp_real_L16_N65536_fp32:backward": {"fetch_kib": 1754308.8, "fetch_scale": 1.999956, "write_kib": 2809141.9, "write_scale": 1.000000},
+        "vstp_real_L16_N65536_fp32": {"fetch_kib": 2381784.8, "fetch_scale": 1.999956, "write_kib": 5198787.8, "write_scale": 1.000000},
+    },
+    "bea351de937a7bd5": {
+        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170282.8, "fetch_scale": 1.999956, "write_kib": 962973.0, "write_scale": 1.000000},
     },
 }
 
