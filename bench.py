@@ -77,8 +77,8 @@ DIGEST_SOURCES = {
     "istp": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "channels": ("cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_plan.cpp", "cgtp_internal.h",
                  "device_common.h"),
-    "istp_real": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_real.hip", "istp_plan.cpp", "istp_internal.h",
-                  "device_common.h"),
+    "istp_real": ("istp_kernels.hip", "istp_kernels_tensor.hip", "istp_kernels_real.hip", "istp_real.hip",
+                  "istp_plan.cpp", "istp_internal.h", "device_common.h"),
     "istp_channels": ("istp_kernels.hip", "istp_kernels_channels.hip", "istp_kernels_channels_tensor.hip",
                       "istp_plan.cpp", "istp_internal.h", "device_common.h"),
 }
@@ -235,7 +235,8 @@ def time_channels(w, steps, warmup):
 
 
 def time_istp_real(w, steps, warmup):
-    """A signal product in the real basis: two conversions, three products and the read-back per step."""
+    """A signal product in the real basis: spin 0 one launch of the real-basis kernel (no workspace); spins 1
+    and 2 two conversions, three products and the read-back per step."""
     import torch
 
     import paper_2602_21466_amd as lib
@@ -244,17 +245,20 @@ def time_istp_real(w, steps, warmup):
     plan = lib.IstpPlan(w.L, w.spin, w.dtype)
     a, b = x1.cuda(), x2.cuda()
     out = torch.empty((w.N, plan.nout), dtype=a.dtype, device="cuda")
-    ws = torch.empty(lib.istp_real_workspace_bytes(plan._h, w.N), dtype=torch.uint8, device="cuda")
+    need = lib.istp_real_workspace_bytes(plan._h, w.N)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     q = dict(plan.query())
-    # the method's work: three products; compulsory bytes: the inputs and the output once
-    q["flops_per_pair"] = 3 * q["flops_per_pair"]
+    # the method's work: one product's (the real-basis kernel) or three products; compulsory bytes: the
+    # inputs and the output once
+    nprod = 1 if need == 0 else 3
+    q["flops_per_pair"] = nprod * q["flops_per_pair"]
     res = {"workload": w.name, "L": w.L, "N": w.N, "dtype": w.dtype, "plan": q, "kind": "istp_real"}
     res.update(_time_launches(lambda st: plan.forward_real(a, b, out, ws, st), w.N, steps, warmup))
-    # both gradients in the real basis: three gradient products each, plus conversions
+    # both gradients in the real basis: one real-basis gradient product each, or three plus conversions
     nbw = lib.istp_real_backward_workspace_bytes(plan._h, w.N)
-    if nbw > 0:
+    if nbw >= 0:
         bq = dict(plan.backward_query())
-        bq["flops_per_pair"] = 3 * bq["flops_per_pair"]
+        bq["flops_per_pair"] = (1 if nbw == 0 else 3) * bq["flops_per_pair"]
         g = torch.randn(out.shape, generator=torch.Generator("cpu").manual_seed(w.seed + 2),
                         dtype=torch.float64).to(out.dtype).cuda()
         g1, g2 = torch.empty_like(a), torch.empty_like(b)

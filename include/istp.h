@@ -150,30 +150,36 @@ int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, cons
  * pointwise product (Section 4.3); for spin 1, whose coupling is i / sqrt 2
  * times the cross product, the real basis of i times the product, so that two
  * constant fields give their cross product over sqrt 2 (label (1, 0) holds a
- * constant field's Cartesian (y, z, x) components times Y_0^0).  The inputs
- * are converted to the real and imaginary parts of their complex
- * coefficients, three products of those parts run on the plan's kernel
- * (Karatsuba's form: P(a1, a2), P(b1, b2), P(a1 + b1, a2 + b2)), and the
- * result is read back in the real basis: three products' work.
- * workspace: caller-owned device memory of istp_real_workspace_bytes(plan, N)
- * bytes or more, 256-byte aligned, not overlapping the other buffers (its
- * contents are scratch).  Otherwise as istp_forward.
+ * constant field's Cartesian (y, z, x) components times Y_0^0).
+ * Spin 0: one launch of a kernel for real-basis rows (the Hermitian
+ * coefficients make each ring's signal real, so the lift, products and
+ * projection take real and imaginary parts where the complex product takes
+ * +m and -m); no workspace (istp_real_workspace_bytes returns 0; workspace
+ * may be NULL, workspace_bytes must be >= 0).  Spin 1 and 2: the inputs are
+ * converted to the real and imaginary parts of their complex coefficients,
+ * three products of those parts run on the plan's kernel (Karatsuba's form:
+ * P(a1, a2), P(b1, b2), P(a1 + b1, a2 + b2)), and the result is read back in
+ * the real basis; workspace: caller-owned device memory of
+ * istp_real_workspace_bytes(plan, N) bytes or more, 256-byte aligned, not
+ * overlapping the other buffers (its contents are scratch).  Otherwise as
+ * istp_forward.
  */
 int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
                       int64_t workspace_bytes, void *hip_stream);
 
-/* Workspace bytes istp_forward_real needs for N pairs; -1 for N < 0 or overflow. */
+/* Workspace bytes istp_forward_real needs for N pairs (0 for spin 0); -1 for N < 0 or overflow. */
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
 
 /*
  * istp_forward_real for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
- * allocation): the same conversions and products, with the workspace taken
+ * allocation): the same kernels, with the workspace of spin 1 and 2 taken
  * from a static device array of ISTP_STATIC_SCRATCH_BYTES (64 MiB) that the
- * library holds on each GPU it runs on until the process ends.  Same
- * arguments and rules as istp_forward_real without the workspace; the plan's
- * device must be current.  CGTP_ESCRATCH when istp_real_workspace_bytes(plan,
- * N) exceeds the array (fp32 spin 0: above 4288 pairs at L = 16, 1119 at L = 32).  The
+ * library holds on each GPU it runs on until the process ends (spin 0 needs
+ * none).  Same arguments and rules as istp_forward_real without the
+ * workspace; the plan's device must be current.  CGTP_ESCRATCH when
+ * istp_real_workspace_bytes(plan, N) exceeds the array (fp32 spin 1: above
+ * 4133 pairs at L = 8, 1118 at L = 16).  The
  * entry point calls no allocating routine; every call on a GPU shares that
  * GPU's array, so calls that overlap in time on one GPU (concurrent streams)
  * race and must be ordered by the caller.  Nothing in the array needs to
@@ -188,11 +194,13 @@ int istp_forward_real_static(istp_plan_t plan, const void *x1, const void *x2, v
  * The integrals of three real harmonics are fully symmetric, so
  *   grad_x1 = Q(grad_out, x2),  grad_x2 = Q(grad_out, x1),
  * with Q the real-basis product of a degree-2L and a degree-L row projected on
- * degrees <= L (three products on the plan's gradient grid; no time reversal).
+ * degrees <= L (on the plan's gradient grid; no time reversal): one launch of
+ * the real-basis kernel per gradient where the plan holds its real-basis
+ * gradient product (no workspace), else three products between conversions.
  * Layouts and rules as istp_backward; workspace: caller-owned, 256-byte
- * aligned, istp_real_backward_workspace_bytes(plan, N) bytes or more, reused
- * by the two gradients.  CGTP_EUNSUP for spin 1 or 2 plans and where the
- * plan has no gradient product.
+ * aligned, istp_real_backward_workspace_bytes(plan, N) bytes or more (0: may
+ * be NULL), reused by the two gradients.  CGTP_EUNSUP for spin 1 or 2 plans
+ * and where the plan has no gradient product.
  */
 int istp_backward_real(istp_plan_t plan, const void *x1, const void *x2, const void *grad_out, void *grad_x1,
                        void *grad_x2, int64_t N, void *workspace, int64_t workspace_bytes, void *hip_stream);

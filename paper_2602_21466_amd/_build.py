@@ -8,7 +8,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libcgtp.so")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in
-           ("cgtp_plan.cpp", "cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_backward.hip", "cgtp_kernels_real.hip", "istp_plan.cpp", "istp_kernels.hip",
+           ("cgtp_plan.cpp", "cgtp_kernels.hip", "cgtp_kernels_channels.hip", "cgtp_backward.hip", "cgtp_kernels_real.hip", "istp_plan.cpp", "istp_kernels.hip", "istp_kernels_real.hip",
             "istp_kernels_channels.hip", "istp_kernels_tensor.hip", "istp_kernels_channels_tensor.hip",
             "istp_real.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -39,6 +39,7 @@ __host__ __device__ constexpr int max_tiles(int S) {
 enum IstpFlags : int32_t {
     kReverseSecond = 1,   // the second input enters time-reversed: x[(j,l), m] -> (-1)^(m+j-l+S) x[(j,l), -m]
     kNegate = 2,          // outputs are negated
+    kRealBasis = 4,       // rows in the real basis (spin 0, its own kernel: launch_istp_real_*)
 };
 struct alignas(16) IstpDesc {
     int32_t L, L2, Lo, spin, C;  // input degree bounds, output bound, spin, C = 2 spin + 1 components
@@ -170,6 +171,10 @@ int launch_real_from_complex_spin_f32(float* out, const float* paa, const float*
                                       int64_t rows, int nout, int s, void* stream);
 int launch_real_from_complex_spin_f64(double* out, const double* paa, const double* pbb, const double* pss,
                                       int64_t rows, int nout, int s, void* stream);
+int launch_istp_real_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                         float* out, int64_t N, void* stream);
+int launch_istp_real_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                         double* out, int64_t N, void* stream);
 int launch_istp_tensor_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
                            float* out, int64_t N, void* stream);
 int launch_istp_tensor_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,

@@ -49,11 +49,26 @@
 #ifndef ISTP_TENSOR_KERNELS
 #define ISTP_TENSOR_KERNELS 0
 #endif
+// With ISTP_REAL_KERNELS set to 1 the Gaunt product for rows in the real
+// spherical-harmonic basis is built (istp_kernels_real.hip): istp_kernel_real.
+// Hermitian coefficients c_{l,-m} = (-1)^m conj(c_lm) make every ring's signal
+// real, so north and south still share one transform; the lift operand holds
+// Re c and Im c at +|m| (in place of the +|m| and -|m| columns), a lane and
+// its partner column form the transforms' inputs at +|m| and -|m|, the
+// products are taken on the whole circle (north = Re, south = Im), and the
+// projection forms Re and Im of each order's spectrum from the analysis at
+// +|m| and -|m|.  Pairs per work-group are at most 4, so that the partner
+// columns share a lift tile.
+#ifndef ISTP_REAL_KERNELS
+#define ISTP_REAL_KERNELS 0
+#endif
 
 namespace istp {
 namespace {
 
 using namespace ::cgtp::dev;
+
+constexpr double kRsqrt2 = 0.70710678118654752440084436210485;
 
 // Lift rows: MFMA row i carries ring ring(i) and the parity par(i) of l - am,
 // chosen so that a lane's four accumulator elements hold (even, odd) for two
@@ -122,7 +137,7 @@ struct ChanPos {
     int c0;
 };
 
-template <typename T, int S, bool CH>
+template <typename T, int S, bool CH, bool RL>
 __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                                    const T* __restrict__ x1, const T* __restrict__ x2, T* acoef,
                                                    T* stage, const IstpChan<T>& ch, ChanPos cp) {
@@ -201,7 +216,10 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         const int sg = col / per_sign, rem = col - sg * per_sign;
         const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
         const int m = sg ? -am : am;
-        const T sign = (sg && (am & 1)) ? (T)-1 : (T)1;
+        // RL: column part sg = 0 holds Re c_{l,am}, 1 holds Im c_{l,am}, with
+        // c_{l,am} = (-1)^am (r_{l,am} - i r_{l,-am}) / sqrt 2 (am > 0), c_{l,0} = r_{l,0}
+        const T sign = RL ? (am ? (T)((am & 1) ? -kRsqrt2 : kRsqrt2) * (sg ? (T)-1 : (T)1) : (T)1)
+                          : ((sg && (am & 1)) ? (T)-1 : (T)1);
         const int Lin = in ? d.L2 : d.L;
         const T* x = in ? stage + nx1 + p * nin2 : stage + p * nin;
 #pragma unroll 4
@@ -210,7 +228,7 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
             T v = (T)0;
             if (l <= Lin) {
                 if (S == 0) {
-                    v = x[l * l + l + m];
+                    v = x[l * l + l + m];   // RL: r_{l,am} (part 0) or r_{l,-am} (part 1)
                 } else if constexpr (S == 2) {
                     // labels j = |l - 2| .. l + 2; label (j, l) starts at 5 l^2 + j^2 - (l - 2)^2
                     const int q = c - 2, mj = m + q, jmin = l >= 2 ? l - 2 : 2 - l;
@@ -239,7 +257,7 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
     }
 }
 
-template <typename T, int A, int B, int S, bool LONG, bool CH>
+template <typename T, int A, int B, int S, bool LONG, bool CH, bool RL>
 __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDesc& d, int64_t p0, int np,
                                           const T* __restrict__ x1, const T* __restrict__ x2, T* __restrict__ out,
                                           const IstpChan<T>& ch, unsigned char* smem) {
@@ -277,7 +295,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         cp.n0 = p0 / ch.channels;
         cp.c0 = (int)(p0 - cp.n0 * ch.channels);
     }
-    build_coefficients<T, S, CH>(tb, d, p0, np, x1, x2, acoef, reinterpret_cast<T*>(fbuf), ch, cp);
+    build_coefficients<T, S, CH, RL>(tb, d, p0, np, x1, x2, acoef, reinterpret_cast<T*>(fbuf), ch, cp);
 
     // projection tiles of this wave: w, w + kWaves, ...  A lane's B operand is
     // column li (sign, component, pair; past the last column: column 0, whose
@@ -347,6 +365,12 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     }
                 }
                 const int col = 16 * lt.ct + li;
+                // RL: the partner column (other part, same input and pair) is lane li ^ per_sign
+                Acc pa = Acc(0);
+                if constexpr (RL) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) pa[v] = __shfl_xor(da[v], 2 * NC * P, 64);
+                }
                 if (col < lt.ncol) {
                     const int per_sign = 2 * NC * P;
                     const int sg = col / per_sign, rem = col - sg * per_sign;
@@ -356,8 +380,18 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const int r = 8 * lt.rb + lift_ring<T>(kq, h);
-                        if (r < G)
-                            dst[(size_t)r * P * ly.unit] = cmk<C2>(da[2 * h] + da[2 * h + 1], da[2 * h] - da[2 * h + 1]);
+                        if (r >= G) continue;
+                        const T e = da[2 * h], o = da[2 * h + 1];
+                        if constexpr (RL) {
+                            // north N = (E + O) over both parts, south S = (E - O); the
+                            // input at +am is N + i S, at -am conj N + i conj S
+                            const T pe = lt.am ? pa[2 * h] : (T)0, po = lt.am ? pa[2 * h + 1] : (T)0;
+                            dst[(size_t)r * P * ly.unit] =
+                                sg ? cmk<C2>(pe + po + (e - o), (pe - po) - (e + o))
+                                   : cmk<C2>(e + o - (pe - po), pe + po + (e - o));
+                        } else {
+                            dst[(size_t)r * P * ly.unit] = cmk<C2>(e + o, e - o);
+                        }
                     }
                 }
             }
@@ -402,7 +436,16 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         lds_barrier();
         // ---- 3. products on half the circle; the product of component c goes to
         // slot NC + c (positions n and -n are read and written by one task)
-        {
+        if constexpr (RL) {
+            // real signals: north = Re, south = Im of each transform, on the whole circle
+            const int ntask = Uq * Phi;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int n = task % Phi, pn = n + n / B;
+                C2* fb = ubuf(task / Phi);
+                const C2 f1 = fb[pn], f2 = fb[FS + pn];
+                fb[FS + pn] = cmk<C2>(f1.x * f2.x, f1.y * f2.y);
+            }
+        } else {
             const int ntask = Uq * H;
             for (int task = tid; task < ntask; task += kThreads) {
                 const int n = task % H;
@@ -534,9 +577,21 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
             for (int s = 0; s < MT; ++s) {
                 if (s < ntw) {
                     const int am = (tw[s] >> 20) & 127;
-                    const int k = sg_l ? (am ? Phi - am : 0) : am;
-                    const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
-                    acc[s] = mfma16(av[s], (tw[s] >> 27) ? zv.x - zv.y : zv.x + zv.y, acc[s]);
+                    T bv;
+                    if constexpr (RL) {
+                        // Re (part 0) and Im (part 1) of (analysis at +am + conj(at -am)) / 2 and of
+                        // (at +am - conj(at -am)) / 2i, north + eps south, doubled (the plan halves it)
+                        const int km = am ? Phi - am : 0;
+                        const C2 zp = *reinterpret_cast<const C2*>(smem + b_lane + (am + am / B) * (int)sizeof(C2) + hofs);
+                        const C2 zm = *reinterpret_cast<const C2*>(smem + b_lane + (km + km / B) * (int)sizeof(C2) + hofs);
+                        const T eps = (tw[s] >> 27) ? (T)-1 : (T)1;
+                        bv = sg_l ? (zp.y - zm.y) - eps * (zp.x - zm.x) : (zp.x + zm.x) + eps * (zp.y + zm.y);
+                    } else {
+                        const int k = sg_l ? (am ? Phi - am : 0) : am;
+                        const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
+                        bv = (tw[s] >> 27) ? zv.x - zv.y : zv.x + zv.y;
+                    }
+                    acc[s] = mfma16(av[s], bv, acc[s]);
                 }
             }
         }
@@ -639,7 +694,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
 // LONG: lifts of more than 4 kMaxLiftSteps degrees (only the gradient
 // product's degree-2L input, fp32, Phi >= 72); a kernel of its own, so that
 // the forward kernels keep their register allocation.
-template <typename T, int S, bool LONG, bool CH>
+template <typename T, int S, bool LONG, bool CH, bool RL = false>
 __device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc& d, const T* __restrict__ x1,
                                          const T* __restrict__ x2, T* __restrict__ out, int64_t N,
                                          const IstpChan<T>& ch) {
@@ -650,7 +705,7 @@ __device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc
     case PHI:                                                                                       \
         if constexpr ((sizeof(T) == 4 || PHI <= 54) && (!LONG || (sizeof(T) == 4 && PHI >= 72)) &&  \
                       (S != 2 || PHI <= 81))                                                        \
-            istp_body<T, A_, B_, S, LONG, CH>(tb, d, p0, np, x1, x2, out, ch, smem);                \
+            istp_body<T, A_, B_, S, LONG, CH, RL>(tb, d, p0, np, x1, x2, out, ch, smem);            \
         break;
     switch (d.Phi) {
         ISTP_CASE(1, 1, 1)
@@ -676,7 +731,35 @@ __device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc
 #undef ISTP_CASE
 }
 
-#if !ISTP_CHANNEL_KERNELS
+#if ISTP_REAL_KERNELS
+template <typename T, bool LONG>
+__global__ __launch_bounds__(kThreads, 1) void istp_kernel_real(IstpTables<T> tb, IstpDesc d,
+                                                                const T* __restrict__ x1, const T* __restrict__ x2,
+                                                                T* __restrict__ out, int64_t N) {
+    run_istp<T, 0, LONG, false, true>(tb, d, x1, x2, out, N, IstpChan<T>{nullptr, nullptr, nullptr, 1, 0, 0, 0, 0});
+}
+
+template <typename T>
+int launch_real(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T* x2, T* out, int64_t N,
+                void* stream) {
+    const int64_t grid = (N + d.pairs - 1) / d.pairs;
+    if (grid <= 0) return 0;
+    if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
+    const int Lm = d.L > d.L2 ? d.L : d.L2;
+    const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
+    if (d.spin != 0 || d.pairs > 4 || d.flags != kRealBasis) return (int)hipErrorInvalidConfiguration;
+    if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
+    void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t) =
+        long_lift ? istp_kernel_real<T, true> : istp_kernel_real<T, false>;
+    if (d.lds_bytes > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
+        if (e != hipSuccess) return (int)e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), d.lds_bytes, (hipStream_t)stream, tb, d, x1, x2,
+                       out, N);
+    return (int)hipGetLastError();
+}
+#elif !ISTP_CHANNEL_KERNELS
 template <typename T, int S, bool LONG>
 __global__ __launch_bounds__(kThreads, 1) void istp_kernel(IstpTables<T> tb, IstpDesc d, const T* __restrict__ x1,
                                                            const T* __restrict__ x2, T* __restrict__ out, int64_t N) {
@@ -749,7 +832,16 @@ int launch_channels(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, con
 // Exported launchers: spins 0 and 1 from istp_kernels.hip and
 // istp_kernels_channels.hip; spin 2 from istp_kernels_tensor.hip and
 // istp_kernels_channels_tensor.hip.
-#if !ISTP_CHANNEL_KERNELS && !ISTP_TENSOR_KERNELS
+#if ISTP_REAL_KERNELS
+int launch_istp_real_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2,
+                         float* out, int64_t N, void* stream) {
+    return launch_real<float>(tb, d, x1, x2, out, N, stream);
+}
+int launch_istp_real_f64(const IstpTables<double>& tb, const IstpDesc& d, const double* x1, const double* x2,
+                         double* out, int64_t N, void* stream) {
+    return launch_real<double>(tb, d, x1, x2, out, N, stream);
+}
+#elif !ISTP_CHANNEL_KERNELS && !ISTP_TENSOR_KERNELS
 int launch_istp_f32(const IstpTables<float>& tb, const IstpDesc& d, const float* x1, const float* x2, float* out,
                     int64_t N, void* stream) {
     return launch<float>(tb, d, x1, x2, out, N, stream);

@@ -35,6 +35,7 @@ struct istp_prod {
 struct istp_plan_s {
     int L = 0, spin = 0, dtype = 0, device = 0;
     istp_prod fwd, bwd;
+    istp_prod rfwd, rbwd;   // spin 0: the same two products for rows in the real basis (when they fit)
 };
 
 namespace {
@@ -181,6 +182,8 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     int bestP = 0, bestG = 0, bestBytes = 0;
     for (int P : {8, 4, 2, 1}) {
         if (2 * NC * P > 16) continue;
+        // real basis: the lift's columns (part, input, pair) on one MFMA tile
+        if ((flags & istp::kRealBasis) && 4 * NC * P > 16) continue;
         // inputs and couplings are staged with one batch of loads per thread
         const int stage = P * (nin + nin2) + (S ? NC * NC * (Lm + 1) * (Lm + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
@@ -324,6 +327,21 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
                         h.coefi[8 * o + q + 2] = (q + 2) * no + l3 * l3 + l3 + ml;
                     }
                 }
+            }
+    } else if (S == ISTP_GAUNT && (flags & istp::kRealBasis)) {
+        // real basis: the kernel's spectrum slots (l3, +mu) and (l3, -mu) hold Re and
+        // Im of 2 Phi / (2 pi) times the complex coefficient h at +mu (exact
+        // unpacking: no doubled factors; the projection's operand is doubled); the
+        // real-basis output reads r_0 = h_0, r_mu = sqrt 2 (-1)^mu Re h_mu,
+        // r_-mu = -sqrt 2 (-1)^mu Im h_mu
+        const double sr = 2.0 * kPi / (2.0 * Phi), rt2 = std::sqrt(2.0);
+        for (int l3 = 0; l3 <= Lo; ++l3)
+            for (int m3 = -l3; m3 <= l3; ++m3) {
+                const int o = l3 * l3 + l3 + m3, mu = std::abs(m3);
+                const double par = (mu & 1) ? -1.0 : 1.0;
+                h.coef[4 * o] = (T)(m3 == 0 ? sr : (m3 > 0 ? sr * rt2 * par : -sr * rt2 * par));
+                h.coefi[4 * o] = h.coefi[4 * o + 1] = h.coefi[4 * o + 2] = o;
+                h.coefi[4 * o + 3] = 1;
             }
     } else if (S == ISTP_GAUNT) {
         for (int l3 = 0; l3 <= Lo; ++l3)
@@ -489,6 +507,18 @@ void free_prod(istp_prod* pr, int* rc) {
 int launch_prod(const istp_plan_s* plan, const istp_prod& pr, int flags, const void* a, const void* b, void* out,
                 int64_t N, void* stream) {
     istp::IstpDesc d = pr.desc;
+    if (d.flags & istp::kRealBasis) {   // the real-basis products run their own kernel
+        const int er = plan->dtype == CGTP_FP32
+                           ? istp::launch_istp_real_f32(pr.tf, d, (const float*)a, (const float*)b, (float*)out, N,
+                                                        stream)
+                           : istp::launch_istp_real_f64(pr.td, d, (const double*)a, (const double*)b, (double*)out,
+                                                        N, stream);
+        if (er != 0) {
+            cgtp::set_last_hip_error(er);
+            return CGTP_EHIP;
+        }
+        return CGTP_OK;
+    }
     d.flags = flags;
     const bool t2 = d.spin == ISTP_TENSOR;
     const int err =
@@ -561,10 +591,25 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
                            : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true);
         if (rb != CGTP_OK && rb != CGTP_EUNSUP) rc = rb;
     }
+    if (rc == CGTP_OK && spin == ISTP_GAUNT) {
+        // the real-basis products (forward and gradients); outside the kernel's
+        // limits they stay unbuilt and the real-basis calls take three products
+        const int f = istp::kRealBasis;
+        int rr = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, f, &p->rfwd, true)
+                                    : make_prod<double>(L, L, 2 * L, spin, f, &p->rfwd, true);
+        if (rr != CGTP_OK && rr != CGTP_EUNSUP) rc = rr;
+        if (rc == CGTP_OK && p->bwd.ok) {
+            rr = dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, f, &p->rbwd, true)
+                                    : make_prod<double>(2 * L, L, L, spin, f, &p->rbwd, true);
+            if (rr != CGTP_OK && rr != CGTP_EUNSUP) rc = rr;
+        }
+    }
     if (rc != CGTP_OK) {
         int ignored = CGTP_OK;
         free_prod(&p->fwd, &ignored);
         free_prod(&p->bwd, &ignored);
+        free_prod(&p->rfwd, &ignored);
+        free_prod(&p->rbwd, &ignored);
         delete p;
         return rc;
     }
@@ -595,6 +640,8 @@ int istp_destroy(istp_plan_t plan) {
     int rc = CGTP_OK;
     free_prod(&plan->fwd, &rc);
     free_prod(&plan->bwd, &rc);
+    free_prod(&plan->rfwd, &rc);
+    free_prod(&plan->rbwd, &rc);
     delete plan;
     return rc;
 }
@@ -693,8 +740,10 @@ int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(nout * esz))) return -1;
-    // spin 0 forms the first product in out and reads it back in place; spin 1
-    // and 2 keep all three products in the workspace
+    // spin 0 runs the real-basis kernel (no workspace) where it is built, else
+    // forms the first product in out and reads it back in place; spin 1 and 2
+    // keep all three products in the workspace
+    if (plan->spin == ISTP_GAUNT && plan->rfwd.ok) return 0;
     const size_t nprod = plan->spin == ISTP_GAUNT ? 2 : 3;
     return (int64_t)(6 * real_part_bytes((size_t)N * nin * esz) + nprod * real_part_bytes((size_t)N * nout * esz));
 }
@@ -703,6 +752,19 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
                       int64_t workspace_bytes, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;
     if (N == 0) return CGTP_OK;
+    if (plan->spin == ISTP_GAUNT && plan->rfwd.ok) {
+        // one launch of the real-basis kernel; the workspace is not used
+        if (!x1 || !x2 || !out || workspace_bytes < 0) return CGTP_EINVAL;
+        if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;
+        const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
+        const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;
+        if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(nout * esz))) return CGTP_EINVAL;
+        const size_t bin = (size_t)N * nin * esz, bout = (size_t)N * nout * esz;
+        if (overlaps(out, bout, x1, bin) || overlaps(out, bout, x2, bin)) return CGTP_EINVAL;
+        const int rc0 = current_device_is(plan->device);
+        if (rc0 != CGTP_OK) return rc0;
+        return launch_prod(plan, plan->rfwd, 0, x1, x2, out, N, hip_stream);
+    }
     if (!x1 || !x2 || !out || !workspace) return CGTP_EINVAL;
     if ((((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) || ((uintptr_t)workspace & 255)) return CGTP_EINVAL;
     const int64_t need = istp_real_workspace_bytes(plan, N);
@@ -805,6 +867,7 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
 // (2L+1)^2), the converted input (three rows of (L+1)^2), two products.
 int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N) {
     if (!plan || N < 0 || plan->spin != ISTP_GAUNT || !plan->bwd.ok) return -1;
+    if (plan->rbwd.ok) return 0;   // the real-basis kernel: no workspace
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t ng = (size_t)plan->fwd.desc.nout, nin = (size_t)plan->fwd.desc.nin;
     if ((uint64_t)N > (uint64_t)(INT64_MAX / 16 / (int64_t)(ng * esz))) return -1;
@@ -813,6 +876,7 @@ int64_t istp_real_backward_workspace_bytes(istp_plan_t plan, int64_t N) {
 
 static int real_bwd_one(istp_plan_t plan, const void* g, const void* x, void* grad, int64_t N, char* w,
                         void* stream) {
+    if (plan->rbwd.ok) return launch_prod(plan, plan->rbwd, 0, g, x, grad, N, stream);
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t ng = (size_t)plan->fwd.desc.nout, nin = (size_t)plan->fwd.desc.nin;
     const size_t pg = real_part_bytes((size_t)N * ng * esz), px = real_part_bytes((size_t)N * nin * esz);
@@ -860,11 +924,11 @@ int istp_backward_real(istp_plan_t plan, const void* x1, const void* x2, const v
     if (!plan || N < 0) return CGTP_EINVAL;
     if (plan->spin != ISTP_GAUNT || !plan->bwd.ok) return CGTP_EUNSUP;
     if (N == 0) return CGTP_OK;
-    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2) || !workspace) return CGTP_EINVAL;
+    const int64_t need = istp_real_backward_workspace_bytes(plan, N);
+    if (!x1 || !x2 || !grad_out || (!grad_x1 && !grad_x2) || (need > 0 && !workspace)) return CGTP_EINVAL;
     if ((((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)grad_out | (uintptr_t)grad_x1 | (uintptr_t)grad_x2) & 15) ||
         ((uintptr_t)workspace & 255))
         return CGTP_EINVAL;
-    const int64_t need = istp_real_backward_workspace_bytes(plan, N);
     if (need < 0 || workspace_bytes < need) return CGTP_EINVAL;
     const size_t esz = plan->dtype == CGTP_FP32 ? 4 : 8;
     const size_t nin = (size_t)plan->fwd.desc.nin, nout = (size_t)plan->fwd.desc.nout;

@@ -58,6 +58,10 @@ int launch_real_from_complex_spin_f32(float*, const float*, const float*, const 
 }
 int launch_real_from_complex_spin_f64(double*, const double*, const double*, const double*, int64_t, int, int,
                                       void*) { return 1; }
+int launch_istp_real_f32(const IstpTables<float>&, const IstpDesc&, const float*, const float*, float*, int64_t,
+                         void*) { return 1; }
+int launch_istp_real_f64(const IstpTables<double>&, const IstpDesc&, const double*, const double*, double*, int64_t,
+                         void*) { return 1; }
 int launch_istp_tensor_f32(const IstpTables<float>&, const IstpDesc&, const float*, const float*, float*, int64_t,
                            void*) { return 1; }
 int launch_istp_tensor_f64(const IstpTables<double>&, const IstpDesc&, const double*, const double*, double*,

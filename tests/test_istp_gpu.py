@@ -322,7 +322,7 @@ def test_real_basis_gradients_largest_degree():
     L = None
     for cand in range(33, 0, -1):
         plan = lib.IstpPlan(cand, 0, "fp32")
-        if lib.istp_real_backward_workspace_bytes(plan._h, 2) > 0:
+        if lib.istp_real_backward_workspace_bytes(plan._h, 2) >= 0:   # -1: no gradient product
             L = cand
             break
         plan.close()
@@ -352,18 +352,24 @@ def test_real_basis_errors():
     lib = _lib()
     plan = lib.IstpPlan(3, 0, "fp32")
     N = 4
-    need = lib.istp_real_workspace_bytes(plan._h, N)
-    assert need > 0 and lib.istp_real_workspace_bytes(plan._h, -1) == -1
+    # spin 0 runs the real-basis kernel: no workspace (gradients likewise)
+    assert lib.istp_real_workspace_bytes(plan._h, N) == 0 and lib.istp_real_workspace_bytes(plan._h, -1) == -1
+    assert lib.istp_real_backward_workspace_bytes(plan._h, N) == 0
     x = torch.zeros((N, plan.nin), device="cuda")
-    out = torch.zeros((N, plan.nout), device="cuda")
-    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
-    lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), 0, ws.data_ptr(), need, None)
-    with pytest.raises(lib.CgtpError) as e:   # workspace too small
-        lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, ws.data_ptr(), need - 1, None)
-    assert e.value.code == lib.CGTP_EINVAL
-    with pytest.raises(lib.CgtpError) as e:   # workspace overlapping the output
-        lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), ws.data_ptr(), N, ws.data_ptr(), need, None)
-    assert e.value.code == lib.CGTP_EINVAL
+    out = torch.full((N, plan.nout), 3.0, device="cuda")
+    lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), 0, None, 0, None)
+    big = torch.zeros(N * plan.nout + 64, device="cuda")
+    for args in [(x.data_ptr(), x.data_ptr(), out.data_ptr() + 4, N, None, 0),       # misaligned output
+                 (x.data_ptr(), x.data_ptr(), out.data_ptr(), N, None, -1),          # negative workspace size
+                 (big.data_ptr(), x.data_ptr(), big.data_ptr() + 64, N, None, 0)]:   # output overlapping an input
+        with pytest.raises(lib.CgtpError) as e:
+            lib.istp_forward_real(plan._h, *args, None)
+        assert e.value.code == lib.CGTP_EINVAL, args
+    torch.cuda.synchronize()
+    assert (out == 3.0).all().item()
+    lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, None, 0, None)
+    torch.cuda.synchronize()
+    assert (out == 0.0).all().item()
     vplan = lib.IstpPlan(3, 1, "fp32")
     vneed = lib.istp_real_workspace_bytes(vplan._h, N)
     assert vneed > 0

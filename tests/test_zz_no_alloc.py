@@ -1,7 +1,8 @@
 """The no-allocation entry point istp_forward_real_static against istp_forward_real
 (same kernels, caller-allocated workspace), through the C ABI, on two calls in a
 row (the second with fewer pairs, reusing the static scratch the first one left
-behind), and its size limit."""
+behind), and its size limit.  Spins 1 and 2 use the scratch (three products);
+spin 0 runs the real-basis kernel, which needs none."""
 import ctypes
 
 import numpy as np
@@ -53,20 +54,46 @@ def test_static_scratch_matches_workspace_entry_point(L, N1, N2, dtype):
 
 
 def test_static_scratch_size_limit():
+    """Spin 1 (three products through the scratch): the largest N whose workspace fits the static array runs,
+    one more is refused with CGTP_ESCRATCH and nothing is written.  Spin 0 runs the real-basis kernel, which
+    needs no workspace: the static entry point takes any N."""
     torch, lib = _setup()
-    L = 16
-    plan = lib.IstpPlan(L, lib.ISTP_GAUNT, "fp32")
-    limit = max(n for n in (4288, 4289) if lib.istp_real_workspace_bytes(plan._h, n) <= (64 << 20))
-    assert limit == 4288
-    n = limit + 1
-    x = torch.zeros(n, plan.nin, device="cuda")
-    out = torch.full((n, plan.nout), 5.0, device="cuda")
-    rc = lib._load().istp_forward_real_static(plan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
-                                             ctypes.c_void_p(out.data_ptr()), n, None)
+    L = 8
+    plan = lib.IstpPlan(L, lib.ISTP_VECTOR, "fp32")
+    cap = 64 << 20
+    lo, hi = 1, 1 << 20
+    while lo < hi:   # the largest n with workspace <= cap
+        mid = (lo + hi + 1) // 2
+        if lib.istp_real_workspace_bytes(plan._h, mid) <= cap:
+            lo = mid
+        else:
+            hi = mid - 1
+    limit = lo
+    assert lib.istp_real_workspace_bytes(plan._h, limit + 1) > cap
+    f = lib._load()
+    x = torch.zeros(limit + 1, plan.nin, device="cuda")
+    out = torch.full((limit + 1, plan.nout), 5.0, device="cuda")
+    rc = f.istp_forward_real_static(plan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                                    ctypes.c_void_p(out.data_ptr()), limit + 1, None)
     assert rc == lib.CGTP_ESCRATCH
     assert lib.cgtp_strerror(rc)
     torch.cuda.synchronize()
     assert (out == 5.0).all().item()
+    rc = f.istp_forward_real_static(plan._h, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+                                    ctypes.c_void_p(out.data_ptr()), limit, None)
+    assert rc == lib.CGTP_OK
+    torch.cuda.synchronize()
+    assert (out[:limit] == 0.0).all().item() and (out[limit] == 5.0).all().item()
+    # spin 0: no workspace, so no limit
+    p0 = lib.IstpPlan(16, lib.ISTP_GAUNT, "fp32")
+    assert lib.istp_real_workspace_bytes(p0._h, 100000) == 0
+    n = 6000
+    x0 = torch.zeros(n, p0.nin, device="cuda")
+    o0 = torch.full((n, p0.nout), 5.0, device="cuda")
+    assert f.istp_forward_real_static(p0._h, ctypes.c_void_p(x0.data_ptr()), ctypes.c_void_p(x0.data_ptr()),
+                                      ctypes.c_void_p(o0.data_ptr()), n, None) == lib.CGTP_OK
+    torch.cuda.synchronize()
+    assert (o0 == 0.0).all().item()
 
 
 @pytest.mark.parametrize("spin,L,N1,N2", [(1, 6, 400, 41), (2, 3, 120, 7)])
