@@ -57,8 +57,8 @@
 // its partner column form the transforms' inputs at +|m| and -|m|, the
 // products are taken on the whole circle (north = Re, south = Im), and the
 // projection forms Re and Im of each order's spectrum from the analysis at
-// +|m| and -|m|.  Pairs per work-group are at most 4, so that the partner
-// columns share a lift tile.
+// +|m| and -|m|.  For |m| > 0 the part is the lowest bit of a lift column, so
+// that a column's partner is the neighbouring lane of the same tile.
 #ifndef ISTP_REAL_KERNELS
 #define ISTP_REAL_KERNELS 0
 #endif
@@ -213,7 +213,9 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
             for (int k = k0; k < k1; ++k) dst[k * cs] = (T)0;
             continue;
         }
-        const int sg = col / per_sign, rem = col - sg * per_sign;
+        // RL, am > 0: the part is the lowest bit of the column (partners are neighbours)
+        const int sg = (RL && am) ? (col & 1) : col / per_sign;
+        const int rem = (RL && am) ? (col >> 1) : col - sg * per_sign;
         const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
         const int m = sg ? -am : am;
         // RL: column part sg = 0 holds Re c_{l,am}, 1 holds Im c_{l,am}, with
@@ -365,15 +367,16 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     }
                 }
                 const int col = 16 * lt.ct + li;
-                // RL: the partner column (other part, same input and pair) is lane li ^ per_sign
+                // RL: the partner column (other part, same input and pair) is lane li ^ 1
                 Acc pa = Acc(0);
                 if constexpr (RL) {
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) pa[v] = __shfl_xor(da[v], 2 * NC * P, 64);
+                    for (int v = 0; v < 4; ++v) pa[v] = __shfl_xor(da[v], 1, 64);
                 }
                 if (col < lt.ncol) {
                     const int per_sign = 2 * NC * P;
-                    const int sg = col / per_sign, rem = col - sg * per_sign;
+                    const int sg = (RL && lt.am) ? (col & 1) : col / per_sign;
+                    const int rem = (RL && lt.am) ? (col >> 1) : col - sg * per_sign;
                     const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
                     const int n = sg ? Phi - lt.am : lt.am;
                     C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
@@ -747,7 +750,7 @@ int launch_real(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     const int Lm = d.L > d.L2 ? d.L : d.L2;
     const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
-    if (d.spin != 0 || d.pairs > 4 || d.flags != kRealBasis) return (int)hipErrorInvalidConfiguration;
+    if (d.spin != 0 || d.flags != kRealBasis) return (int)hipErrorInvalidConfiguration;
     if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
     void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t) =
         long_lift ? istp_kernel_real<T, true> : istp_kernel_real<T, false>;

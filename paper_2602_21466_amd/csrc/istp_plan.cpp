@@ -182,8 +182,6 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     int bestP = 0, bestG = 0, bestBytes = 0;
     for (int P : {8, 4, 2, 1}) {
         if (2 * NC * P > 16) continue;
-        // real basis: the lift's columns (part, input, pair) on one MFMA tile
-        if ((flags & istp::kRealBasis) && 4 * NC * P > 16) continue;
         // inputs and couplings are staged with one batch of loads per thread
         const int stage = P * (nin + nin2) + (S ? NC * NC * (Lm + 1) * (Lm + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
