@@ -39,7 +39,7 @@ __host__ __device__ constexpr int max_tiles(int S) {
 enum IstpFlags : int32_t {
     kReverseSecond = 1,   // the second input enters time-reversed: x[(j,l), m] -> (-1)^(m+j-l+S) x[(j,l), -m]
     kNegate = 2,          // outputs are negated
-    kRealBasis = 4,       // rows in the real basis (spin 0, its own kernel: launch_istp_real_*)
+    kRealBasis = 4,       // rows in the real basis (spin 0 and 1, their own kernel: launch_istp_real_*)
 };
 struct alignas(16) IstpDesc {
     int32_t L, L2, Lo, spin, C;  // input degree bounds, output bound, spin, C = 2 spin + 1 components

@@ -204,7 +204,8 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
         const int ci = it % d.n_bcol, k0 = 8 * (it / d.n_bcol);
         const int2 bc = tb.bcol[ci];
         const int am = bc.x & 255, col = bc.x >> 8;
-        const int ncol = (am ? 2 : 1) * per_sign, cs = istp_cstride(ncol);
+        const bool two = RL ? (am || S == 1) : am;   // columns of both signs / parts at this order
+        const int ncol = (two ? 2 : 1) * per_sign, cs = istp_cstride(ncol);
         const int kp = (Lm - am + 4) / 4 * 4;
         if (k0 >= kp) continue;
         const int k1 = min(k0 + 8, kp);
@@ -214,13 +215,13 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
             continue;
         }
         // RL, am > 0: the part is the lowest bit of the column (partners are neighbours)
-        const int sg = (RL && am) ? (col & 1) : col / per_sign;
-        const int rem = (RL && am) ? (col >> 1) : col - sg * per_sign;
+        const int sg = (RL && two) ? (col & 1) : col / per_sign;
+        const int rem = (RL && two) ? (col >> 1) : col - sg * per_sign;
         const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
         const int m = sg ? -am : am;
         // RL: column part sg = 0 holds Re c_{l,am}, 1 holds Im c_{l,am}, with
         // c_{l,am} = (-1)^am (r_{l,am} - i r_{l,-am}) / sqrt 2 (am > 0), c_{l,0} = r_{l,0}
-        const T sign = RL ? (am ? (T)((am & 1) ? -kRsqrt2 : kRsqrt2) * (sg ? (T)-1 : (T)1) : (T)1)
+        const T sign = RL ? (S == 1 ? (T)1 : (am ? (T)((am & 1) ? -kRsqrt2 : kRsqrt2) * (sg ? (T)-1 : (T)1) : (T)1))
                           : ((sg && (am & 1)) ? (T)-1 : (T)1);
         const int Lin = in ? d.L2 : d.L;
         const T* x = in ? stage + nx1 + p * nin2 : stage + p * nin;
@@ -241,6 +242,36 @@ __device__ __forceinline__ void build_coefficients(const IstpTables<T>& tb, cons
                         if (j < jmin || mj < -j || mj > j) continue;
                         const int lo = 5 * l * l + j * j - (l - 2) * (l - 2);
                         v += cg[(jj * 5 + c) * (2 * l + 1)] * x[lo + j + mj];
+                    }
+                } else if (RL) {
+                    // spin 1, real-basis rows: Re (sg = 0) or Im (sg = 1) of a_q[l][am] =
+                    // sum_j C^{j,am+q}_{l,am,1,q} c^(j,l)_{am+q}; the label's complex
+                    // coefficient from its real-basis row, times -i where
+                    // sigma = (-1)^(l+1-j) = -1
+                    const int q = c - 1, mj = am + q;
+                    const T* cg = cgs + 9 * l * l + am + l;
+#pragma unroll
+                    for (int jj = 0; jj < 3; ++jj) {
+                        const int j = l - 1 + jj;
+                        if (j < 0 || j + l < 1 || mj < -j || mj > j) continue;
+                        const int lo = 3 * l * l + (jj == 0 ? 0 : (jj == 1 ? 2 * l - 1 : 4 * l));
+                        const T* r0 = x + lo + j;
+                        const int mu = mj < 0 ? -mj : mj;
+                        T wr, wi;
+                        if (mj == 0) {
+                            wr = r0[0];
+                            wi = (T)0;
+                        } else if (mj > 0) {
+                            const T h = (mu & 1) ? (T)-kRsqrt2 : (T)kRsqrt2;
+                            wr = h * r0[mu];
+                            wi = -h * r0[-mu];
+                        } else {
+                            wr = (T)kRsqrt2 * r0[mu];
+                            wi = (T)kRsqrt2 * r0[-mu];
+                        }
+                        const bool flip = jj == 1;   // sigma = (-1)^(l+1-j) = -1 for j = l: c = -i w
+                        const T cpart = sg ? (flip ? -wr : wi) : (flip ? wi : wr);
+                        v += cg[(jj * 3 + c) * (2 * l + 1)] * cpart;
                     }
                 } else {
                     const int q = c - 1, mj = m + q;
@@ -375,23 +406,44 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                 }
                 if (col < lt.ncol) {
                     const int per_sign = 2 * NC * P;
-                    const int sg = (RL && lt.am) ? (col & 1) : col / per_sign;
-                    const int rem = (RL && lt.am) ? (col >> 1) : col - sg * per_sign;
+                    const bool two = RL && (lt.am || S == 1);   // both parts at this order
+                    const int sg = two ? (col & 1) : col / per_sign;
+                    const int rem = two ? (col >> 1) : col - sg * per_sign;
                     const int in = rem / (NC * P), c = (rem / P) % NC, p = rem % P;
-                    const int n = sg ? Phi - lt.am : lt.am;
-                    C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + c) * FS + (n % A) * BP + n / A;
+                    // RL spin 1: f_0 (c = 1) is real per ring and is stored like spin 0;
+                    // f_+1 is complex: its north and south take slots 0 and 2 of the
+                    // input (c = 2 gives them at +am, c = 0 at -am as f_+1[-m] =
+                    // -conj f_-1[m]); at am = 0 only c = 2 and f_0's part Re store
+                    int slot = c, n = sg ? Phi - lt.am : lt.am;
+                    bool skip = false;
+                    if constexpr (RL && S == 1) {
+                        if (c == 1) skip = sg && lt.am == 0;
+                        else {
+                            slot = sg ? 2 : 0;
+                            n = c == 2 ? lt.am : Phi - lt.am;
+                            skip = c == 0 && lt.am == 0;
+                        }
+                    }
+                    C2* dst = fbuf + (size_t)p * ly.unit + (in * NC + slot) * FS + (n % A) * BP + n / A;
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const int r = 8 * lt.rb + lift_ring<T>(kq, h);
-                        if (r >= G) continue;
+                        if (r >= G || skip) continue;
                         const T e = da[2 * h], o = da[2 * h + 1];
                         if constexpr (RL) {
-                            // north N = (E + O) over both parts, south S = (E - O); the
-                            // input at +am is N + i S, at -am conj N + i conj S
-                            const T pe = lt.am ? pa[2 * h] : (T)0, po = lt.am ? pa[2 * h + 1] : (T)0;
-                            dst[(size_t)r * P * ly.unit] =
-                                sg ? cmk<C2>(pe + po + (e - o), (pe - po) - (e + o))
-                                   : cmk<C2>(e + o - (pe - po), pe + po + (e - o));
+                            const T pe = two ? pa[2 * h] : (T)0, po = two ? pa[2 * h + 1] : (T)0;
+                            if (S == 1 && c != 1) {
+                                // part Re: N = (e + o) + i (pe + po); part Im: S = (pe - po) + i (e - o);
+                                // c = 0 stores -conj of them
+                                const C2 v = sg ? cmk<C2>(pe - po, e - o) : cmk<C2>(e + o, pe + po);
+                                dst[(size_t)r * P * ly.unit] = c == 2 ? v : cmk<C2>(-v.x, v.y);
+                            } else {
+                                // north N = (E + O) over both parts, south S = (E - O); the
+                                // input at +am is N + i S, at -am conj N + i conj S
+                                dst[(size_t)r * P * ly.unit] =
+                                    sg ? cmk<C2>(pe + po + (e - o), (pe - po) - (e + o))
+                                       : cmk<C2>(e + o - (pe - po), pe + po + (e - o));
+                            }
                         } else {
                             dst[(size_t)r * P * ly.unit] = cmk<C2>(e + o, e - o);
                         }
@@ -439,7 +491,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         lds_barrier();
         // ---- 3. products on half the circle; the product of component c goes to
         // slot NC + c (positions n and -n are read and written by one task)
-        if constexpr (RL) {
+        if constexpr (RL && S == 0) {
             // real signals: north = Re, south = Im of each transform, on the whole circle
             const int ntask = Uq * Phi;
             for (int task = tid; task < ntask; task += kThreads) {
@@ -447,6 +499,21 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                 C2* fb = ubuf(task / Phi);
                 const C2 f1 = fb[pn], f2 = fb[FS + pn];
                 fb[FS + pn] = cmk<C2>(f1.x * f2.x, f1.y * f2.y);
+            }
+        } else if constexpr (RL) {
+            // spin 1, real fields: per hemisphere f_+1 (slot 0 north, slot 2 south), f_0 =
+            // Re / Im of slot 1, f_-1 = -conj f_+1; the coupling gives g_+1 = b0 a+ - a0 b+
+            // and g_0 = a+ b- - a- b+ = -2 i Im(a+ conj b+) (g_-1 = conj g_+1): slot 3 and 5
+            // take g_+1's north and south, slot 4 Im g_0 (north + i south)
+            const int ntask = Uq * Phi;
+            for (int task = tid; task < ntask; task += kThreads) {
+                const int n = task % Phi, pn = n + n / B;
+                C2* fb = ubuf(task / Phi);
+                const C2 an = fb[pn], a0 = fb[FS + pn], as = fb[2 * FS + pn];
+                const C2 bn = fb[3 * FS + pn], b0 = fb[4 * FS + pn], bs = fb[5 * FS + pn];
+                fb[3 * FS + pn] = cmk<C2>(b0.x * an.x - a0.x * bn.x, b0.x * an.y - a0.x * bn.y);
+                fb[5 * FS + pn] = cmk<C2>(b0.y * as.x - a0.y * bs.x, b0.y * as.y - a0.y * bs.y);
+                fb[4 * FS + pn] = cmk<C2>((T)-2 * (an.y * bn.x - an.x * bn.y), (T)-2 * (as.y * bs.x - as.x * bs.y));
             }
         } else {
             const int ntask = Uq * H;
@@ -582,13 +649,24 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
                     const int am = (tw[s] >> 20) & 127;
                     T bv;
                     if constexpr (RL) {
-                        // Re (part 0) and Im (part 1) of (analysis at +am + conj(at -am)) / 2 and of
-                        // (at +am - conj(at -am)) / 2i, north + eps south, doubled (the plan halves it)
                         const int km = am ? Phi - am : 0;
-                        const C2 zp = *reinterpret_cast<const C2*>(smem + b_lane + (am + am / B) * (int)sizeof(C2) + hofs);
-                        const C2 zm = *reinterpret_cast<const C2*>(smem + b_lane + (km + km / B) * (int)sizeof(C2) + hofs);
                         const T eps = (tw[s] >> 27) ? (T)-1 : (T)1;
-                        bv = sg_l ? (zp.y - zm.y) - eps * (zp.x - zm.x) : (zp.x + zm.x) + eps * (zp.y + zm.y);
+                        if (S == 0 || c_l == 1) {
+                            // Re (part 0) and Im (part 1) of (analysis at +am + conj(at -am)) / 2 and of
+                            // (at +am - conj(at -am)) / 2i, north + eps south, doubled (the plan halves it)
+                            const C2 zp = *reinterpret_cast<const C2*>(smem + b_lane + (am + am / B) * (int)sizeof(C2) + hofs);
+                            const C2 zm = *reinterpret_cast<const C2*>(smem + b_lane + (km + km / B) * (int)sizeof(C2) + hofs);
+                            bv = sg_l ? (zp.y - zm.y) - eps * (zp.x - zm.x) : (zp.x + zm.x) + eps * (zp.y + zm.y);
+                        } else {
+                            // spin 1, g_+1 (c = 2) at +am, g_-1 = conj g_+1(-m) (c = 0): north in
+                            // slot 0, south in slot 2 of the unit (b_lane points at slot c_l)
+                            const int k = c_l == 2 ? am : km;
+                            const int u0 = b_lane - c_l * FS * (int)sizeof(C2) + (k + k / B) * (int)sizeof(C2) + hofs;
+                            const C2 zn = *reinterpret_cast<const C2*>(smem + u0);
+                            const C2 zs = *reinterpret_cast<const C2*>(smem + u0 + 2 * FS * (int)sizeof(C2));
+                            const T re = zn.x + eps * zs.x, im = zn.y + eps * zs.y;
+                            bv = sg_l ? (c_l == 2 ? im : -im) : re;
+                        }
                     } else {
                         const int k = sg_l ? (am ? Phi - am : 0) : am;
                         const C2 zv = *reinterpret_cast<const C2*>(smem + b_lane + (k + k / B) * (int)sizeof(C2) + hofs);
@@ -601,21 +679,25 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
         lds_barrier();
     }
 
-    // ---- spectra of every pair to LDS: [pair][component][l3^2 + l3 + m]
+    // ---- spectra of every pair to LDS: [pair][component][l3^2 + l3 + m]; the
+    // real-basis spin-1 kernel keeps its order-0 imaginary parts after them
+    // ([(Lo + 1)^2 + l3])
     const int no = (Lo + 1) * (Lo + 1);
+    const int nos = (RL && S == 1) ? no + Lo + 1 : no;   // per-component stride
 #pragma unroll
     for (int s = 0; s < MT; ++s) {
         if (s < ntw) {
             const ProjTile pt = tb.proj[wave + kWaves * s];
-            const int ncp = (pt.am ? 2 : 1) * NC * P;
+            const int ncp = ((pt.am || (RL && S == 1)) ? 2 : 1) * NC * P;
             if (li < ncp) {
                 const int sg = li / (NC * P), c = (li / P) % NC, p = li % P;
+                const bool im0 = RL && S == 1 && sg && pt.am == 0;
                 const int m = sg ? -pt.am : pt.am;
-                T* hp = hc + (size_t)(p * NC + c) * no + m;
+                T* hp = hc + (size_t)(p * NC + c) * nos + (im0 ? no : m);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int l3 = pt.am + pt.par + 2 * (acc_row<T>(kq, v) + 16 * pt.rt);
-                    if (l3 <= Lo) hp[l3 * l3 + l3] = acc[s][v];
+                    if (l3 <= Lo) hp[im0 ? l3 : l3 * l3 + l3] = acc[s][v];
                 }
             }
         }
@@ -650,7 +732,7 @@ __device__ __forceinline__ void istp_body(const IstpTables<T>& tb, const IstpDes
     } else {
         const Acc* cf4 = reinterpret_cast<const Acc*>(tb.coef);
         const int4* ci4 = reinterpret_cast<const int4*>(tb.coefi);
-        const int nout = d.nout, hs = NC * no;
+        const int nout = d.nout, hs = NC * nos;
         for (int o0 = tid; o0 < nout; o0 += 4 * kThreads) {
             Acc cf[4];
             int4 ix[4];
@@ -735,11 +817,11 @@ __device__ __forceinline__ void run_istp(const IstpTables<T>& tb, const IstpDesc
 }
 
 #if ISTP_REAL_KERNELS
-template <typename T, bool LONG>
+template <typename T, int S, bool LONG>
 __global__ __launch_bounds__(kThreads, 1) void istp_kernel_real(IstpTables<T> tb, IstpDesc d,
                                                                 const T* __restrict__ x1, const T* __restrict__ x2,
                                                                 T* __restrict__ out, int64_t N) {
-    run_istp<T, 0, LONG, false, true>(tb, d, x1, x2, out, N, IstpChan<T>{nullptr, nullptr, nullptr, 1, 0, 0, 0, 0});
+    run_istp<T, S, LONG, false, true>(tb, d, x1, x2, out, N, IstpChan<T>{nullptr, nullptr, nullptr, 1, 0, 0, 0, 0});
 }
 
 template <typename T>
@@ -750,10 +832,11 @@ int launch_real(const IstpTables<T>& tb, const IstpDesc& d, const T* x1, const T
     if (grid > 0x7fffffffLL) return (int)hipErrorInvalidConfiguration;
     const int Lm = d.L > d.L2 ? d.L : d.L2;
     const bool long_lift = Lm + 1 > 4 * kMaxLiftSteps;
-    if (d.spin != 0 || d.flags != kRealBasis) return (int)hipErrorInvalidConfiguration;
-    if (long_lift && (sizeof(T) != 4 || d.Phi < 72)) return (int)hipErrorInvalidConfiguration;
+    if ((d.spin != 0 && d.spin != 1) || d.flags != kRealBasis) return (int)hipErrorInvalidConfiguration;
+    if (long_lift && (sizeof(T) != 4 || d.Phi < 72 || d.spin != 0)) return (int)hipErrorInvalidConfiguration;
     void (*kern)(IstpTables<T>, IstpDesc, const T*, const T*, T*, int64_t) =
-        long_lift ? istp_kernel_real<T, true> : istp_kernel_real<T, false>;
+        d.spin ? istp_kernel_real<T, 1, false>
+               : (long_lift ? istp_kernel_real<T, 0, true> : istp_kernel_real<T, 0, false>);
     if (d.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, d.lds_bytes);
         if (e != hipSuccess) return (int)e;

@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <map>
 #include <new>
 #include <vector>
 
@@ -104,11 +105,13 @@ int proj_rows(int Lo, int am, int par) {
 }
 
 int lift_kp(int L, int am) { return (L - am + 1 + 3) / 4 * 4; }
-int lift_ncol(int NC, int P, int am) { return (am ? 2 : 1) * 2 * NC * P; }
+// both signs (complex basis) or parts (real basis) at order am; the real-basis
+// spin-1 lift has both parts at am = 0 too
+int lift_ncol(int NC, int P, int am, bool both0 = false) { return ((am || both0) ? 2 : 1) * 2 * NC * P; }
 
-int acoef_len(int L, int NC, int P) {
+int acoef_len(int L, int NC, int P, bool both0 = false) {
     int n = 0;
-    for (int am = 0; am <= L; ++am) n += lift_kp(L, am) * istp::istp_cstride(lift_ncol(NC, P, am));
+    for (int am = 0; am <= L; ++am) n += lift_kp(L, am) * istp::istp_cstride(lift_ncol(NC, P, am, both0));
     return n;
 }
 
@@ -177,7 +180,10 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     // (each pair more fills more of the lift's and the projection's columns),
     // then the most ring pairs (more units fill more of the work-group's
     // threads in the transform phases and take fewer passes over the rings).
-    const int hc_len = NC * (Lo + 1) * (Lo + 1);
+    const bool rl1 = (flags & istp::kRealBasis) && S == ISTP_VECTOR;   // real basis, spin 1
+    // spectra per pair: [component][(Lo + 1)^2] (the real-basis spin-1 kernel adds
+    // the order-0 imaginary parts, Lo + 1 per component)
+    const int hc_len = NC * ((Lo + 1) * (Lo + 1) + (rl1 ? Lo + 1 : 0));
     const int nin = (int)row_size(L1, S), nin2 = (int)row_size(L2, S);
     int bestP = 0, bestG = 0, bestBytes = 0;
     for (int P : {8, 4, 2, 1}) {
@@ -186,7 +192,7 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
         const int stage = P * (nin + nin2) + (S ? NC * NC * (Lm + 1) * (Lm + 1) : 0);
         if (stage > istp::kStageLoads * istp::kThreads) continue;
         for (int G : {16, 12, 8, 4}) {
-            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(Lm, NC, P), hc_len,
+            const istp::IstpLayout ly = istp::istp_layout<T>(A, B, NC, G, P, acoef_len(Lm, NC, P, rl1), hc_len,
                                                              istp::istp_stage_len(P, nin, nin2, Lm, S), nproj);
             if (ly.bytes > istp::kLdsBudget) continue;
             if (P > bestP || (P == bestP && G > bestG)) {
@@ -267,7 +273,7 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
     // coefficient operand geometry and lift tiles
     int aoff = 0;
     for (int am = 0; am <= Lm; ++am) {
-        const int kp = lift_kp(Lm, am), ncol = lift_ncol(NC, P, am), cs = istp::istp_cstride(ncol);
+        const int kp = lift_kp(Lm, am), ncol = lift_ncol(NC, P, am, rl1), cs = istp::istp_cstride(ncol);
         for (int col = 0; col < cs; ++col) h.bcol.insert(h.bcol.end(), {am | (col << 8), aoff + col});
         for (int rb = 0; rb < (G + 7) / 8; ++rb)
             for (int ct = 0; ct < (ncol + 15) / 16; ++ct)
@@ -348,6 +354,88 @@ int build(int L1, int L2, int Lo, int S, int flags, istp_prod* pr, Host<T>& h) {
                 h.coef[4 * o] = (T)(scale * sgn(m3));
                 h.coefi[4 * o] = h.coefi[4 * o + 1] = h.coefi[4 * o + 2] = o;
                 h.coefi[4 * o + 3] = 1;
+            }
+    } else if (rl1) {
+        // real basis, spin 1.  Spectrum slots (c, part, l3, m' >= 0): part Re at
+        // l3^2 + l3 + m', part Im at l3^2 + l3 - m' (m' > 0) or (Lo + 1)^2 + l3 (m' = 0),
+        // per component c at c * nos.  They are Phi / (2 pi) times the true
+        // projections of g_+1 (c = 2) and g_-1 (c = 0) at +m', and 2 Phi / (2 pi) times
+        // that of Im g_0 (c = 1; g_0 = i Im g_0).  Orders m' < 0 follow from the
+        // product being i times a real field h: g_q[-m] = -(-1)^(m+q) conj g_-q[m].  A
+        // label's complex output z (sum over q of C^{j3 m3}_{l3,m3-q,1,q} times the
+        // coupling C^{1 1}_{1 1 1 0} times g_q) is read back as the three-product path
+        // does: w = i^t z at order -|m3|, t = 1 + [sigma3 = -1], r_0 = Re w_0,
+        // r_mu = sqrt 2 Re w_-mu, r_-mu = sqrt 2 Im w_-mu.
+        const double c1 = cgtp_cg_vector(1, 1, 0, 1, 1);
+        const int nos = no + Lo + 1;
+        const double k1 = 2.0 * kPi / Phi, k0 = kPi / Phi, rt2 = std::sqrt(2.0);
+        auto at = [&](int c, int part, int l3, int mp) {
+            return c * nos + (part == 0 ? l3 * l3 + l3 + mp : (mp ? l3 * l3 + l3 - mp : no + l3));
+        };
+        using Form = std::map<int, double>;
+        // adds a * (Re, Im) of the true projection of g_q at (l3, m') to (fr, fi)
+        auto addg = [&](Form& fr, Form& fi, int q, int l3, int mp, double a) {
+            if (mp >= 0) {
+                if (q == 0) {   // g_0 = i H, H from c = 1 (doubled)
+                    fr[at(1, 1, l3, mp)] += -a * k0;
+                    fi[at(1, 0, l3, mp)] += a * k0;
+                } else {
+                    const int c = q == 1 ? 2 : 0;
+                    fr[at(c, 0, l3, mp)] += a * k1;
+                    fi[at(c, 1, l3, mp)] += a * k1;
+                }
+                return;
+            }
+            // g_q[-m] = s conj g_-q[m], s = -(-1)^(m+q)
+            const int m = -mp;
+            const double sgn = ((m + q) & 1) ? 1.0 : -1.0;
+            Form xr, xi;
+            if (q == 0) {
+                xr[at(1, 1, l3, m)] += -k0;
+                xi[at(1, 0, l3, m)] += k0;
+            } else {
+                const int c = q == 1 ? 0 : 2;   // -q
+                xr[at(c, 0, l3, m)] += k1;
+                xi[at(c, 1, l3, m)] += k1;
+            }
+            for (const auto& kv : xr) fr[kv.first] += a * sgn * kv.second;
+            for (const auto& kv : xi) fi[kv.first] += -a * sgn * kv.second;
+        };
+        for (int l3 = 0; l3 <= Lo; ++l3)
+            for (int j3 = l3 - 1; j3 <= l3 + 1; ++j3) {
+                const int64_t off = label_offset(ISTP_VECTOR, j3, l3);
+                if (off < 0) continue;
+                const int turns = 1 + (((l3 + 1 - j3) & 1) ? 1 : 0);
+                for (int m3 = -j3; m3 <= j3; ++m3) {
+                    const int64_t o = off + j3 + m3;
+                    const int M = -std::abs(m3);
+                    Form zr, zi;
+                    for (int q = -1; q <= 1; ++q) {
+                        const int ml = M - q;
+                        if (std::abs(ml) > l3) continue;
+                        addg(zr, zi, q, l3, ml, c1 * cgtp_cg_vector(l3, ml, q, j3, M));
+                    }
+                    // w = i^turns z: one turn Re w = -Im z, Im w = Re z; two turns w = -z
+                    const bool want_re = m3 >= 0;
+                    const Form* f;
+                    double sg = m3 == 0 ? 1.0 : rt2;
+                    if (turns == 1) {
+                        f = want_re ? &zi : &zr;
+                        if (want_re) sg = -sg;
+                    } else {
+                        f = want_re ? &zr : &zi;
+                        sg = -sg;
+                    }
+                    int k = 0;
+                    for (const auto& kv : *f) {
+                        if (kv.second == 0.0) continue;
+                        if (k == 3) return CGTP_EINVAL;   // at most one entry per q
+                        h.coef[4 * o + k] = (T)(sg * kv.second);
+                        h.coefi[4 * o + k] = kv.first;
+                        ++k;
+                    }
+                    for (; k < 3; ++k) h.coefi[4 * o + k] = at(1, 0, l3, 0);   // zero weight
+                }
             }
     } else {
         // the kernel forms the antisymmetric 1 (x) 1 -> 1 combinations; their
@@ -589,14 +677,14 @@ int istp_plan(int32_t L, int32_t spin, int32_t dtype, istp_plan_t* plan_out) {
                            : make_prod<double>(2 * L, L, L, spin, istp::kReverseSecond, &p->bwd, true);
         if (rb != CGTP_OK && rb != CGTP_EUNSUP) rc = rb;
     }
-    if (rc == CGTP_OK && spin == ISTP_GAUNT) {
-        // the real-basis products (forward and gradients); outside the kernel's
-        // limits they stay unbuilt and the real-basis calls take three products
+    if (rc == CGTP_OK && spin != ISTP_TENSOR) {
+        // the real-basis products (forward; spin 0 also the gradients); outside the
+        // kernel's limits they stay unbuilt and the real-basis calls take three products
         const int f = istp::kRealBasis;
         int rr = dtype == CGTP_FP32 ? make_prod<float>(L, L, 2 * L, spin, f, &p->rfwd, true)
                                     : make_prod<double>(L, L, 2 * L, spin, f, &p->rfwd, true);
         if (rr != CGTP_OK && rr != CGTP_EUNSUP) rc = rr;
-        if (rc == CGTP_OK && p->bwd.ok) {
+        if (rc == CGTP_OK && spin == ISTP_GAUNT && p->bwd.ok) {
             rr = dtype == CGTP_FP32 ? make_prod<float>(2 * L, L, L, spin, f, &p->rbwd, true)
                                     : make_prod<double>(2 * L, L, L, spin, f, &p->rbwd, true);
             if (rr != CGTP_OK && rr != CGTP_EUNSUP) rc = rr;
@@ -741,7 +829,7 @@ int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N) {
     // spin 0 runs the real-basis kernel (no workspace) where it is built, else
     // forms the first product in out and reads it back in place; spin 1 and 2
     // keep all three products in the workspace
-    if (plan->spin == ISTP_GAUNT && plan->rfwd.ok) return 0;
+    if (plan->rfwd.ok) return 0;
     const size_t nprod = plan->spin == ISTP_GAUNT ? 2 : 3;
     return (int64_t)(6 * real_part_bytes((size_t)N * nin * esz) + nprod * real_part_bytes((size_t)N * nout * esz));
 }
@@ -750,7 +838,7 @@ int istp_forward_real(istp_plan_t plan, const void* x1, const void* x2, void* ou
                       int64_t workspace_bytes, void* hip_stream) {
     if (!plan || N < 0) return CGTP_EINVAL;
     if (N == 0) return CGTP_OK;
-    if (plan->spin == ISTP_GAUNT && plan->rfwd.ok) {
+    if (plan->rfwd.ok) {
         // one launch of the real-basis kernel; the workspace is not used
         if (!x1 || !x2 || !out || workspace_bytes < 0) return CGTP_EINVAL;
         if (((uintptr_t)x1 | (uintptr_t)x2 | (uintptr_t)out) & 15) return CGTP_EINVAL;

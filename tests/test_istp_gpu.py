@@ -370,13 +370,14 @@ def test_real_basis_errors():
     lib.istp_forward_real(plan._h, x.data_ptr(), x.data_ptr(), out.data_ptr(), N, None, 0, None)
     torch.cuda.synchronize()
     assert (out == 0.0).all().item()
-    vplan = lib.IstpPlan(3, 1, "fp32")
+    assert lib.istp_real_workspace_bytes(lib.IstpPlan(3, 1, "fp32")._h, N) == 0   # spin 1: real-basis kernel too
+    vplan = lib.IstpPlan(3, 2, "fp32")
     vneed = lib.istp_real_workspace_bytes(vplan._h, N)
     assert vneed > 0
     vx = torch.zeros((N, vplan.nin), device="cuda")
     vout = torch.zeros((N, vplan.nout), device="cuda")
     vws = torch.zeros(vneed, dtype=torch.uint8, device="cuda")
-    with pytest.raises(lib.CgtpError) as e:   # a spin-1 workspace too small
+    with pytest.raises(lib.CgtpError) as e:   # a spin-2 workspace too small
         lib.istp_forward_real(vplan._h, vx.data_ptr(), vx.data_ptr(), vout.data_ptr(), N, vws.data_ptr(),
                               vneed - 1, None)
     assert e.value.code == lib.CGTP_EINVAL

@@ -1,8 +1,8 @@
 """The no-allocation entry point istp_forward_real_static against istp_forward_real
 (same kernels, caller-allocated workspace), through the C ABI, on two calls in a
 row (the second with fewer pairs, reusing the static scratch the first one left
-behind), and its size limit.  Spins 1 and 2 use the scratch (three products);
-spin 0 runs the real-basis kernel, which needs none."""
+behind), and its size limit.  Spin 2 uses the scratch (three products); spins
+0 and 1 run the real-basis kernel, which needs none."""
 import ctypes
 
 import numpy as np
@@ -54,12 +54,12 @@ def test_static_scratch_matches_workspace_entry_point(L, N1, N2, dtype):
 
 
 def test_static_scratch_size_limit():
-    """Spin 1 (three products through the scratch): the largest N whose workspace fits the static array runs,
+    """Spin 2 (three products through the scratch): the largest N whose workspace fits the static array runs,
     one more is refused with CGTP_ESCRATCH and nothing is written.  Spin 0 runs the real-basis kernel, which
     needs no workspace: the static entry point takes any N."""
     torch, lib = _setup()
     L = 8
-    plan = lib.IstpPlan(L, lib.ISTP_VECTOR, "fp32")
+    plan = lib.IstpPlan(L, lib.ISTP_TENSOR, "fp32")
     cap = 64 << 20
     lo, hi = 1, 1 << 20
     while lo < hi:   # the largest n with workspace <= cap
