@@ -151,11 +151,12 @@ int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, cons
  * times the cross product, the real basis of i times the product, so that two
  * constant fields give their cross product over sqrt 2 (label (1, 0) holds a
  * constant field's Cartesian (y, z, x) components times Y_0^0).
- * Spin 0: one launch of a kernel for real-basis rows (the Hermitian
- * coefficients make each ring's signal real, so the lift, products and
- * projection take real and imaginary parts where the complex product takes
- * +m and -m); no workspace (istp_real_workspace_bytes returns 0; workspace
- * may be NULL, workspace_bytes must be >= 0).  Spin 1 and 2: the inputs are
+ * Spin 0 and 1: one launch of a kernel for real-basis rows (the real field's
+ * symmetry makes each ring's scalar signal real and the spin-1 components
+ * f_-1 = -conj f_+1, so the lift, products and projection take real and
+ * imaginary parts where the complex product takes +m and -m); no workspace
+ * (istp_real_workspace_bytes returns 0; workspace may be NULL,
+ * workspace_bytes must be >= 0).  Spin 2: the inputs are
  * converted to the real and imaginary parts of their complex coefficients,
  * three products of those parts run on the plan's kernel (Karatsuba's form:
  * P(a1, a2), P(b1, b2), P(a1 + b1, a2 + b2)), and the result is read back in
@@ -167,19 +168,19 @@ int istp_forward_weighted(istp_plan_t plan, const void *x1, const void *x2, cons
 int istp_forward_real(istp_plan_t plan, const void *x1, const void *x2, void *out, int64_t N, void *workspace,
                       int64_t workspace_bytes, void *hip_stream);
 
-/* Workspace bytes istp_forward_real needs for N pairs (0 for spin 0); -1 for N < 0 or overflow. */
+/* Workspace bytes istp_forward_real needs for N pairs (0 for spin 0 and 1); -1 for N < 0 or overflow. */
 int64_t istp_real_workspace_bytes(istp_plan_t plan, int64_t N);
 
 /*
  * istp_forward_real for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
- * allocation): the same kernels, with the workspace of spin 1 and 2 taken
- * from a static device array of ISTP_STATIC_SCRATCH_BYTES (64 MiB) that the
- * library holds on each GPU it runs on until the process ends (spin 0 needs
+ * allocation): the same kernels, with the workspace of spin 2 taken from a
+ * static device array of ISTP_STATIC_SCRATCH_BYTES (64 MiB) that the library
+ * holds on each GPU it runs on until the process ends (spins 0 and 1 need
  * none).  Same arguments and rules as istp_forward_real without the
  * workspace; the plan's device must be current.  CGTP_ESCRATCH when
- * istp_real_workspace_bytes(plan, N) exceeds the array (fp32 spin 1: above
- * 4133 pairs at L = 8, 1118 at L = 16).  The
+ * istp_real_workspace_bytes(plan, N) exceeds the array (fp32 spin 2: above
+ * 2479 pairs at L = 8, 670 at L = 16).  The
  * entry point calls no allocating routine; every call on a GPU shares that
  * GPU's array, so calls that overlap in time on one GPU (concurrent streams)
  * race and must be ordered by the caller.  Nothing in the array needs to
