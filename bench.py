@@ -38,34 +38,34 @@ PEAK_HBM_GBS = 8000.0
 # kernel and traffic is null.
 MEASURED_TRAFFIC = {
     "3ce5aa064a526a45": {
-        "cgtp_L32_N1024_fp32": {"fetch_kib": 220648.2, "fetch_scale": 1.999956, "write_kib": 5701608.2, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32": {"fetch_kib": 41325.5, "fetch_scale": 1.999956, "write_kib": 3153575.6, "write_scale": 1.000000},
+        "cgtp_L32_N1024_fp32": {"fetch_kib": 220638.0, "fetch_scale": 1.999956, "write_kib": 5700909.3, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32": {"fetch_kib": 41325.7, "fetch_scale": 1.999956, "write_kib": 3153892.5, "write_scale": 1.000000},
     },
     "4173d62bb601274c": {
-        "cgtp_L32_N1024_fp32:backward": {"fetch_kib": 2961072.8, "fetch_scale": 1.999956, "write_kib": 300568.0, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32:backward": {"fetch_kib": 2115042.4, "fetch_scale": 1.999956, "write_kib": 342208.0, "write_scale": 1.000000},
+        "cgtp_L32_N1024_fp32:backward": {"fetch_kib": 2961079.4, "fetch_scale": 1.999956, "write_kib": 300568.0, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32:backward": {"fetch_kib": 2115047.4, "fetch_scale": 1.999956, "write_kib": 342208.0, "write_scale": 1.000000},
     },
     "57413782ae7a98b8": {
-        "cgtp_L32_N1024_fp32:real": {"fetch_kib": 223100.4, "fetch_scale": 1.999956, "write_kib": 5900140.5, "write_scale": 1.000000},
-        "cgtp_L16_N8192_fp32:real": {"fetch_kib": 41482.0, "fetch_scale": 1.999956, "write_kib": 3286307.8, "write_scale": 1.000000},
+        "cgtp_L32_N1024_fp32:real": {"fetch_kib": 223081.2, "fetch_scale": 1.999956, "write_kib": 5899909.1, "write_scale": 1.000000},
+        "cgtp_L16_N8192_fp32:real": {"fetch_kib": 41486.2, "fetch_scale": 1.999956, "write_kib": 3286035.5, "write_scale": 1.000000},
     },
     "0cf4273a768d508c": {
-        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 30599.1, "fetch_scale": 1.999956, "write_kib": 3090072.7, "write_scale": 1.000000},
+        "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 30598.2, "fetch_scale": 1.999956, "write_kib": 3090242.9, "write_scale": 1.000000},
     },
-    "a46e27aaf2e902fb": {
-        "vstp_L32_N16384_fp32": {"fetch_kib": 216648.6, "fetch_scale": 1.999956, "write_kib": 986845.3, "write_scale": 1.000000},
-        "gtp_L32_N65536_fp32": {"fetch_kib": 284794.2, "fetch_scale": 1.999956, "write_kib": 1311305.5, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32": {"fetch_kib": 227504.5, "fetch_scale": 1.999956, "write_kib": 1006590.0, "write_scale": 1.000000},
-        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068316.0, "fetch_scale": 1.999956, "write_kib": 522849.4, "write_scale": 1.000000},
-        "tstp_L16_N16384_fp32": {"fetch_kib": 97086.0, "fetch_scale": 1.999956, "write_kib": 428103.1, "write_scale": 1.000000},
+    "d4cf5e7818a1dfac": {
+        "vstp_L32_N16384_fp32": {"fetch_kib": 216646.2, "fetch_scale": 1.999956, "write_kib": 986951.0, "write_scale": 1.000000},
+        "gtp_L32_N65536_fp32": {"fetch_kib": 284794.3, "fetch_scale": 1.999956, "write_kib": 1315294.1, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32": {"fetch_kib": 227504.5, "fetch_scale": 1.999956, "write_kib": 1012613.4, "write_scale": 1.000000},
+        "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068318.4, "fetch_scale": 1.999956, "write_kib": 522948.3, "write_scale": 1.000000},
+        "tstp_L16_N16384_fp32": {"fetch_kib": 97086.0, "fetch_scale": 1.999956, "write_kib": 428108.2, "write_scale": 1.000000},
     },
-    "a3adfc16bb75e8b2": {
-        "gtp_real_L16_N65536_fp32": {"fetch_kib": 769738.5, "fetch_scale": 1.999956, "write_kib": 1763803.6, "write_scale": 1.000000},
-        "gtp_real_L16_N65536_fp32:backward": {"fetch_kib": 1754308.8, "fetch_scale": 1.999956, "write_kib": 2809141.9, "write_scale": 1.000000},
-        "vstp_real_L16_N65536_fp32": {"fetch_kib": 2381784.8, "fetch_scale": 1.999956, "write_kib": 5198787.8, "write_scale": 1.000000},
+    "e9f7d0b3dbc118df": {
+        "gtp_real_L16_N65536_fp32": {"fetch_kib": 76038.6, "fetch_scale": 1.999956, "write_kib": 347102.0, "write_scale": 1.000000},
+        "gtp_real_L16_N65536_fp32:backward": {"fetch_kib": 355974.0, "fetch_scale": 1.999956, "write_kib": 174806.9, "write_scale": 1.000000},
+        "vstp_real_L16_N65536_fp32": {"fetch_kib": 228014.8, "fetch_scale": 1.999956, "write_kib": 1004219.9, "write_scale": 1.000000},
     },
-    "bea351de937a7bd5": {
-        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170282.8, "fetch_scale": 1.999956, "write_kib": 962973.0, "write_scale": 1.000000},
+    "2d6925f7a9941d27": {
+        "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170283.1, "fetch_scale": 1.999956, "write_kib": 962969.8, "write_scale": 1.000000},
     },
 }
 
