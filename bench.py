@@ -37,34 +37,34 @@ PEAK_HBM_GBS = 8000.0
 # kernel and plan sources: once they change, the figures no longer describe the
 # kernel and traffic is null.
 MEASURED_TRAFFIC = {
-    "3ce5aa064a526a45": {
+    "f1eba0e1f7a0f3fb": {
         "cgtp_L32_N1024_fp32": {"fetch_kib": 220638.0, "fetch_scale": 1.999956, "write_kib": 5700909.3, "write_scale": 1.000000},
         "cgtp_L16_N8192_fp32": {"fetch_kib": 41325.7, "fetch_scale": 1.999956, "write_kib": 3153892.5, "write_scale": 1.000000},
     },
-    "4173d62bb601274c": {
+    "f6eb89e53597bd25": {
         "cgtp_L32_N1024_fp32:backward": {"fetch_kib": 2961079.4, "fetch_scale": 1.999956, "write_kib": 300568.0, "write_scale": 1.000000},
         "cgtp_L16_N8192_fp32:backward": {"fetch_kib": 2115047.4, "fetch_scale": 1.999956, "write_kib": 342208.0, "write_scale": 1.000000},
     },
-    "57413782ae7a98b8": {
+    "3d77194f66694e60": {
         "cgtp_L32_N1024_fp32:real": {"fetch_kib": 223081.2, "fetch_scale": 1.999956, "write_kib": 5899909.1, "write_scale": 1.000000},
         "cgtp_L16_N8192_fp32:real": {"fetch_kib": 41486.2, "fetch_scale": 1.999956, "write_kib": 3286035.5, "write_scale": 1.000000},
     },
-    "0cf4273a768d508c": {
+    "3d664f5385b1d8cb": {
         "cgtp_L16_N512_C16_fp32_x2shared_weighted": {"fetch_kib": 30598.2, "fetch_scale": 1.999956, "write_kib": 3090242.9, "write_scale": 1.000000},
     },
-    "d4cf5e7818a1dfac": {
+    "aa708499db6f84ef": {
         "vstp_L32_N16384_fp32": {"fetch_kib": 216646.2, "fetch_scale": 1.999956, "write_kib": 986951.0, "write_scale": 1.000000},
         "gtp_L32_N65536_fp32": {"fetch_kib": 284794.3, "fetch_scale": 1.999956, "write_kib": 1315294.1, "write_scale": 1.000000},
         "vstp_L16_N65536_fp32": {"fetch_kib": 227504.5, "fetch_scale": 1.999956, "write_kib": 1012613.4, "write_scale": 1.000000},
         "vstp_L16_N65536_fp32:backward": {"fetch_kib": 1068318.4, "fetch_scale": 1.999956, "write_kib": 522948.3, "write_scale": 1.000000},
         "tstp_L16_N16384_fp32": {"fetch_kib": 97086.0, "fetch_scale": 1.999956, "write_kib": 428108.2, "write_scale": 1.000000},
     },
-    "e9f7d0b3dbc118df": {
+    "44cecb23916b05e1": {
         "gtp_real_L16_N65536_fp32": {"fetch_kib": 76038.6, "fetch_scale": 1.999956, "write_kib": 347102.0, "write_scale": 1.000000},
         "gtp_real_L16_N65536_fp32:backward": {"fetch_kib": 355974.0, "fetch_scale": 1.999956, "write_kib": 174806.9, "write_scale": 1.000000},
         "vstp_real_L16_N65536_fp32": {"fetch_kib": 228014.8, "fetch_scale": 1.999956, "write_kib": 1004219.9, "write_scale": 1.000000},
     },
-    "2d6925f7a9941d27": {
+    "63ca53a0d065cc33": {
         "vstp_L16_N4096_C16_fp32_x2shared_weighted": {"fetch_kib": 170283.1, "fetch_scale": 1.999956, "write_kib": 962969.8, "write_scale": 1.000000},
     },
 }
@@ -84,11 +84,36 @@ DIGEST_SOURCES = {
 }
 
 
+def code_only(text):
+    """C/C++ source without its comments, whitespace runs collapsed to one space:
+    what the compiler sees, so that edits to comments keep a kernel's digest."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == "/" and text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif c == "/" and text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_digest(kind="cgtp"):
     h = hashlib.sha256()
     for name in DIGEST_SOURCES[kind]:
-        with open(os.path.join(ROOT, "paper_2602_21466_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2602_21466_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

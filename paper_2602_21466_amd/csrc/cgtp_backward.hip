@@ -23,15 +23,15 @@
 // transpose below uses the equivalent full-circle form z(k) = F0(k) F1(k),
 // which is the same function of the inputs and so has the same gradient.
 //
-// One work-group computes one (j1, j2) block for one pair: the block's
-// contribution to the pair's gradient rows of degree j1 (x1) and j2 (x2),
-// written to a workspace; a last kernel sums the contributions over the other
-// degree in a fixed order.  The phases are work-group-wide task pools
+// One work-group computes one (j1, j2) block for a tile of two pairs: the
+// block's contribution to the pairs' gradient rows of degree j1 (x1) and j2
+// (x2), written to a workspace; a last kernel sums the contributions over the
+// other degree in a fixed order.  The phases are work-group-wide task pools
 // separated by barriers; rings go bd.bwd_rings at a time.  Small blocks run
-// on 256-thread work-groups with the accumulator-entry gradients in LDS; large
-// ones on 768 threads with one column of entry gradients per thread in
-// registers (the LDS they would take limits large blocks to one work-group
-// per CU).
+// on 256-thread work-groups, large ones on 768 threads; in both the
+// accumulator-entry gradients are held in registers as the B operands of the
+// transposed projection (wave w owns |m| = w, w + waves, ...), and the two
+// pairs share the staged Legendre values, the weight loads and the barriers.
 
 #include <hip/hip_runtime.h>
 

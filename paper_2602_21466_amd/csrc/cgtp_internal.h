@@ -187,11 +187,13 @@ struct TileGeom {
 //
 // The gradient kernel (cgtp_backward.hip) runs one work-group per (block,
 // tile of pairs), in two sizes: 256 threads and kBwdSmallPairs pairs for
-// blocks with (2 J + 1) * components <= kBwdSmallThreads, 768 threads and one
-// pair for the others.  The transposed Legendre projection
+// blocks with (2 J + 1) * components <= kBwdSmallThreads, 768 threads and
+// kBwdLargePairs pairs for the others.  The transposed Legendre projection
 // runs on 16x16x4 MFMA per |m|: wave w owns |m| = w, w + waves, ..., and holds
 // the gradients of those accumulator entries in registers as B operands
-// (lane: rows 4 s + lane / 16, column lane % 16 = (sign, component)).  LDS, in
+// (lane: column lane % 16 = (pair, sign, component); with ks = ceil(rows / 4)
+// K steps, step s takes row ks * (lane / 16) + s, so a lane's rows are
+// consecutive).  LDS, in
 // byte offsets: couplings [3][n1 + n2], twiddles in pass layout, the pair's
 // lifted coefficients and their gradients ([pair][slot][Phi] each), then per
 // ring group the Legendre values [ring][input][Phi] and kBwdSlots transforms
