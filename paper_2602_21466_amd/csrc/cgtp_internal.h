@@ -20,7 +20,7 @@ namespace cgtp {
 constexpr int kThreads = CGTP_THREADS;   // work-group size of the block kernel (wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
 constexpr int kRingGroup = CGTP_RING_GROUP;   // rings per pass: K = 4 steps of a 16x16x4 MFMA
-constexpr int kLdsBudget = 156 * 1024;
+constexpr int kLdsBudget = 160 * 1024;   // all of a gfx950 CU's LDS (one work-group per CU)
 constexpr int kMaxPairs = 16;
 
 // MFMA accumulator tiles (16 x 16) each wave may hold, per precision.

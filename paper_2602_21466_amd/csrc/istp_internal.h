@@ -11,7 +11,7 @@ namespace istp {
 
 constexpr int kThreads = 1024;   // work-group size (16 wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
-constexpr int kLdsBudget = 156 * 1024;
+constexpr int kLdsBudget = 160 * 1024;   // all of a gfx950 CU's LDS (one work-group per CU)
 constexpr int kMaxLiftSteps = 9;   // K = 4 lift steps whose weights a wave loads at once
 
 // Projection accumulator tiles (16 x 16) a wave may hold, per precision.
