@@ -204,6 +204,7 @@ constexpr int kBwdSmallLds = 52 * 1024;  // small blocks: ring groups sized for 
 constexpr int kBwdSmallPairs = 2;        // small blocks: pairs per work-group (a cross block's 8 columns each)
 constexpr int kBwdLargePairs = 2;        // large blocks: pairs per work-group
 constexpr int kBwdSlots = 8;   // 4 lifts, 2 analysis gradients, 2 product gradients
+constexpr int kBwdMaxRings = 16;   // rings per group: the 16 rows of the transposed projection's MFMA tile
 // Register budget of the B operands: |m| values per wave (mpw) and, for the
 // t-th of them (|m| >= waves * t), K steps of 4 rows.  A block's |m| has at
 // most floor((J - |m|) / 2) + 1 <= rmax - floor(|m| / 2) rows (rmax = Jmax / 2

@@ -565,14 +565,14 @@ int build(cgtp_plan_s* p, std::vector<BlockDesc>& blocks, HostTables<T>& h, std:
             const int lds_x2 = lds_for<T>(b, pairs, true);
             b.x2share = lds_x2 <= cgtp::kLdsBudget ? 1 : 0;
             p->lds_bytes_ch = std::max(p->lds_bytes_ch, b.x2share ? lds_x2 : b.lds_bytes);
-            // gradient kernel: the largest ring group (8 down to 1) whose LDS fits, for
-            // small blocks within kBwdSmallLds where one does
+            // gradient kernel: the largest ring group (kBwdMaxRings down to 1) whose LDS
+            // fits, for small blocks within kBwdSmallLds where one does
             b.bwd_rings = 0;
             {
                 const bool small = cgtp::bwd_small(b);
                 const int bp = small ? cgtp::kBwdSmallPairs : cgtp::kBwdLargePairs;
                 for (int pass = small ? 0 : 1; pass < 2 && !b.bwd_rings; ++pass)
-                    for (int G = 8; G >= 1 && !b.bwd_rings; --G)
+                    for (int G = cgtp::kBwdMaxRings; G >= 1 && !b.bwd_rings; --G)
                         if (cgtp::bwd_layout(b, (int)sizeof(T), G, bp).end <=
                             (pass ? cgtp::kLdsBudget : cgtp::kBwdSmallLds))
                             b.bwd_rings = G;
