@@ -4,8 +4,9 @@ sum).
 
 Bar: per-degree relative L2 error of each gradient (over every checked pair
 and the 2l + 1 components of degree l) <= 1e-4 for fp32 and <= 1e-10 for
-fp64.  Degrees L <= 8 are compared on every pair (N ragged: not a multiple of
-any tile); L = 16 and 32 on a seeded subsample of pairs, plus the adjoint
+fp64.  Degrees L <= 8 (and L = 12, 16 in fp64) are compared on every pair (N
+ragged: not a multiple of any tile); L = 16 and 32 in fp32 on a seeded
+subsample of pairs, plus the adjoint
 identity <grad_x1, d> = <grad_out, forward(d, x2)> on every pair, which holds
 at any size.
 """
@@ -73,7 +74,9 @@ def _check(L, host, got, dtype, idx=None, what=""):
 
 @pytest.mark.parametrize("L,N,dtype", [(0, 5, "fp32"), (1, 37, "fp32"), (2, 37, "fp32"), (3, 29, "fp32"),
                                        (4, 37, "fp32"), (5, 21, "fp32"), (8, 19, "fp32"),
-                                       (1, 9, "fp64"), (3, 17, "fp64"), (4, 13, "fp64"), (8, 7, "fp64")])
+                                       (1, 9, "fp64"), (3, 17, "fp64"), (4, 13, "fp64"), (8, 7, "fp64"),
+                                       # grids of more rings than one group holds, in both variants
+                                       (12, 7, "fp64"), (16, 5, "fp64")])
 def test_backward_all_pairs(L, N, dtype):
     _, host, _, got = _grads(L, N, dtype, seed=100 + L)
     _check(L, host, got, dtype, what="all pairs")
