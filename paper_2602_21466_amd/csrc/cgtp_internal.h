@@ -145,21 +145,24 @@ inline bool fft_factors(int phi, int* A, int* B) {
 }
 
 // Strides of the per-ring working set, in complex entries: one transform in
-// pass layout (slot), one (ring, pair) unit, one ring.  With fp32 they put the
-// 16 columns (sign, component, pair) of an MFMA B operand read in place, and
-// the rings of the operand, on distinct 4-byte LDS banks where the column
-// pattern allows: slot = 1, unit = 2 and ring = 2 P (mod 16) entries.
+// pass layout (slot), one (ring, pair) unit, one ring.  The transform passes
+// put the rows or columns of several transforms of a unit in one wave's
+// lanes; a slot stride of 8 (mod 16) entries starts neighbouring transforms
+// 16 four-byte banks apart, so their accesses overlap on fewer banks than
+// with the stride of 1 (mod 16) that suits the MFMA operand reads alone.
+// Units are 2 and rings 1 (mod 16) entries apart.  (fp32; fp64 plans use
+// the same strides.)
 #ifndef CGTP_PAD
 #define CGTP_PAD 1
 #endif
 __host__ __device__ constexpr int slot_stride(int A, int B) {
-    return CGTP_PAD ? A * (B + 1) + ((1 - A * (B + 1)) & 15) : A * (B + 1);
+    return CGTP_PAD ? A * (B + 1) + ((8 - A * (B + 1)) & 15) : A * (B + 1);
 }
 __host__ __device__ constexpr int unit_stride(int nslot, int fs) {
     return CGTP_PAD ? nslot * fs + ((2 - nslot * fs) & 15) : nslot * fs;
 }
 __host__ __device__ constexpr int ring_stride(int pairs, int per_rp) {
-    return CGTP_PAD ? pairs * per_rp + (((pairs <= 4 ? 2 * pairs : 1) - pairs * per_rp) & 15) : pairs * per_rp + 8;
+    return CGTP_PAD ? pairs * per_rp + ((1 - pairs * per_rp) & 15) : pairs * per_rp + 8;
 }
 
 // Channel-wise launches with a shared second input synthesise it once per

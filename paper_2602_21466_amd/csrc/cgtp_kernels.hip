@@ -71,7 +71,8 @@ __device__ __forceinline__ BlockDesc uniform_desc(const BlockDesc& g) {
 // first pass writes rows, the second reads and rewrites columns in place, and
 // the padding keeps both access patterns free of bank conflicts.  Slots,
 // (ring, pair) units and rings are padded (slot_stride, unit_stride,
-// ring_stride) so that the MFMA operands read in place spread over the banks.
+// ring_stride) so that the transforms one wave works on, and the MFMA
+// operands read in place, spread over the banks.
 
 struct Layout {
     int lc, prn, tw2, tdl, cvn, x2b, fbuf, bbuf;   // byte offsets
