@@ -150,14 +150,18 @@ inline bool fft_factors(int phi, int* A, int* B) {
 // lanes; a slot stride of 8 (mod 16) entries starts neighbouring transforms
 // 16 four-byte banks apart, so their accesses overlap on fewer banks than
 // with the stride of 1 (mod 16) that suits the MFMA operand reads alone.
-// The 24- and 54-point grids keep 1 (mod 16): there the larger padding
-// costs their blocks half their pairs per work-group at the LDS budget,
-// which outweighs the conflicts it saves.  Units are 2 and rings 1 (mod 16)
-// entries apart.  (fp32; fp64 plans use the same strides.)
+// Per grid (a model of the passes' bank conflicts, each entry checked by
+// measurement): 12 (no padding) for 144 points, 9 for 81 and 108; the 24-
+// and 54-point grids keep 1, since there the larger padding costs their
+// blocks half their pairs per work-group at the LDS budget.  Units are 2
+// and rings 1 (mod 16) entries apart.  (fp32; fp64 plans use the same
+// strides.)
 #ifndef CGTP_PAD
 #define CGTP_PAD 1
 #endif
-__host__ __device__ constexpr int slot_mod(int A, int B) { return (A * B == 24 || A * B == 54) ? 1 : 8; }
+__host__ __device__ constexpr int slot_mod(int A, int B) {
+    return (A * B == 24 || A * B == 54) ? 1 : A * B == 144 ? 12 : (A * B == 81 || A * B == 108) ? 9 : 8;
+}
 __host__ __device__ constexpr int slot_stride(int A, int B) {
     return CGTP_PAD ? A * (B + 1) + ((slot_mod(A, B) - A * (B + 1)) & 15) : A * (B + 1);
 }
