@@ -165,6 +165,25 @@ __host__ __device__ constexpr int slot_mod(int A, int B) {
 __host__ __device__ constexpr int slot_stride(int A, int B) {
     return CGTP_PAD ? A * (B + 1) + ((slot_mod(A, B) - A * (B + 1)) & 15) : A * (B + 1);
 }
+// Row strides of the lifted coefficients ([pair][slot][row], complex) and of
+// the Legendre values ([ring][input][row], real), which the first synthesis
+// pass reads for several transforms at once: a row of Phi entries padded per
+// grid (from the same bank-conflict model, checked by measurement) so that
+// power-of-two and other multiple-of-16 lengths do not start every row on the
+// same bank.
+__host__ __device__ constexpr int cv_mod(int phi) {
+    return phi == 96 ? 12 : phi == 72 ? 9 : (phi == 64 || phi == 48) ? 8 : phi == 36 ? 3 : -1;
+}
+__host__ __device__ constexpr int pr_mod(int phi) {
+    return phi == 128 ? 16 : (phi == 96 || phi == 72) ? 2 : (phi == 64 || phi == 48 || phi == 36) ? 8
+         : phi == 54 ? 9 : phi == 144 ? 1 : -1;
+}
+__host__ __device__ constexpr int cv_stride(int phi) {
+    return cv_mod(phi) < 0 ? phi : phi + ((cv_mod(phi) - phi) & 15);
+}
+__host__ __device__ constexpr int pr_stride(int phi) {
+    return pr_mod(phi) < 0 ? phi : phi + ((pr_mod(phi) - phi) & 31);
+}
 __host__ __device__ constexpr int unit_stride(int nslot, int fs) {
     return CGTP_PAD ? nslot * fs + ((2 - nslot * fs) & 15) : nslot * fs;
 }

@@ -94,10 +94,10 @@ __device__ __forceinline__ Layout make_layout(const BlockDesc& b, int nslot, boo
     const int P = b.pairs, n1 = 2 * b.j1 + 1, n2 = 2 * b.j2 + 1;
     int o = 0;
     l.lc = o; o = align16(o + (int)sizeof(T) * 3 * (n1 + n2));
-    l.prn = o; o = align16(o + (int)sizeof(T) * b.R * 2 * A * B);
+    l.prn = o; o = align16(o + (int)sizeof(T) * b.R * 2 * pr_stride(A * B));
     l.tw2 = o; o = align16(o + (int)sizeof(C) * FS);
     l.tdl = o; o = align16(o + 4 * b.ntiles);
-    l.cvn = o; o = align16(o + (int)sizeof(C) * P * nslot * A * B);
+    l.cvn = o; o = align16(o + (int)sizeof(C) * P * nslot * cv_stride(A * B));
     l.x2b = o;
     if (x2buf) o = align16(o + (int)sizeof(C) * x2buf_entries(nslot, FSS, kRingGroup));
     l.per_rp = unit_stride(nslot, FSS);
@@ -132,6 +132,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     constexpr int BP = B + 1;          // padded row of the pass layout
     constexpr int FS = slot_stride(A, B);   // padded transform plus the slot padding
     constexpr int MT = MaxTiles<T>::value;
+    constexpr int CVS = cv_stride(Phi), PRS = pr_stride(Phi);   // row strides of cvn and prn
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -151,11 +152,11 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
     const bool xsh = CH && bd.x2share && (ch.flags & kX2Shared) && ch.channels % P == 0;
     C* x2buf = reinterpret_cast<C*>(smem + ly.x2b);      // [ring][second-input slot], pass layout
     T* lc = reinterpret_cast<T*>(smem + ly.lc);          // [3][n1] then [3][n2]
-    T* prn = reinterpret_cast<T*>(smem + ly.prn);        // [ring][input][longitude n]: P_j^|m(n)|, zero for |m| > j
+    T* prn = reinterpret_cast<T*>(smem + ly.prn);        // [ring][input][longitude n], rows PRS apart: P_j^|m(n)|, zero for |m| > j
     C* tw2 = reinterpret_cast<C*>(smem + ly.tw2);        // [t][k2] = exp(-2 pi i t k2 / Phi), pass layout
     int* tdl = reinterpret_cast<int*>(smem + ly.tdl);    // per MFMA tile: weight offset in bytes
 
-    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [pair][slot][longitude n]: lifted coefficients, two series
+    C* cvn = reinterpret_cast<C*>(smem + ly.cvn);        // [pair][slot][longitude n], rows CVS apart: lifted coefficients, two series
     C* fbuf = reinterpret_cast<C*>(smem + ly.fbuf);      // per (ring, pair): nslot transforms, pass layout
     T* bbuf = reinterpret_cast<T*>(smem + ly.bbuf);      // MFMA tiles, end phase only
     // transforms of (ring, pair) rp = ring * P + pair
@@ -190,8 +191,10 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
             v[u] = (e < R * 2 * Phi && am <= j) ? prow[j * (j + 1) / 2 + am] : (T)0;
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (e0 + u * kThreads < R * 2 * Phi) prn[e0 + u * kThreads] = v[u];
+        for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * kThreads, ri = e / Phi;
+            if (e < R * 2 * Phi) prn[ri * PRS + (e - ri * Phi)] = v[u];
+        }
     }
 
     for (int u = tid; u < bd.ntiles; u += kThreads) {
@@ -317,7 +320,7 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 val = cmk<C>(sg * lcj[mj] * xlo, sg * lcj[2 * nj + mj] * xhi);
             }
         }
-        cvn[e] = val;
+        cvn[ps * CVS + n] = val;
     }
 
     Acc acc[MT];
@@ -374,8 +377,8 @@ __device__ __forceinline__ void block_body(const Tables<T>& tb, const TileDesc* 
                 const bool first = cross ? (s < 2) : (s == 0);
                 // inputs n = t + A n2i: both factors in longitude order, read at
                 // constant offsets from the task's first element
-                const C* cv = cvn + (size_t)((p << lgS) + s) * Phi + t;
-                const T* pr = prn + (size_t)(((rg0 + r) << 1) + (first ? 0 : 1)) * Phi + t;
+                const C* cv = cvn + (size_t)((p << lgS) + s) * CVS + t;
+                const T* pr = prn + (size_t)(((rg0 + r) << 1) + (first ? 0 : 1)) * PRS + t;
                 C v[B];
 #pragma unroll
                 for (int n2i = 0; n2i < B; ++n2i) {

@@ -396,10 +396,10 @@ int lds_for(const BlockDesc& b, int pairs, bool x2buf = false) {
     const int per_r = cgtp::ring_stride(pairs, cgtp::unit_stride(nslot, cgtp::slot_stride(b.A, b.B)));
     int o = 0;
     o = align16h(o + sz * 3 * (n1 + n2));
-    o = align16h(o + sz * b.R * 2 * b.Phi);
+    o = align16h(o + sz * b.R * 2 * cgtp::pr_stride(b.Phi));
     o = align16h(o + csz * FS);
     o = align16h(o + 4 * block_tiles(b, pairs));
-    o = align16h(o + csz * pairs * nslot * b.Phi);
+    o = align16h(o + csz * pairs * nslot * cgtp::cv_stride(b.Phi));
     if (x2buf) o = align16h(o + csz * cgtp::x2buf_entries(nslot, cgtp::slot_stride(b.A, b.B), cgtp::kRingGroup));
     const int fbuf = o;
     o += csz * cgtp::kRingGroup * per_r;
