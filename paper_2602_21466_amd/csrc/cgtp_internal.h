@@ -14,8 +14,11 @@ namespace cgtp {
 #ifndef CGTP_RING_GROUP
 #define CGTP_RING_GROUP 8
 #endif
+// MFMA accumulator tiles per wave (fp32): 9 x 12 waves = 108 tiles hold the
+// largest block of degree 32 (99 tiles at one pair); fewer registers than 10
+// per wave, and faster in measurement although some blocks take fewer pairs
 #ifndef CGTP_MAX_TILES_F32
-#define CGTP_MAX_TILES_F32 10
+#define CGTP_MAX_TILES_F32 9
 #endif
 constexpr int kThreads = CGTP_THREADS;   // work-group size of the block kernel (wave64s, one work-group per CU)
 constexpr int kWaves = kThreads / 64;
